@@ -1,0 +1,538 @@
+"""Pins for the CPU oracle: what the paper and the mathematics fix, independent
+of the oracle's own code.
+
+Each test names the passage it checks.  A plausible slip in the oracle (a
+dropped bias, a transposed weight, a wrong mask offset, a position off by one,
+a cache that keeps noise K/V, a >= instead of > in the inverse CDF) fails at
+least one of them.
+"""
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import kf_synth as S
+import oracle as O
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+# a small model for brute force: 2 layers, d=64, 4 heads, MLP 128, V=96, n_ctx=64
+SMALL = S.ModelConfig(2, 64, 4, 128, 96, 64, S.DTYPE_FP32)
+
+
+def _blob(cfg, seed=0, affine=True):
+    return S.pack_blob(cfg, S.make_weights(cfg, seed=seed, random_affine=affine))
+
+
+@pytest.fixture(scope="module")
+def small():
+    blob = _blob(SMALL)
+    return blob, O.Model(blob)
+
+
+@pytest.fixture(scope="module")
+def toy():
+    w = S.WORKLOADS["toy"]
+    blob = _blob(w["cfg"], affine=True)
+    return blob, O.Model(blob)
+
+
+# ------------------------------------------------------------------ Philox
+
+def test_oracle_philox_kat():
+    """Salmon et al. SC'11 known-answer vectors (tests/golden)."""
+    for line in open(os.path.join(GOLD, "philox4x32_10_kat.txt")):
+        if line.startswith("#") or not line.strip():
+            continue
+        w = [int(x, 16) for x in line.split()]
+        assert list(O.philox4x32_10(w[:4], w[4:6])) == w[6:10]
+
+
+# --------------------------------------------------------- inverse CDF
+
+def _frac(s):
+    return Fraction(s)
+
+
+def _appB():
+    cond, regions, mass = {}, [], {}
+    for line in open(os.path.join(GOLD, "appB_pushforward_example.txt")):
+        if line.startswith("#") or not line.strip():
+            continue
+        w = line.split()
+        if w[0] == "cond":
+            cond[w[1]] = [_frac(x) for x in w[2:5]]
+        elif w[0] == "region":
+            regions.append(([_frac(x) for x in w[1:5]], (w[5], w[6])))
+        elif w[0] == "mass":
+            mass[(w[1], w[2])] = _frac(w[3])
+    return cond, regions, mass
+
+
+NAMES = "ABC"
+
+
+def _gstar(cond, z1, z2):
+    q1 = [float(x) for x in cond["sos"]]
+    a = NAMES[O.icdf(q1, z1)]
+    b = NAMES[O.icdf([float(x) for x in cond[a]], z2)]
+    return a, b
+
+
+def test_appendix_b_regions():
+    """Appendix B example: the unrolled inverse-CDF map partitions [0,1)^2 into
+    the three printed regions; interior points and the boundary points
+    z1 = 1/3, z2 = 1/2 (which belong to the right-hand interval)."""
+    cond, regions, _ = _appB()
+    rng = np.random.default_rng(0)
+    for (z1lo, z1hi, z2lo, z2hi), want in regions:
+        for _ in range(200):
+            z1 = float(z1lo) + (float(z1hi) - float(z1lo)) * rng.random()
+            z2 = float(z2lo) + (float(z2hi) - float(z2lo)) * rng.random()
+            assert _gstar(cond, z1, z2) == want
+        # the lower corner belongs to the region (half-open intervals)
+        assert _gstar(cond, float(z1lo), float(z2lo)) == want
+    assert _gstar(cond, 1 / 3, 0.0) == ("B", "A")
+    assert _gstar(cond, 1 / 3, 0.5) == ("B", "C")
+    assert _gstar(cond, 0.0, 0.0) == ("A", "B")   # never the zero-probability A after A
+
+
+def _measure(q, v):
+    """Lebesgue measure of {z in [0,1): icdf(q, z) == v}, found by bisection on
+    the black-box map (the map is monotone non-decreasing in z)."""
+    def first_at_least(target):
+        lo, hi = 0.0, 1.0
+        if O.icdf(q, 0.0) >= target:
+            return 0.0
+        for _ in range(80):
+            mid = 0.5 * (lo + hi)
+            if O.icdf(q, mid) >= target:
+                hi = mid
+            else:
+                lo = mid
+        return hi
+    a = first_at_least(v)
+    b = first_at_least(v + 1) if v + 1 < len(q) else 1.0
+    return max(0.0, b - a)
+
+
+def test_appendix_b_masses():
+    """Each region has mass 1/3 (Appendix B)."""
+    cond, _, mass = _appB()
+    q1 = [float(x) for x in cond["sos"]]
+    for (a, b), m in mass.items():
+        ma = _measure(q1, NAMES.index(a))
+        mb = _measure([float(x) for x in cond[a]], NAMES.index(b))
+        assert abs(ma * mb - float(m)) < 1e-12
+
+
+def test_icdf_pushes_uniform_to_q():
+    """Standard result stated in Appendix B: with z ~ U(0,1), the inverse-CDF
+    map samples q.  Checked on random q including zero-probability tokens."""
+    rng = np.random.default_rng(1)
+    for trial in range(20):
+        V = int(rng.integers(2, 9))
+        q = rng.random(V)
+        q[rng.random(V) < 0.3] = 0.0
+        if q.sum() == 0:
+            q[0] = 1.0
+        q = q / q.sum()
+        for v in range(V):
+            assert abs(_measure(list(q), v) - q[v]) < 1e-12
+
+
+def test_gstar_reproduces_ar_joint():
+    """Eq. (correctness): the sequential inverse-CDF map reproduces the AR
+    joint p(v1..vk) = prod_j q(v_j | prefix).  A context-dependent random table
+    model, V = 3, k = 3; the measure of each output block is computed from the
+    black-box map and compared with the chain rule."""
+    rng = np.random.default_rng(2)
+    V, k = 3, 3
+    table = {}
+
+    def cond(prefix):
+        if prefix not in table:
+            q = rng.random(V) + 0.05
+            table[prefix] = q / q.sum()
+        return table[prefix]
+
+    total = 0.0
+    for seq in np.ndindex(*(V,) * k):
+        meas, chain = 1.0, 1.0
+        for j in range(k):
+            q = cond(tuple(seq[:j]))
+            meas *= _measure(list(q), seq[j])
+            chain *= q[seq[j]]
+        assert abs(meas - chain) < 1e-12
+        total += meas
+    assert abs(total - 1.0) < 1e-12
+
+
+# ------------------------------------------------------------- mask counts
+
+def _counts():
+    nnz, nfe, params = [], [], []
+    for line in open(os.path.join(GOLD, "paper_counts.txt")):
+        if line.startswith("#") or not line.strip():
+            continue
+        w = line.split()
+        if w[0] == "nnz":
+            nnz.append(tuple(int(x) for x in w[1:5]))
+        elif w[0] == "nfe":
+            nfe.append((w[1], int(w[2]), int(w[3])))
+        elif w[0] == "params":
+            params.append((w[1], int(w[2]), int(w[3]), int(w[4])))
+    return nnz, nfe, params
+
+
+def test_mask_nnz_closed_forms():
+    """Appendix C.2 cost analysis: the mask builders used by the brute force
+    have exactly |M_S| and |M_D| non-zeros."""
+    nnz, _, _ = _counts()
+    for N, k, ms, md in nnz:
+        M, _, _ = O.single_forward_layout(N, k)
+        assert int(M.sum()) == ms == O.nnz_single(N, k)
+        MD, _ = O.double_forward_layout(N, k)
+        f2 = slice(N + N * k, N + 2 * N * k)
+        assert int(MD[f2].sum()) == md == O.nnz_double(N, k)
+    for N in range(1, 9):
+        for k in range(1, 5):
+            M, _, _ = O.single_forward_layout(N, k)
+            assert int(M.sum()) == O.nnz_single(N, k)
+            MD, _ = O.double_forward_layout(N, k)
+            assert int(MD[N + N * k:].sum()) == O.nnz_double(N, k)
+            # F1 rows of M_D are the noise rows of M_S (same staircase + block-causal)
+            assert int(MD[N:N + N * k].sum()) == int(M[N:].sum())
+
+
+def test_table4_backbone_size():
+    """Table 4: ~124 M (OWT) / ~108 M (LM1B) parameters.  The counts match only
+    with the head tied to the token table; checked on the blob layout without
+    the noise encoder (the paper lists it separately)."""
+    _, _, params = _counts()
+    for name, V, T, pm in params:
+        cfg = S.ModelConfig(12, 768, 12, 3072, V, T, S.DTYPE_BF16)
+        noise = 4 * 768 * 768 * 2 + 4 * 768 + 768
+        got = (S.n_params(cfg) - noise) / 1e6
+        assert abs(got - pm) / pm < 0.01, (name, got)
+
+
+# -------------------------------------------------------------- components
+
+def test_components_textbook():
+    d = 16
+    rng = np.random.default_rng(3)
+    g, b = rng.normal(size=d), rng.normal(size=d)
+    # LayerNorm of a constant vector is the shift beta
+    np.testing.assert_allclose(O.layernorm(np.full(d, 3.25), g, b), b, atol=0, rtol=0)
+    # LayerNorm output has zero mean / unit variance before the affine map
+    x = rng.normal(size=d) * 5 + 2
+    y = O.layernorm(x, np.ones(d), np.zeros(d))
+    assert abs(y.mean()) < 1e-12 and abs((y ** 2).mean() - 1) < 1e-5
+    # GELU
+    assert O.gelu(0.0) == 0.0
+    assert abs(O.gelu(12.0) - 12.0) < 1e-12 and abs(O.gelu(-12.0)) < 1e-12
+    for x in np.linspace(-6, 6, 241):
+        exact = 0.5 * x * (1 + math.erf(x / math.sqrt(2)))
+        assert abs(O.gelu(x) - exact) < 1e-3   # tanh form vs erf form
+    # sinusoid(0) = [1..1, 0..0]; each (cos, sin) pair on the unit circle
+    e = O.sinusoid(0.0, 64)
+    np.testing.assert_array_equal(e, np.r_[np.ones(32), np.zeros(32)])
+    e = O.sinusoid(0.7316, 64)
+    np.testing.assert_allclose(e[:32] ** 2 + e[32:] ** 2, 1.0, atol=1e-14)
+    assert abs(e[0] - math.cos(731.6)) < 1e-12          # frequency 1 at i = 0
+    assert abs(e[31] - math.cos(731.6 * 10000 ** (-31 / 32))) < 1e-12
+    # attention: one key returns its value; equal scores average the values
+    q = rng.normal(size=8)
+    K, Vv = rng.normal(size=(1, 8)), rng.normal(size=(1, 8))
+    o, s = O.attend(q, K, Vv)
+    np.testing.assert_allclose(o, Vv[0], rtol=0, atol=1e-15)
+    K, Vv = rng.normal(size=(5, 8)), rng.normal(size=(5, 8))
+    o, s = O.attend(np.zeros(8), K, Vv)
+    np.testing.assert_allclose(o, Vv.mean(0), atol=1e-15)
+    assert abs(s - 1) < 1e-15
+    # softmax weights: scaled dot products, 1/sqrt(dh)
+    K = np.eye(8)[:2] * 4.0
+    Vv = np.array([[1.0] * 8, [0.0] * 8])
+    q = np.eye(8)[0]
+    o, _ = O.attend(q, K, Vv)
+    w = 1 / (1 + math.exp(-4.0 / math.sqrt(8)))
+    assert abs(o[0] - w) < 1e-14
+    # bf16 round-to-nearest-even
+    assert O.round_bf16(1.0 + 2 ** -8) == 1.0
+    assert O.round_bf16(1.0 + 3 * 2 ** -8) == 1.0 + 2 ** -6
+    assert O.round_bf16(1.0 + 2 ** -8 + 2 ** -20) == 1.0 + 2 ** -7
+    # greedy decoding: ties to the lowest id
+    assert list(O.argmax(np.array([[0.0, 2.0, 2.0, 1.0]]))) == [1]
+
+
+def test_zero_head_weights_all_tie(small):
+    """A zero token table gives all-zero logits and token 0 everywhere."""
+    w = S.make_weights(SMALL, seed=4, random_affine=True)
+    w["tok_emb"][:] = 0.0
+    m = O.Model(S.pack_blob(SMALL, w))
+    s, logits, toks = O.prefill(m, [1, 2, 3], [0.1, 0.6])
+    assert np.all(logits == 0) and list(toks) == [0, 0]
+
+
+# ------------------------------------------------- (a) k = 1 and prefixes
+
+def test_prefix_consistency(small):
+    """Fully causal design (Sec. 3.3): the j-th output depends only on the
+    context and z_1..z_j, so outputs 1..j of a k-block equal a j-block's."""
+    _, m = small
+    prompt = [5, 17, 3, 90, 44, 2]
+    u = [0.13, 0.77, 0.41, 0.93]
+    s4, l4, t4 = O.prefill(m, prompt, u)
+    for j in (1, 2, 3):
+        sj, lj, tj = O.prefill(m, prompt, u[:j])
+        np.testing.assert_array_equal(lj, l4[:j])
+    # decode-step prefixes
+    base = m.seq(); base.step(prompt, [0.5], commit=True)
+    a = m.seq(); a.step(prompt, [0.5], commit=True)
+    l4, _ = base.step([7, 8, 9, 10], [0.2, 0.5, 0.8, 0.3], commit=False)
+    for j in (1, 2, 3):
+        lj, _ = a.step([7, 8, 9, 10], [0.2, 0.5, 0.8, 0.3][:j], commit=False)
+        np.testing.assert_array_equal(lj, l4[:j])
+
+
+def test_k1_commits_like_ar(small):
+    """(a) k = 1: each step commits one position, and the cache equals the one
+    an ordinary causal KV-cached AR decode builds from the same tokens."""
+    _, m = small
+    prompt = [4, 8, 15, 16, 23, 42]
+    kf, ar = m.seq(), m.seq()
+    lk, _ = kf.step(prompt, [0.31], commit=True)
+    ar.step(prompt, [], commit=True)
+    pending = list(O.argmax(lk))
+    rng = np.random.default_rng(5)
+    for step in range(8):
+        lk, _ = kf.step(pending, [float(rng.random())], commit=True)
+        ar.step(pending, [], commit=True)
+        assert kf.C == ar.C == len(prompt) + step + 1
+        pending = list(O.argmax(lk))
+    for l in range(m.n_layer):
+        for which in (0, 1):
+            np.testing.assert_array_equal(kf.kv(l, which), ar.kv(l, which))
+
+
+def _dense_ar_logits(cfg, W, seq):
+    n = len(seq)
+    M = np.tril(np.ones((n, n), bool))
+    return O.dense_forward(cfg, W, [("tok", t) for t in seq], list(range(n)), M)[-1]
+
+
+def test_ar_mode_is_sequential_icdf(small):
+    """(a) AR mode equals the closed-form map G* (Eq. sequential-icdf) built
+    from the dense no-cache forward pass and a numpy inverse CDF."""
+    blob, m = small
+    cfg, W = O.parse_blob(blob)
+    prompt = np.array([[3, 1, 4, 1, 5]], np.int32)
+    seed = 11
+    got = O.generate_ar(m, prompt, 10, seed)[0]
+    seq = list(prompt[0])
+    for p in range(5, 15):
+        lg = _dense_ar_logits(cfg, W, seq)
+        q = np.exp(lg - lg.max()); q /= q.sum()
+        F = np.cumsum(q)
+        z = O.noise_u(seed, 0, p)
+        assert np.min(np.abs(F - z)) > 1e-9
+        want = int(np.argmax(F > z))
+        assert got[p - 5] == want
+        seq.append(want)
+
+
+# ------------------------------------------- (b) incremental == recompute
+
+def test_incremental_equals_full_recompute(toy):
+    """(b) Appendix C.1: the cached decode equals a no-cache forward over
+    [prompt, emitted tokens, k noise rows] -- bitwise in the oracle, since
+    every row's arithmetic is the same in both modes."""
+    _, m = toy
+    w = S.WORKLOADS["toy"]
+    prompt = S.prompts_uniform(1, 1, 16, 1024)[0]
+    k, seed = 4, 2
+    s = m.seq()
+    history = list(prompt)
+    pending = list(prompt)
+    p = 16
+    for step in range(6):
+        u = [O.noise_u(seed, 0, p + j) for j in range(k)]
+        lg, _ = s.step(pending, u, commit=True)
+        full = O.full_recompute(m, history, u)
+        np.testing.assert_array_equal(lg, full)
+        toks = list(O.argmax(lg))
+        history += toks
+        pending = toks
+        p += k
+
+
+# ------------------------------------------------------------ (c) causality
+
+def test_causality_noise(small):
+    """(c) Perturbing z_j leaves outputs before j unchanged (Sec. 3.3)."""
+    _, m = small
+    prompt = [9, 8, 7, 6]
+    u = [0.1, 0.2, 0.3, 0.4]
+    _, base, _ = O.prefill(m, prompt, u)
+    for j in range(4):
+        v = list(u); v[j] = 0.9
+        _, pert, _ = O.prefill(m, prompt, v)
+        np.testing.assert_array_equal(pert[:j], base[:j])
+        assert np.max(np.abs(pert[j] - base[j])) > 0
+
+
+def test_causality_prompt(small):
+    """(c) Perturbing the prompt token at position p leaves earlier rows and
+    their committed K/V unchanged."""
+    _, m = small
+    prompt = [9, 8, 7, 6, 5, 4]
+    a, b = m.seq(), m.seq()
+    _, _, ha = a.step(prompt, [0.5, 0.25], commit=True, want_hidden=True)
+    pert = list(prompt); pert[3] = 60
+    _, _, hb = b.step(pert, [0.5, 0.25], commit=True, want_hidden=True)
+    np.testing.assert_array_equal(ha[:3], hb[:3])
+    assert np.max(np.abs(ha[3] - hb[3])) > 0
+    for l in range(m.n_layer):
+        np.testing.assert_array_equal(a.kv(l, 0)[:3], b.kv(l, 0)[:3])
+        np.testing.assert_array_equal(a.kv(l, 1)[:3], b.kv(l, 1)[:3])
+
+
+def test_noise_kv_discarded(small):
+    """(c) Appendix C.1 cache rule: noise K/V are dropped, so a different noise
+    block at step s (with the same emitted tokens fed back) leaves step s+1
+    unchanged."""
+    _, m = small
+    prompt = [1, 2, 3, 4, 5]
+    a, b = m.seq(), m.seq()
+    a.step(prompt, [0.1, 0.2, 0.3], commit=True)
+    b.step(prompt, [0.9, 0.8, 0.7], commit=True)
+    forced = [11, 12, 13]
+    la, _ = a.step(forced, [0.5, 0.6, 0.7], commit=True)
+    lb, _ = b.step(forced, [0.5, 0.6, 0.7], commit=True)
+    np.testing.assert_array_equal(la, lb)
+    assert a.C == b.C == 8
+
+
+# ------------------------------------------------------- (d) softmax sums
+
+def test_softmax_rows_sum_to_one(toy):
+    _, m = toy
+    s = m.seq()
+    lg, dev = s.step(list(range(16)), [0.1, 0.2, 0.3, 0.4], commit=True)
+    assert dev < 1e-12
+    lg, dev = s.step([1, 2, 3, 4], [0.5, 0.6, 0.7, 0.8], commit=True)
+    assert dev < 1e-12
+    q = O.softmax(lg[0])
+    assert abs(q.sum() - 1) < 1e-12 and (q >= 0).all()
+
+
+# ---------------------------------------------------- (e) dense brute force
+
+def _check_single_forward(blob, m, N, k, rng, tol=1e-10):
+    cfg, W = O.parse_blob(blob)
+    x = [int(t) for t in rng.integers(0, cfg["V"], N)]
+    z = rng.random((N, k))
+    M, pos, grp = O.single_forward_layout(N, k)
+    rows = [("tok", t) for t in x] + [("noise", float(z[t, j])) for t in range(N) for j in range(k)]
+    dense = O.dense_forward(cfg, W, rows, pos, M)
+    outs = {}
+    for t in range(1, N + 1):
+        s, lg, toks = O.prefill(m, x[:t], z[t - 1])
+        ref = dense[N + (t - 1) * k:N + t * k]
+        scale = np.abs(ref).max()
+        assert np.max(np.abs(lg - ref)) <= tol * scale, (t, np.max(np.abs(lg - ref)) / scale)
+        outs[t] = (s, list(toks))
+    return cfg, W, x, outs
+
+
+def test_single_forward_brute_force(small):
+    """(e) SingleForward (Appendix C.2): one dense-masked pass over N context
+    tokens and N*k noise tokens equals, group by group, the oracle's prefill of
+    x_1..x_t with that group's noise."""
+    blob, m = small
+    _check_single_forward(blob, m, N=6, k=3, rng=np.random.default_rng(6))
+
+
+def test_double_forward_brute_force(small):
+    """(e) DoubleForward (Appendix C.2): the Future-2 outputs of the fused
+    two-round mask equal the oracle's decode step that feeds the first round's
+    tokens as real rows after a prefill of x_1..x_t."""
+    blob, m = small
+    N, k = 5, 3
+    rng = np.random.default_rng(7)
+    cfg, W, x, outs = _check_single_forward(blob, m, N, k, rng)
+    z2 = rng.random((N, k))
+    MD, pos = O.double_forward_layout(N, k)
+    rows = [("tok", t) for t in x]
+    rows += [("tok", outs[t][1][j]) for t in range(1, N + 1) for j in range(k)]
+    rows += [("noise", float(z2[t - 1, j])) for t in range(1, N + 1) for j in range(k)]
+    dense = O.dense_forward(cfg, W, rows, pos, MD)
+    for t in range(1, N + 1):
+        s, _ = outs[t]
+        lg, _ = O.decode(s, outs[t][1], z2[t - 1])
+        ref = dense[N + N * k + (t - 1) * k:N + N * k + t * k]
+        assert np.max(np.abs(lg - ref)) <= 1e-10 * np.abs(ref).max()
+
+
+def test_brute_force_bf16_weights():
+    """(e) with a bf16 model: both the C oracle and the numpy brute force round
+    2-D tensors to bf16; a mismatch in that rule shows here."""
+    cfg = S.ModelConfig(2, 64, 4, 128, 96, 64, S.DTYPE_BF16)
+    blob = _blob(cfg, seed=9)
+    _check_single_forward(blob, O.Model(blob), N=4, k=2, rng=np.random.default_rng(8))
+
+
+def test_toy_config_brute_force(toy):
+    """(e) on the 2-layer toy configuration itself (d=128, 4 heads, V=1024)."""
+    blob, m = toy
+    _check_single_forward(blob, m, N=4, k=4, rng=np.random.default_rng(10))
+
+
+# --------------------------------------------------------------- NFE
+
+def test_nfe_counts(small):
+    """Table 3: NFE = new tokens / k with the prefill as the first pass."""
+    _, nfe, _ = _counts()
+    for _, k, want in nfe:
+        assert 960 // k == want
+    _, m = small
+    prompt = np.array([[1, 2, 3]], np.int32)
+    for k in (1, 2, 4):
+        toks, passes = O.generate(m, prompt, 8, k, seed=3)
+        assert passes == 8 // k and toks.shape == (1, 8)
+
+
+def test_generate_matches_manual_steps(small):
+    """The generation driver feeds each block's argmax back as the next real
+    rows and draws u by absolute position (noise stream 2)."""
+    _, m = small
+    prompt = np.array([[5, 6, 7, 8]], np.int32)
+    toks, _ = O.generate(m, prompt, 6, 3, seed=21)
+    s, lg, t = O.prefill(m, prompt[0], [O.noise_u(21, 0, 4 + j) for j in range(3)])
+    lg2, t2 = O.decode(s, t, [O.noise_u(21, 0, 7 + j) for j in range(3)])
+    assert list(toks[0]) == list(t) + list(t2)
+
+
+def test_f32_instantiation_close(toy):
+    """The fp32 instantiation (CPU timing) computes the same function."""
+    blob, m = toy
+    m32 = O.Model(blob, "f32")
+    a, b = m.seq(), m32.seq()
+    la, _ = a.step(list(range(20)), [0.3, 0.6], commit=True)
+    lb, _ = b.step(list(range(20)), [0.3, 0.6], commit=True)
+    assert np.max(np.abs(la - lb)) < 1e-4 * np.abs(la).max()
+
+
+def test_bad_arguments_rejected(small):
+    _, m = small
+    s = m.seq()
+    with pytest.raises(ValueError):
+        s.step([1000], [0.5])          # token outside the vocabulary
+    with pytest.raises(ValueError):
+        s.step([], [])                 # nothing to run
+    with pytest.raises(ValueError):
+        s.step(list(range(60)), [0.1] * 5)   # past n_ctx
+    assert s.C == 0
