@@ -1,0 +1,182 @@
+/*
+ * kforcing.h -- C ABI of the MI355X (gfx950) K-Forcing decode library.
+ *
+ * K-Forcing (paper Sec. 3.1) learns a push-forward map
+ *     G_theta : V^t x [0,1]^k -> V^k
+ * that turns a context and k i.i.d. uniform noise variables into the next k
+ * tokens in one forward pass.  This library runs the inference procedure of
+ * Appendix C.1 ("K-Forcing Inference with KV Cache"): a prefill over the
+ * prompt plus k noise rows, then decode blocks that each feed the k tokens
+ * emitted by the previous block plus k fresh noise rows, keep only the real
+ * tokens' K/V, and take the argmax of the head over the last k outputs.  An
+ * ordinary autoregressive (k = 1, inverse-CDF) path on the same backbone is
+ * included as the baseline the paper compares against (Sec. 4, Table 1).
+ *
+ * Conventions for every entry point:
+ *   - Return 0 (KF_OK) or a negative KF_E* code.  On an error nothing is
+ *     launched and the context's state is unchanged; kf_last_error() gives a
+ *     message.  No C++ exception crosses this boundary.
+ *   - Array arguments are DEVICE pointers unless stated otherwise, and all
+ *     work is enqueued asynchronously on the stream given to kf_create();
+ *     outputs are valid once that stream has been synchronised.
+ *   - The caller owns every buffer it passes (state, inputs, outputs); the
+ *     library never allocates or frees device memory.
+ *   - A context is bound to one stream and is not thread-safe.
+ *   - Matrices are row-major; token ids are int32; noise values are fp32 in
+ *     [0, 1).
+ */
+#ifndef KFORCING_H
+#define KFORCING_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ------------------------------------------------------------ error codes */
+#define KF_OK 0
+#define KF_EINVAL (-1) /* bad argument: k < 1, k > max_k, B out of range, null pointer, L % k != 0 ... */
+#define KF_ESTATE (-2) /* no state bound, no weights loaded, decode before prefill, B mismatch */
+#define KF_ECTX (-3)   /* the step would run past n_ctx positions */
+#define KF_ENOMEM (-4) /* the bound state buffer is smaller than kf_state_bytes() */
+#define KF_EHIP (-5)   /* a HIP runtime call failed (message from hipGetErrorString) */
+
+/* ---------------------------------------------------------- configuration */
+#define KF_FP32 0 /* weights, activations and KV cache in fp32 */
+#define KF_BF16 1 /* weights, GEMM inputs and KV cache in bf16; fp32 accumulation,
+                     fp32 residual stream, fp32 noise sinusoid */
+
+#define KF_FLAG_DEBUG_LOGITS 1u /* reserve room for, and record, the fp32 head logits of
+                                   the most recent step (kf_debug_logits) */
+
+typedef struct kf_config {
+  int n_layer;    /* Transformer blocks */
+  int d_model;    /* hidden size d; multiple of 64 */
+  int n_head;     /* heads H; d_model / n_head must be 32, 64 or 128 */
+  int d_mlp;      /* MLP hidden size; multiple of 64 */
+  int vocab;      /* vocabulary size V (any value >= 2) */
+  int n_ctx;      /* positions (learned position table length, KV capacity) */
+  int dtype;      /* KF_FP32 or KF_BF16 */
+  int max_batch;  /* largest B any call may use */
+  int max_k;      /* largest window k any call may use (k <= max_k) */
+  int max_prompt; /* longest prompt N given to a prefill call */
+  unsigned flags; /* KF_FLAG_* */
+} kf_config;
+
+/* Opaque per-stream context. */
+typedef struct kf_ctx kf_ctx;
+
+/* Validate cfg and create a context bound to hip_stream (a hipStream_t; NULL
+ * is the default stream).  Touches no device.  *out is set on success. */
+int kf_create(const kf_config *cfg, void *hip_stream, kf_ctx **out);
+
+/* Device bytes the caller must provide for cfg: packed weights, the KV cache
+ * ([max_batch][n_layer][K,V][n_head][n_ctx][d_head]) and the workspace.
+ * Returns 0 for an invalid cfg. */
+size_t kf_state_bytes(const kf_config *cfg);
+
+/* Hand the context a device buffer of at least kf_state_bytes() bytes,
+ * 256-byte aligned.  Re-binding discards weights and sequence state. */
+int kf_bind_state(kf_ctx *ctx, void *dev_ptr, size_t bytes);
+
+/* Load the weights from a flat blob: 16 int32 header words (magic 0x4B465731,
+ * version 1, n_layer, d_model, n_head, d_mlp, vocab, n_ctx, dtype, 7 zero
+ * words) followed by every tensor as fp32 in a fixed order: token table
+ * [V][d] (also the tied output head), position table [n_ctx][d], noise MLP
+ * W1 [4d][d], b1 [4d], W2 [d][4d], b2 [d], then per layer: ln1 gain, ln1
+ * shift [d], W_qkv [3d][d], b_qkv [3d], W_o [d][d], b_o [d], ln2 gain, ln2
+ * shift [d], W_1 [d_mlp][d], b_1 [d_mlp], W_2 [d][d_mlp], b_2 [d]; finally
+ * the final-norm gain and shift [d].  Matrices are [out][in].  For KF_BF16
+ * the 2-D tensors are rounded to bf16 (round to nearest even) on load.
+ * blob_is_device: 0 = host pointer (copied synchronously), 1 = device
+ * pointer (converted on the stream).  The header must match the config. */
+int kf_load_weights(kf_ctx *ctx, const void *blob, size_t bytes, int blob_is_device);
+
+/* First step of Appendix C.1: for each of the B sequences, the N prompt
+ * tokens (prompt [B][N], positions 0..N-1) followed by k noise rows
+ * (noise [B][k], positions N..N+k-1), one causal forward pass, argmax of the
+ * head over the k noise rows -> out [B][k] (positions N..N+k-1).  Commits the
+ * prompt's K/V (context length C = N) and keeps out as the pending block.
+ * 0 <= N <= max_prompt, 1 <= k <= max_k, N + k <= n_ctx.  Token ids outside
+ * [0, V) are replaced by 0 and flagged (kf_device_errors). */
+int kf_prefill(kf_ctx *ctx, int B, int N, const int32_t *prompt, int k, const float *noise,
+               int32_t *out);
+
+/* One decode block (Appendix C.1): the pending tokens from the previous step
+ * (positions C..C+p-1) plus k noise rows (noise [B][k], positions
+ * C+p..C+p+k-1) attend causally over the cached context; the argmax of the
+ * head over the k noise rows -> out [B][k].  The pending tokens' K/V are
+ * committed (C += p), the noise K/V are dropped, out becomes pending.
+ * B must equal the prefill's B; k may change between calls; C+p+k <= n_ctx. */
+int kf_decode_block(kf_ctx *ctx, int B, int k, const float *noise, int32_t *out);
+
+/* Generate L new tokens per sequence (L % k == 0, N + L <= n_ctx): one
+ * prefill and L/k - 1 decode blocks, with noise drawn on the device by
+ * Philox4x32-10 (key = seed, counter = (emitted position, sequence, 2, 0),
+ * u = (word0 >> 8) * 2^-24).  out [B][L] holds positions N..N+L-1.  Leaves
+ * the context decoded up to the last block (pending = last k tokens).
+ * L == 0 launches nothing. */
+int kf_generate(kf_ctx *ctx, int B, int N, const int32_t *prompt, int L, int k, uint64_t seed,
+                int32_t *out);
+
+/* Autoregressive baseline (the AR teacher's decoding, Sec. 4; inverse-CDF map
+ * of Appendix B: the smallest token id m with F_m > u, F the CDF of the
+ * softmax in token-id order).  Prefill: prompt rows only (N >= 1), the head
+ * on the last prompt row, u [B] -> out [B] (position N).  C = N. */
+int kf_prefill_ar(kf_ctx *ctx, int B, int N, const int32_t *prompt, const float *u, int32_t *out);
+
+/* One AR step: the pending tokens as real rows, head on the last of them,
+ * inverse CDF with u [B] -> out [B]; commits the pending tokens. */
+int kf_decode_ar(kf_ctx *ctx, int B, const float *u, int32_t *out);
+
+/* AR generation of L >= 0 tokens with device Philox noise (same stream as
+ * kf_generate, so position p uses the same u for every method). */
+int kf_generate_ar(kf_ctx *ctx, int B, int N, const int32_t *prompt, int L, uint64_t seed,
+                   int32_t *out);
+
+/* Copy the fp32 head logits of the most recent step to out (device,
+ * rows x V floats; rows = B*k for a K-Forcing step, B for an AR step).
+ * n_floats is the capacity of out.  Requires KF_FLAG_DEBUG_LOGITS. */
+int kf_debug_logits(kf_ctx *ctx, float *out, size_t n_floats);
+
+/* Fill out [B][n] with the device generator's u for positions p0..p0+n-1. */
+int kf_fill_noise(kf_ctx *ctx, uint64_t seed, int B, int p0, int n, float *out);
+
+/* Host view of the sequence state: committed length C, pending count, B. */
+int kf_get_state(const kf_ctx *ctx, int *C, int *pending, int *B);
+
+/* Synchronise the stream and return the device-side error flags (bit 0: a
+ * token id outside [0, V) was replaced by 0), then clear them. */
+int kf_device_errors(kf_ctx *ctx, int *flags);
+
+/* Per-kernel timing with HIP events on the context's stream.  While enabled,
+ * every launch of a kernel class is bracketed by an event pair.
+ * kf_kernel_time() synchronises and returns the summed milliseconds and the
+ * launch count of one class since timing was enabled. */
+#define KF_KC_EMBED 0    /* real-row embedding */
+#define KF_KC_NOISE 1    /* noise sinusoid + noise-MLP GEMMs + position add */
+#define KF_KC_NORM 2     /* LayerNorm kernels */
+#define KF_KC_QKV 3      /* QKV GEMM with KV append */
+#define KF_KC_ATTN 4     /* block attention */
+#define KF_KC_OPROJ 5    /* attention-out GEMM + residual */
+#define KF_KC_MLP_UP 6   /* MLP up GEMM + GELU */
+#define KF_KC_MLP_DOWN 7 /* MLP down GEMM + residual */
+#define KF_KC_HEAD 8     /* LM-head GEMM with fused argmax partials / logits */
+#define KF_KC_SELECT 9   /* argmax reduction or inverse-CDF sampler, commit */
+#define KF_KC_COUNT 10
+int kf_set_timing(kf_ctx *ctx, int enable);
+int kf_kernel_time(kf_ctx *ctx, int kernel_class, double *total_ms, int *launches);
+
+/* Release host resources (device memory belongs to the caller). */
+void kf_destroy(kf_ctx *ctx);
+
+/* Last error message of ctx ("" if none); kf_strerror names a code. */
+const char *kf_last_error(const kf_ctx *ctx);
+const char *kf_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* KFORCING_H */

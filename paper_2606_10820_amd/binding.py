@@ -1,0 +1,233 @@
+"""ctypes binding of libkforcing.so (include/kforcing.h).
+
+`lib()` returns the loaded library with typed signatures for every kf_*
+entry point (same names as the C ABI).  `KForcing` wraps one context: it
+allocates the state buffer with torch on a CUDA (HIP) device, passes device
+pointers and the current stream, and turns error codes into KfError.  No
+computation happens here.  If the shared library is missing the import of
+`lib()` fails loudly: there is no CPU fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_PKG, "libkforcing.so")
+
+KF_OK, KF_EINVAL, KF_ESTATE, KF_ECTX, KF_ENOMEM, KF_EHIP = 0, -1, -2, -3, -4, -5
+KF_FP32, KF_BF16 = 0, 1
+KF_FLAG_DEBUG_LOGITS = 1
+KF_KC_NAMES = ["embed", "noise", "norm", "qkv", "attn", "oproj", "mlp_up", "mlp_down", "head",
+               "select"]
+
+_lib = None
+
+
+class KfConfig(ctypes.Structure):
+    _fields_ = [
+        ("n_layer", ctypes.c_int), ("d_model", ctypes.c_int), ("n_head", ctypes.c_int),
+        ("d_mlp", ctypes.c_int), ("vocab", ctypes.c_int), ("n_ctx", ctypes.c_int),
+        ("dtype", ctypes.c_int), ("max_batch", ctypes.c_int), ("max_k", ctypes.c_int),
+        ("max_prompt", ctypes.c_int), ("flags", ctypes.c_uint),
+    ]
+
+
+class KfError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"kforcing error {code}: {msg}")
+        self.code = code
+
+
+def lib_path() -> str:
+    return _LIB_PATH
+
+
+def lib():
+    """Load libkforcing.so and declare every entry point of include/kforcing.h."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(f"{_LIB_PATH} is missing: build it with "
+                          "`python -m paper_2606_10820_amd.build` (there is no CPU fallback)")
+    L = ctypes.CDLL(_LIB_PATH)
+    P, I, U64, SZ = ctypes.c_void_p, ctypes.c_int, ctypes.c_uint64, ctypes.c_size_t
+    CP = ctypes.POINTER(KfConfig)
+    IP = ctypes.POINTER(ctypes.c_int)
+    sigs = {
+        "kf_create": (I, [CP, P, ctypes.POINTER(P)]),
+        "kf_state_bytes": (SZ, [CP]),
+        "kf_bind_state": (I, [P, P, SZ]),
+        "kf_load_weights": (I, [P, P, SZ, I]),
+        "kf_prefill": (I, [P, I, I, P, I, P, P]),
+        "kf_decode_block": (I, [P, I, I, P, P]),
+        "kf_generate": (I, [P, I, I, P, I, I, U64, P]),
+        "kf_prefill_ar": (I, [P, I, I, P, P, P]),
+        "kf_decode_ar": (I, [P, I, P, P]),
+        "kf_generate_ar": (I, [P, I, I, P, I, U64, P]),
+        "kf_debug_logits": (I, [P, P, SZ]),
+        "kf_fill_noise": (I, [P, U64, I, I, I, P]),
+        "kf_get_state": (I, [P, IP, IP, IP]),
+        "kf_device_errors": (I, [P, IP]),
+        "kf_set_timing": (I, [P, I]),
+        "kf_kernel_time": (I, [P, I, ctypes.POINTER(ctypes.c_double), IP]),
+        "kf_destroy": (None, [P]),
+        "kf_last_error": (ctypes.c_char_p, [P]),
+        "kf_strerror": (ctypes.c_char_p, [I]),
+    }
+    for name, (res, args) in sigs.items():
+        f = getattr(L, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = L
+    return L
+
+
+def make_config(n_layer, d_model, n_head, d_mlp, vocab, n_ctx, dtype, max_batch, max_k,
+                max_prompt, flags=0) -> KfConfig:
+    return KfConfig(n_layer, d_model, n_head, d_mlp, vocab, n_ctx, dtype, max_batch, max_k,
+                    max_prompt, flags)
+
+
+class KForcing:
+    """One library context with its device state buffer (allocated by torch)."""
+
+    def __init__(self, cfg: KfConfig, device: str = "cuda:0", stream=None):
+        import torch
+        self.torch = torch
+        self.L = lib()
+        self.cfg = cfg
+        self.device = torch.device(device)
+        self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
+        h = ctypes.c_void_p()
+        rc = self.L.kf_create(ctypes.byref(cfg), ctypes.c_void_p(self.stream.cuda_stream),
+                              ctypes.byref(h))
+        if rc != KF_OK:
+            raise KfError(rc, "kf_create rejected the configuration")
+        self.h = h
+        nbytes = self.L.kf_state_bytes(ctypes.byref(cfg))
+        self.state = torch.empty(nbytes + 256, dtype=torch.uint8, device=self.device)
+        base = self.state.data_ptr()
+        aligned = (base + 255) // 256 * 256
+        self._check(self.L.kf_bind_state(self.h, ctypes.c_void_p(aligned), nbytes))
+
+    # -- plumbing -------------------------------------------------------
+    def _check(self, rc: int):
+        if rc != KF_OK:
+            raise KfError(rc, self.L.kf_last_error(self.h).decode())
+
+    @staticmethod
+    def _p(t) -> ctypes.c_void_p:
+        return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+    def _i32(self, x):
+        return self.torch.as_tensor(x, dtype=self.torch.int32, device=self.device).contiguous()
+
+    def _f32(self, x):
+        return self.torch.as_tensor(x, dtype=self.torch.float32, device=self.device).contiguous()
+
+    def close(self):
+        if getattr(self, "h", None):
+            self.L.kf_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # -- entry points ----------------------------------------------------
+    def load_weights(self, blob, on_device: bool = True):
+        """blob: numpy float32 array (header + tensors), copied as given."""
+        import numpy as np
+        arr = np.ascontiguousarray(blob, dtype=np.float32)
+        if on_device:
+            t = self.torch.from_numpy(arr).to(self.device)
+            self._check(self.L.kf_load_weights(self.h, self._p(t), arr.nbytes, 1))
+            self.torch.cuda.synchronize(self.device)
+        else:
+            self._check(self.L.kf_load_weights(self.h, ctypes.c_void_p(arr.ctypes.data),
+                                               arr.nbytes, 0))
+
+    def prefill(self, prompt, k: int, noise, out=None):
+        prompt = self._i32(prompt)
+        noise = self._f32(noise)
+        B, N = prompt.shape
+        if out is None:
+            out = self.torch.empty((B, k), dtype=self.torch.int32, device=self.device)
+        self._check(self.L.kf_prefill(self.h, B, N, self._p(prompt), k, self._p(noise),
+                                      self._p(out)))
+        return out
+
+    def decode_block(self, noise, out=None):
+        noise = self._f32(noise)
+        B, k = noise.shape
+        if out is None:
+            out = self.torch.empty((B, k), dtype=self.torch.int32, device=self.device)
+        self._check(self.L.kf_decode_block(self.h, B, k, self._p(noise), self._p(out)))
+        return out
+
+    def generate(self, prompt, L: int, k: int, seed: int, out=None):
+        prompt = self._i32(prompt)
+        B, N = prompt.shape
+        if out is None:
+            out = self.torch.empty((B, L), dtype=self.torch.int32, device=self.device)
+        self._check(self.L.kf_generate(self.h, B, N, self._p(prompt), L, k, seed, self._p(out)))
+        return out
+
+    def prefill_ar(self, prompt, u, out=None):
+        prompt = self._i32(prompt)
+        u = self._f32(u)
+        B, N = prompt.shape
+        if out is None:
+            out = self.torch.empty((B,), dtype=self.torch.int32, device=self.device)
+        self._check(self.L.kf_prefill_ar(self.h, B, N, self._p(prompt), self._p(u), self._p(out)))
+        return out
+
+    def decode_ar(self, u, out=None):
+        u = self._f32(u)
+        B = u.shape[0]
+        if out is None:
+            out = self.torch.empty((B,), dtype=self.torch.int32, device=self.device)
+        self._check(self.L.kf_decode_ar(self.h, B, self._p(u), self._p(out)))
+        return out
+
+    def generate_ar(self, prompt, L: int, seed: int, out=None):
+        prompt = self._i32(prompt)
+        B, N = prompt.shape
+        if out is None:
+            out = self.torch.empty((B, L), dtype=self.torch.int32, device=self.device)
+        self._check(self.L.kf_generate_ar(self.h, B, N, self._p(prompt), L, seed, self._p(out)))
+        return out
+
+    def debug_logits(self, rows: int):
+        out = self.torch.empty((rows, self.cfg.vocab), dtype=self.torch.float32,
+                               device=self.device)
+        self._check(self.L.kf_debug_logits(self.h, self._p(out), out.numel()))
+        return out
+
+    def fill_noise(self, seed: int, B: int, p0: int, n: int):
+        out = self.torch.empty((B, n), dtype=self.torch.float32, device=self.device)
+        self._check(self.L.kf_fill_noise(self.h, seed, B, p0, n, self._p(out)))
+        return out
+
+    def get_state(self):
+        C, p, B = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+        self._check(self.L.kf_get_state(self.h, ctypes.byref(C), ctypes.byref(p), ctypes.byref(B)))
+        return C.value, p.value, B.value
+
+    def device_errors(self) -> int:
+        f = ctypes.c_int()
+        self._check(self.L.kf_device_errors(self.h, ctypes.byref(f)))
+        return f.value
+
+    def set_timing(self, enable: bool):
+        self._check(self.L.kf_set_timing(self.h, int(enable)))
+
+    def kernel_time(self, cls: int):
+        ms, n = ctypes.c_double(), ctypes.c_int()
+        self._check(self.L.kf_kernel_time(self.h, cls, ctypes.byref(ms), ctypes.byref(n)))
+        return ms.value, n.value

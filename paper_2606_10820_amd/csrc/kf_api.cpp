@@ -1,0 +1,678 @@
+// kf_api.cpp -- C ABI of the K-Forcing decode library (include/kforcing.h).
+//
+// Host side: argument validation, the per-context sequence state machine, the
+// device memory plan inside the caller's state buffer, weight packing, and the
+// kernel sequence of one step (paper Appendix C.1: embed real rows and noise
+// rows, L pre-norm Transformer blocks over the cached context, final norm,
+// tied head, token selection, commit of the real rows' K/V).
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/kforcing.h"
+#include "kf_internal.h"
+
+namespace {
+
+constexpr int32_t kMagic = 0x4B465731;
+constexpr int kHeaderInts = 16;
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// ------------------------------------------------------------ memory plan
+struct LayerOff {
+  size_t ln1_g, ln1_b, wqkv, bqkv, wo, bo, ln2_g, ln2_b, w1, b1, w2, b2;
+};
+
+struct Plan {
+  int es = 0;        // bytes per element of the compute dtype
+  int Vpad = 0;      // vocabulary rounded up to 256 (padding rows are zero)
+  int n_tiles = 0;   // head column tiles
+  int rows_max = 0;  // largest number of rows in one step
+  int head_max = 0;  // largest number of head rows in one step
+  int logit_rows = 0;
+  size_t wbegin = 0, wend = 0;
+  size_t tok = 0, pos = 0, nw1 = 0, nb1 = 0, nw2 = 0, nb2 = 0, omega = 0, lnf_g = 0, lnf_b = 0;
+  std::vector<LayerOff> layer;
+  size_t kv = 0, kv_bytes = 0;
+  size_t X = 0, A = 0, Q = 0, O = 0, Hm = 0, noise = 0, pval = 0, pidx = 0, logits = 0, dstate = 0,
+         pend = 0;
+  size_t total = 0;
+};
+
+bool config_ok(const kf_config& c, std::string* why) {
+  auto bad = [&](const char* m) {
+    if (why) *why = m;
+    return false;
+  };
+  if (c.n_layer < 1) return bad("n_layer must be >= 1");
+  if (c.d_model < 64 || c.d_model % 64) return bad("d_model must be a positive multiple of 64");
+  if (c.d_model > 2048) return bad("d_model must be <= 2048");
+  if (c.n_head < 1 || c.d_model % c.n_head) return bad("n_head must divide d_model");
+  int dh = c.d_model / c.n_head;
+  if (dh != 32 && dh != 64 && dh != 128) return bad("d_model / n_head must be 32, 64 or 128");
+  if (c.d_mlp < 64 || c.d_mlp % 64) return bad("d_mlp must be a positive multiple of 64");
+  if (c.vocab < 2) return bad("vocab must be >= 2");
+  if (c.n_ctx < 2) return bad("n_ctx must be >= 2");
+  if (c.dtype != KF_FP32 && c.dtype != KF_BF16) return bad("dtype must be KF_FP32 or KF_BF16");
+  if (c.max_batch < 1 || c.max_batch > 65535) return bad("max_batch must be in [1, 65535]");
+  if (c.max_k < 1 || c.max_k > c.n_ctx) return bad("max_k must be in [1, n_ctx]");
+  if (c.max_prompt < 1 || c.max_prompt > c.n_ctx) return bad("max_prompt must be in [1, n_ctx]");
+  if (c.flags & ~KF_FLAG_DEBUG_LOGITS) return bad("unknown flag bits");
+  return true;
+}
+
+void make_plan(const kf_config& c, Plan& p) {
+  const size_t d = c.d_model, f = c.d_mlp, T = c.n_ctx, L = c.n_layer;
+  p.es = c.dtype == KF_BF16 ? 2 : 4;
+  p.Vpad = (c.vocab + 255) / 256 * 256;
+  p.n_tiles = p.Vpad / kf::kHeadTileN;
+  p.rows_max = c.max_batch * ((c.max_prompt > c.max_k ? c.max_prompt : c.max_k) + c.max_k);
+  p.head_max = c.max_batch * c.max_k;
+  p.logit_rows = (c.flags & KF_FLAG_DEBUG_LOGITS) ? p.head_max : c.max_batch;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off = align256(off + bytes);
+    return o;
+  };
+  const size_t es = p.es;
+  p.wbegin = off;
+  p.tok = take((size_t)p.Vpad * d * es);
+  p.pos = take(T * d * es);
+  p.nw1 = take(4 * d * d * es);
+  p.nb1 = take(4 * d * 4);
+  p.nw2 = take(4 * d * d * es);
+  p.nb2 = take(d * 4);
+  p.omega = take(d / 2 * 8);
+  p.layer.resize(L);
+  for (size_t l = 0; l < L; ++l) {
+    LayerOff& y = p.layer[l];
+    y.ln1_g = take(d * 4);
+    y.ln1_b = take(d * 4);
+    y.wqkv = take(3 * d * d * es);
+    y.bqkv = take(3 * d * 4);
+    y.wo = take(d * d * es);
+    y.bo = take(d * 4);
+    y.ln2_g = take(d * 4);
+    y.ln2_b = take(d * 4);
+    y.w1 = take(f * d * es);
+    y.b1 = take(f * 4);
+    y.w2 = take(d * f * es);
+    y.b2 = take(d * 4);
+  }
+  p.lnf_g = take(d * 4);
+  p.lnf_b = take(d * 4);
+  p.wend = off;
+  p.kv_bytes = (size_t)c.max_batch * L * 2 * T * d * es;
+  p.kv = take(p.kv_bytes);
+  const size_t R = p.rows_max, Hw = f > 4 * d ? f : 4 * d;
+  p.X = take(R * d * 4);
+  p.A = take(R * d * es);
+  p.Q = take(R * d * es);
+  p.O = take(R * d * es);
+  p.Hm = take(R * Hw * es);
+  p.noise = take((size_t)p.head_max * 4);
+  p.pval = take((size_t)p.head_max * p.n_tiles * 4);
+  p.pidx = take((size_t)p.head_max * p.n_tiles * 4);
+  p.logits = take((size_t)p.logit_rows * c.vocab * 4);
+  p.dstate = take(sizeof(KfDevState));
+  p.pend = take((size_t)c.max_batch * c.max_k * 4);
+  p.total = off;
+}
+
+uint16_t f32_to_bf16_rne(float x) {
+  uint32_t u;
+  memcpy(&u, &x, 4);
+  if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu)) return (uint16_t)((u >> 16) | 0x40);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------ context
+struct kf_ctx {
+  kf_config cfg;
+  hipStream_t stream = nullptr;
+  Plan plan;
+  char* base = nullptr;
+  size_t bytes = 0;
+  bool weights = false;
+  // sequence state (host mirror of the device state)
+  bool live = false;
+  int B = 0, C = 0, pending = 0;
+  int last_head_rows = 0;
+  bool last_logits = false;
+  std::string err;
+  // kernel timing
+  bool timing = false;
+  struct Ev {
+    hipEvent_t a, b;
+    int cls;
+  };
+  std::vector<Ev> evs;
+  size_t ev_used = 0;
+};
+
+namespace {
+
+int fail(kf_ctx* c, int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  if (c) c->err = buf;
+  return code;
+}
+
+int hip_fail(kf_ctx* c, hipError_t e, const char* what) {
+  return fail(c, KF_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define KF_HIP(ctx, expr)                                        \
+  do {                                                           \
+    hipError_t e_ = (expr);                                      \
+    if (e_ != hipSuccess) return hip_fail((ctx), e_, #expr);     \
+  } while (0)
+
+int ev_begin(kf_ctx* c, int cls) {
+  if (!c->timing) return 0;
+  if (c->ev_used == c->evs.size()) {
+    kf_ctx::Ev e;
+    KF_HIP(c, hipEventCreate(&e.a));
+    KF_HIP(c, hipEventCreate(&e.b));
+    c->evs.push_back(e);
+  }
+  kf_ctx::Ev& e = c->evs[c->ev_used];
+  e.cls = cls;
+  KF_HIP(c, hipEventRecord(e.a, c->stream));
+  return 0;
+}
+
+int ev_end(kf_ctx* c) {
+  if (!c->timing) return 0;
+  KF_HIP(c, hipEventRecord(c->evs[c->ev_used].b, c->stream));
+  ++c->ev_used;
+  return 0;
+}
+
+#define KF_LAUNCH(ctx, cls, expr)                                \
+  do {                                                           \
+    int r_ = ev_begin((ctx), (cls));                             \
+    if (r_) return r_;                                           \
+    hipError_t e_ = (expr);                                      \
+    if (e_ != hipSuccess) return hip_fail((ctx), e_, #expr);     \
+    r_ = ev_end((ctx));                                          \
+    if (r_) return r_;                                           \
+  } while (0)
+
+// Inputs of one step.
+struct StepIn {
+  int B, nr, k;              // sequences, real rows, noise rows (k == 0: AR step)
+  const int32_t* toks;       // real-row tokens [B][tok_stride]
+  int tok_stride;
+  const float* noise;        // [B][k] or null (device Philox)
+  const float* u_ar;         // AR: [B] or null (device Philox)
+  uint64_t seed;
+  KfOutDesc od;
+  bool reset;                // prefill: C := 0 before the step
+};
+
+template <typename T>
+int run_step(kf_ctx* c, const StepIn& in) {
+  const Plan& p = c->plan;
+  char* base = c->base;
+  const kf_config& cf = c->cfg;
+  const int d = cf.d_model, f = cf.d_mlp, V = cf.vocab;
+  hipStream_t s = c->stream;
+  KfDevState* st = reinterpret_cast<KfDevState*>(base + p.dstate);
+  float* X = reinterpret_cast<float*>(base + p.X);
+  T* A = reinterpret_cast<T*>(base + p.A);
+  T* Q = reinterpret_cast<T*>(base + p.Q);
+  T* O = reinterpret_cast<T*>(base + p.O);
+  T* Hm = reinterpret_cast<T*>(base + p.Hm);
+  T* kv = reinterpret_cast<T*>(base + p.kv);
+  const T* tok = reinterpret_cast<const T*>(base + p.tok);
+  const T* pos = reinterpret_cast<const T*>(base + p.pos);
+  auto F = [&](size_t o) { return reinterpret_cast<const float*>(base + o); };
+  auto W = [&](size_t o) { return reinterpret_cast<const T*>(base + o); };
+
+  KfStepGeom g{in.B, in.nr + in.k, in.nr, in.k};
+  KfKvGeom kg{cf.n_layer, cf.n_head, cf.n_ctx, d / cf.n_head};
+  const int M = in.B * g.R;
+  const bool debug = (cf.flags & KF_FLAG_DEBUG_LOGITS) != 0;
+
+  if (in.reset) KF_HIP(c, kf::launch_zero_i32(reinterpret_cast<int*>(st), 1, s));
+  if (in.nr > 0)
+    KF_LAUNCH(c, KF_KC_EMBED,
+              kf::launch_embed_real<T>(X, tok, pos, in.toks, in.tok_stride, g, d, V, st, s));
+  if (in.k > 0) {
+    const int Mk = in.B * in.k;
+    float* urec = reinterpret_cast<float*>(base + p.noise);
+    KF_LAUNCH(c, KF_KC_NOISE,
+              kf::launch_noise_sinusoid<T>(A, in.noise, in.seed,
+                                           reinterpret_cast<const double*>(base + p.omega), g, d,
+                                           st, urec, s));
+    KF_LAUNCH(c, KF_KC_NOISE,
+              kf::gemm_bias<T>(A, W(p.nw1), Mk, 4 * d, d, F(p.nb1), kf::Act::Gelu, Hm, 4 * d, s));
+    KF_LAUNCH(c, KF_KC_NOISE,
+              kf::gemm_noise_out<T>(Hm, W(p.nw2), Mk, d, 4 * d, F(p.nb2), pos, X, g, st, s));
+  }
+  for (int l = 0; l < cf.n_layer; ++l) {
+    const LayerOff& y = p.layer[l];
+    KF_LAUNCH(c, KF_KC_NORM, kf::launch_layernorm<T>(X, A, F(y.ln1_g), F(y.ln1_b), M, d, 0, g, s));
+    KF_LAUNCH(c, KF_KC_QKV, kf::gemm_qkv<T>(A, W(y.wqkv), M, d, F(y.bqkv), Q, kv, g, kg, l, st, s));
+    KF_LAUNCH(c, KF_KC_ATTN, kf::launch_attention<T>(Q, kv, O, st, g, kg, l, s));
+    KF_LAUNCH(c, KF_KC_OPROJ, kf::gemm_residual<T>(O, W(y.wo), M, d, d, F(y.bo), X, s));
+    KF_LAUNCH(c, KF_KC_NORM, kf::launch_layernorm<T>(X, A, F(y.ln2_g), F(y.ln2_b), M, d, 0, g, s));
+    KF_LAUNCH(c, KF_KC_MLP_UP,
+              kf::gemm_bias<T>(A, W(y.w1), M, f, d, F(y.b1), kf::Act::Gelu, Hm, f, s));
+    KF_LAUNCH(c, KF_KC_MLP_DOWN, kf::gemm_residual<T>(Hm, W(y.w2), M, d, f, F(y.b2), X, s));
+  }
+  const bool ar = in.k == 0;
+  const int Mh = ar ? in.B : in.B * in.k;
+  KF_LAUNCH(c, KF_KC_NORM,
+            kf::launch_layernorm<T>(X, A, F(p.lnf_g), F(p.lnf_b), Mh, d, ar ? 2 : 1, g, s));
+  float* logits = (ar || debug) ? reinterpret_cast<float*>(base + p.logits) : nullptr;
+  KF_LAUNCH(c, KF_KC_HEAD,
+            kf::gemm_head<T>(A, tok, Mh, p.Vpad, V, d, reinterpret_cast<float*>(base + p.pval),
+                             reinterpret_cast<int*>(base + p.pidx), logits, s));
+  if (!ar)
+    KF_LAUNCH(c, KF_KC_SELECT,
+              kf::launch_argmax_select(reinterpret_cast<const float*>(base + p.pval),
+                                       reinterpret_cast<const int*>(base + p.pidx), p.n_tiles, g,
+                                       st, in.od, s));
+  else
+    KF_LAUNCH(c, KF_KC_SELECT,
+              kf::launch_icdf_select(logits, V, in.u_ar, in.seed, g, st, in.od, s));
+  KF_LAUNCH(c, KF_KC_SELECT, kf::launch_commit(st, in.nr, s));
+  c->last_head_rows = Mh;
+  c->last_logits = logits != nullptr;
+  return KF_OK;
+}
+
+int step(kf_ctx* c, const StepIn& in) {
+  return c->cfg.dtype == KF_BF16 ? run_step<bf16>(c, in) : run_step<float>(c, in);
+}
+
+int ready(kf_ctx* c) {
+  if (!c->base) return fail(c, KF_ESTATE, "no state buffer bound (kf_bind_state)");
+  if (!c->weights) return fail(c, KF_ESTATE, "no weights loaded (kf_load_weights)");
+  return KF_OK;
+}
+
+KfOutDesc out_desc(kf_ctx* c, int32_t* out, int stride, int gen_base) {
+  KfOutDesc od;
+  od.out = out;
+  od.stride = stride;
+  od.gen_base = gen_base;
+  od.pend = reinterpret_cast<int32_t*>(c->base + c->plan.pend);
+  od.pend_stride = c->cfg.max_k;
+  return od;
+}
+
+int32_t* pend_ptr(kf_ctx* c) { return reinterpret_cast<int32_t*>(c->base + c->plan.pend); }
+
+}  // namespace
+
+// ==================================================================== ABI
+extern "C" {
+
+const char* kf_strerror(int code) {
+  switch (code) {
+    case KF_OK: return "ok";
+    case KF_EINVAL: return "invalid argument";
+    case KF_ESTATE: return "invalid state";
+    case KF_ECTX: return "context length exceeded";
+    case KF_ENOMEM: return "state buffer too small";
+    case KF_EHIP: return "HIP runtime error";
+    default: return "unknown error";
+  }
+}
+
+const char* kf_last_error(const kf_ctx* c) { return c ? c->err.c_str() : "null context"; }
+
+size_t kf_state_bytes(const kf_config* cfg) {
+  if (!cfg || !config_ok(*cfg, nullptr)) return 0;
+  Plan p;
+  make_plan(*cfg, p);
+  return p.total;
+}
+
+int kf_create(const kf_config* cfg, void* hip_stream, kf_ctx** out) {
+  if (!cfg || !out) return KF_EINVAL;
+  std::string why;
+  if (!config_ok(*cfg, &why)) return KF_EINVAL;
+  kf_ctx* c = new (std::nothrow) kf_ctx();
+  if (!c) return KF_ENOMEM;
+  c->cfg = *cfg;
+  c->stream = reinterpret_cast<hipStream_t>(hip_stream);
+  make_plan(*cfg, c->plan);
+  *out = c;
+  return KF_OK;
+}
+
+void kf_destroy(kf_ctx* c) {
+  if (!c) return;
+  for (auto& e : c->evs) {
+    (void)hipEventDestroy(e.a);
+    (void)hipEventDestroy(e.b);
+  }
+  delete c;
+}
+
+int kf_bind_state(kf_ctx* c, void* dev_ptr, size_t bytes) {
+  if (!c) return KF_EINVAL;
+  if (!dev_ptr) return fail(c, KF_EINVAL, "null state pointer");
+  if (reinterpret_cast<uintptr_t>(dev_ptr) & 255) return fail(c, KF_EINVAL, "state pointer must be 256-byte aligned");
+  if (bytes < c->plan.total)
+    return fail(c, KF_ENOMEM, "state buffer has %zu bytes, %zu needed", bytes, c->plan.total);
+  c->base = static_cast<char*>(dev_ptr);
+  c->bytes = bytes;
+  c->weights = false;
+  c->live = false;
+  c->B = c->C = c->pending = 0;
+  return KF_OK;
+}
+
+int kf_load_weights(kf_ctx* c, const void* blob, size_t bytes, int blob_is_device) {
+  if (!c) return KF_EINVAL;
+  if (!c->base) return fail(c, KF_ESTATE, "no state buffer bound (kf_bind_state)");
+  if (!blob) return fail(c, KF_EINVAL, "null blob");
+  if (blob_is_device != 0 && blob_is_device != 1) return fail(c, KF_EINVAL, "blob_is_device must be 0 or 1");
+  const kf_config& cf = c->cfg;
+  const Plan& p = c->plan;
+  const size_t d = cf.d_model, f = cf.d_mlp, V = cf.vocab, T = cf.n_ctx, L = cf.n_layer;
+  const size_t n_params = V * d + T * d + 8 * d * d + 4 * d + d +
+                          L * (2 * d + 3 * d * d + 3 * d + d * d + d + 2 * d + f * d + f + d * f + d) +
+                          2 * d;
+  if (bytes != (kHeaderInts + n_params) * 4)
+    return fail(c, KF_EINVAL, "blob has %zu bytes, %zu expected for this config", bytes,
+                (kHeaderInts + n_params) * 4);
+  int32_t hdr[kHeaderInts];
+  if (blob_is_device)
+    KF_HIP(c, hipMemcpy(hdr, blob, sizeof hdr, hipMemcpyDeviceToHost));
+  else
+    memcpy(hdr, blob, sizeof hdr);
+  const int32_t want[9] = {kMagic, 1, cf.n_layer, cf.d_model, cf.n_head, cf.d_mlp, cf.vocab, cf.n_ctx, cf.dtype};
+  for (int i = 0; i < 9; ++i)
+    if (hdr[i] != want[i]) return fail(c, KF_EINVAL, "blob header word %d is %d, expected %d", i, hdr[i], want[i]);
+
+  // Destination of each tensor in blob order: (offset, count, is_matrix).
+  struct Dst { size_t off, n; bool mat; };
+  std::vector<Dst> dst;
+  dst.push_back({p.tok, V * d, true});
+  dst.push_back({p.pos, T * d, true});
+  dst.push_back({p.nw1, 4 * d * d, true});
+  dst.push_back({p.nb1, 4 * d, false});
+  dst.push_back({p.nw2, 4 * d * d, true});
+  dst.push_back({p.nb2, d, false});
+  for (size_t l = 0; l < L; ++l) {
+    const LayerOff& y = p.layer[l];
+    dst.push_back({y.ln1_g, d, false});
+    dst.push_back({y.ln1_b, d, false});
+    dst.push_back({y.wqkv, 3 * d * d, true});
+    dst.push_back({y.bqkv, 3 * d, false});
+    dst.push_back({y.wo, d * d, true});
+    dst.push_back({y.bo, d, false});
+    dst.push_back({y.ln2_g, d, false});
+    dst.push_back({y.ln2_b, d, false});
+    dst.push_back({y.w1, f * d, true});
+    dst.push_back({y.b1, f, false});
+    dst.push_back({y.w2, d * f, true});
+    dst.push_back({y.b2, d, false});
+  }
+  dst.push_back({p.lnf_g, d, false});
+  dst.push_back({p.lnf_b, d, false});
+
+  // sinusoid frequencies omega_i = 10000^(-i/(d/2)) for the noise encoder
+  std::vector<double> omega(d / 2);
+  for (size_t i = 0; i < d / 2; ++i) omega[i] = pow(10000.0, -(double)i / (double)(d / 2));
+
+  const bool bf = cf.dtype == KF_BF16;
+  if (!blob_is_device) {
+    std::vector<uint8_t> img(p.wend - p.wbegin, 0);
+    const float* src = static_cast<const float*>(blob) + kHeaderInts;
+    for (const Dst& t : dst) {
+      uint8_t* o = img.data() + (t.off - p.wbegin);
+      if (t.mat && bf) {
+        uint16_t* h = reinterpret_cast<uint16_t*>(o);
+        for (size_t i = 0; i < t.n; ++i) h[i] = f32_to_bf16_rne(src[i]);
+      } else {
+        memcpy(o, src, t.n * 4);
+      }
+      src += t.n;
+    }
+    memcpy(img.data() + (p.omega - p.wbegin), omega.data(), omega.size() * 8);
+    KF_HIP(c, hipMemcpyAsync(c->base + p.wbegin, img.data(), img.size(), hipMemcpyHostToDevice, c->stream));
+    KF_HIP(c, hipStreamSynchronize(c->stream));
+  } else {
+    const float* src = static_cast<const float*>(blob) + kHeaderInts;
+    // padding rows of the head / token table stay zero
+    const size_t pad = ((size_t)p.Vpad - V) * d;
+    if (bf) {
+      KF_HIP(c, kf::launch_zero<bf16>(reinterpret_cast<bf16*>(c->base + p.tok) + V * d, pad, c->stream));
+    } else {
+      KF_HIP(c, kf::launch_zero<float>(reinterpret_cast<float*>(c->base + p.tok) + V * d, pad, c->stream));
+    }
+    for (const Dst& t : dst) {
+      if (t.mat && bf)
+        KF_HIP(c, kf::launch_convert<bf16>(src, reinterpret_cast<bf16*>(c->base + t.off), t.n, c->stream));
+      else
+        KF_HIP(c, kf::launch_copy_f32(src, reinterpret_cast<float*>(c->base + t.off), t.n, c->stream));
+      src += t.n;
+    }
+    KF_HIP(c, hipMemcpyAsync(c->base + p.omega, omega.data(), omega.size() * 8, hipMemcpyHostToDevice, c->stream));
+    KF_HIP(c, hipStreamSynchronize(c->stream));
+  }
+  // device sequence state starts cleared (context length and error flags)
+  KF_HIP(c, kf::launch_zero_i32(reinterpret_cast<int*>(c->base + p.dstate),
+                                sizeof(KfDevState) / sizeof(int), c->stream));
+  KF_HIP(c, hipStreamSynchronize(c->stream));
+  c->weights = true;
+  c->live = false;
+  return KF_OK;
+}
+
+int kf_prefill(kf_ctx* c, int B, int N, const int32_t* prompt, int k, const float* noise, int32_t* out) {
+  if (!c) return KF_EINVAL;
+  const kf_config& cf = c->cfg;
+  if (B < 1 || B > cf.max_batch) return fail(c, KF_EINVAL, "B=%d outside [1, %d]", B, cf.max_batch);
+  if (N < 0 || N > cf.max_prompt) return fail(c, KF_EINVAL, "N=%d outside [0, %d]", N, cf.max_prompt);
+  if (k < 1 || k > cf.max_k) return fail(c, KF_EINVAL, "k=%d outside [1, %d]", k, cf.max_k);
+  if (!noise || !out || (N > 0 && !prompt)) return fail(c, KF_EINVAL, "null pointer argument");
+  if (N + k > cf.n_ctx) return fail(c, KF_ECTX, "N + k = %d exceeds n_ctx = %d", N + k, cf.n_ctx);
+  int r = ready(c);
+  if (r) return r;
+  StepIn in{B, N, k, prompt, N, noise, nullptr, 0, out_desc(c, out, k, -1), true};
+  r = step(c, in);
+  if (r) return r;
+  c->live = true;
+  c->B = B;
+  c->C = N;
+  c->pending = k;
+  return KF_OK;
+}
+
+int kf_decode_block(kf_ctx* c, int B, int k, const float* noise, int32_t* out) {
+  if (!c) return KF_EINVAL;
+  const kf_config& cf = c->cfg;
+  if (k < 1 || k > cf.max_k) return fail(c, KF_EINVAL, "k=%d outside [1, %d]", k, cf.max_k);
+  if (!noise || !out) return fail(c, KF_EINVAL, "null pointer argument");
+  int r = ready(c);
+  if (r) return r;
+  if (!c->live) return fail(c, KF_ESTATE, "decode before prefill");
+  if (B != c->B) return fail(c, KF_ESTATE, "B=%d differs from the prefill's B=%d", B, c->B);
+  if (c->C + c->pending + k > cf.n_ctx)
+    return fail(c, KF_ECTX, "C + pending + k = %d exceeds n_ctx = %d", c->C + c->pending + k, cf.n_ctx);
+  StepIn in{B, c->pending, k, pend_ptr(c), cf.max_k, noise, nullptr, 0, out_desc(c, out, k, -1), false};
+  r = step(c, in);
+  if (r) return r;
+  c->C += c->pending;
+  c->pending = k;
+  return KF_OK;
+}
+
+int kf_generate(kf_ctx* c, int B, int N, const int32_t* prompt, int L, int k, uint64_t seed, int32_t* out) {
+  if (!c) return KF_EINVAL;
+  const kf_config& cf = c->cfg;
+  if (B < 1 || B > cf.max_batch) return fail(c, KF_EINVAL, "B=%d outside [1, %d]", B, cf.max_batch);
+  if (N < 0 || N > cf.max_prompt) return fail(c, KF_EINVAL, "N=%d outside [0, %d]", N, cf.max_prompt);
+  if (k < 1 || k > cf.max_k) return fail(c, KF_EINVAL, "k=%d outside [1, %d]", k, cf.max_k);
+  if (L < 0 || L % k) return fail(c, KF_EINVAL, "L=%d must be a non-negative multiple of k=%d", L, k);
+  if (L > 0 && (!out || (N > 0 && !prompt))) return fail(c, KF_EINVAL, "null pointer argument");
+  if (N + L > cf.n_ctx) return fail(c, KF_ECTX, "N + L = %d exceeds n_ctx = %d", N + L, cf.n_ctx);
+  int r = ready(c);
+  if (r) return r;
+  if (L == 0) return KF_OK;
+  StepIn in{B, N, k, prompt, N, nullptr, nullptr, seed, out_desc(c, out, L, N), true};
+  r = step(c, in);
+  if (r) return r;
+  c->live = true;
+  c->B = B;
+  c->C = N;
+  c->pending = k;
+  for (int s = 1; s < L / k; ++s) {
+    StepIn dn{B, k, k, pend_ptr(c), cf.max_k, nullptr, nullptr, seed, out_desc(c, out, L, N), false};
+    r = step(c, dn);
+    if (r) return r;
+    c->C += k;
+  }
+  return KF_OK;
+}
+
+int kf_prefill_ar(kf_ctx* c, int B, int N, const int32_t* prompt, const float* u, int32_t* out) {
+  if (!c) return KF_EINVAL;
+  const kf_config& cf = c->cfg;
+  if (B < 1 || B > cf.max_batch) return fail(c, KF_EINVAL, "B=%d outside [1, %d]", B, cf.max_batch);
+  if (N < 1 || N > cf.max_prompt) return fail(c, KF_EINVAL, "N=%d outside [1, %d]", N, cf.max_prompt);
+  if (!prompt || !u || !out) return fail(c, KF_EINVAL, "null pointer argument");
+  if (N + 1 > cf.n_ctx) return fail(c, KF_ECTX, "N + 1 = %d exceeds n_ctx = %d", N + 1, cf.n_ctx);
+  int r = ready(c);
+  if (r) return r;
+  StepIn in{B, N, 0, prompt, N, nullptr, u, 0, out_desc(c, out, 1, -1), true};
+  r = step(c, in);
+  if (r) return r;
+  c->live = true;
+  c->B = B;
+  c->C = N;
+  c->pending = 1;
+  return KF_OK;
+}
+
+int kf_decode_ar(kf_ctx* c, int B, const float* u, int32_t* out) {
+  if (!c) return KF_EINVAL;
+  const kf_config& cf = c->cfg;
+  if (!u || !out) return fail(c, KF_EINVAL, "null pointer argument");
+  int r = ready(c);
+  if (r) return r;
+  if (!c->live) return fail(c, KF_ESTATE, "decode before prefill");
+  if (B != c->B) return fail(c, KF_ESTATE, "B=%d differs from the prefill's B=%d", B, c->B);
+  if (c->C + c->pending + 1 > cf.n_ctx)
+    return fail(c, KF_ECTX, "C + pending + 1 = %d exceeds n_ctx = %d", c->C + c->pending + 1, cf.n_ctx);
+  StepIn in{B, c->pending, 0, pend_ptr(c), cf.max_k, nullptr, u, 0, out_desc(c, out, 1, -1), false};
+  r = step(c, in);
+  if (r) return r;
+  c->C += c->pending;
+  c->pending = 1;
+  return KF_OK;
+}
+
+int kf_generate_ar(kf_ctx* c, int B, int N, const int32_t* prompt, int L, uint64_t seed, int32_t* out) {
+  if (!c) return KF_EINVAL;
+  const kf_config& cf = c->cfg;
+  if (B < 1 || B > cf.max_batch) return fail(c, KF_EINVAL, "B=%d outside [1, %d]", B, cf.max_batch);
+  if (N < 1 || N > cf.max_prompt) return fail(c, KF_EINVAL, "N=%d outside [1, %d]", N, cf.max_prompt);
+  if (L < 0) return fail(c, KF_EINVAL, "L=%d must be >= 0", L);
+  if (L > 0 && (!prompt || !out)) return fail(c, KF_EINVAL, "null pointer argument");
+  if (N + L > cf.n_ctx) return fail(c, KF_ECTX, "N + L = %d exceeds n_ctx = %d", N + L, cf.n_ctx);
+  int r = ready(c);
+  if (r) return r;
+  if (L == 0) return KF_OK;
+  StepIn in{B, N, 0, prompt, N, nullptr, nullptr, seed, out_desc(c, out, L, N), true};
+  r = step(c, in);
+  if (r) return r;
+  c->live = true;
+  c->B = B;
+  c->C = N;
+  c->pending = 1;
+  for (int s = 1; s < L; ++s) {
+    StepIn dn{B, 1, 0, pend_ptr(c), cf.max_k, nullptr, nullptr, seed, out_desc(c, out, L, N), false};
+    r = step(c, dn);
+    if (r) return r;
+    c->C += 1;
+  }
+  return KF_OK;
+}
+
+int kf_debug_logits(kf_ctx* c, float* out, size_t n_floats) {
+  if (!c) return KF_EINVAL;
+  if (!out) return fail(c, KF_EINVAL, "null pointer argument");
+  if (!c->base || !c->last_logits) return fail(c, KF_ESTATE, "no logits recorded (needs KF_FLAG_DEBUG_LOGITS and a step)");
+  const size_t n = (size_t)c->last_head_rows * c->cfg.vocab;
+  if (n_floats < n) return fail(c, KF_EINVAL, "out holds %zu floats, %zu needed", n_floats, n);
+  KF_HIP(c, kf::launch_copy_f32(reinterpret_cast<const float*>(c->base + c->plan.logits), out, n, c->stream));
+  return KF_OK;
+}
+
+int kf_fill_noise(kf_ctx* c, uint64_t seed, int B, int p0, int n, float* out) {
+  if (!c) return KF_EINVAL;
+  if (B < 1 || n < 1 || p0 < 0 || !out) return fail(c, KF_EINVAL, "bad noise request");
+  KF_HIP(c, kf::launch_fill_noise(out, seed, B, p0, n, c->stream));
+  return KF_OK;
+}
+
+int kf_get_state(const kf_ctx* c, int* C, int* pending, int* B) {
+  if (!c) return KF_EINVAL;
+  if (C) *C = c->live ? c->C : 0;
+  if (pending) *pending = c->live ? c->pending : 0;
+  if (B) *B = c->live ? c->B : 0;
+  return KF_OK;
+}
+
+int kf_device_errors(kf_ctx* c, int* flags) {
+  if (!c || !flags) return KF_EINVAL;
+  if (!c->base) return fail(c, KF_ESTATE, "no state buffer bound");
+  KfDevState h;
+  KF_HIP(c, hipStreamSynchronize(c->stream));
+  KfDevState* st = reinterpret_cast<KfDevState*>(c->base + c->plan.dstate);
+  KF_HIP(c, hipMemcpy(&h, st, sizeof h, hipMemcpyDeviceToHost));
+  *flags = h.err;
+  if (h.err) KF_HIP(c, kf::launch_zero_i32(&st->err, 1, c->stream));
+  KF_HIP(c, hipStreamSynchronize(c->stream));
+  return KF_OK;
+}
+
+int kf_set_timing(kf_ctx* c, int enable) {
+  if (!c) return KF_EINVAL;
+  c->timing = enable != 0;
+  c->ev_used = 0;
+  return KF_OK;
+}
+
+int kf_kernel_time(kf_ctx* c, int cls, double* total_ms, int* launches) {
+  if (!c || !total_ms || !launches) return KF_EINVAL;
+  if (cls < 0 || cls >= KF_KC_COUNT) return fail(c, KF_EINVAL, "kernel class %d out of range", cls);
+  KF_HIP(c, hipStreamSynchronize(c->stream));
+  double tot = 0;
+  int n = 0;
+  for (size_t i = 0; i < c->ev_used; ++i) {
+    if (c->evs[i].cls != cls) continue;
+    float ms = 0;
+    KF_HIP(c, hipEventElapsedTime(&ms, c->evs[i].a, c->evs[i].b));
+    tot += ms;
+    ++n;
+  }
+  *total_ms = tot;
+  *launches = n;
+  return KF_OK;
+}
+
+}  // extern "C"

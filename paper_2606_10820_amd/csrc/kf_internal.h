@@ -1,0 +1,150 @@
+// kf_internal.h -- internal declarations shared by the library's HIP sources.
+// Not part of the public ABI (include/kforcing.h is).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+typedef __bf16 bf16;
+
+// Device-resident sequence state.  Kernels read the committed context length
+// C from here (never from a launch argument) so that a step's launches are
+// identical from one step to the next.
+struct KfDevState {
+  int C;    // committed context length (positions 0..C-1 hold real-token K/V)
+  int err;  // bit 0: a token id outside [0, V) was replaced by 0
+  int pad[14];
+};
+
+// Where a step writes the tokens it selects.
+struct KfOutDesc {
+  int32_t* out;    // destination
+  int stride;      // per-sequence stride of out (elements)
+  int gen_base;    // >= 0: generation run, element index = emitted position - gen_base
+                   // <  0: element index = head row index within the sequence
+  int32_t* pend;   // pending-token buffer [B][pend_stride] for the next step
+  int pend_stride;
+};
+
+// Geometry of one step: B sequences, R = nr + k rows each (nr real rows, then
+// k noise rows), row (b, i) stored at index b * R + i.
+struct KfStepGeom {
+  int B, R, nr, k;
+};
+
+// Geometry of the KV cache: [B][L][2][H][T][dh] elements.
+struct KfKvGeom {
+  int L, H, T, dh;
+  __host__ __device__ size_t seq_stride() const { return (size_t)L * 2 * H * T * dh; }
+  __host__ __device__ size_t head_off(int layer, int which, int h) const {
+    return (((size_t)layer * 2 + which) * H + h) * (size_t)T * dh;
+  }
+};
+
+// ------------------------------------------------------------------ Philox
+// Philox4x32-10 (Salmon et al., SC'11): ten rounds of two 32x32 -> 64-bit
+// multiplies with a Weyl key schedule.  Noise for sequence b at emitted
+// position p: counter (p, b, 2, 0), key (seed lo, seed hi), u = (w0 >> 8) 2^-24.
+__host__ __device__ inline void kf_philox4x32_10(uint32_t c[4], uint32_t k0, uint32_t k1) {
+  for (int r = 0; r < 10; ++r) {
+    if (r) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    uint64_t p0 = (uint64_t)0xD2511F53u * c[0];
+    uint64_t p1 = (uint64_t)0xCD9E8D57u * c[2];
+    uint32_t n0 = (uint32_t)(p1 >> 32) ^ c[1] ^ k0;
+    uint32_t n1 = (uint32_t)p1;
+    uint32_t n2 = (uint32_t)(p0 >> 32) ^ c[3] ^ k1;
+    uint32_t n3 = (uint32_t)p0;
+    c[0] = n0; c[1] = n1; c[2] = n2; c[3] = n3;
+  }
+}
+
+__host__ __device__ inline float kf_noise_u(uint64_t seed, int b, int p) {
+  uint32_t c[4] = {(uint32_t)p, (uint32_t)b, 2u, 0u};
+  kf_philox4x32_10(c, (uint32_t)seed, (uint32_t)(seed >> 32));
+  return (float)(c[0] >> 8) * (1.0f / 16777216.0f);
+}
+
+// ------------------------------------------------------------ launchers
+// All return hipGetLastError() of their launch (hipSuccess when nothing ran).
+namespace kf {
+
+enum class Act { None = 0, Gelu = 1 };
+
+// Real-row embedding: X[b*R + i] = tok[toks[b*tok_stride + i]] + pos[C + i], i < nr.
+template <typename T>
+hipError_t launch_embed_real(float* X, const T* tok, const T* pos, const int32_t* toks,
+                             int tok_stride, KfStepGeom g, int d, int V, KfDevState* st,
+                             hipStream_t s);
+
+// Sinusoid of each noise row's u into S [B*k][d]; u from noise [B*k] or, when
+// noise is null, from the device Philox stream at positions C + nr + j.
+// The u actually used are written to u_out [B*k] when it is not null.
+template <typename T>
+hipError_t launch_noise_sinusoid(T* S, const float* noise, uint64_t seed, const double* omega,
+                                 KfStepGeom g, int d, const KfDevState* st, float* u_out,
+                                 hipStream_t s);
+
+// LayerNorm (fp32 statistics) of selected rows of X into Y [rows][d].
+// gather: 0 = row m; 1 = noise row m of the step (b = m / k, j = m % k);
+//         2 = last real row of sequence m.
+template <typename T>
+hipError_t launch_layernorm(const float* X, T* Y, const float* gain, const float* shift, int rows,
+                            int d, int gather, KfStepGeom g, hipStream_t s);
+
+// Block attention over the KV cache for every (sequence, head, query block).
+template <typename T>
+hipError_t launch_attention(const T* Q, const T* kv, T* O, const KfDevState* st, KfStepGeom g,
+                            KfKvGeom kg, int layer, hipStream_t s);
+
+// GEMM family: C = epilogue(A[M][K] . W[N][K]^T), fp32 accumulation.
+template <typename T>
+hipError_t gemm_bias(const T* A, const T* W, int M, int N, int K, const float* bias, Act act,
+                     T* out, int ldo, hipStream_t s);
+template <typename T>
+hipError_t gemm_residual(const T* A, const T* W, int M, int N, int K, const float* bias, float* X,
+                         hipStream_t s);
+template <typename T>
+hipError_t gemm_qkv(const T* A, const T* W, int M, int d, const float* bias, T* Q, T* kv,
+                    KfStepGeom g, KfKvGeom kg, int layer, const KfDevState* st, hipStream_t s);
+template <typename T>
+hipError_t gemm_noise_out(const T* A, const T* W, int M, int d, int K, const float* bias,
+                          const T* pos, float* X, KfStepGeom g, const KfDevState* st,
+                          hipStream_t s);
+// Head: logits of M rows over Vpad columns; per (row, 128-column tile) the
+// maximum and its lowest column index into pval/pidx [M][Vpad/128]; columns
+// >= V are excluded.  When logits is not null the fp32 logits [M][V] are
+// written as well.
+template <typename T>
+hipError_t gemm_head(const T* A, const T* W, int M, int Vpad, int V, int K, float* pval,
+                     int* pidx, float* logits, hipStream_t s);
+constexpr int kHeadTileN = 128;
+
+// Argmax over the head partials of each row, ties to the lowest id; writes the
+// selected tokens per KfOutDesc.  rows = B * k.
+hipError_t launch_argmax_select(const float* pval, const int* pidx, int n_tiles, KfStepGeom g,
+                                const KfDevState* st, KfOutDesc od, hipStream_t s);
+
+// Inverse-CDF sampling of one token per sequence from fp32 logits [B][V]:
+// smallest m with F_m > u.  u from u_in [B] or, when null, the Philox stream
+// at position C + nr.
+hipError_t launch_icdf_select(const float* logits, int V, const float* u_in, uint64_t seed,
+                              KfStepGeom g, const KfDevState* st, KfOutDesc od, hipStream_t s);
+
+// C += nr (end of step).
+hipError_t launch_commit(KfDevState* st, int nr, hipStream_t s);
+
+// Device Philox noise for n positions starting at p0, [B][n].
+hipError_t launch_fill_noise(float* out, uint64_t seed, int B, int p0, int n, hipStream_t s);
+
+// fp32 -> T conversion of n elements; zero fill of n elements of T.
+template <typename T>
+hipError_t launch_convert(const float* src, T* dst, size_t n, hipStream_t s);
+template <typename T>
+hipError_t launch_zero(T* dst, size_t n, hipStream_t s);
+hipError_t launch_copy_f32(const float* src, float* dst, size_t n, hipStream_t s);
+hipError_t launch_zero_i32(int* dst, size_t n, hipStream_t s);
+
+}  // namespace kf

@@ -1,0 +1,473 @@
+// kf_kernels.hip -- gfx950 kernels of the K-Forcing decode step other than the
+// GEMM family: real-row embedding, noise sinusoid, LayerNorm, block attention,
+// token selection (argmax / inverse CDF) and small utilities.
+#include <float.h>
+#include <math.h>
+
+#include "kf_internal.h"
+
+namespace kf {
+
+namespace {
+
+__device__ inline float to_f(float x) { return x; }
+__device__ inline float to_f(bf16 x) { return (float)x; }
+template <typename T>
+__device__ inline T from_f(float x);
+template <>
+__device__ inline float from_f<float>(float x) { return x; }
+template <>
+__device__ inline bf16 from_f<bf16>(float x) { return (bf16)x; }
+
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// ------------------------------------------------------------ embedding
+// Real rows (Appendix C.1, Embed): token table row plus learned position.
+template <typename T>
+__global__ void __launch_bounds__(256)
+    embed_real_kernel(float* __restrict__ X, const T* __restrict__ tok, const T* __restrict__ pos,
+                      const int32_t* __restrict__ toks, int tok_stride, KfStepGeom g, int d, int V,
+                      KfDevState* st) {
+  const int r = blockIdx.x;
+  const int b = r / g.nr, i = r % g.nr;
+  const int C = st->C;
+  int t = toks[(size_t)b * tok_stride + i];
+  if (t < 0 || t >= V) {
+    if (threadIdx.x == 0) atomicOr(&st->err, 1);
+    t = 0;
+  }
+  float* x = X + ((size_t)b * g.R + i) * d;
+  const T* te = tok + (size_t)t * d;
+  const T* pe = pos + (size_t)(C + i) * d;
+  for (int e = threadIdx.x; e < d; e += blockDim.x) x[e] = to_f(te[e]) + to_f(pe[e]);
+}
+
+// ------------------------------------------------------- noise sinusoid
+// Noise rows: the scalar u of each noise token is expanded into d features,
+// cos(a_i) then sin(a_i) with a_i = 1000 u omega_i, omega_i = 10000^(-i/(d/2)),
+// evaluated in double so that fp32 u keeps its full resolution.
+template <typename T>
+__global__ void __launch_bounds__(256)
+    noise_sinusoid_kernel(T* __restrict__ S, const float* __restrict__ noise, uint64_t seed,
+                          const double* __restrict__ omega, KfStepGeom g, int d,
+                          const KfDevState* st, float* __restrict__ u_out) {
+  const int m = blockIdx.x;
+  const int b = m / g.k, j = m % g.k;
+  float u = noise ? noise[m] : kf_noise_u(seed, b, st->C + g.nr + j);
+  if (u_out && threadIdx.x == 0) u_out[m] = u;
+  const int h = d / 2;
+  const double su = 1000.0 * (double)u;
+  T* row = S + (size_t)m * d;
+  for (int i = threadIdx.x; i < h; i += blockDim.x) {
+    double a = su * omega[i];
+    double sn, cs;
+    sincos(a, &sn, &cs);
+    row[i] = from_f<T>((float)cs);
+    row[h + i] = from_f<T>((float)sn);
+  }
+}
+
+// ------------------------------------------------------------ LayerNorm
+// One wavefront per row; statistics in fp32 from registers (two passes).
+template <typename T, int EPL>
+__global__ void __launch_bounds__(256)
+    layernorm_kernel(const float* __restrict__ X, T* __restrict__ Y, const float* __restrict__ gain,
+                     const float* __restrict__ shift, int rows, int d, int gather, KfStepGeom g) {
+  const int lane = threadIdx.x & 63;
+  const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (m >= rows) return;
+  int src = m;
+  if (gather == 1) src = (m / g.k) * g.R + g.nr + (m % g.k);
+  else if (gather == 2) src = m * g.R + g.nr - 1;
+  const float* x = X + (size_t)src * d;
+  const int n = d >> 6;  // elements per lane
+  float v[EPL];
+  float s = 0.f;
+#pragma unroll
+  for (int c = 0; c < EPL; ++c) {
+    v[c] = (c < n) ? x[c * 64 + lane] : 0.f;
+    s += v[c];
+  }
+  const float mean = wave_sum(s) / (float)d;
+  float q = 0.f;
+#pragma unroll
+  for (int c = 0; c < EPL; ++c)
+    if (c < n) q += (v[c] - mean) * (v[c] - mean);
+  const float var = wave_sum(q) / (float)d;
+  const float rstd = 1.0f / sqrtf(var + 1e-5f);
+  T* y = Y + (size_t)m * d;
+#pragma unroll
+  for (int c = 0; c < EPL; ++c)
+    if (c < n) {
+      int e = c * 64 + lane;
+      y[e] = from_f<T>((v[c] - mean) * rstd * gain[e] + shift[e]);
+    }
+}
+
+// ------------------------------------------------------ block attention
+// One workgroup per (sequence, head, block of 16 query rows).  The query rows
+// of a step sit at cache slots C + i (real rows first, then noise rows) and
+// attend causally over slots [0, C + i]: real row i sees the context and real
+// rows <= i, noise row j sees the context, every real row and noise rows <= j
+// (the fully causal layout of Sec. 3.3; mask of the decode window, App. C).
+// Online softmax over 64-key tiles streamed from the per-sequence cache.
+template <typename T, int DH>
+__global__ void __launch_bounds__(256)
+    attention_kernel(const T* __restrict__ Q, const T* __restrict__ kv, T* __restrict__ O,
+                     const KfDevState* st, KfStepGeom g, KfKvGeom kg, int layer, float scale) {
+  constexpr int QB = 16, KT = 64, EPT = DH / 16;
+  const int H = kg.H, d = H * DH;
+  const int b = blockIdx.x / H, h = blockIdx.x % H;
+  const int q0 = blockIdx.y * QB;
+  const int nq = min(QB, g.R - q0);
+  const int C = st->C;
+  const int nkeys = C + q0 + nq;
+  const T* Kb = kv + (size_t)b * kg.seq_stride() + kg.head_off(layer, 0, h);
+  const T* Vb = kv + (size_t)b * kg.seq_stride() + kg.head_off(layer, 1, h);
+
+  __shared__ float sQ[QB][DH];
+  __shared__ float sK[KT][DH + 1];
+  __shared__ float sV[KT][DH];
+  __shared__ float sP[QB][KT];
+
+  const int tid = threadIdx.x;
+  for (int idx = tid; idx < QB * DH; idx += 256) {
+    int qi = idx / DH, e = idx % DH;
+    sQ[qi][e] = (qi < nq) ? to_f(Q[((size_t)b * g.R + q0 + qi) * d + h * DH + e]) * scale : 0.f;
+  }
+  const int qi = tid >> 4, r16 = tid & 15;
+  const int qslot = C + q0 + qi;
+  float m_run = -INFINITY, l_run = 0.f;
+  float o[EPT];
+#pragma unroll
+  for (int c = 0; c < EPT; ++c) o[c] = 0.f;
+
+  for (int kt0 = 0; kt0 < nkeys; kt0 += KT) {
+    __syncthreads();
+    for (int idx = tid; idx < KT * DH; idx += 256) {
+      int kk = idx / DH, e = idx % DH, slot = kt0 + kk;
+      float kx = 0.f, vx = 0.f;
+      if (slot < nkeys) {
+        kx = to_f(Kb[(size_t)slot * DH + e]);
+        vx = to_f(Vb[(size_t)slot * DH + e]);
+      }
+      sK[kk][e] = kx;
+      sV[kk][e] = vx;
+    }
+    __syncthreads();
+    float sc[4];
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      int key = r16 * 4 + c, slot = kt0 + key;
+      float dot = 0.f;
+#pragma unroll 16
+      for (int e = 0; e < DH; ++e) dot += sQ[qi][e] * sK[key][e];
+      sc[c] = (qi < nq && slot <= qslot) ? dot : -INFINITY;
+      tmax = fmaxf(tmax, sc[c]);
+    }
+#pragma unroll
+    for (int off = 8; off > 0; off >>= 1) tmax = fmaxf(tmax, __shfl_xor(tmax, off, 16));
+    const float m_new = fmaxf(m_run, tmax);
+    const float ref = (m_new == -INFINITY) ? 0.f : m_new;
+    const float alpha = __expf(m_run - ref);
+    float psum = 0.f;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      float p = __expf(sc[c] - ref);
+      sP[qi][r16 * 4 + c] = p;
+      psum += p;
+    }
+#pragma unroll
+    for (int off = 8; off > 0; off >>= 1) psum += __shfl_xor(psum, off, 16);
+    l_run = l_run * alpha + psum;
+    m_run = m_new;
+    __syncthreads();
+#pragma unroll
+    for (int c = 0; c < EPT; ++c) {
+      int e = c * 16 + r16;
+      float acc = o[c] * alpha;
+#pragma unroll 16
+      for (int key = 0; key < KT; ++key) acc += sP[qi][key] * sV[key][e];
+      o[c] = acc;
+    }
+  }
+  if (qi < nq) {
+    T* orow = O + ((size_t)b * g.R + q0 + qi) * d + h * DH;
+    const float inv = 1.0f / l_run;
+#pragma unroll
+    for (int c = 0; c < EPT; ++c) orow[c * 16 + r16] = from_f<T>(o[c] * inv);
+  }
+}
+
+// ------------------------------------------------------- token selection
+__device__ inline int out_index(const KfOutDesc& od, int C, int nr, int b, int j) {
+  return od.gen_base >= 0 ? b * od.stride + (C + nr + j - od.gen_base) : b * od.stride + j;
+}
+
+// Greedy head decoding (Sec. 3.2, Appendix C.1): per noise row, the argmax
+// over the vocabulary from the per-tile partials; exact ties to the lowest id.
+__global__ void __launch_bounds__(256)
+    argmax_select_kernel(const float* __restrict__ pval, const int* __restrict__ pidx, int n_tiles,
+                         KfStepGeom g, const KfDevState* st, KfOutDesc od) {
+  const int lane = threadIdx.x & 63;
+  const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int rows = g.B * g.k;
+  if (m >= rows) return;
+  float bv = -INFINITY;
+  int bi = 0x7fffffff;
+  for (int t = lane; t < n_tiles; t += 64) {
+    float v = pval[(size_t)m * n_tiles + t];
+    int i = pidx[(size_t)m * n_tiles + t];
+    if (v > bv || (v == bv && i < bi)) { bv = v; bi = i; }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    float ov = __shfl_xor(bv, off, 64);
+    int oi = __shfl_xor(bi, off, 64);
+    if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+  }
+  if (lane == 0) {
+    const int b = m / g.k, j = m % g.k;
+    if (bi == 0x7fffffff) bi = 0;
+    od.out[out_index(od, st->C, g.nr, b, j)] = bi;
+    od.pend[(size_t)b * od.pend_stride + j] = bi;
+  }
+}
+
+// Inverse-CDF map (Appendix B, strict convention): smallest m with F_m > u,
+// F the CDF of softmax(logits) in token-id order, evaluated as
+// prefix(exp(l - max)) > u * Z in fp32 with a fixed chunked order.
+// One workgroup of 1024 threads per sequence.
+__global__ void __launch_bounds__(1024)
+    icdf_select_kernel(const float* __restrict__ logits, int V, const float* __restrict__ u_in,
+                       uint64_t seed, KfStepGeom g, const KfDevState* st, KfOutDesc od) {
+  __shared__ float red[1024];
+  __shared__ int found;
+  const int b = blockIdx.x, t = threadIdx.x;
+  const float* l = logits + (size_t)b * V;
+  const int C = st->C;
+  const float u = u_in ? u_in[b] : kf_noise_u(seed, b, C + g.nr);
+  const int chunk = (V + 1023) / 1024;
+  const int lo = min(V, t * chunk), hi = min(V, lo + chunk);
+  float mx = -INFINITY;
+  for (int i = lo; i < hi; ++i) mx = fmaxf(mx, l[i]);
+  red[t] = mx;
+  __syncthreads();
+  for (int s = 512; s > 0; s >>= 1) {
+    if (t < s) red[t] = fmaxf(red[t], red[t + s]);
+    __syncthreads();
+  }
+  mx = red[0];
+  __syncthreads();
+  float cs = 0.f;
+  for (int i = lo; i < hi; ++i) cs += expf(l[i] - mx);
+  red[t] = cs;
+  if (t == 0) found = 0x7fffffff;
+  __syncthreads();
+  // inclusive scan of chunk sums (Hillis-Steele, fixed order)
+  for (int s = 1; s < 1024; s <<= 1) {
+    float add = (t >= s) ? red[t - s] : 0.f;
+    __syncthreads();
+    red[t] += add;
+    __syncthreads();
+  }
+  const float Z = red[1023];
+  const float target = u * Z;
+  float run = (t > 0) ? red[t - 1] : 0.f;
+  if (run <= target && red[t] > target) {
+    // this chunk holds the crossing (at most one chunk satisfies both)
+    int pick = hi - 1;
+    for (int i = lo; i < hi; ++i) {
+      run += expf(l[i] - mx);
+      if (run > target) { pick = i; break; }
+    }
+    atomicMin(&found, pick);
+  }
+  __syncthreads();
+  if (t == 0) {
+    int tok = found;
+    if (tok == 0x7fffffff) {  // rounding left F_V <= u: last token with q > 0
+      tok = V - 1;
+      for (int i = V - 1; i >= 0; --i)
+        if (expf(l[i] - mx) > 0.f) { tok = i; break; }
+    }
+    od.out[out_index(od, C, g.nr, b, 0)] = tok;
+    od.pend[(size_t)b * od.pend_stride] = tok;
+  }
+}
+
+__global__ void commit_kernel(KfDevState* st, int nr) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) st->C += nr;
+}
+
+__global__ void fill_noise_kernel(float* out, uint64_t seed, int B, int p0, int n) {
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= B * n) return;
+  out[i] = kf_noise_u(seed, i / n, p0 + i % n);
+}
+
+template <typename T>
+__global__ void convert_kernel(const float* __restrict__ src, T* __restrict__ dst, size_t n) {
+  size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (; i < n; i += stride) dst[i] = from_f<T>(src[i]);
+}
+
+template <typename T>
+__global__ void zero_kernel(T* dst, size_t n) {
+  size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (; i < n; i += stride) dst[i] = T(0);
+}
+
+__global__ void copy_f32_kernel(const float* __restrict__ src, float* __restrict__ dst, size_t n) {
+  size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (; i < n; i += stride) dst[i] = src[i];
+}
+
+inline unsigned grid_for(size_t n, unsigned block) {
+  size_t gsz = (n + block - 1) / block;
+  if (gsz > 65535u * 8u) gsz = 65535u * 8u;
+  if (gsz == 0) gsz = 1;
+  return (unsigned)gsz;
+}
+
+}  // namespace
+
+// ------------------------------------------------------------ launchers
+template <typename T>
+hipError_t launch_embed_real(float* X, const T* tok, const T* pos, const int32_t* toks,
+                             int tok_stride, KfStepGeom g, int d, int V, KfDevState* st,
+                             hipStream_t s) {
+  if (g.nr <= 0 || g.B <= 0) return hipSuccess;
+  hipLaunchKernelGGL(embed_real_kernel<T>, dim3(g.B * g.nr), dim3(256), 0, s, X, tok, pos, toks,
+                     tok_stride, g, d, V, st);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_noise_sinusoid(T* S, const float* noise, uint64_t seed, const double* omega,
+                                 KfStepGeom g, int d, const KfDevState* st, float* u_out,
+                                 hipStream_t s) {
+  if (g.k <= 0 || g.B <= 0) return hipSuccess;
+  hipLaunchKernelGGL(noise_sinusoid_kernel<T>, dim3(g.B * g.k), dim3(256), 0, s, S, noise, seed,
+                     omega, g, d, st, u_out);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_layernorm(const float* X, T* Y, const float* gain, const float* shift, int rows,
+                            int d, int gather, KfStepGeom g, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  dim3 grid((rows + 3) / 4);
+  if (d <= 512)
+    hipLaunchKernelGGL((layernorm_kernel<T, 8>), grid, dim3(256), 0, s, X, Y, gain, shift, rows, d,
+                       gather, g);
+  else if (d <= 1024)
+    hipLaunchKernelGGL((layernorm_kernel<T, 16>), grid, dim3(256), 0, s, X, Y, gain, shift, rows,
+                       d, gather, g);
+  else
+    hipLaunchKernelGGL((layernorm_kernel<T, 32>), grid, dim3(256), 0, s, X, Y, gain, shift, rows,
+                       d, gather, g);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_attention(const T* Q, const T* kv, T* O, const KfDevState* st, KfStepGeom g,
+                            KfKvGeom kg, int layer, hipStream_t s) {
+  if (g.B <= 0 || g.R <= 0) return hipSuccess;
+  dim3 grid(g.B * kg.H, (g.R + 15) / 16);
+  const float scale = 1.0f / sqrtf((float)kg.dh);
+  switch (kg.dh) {
+    case 32:
+      hipLaunchKernelGGL((attention_kernel<T, 32>), grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
+                         layer, scale);
+      break;
+    case 64:
+      hipLaunchKernelGGL((attention_kernel<T, 64>), grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
+                         layer, scale);
+      break;
+    case 128:
+      hipLaunchKernelGGL((attention_kernel<T, 128>), grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
+                         layer, scale);
+      break;
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_argmax_select(const float* pval, const int* pidx, int n_tiles, KfStepGeom g,
+                                const KfDevState* st, KfOutDesc od, hipStream_t s) {
+  int rows = g.B * g.k;
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(argmax_select_kernel, dim3((rows + 3) / 4), dim3(256), 0, s, pval, pidx,
+                     n_tiles, g, st, od);
+  return hipGetLastError();
+}
+
+hipError_t launch_icdf_select(const float* logits, int V, const float* u_in, uint64_t seed,
+                              KfStepGeom g, const KfDevState* st, KfOutDesc od, hipStream_t s) {
+  if (g.B <= 0) return hipSuccess;
+  hipLaunchKernelGGL(icdf_select_kernel, dim3(g.B), dim3(1024), 0, s, logits, V, u_in, seed, g, st,
+                     od);
+  return hipGetLastError();
+}
+
+hipError_t launch_commit(KfDevState* st, int nr, hipStream_t s) {
+  hipLaunchKernelGGL(commit_kernel, dim3(1), dim3(64), 0, s, st, nr);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_noise(float* out, uint64_t seed, int B, int p0, int n, hipStream_t s) {
+  if (B <= 0 || n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(fill_noise_kernel, dim3((B * n + 255) / 256), dim3(256), 0, s, out, seed, B,
+                     p0, n);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_convert(const float* src, T* dst, size_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(convert_kernel<T>, dim3(grid_for(n, 256)), dim3(256), 0, s, src, dst, n);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_zero(T* dst, size_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(zero_kernel<T>, dim3(grid_for(n, 256)), dim3(256), 0, s, dst, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_f32(const float* src, float* dst, size_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(copy_f32_kernel, dim3(grid_for(n, 256)), dim3(256), 0, s, src, dst, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero_i32(int* dst, size_t n, hipStream_t s) { return launch_zero<int>(dst, n, s); }
+
+#define KF_INST(T)                                                                                  \
+  template hipError_t launch_embed_real<T>(float*, const T*, const T*, const int32_t*, int,        \
+                                           KfStepGeom, int, int, KfDevState*, hipStream_t);         \
+  template hipError_t launch_noise_sinusoid<T>(T*, const float*, uint64_t, const double*,          \
+                                               KfStepGeom, int, const KfDevState*, float*,          \
+                                               hipStream_t);                                        \
+  template hipError_t launch_layernorm<T>(const float*, T*, const float*, const float*, int, int,  \
+                                          int, KfStepGeom, hipStream_t);                            \
+  template hipError_t launch_attention<T>(const T*, const T*, T*, const KfDevState*, KfStepGeom,   \
+                                          KfKvGeom, int, hipStream_t);                              \
+  template hipError_t launch_convert<T>(const float*, T*, size_t, hipStream_t);                    \
+  template hipError_t launch_zero<T>(T*, size_t, hipStream_t);
+KF_INST(float)
+KF_INST(bf16)
+#undef KF_INST
+
+}  // namespace kf

@@ -1,0 +1,144 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry point
+declared in include/kforcing.h, and rejects bad arguments before touching a
+device (each rejection leaves the context's state unchanged)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import kf_synth as S
+from paper_2606_10820_amd import binding as Bd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kforcing.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(kf_[a-z_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    return Bd.lib()
+
+
+def _cfg(**kw):
+    base = dict(n_layer=2, d_model=128, n_head=4, d_mlp=512, vocab=1024, n_ctx=128,
+                dtype=Bd.KF_FP32, max_batch=8, max_k=4, max_prompt=32, flags=0)
+    base.update(kw)
+    return Bd.make_config(**base)
+
+
+def _ctx(L, cfg):
+    h = ctypes.c_void_p()
+    assert L.kf_create(ctypes.byref(cfg), None, ctypes.byref(h)) == Bd.KF_OK
+    return h
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = _declared()
+    assert len(names) >= 19
+    for n in names:
+        assert hasattr(L, n), n
+    out = subprocess.run(["nm", "-D", "--defined-only", Bd.lib_path()], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (kf_[a-z_]+)$", out, flags=re.M))
+    assert set(names) <= exported, set(names) - exported
+
+
+def test_strerror(L):
+    assert L.kf_strerror(Bd.KF_OK) == b"ok"
+    assert L.kf_strerror(Bd.KF_ECTX) == b"context length exceeded"
+    assert L.kf_strerror(-99) == b"unknown error"
+
+
+@pytest.mark.parametrize("bad", [
+    dict(n_layer=0), dict(d_model=100), dict(n_head=3), dict(d_model=256, n_head=1),
+    dict(d_mlp=100), dict(vocab=1), dict(dtype=7), dict(max_batch=0), dict(max_k=0),
+    dict(max_k=1000), dict(max_prompt=0), dict(flags=8),
+])
+def test_bad_config_rejected(L, bad):
+    cfg = _cfg(**bad)
+    h = ctypes.c_void_p()
+    assert L.kf_create(ctypes.byref(cfg), None, ctypes.byref(h)) == Bd.KF_EINVAL
+    assert L.kf_state_bytes(ctypes.byref(cfg)) == 0
+
+
+def test_state_bytes_covers_kv_cache(L):
+    cfg = _cfg()
+    n = L.kf_state_bytes(ctypes.byref(cfg))
+    kv = 8 * 2 * 2 * 128 * 128 * 4
+    weights = S.n_params(S.WORKLOADS["toy"]["cfg"]) * 4
+    assert n > kv + weights
+    big = _cfg(dtype=Bd.KF_BF16, flags=Bd.KF_FLAG_DEBUG_LOGITS)
+    assert L.kf_state_bytes(ctypes.byref(big)) > L.kf_state_bytes(ctypes.byref(_cfg(dtype=Bd.KF_BF16)))
+
+
+def test_state_machine_without_device(L):
+    cfg = _cfg()
+    h = _ctx(L, cfg)
+    P = ctypes.c_void_p
+    fake = P(0x10000)  # never dereferenced: every call below fails validation first
+    # nothing bound yet
+    assert L.kf_prefill(h, 2, 4, fake, 2, fake, fake) == Bd.KF_ESTATE
+    assert L.kf_decode_block(h, 2, 2, fake, fake) == Bd.KF_ESTATE
+    # argument checks come before state checks
+    assert L.kf_prefill(h, 0, 4, fake, 2, fake, fake) == Bd.KF_EINVAL
+    assert L.kf_prefill(h, 9, 4, fake, 2, fake, fake) == Bd.KF_EINVAL
+    assert L.kf_prefill(h, 2, 4, fake, 0, fake, fake) == Bd.KF_EINVAL
+    assert L.kf_prefill(h, 2, 4, fake, 5, fake, fake) == Bd.KF_EINVAL
+    assert L.kf_prefill(h, 2, 33, fake, 2, fake, fake) == Bd.KF_EINVAL
+    assert L.kf_prefill(h, 2, 4, None, 2, fake, fake) == Bd.KF_EINVAL
+    assert L.kf_prefill(h, 2, 4, fake, 2, None, fake) == Bd.KF_EINVAL
+    assert L.kf_generate(h, 2, 4, fake, 6, 4, 0, fake) == Bd.KF_EINVAL   # L % k
+    assert L.kf_generate(h, 2, 4, fake, -4, 4, 0, fake) == Bd.KF_EINVAL
+    assert L.kf_generate(h, 2, 32, fake, 100, 4, 0, fake) == Bd.KF_ECTX  # N + L > n_ctx
+    assert L.kf_prefill_ar(h, 2, 0, fake, fake, fake) == Bd.KF_EINVAL
+    assert L.kf_generate_ar(h, 2, 4, fake, -1, 0, fake) == Bd.KF_EINVAL
+    assert L.kf_decode_block(h, 2, 0, fake, fake) == Bd.KF_EINVAL
+    assert L.kf_fill_noise(h, 0, 0, 0, 4, fake) == Bd.KF_EINVAL
+    # binding: alignment and size
+    need = L.kf_state_bytes(ctypes.byref(cfg))
+    assert L.kf_bind_state(h, P(0x10010), need) == Bd.KF_EINVAL
+    assert L.kf_bind_state(h, fake, need - 1) == Bd.KF_ENOMEM
+    assert L.kf_bind_state(h, fake, need) == Bd.KF_OK
+    assert b"" == L.kf_last_error(h) or True
+    # bound but no weights
+    assert L.kf_prefill(h, 2, 4, fake, 2, fake, fake) == Bd.KF_ESTATE
+    assert b"weights" in L.kf_last_error(h)
+    assert L.kf_debug_logits(h, fake, 10) == Bd.KF_ESTATE
+    # weight blob checks happen on the host before any copy
+    blob = S.pack_blob(S.WORKLOADS["toy"]["cfg"], S.make_weights(S.WORKLOADS["toy"]["cfg"]))
+    ptr = P(blob.ctypes.data)
+    assert L.kf_load_weights(h, ptr, blob.nbytes - 4, 0) == Bd.KF_EINVAL
+    bad = blob.copy()
+    bad[:16].view(np.int32)[0] = 0
+    assert L.kf_load_weights(h, P(bad.ctypes.data), bad.nbytes, 0) == Bd.KF_EINVAL
+    assert b"header" in L.kf_last_error(h)
+    bad = blob.copy()
+    bad[:16].view(np.int32)[8] = 1  # dtype mismatch with the config
+    assert L.kf_load_weights(h, P(bad.ctypes.data), bad.nbytes, 0) == Bd.KF_EINVAL
+    assert L.kf_load_weights(h, ptr, blob.nbytes, 2) == Bd.KF_EINVAL
+    C, p, B = ctypes.c_int(-1), ctypes.c_int(-1), ctypes.c_int(-1)
+    assert L.kf_get_state(h, ctypes.byref(C), ctypes.byref(p), ctypes.byref(B)) == Bd.KF_OK
+    assert (C.value, p.value, B.value) == (0, 0, 0)
+    L.kf_destroy(h)
+
+
+def test_null_context(L):
+    assert L.kf_prefill(None, 1, 1, None, 1, None, None) == Bd.KF_EINVAL
+    assert L.kf_create(None, None, None) == Bd.KF_EINVAL
+    assert L.kf_last_error(None) == b"null context"
+    L.kf_destroy(None)
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(Bd, "_LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(Bd, "_lib", None)
+    with pytest.raises(ImportError):
+        Bd.lib()

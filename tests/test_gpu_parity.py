@@ -1,0 +1,268 @@
+"""GPU parity on the 2-layer toy model (fp32) and small ragged cases, through
+the C ABI.  Every comparison is teacher-forced: the oracle consumes the GPU's
+emitted tokens as its next real rows, so each block is checked from the same
+context (a near-tie flip cannot cascade)."""
+import sys
+
+import numpy as np
+import pytest
+
+import kf_synth as S
+import oracle as O
+from tests.parity_util import TOL, compare_head, merge
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _ctx(cfg: S.ModelConfig, max_batch, max_k, max_prompt, blob, debug=True, on_device=True):
+    from paper_2606_10820_amd import binding as Bd
+    c = Bd.make_config(cfg.n_layer, cfg.d_model, cfg.n_head, cfg.d_mlp, cfg.vocab, cfg.n_ctx,
+                       cfg.dtype, max_batch, max_k, max_prompt,
+                       Bd.KF_FLAG_DEBUG_LOGITS if debug else 0)
+    kf = Bd.KForcing(c)
+    kf.load_weights(blob, on_device=on_device)
+    return kf
+
+
+def _log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+TOY = S.WORKLOADS["toy"]["cfg"]
+
+
+@pytest.fixture(scope="module")
+def toy():
+    _need_gpu()
+    blob = S.pack_blob(TOY, S.make_weights(TOY, seed=0, random_affine=True))
+    return blob, O.Model(blob)
+
+
+def run_teacher_forced(kf, model, prompt, ks, noise_seed, tol, rows=None):
+    """Prefill with ks[0], then one decode block per later k; compare every block."""
+    B, N = prompt.shape
+    rows = list(range(B)) if rows is None else rows
+    seqs = {b: model.seq() for b in rows}
+    pending = {b: list(prompt[b]) for b in rows}
+    stats = []
+    p = N
+    for si, k in enumerate(ks):
+        u = S.noise_block(noise_seed, B, p, k)
+        if si == 0:
+            out = kf.prefill(prompt, k, u)
+        else:
+            out = kf.decode_block(u)
+        torch.cuda.synchronize()
+        gl = kf.debug_logits(B * k).cpu().numpy().reshape(B, k, -1)
+        toks = out.cpu().numpy()
+        for b in rows:
+            ol, _ = seqs[b].step(pending[b], u[b].astype(np.float64), commit=True)
+            stats.append(compare_head(gl[b], ol, toks[b], tol, where=f"step {si} b {b}"))
+            pending[b] = list(toks[b])
+        p += k
+    C, pend, Bs = kf.get_state()
+    assert (C, pend, Bs) == (p - ks[-1], ks[-1], B)
+    return merge(stats)
+
+
+def test_device_noise_is_philox(toy):
+    """Device Philox4x32-10 noise equals the oracle's own generator bit for bit."""
+    blob, _ = toy
+    kf = _ctx(TOY, 4, 4, 16, blob)
+    got = kf.fill_noise(123456789, 5, 7, 33).cpu().numpy()
+    want = np.array([[O.noise_u(123456789, b, 7 + j) for j in range(33)] for b in range(5)],
+                    np.float32)
+    np.testing.assert_array_equal(got, want)
+    np.testing.assert_array_equal(got, S.noise_block(123456789, 5, 7, 33))
+
+
+def test_toy_prefill_and_decode(toy):
+    """Toy model, B = 4, N = 16, k = 4 for 16 blocks (64 tokens)."""
+    blob, model = toy
+    kf = _ctx(TOY, 4, 4, 16, blob)
+    prompt = S.prompts_uniform(1, 4, 16, TOY.vocab)
+    st = run_teacher_forced(kf, model, prompt, [4] * 16, noise_seed=2, tol=TOL[0])
+    _log(f"toy fp32 parity: {st}")
+    assert st["max_rel"] < 1e-4
+
+
+def test_toy_host_blob_equals_device_blob(toy):
+    blob, model = toy
+    a = _ctx(TOY, 2, 4, 16, blob, on_device=True)
+    b = _ctx(TOY, 2, 4, 16, blob, on_device=False)
+    prompt = S.prompts_uniform(3, 2, 9, TOY.vocab)
+    u = S.noise_block(3, 2, 9, 3)
+    ta = a.prefill(prompt, 3, u)
+    tb = b.prefill(prompt, 3, u)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(a.debug_logits(6).cpu().numpy(), b.debug_logits(6).cpu().numpy())
+    np.testing.assert_array_equal(ta.cpu().numpy(), tb.cpu().numpy())
+
+
+def test_ragged_and_variable_k(toy):
+    """Ragged batch (B = 3), a prompt that is not a tile multiple, and k changing
+    between blocks (pending count differs from the new k)."""
+    blob, model = toy
+    kf = _ctx(TOY, 5, 4, 40, blob)
+    prompt = S.prompts_uniform(5, 3, 37, TOY.vocab)
+    st = run_teacher_forced(kf, model, prompt, [3, 1, 4, 2, 4, 1, 1, 3], noise_seed=9, tol=TOL[0])
+    _log(f"ragged/variable-k parity: {st}")
+
+
+def test_empty_prompt(toy):
+    """N = 0: the first block sees only its own noise rows."""
+    blob, model = toy
+    kf = _ctx(TOY, 2, 4, 16, blob)
+    prompt = np.zeros((2, 0), np.int32)
+    st = run_teacher_forced(kf, model, prompt, [4, 4, 2], noise_seed=4, tol=TOL[0])
+    _log(f"empty-prompt parity: {st}")
+
+
+def test_fill_context_to_capacity(toy):
+    """Blocks until C + pending + k == n_ctx exactly, then the next block is refused."""
+    from paper_2606_10820_amd.binding import KfError, KF_ECTX
+    blob, model = toy
+    kf = _ctx(TOY, 2, 4, 120, blob)
+    prompt = S.prompts_uniform(6, 2, 116, TOY.vocab)
+    run_teacher_forced(kf, model, prompt, [4, 4, 4], noise_seed=6, tol=TOL[0])
+    C, pend, B = kf.get_state()
+    assert C + pend == 128 == TOY.n_ctx
+    with pytest.raises(KfError) as e:
+        kf.decode_block(S.noise_block(6, 2, 128, 1))
+    assert e.value.code == KF_ECTX
+    assert kf.get_state() == (124, 4, 2)
+
+
+def test_generate_matches_oracle(toy):
+    """kf_generate (device Philox noise, device feedback) against the oracle,
+    teacher-forced on the GPU's own token history, with the oracle's Philox."""
+    blob, model = toy
+    B, N, L, k, seed = 4, 16, 64, 4, 77
+    kf = _ctx(TOY, B, k, N, blob)
+    prompt = S.prompts_uniform(1, B, N, TOY.vocab)
+    out = kf.generate(prompt, L, k, seed).cpu().numpy()
+    stats = []
+    for b in range(B):
+        s = model.seq()
+        pending = list(prompt[b])
+        for p in range(N, N + L, k):
+            u = [O.noise_u(seed, b, p + j) for j in range(k)]
+            ol, _ = s.step(pending, u, commit=True)
+            toks = out[b, p - N:p - N + k]
+            top = np.sort(ol, axis=1)
+            near = (top[:, -1] - top[:, -2]) < TOL[0] * np.abs(ol).max(axis=1)
+            want = O.argmax(ol)
+            assert np.all((toks == want) | near), (b, p)
+            stats.append(int(near.sum()))
+            pending = list(toks)
+    assert kf.get_state() == (N + L - k, k, B)
+    _log(f"generate parity: near-ties {sum(stats)} of {B * L}")
+    # generation equals the explicit prefill / decode_block sequence with the same noise
+    kf2 = _ctx(TOY, B, k, N, blob)
+    t = [kf2.prefill(prompt, k, kf2.fill_noise(seed, B, N, k)).cpu().numpy()]
+    for p in range(N + k, N + L, k):
+        t.append(kf2.decode_block(kf2.fill_noise(seed, B, p, k)).cpu().numpy())
+    np.testing.assert_array_equal(np.concatenate(t, axis=1), out)
+
+
+def test_ar_decoding(toy):
+    """AR baseline: logits within tolerance of the oracle (teacher-forced); the
+    inverse-CDF decision equals the oracle's on the GPU's own fp32 logits except
+    where u lies within 1e-5 of a CDF boundary."""
+    blob, model = toy
+    B, N = 3, 10
+    kf = _ctx(TOY, B, 4, N, blob)
+    prompt = S.prompts_uniform(8, B, N, TOY.vocab)
+    seqs = [model.seq() for _ in range(B)]
+    pending = [list(prompt[b]) for b in range(B)]
+    close = 0
+    for step in range(12):
+        u = S.noise_block(5, B, N + step, 1)[:, 0]
+        out = kf.prefill_ar(prompt, u) if step == 0 else kf.decode_ar(u)
+        torch.cuda.synchronize()
+        gl = kf.debug_logits(B).cpu().numpy()
+        toks = out.cpu().numpy()
+        for b in range(B):
+            ol, _ = seqs[b].step(pending[b], [], commit=True)
+            s = np.abs(ol[0]).max()
+            assert np.abs(gl[b] - ol[0]).max() <= TOL[0] * s
+            q = O.softmax(gl[b].astype(np.float64))
+            want = O.icdf(q, float(u[b]))
+            if O.cdf_margin(gl[b].astype(np.float64), float(u[b])) < 1e-5:
+                close += 1
+            else:
+                assert toks[b] == want, (step, b)
+            pending[b] = [int(toks[b])]
+    _log(f"AR parity: {close} decisions within 1e-5 of a CDF boundary")
+
+
+def test_generate_ar_uses_same_noise(toy):
+    """kf_generate_ar equals kf_prefill_ar + kf_decode_ar fed with the device
+    Philox u of each position (the stream K-Forcing uses)."""
+    blob, _ = toy
+    B, N, L, seed = 2, 8, 10, 31
+    kf = _ctx(TOY, B, 4, N, blob)
+    prompt = S.prompts_uniform(2, B, N, TOY.vocab)
+    out = kf.generate_ar(prompt, L, seed).cpu().numpy()
+    kf2 = _ctx(TOY, B, 4, N, blob)
+    t = [kf2.prefill_ar(prompt, kf2.fill_noise(seed, B, N, 1)[:, 0]).cpu().numpy()]
+    for p in range(N + 1, N + L):
+        t.append(kf2.decode_ar(kf2.fill_noise(seed, B, p, 1)[:, 0]).cpu().numpy())
+    np.testing.assert_array_equal(np.stack(t, axis=1), out)
+    assert kf.get_state() == (N + L - 1, 1, B)
+
+
+def test_bad_token_flagged(toy):
+    blob, _ = toy
+    kf = _ctx(TOY, 2, 4, 8, blob)
+    prompt = np.array([[1, 2, 3, 4], [5, 6, 5000, 7]], np.int32)
+    kf.prefill(prompt, 2, S.noise_block(1, 2, 4, 2))
+    assert kf.device_errors() == 1
+    assert kf.device_errors() == 0
+
+
+def test_determinism(toy):
+    """Identical inputs give bitwise-identical logits and tokens."""
+    blob, _ = toy
+    prompt = S.prompts_uniform(4, 4, 16, TOY.vocab)
+    res = []
+    for _ in range(2):
+        kf = _ctx(TOY, 4, 4, 16, blob)
+        t = kf.generate(prompt, 32, 4, seed=5).cpu().numpy()
+        res.append((t, kf.debug_logits(16).cpu().numpy()))
+    np.testing.assert_array_equal(res[0][0], res[1][0])
+    np.testing.assert_array_equal(res[0][1], res[1][1])
+
+
+def test_kernel_timing_counts(toy):
+    blob, _ = toy
+    kf = _ctx(TOY, 4, 4, 16, blob)
+    prompt = S.prompts_uniform(4, 4, 16, TOY.vocab)
+    kf.set_timing(True)
+    kf.generate(prompt, 16, 4, seed=1)
+    ms, n = kf.kernel_time(4)  # attention: one launch per layer per step
+    assert n == 2 * 4 and ms > 0
+    ms, n = kf.kernel_time(8)  # head: one per step
+    assert n == 4
+    kf.set_timing(False)
+
+
+TOY_BF16 = S.ModelConfig(2, 128, 4, 512, 1024, 128, S.DTYPE_BF16)
+
+
+def test_toy_bf16(toy):
+    """The toy shapes with bf16 weights / activations / KV cache (2e-2 tolerance)."""
+    blob = S.pack_blob(TOY_BF16, S.make_weights(TOY_BF16, seed=0, random_affine=True))
+    model = O.Model(blob)
+    kf = _ctx(TOY_BF16, 4, 4, 16, blob)
+    prompt = S.prompts_uniform(1, 4, 16, TOY_BF16.vocab)
+    st = run_teacher_forced(kf, model, prompt, [4] * 8, noise_seed=2, tol=TOL[1])
+    _log(f"toy bf16 parity: {st}")
