@@ -1,0 +1,268 @@
+#!/usr/bin/env python3
+"""Throughput of K-Forcing joint next-k-token decoding on one MI355X.
+
+A step is one kf_generate call over the whole batch: the prefill (prompt +
+k noise rows) and every decode block (k emitted tokens + k fresh noise rows)
+until L new tokens per sequence exist.  Default workload: the LM1B-shaped
+GPT-2-small backbone in bf16 (12 layers, d=768, 12 heads, MLP 3072,
+vocab 30522, context 128), batch 64, prompt 16 Zipf(1.1) tokens, k = 4,
+112 new tokens (28 forward passes).  Weights, prompts and noise are seeded and
+synthetic.
+
+Printed (one JSON line): generated tokens/s at k (value), the k=1
+autoregressive baseline on the same workload, the roofline position of the
+dominant kernel class (HIP events on the library's stream), and the CPU oracle
+timed on a bounded sample on the host.
+
+    python bench.py [--steps K] [--warmup W] [--workload lm1b|owt|large|toy]
+                    [--batch B] [--k K] [--no-cpu] [--no-ar]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+import kf_synth as S  # noqa: E402
+
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+PEAK_MFMA_TFLOPS = {1: 2500.0,  # dense bf16
+                    0: 157.3}   # fp32 (matrix and vector)
+METRIC = "generated tokens/sec at k=4 vs k=1 per batch size; HBM GB/s / MFMA util"
+CLASSES = ["embed", "noise", "norm", "qkv", "attn", "oproj", "mlp_up", "mlp_down", "head",
+           "select"]
+
+
+# --------------------------------------------------------------------------
+# Algorithmic cost of each kernel class (minimum bytes moved, flops)
+# --------------------------------------------------------------------------
+
+def step_costs(cfg: S.ModelConfig, B: int, nr: int, k: int, C: int) -> dict:
+    """Per kernel class: (bytes, flops) that one step must move / compute.
+
+    Bytes count every operand once: weights, activations in and out, the KV
+    cache rows each (sequence, head) attends to, the K/V rows written."""
+    es = 2 if cfg.dtype == S.DTYPE_BF16 else 4
+    d, f, V, L, H = cfg.d_model, cfg.d_mlp, cfg.vocab, cfg.n_layer, cfg.n_head
+    R = nr + k
+    M = B * R
+    Mk = B * k
+    Mh = Mk if k > 0 else B
+    c = {n: [0.0, 0.0] for n in CLASSES}
+
+    def add(n, by, fl):
+        c[n][0] += by
+        c[n][1] += fl
+
+    add("embed", B * nr * (2 * d * es + 4 * d), 0)
+    if k > 0:
+        add("noise", Mk * d * es + 4 * d * d * es + Mk * 4 * d * es, 2 * Mk * 4 * d * d)
+        add("noise", 4 * d * d * es + Mk * 4 * d * es + Mk * d * (4 + es), 2 * Mk * d * 4 * d)
+    visible = sum(C + i + 1 for i in range(R))  # keys seen by the R queries of a sequence
+    for _ in range(L):
+        add("norm", 2 * M * d * (4 + es), 0)
+        add("qkv", 3 * d * d * es + M * d * es + M * 3 * d * es, 2 * M * 3 * d * d)
+        add("attn", B * (C + R) * 2 * d * es + 2 * M * d * es, 4 * B * visible * d)
+        add("oproj", d * d * es + M * d * es + 2 * M * d * 4, 2 * M * d * d)
+        add("mlp_up", f * d * es + M * d * es + M * f * es, 2 * M * f * d)
+        add("mlp_down", d * f * es + M * f * es + 2 * M * d * 4, 2 * M * d * f)
+    add("norm", Mh * d * (4 + es), 0)
+    add("head", V * d * es + Mh * d * es, 2 * Mh * V * d)
+    add("select", Mh * 8, 0)
+    return c
+
+
+def generate_costs(cfg, B, N, L, k) -> dict:
+    tot = {n: [0.0, 0.0] for n in CLASSES}
+    steps = [(N, k, 0)] + [(k, k, N + (s - 1) * k) for s in range(1, L // k)]
+    for nr, kk, C in steps:
+        for n, (by, fl) in step_costs(cfg, B, nr, kk, C).items():
+            tot[n][0] += by
+            tot[n][1] += fl
+    return tot
+
+
+def generate_ar_costs(cfg, B, N, L) -> dict:
+    tot = {n: [0.0, 0.0] for n in CLASSES}
+    steps = [(N, 0)] + [(1, N + s - 1) for s in range(1, L)]
+    for nr, C in steps:
+        for n, (by, fl) in step_costs(cfg, B, nr, 0, C).items():
+            tot[n][0] += by
+            tot[n][1] += fl
+    return tot
+
+
+# --------------------------------------------------------------------------
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="lm1b", choices=sorted(S.WORKLOADS))
+    ap.add_argument("--batch", type=int, default=None)
+    ap.add_argument("--k", type=int, default=None)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-ar", action="store_true", help="skip the k=1 AR baseline")
+    ap.add_argument("--cpu-blocks", type=int, default=8,
+                    help="decode blocks per sequence in the CPU oracle sample")
+    return ap.parse_args()
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(blob, prompt, k, seed, blocks):
+    """Oracle (fp32 instantiation, OpenMP over sequences) on a bounded sample."""
+    import oracle as O
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
+    threads = max(1, min(threads, len(os.sched_getaffinity(0))))
+    os.environ["OMP_NUM_THREADS"] = str(threads)
+    nseq = min(prompt.shape[0], threads)
+    m = O.Model(blob, "f32")
+    L = blocks * k
+    t0 = time.perf_counter()
+    O.generate_batched(m, prompt[:nseq], L, k, seed)
+    dt = time.perf_counter() - t0
+    return {"value": nseq * L / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": (f"fp32 oracle loop nest, {nseq} sequences x {L} new tokens "
+                       f"(prefill + {blocks - 1} decode blocks at k={k}), {dt:.1f} s"),
+            "seconds": round(dt, 2)}
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {a.gpus}); the decode path "
+              "shards by sequence and is measured at one GPU's share.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2606_10820_amd import binding as Bd
+
+    w = S.WORKLOADS[a.workload]
+    cfg: S.ModelConfig = w["cfg"]
+    B = a.batch or w["B"]
+    k = a.k or w["k"]
+    N, L = w["N"], w["L"] - (w["L"] % k)
+    seed = 2
+    dev = torch.device("cuda:0")
+
+    log(f"[bench] workload {a.workload}: generating weights ({S.n_params(cfg) / 1e6:.1f} M params)")
+    blob = S.pack_blob(cfg, S.make_weights(cfg, seed=0))
+    prompt = S.make_prompts(w["prompts"], 1, B, N, cfg.vocab)
+    kc = Bd.make_config(cfg.n_layer, cfg.d_model, cfg.n_head, cfg.d_mlp, cfg.vocab, cfg.n_ctx,
+                        cfg.dtype, B, max(k, 1), N, 0)
+    kf = Bd.KForcing(kc, device="cuda:0")
+    kf.load_weights(blob)
+    dprompt = torch.as_tensor(prompt, device=dev)
+    out = torch.empty((B, L), dtype=torch.int32, device=dev)
+
+    def run_kf():
+        kf.generate(dprompt, L, k, seed, out=out)
+
+    def run_ar():
+        kf.generate_ar(dprompt, L, seed, out=out)
+
+    def timed(fn, steps):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            fn()
+        torch.cuda.synchronize()
+        return time.perf_counter() - t0
+
+    log(f"[bench] warmup {a.warmup} x kf_generate (B={B}, N={N}, L={L}, k={k})")
+    for _ in range(a.warmup):
+        run_kf()
+    dt = timed(run_kf, a.steps)
+    tokens = B * L * a.steps
+    value = tokens / dt
+    ms_step = dt / a.steps * 1e3
+    log(f"[bench] k={k}: {value:,.0f} tokens/s, {ms_step:.3f} ms per generate")
+
+    # per-class kernel time over one generate (all classes bracketed)
+    kf.set_timing(Bd.KF_TIMING_ALL)
+    run_kf()
+    per = {}
+    for ci, name in enumerate(CLASSES):
+        ms, n = kf.kernel_time(ci)
+        per[name] = (ms, n)
+    kf.set_timing(0)
+    costs = generate_costs(cfg, B, N, L, k)
+    dom = max(CLASSES, key=lambda n: per[n][0])
+    # the timed region again, with only the dominant class bracketed by events
+    di = CLASSES.index(dom)
+    kf.set_timing(1 << di)
+    timed(run_kf, a.steps)
+    dom_ms, dom_n = kf.kernel_time(di)
+    kf.set_timing(0)
+    by, fl = costs[dom]
+    by *= a.steps
+    fl *= a.steps
+    peak_f = PEAK_MFMA_TFLOPS[cfg.dtype]
+    t_mem, t_fl = by / (PEAK_HBM_GBS * 1e9), fl / (peak_f * 1e12)
+    if t_fl >= t_mem and fl > 0:
+        roof = {"bound": "mfma", "achieved": fl / (dom_ms * 1e-3) / 1e12, "peak": peak_f,
+                "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": by / (dom_ms * 1e-3) / 1e9, "peak": PEAK_HBM_GBS,
+                "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = None
+    roof["kernel_class"] = dom
+    roof["launches"] = dom_n
+    roof["avg_launch_us"] = dom_ms * 1e3 / max(dom_n, 1)
+    roof["algorithmic_per_launch"] = {"bytes": by / max(dom_n, 1), "flops": fl / max(dom_n, 1)}
+    gen_bytes = sum(v[0] for v in costs.values())
+    gen_flops = sum(v[1] for v in costs.values())
+    step_roof_ms = max(gen_bytes / (PEAK_HBM_GBS * 1e9), gen_flops / (peak_f * 1e12)) * 1e3
+
+    res = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if cfg.dtype == S.DTYPE_BF16 else "fp32",
+        "data": "synthetic (seeded N(0,0.02) weights, Zipf/uniform prompts, Philox noise)",
+        "config": {"workload": (f"{a.workload}-shaped: {cfg.n_layer} layers, d={cfg.d_model}, "
+                                f"{cfg.n_head} heads, MLP {cfg.d_mlp}, vocab {cfg.vocab}, "
+                                f"context {cfg.n_ctx}; batch {B}, prompt {N}, k={k}, "
+                                f"{L} new tokens per sequence"),
+                   "batch": B, "k": k, "prompt": N, "new_tokens": L, "passes": L // k},
+        "roofline": roof,
+        "step_roofline": {"generate_algorithmic_bytes": gen_bytes,
+                          "generate_algorithmic_flops": gen_flops,
+                          "roofline_ms": round(step_roof_ms, 4),
+                          "frac": round(step_roof_ms / ms_step, 4)},
+        "kernel_ms_per_generate": {n: round(per[n][0], 4) for n in CLASSES},
+    }
+
+    if not a.no_ar:
+        ar_steps = max(1, a.steps // 4)
+        run_ar()
+        dt_ar = timed(run_ar, ar_steps)
+        v_ar = B * L * ar_steps / dt_ar
+        res["k1_ar_baseline"] = {"value": round(v_ar, 1), "unit": "tokens/s",
+                                 "ms_per_step": round(dt_ar / ar_steps * 1e3, 4),
+                                 "passes": L, "speedup_k_vs_ar": round(value / v_ar, 3)}
+        log(f"[bench] AR k=1: {v_ar:,.0f} tokens/s -> speedup {value / v_ar:.2f}x")
+
+    if not a.no_cpu:
+        log("[bench] CPU oracle sample ...")
+        res["cpu_baseline"] = cpu_baseline(blob, prompt, k, seed, a.cpu_blocks)
+        log(f"[bench] CPU oracle: {res['cpu_baseline']['value']:.1f} tokens/s")
+    else:
+        res["cpu_baseline"] = None
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

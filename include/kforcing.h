@@ -57,7 +57,7 @@ typedef struct kf_config {
   int n_head;     /* heads H; d_model / n_head must be 32, 64 or 128 */
   int d_mlp;      /* MLP hidden size; multiple of 64 */
   int vocab;      /* vocabulary size V (any value >= 2) */
-  int n_ctx;      /* positions (learned position table length, KV capacity) */
+  int n_ctx;      /* positions (learned position table length, KV capacity); multiple of 8 */
   int dtype;      /* KF_FP32 or KF_BF16 */
   int max_batch;  /* largest B any call may use */
   int max_k;      /* largest window k any call may use (k <= max_k) */
@@ -151,10 +151,12 @@ int kf_get_state(const kf_ctx *ctx, int *C, int *pending, int *B);
  * token id outside [0, V) was replaced by 0), then clear them. */
 int kf_device_errors(kf_ctx *ctx, int *flags);
 
-/* Per-kernel timing with HIP events on the context's stream.  While enabled,
- * every launch of a kernel class is bracketed by an event pair.
- * kf_kernel_time() synchronises and returns the summed milliseconds and the
- * launch count of one class since timing was enabled. */
+/* Per-kernel timing with HIP events on the context's stream.  kf_set_timing
+ * takes a bit mask over the kernel classes below (bit c = class c; 0 turns
+ * timing off; KF_TIMING_ALL brackets every class) and clears earlier records.
+ * While a class is selected, each of its launches is bracketed by an event
+ * pair.  kf_kernel_time() synchronises and returns the summed milliseconds
+ * and the launch count of one class since timing was last set. */
 #define KF_KC_EMBED 0    /* real-row embedding */
 #define KF_KC_NOISE 1    /* noise sinusoid + noise-MLP GEMMs + position add */
 #define KF_KC_NORM 2     /* LayerNorm kernels */
@@ -166,7 +168,8 @@ int kf_device_errors(kf_ctx *ctx, int *flags);
 #define KF_KC_HEAD 8     /* LM-head GEMM with fused argmax partials / logits */
 #define KF_KC_SELECT 9   /* argmax reduction or inverse-CDF sampler, commit */
 #define KF_KC_COUNT 10
-int kf_set_timing(kf_ctx *ctx, int enable);
+#define KF_TIMING_ALL ((1 << KF_KC_COUNT) - 1)
+int kf_set_timing(kf_ctx *ctx, int class_mask);
 int kf_kernel_time(kf_ctx *ctx, int kernel_class, double *total_ms, int *launches);
 
 /* Release host resources (device memory belongs to the caller). */

@@ -472,3 +472,25 @@ def nnz_single(N: int, k: int) -> int:
 def nnz_double(N: int, k: int) -> int:
     """|M_D| closed form over the Future-2 queries (Appendix C.2)."""
     return k * N * (N + 1) // 2 + N * k * k + N * k * (k + 1) // 2
+
+
+def generate_batched(model: Model, prompt: np.ndarray, L: int, k: int, seed: int) -> np.ndarray:
+    """generate() over all rows at once, one orc_step_batch call per block
+    (OpenMP over sequences in the C core).  Same result as generate()."""
+    prompt = np.ascontiguousarray(prompt, np.int32)
+    B, N = prompt.shape
+    seqs = [model.seq() for _ in range(B)]
+    arr = (ctypes.c_void_p * B)(*[s.h for s in seqs])
+    out = np.zeros((B, L), np.int32)
+    pending = prompt
+    f = _f("orc_step_batch", model.prec)
+    for p in range(N, N + L, k):
+        u = np.array([[noise_u(seed, b, p + j) for j in range(k)] for b in range(B)], np.float64)
+        logits = np.zeros((B, k, model.V), np.float64)
+        toks = np.ascontiguousarray(pending, np.int32)
+        rc = f(arr, B, toks.shape[1], _ip(toks), k, _dp(u), 1, _dp(logits))
+        if rc < 0:
+            raise ValueError("oracle batched step rejected")
+        pending = np.stack([argmax(logits[b]) for b in range(B)])
+        out[:, p - N:p - N + k] = pending
+    return out

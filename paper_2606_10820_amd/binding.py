@@ -21,6 +21,7 @@ KF_FP32, KF_BF16 = 0, 1
 KF_FLAG_DEBUG_LOGITS = 1
 KF_KC_NAMES = ["embed", "noise", "norm", "qkv", "attn", "oproj", "mlp_up", "mlp_down", "head",
                "select"]
+KF_TIMING_ALL = (1 << len(KF_KC_NAMES)) - 1
 
 _lib = None
 
@@ -224,8 +225,9 @@ class KForcing:
         self._check(self.L.kf_device_errors(self.h, ctypes.byref(f)))
         return f.value
 
-    def set_timing(self, enable: bool):
-        self._check(self.L.kf_set_timing(self.h, int(enable)))
+    def set_timing(self, class_mask: int = KF_TIMING_ALL):
+        """Bracket launches of the selected kernel classes (bit mask) with HIP events."""
+        self._check(self.L.kf_set_timing(self.h, int(class_mask)))
 
     def kernel_time(self, cls: int):
         ms, n = ctypes.c_double(), ctypes.c_int()

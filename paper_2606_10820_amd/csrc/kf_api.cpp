@@ -58,7 +58,7 @@ bool config_ok(const kf_config& c, std::string* why) {
   if (dh != 32 && dh != 64 && dh != 128) return bad("d_model / n_head must be 32, 64 or 128");
   if (c.d_mlp < 64 || c.d_mlp % 64) return bad("d_mlp must be a positive multiple of 64");
   if (c.vocab < 2) return bad("vocab must be >= 2");
-  if (c.n_ctx < 2) return bad("n_ctx must be >= 2");
+  if (c.n_ctx < 8 || c.n_ctx % 8) return bad("n_ctx must be a positive multiple of 8");
   if (c.dtype != KF_FP32 && c.dtype != KF_BF16) return bad("dtype must be KF_FP32 or KF_BF16");
   if (c.max_batch < 1 || c.max_batch > 65535) return bad("max_batch must be in [1, 65535]");
   if (c.max_k < 1 || c.max_k > c.n_ctx) return bad("max_k must be in [1, n_ctx]");
@@ -150,14 +150,15 @@ struct kf_ctx {
   int last_head_rows = 0;
   bool last_logits = false;
   std::string err;
-  // kernel timing
-  bool timing = false;
+  // kernel timing: bit c set = bracket launches of class c
+  int timing = 0;
   struct Ev {
     hipEvent_t a, b;
     int cls;
   };
   std::vector<Ev> evs;
   size_t ev_used = 0;
+  bool ev_open = false;
 };
 
 namespace {
@@ -183,7 +184,8 @@ int hip_fail(kf_ctx* c, hipError_t e, const char* what) {
   } while (0)
 
 int ev_begin(kf_ctx* c, int cls) {
-  if (!c->timing) return 0;
+  c->ev_open = false;
+  if (!(c->timing & (1 << cls))) return 0;
   if (c->ev_used == c->evs.size()) {
     kf_ctx::Ev e;
     KF_HIP(c, hipEventCreate(&e.a));
@@ -193,11 +195,13 @@ int ev_begin(kf_ctx* c, int cls) {
   kf_ctx::Ev& e = c->evs[c->ev_used];
   e.cls = cls;
   KF_HIP(c, hipEventRecord(e.a, c->stream));
+  c->ev_open = true;
   return 0;
 }
 
 int ev_end(kf_ctx* c) {
-  if (!c->timing) return 0;
+  if (!c->ev_open) return 0;
+  c->ev_open = false;
   KF_HIP(c, hipEventRecord(c->evs[c->ev_used].b, c->stream));
   ++c->ev_used;
   return 0;
@@ -650,9 +654,10 @@ int kf_device_errors(kf_ctx* c, int* flags) {
   return KF_OK;
 }
 
-int kf_set_timing(kf_ctx* c, int enable) {
+int kf_set_timing(kf_ctx* c, int class_mask) {
   if (!c) return KF_EINVAL;
-  c->timing = enable != 0;
+  if (class_mask & ~KF_TIMING_ALL) return fail(c, KF_EINVAL, "timing mask 0x%x has unknown bits", class_mask);
+  c->timing = class_mask;
   c->ev_used = 0;
   return KF_OK;
 }

@@ -22,6 +22,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));  // one 16-byte chunk
 
 __device__ inline float to_f(float x) { return x; }
 __device__ inline float to_f(bf16 x) { return (float)x; }
@@ -42,18 +43,18 @@ template <typename T>
 struct Mfma;
 template <>
 struct Mfma<bf16> {
-  __device__ static inline void mma(const uint4& a, const uint4& b, f32x4& c) {
+  __device__ static inline void mma(const u32x4& a, const u32x4& b, f32x4& c) {
     c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
   }
 };
 template <>
 struct Mfma<float> {
-  __device__ static inline void mma(const uint4& a, const uint4& b, f32x4& c) {
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
+  __device__ static inline void mma(const u32x4& a, const u32x4& b, f32x4& c) {
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[0]), __uint_as_float(b[0]), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[1]), __uint_as_float(b[1]), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[2]), __uint_as_float(b[2]), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[3]), __uint_as_float(b[3]), c, 0, 0, 0);
   }
 };
 
@@ -93,7 +94,8 @@ struct EpResidual {
 };
 
 // QKV projection: q goes to Q [M][d]; k and v of row (b, i) go straight into
-// the KV cache slot C + i of sequence b (the KV append of the step).
+// the KV cache slot C + i of sequence b (the KV append of the step).  Keys are
+// stored [slot][d_head] and values transposed, [d_head][slot], per head.
 template <typename T>
 struct EpQKV {
   T* Q;
@@ -106,17 +108,24 @@ struct EpQKV {
   __device__ inline void store4(int m, int n, f32x4 v) const {
     const int d = kg.H * kg.dh;
     const int which = n / d, c = n - which * d;
-    T* dst;
     if (which == 0) {
-      dst = Q + (size_t)m * d + c;
-    } else {
-      const int b = m / g.R, i = m - b * g.R;
-      const int h = c / kg.dh, e = c - h * kg.dh;
-      dst = kv + (size_t)b * kg.seq_stride() + kg.head_off(layer, which - 1, h) +
-            (size_t)(st->C + i) * kg.dh + e;
-    }
+      T* dst = Q + (size_t)m * d + c;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) dst[i] = from_f<T>(v[i] + bias[n + i]);
+      for (int i = 0; i < 4; ++i) dst[i] = from_f<T>(v[i] + bias[n + i]);
+      return;
+    }
+    const int b = m / g.R, i = m - b * g.R;
+    const int h = c / kg.dh, e = c - h * kg.dh;
+    const int slot = st->C + i;
+    T* base = kv + (size_t)b * kg.seq_stride() + kg.head_off(layer, which - 1, h);
+    if (which == 1) {  // keys: [slot][dh]
+      T* dst = base + (size_t)slot * kg.dh + e;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) dst[r] = from_f<T>(v[r] + bias[n + r]);
+    } else {           // values, transposed: [dh][slot]
+#pragma unroll
+      for (int r = 0; r < 4; ++r) base[(size_t)(e + r) * kg.T + slot] = from_f<T>(v[r] + bias[n + r]);
+    }
   }
 };
 
@@ -159,61 +168,92 @@ struct IsHead<EpHead> {
 };
 
 // ---------------------------------------------------------------- kernel
+// LDS tiles hold 8 16-byte chunks per row (one 128-byte K slab).  Chunk c of
+// row r is stored at position c ^ ((r >> 1) & 7): sixteen lanes reading the
+// same chunk of sixteen consecutive rows (one MFMA operand fetch) then touch
+// sixteen distinct 16-byte bank groups, and so do the 16-byte stores.
+__device__ inline int swz(int r, int c) { return r * 8 + (c ^ ((r >> 1) & 7)); }
+
+// Workgroups are dealt to the eight XCDs round-robin by linear id; give each
+// XCD a contiguous run of tiles (M fastest) so that the workgroups sharing a
+// weight strip share one L2.
+__device__ inline int xcd_tile(int lin, int total) {
+  const int q = total >> 3, r = total & 7;
+  const int x = lin & 7, j = lin >> 3;
+  return x * q + (x < r ? x : r) + j;
+}
+
+typedef const u32x4 __attribute__((address_space(1)))* gptr16;
+
+// Load this thread's chunks of one K slab of a ROWS x 128-byte tile starting
+// at global row row0.  Rows past the end re-read the last valid row: a tile
+// row only ever feeds its own output row or column, and those outputs are
+// never stored, so the loads need no predicate (and stay branch-free).
+template <int L, typename T>
+__device__ __forceinline__ void gload_tile(u32x4 (&r)[L], const T* __restrict__ base, int ld,
+                                           int row0, int nrows, int k0, int tid) {
+  constexpr int CH = 16 / (int)sizeof(T);
+#pragma unroll
+  for (int i = 0; i < L; ++i) {
+    const int c = tid + i * 256, gr = row0 + (c >> 3);
+    const int rr = gr < nrows ? gr : nrows - 1;
+    r[i] = *(gptr16)(const void*)(base + (size_t)rr * ld + k0 + (c & 7) * CH);
+  }
+}
+
+template <int L>
+__device__ __forceinline__ void sstore_tile(const u32x4 (&r)[L], u32x4* __restrict__ lds, int tid) {
+#pragma unroll
+  for (int i = 0; i < L; ++i) {
+    const int c = tid + i * 256;
+    lds[swz(c >> 3, c & 7)] = r[i];
+  }
+}
+
+// One 128-byte K slab of this wavefront's TN x TM block of 16x16 tiles.
+template <typename T, int TM, int TN>
+__device__ __forceinline__ void mma_slab(f32x4 (&acc)[TN][TM], const u32x4* __restrict__ la,
+                                         const u32x4* __restrict__ lw, int arow, int wrow,
+                                         int lane) {
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    u32x4 af[TN], bfr[TM];
+    const int ch = s * 4 + (lane >> 4);
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) af[tn] = lw[swz(wrow + tn * 16, ch)];
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) bfr[tm] = la[swz(arow + tm * 16, ch)];
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm) Mfma<T>::mma(af[tn], bfr[tm], acc[tn][tm]);
+  }
+}
+
 template <typename T, int BM, int BN, int WM, int WN, class Ep>
 __global__ void __launch_bounds__(256)
     gemm_kernel(const T* __restrict__ A, int lda, const T* __restrict__ W, int ldw, int M, int N,
                 int K, Ep ep) {
   constexpr int CH = 16 / (int)sizeof(T);  // elements per 16-byte chunk
   constexpr int BK = 8 * CH;               // K per slab (128 bytes per row)
-  constexpr int ROW = 9;                   // chunks per LDS row (8 + 1 padding)
   constexpr int MW = BM / WM, NW = BN / WN;
   constexpr int TM = MW / 16, TN = NW / 16;
-  constexpr int LA = (BM * 8 + 255) / 256, LW = (BN * 8 + 255) / 256;
+  constexpr int LA = BM * 8 / 256, LW = BN * 8 / 256;
   static_assert(WM * WN == 4, "four wavefronts");
   static_assert(MW % 16 == 0 && NW % 16 == 0, "16x16 MFMA tiles");
+  static_assert((BM * 8) % 256 == 0 && (BN * 8) % 256 == 0, "whole chunks per thread");
 
-  __shared__ uint4 sA[2][BM * ROW];
-  __shared__ uint4 sW[2][BN * ROW];
+  __shared__ u32x4 sA[2][BM * 8];
+  __shared__ u32x4 sW[2][BN * 8];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  const int gm = (M + BM - 1) / BM, gn = (N + BN - 1) / BN;
+  const int tile = xcd_tile(blockIdx.x, gm * gn);
+  const int m0 = (tile % gm) * BM, n0 = (tile / gm) * BN;
 
-  uint4 ra[LA], rw[LW];
-  const uint4 z4 = make_uint4(0u, 0u, 0u, 0u);
-
-  auto gload = [&](int kt) {
-#pragma unroll
-    for (int i = 0; i < LA; ++i) {
-      int c = tid + i * 256;
-      int r = c >> 3, cc = c & 7;
-      int gm = m0 + r;
-      ra[i] = (c < BM * 8 && gm < M)
-                  ? *reinterpret_cast<const uint4*>(A + (size_t)gm * lda + (size_t)kt * BK + cc * CH)
-                  : z4;
-    }
-#pragma unroll
-    for (int i = 0; i < LW; ++i) {
-      int c = tid + i * 256;
-      int r = c >> 3, cc = c & 7;
-      int gn = n0 + r;
-      rw[i] = (c < BN * 8 && gn < N)
-                  ? *reinterpret_cast<const uint4*>(W + (size_t)gn * ldw + (size_t)kt * BK + cc * CH)
-                  : z4;
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < LA; ++i) {
-      int c = tid + i * 256;
-      if (c < BM * 8) sA[buf][(c >> 3) * ROW + (c & 7)] = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < LW; ++i) {
-      int c = tid + i * 256;
-      if (c < BN * 8) sW[buf][(c >> 3) * ROW + (c & 7)] = rw[i];
-    }
-  };
+  // two register stages of prefetched chunks (loads run two slabs ahead)
+  u32x4 ra0[LA], rw0[LW], ra1[LA], rw1[LW];
 
   f32x4 acc[TN][TM];
 #pragma unroll
@@ -221,30 +261,40 @@ __global__ void __launch_bounds__(256)
 #pragma unroll
     for (int b = 0; b < TM; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  const int arow = wm * MW + (lane & 15), wrow = wn * NW + (lane & 15);
   const int nk = K / BK;
-  gload(0);
-  sstore(0);
+  // Prefetches are issued unconditionally (past the last slab they re-read
+  // it) so that the count of loads in flight is the same on every path and
+  // the waits before each LDS store cover only the older slab.
+  auto kofs = [nk](int k) { return (k < nk ? k : nk - 1) * BK; };
+  gload_tile<LA>(ra0, A, lda, m0, M, 0, tid);
+  gload_tile<LW>(rw0, W, ldw, n0, N, 0, tid);
+  gload_tile<LA>(ra1, A, lda, m0, M, kofs(1), tid);
+  gload_tile<LW>(rw1, W, ldw, n0, N, kofs(1), tid);
+  sstore_tile<LA>(ra0, sA[0], tid);
+  sstore_tile<LW>(rw0, sW[0], tid);
   __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) gload(kt + 1);
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      uint4 af[TN], bfr[TM];
-#pragma unroll
-      for (int tn = 0; tn < TN; ++tn)
-        af[tn] = sW[cur][(wn * NW + tn * 16 + (lane & 15)) * ROW + s * 4 + (lane >> 4)];
-#pragma unroll
-      for (int tm = 0; tm < TM; ++tm)
-        bfr[tm] = sA[cur][(wm * MW + tm * 16 + (lane & 15)) * ROW + s * 4 + (lane >> 4)];
-#pragma unroll
-      for (int tn = 0; tn < TN; ++tn)
-#pragma unroll
-        for (int tm = 0; tm < TM; ++tm) Mfma<T>::mma(af[tn], bfr[tm], acc[tn][tm]);
-    }
-    if (kt + 1 < nk) sstore(cur ^ 1);
+  // Slab kt is in LDS buffer kt&1; register stage kt&1 is free, stage
+  // (kt+1)&1 holds slab kt+1.  Pairs of slabs per trip keep the register
+  // stages statically addressed; an odd last slab is peeled.
+  int kt = 0;
+  for (; kt + 2 <= nk; kt += 2) {
+    gload_tile<LA>(ra0, A, lda, m0, M, kofs(kt + 2), tid);
+    gload_tile<LW>(rw0, W, ldw, n0, N, kofs(kt + 2), tid);
+    mma_slab<T, TM, TN>(acc, sA[0], sW[0], arow, wrow, lane);
+    sstore_tile<LA>(ra1, sA[1], tid);
+    sstore_tile<LW>(rw1, sW[1], tid);
+    __syncthreads();
+    gload_tile<LA>(ra1, A, lda, m0, M, kofs(kt + 3), tid);
+    gload_tile<LW>(rw1, W, ldw, n0, N, kofs(kt + 3), tid);
+    mma_slab<T, TM, TN>(acc, sA[1], sW[1], arow, wrow, lane);
+    // unconditional: past the end it rewrites buffer 0, which nothing reads
+    // any more (an odd last slab has kt + 2 == nk - 1 and is the real one)
+    sstore_tile<LA>(ra0, sA[0], tid);
+    sstore_tile<LW>(rw0, sW[0], tid);
     __syncthreads();
   }
+  if (kt < nk) mma_slab<T, TM, TN>(acc, sA[0], sW[0], arow, wrow, lane);
 
   if constexpr (!IsHead<Ep>::value) {
 #pragma unroll
@@ -303,8 +353,9 @@ __global__ void __launch_bounds__(256)
       }
       const int m = m0 + tid;
       if (m < M) {
-        ep.pval[(size_t)m * ep.n_tiles + blockIdx.x] = bv;
-        ep.pidx[(size_t)m * ep.n_tiles + blockIdx.x] = bi;
+        const int nt = n0 / BN;
+        ep.pval[(size_t)m * ep.n_tiles + nt] = bv;
+        ep.pidx[(size_t)m * ep.n_tiles + nt] = bi;
       }
     }
   }
@@ -313,20 +364,26 @@ __global__ void __launch_bounds__(256)
 template <typename T, int BM, int BN, int WM, int WN, class Ep>
 hipError_t run(const T* A, int lda, const T* W, int ldw, int M, int N, int K, const Ep& ep,
                hipStream_t s) {
-  dim3 grid((N + BN - 1) / BN, (M + BM - 1) / BM);
-  hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN, Ep>), grid, dim3(256), 0, s, A, lda, W, ldw,
-                     M, N, K, ep);
+  const int tiles = ((N + BN - 1) / BN) * ((M + BM - 1) / BM);
+  hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN, Ep>), dim3(tiles), dim3(256), 0, s, A, lda,
+                     W, ldw, M, N, K, ep);
   return hipGetLastError();
 }
 
-// Tile choice by M (rows of activations).
+inline int cdiv(int a, int b) { return (a + b - 1) / b; }
+
+// Tile choice: the largest tile that still gives at least one workgroup per
+// CU (256), else the smallest tile.
 template <typename T, class Ep>
 hipError_t dispatch(const T* A, int lda, const T* W, int ldw, int M, int N, int K, const Ep& ep,
                     hipStream_t s) {
   if (M <= 0 || N <= 0) return hipSuccess;
-  if (M <= 32) return run<T, 32, 64, 1, 4>(A, lda, W, ldw, M, N, K, ep, s);
-  if (M <= 256) return run<T, 64, 64, 2, 2>(A, lda, W, ldw, M, N, K, ep, s);
-  return run<T, 128, 128, 2, 2>(A, lda, W, ldw, M, N, K, ep, s);
+  constexpr int kFill = 256;
+  if (cdiv(M, 128) * cdiv(N, 128) >= kFill) return run<T, 128, 128, 2, 2>(A, lda, W, ldw, M, N, K, ep, s);
+  if (cdiv(M, 64) * cdiv(N, 128) >= kFill) return run<T, 64, 128, 2, 2>(A, lda, W, ldw, M, N, K, ep, s);
+  if (cdiv(M, 64) * cdiv(N, 64) >= kFill) return run<T, 64, 64, 2, 2>(A, lda, W, ldw, M, N, K, ep, s);
+  if (cdiv(M, 32) * cdiv(N, 64) >= kFill) return run<T, 32, 64, 2, 2>(A, lda, W, ldw, M, N, K, ep, s);
+  return run<T, 32, 32, 2, 2>(A, lda, W, ldw, M, N, K, ep, s);
 }
 
 }  // namespace
@@ -366,7 +423,8 @@ hipError_t gemm_head(const T* A, const T* W, int M, int Vpad, int V, int K, floa
   if (M <= 0) return hipSuccess;
   EpHead ep{pval, pidx, logits, V, Vpad / kHeadTileN};
   if (M <= 32) return run<T, 32, kHeadTileN, 1, 4>(A, K, W, K, M, Vpad, K, ep, s);
-  return run<T, 64, kHeadTileN, 2, 2>(A, K, W, K, M, Vpad, K, ep, s);
+  if (M <= 512) return run<T, 64, kHeadTileN, 2, 2>(A, K, W, K, M, Vpad, K, ep, s);
+  return run<T, 128, kHeadTileN, 2, 2>(A, K, W, K, M, Vpad, K, ep, s);
 }
 
 #define KF_INST(T)                                                                                 \

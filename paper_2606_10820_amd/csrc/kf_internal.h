@@ -32,7 +32,8 @@ struct KfStepGeom {
   int B, R, nr, k;
 };
 
-// Geometry of the KV cache: [B][L][2][H][T][dh] elements.
+// Geometry of the KV cache: [B][L][2][H][T * dh] elements; per head the keys
+// are [T][dh] (slot-major) and the values [dh][T] (transposed).
 struct KfKvGeom {
   int L, H, T, dh;
   __host__ __device__ size_t seq_stride() const { return (size_t)L * 2 * H * T * dh; }

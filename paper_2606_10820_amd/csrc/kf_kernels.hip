@@ -153,7 +153,7 @@ __global__ void __launch_bounds__(256)
       float kx = 0.f, vx = 0.f;
       if (slot < nkeys) {
         kx = to_f(Kb[(size_t)slot * DH + e]);
-        vx = to_f(Vb[(size_t)slot * DH + e]);
+        vx = to_f(Vb[(size_t)e * kg.T + slot]);
       }
       sK[kk][e] = kx;
       sV[kk][e] = vx;
@@ -201,6 +201,146 @@ __global__ void __launch_bounds__(256)
     const float inv = 1.0f / l_run;
 #pragma unroll
     for (int c = 0; c < EPT; ++c) orow[c * 16 + r16] = from_f<T>(o[c] * inv);
+  }
+}
+
+// Block attention on MFMA (bf16).  One workgroup per (sequence, head, block of
+// 16 query rows); its four wavefronts take 32-key tiles round-robin and merge
+// their online-softmax states through LDS at the end.
+//   S^T = K Q^T   with v_mfma_f32_16x16x32_bf16: A = 16 keys x 32 d_head,
+//                 B = 32 d_head x 16 queries.  MFMA row i of key group grp is
+//                 key 8*(i/4) + 4*grp + i%4 of the tile, so the output rows a
+//                 lane holds (4 per group, 2 groups) are 8 consecutive keys.
+//   O^T += V^T P^T  A = 16 d_head x 32 keys read straight from the transposed
+//                 value cache (8 consecutive slots = one 16-byte load), B = the
+//                 lane's own 8 probabilities -- no data exchange between lanes.
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ inline bf16x8_t load8(const bf16* p) {
+  return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(p));
+}
+
+template <int DH>
+__global__ void __launch_bounds__(256)
+    attention_mfma_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ kv,
+                          bf16* __restrict__ O, const KfDevState* st, KfStepGeom g, KfKvGeom kg,
+                          int layer, float scale) {
+  constexpr int QB = 16, KT = 32, NDC = DH / 32, NDB = DH / 16;
+  const int H = kg.H, T = kg.T, d = H * DH;
+  const int nqb = (g.R + QB - 1) / QB;
+  const int qb = blockIdx.x % nqb, bh = blockIdx.x / nqb;
+  const int b = bh / H, h = bh % H;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int gq = lane >> 4, lq = lane & 15;
+  const int C = st->C;
+  const int q0 = qb * QB, nq = min(QB, g.R - q0);
+  const int nkeys = C + q0 + nq;
+  const bf16* Kb = kv + (size_t)b * kg.seq_stride() + kg.head_off(layer, 0, h);
+  const bf16* Vt = kv + (size_t)b * kg.seq_stride() + kg.head_off(layer, 1, h);
+
+  const bf16x8_t zero8 = {};
+  bf16x8_t qf[NDC];
+  const bf16* qrow = Q + ((size_t)b * g.R + q0 + lq) * d + h * DH + 8 * gq;
+#pragma unroll
+  for (int c = 0; c < NDC; ++c) qf[c] = (lq < nq) ? load8(qrow + c * 32) : zero8;
+  const int qslot = C + q0 + lq;
+
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x4_t o[NDB];
+#pragma unroll
+  for (int i = 0; i < NDB; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  for (int t0 = w * KT; t0 < nkeys; t0 += 4 * KT) {
+    f32x4_t s[2];
+#pragma unroll
+    for (int grp = 0; grp < 2; ++grp) {
+      const int key = t0 + 8 * (lq >> 2) + 4 * grp + (lq & 3);  // MFMA row lq of group grp
+      s[grp] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < NDC; ++c) {
+        bf16x8_t kf = key < nkeys ? load8(Kb + (size_t)key * DH + c * 32 + 8 * gq) : zero8;
+        s[grp] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[c], s[grp], 0, 0, 0);
+      }
+    }
+    // this lane: query lq, keys t0 + 8*gq + 4*grp + r
+    float p[8];
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int grp = 0; grp < 2; ++grp)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int key = t0 + 8 * gq + 4 * grp + r;
+        const float v = (key <= qslot && key < nkeys) ? s[grp][r] * scale : -INFINITY;
+        p[grp * 4 + r] = v;
+        tmax = fmaxf(tmax, v);
+      }
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    const float m_new = fmaxf(m_run, tmax);
+    const float ref = (m_new == -INFINITY) ? 0.f : m_new;
+    const float alpha = __expf(m_run - ref);
+    float psum = 0.f;
+    bf16x8_t pf;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      p[i] = __expf(p[i] - ref);
+      psum += p[i];
+      pf[i] = (bf16)p[i];
+    }
+    psum += __shfl_xor(psum, 16, 64);
+    psum += __shfl_xor(psum, 32, 64);
+    l_run = l_run * alpha + psum;
+    m_run = m_new;
+    const int kb = t0 + 8 * gq;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      const bf16* vp = Vt + (size_t)(db * 16 + lq) * T + kb;
+      bf16x8_t vf;
+      if (kb + 8 <= nkeys) {
+        vf = load8(vp);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) vf[e] = (kb + e < nkeys) ? vp[e] : (bf16)0.f;
+      }
+      o[db] *= alpha;
+      o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[db], 0, 0, 0);
+    }
+  }
+
+  // merge the four wavefronts' partial states
+  __shared__ float sm[4][QB], sl[4][QB];
+  __shared__ float so[4][QB][DH + 1];
+  if (gq == 0) {
+    sm[w][lq] = m_run;
+    sl[w][lq] = l_run;
+  }
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) so[w][lq][db * 16 + 4 * gq + r] = o[db][r];
+  __syncthreads();
+  constexpr int EPT = DH / 16;
+  const int q = threadIdx.x >> 4, e0 = (threadIdx.x & 15) * EPT;
+  if (q < nq) {
+    float M = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) M = fmaxf(M, sm[i][q]);
+    float f[4], den = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      f[i] = (sm[i][q] == -INFINITY) ? 0.f : __expf(sm[i][q] - M);
+      den += f[i] * sl[i][q];
+    }
+    const float inv = 1.0f / den;
+    bf16* orow = O + ((size_t)b * g.R + q0 + q) * d + h * DH + e0;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      float acc = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc += f[i] * so[i][q][e0 + e];
+      orow[e] = (bf16)(acc * inv);
+    }
   }
 }
 
@@ -382,8 +522,28 @@ template <typename T>
 hipError_t launch_attention(const T* Q, const T* kv, T* O, const KfDevState* st, KfStepGeom g,
                             KfKvGeom kg, int layer, hipStream_t s) {
   if (g.B <= 0 || g.R <= 0) return hipSuccess;
-  dim3 grid(g.B * kg.H, (g.R + 15) / 16);
   const float scale = 1.0f / sqrtf((float)kg.dh);
+  if constexpr (sizeof(T) == 2) {
+    dim3 grid(g.B * kg.H * ((g.R + 15) / 16));
+    switch (kg.dh) {
+      case 32:
+        hipLaunchKernelGGL(attention_mfma_kernel<32>, grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
+                           layer, scale);
+        break;
+      case 64:
+        hipLaunchKernelGGL(attention_mfma_kernel<64>, grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
+                           layer, scale);
+        break;
+      case 128:
+        hipLaunchKernelGGL(attention_mfma_kernel<128>, grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
+                           layer, scale);
+        break;
+      default:
+        return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  }
+  dim3 grid(g.B * kg.H, (g.R + 15) / 16);
   switch (kg.dh) {
     case 32:
       hipLaunchKernelGGL((attention_kernel<T, 32>), grid, dim3(256), 0, s, Q, kv, O, st, g, kg,

@@ -59,7 +59,7 @@ def test_strerror(L):
 
 @pytest.mark.parametrize("bad", [
     dict(n_layer=0), dict(d_model=100), dict(n_head=3), dict(d_model=256, n_head=1),
-    dict(d_mlp=100), dict(vocab=1), dict(dtype=7), dict(max_batch=0), dict(max_k=0),
+    dict(d_mlp=100), dict(vocab=1), dict(n_ctx=100), dict(dtype=7), dict(max_batch=0), dict(max_k=0),
     dict(max_k=1000), dict(max_prompt=0), dict(flags=8),
 ])
 def test_bad_config_rejected(L, bad):

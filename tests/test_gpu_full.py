@@ -1,0 +1,180 @@
+"""GPU parity at the full workload sizes, on sampled sequences.
+
+The LM1B-shaped model (12 layers, d=768, 12 heads, MLP 3072, vocab 30522,
+context 128, bf16) runs at the benchmark's launch configuration (batch 64,
+prompt 16 Zipf(1.1) tokens, k = 4).  The fp64 oracle follows sequences 0 and
+B-1 (sequences are independent, so a subset is a valid check), teacher-forced
+on the GPU's emitted tokens: the prefill, the first decode blocks, and the
+last block of a full kf_generate run whose context the oracle rebuilds from
+the GPU's own token history.  The same shapes in fp32 give a 1e-4 check on
+the tokens.  OpenWebText-shaped (vocab 50257, context 1024) and the 24-layer
+backbone get a prefill + decode check at a small batch.
+"""
+import sys
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+import pytest
+
+import kf_synth as S
+import oracle as O
+from tests.parity_util import TOL, compare_head, merge
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+_CACHE = {}
+
+
+def _log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _blob(cfg):
+    key = (cfg, "blob")
+    if key not in _CACHE:
+        _CACHE[key] = S.pack_blob(cfg, S.make_weights(cfg, seed=0, random_affine=True))
+    return _CACHE[key]
+
+
+def _model(cfg):
+    key = (cfg, "model")
+    if key not in _CACHE:
+        _CACHE[key] = O.Model(_blob(cfg))
+    return _CACHE[key]
+
+
+def _ctx(cfg, max_batch, max_k, max_prompt):
+    from paper_2606_10820_amd import binding as Bd
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    c = Bd.make_config(cfg.n_layer, cfg.d_model, cfg.n_head, cfg.d_mlp, cfg.vocab, cfg.n_ctx,
+                       cfg.dtype, max_batch, max_k, max_prompt, Bd.KF_FLAG_DEBUG_LOGITS)
+    kf = Bd.KForcing(c)
+    kf.load_weights(_blob(cfg))
+    return kf
+
+
+def _blocks(kf, model, prompt, ks, seed, tol, rows):
+    B, N = prompt.shape
+    seqs = {b: model.seq() for b in rows}
+    pending = {b: list(prompt[b]) for b in rows}
+    stats = []
+    p = N
+    for si, k in enumerate(ks):
+        u = S.noise_block(seed, B, p, k)
+        out = kf.prefill(prompt, k, u) if si == 0 else kf.decode_block(u)
+        torch.cuda.synchronize()
+        gl = kf.debug_logits(B * k).cpu().numpy().reshape(B, k, -1)
+        toks = out.cpu().numpy()
+        with ThreadPoolExecutor(len(rows)) as ex:  # sequences are independent
+            ols = list(ex.map(lambda b: seqs[b].step(pending[b], u[b].astype(np.float64),
+                                                     commit=True)[0], rows))
+        for b, ol in zip(rows, ols):
+            stats.append(compare_head(gl[b], ol, toks[b], tol, where=f"block {si} seq {b}"))
+            pending[b] = list(toks[b])
+        p += k
+    return merge(stats)
+
+
+LM1B = S.WORKLOADS["lm1b"]["cfg"]
+LM1B_F32 = S.ModelConfig(12, 768, 12, 3072, 30522, 128, S.DTYPE_FP32)
+
+
+def test_lm1b_bf16_bench_configuration():
+    """Batch 64, prompt 16, k = 4: prefill and two decode blocks, rows 0 and 63."""
+    w = S.WORKLOADS["lm1b"]
+    B, N, k = w["B"], w["N"], w["k"]
+    kf = _ctx(LM1B, B, k, N)
+    prompt = S.prompts_zipf(1, B, N, LM1B.vocab)
+    st = _blocks(kf, _model(LM1B), prompt, [k, k, k], seed=2, tol=TOL[1], rows=[0, B - 1])
+    _log(f"lm1b bf16 B=64 parity: {st}")
+
+
+def test_lm1b_bf16_generate_last_block():
+    """A full kf_generate run (28 passes, device noise); the oracle rebuilds the
+    context of the last block from the GPU's own history (a prefill over the
+    prompt and the first 108 emitted tokens) and checks the last 4 tokens."""
+    w = S.WORKLOADS["lm1b"]
+    B, N, k, L, seed = w["B"], w["N"], w["k"], w["L"], 77
+    kf = _ctx(LM1B, B, k, N)
+    prompt = S.prompts_zipf(1, B, N, LM1B.vocab)
+    out = kf.generate(prompt, L, k, seed).cpu().numpy()
+    gl = kf.debug_logits(B * k).cpu().numpy().reshape(B, k, -1)
+    model = _model(LM1B)
+
+    def last_block(b):
+        hist = list(prompt[b]) + list(out[b, :L - 2 * k])
+        pend = list(out[b, L - 2 * k:L - k])
+        s = model.seq()
+        s.step(hist, [], commit=True)  # context of the last block
+        u = [O.noise_u(seed, b, N + L - k + j) for j in range(k)]
+        return s.step(pend, u, commit=True)[0]
+
+    rows = (0, B - 1)
+    with ThreadPoolExecutor(len(rows)) as ex:
+        ols = list(ex.map(last_block, rows))
+    stats = [compare_head(gl[b], ol, out[b, L - k:], TOL[1], where=f"last block seq {b}")
+             for b, ol in zip(rows, ols)]
+    _log(f"lm1b bf16 generate last-block parity: {merge(stats)}")
+
+
+def test_lm1b_fp32_tokens():
+    """The same shapes with fp32 weights, activations and KV cache: logits
+    within 1e-4 and tokens exact except near-ties."""
+    B, N, k = 4, 16, 4
+    kf = _ctx(LM1B_F32, B, k, N)
+    prompt = S.prompts_zipf(1, B, N, LM1B_F32.vocab)
+    st = _blocks(kf, _model(LM1B_F32), prompt, [k, k], seed=2, tol=TOL[0], rows=[0, B - 1])
+    _log(f"lm1b fp32 parity: {st}")
+
+
+def test_lm1b_bf16_ar_baseline():
+    """AR baseline at the LM1B shape: logits within 2e-2 of the oracle."""
+    B, N = 64, 16
+    kf = _ctx(LM1B, B, 4, N)
+    prompt = S.prompts_zipf(1, B, N, LM1B.vocab)
+    model = _model(LM1B)
+    rows = [0, B - 1]
+    seqs = {b: model.seq() for b in rows}
+    pend = {b: list(prompt[b]) for b in rows}
+    worst = 0.0
+    for step in range(3):
+        u = S.noise_block(5, B, N + step, 1)[:, 0]
+        out = kf.prefill_ar(prompt, u) if step == 0 else kf.decode_ar(u)
+        torch.cuda.synchronize()
+        gl = kf.debug_logits(B).cpu().numpy()
+        toks = out.cpu().numpy()
+        for b in rows:
+            ol, _ = seqs[b].step(pend[b], [], commit=True)
+            rel = np.abs(gl[b] - ol[0]).max() / np.abs(ol[0]).max()
+            worst = max(worst, rel)
+            assert rel <= TOL[1]
+            pend[b] = [int(toks[b])]
+    _log(f"lm1b AR logit rel err {worst:.3e}")
+
+
+OWT = S.WORKLOADS["owt"]["cfg"]
+
+
+def test_owt_shape_prefill_decode():
+    """OpenWebText-shaped model (vocab 50257, context 1024): batch 4 with a
+    64-token prompt, prefill and one decode block, rows 0 and 3."""
+    B, N, k = 4, 64, 4
+    kf = _ctx(OWT, B, k, N)
+    prompt = S.prompts_zipf(1, B, N, OWT.vocab)
+    st = _blocks(kf, _model(OWT), prompt, [k, k], seed=2, tol=TOL[1], rows=[0, B - 1])
+    _log(f"owt bf16 parity: {st}")
+
+
+LARGE = S.WORKLOADS["large"]["cfg"]
+
+
+def test_large_backbone_prefill_decode():
+    """24 layers, d = 1024, 16 heads: batch 2, prompt 16, prefill + one block."""
+    B, N, k = 2, 16, 4
+    kf = _ctx(LARGE, B, k, N)
+    prompt = S.prompts_zipf(1, B, N, LARGE.vocab)
+    st = _blocks(kf, _model(LARGE), prompt, [k, k], seed=2, tol=TOL[1], rows=[0, 1])
+    _log(f"large bf16 parity: {st}")

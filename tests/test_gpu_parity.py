@@ -246,13 +246,16 @@ def test_kernel_timing_counts(toy):
     blob, _ = toy
     kf = _ctx(TOY, 4, 4, 16, blob)
     prompt = S.prompts_uniform(4, 4, 16, TOY.vocab)
-    kf.set_timing(True)
+    kf.set_timing()
     kf.generate(prompt, 16, 4, seed=1)
     ms, n = kf.kernel_time(4)  # attention: one launch per layer per step
     assert n == 2 * 4 and ms > 0
     ms, n = kf.kernel_time(8)  # head: one per step
     assert n == 4
-    kf.set_timing(False)
+    kf.set_timing(1 << 4)  # attention only
+    kf.generate(prompt, 16, 4, seed=1)
+    assert kf.kernel_time(4)[1] == 8 and kf.kernel_time(8)[1] == 0
+    kf.set_timing(0)
 
 
 TOY_BF16 = S.ModelConfig(2, 128, 4, 512, 1024, 128, S.DTYPE_BF16)
