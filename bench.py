@@ -114,6 +114,9 @@ def parse():
     ap.add_argument("--no-ar", action="store_true", help="skip the k=1 AR baseline")
     ap.add_argument("--cpu-blocks", type=int, default=8,
                     help="decode blocks per sequence in the CPU oracle sample")
+    ap.add_argument("--summarize", metavar="DIR", default=None,
+                    help="print a markdown summary of rocprofv3 CSV output under DIR "
+                         "(kernel stats, and FETCH_SIZE / WRITE_SIZE counter runs) and exit")
     return ap.parse_args()
 
 
@@ -139,8 +142,71 @@ def cpu_baseline(blob, prompt, k, seed, blocks):
             "seconds": round(dt, 2)}
 
 
+def _short(name: str) -> str:
+    import re
+    n = name.replace("_ZN2kf12_GLOBAL__N_1", "").replace("kf::(anonymous namespace)::", "")
+    m = re.match(r"\d+(\w+?)I(.*)", n)
+    if m and "gemm_kernel" in m.group(1):
+        t = re.findall(r"Li(\d+)E", m.group(2))
+        ep = re.search(r"NS0_\d+(Ep\w+?)I|NS0_\d+(Ep\w+?)E", m.group(2))
+        epn = (ep.group(1) or ep.group(2)) if ep else "?"
+        return f"gemm {'x'.join(t[:2])} {epn}" + (" bf16" if "DF16b" in n else " f32")
+    if m:
+        return m.group(1) + (" bf16" if "DF16b" in n else "")
+    return n.split("(")[0]
+
+
+def summarize(root: str) -> None:
+    """Markdown summary of rocprofv3 --stats / --pmc CSV output (no GPU needed)."""
+    import csv
+    import glob
+    stats = glob.glob(os.path.join(root, "**", "*_kernel_stats.csv"), recursive=True)
+    for path in stats:
+        rows = list(csv.DictReader(open(path)))
+        tot = sum(float(r["TotalDurationNs"]) for r in rows)
+        print(f"### kernel time ({os.path.relpath(path, root)})\n")
+        print("| kernel | calls | avg us | min us | share |\n|---|---|---|---|---|")
+        for r in rows[:16]:
+            print(f"| {_short(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                  f"{float(r['MinNs']) / 1e3:.2f} | {float(r['TotalDurationNs']) / tot * 100:.1f}% |")
+        print()
+    pmc = {}
+    for path in glob.glob(os.path.join(root, "**", "*_counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(path)):
+            key = (_short(r["Kernel_Name"]), int(r["Grid_Size"]))
+            pmc.setdefault(r["Counter_Name"], {}).setdefault(key, []).append(float(r["Counter_Value"]))
+    if not pmc:
+        return
+    # calibration: fp32 -> bf16 weight conversion of the token table reads 4n, writes 2n bytes
+    conv = [k for k in pmc.get("FETCH_SIZE", {}) if k[0].startswith("convert_kernel")]
+    cal = max(conv, key=lambda k: k[1]) if conv else None
+    f_scale = w_scale = None
+    if cal:
+        n = cal[1]
+        f_scale = 4 * n / 1024 / np.mean(pmc["FETCH_SIZE"][cal])
+        if "WRITE_SIZE" in pmc and cal in pmc["WRITE_SIZE"]:
+            w_scale = 2 * n / 1024 / np.mean(pmc["WRITE_SIZE"][cal])
+        ws = f"{w_scale:.4f}" if w_scale else "n/a"
+        print(f"calibration on {cal[0]} over {n} elements: FETCH_SIZE x {f_scale:.4f}, "
+              f"WRITE_SIZE x {ws} (true bytes / counter bytes)\n")
+    print("| kernel | grid | dispatches | FETCH KiB | WRITE KiB | scaled MB read | scaled MB written |")
+    print("|---|---|---|---|---|---|---|")
+    keys = sorted(set(pmc.get("FETCH_SIZE", {})) | set(pmc.get("WRITE_SIZE", {})),
+                  key=lambda k: -np.mean(pmc.get("FETCH_SIZE", {}).get(k, [0])))
+    for k in keys[:16]:
+        fv = pmc.get("FETCH_SIZE", {}).get(k)
+        wv = pmc.get("WRITE_SIZE", {}).get(k)
+        fm = np.mean(fv) if fv else float("nan")
+        wm = np.mean(wv) if wv else float("nan")
+        print(f"| {k[0]} | {k[1]} | {len(fv or wv)} | {fm:.1f} | {wm:.1f} | "
+              f"{fm * 1024 * (f_scale or 1) / 1e6:.2f} | {wm * 1024 * (w_scale or 1) / 1e6:.2f} |")
+
+
 def main():
     a = parse()
+    if a.summarize:
+        summarize(a.summarize)
+        return
     if a.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {a.gpus}); the decode path "
               "shards by sequence and is measured at one GPU's share.", file=sys.stderr)

@@ -168,11 +168,17 @@ struct IsHead<EpHead> {
 };
 
 // ---------------------------------------------------------------- kernel
-// LDS tiles hold 8 16-byte chunks per row (one 128-byte K slab).  Chunk c of
-// row r is stored at position c ^ ((r >> 1) & 7): sixteen lanes reading the
-// same chunk of sixteen consecutive rows (one MFMA operand fetch) then touch
-// sixteen distinct 16-byte bank groups, and so do the 16-byte stores.
-__device__ inline int swz(int r, int c) { return r * 8 + (c ^ ((r >> 1) & 7)); }
+// LDS tiles hold KCH 16-byte chunks per row (one K slab of KCH * 16 bytes).
+// Chunk c of row r is stored at position c ^ f(r) with f(r) = (r >> 1) & 7 for
+// 8 chunks (128-byte rows) and r & 15 for 16 chunks (256-byte rows): sixteen
+// lanes reading the same chunk of sixteen consecutive rows (one MFMA operand
+// fetch) then touch sixteen distinct 16-byte bank groups, and so do the
+// 16-byte stores of a row.
+template <int KCH>
+__device__ inline int swz(int r, int c) {
+  if constexpr (KCH == 8) return r * 8 + (c ^ ((r >> 1) & 7));
+  else return r * KCH + (c ^ (r & (KCH - 1)));
+}
 
 // Workgroups are dealt to the eight XCDs round-robin by linear id; give each
 // XCD a contiguous run of tiles (M fastest) so that the workgroups sharing a
@@ -185,44 +191,44 @@ __device__ inline int xcd_tile(int lin, int total) {
 
 typedef const u32x4 __attribute__((address_space(1)))* gptr16;
 
-// Load this thread's chunks of one K slab of a ROWS x 128-byte tile starting
-// at global row row0.  Rows past the end re-read the last valid row: a tile
-// row only ever feeds its own output row or column, and those outputs are
-// never stored, so the loads need no predicate (and stay branch-free).
-template <int L, typename T>
+// Load this thread's chunks of one K slab (KCH chunks per row) of a tile
+// starting at global row row0.  Rows past the end re-read the last valid row:
+// a tile row only ever feeds its own output row or column, and those outputs
+// are never stored, so the loads need no predicate (and stay branch-free).
+template <int L, int KCH, typename T>
 __device__ __forceinline__ void gload_tile(u32x4 (&r)[L], const T* __restrict__ base, int ld,
                                            int row0, int nrows, int k0, int tid) {
   constexpr int CH = 16 / (int)sizeof(T);
 #pragma unroll
   for (int i = 0; i < L; ++i) {
-    const int c = tid + i * 256, gr = row0 + (c >> 3);
+    const int c = tid + i * 256, gr = row0 + c / KCH;
     const int rr = gr < nrows ? gr : nrows - 1;
-    r[i] = *(gptr16)(const void*)(base + (size_t)rr * ld + k0 + (c & 7) * CH);
+    r[i] = *(gptr16)(const void*)(base + (size_t)rr * ld + k0 + (c % KCH) * CH);
   }
 }
 
-template <int L>
+template <int L, int KCH>
 __device__ __forceinline__ void sstore_tile(const u32x4 (&r)[L], u32x4* __restrict__ lds, int tid) {
 #pragma unroll
   for (int i = 0; i < L; ++i) {
     const int c = tid + i * 256;
-    lds[swz(c >> 3, c & 7)] = r[i];
+    lds[swz<KCH>(c / KCH, c % KCH)] = r[i];
   }
 }
 
-// One 128-byte K slab of this wavefront's TN x TM block of 16x16 tiles.
-template <typename T, int TM, int TN>
+// One K slab of this wavefront's TN x TM block of 16x16 tiles.
+template <typename T, int TM, int TN, int KCH>
 __device__ __forceinline__ void mma_slab(f32x4 (&acc)[TN][TM], const u32x4* __restrict__ la,
                                          const u32x4* __restrict__ lw, int arow, int wrow,
                                          int lane) {
 #pragma unroll
-  for (int s = 0; s < 2; ++s) {
+  for (int s = 0; s < KCH / 4; ++s) {
     u32x4 af[TN], bfr[TM];
     const int ch = s * 4 + (lane >> 4);
 #pragma unroll
-    for (int tn = 0; tn < TN; ++tn) af[tn] = lw[swz(wrow + tn * 16, ch)];
+    for (int tn = 0; tn < TN; ++tn) af[tn] = lw[swz<KCH>(wrow + tn * 16, ch)];
 #pragma unroll
-    for (int tm = 0; tm < TM; ++tm) bfr[tm] = la[swz(arow + tm * 16, ch)];
+    for (int tm = 0; tm < TM; ++tm) bfr[tm] = la[swz<KCH>(arow + tm * 16, ch)];
 #pragma unroll
     for (int tn = 0; tn < TN; ++tn)
 #pragma unroll
@@ -230,21 +236,21 @@ __device__ __forceinline__ void mma_slab(f32x4 (&acc)[TN][TM], const u32x4* __re
   }
 }
 
-template <typename T, int BM, int BN, int WM, int WN, class Ep>
+template <typename T, int BM, int BN, int WM, int WN, int KCH, class Ep>
 __global__ void __launch_bounds__(256)
     gemm_kernel(const T* __restrict__ A, int lda, const T* __restrict__ W, int ldw, int M, int N,
                 int K, Ep ep) {
   constexpr int CH = 16 / (int)sizeof(T);  // elements per 16-byte chunk
-  constexpr int BK = 8 * CH;               // K per slab (128 bytes per row)
+  constexpr int BK = KCH * CH;             // K per slab (KCH * 16 bytes per row)
   constexpr int MW = BM / WM, NW = BN / WN;
   constexpr int TM = MW / 16, TN = NW / 16;
-  constexpr int LA = BM * 8 / 256, LW = BN * 8 / 256;
+  constexpr int LA = BM * KCH / 256, LW = BN * KCH / 256;
   static_assert(WM * WN == 4, "four wavefronts");
   static_assert(MW % 16 == 0 && NW % 16 == 0, "16x16 MFMA tiles");
-  static_assert((BM * 8) % 256 == 0 && (BN * 8) % 256 == 0, "whole chunks per thread");
+  static_assert((BM * KCH) % 256 == 0 && (BN * KCH) % 256 == 0, "whole chunks per thread");
 
-  __shared__ u32x4 sA[2][BM * 8];
-  __shared__ u32x4 sW[2][BN * 8];
+  __shared__ u32x4 sA[2][BM * KCH];
+  __shared__ u32x4 sW[2][BN * KCH];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
@@ -267,34 +273,34 @@ __global__ void __launch_bounds__(256)
   // it) so that the count of loads in flight is the same on every path and
   // the waits before each LDS store cover only the older slab.
   auto kofs = [nk](int k) { return (k < nk ? k : nk - 1) * BK; };
-  gload_tile<LA>(ra0, A, lda, m0, M, 0, tid);
-  gload_tile<LW>(rw0, W, ldw, n0, N, 0, tid);
-  gload_tile<LA>(ra1, A, lda, m0, M, kofs(1), tid);
-  gload_tile<LW>(rw1, W, ldw, n0, N, kofs(1), tid);
-  sstore_tile<LA>(ra0, sA[0], tid);
-  sstore_tile<LW>(rw0, sW[0], tid);
+  gload_tile<LA, KCH>(ra0, A, lda, m0, M, 0, tid);
+  gload_tile<LW, KCH>(rw0, W, ldw, n0, N, 0, tid);
+  gload_tile<LA, KCH>(ra1, A, lda, m0, M, kofs(1), tid);
+  gload_tile<LW, KCH>(rw1, W, ldw, n0, N, kofs(1), tid);
+  sstore_tile<LA, KCH>(ra0, sA[0], tid);
+  sstore_tile<LW, KCH>(rw0, sW[0], tid);
   __syncthreads();
   // Slab kt is in LDS buffer kt&1; register stage kt&1 is free, stage
   // (kt+1)&1 holds slab kt+1.  Pairs of slabs per trip keep the register
   // stages statically addressed; an odd last slab is peeled.
   int kt = 0;
   for (; kt + 2 <= nk; kt += 2) {
-    gload_tile<LA>(ra0, A, lda, m0, M, kofs(kt + 2), tid);
-    gload_tile<LW>(rw0, W, ldw, n0, N, kofs(kt + 2), tid);
-    mma_slab<T, TM, TN>(acc, sA[0], sW[0], arow, wrow, lane);
-    sstore_tile<LA>(ra1, sA[1], tid);
-    sstore_tile<LW>(rw1, sW[1], tid);
+    gload_tile<LA, KCH>(ra0, A, lda, m0, M, kofs(kt + 2), tid);
+    gload_tile<LW, KCH>(rw0, W, ldw, n0, N, kofs(kt + 2), tid);
+    mma_slab<T, TM, TN, KCH>(acc, sA[0], sW[0], arow, wrow, lane);
+    sstore_tile<LA, KCH>(ra1, sA[1], tid);
+    sstore_tile<LW, KCH>(rw1, sW[1], tid);
     __syncthreads();
-    gload_tile<LA>(ra1, A, lda, m0, M, kofs(kt + 3), tid);
-    gload_tile<LW>(rw1, W, ldw, n0, N, kofs(kt + 3), tid);
-    mma_slab<T, TM, TN>(acc, sA[1], sW[1], arow, wrow, lane);
+    gload_tile<LA, KCH>(ra1, A, lda, m0, M, kofs(kt + 3), tid);
+    gload_tile<LW, KCH>(rw1, W, ldw, n0, N, kofs(kt + 3), tid);
+    mma_slab<T, TM, TN, KCH>(acc, sA[1], sW[1], arow, wrow, lane);
     // unconditional: past the end it rewrites buffer 0, which nothing reads
     // any more (an odd last slab has kt + 2 == nk - 1 and is the real one)
-    sstore_tile<LA>(ra0, sA[0], tid);
-    sstore_tile<LW>(rw0, sW[0], tid);
+    sstore_tile<LA, KCH>(ra0, sA[0], tid);
+    sstore_tile<LW, KCH>(rw0, sW[0], tid);
     __syncthreads();
   }
-  if (kt < nk) mma_slab<T, TM, TN>(acc, sA[0], sW[0], arow, wrow, lane);
+  if (kt < nk) mma_slab<T, TM, TN, KCH>(acc, sA[0], sW[0], arow, wrow, lane);
 
   if constexpr (!IsHead<Ep>::value) {
 #pragma unroll
@@ -361,12 +367,12 @@ __global__ void __launch_bounds__(256)
   }
 }
 
-template <typename T, int BM, int BN, int WM, int WN, class Ep>
+template <typename T, int BM, int BN, int WM, int WN, int KCH = 8, class Ep>
 hipError_t run(const T* A, int lda, const T* W, int ldw, int M, int N, int K, const Ep& ep,
                hipStream_t s) {
   const int tiles = ((N + BN - 1) / BN) * ((M + BM - 1) / BM);
-  hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN, Ep>), dim3(tiles), dim3(256), 0, s, A, lda,
-                     W, ldw, M, N, K, ep);
+  hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN, KCH, Ep>), dim3(tiles), dim3(256), 0, s, A,
+                     lda, W, ldw, M, N, K, ep);
   return hipGetLastError();
 }
 
