@@ -227,7 +227,9 @@ def main():
     prompt = S.make_prompts(w["prompts"], 1, B, N, cfg.vocab)
     kc = Bd.make_config(cfg.n_layer, cfg.d_model, cfg.n_head, cfg.d_mlp, cfg.vocab, cfg.n_ctx,
                         cfg.dtype, B, max(k, 1), N, 0)
-    kf = Bd.KForcing(kc, device="cuda:0")
+    stream = torch.cuda.Stream(device=dev)  # a real stream: decode blocks replay as a HIP graph
+    torch.cuda.set_stream(stream)
+    kf = Bd.KForcing(kc, device="cuda:0", stream=stream)
     kf.load_weights(blob)
     dprompt = torch.as_tensor(prompt, device=dev)
     out = torch.empty((B, L), dtype=torch.int32, device=dev)

@@ -144,6 +144,14 @@ int kf_debug_logits(kf_ctx *ctx, float *out, size_t n_floats);
 /* Fill out [B][n] with the device generator's u for positions p0..p0+n-1. */
 int kf_fill_noise(kf_ctx *ctx, uint64_t seed, int B, int p0, int n, float *out);
 
+/* Replay the decode blocks of kf_generate / kf_generate_ar as one captured
+ * HIP graph per argument set (default on).  Every launch of a decode block
+ * reads the context length from device memory, so a captured block replays
+ * unchanged; the instantiated graph is kept on the context until the
+ * arguments, the state buffer or the weights change.  Used only on a non-null
+ * stream and while kernel timing is off; results are identical either way. */
+int kf_set_graphs(kf_ctx *ctx, int enable);
+
 /* Host view of the sequence state: committed length C, pending count, B. */
 int kf_get_state(const kf_ctx *ctx, int *C, int *pending, int *B);
 
@@ -159,13 +167,13 @@ int kf_device_errors(kf_ctx *ctx, int *flags);
  * and the launch count of one class since timing was last set. */
 #define KF_KC_EMBED 0    /* real-row embedding */
 #define KF_KC_NOISE 1    /* noise sinusoid + noise-MLP GEMMs + position add */
-#define KF_KC_NORM 2     /* LayerNorm kernels */
-#define KF_KC_QKV 3      /* QKV GEMM with KV append */
+#define KF_KC_NORM 2     /* standalone LayerNorm (none: every LayerNorm is folded into the GEMM that consumes it) */
+#define KF_KC_QKV 3      /* LayerNorm-folded QKV GEMM with KV append */
 #define KF_KC_ATTN 4     /* block attention */
 #define KF_KC_OPROJ 5    /* attention-out GEMM + residual */
-#define KF_KC_MLP_UP 6   /* MLP up GEMM + GELU */
+#define KF_KC_MLP_UP 6   /* LayerNorm-folded MLP up GEMM + GELU */
 #define KF_KC_MLP_DOWN 7 /* MLP down GEMM + residual */
-#define KF_KC_HEAD 8     /* LM-head GEMM with fused argmax partials / logits */
+#define KF_KC_HEAD 8     /* final-LayerNorm-folded head GEMM with argmax partials / logits */
 #define KF_KC_SELECT 9   /* argmax reduction or inverse-CDF sampler, commit */
 #define KF_KC_COUNT 10
 #define KF_TIMING_ALL ((1 << KF_KC_COUNT) - 1)

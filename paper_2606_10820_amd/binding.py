@@ -72,6 +72,7 @@ def lib():
         "kf_fill_noise": (I, [P, U64, I, I, I, P]),
         "kf_get_state": (I, [P, IP, IP, IP]),
         "kf_device_errors": (I, [P, IP]),
+        "kf_set_graphs": (I, [P, I]),
         "kf_set_timing": (I, [P, I]),
         "kf_kernel_time": (I, [P, I, ctypes.POINTER(ctypes.c_double), IP]),
         "kf_destroy": (None, [P]),
@@ -224,6 +225,9 @@ class KForcing:
         f = ctypes.c_int()
         self._check(self.L.kf_device_errors(self.h, ctypes.byref(f)))
         return f.value
+
+    def set_graphs(self, enable: bool):
+        self._check(self.L.kf_set_graphs(self.h, int(enable)))
 
     def set_timing(self, class_mask: int = KF_TIMING_ALL):
         """Bracket launches of the selected kernel classes (bit mask) with HIP events."""

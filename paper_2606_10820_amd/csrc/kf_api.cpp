@@ -27,6 +27,7 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // ------------------------------------------------------------ memory plan
 struct LayerOff {
   size_t ln1_g, ln1_b, wqkv, bqkv, wo, bo, ln2_g, ln2_b, w1, b1, w2, b2;
+  size_t qkv_c1, qkv_c2, up_c1, up_c2;  // folded LayerNorm sums (fp32)
 };
 
 struct Plan {
@@ -38,6 +39,7 @@ struct Plan {
   int logit_rows = 0;
   size_t wbegin = 0, wend = 0;
   size_t tok = 0, pos = 0, nw1 = 0, nb1 = 0, nw2 = 0, nb2 = 0, omega = 0, lnf_g = 0, lnf_b = 0;
+  size_t head_c1 = 0, head_c2 = 0;
   std::vector<LayerOff> layer;
   size_t kv = 0, kv_bytes = 0;
   size_t X = 0, A = 0, Q = 0, O = 0, Hm = 0, noise = 0, pval = 0, pidx = 0, logits = 0, dstate = 0,
@@ -105,9 +107,15 @@ void make_plan(const kf_config& c, Plan& p) {
     y.b1 = take(f * 4);
     y.w2 = take(d * f * es);
     y.b2 = take(d * 4);
+    y.qkv_c1 = take(3 * d * 4);
+    y.qkv_c2 = take(3 * d * 4);
+    y.up_c1 = take(f * 4);
+    y.up_c2 = take(f * 4);
   }
   p.lnf_g = take(d * 4);
   p.lnf_b = take(d * 4);
+  p.head_c1 = take((size_t)p.Vpad * 4);
+  p.head_c2 = take((size_t)p.Vpad * 4);
   p.wend = off;
   p.kv_bytes = (size_t)c.max_batch * L * 2 * T * d * es;
   p.kv = take(p.kv_bytes);
@@ -159,6 +167,18 @@ struct kf_ctx {
   std::vector<Ev> evs;
   size_t ev_used = 0;
   bool ev_open = false;
+  // HIP-graph replay of the fixed-shape decode block of a generation run
+  bool graphs = true;
+  hipGraphExec_t gexec = nullptr;
+  struct GraphKey {
+    int B, nr, k, N, L;
+    uint64_t seed;
+    const void* out;
+    bool operator==(const GraphKey& o) const {
+      return B == o.B && nr == o.nr && k == o.k && N == o.N && L == o.L && seed == o.seed &&
+             out == o.out;
+    }
+  } gkey{};
 };
 
 namespace {
@@ -238,7 +258,7 @@ int run_step(kf_ctx* c, const StepIn& in) {
   hipStream_t s = c->stream;
   KfDevState* st = reinterpret_cast<KfDevState*>(base + p.dstate);
   float* X = reinterpret_cast<float*>(base + p.X);
-  T* A = reinterpret_cast<T*>(base + p.A);
+  T* A = reinterpret_cast<T*>(base + p.A);  // noise sinusoid staging
   T* Q = reinterpret_cast<T*>(base + p.Q);
   T* O = reinterpret_cast<T*>(base + p.O);
   T* Hm = reinterpret_cast<T*>(base + p.Hm);
@@ -271,23 +291,23 @@ int run_step(kf_ctx* c, const StepIn& in) {
   }
   for (int l = 0; l < cf.n_layer; ++l) {
     const LayerOff& y = p.layer[l];
-    KF_LAUNCH(c, KF_KC_NORM, kf::launch_layernorm<T>(X, A, F(y.ln1_g), F(y.ln1_b), M, d, 0, g, s));
-    KF_LAUNCH(c, KF_KC_QKV, kf::gemm_qkv<T>(A, W(y.wqkv), M, d, F(y.bqkv), Q, kv, g, kg, l, st, s));
+    const kf::LnFold ln1{F(y.ln1_g), F(y.qkv_c1), F(y.qkv_c2)};
+    const kf::LnFold ln2{F(y.ln2_g), F(y.up_c1), F(y.up_c2)};
+    KF_LAUNCH(c, KF_KC_QKV,
+              kf::gemm_qkv_ln<T>(X, ln1, W(y.wqkv), M, d, F(y.bqkv), Q, kv, g, kg, l, st, s));
     KF_LAUNCH(c, KF_KC_ATTN, kf::launch_attention<T>(Q, kv, O, st, g, kg, l, s));
     KF_LAUNCH(c, KF_KC_OPROJ, kf::gemm_residual<T>(O, W(y.wo), M, d, d, F(y.bo), X, s));
-    KF_LAUNCH(c, KF_KC_NORM, kf::launch_layernorm<T>(X, A, F(y.ln2_g), F(y.ln2_b), M, d, 0, g, s));
-    KF_LAUNCH(c, KF_KC_MLP_UP,
-              kf::gemm_bias<T>(A, W(y.w1), M, f, d, F(y.b1), kf::Act::Gelu, Hm, f, s));
+    KF_LAUNCH(c, KF_KC_MLP_UP, kf::gemm_up_ln<T>(X, ln2, W(y.w1), M, f, d, F(y.b1), Hm, s));
     KF_LAUNCH(c, KF_KC_MLP_DOWN, kf::gemm_residual<T>(Hm, W(y.w2), M, d, f, F(y.b2), X, s));
   }
   const bool ar = in.k == 0;
   const int Mh = ar ? in.B : in.B * in.k;
-  KF_LAUNCH(c, KF_KC_NORM,
-            kf::launch_layernorm<T>(X, A, F(p.lnf_g), F(p.lnf_b), Mh, d, ar ? 2 : 1, g, s));
   float* logits = (ar || debug) ? reinterpret_cast<float*>(base + p.logits) : nullptr;
+  const kf::LnFold lnf{F(p.lnf_g), F(p.head_c1), F(p.head_c2)};
   KF_LAUNCH(c, KF_KC_HEAD,
-            kf::gemm_head<T>(A, tok, Mh, p.Vpad, V, d, reinterpret_cast<float*>(base + p.pval),
-                             reinterpret_cast<int*>(base + p.pidx), logits, s));
+            kf::gemm_head_ln<T>(X, lnf, tok, Mh, p.Vpad, V, d, ar ? 2 : 1, g,
+                                reinterpret_cast<float*>(base + p.pval),
+                                reinterpret_cast<int*>(base + p.pidx), logits, s));
   if (!ar)
     KF_LAUNCH(c, KF_KC_SELECT,
               kf::launch_argmax_select(reinterpret_cast<const float*>(base + p.pval),
@@ -323,6 +343,74 @@ KfOutDesc out_desc(kf_ctx* c, int32_t* out, int stride, int gen_base) {
 }
 
 int32_t* pend_ptr(kf_ctx* c) { return reinterpret_cast<int32_t*>(c->base + c->plan.pend); }
+
+// Per-column sums of the LayerNorm-folded GEMMs: QKV (ln1), MLP up (ln2) and
+// the head (final norm, over all V_pad rows of the token table).
+template <typename T>
+int fold_layernorms(kf_ctx* c) {
+  const Plan& p = c->plan;
+  char* base = c->base;
+  const int d = c->cfg.d_model, f = c->cfg.d_mlp;
+  auto F = [&](size_t o) { return reinterpret_cast<float*>(base + o); };
+  auto W = [&](size_t o) { return reinterpret_cast<const T*>(base + o); };
+  for (const LayerOff& y : p.layer) {
+    KF_HIP(c, kf::launch_ln_fold<T>(W(y.wqkv), F(y.ln1_g), F(y.ln1_b), 3 * d, d, F(y.qkv_c1),
+                                    F(y.qkv_c2), c->stream));
+    KF_HIP(c, kf::launch_ln_fold<T>(W(y.w1), F(y.ln2_g), F(y.ln2_b), f, d, F(y.up_c1), F(y.up_c2),
+                                    c->stream));
+  }
+  KF_HIP(c, kf::launch_ln_fold<T>(W(p.tok), F(p.lnf_g), F(p.lnf_b), p.Vpad, d, F(p.head_c1),
+                                  F(p.head_c2), c->stream));
+  return KF_OK;
+}
+
+void drop_graph(kf_ctx* c) {
+  if (c->gexec) (void)hipGraphExecDestroy(c->gexec);
+  c->gexec = nullptr;
+}
+
+// Run `count` identical steps and advance the host view of C by `adv` after
+// each.  Every launch of such a step reads C from device memory, so one
+// captured step replays unchanged; the instantiated graph is cached on the
+// context for the next call with the same arguments.  Graphs need a real
+// stream (capture is impossible on the legacy null stream) and are not used
+// while kernel timing is on.
+int repeat_step(kf_ctx* c, const StepIn& in, int count, int adv, int N, int L) {
+  if (count <= 0) return KF_OK;
+  if (!c->graphs || c->stream == nullptr || c->timing) {
+    for (int i = 0; i < count; ++i) {
+      int r = step(c, in);
+      if (r) return r;
+      c->C += adv;
+    }
+    return KF_OK;
+  }
+  kf_ctx::GraphKey key{in.B, in.nr, in.k, N, L, in.seed, in.od.out};
+  if (!c->gexec || !(key == c->gkey)) {
+    drop_graph(c);
+    KF_HIP(c, hipStreamBeginCapture(c->stream, hipStreamCaptureModeRelaxed));
+    int r = step(c, in);
+    hipGraph_t g = nullptr;
+    hipError_t e = hipStreamEndCapture(c->stream, &g);
+    if (r) {
+      if (e == hipSuccess && g) (void)hipGraphDestroy(g);
+      return r;
+    }
+    if (e != hipSuccess) return hip_fail(c, e, "hipStreamEndCapture");
+    e = hipGraphInstantiate(&c->gexec, g, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(g);
+    if (e != hipSuccess) {
+      c->gexec = nullptr;
+      return hip_fail(c, e, "hipGraphInstantiate");
+    }
+    c->gkey = key;
+  }
+  for (int i = 0; i < count; ++i) {
+    KF_HIP(c, hipGraphLaunch(c->gexec, c->stream));
+    c->C += adv;
+  }
+  return KF_OK;
+}
 
 }  // namespace
 
@@ -365,6 +453,7 @@ int kf_create(const kf_config* cfg, void* hip_stream, kf_ctx** out) {
 
 void kf_destroy(kf_ctx* c) {
   if (!c) return;
+  drop_graph(c);
   for (auto& e : c->evs) {
     (void)hipEventDestroy(e.a);
     (void)hipEventDestroy(e.b);
@@ -378,6 +467,7 @@ int kf_bind_state(kf_ctx* c, void* dev_ptr, size_t bytes) {
   if (reinterpret_cast<uintptr_t>(dev_ptr) & 255) return fail(c, KF_EINVAL, "state pointer must be 256-byte aligned");
   if (bytes < c->plan.total)
     return fail(c, KF_ENOMEM, "state buffer has %zu bytes, %zu needed", bytes, c->plan.total);
+  drop_graph(c);
   c->base = static_cast<char*>(dev_ptr);
   c->bytes = bytes;
   c->weights = false;
@@ -393,6 +483,7 @@ int kf_load_weights(kf_ctx* c, const void* blob, size_t bytes, int blob_is_devic
   if (blob_is_device != 0 && blob_is_device != 1) return fail(c, KF_EINVAL, "blob_is_device must be 0 or 1");
   const kf_config& cf = c->cfg;
   const Plan& p = c->plan;
+  drop_graph(c);
   const size_t d = cf.d_model, f = cf.d_mlp, V = cf.vocab, T = cf.n_ctx, L = cf.n_layer;
   const size_t n_params = V * d + T * d + 8 * d * d + 4 * d + d +
                           L * (2 * d + 3 * d * d + 3 * d + d * d + d + 2 * d + f * d + f + d * f + d) +
@@ -476,6 +567,10 @@ int kf_load_weights(kf_ctx* c, const void* blob, size_t bytes, int blob_is_devic
     KF_HIP(c, hipMemcpyAsync(c->base + p.omega, omega.data(), omega.size() * 8, hipMemcpyHostToDevice, c->stream));
     KF_HIP(c, hipStreamSynchronize(c->stream));
   }
+  {
+    int r = bf ? fold_layernorms<bf16>(c) : fold_layernorms<float>(c);
+    if (r) return r;
+  }
   // device sequence state starts cleared (context length and error flags)
   KF_HIP(c, kf::launch_zero_i32(reinterpret_cast<int*>(c->base + p.dstate),
                                 sizeof(KfDevState) / sizeof(int), c->stream));
@@ -543,13 +638,8 @@ int kf_generate(kf_ctx* c, int B, int N, const int32_t* prompt, int L, int k, ui
   c->B = B;
   c->C = N;
   c->pending = k;
-  for (int s = 1; s < L / k; ++s) {
-    StepIn dn{B, k, k, pend_ptr(c), cf.max_k, nullptr, nullptr, seed, out_desc(c, out, L, N), false};
-    r = step(c, dn);
-    if (r) return r;
-    c->C += k;
-  }
-  return KF_OK;
+  StepIn dn{B, k, k, pend_ptr(c), cf.max_k, nullptr, nullptr, seed, out_desc(c, out, L, N), false};
+  return repeat_step(c, dn, L / k - 1, k, N, L);
 }
 
 int kf_prefill_ar(kf_ctx* c, int B, int N, const int32_t* prompt, const float* u, int32_t* out) {
@@ -607,13 +697,8 @@ int kf_generate_ar(kf_ctx* c, int B, int N, const int32_t* prompt, int L, uint64
   c->B = B;
   c->C = N;
   c->pending = 1;
-  for (int s = 1; s < L; ++s) {
-    StepIn dn{B, 1, 0, pend_ptr(c), cf.max_k, nullptr, nullptr, seed, out_desc(c, out, L, N), false};
-    r = step(c, dn);
-    if (r) return r;
-    c->C += 1;
-  }
-  return KF_OK;
+  StepIn dn{B, 1, 0, pend_ptr(c), cf.max_k, nullptr, nullptr, seed, out_desc(c, out, L, N), false};
+  return repeat_step(c, dn, L - 1, 1, N, L);
 }
 
 int kf_debug_logits(kf_ctx* c, float* out, size_t n_floats) {
@@ -651,6 +736,13 @@ int kf_device_errors(kf_ctx* c, int* flags) {
   *flags = h.err;
   if (h.err) KF_HIP(c, kf::launch_zero_i32(&st->err, 1, c->stream));
   KF_HIP(c, hipStreamSynchronize(c->stream));
+  return KF_OK;
+}
+
+int kf_set_graphs(kf_ctx* c, int enable) {
+  if (!c) return KF_EINVAL;
+  c->graphs = enable != 0;
+  if (!c->graphs) drop_graph(c);
   return KF_OK;
 }
 

@@ -88,13 +88,6 @@ hipError_t launch_noise_sinusoid(T* S, const float* noise, uint64_t seed, const 
                                  KfStepGeom g, int d, const KfDevState* st, float* u_out,
                                  hipStream_t s);
 
-// LayerNorm (fp32 statistics) of selected rows of X into Y [rows][d].
-// gather: 0 = row m; 1 = noise row m of the step (b = m / k, j = m % k);
-//         2 = last real row of sequence m.
-template <typename T>
-hipError_t launch_layernorm(const float* X, T* Y, const float* gain, const float* shift, int rows,
-                            int d, int gather, KfStepGeom g, hipStream_t s);
-
 // Block attention over the KV cache for every (sequence, head, query block).
 template <typename T>
 hipError_t launch_attention(const T* Q, const T* kv, T* O, const KfDevState* st, KfStepGeom g,
@@ -107,20 +100,38 @@ hipError_t gemm_bias(const T* A, const T* W, int M, int N, int K, const float* b
 template <typename T>
 hipError_t gemm_residual(const T* A, const T* W, int M, int N, int K, const float* bias, float* X,
                          hipStream_t s);
+// LayerNorm folded into a GEMM (gain, shift and the precomputed per-column
+// sums c1 = W.gain, c2 = W.shift).  A rows are read from the fp32 residual
+// stream X [rows][d].
+struct LnFold {
+  const float* gain;
+  const float* c1;
+  const float* c2;
+};
 template <typename T>
-hipError_t gemm_qkv(const T* A, const T* W, int M, int d, const float* bias, T* Q, T* kv,
-                    KfStepGeom g, KfKvGeom kg, int layer, const KfDevState* st, hipStream_t s);
+hipError_t gemm_qkv_ln(const float* X, const LnFold& ln, const T* W, int M, int d,
+                       const float* bias, T* Q, T* kv, KfStepGeom g, KfKvGeom kg, int layer,
+                       const KfDevState* st, hipStream_t s);
+template <typename T>
+hipError_t gemm_up_ln(const float* X, const LnFold& ln, const T* W, int M, int N, int d,
+                      const float* bias, T* out, hipStream_t s);
 template <typename T>
 hipError_t gemm_noise_out(const T* A, const T* W, int M, int d, int K, const float* bias,
                           const T* pos, float* X, KfStepGeom g, const KfDevState* st,
                           hipStream_t s);
-// Head: logits of M rows over Vpad columns; per (row, 128-column tile) the
+// Head over the final LayerNorm of the selected rows (gather: 1 = noise rows
+// of the step, 2 = last real row per sequence): per (row, 128-column tile) the
 // maximum and its lowest column index into pval/pidx [M][Vpad/128]; columns
 // >= V are excluded.  When logits is not null the fp32 logits [M][V] are
 // written as well.
 template <typename T>
-hipError_t gemm_head(const T* A, const T* W, int M, int Vpad, int V, int K, float* pval,
-                     int* pidx, float* logits, hipStream_t s);
+hipError_t gemm_head_ln(const float* X, const LnFold& ln, const T* W, int M, int Vpad, int V,
+                        int d, int gather, KfStepGeom g, float* pval, int* pidx, float* logits,
+                        hipStream_t s);
+// c1 = W gain and c2 = W shift for a folded LayerNorm, W [N][K].
+template <typename T>
+hipError_t launch_ln_fold(const T* W, const float* gain, const float* shift, int N, int K,
+                          float* c1, float* c2, hipStream_t s);
 constexpr int kHeadTileN = 128;
 
 // Argmax over the head partials of each row, ties to the lowest id; writes the

@@ -1,5 +1,5 @@
 // kf_kernels.hip -- gfx950 kernels of the K-Forcing decode step other than the
-// GEMM family: real-row embedding, noise sinusoid, LayerNorm, block attention,
+// GEMM family: real-row embedding, noise sinusoid, block attention,
 // token selection (argmax / inverse CDF) and small utilities.
 #include <float.h>
 #include <math.h>
@@ -69,43 +69,6 @@ __global__ void __launch_bounds__(256)
     row[i] = from_f<T>((float)cs);
     row[h + i] = from_f<T>((float)sn);
   }
-}
-
-// ------------------------------------------------------------ LayerNorm
-// One wavefront per row; statistics in fp32 from registers (two passes).
-template <typename T, int EPL>
-__global__ void __launch_bounds__(256)
-    layernorm_kernel(const float* __restrict__ X, T* __restrict__ Y, const float* __restrict__ gain,
-                     const float* __restrict__ shift, int rows, int d, int gather, KfStepGeom g) {
-  const int lane = threadIdx.x & 63;
-  const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (m >= rows) return;
-  int src = m;
-  if (gather == 1) src = (m / g.k) * g.R + g.nr + (m % g.k);
-  else if (gather == 2) src = m * g.R + g.nr - 1;
-  const float* x = X + (size_t)src * d;
-  const int n = d >> 6;  // elements per lane
-  float v[EPL];
-  float s = 0.f;
-#pragma unroll
-  for (int c = 0; c < EPL; ++c) {
-    v[c] = (c < n) ? x[c * 64 + lane] : 0.f;
-    s += v[c];
-  }
-  const float mean = wave_sum(s) / (float)d;
-  float q = 0.f;
-#pragma unroll
-  for (int c = 0; c < EPL; ++c)
-    if (c < n) q += (v[c] - mean) * (v[c] - mean);
-  const float var = wave_sum(q) / (float)d;
-  const float rstd = 1.0f / sqrtf(var + 1e-5f);
-  T* y = Y + (size_t)m * d;
-#pragma unroll
-  for (int c = 0; c < EPL; ++c)
-    if (c < n) {
-      int e = c * 64 + lane;
-      y[e] = from_f<T>((v[c] - mean) * rstd * gain[e] + shift[e]);
-    }
 }
 
 // ------------------------------------------------------ block attention
@@ -502,23 +465,6 @@ hipError_t launch_noise_sinusoid(T* S, const float* noise, uint64_t seed, const 
 }
 
 template <typename T>
-hipError_t launch_layernorm(const float* X, T* Y, const float* gain, const float* shift, int rows,
-                            int d, int gather, KfStepGeom g, hipStream_t s) {
-  if (rows <= 0) return hipSuccess;
-  dim3 grid((rows + 3) / 4);
-  if (d <= 512)
-    hipLaunchKernelGGL((layernorm_kernel<T, 8>), grid, dim3(256), 0, s, X, Y, gain, shift, rows, d,
-                       gather, g);
-  else if (d <= 1024)
-    hipLaunchKernelGGL((layernorm_kernel<T, 16>), grid, dim3(256), 0, s, X, Y, gain, shift, rows,
-                       d, gather, g);
-  else
-    hipLaunchKernelGGL((layernorm_kernel<T, 32>), grid, dim3(256), 0, s, X, Y, gain, shift, rows,
-                       d, gather, g);
-  return hipGetLastError();
-}
-
-template <typename T>
 hipError_t launch_attention(const T* Q, const T* kv, T* O, const KfDevState* st, KfStepGeom g,
                             KfKvGeom kg, int layer, hipStream_t s) {
   if (g.B <= 0 || g.R <= 0) return hipSuccess;
@@ -620,8 +566,6 @@ hipError_t launch_zero_i32(int* dst, size_t n, hipStream_t s) { return launch_ze
   template hipError_t launch_noise_sinusoid<T>(T*, const float*, uint64_t, const double*,          \
                                                KfStepGeom, int, const KfDevState*, float*,          \
                                                hipStream_t);                                        \
-  template hipError_t launch_layernorm<T>(const float*, T*, const float*, const float*, int, int,  \
-                                          int, KfStepGeom, hipStream_t);                            \
   template hipError_t launch_attention<T>(const T*, const T*, T*, const KfDevState*, KfStepGeom,   \
                                           KfKvGeom, int, hipStream_t);                              \
   template hipError_t launch_convert<T>(const float*, T*, size_t, hipStream_t);                    \

@@ -269,3 +269,30 @@ def test_toy_bf16(toy):
     prompt = S.prompts_uniform(1, 4, 16, TOY_BF16.vocab)
     st = run_teacher_forced(kf, model, prompt, [4] * 8, noise_seed=2, tol=TOL[1])
     _log(f"toy bf16 parity: {st}")
+
+
+def test_graph_replay_matches_direct(toy):
+    """On a real stream, kf_generate replays the decode block as a HIP graph;
+    tokens and the last logits equal the direct launches, across repeated calls
+    (graph reuse) and after the arguments change (re-capture)."""
+    from paper_2606_10820_amd import binding as Bd
+    blob, _ = toy
+    stream = torch.cuda.Stream()
+    prompt = S.prompts_uniform(4, 4, 16, TOY.vocab)
+    c = Bd.make_config(TOY.n_layer, TOY.d_model, TOY.n_head, TOY.d_mlp, TOY.vocab, TOY.n_ctx,
+                       TOY.dtype, 4, 4, 16, Bd.KF_FLAG_DEBUG_LOGITS)
+    res = {}
+    with torch.cuda.stream(stream):
+        for graphs in (False, True):
+            kf = Bd.KForcing(c, stream=stream)
+            kf.load_weights(blob)
+            kf.set_graphs(graphs)
+            outs = []
+            for seed in (5, 5, 6):
+                outs.append(kf.generate(prompt, 48, 4, seed=seed).cpu().numpy())
+                outs.append(kf.debug_logits(16).cpu().numpy())
+                outs.append(kf.generate_ar(prompt, 8, seed=seed).cpu().numpy())
+            stream.synchronize()
+            res[graphs] = outs
+    for a, b in zip(res[False], res[True]):
+        np.testing.assert_array_equal(a, b)
