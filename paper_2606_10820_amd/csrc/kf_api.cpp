@@ -39,10 +39,10 @@ struct Plan {
   int logit_rows = 0;
   size_t wbegin = 0, wend = 0;
   size_t tok = 0, pos = 0, nw1 = 0, nb1 = 0, nw2 = 0, nb2 = 0, omega = 0, lnf_g = 0, lnf_b = 0;
-  size_t head_c1 = 0, head_c2 = 0;
+  size_t head_c1 = 0, head_c2 = 0, head_w = 0;  // folded final norm; gain-scaled token table
   std::vector<LayerOff> layer;
   size_t kv = 0, kv_bytes = 0;
-  size_t X = 0, A = 0, Q = 0, O = 0, Hm = 0, noise = 0, pval = 0, pidx = 0, logits = 0, dstate = 0,
+  size_t X = 0, Xh = 0, A = 0, Q = 0, O = 0, Hm = 0, noise = 0, pval = 0, pidx = 0, logits = 0, dstate = 0,
          pend = 0;
   size_t total = 0;
 };
@@ -116,11 +116,13 @@ void make_plan(const kf_config& c, Plan& p) {
   p.lnf_b = take(d * 4);
   p.head_c1 = take((size_t)p.Vpad * 4);
   p.head_c2 = take((size_t)p.Vpad * 4);
+  p.head_w = take((size_t)p.Vpad * d * es);
   p.wend = off;
   p.kv_bytes = (size_t)c.max_batch * L * 2 * T * d * es;
   p.kv = take(p.kv_bytes);
   const size_t R = p.rows_max, Hw = f > 4 * d ? f : 4 * d;
   p.X = take(R * d * 4);
+  p.Xh = es == 2 ? take(R * d * es) : p.X;
   p.A = take(R * d * es);
   p.Q = take(R * d * es);
   p.O = take(R * d * es);
@@ -258,6 +260,7 @@ int run_step(kf_ctx* c, const StepIn& in) {
   hipStream_t s = c->stream;
   KfDevState* st = reinterpret_cast<KfDevState*>(base + p.dstate);
   float* X = reinterpret_cast<float*>(base + p.X);
+  T* Xh = reinterpret_cast<T*>(base + p.Xh);  // compute-dtype residual copy (X itself for fp32)
   T* A = reinterpret_cast<T*>(base + p.A);  // noise sinusoid staging
   T* Q = reinterpret_cast<T*>(base + p.Q);
   T* O = reinterpret_cast<T*>(base + p.O);
@@ -276,7 +279,7 @@ int run_step(kf_ctx* c, const StepIn& in) {
   if (in.reset) KF_HIP(c, kf::launch_zero_i32(reinterpret_cast<int*>(st), 1, s));
   if (in.nr > 0)
     KF_LAUNCH(c, KF_KC_EMBED,
-              kf::launch_embed_real<T>(X, tok, pos, in.toks, in.tok_stride, g, d, V, st, s));
+              kf::launch_embed_real<T>(X, Xh, tok, pos, in.toks, in.tok_stride, g, d, V, st, s));
   if (in.k > 0) {
     const int Mk = in.B * in.k;
     float* urec = reinterpret_cast<float*>(base + p.noise);
@@ -287,25 +290,25 @@ int run_step(kf_ctx* c, const StepIn& in) {
     KF_LAUNCH(c, KF_KC_NOISE,
               kf::gemm_bias<T>(A, W(p.nw1), Mk, 4 * d, d, F(p.nb1), kf::Act::Gelu, Hm, 4 * d, s));
     KF_LAUNCH(c, KF_KC_NOISE,
-              kf::gemm_noise_out<T>(Hm, W(p.nw2), Mk, d, 4 * d, F(p.nb2), pos, X, g, st, s));
+              kf::gemm_noise_out<T>(Hm, W(p.nw2), Mk, d, 4 * d, F(p.nb2), pos, X, Xh, g, st, s));
   }
   for (int l = 0; l < cf.n_layer; ++l) {
     const LayerOff& y = p.layer[l];
-    const kf::LnFold ln1{F(y.ln1_g), F(y.qkv_c1), F(y.qkv_c2)};
-    const kf::LnFold ln2{F(y.ln2_g), F(y.up_c1), F(y.up_c2)};
+    const kf::LnFold ln1{F(y.qkv_c1), F(y.qkv_c2)};
+    const kf::LnFold ln2{F(y.up_c1), F(y.up_c2)};
     KF_LAUNCH(c, KF_KC_QKV,
-              kf::gemm_qkv_ln<T>(X, ln1, W(y.wqkv), M, d, F(y.bqkv), Q, kv, g, kg, l, st, s));
+              kf::gemm_qkv_ln<T>(Xh, ln1, W(y.wqkv), M, d, F(y.bqkv), Q, kv, g, kg, l, st, s));
     KF_LAUNCH(c, KF_KC_ATTN, kf::launch_attention<T>(Q, kv, O, st, g, kg, l, s));
-    KF_LAUNCH(c, KF_KC_OPROJ, kf::gemm_residual<T>(O, W(y.wo), M, d, d, F(y.bo), X, s));
-    KF_LAUNCH(c, KF_KC_MLP_UP, kf::gemm_up_ln<T>(X, ln2, W(y.w1), M, f, d, F(y.b1), Hm, s));
-    KF_LAUNCH(c, KF_KC_MLP_DOWN, kf::gemm_residual<T>(Hm, W(y.w2), M, d, f, F(y.b2), X, s));
+    KF_LAUNCH(c, KF_KC_OPROJ, kf::gemm_residual<T>(O, W(y.wo), M, d, d, F(y.bo), X, Xh, s));
+    KF_LAUNCH(c, KF_KC_MLP_UP, kf::gemm_up_ln<T>(Xh, ln2, W(y.w1), M, f, d, F(y.b1), Hm, s));
+    KF_LAUNCH(c, KF_KC_MLP_DOWN, kf::gemm_residual<T>(Hm, W(y.w2), M, d, f, F(y.b2), X, Xh, s));
   }
   const bool ar = in.k == 0;
   const int Mh = ar ? in.B : in.B * in.k;
   float* logits = (ar || debug) ? reinterpret_cast<float*>(base + p.logits) : nullptr;
-  const kf::LnFold lnf{F(p.lnf_g), F(p.head_c1), F(p.head_c2)};
+  const kf::LnFold lnf{F(p.head_c1), F(p.head_c2)};
   KF_LAUNCH(c, KF_KC_HEAD,
-            kf::gemm_head_ln<T>(X, lnf, tok, Mh, p.Vpad, V, d, ar ? 2 : 1, g,
+            kf::gemm_head_ln<T>(Xh, lnf, W(p.head_w), Mh, p.Vpad, V, d, ar ? 2 : 1, g,
                                 reinterpret_cast<float*>(base + p.pval),
                                 reinterpret_cast<int*>(base + p.pidx), logits, s));
   if (!ar)
@@ -344,23 +347,25 @@ KfOutDesc out_desc(kf_ctx* c, int32_t* out, int stride, int gen_base) {
 
 int32_t* pend_ptr(kf_ctx* c) { return reinterpret_cast<int32_t*>(c->base + c->plan.pend); }
 
-// Per-column sums of the LayerNorm-folded GEMMs: QKV (ln1), MLP up (ln2) and
-// the head (final norm, over all V_pad rows of the token table).
+// Fold each LayerNorm into the GEMM after it: the QKV and MLP-up weights are
+// scaled by the gain in place, the head gets a gain-scaled copy of the token
+// table (the table itself stays the embedding), and the per-column sums c1, c2
+// are computed.  The fold is exact up to the rounding of the scaled weights.
 template <typename T>
 int fold_layernorms(kf_ctx* c) {
   const Plan& p = c->plan;
   char* base = c->base;
   const int d = c->cfg.d_model, f = c->cfg.d_mlp;
   auto F = [&](size_t o) { return reinterpret_cast<float*>(base + o); };
-  auto W = [&](size_t o) { return reinterpret_cast<const T*>(base + o); };
+  auto W = [&](size_t o) { return reinterpret_cast<T*>(base + o); };
   for (const LayerOff& y : p.layer) {
-    KF_HIP(c, kf::launch_ln_fold<T>(W(y.wqkv), F(y.ln1_g), F(y.ln1_b), 3 * d, d, F(y.qkv_c1),
-                                    F(y.qkv_c2), c->stream));
-    KF_HIP(c, kf::launch_ln_fold<T>(W(y.w1), F(y.ln2_g), F(y.ln2_b), f, d, F(y.up_c1), F(y.up_c2),
-                                    c->stream));
+    KF_HIP(c, kf::launch_ln_fold<T>(W(y.wqkv), W(y.wqkv), F(y.ln1_g), F(y.ln1_b), 3 * d, d,
+                                    F(y.qkv_c1), F(y.qkv_c2), c->stream));
+    KF_HIP(c, kf::launch_ln_fold<T>(W(y.w1), W(y.w1), F(y.ln2_g), F(y.ln2_b), f, d, F(y.up_c1),
+                                    F(y.up_c2), c->stream));
   }
-  KF_HIP(c, kf::launch_ln_fold<T>(W(p.tok), F(p.lnf_g), F(p.lnf_b), p.Vpad, d, F(p.head_c1),
-                                  F(p.head_c2), c->stream));
+  KF_HIP(c, kf::launch_ln_fold<T>(W(p.tok), W(p.head_w), F(p.lnf_g), F(p.lnf_b), p.Vpad, d,
+                                  F(p.head_c1), F(p.head_c2), c->stream));
   return KF_OK;
 }
 

@@ -15,12 +15,15 @@
 #include <float.h>
 #include <math.h>
 
+#include <type_traits>
+
 #include "kf_internal.h"
 
 namespace kf {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));  // one 16-byte chunk
 
@@ -33,10 +36,14 @@ __device__ inline float from_f<float>(float x) { return x; }
 template <>
 __device__ inline bf16 from_f<bf16>(float x) { return (bf16)x; }
 
-// GELU, tanh form (GPT-2 style), evaluated with the device tanhf.
+// GELU, tanh form (GPT-2 style): 0.5 x (1 + tanh u) with u = c (x + 0.044715 x^3),
+// evaluated as x * sigmoid(2u) = x / (1 + exp(-2u)) (the same function; one
+// exponential and one fast division).  Saturates correctly at both ends:
+// exp(-2u) -> inf gives -0, exp(-2u) -> 0 gives x.
 __device__ inline float gelu_f(float x) {
   const float c = 0.7978845608028654f;
-  return 0.5f * x * (1.0f + tanhf(c * (x + 0.044715f * x * x * x)));
+  const float u = c * (x + 0.044715f * x * x * x);
+  return __fdividef(x, 1.0f + __expf(-2.0f * u));
 }
 
 template <typename T>
@@ -59,7 +66,23 @@ struct Mfma<float> {
 };
 
 // ------------------------------------------------------------ epilogues
-// store4(m, n, v): v holds C[m][n .. n+3]; N is a multiple of 4.
+// store4(m, n, v): v holds C[m][n .. n+3] with the bias already added (the
+// kernel loads each lane's bias columns before its K loop); N is a multiple
+// of 4.
+
+// Four consecutive values to T memory in one store.
+template <typename T>
+__device__ inline void put4(T* p, float a, float b, float c, float d) {
+  if constexpr (sizeof(T) == 2) {
+    const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (bf16)a) |
+                        ((uint32_t)__builtin_bit_cast(uint16_t, (bf16)b) << 16);
+    const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (bf16)c) |
+                        ((uint32_t)__builtin_bit_cast(uint16_t, (bf16)d) << 16);
+    *reinterpret_cast<uint2*>(p) = make_uint2(lo, hi);
+  } else {
+    *reinterpret_cast<float4*>(p) = make_float4(a, b, c, d);
+  }
+}
 
 template <typename T>
 struct EpBias {
@@ -68,28 +91,31 @@ struct EpBias {
   const float* bias;
   int gelu;
   __device__ inline void store4(int m, int n, f32x4 v) const {
-    T* o = out + (size_t)m * ldo + n;
+    float x[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float x = v[i] + (bias ? bias[n + i] : 0.f);
-      if (gelu) x = gelu_f(x);
-      o[i] = from_f<T>(x);
-    }
+    for (int i = 0; i < 4; ++i) x[i] = gelu ? gelu_f(v[i]) : v[i];
+    put4(out + (size_t)m * ldo + n, x[0], x[1], x[2], x[3]);
   }
 };
 
+// Residual update X += C + bias.  With a 16-bit compute dtype the updated row
+// is also written to Xh, the compute-dtype copy of the residual stream that the
+// LayerNorm-folded GEMMs read (for fp32, Xh is X itself).
+template <typename T>
 struct EpResidual {
   float* X;
+  T* Xh;
   int ldx;
   const float* bias;
   __device__ inline void store4(int m, int n, f32x4 v) const {
     float4* p = reinterpret_cast<float4*>(X + (size_t)m * ldx + n);
     float4 x = *p;
-    x.x += v[0] + bias[n + 0];
-    x.y += v[1] + bias[n + 1];
-    x.z += v[2] + bias[n + 2];
-    x.w += v[3] + bias[n + 3];
+    x.x += v[0];
+    x.y += v[1];
+    x.z += v[2];
+    x.w += v[3];
     *p = x;
+    if constexpr (sizeof(T) == 2) put4(Xh + (size_t)m * ldx + n, x.x, x.y, x.z, x.w);
   }
 };
 
@@ -109,9 +135,7 @@ struct EpQKV {
     const int d = kg.H * kg.dh;
     const int which = n / d, c = n - which * d;
     if (which == 0) {
-      T* dst = Q + (size_t)m * d + c;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) dst[i] = from_f<T>(v[i] + bias[n + i]);
+      put4(Q + (size_t)m * d + c, v[0], v[1], v[2], v[3]);
       return;
     }
     const int b = m / g.R, i = m - b * g.R;
@@ -119,12 +143,10 @@ struct EpQKV {
     const int slot = st->C + i;
     T* base = kv + (size_t)b * kg.seq_stride() + kg.head_off(layer, which - 1, h);
     if (which == 1) {  // keys: [slot][dh]
-      T* dst = base + (size_t)slot * kg.dh + e;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) dst[r] = from_f<T>(v[r] + bias[n + r]);
+      put4(base + (size_t)slot * kg.dh + e, v[0], v[1], v[2], v[3]);
     } else {           // values, transposed: [dh][slot]
 #pragma unroll
-      for (int r = 0; r < 4; ++r) base[(size_t)(e + r) * kg.T + slot] = from_f<T>(v[r] + bias[n + r]);
+      for (int r = 0; r < 4; ++r) base[(size_t)(e + r) * kg.T + slot] = from_f<T>(v[r]);
     }
   }
 };
@@ -134,6 +156,7 @@ struct EpQKV {
 template <typename T>
 struct EpNoiseOut {
   float* X;
+  T* Xh;
   const float* bias;
   const T* pos;
   const KfDevState* st;
@@ -142,15 +165,19 @@ struct EpNoiseOut {
   __device__ inline void store4(int m, int n, f32x4 v) const {
     const int b = m / g.k, j = m - b * g.k;
     const int p = st->C + g.nr + j;
-    float* x = X + ((size_t)b * g.R + g.nr + j) * d + n;
+    const size_t row = (size_t)b * g.R + g.nr + j;
     const T* pe = pos + (size_t)p * d + n;
+    float x[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) x[i] = v[i] + bias[n + i] + to_f(pe[i]);
+    for (int i = 0; i < 4; ++i) x[i] = v[i] + to_f(pe[i]);
+    *reinterpret_cast<float4*>(X + row * d + n) = make_float4(x[0], x[1], x[2], x[3]);
+    if constexpr (sizeof(T) == 2) put4(Xh + row * d + n, x[0], x[1], x[2], x[3]);
   }
 };
 
 // Head: no store; per-tile argmax partials (and optional fp32 logits).
 struct EpHead {
+  const float* bias;  // always null: the tied head has no bias
   float* pval;
   int* pidx;
   float* logits;
@@ -184,68 +211,52 @@ __device__ inline int xcd_tile(int lin, int total) {
   return x * q + (x < r ? x : r) + j;
 }
 
-typedef const u32x4 __attribute__((address_space(1)))* gptr16;
-__device__ inline u32x4 gload16(const void* p) { return *(gptr16)p; }
+// ------------------------------------------------------------ memory ops
+// Operand tiles travel from global memory straight into LDS (buffer loads
+// with the lds modifier: no register staging).  The compiler cannot track
+// those LDS writes against ordinary LDS reads and would wait for every
+// outstanding load before each read, which serialises the pipeline; so the
+// kernel reads its tiles with explicit ds_read_b128 instructions and manages
+// both counters itself: vmcnt before the barrier that publishes a stage,
+// lgkmcnt before the MFMAs that consume the reads.
+typedef __attribute__((address_space(3))) void* lds_ptr;
 
-// Buffer resource over [base, base + bytes) and a 16-byte buffer load at a
-// byte offset.
+__device__ inline uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
+}
+
 __device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
                                            0x00020000);
 }
-__device__ inline u32x4 bload16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+
+// 16 bytes per lane, global byte offset voff + soff, into LDS at dst + 16 * lane
+// (dst is uniform across the wavefront).
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff,
+                                      void* dst) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr)dst, 16, voff, soff, 0, 0);
 }
 
-// ------------------------------------------------------------ A loaders
-// An A loader stages one K slab of the BM-row activation tile.  Each thread
-// owns L chunks of the slab: chunk c = tid + i*256 -> row c / 8, column chunk
-// c % 8 (a row's chunks sit in 8 consecutive lanes).  Rows past the end
-// re-read the last valid row: a tile row only feeds its own output row, which
-// is never stored, so the loads need no predicate and stay branch-free.
+__device__ __forceinline__ u32x4 ds_read16(uint32_t addr) {
+  u32x4 v;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr) : "memory");
+  return v;
+}
 
-// Plain: A is the compute-dtype matrix [M][lda].
-template <typename T, int BM>
-struct APlain {
-  static constexpr int L = BM * KCH / 256;
-  static constexpr int CH = 16 / (int)sizeof(T);
-  static constexpr bool kNorm = false;
-  static constexpr int kRegs = 4 * L;  // VGPRs per staged slab
-  struct Stage {
-    u32x4 r[L];
-  };
-  const T* A;
-  int lda;
-  int M;
-  __device__ void init(int, int) {}
-  __device__ void load(Stage& st, int m0, int k0, int tid) const {
-#ifdef KF_GEMM_BUFLOAD
-    const __amdgpu_buffer_rsrc_t rs = make_rsrc(A, (uint32_t)((size_t)M * lda * sizeof(T)));
-#endif
-#pragma unroll
-    for (int i = 0; i < L; ++i) {
-      const int c = tid + i * 256, gr = m0 + c / KCH;
-      const int rr = gr < M ? gr : M - 1;
-#ifdef KF_GEMM_BUFLOAD
-      st.r[i] = bload16(rs, (uint32_t)(((size_t)rr * lda + k0 + (c % KCH) * CH) * sizeof(T)));
-#else
-      st.r[i] = gload16(A + (size_t)rr * lda + k0 + (c % KCH) * CH);
-#endif
-    }
-  }
-  __device__ void store(const Stage& st, u32x4* __restrict__ lds, int tid) {
-#pragma unroll
-    for (int i = 0; i < L; ++i) {
-      const int c = tid + i * 256;
-      lds[swz(c / KCH, c % KCH)] = st.r[i];
-    }
-  }
-  __device__ void finish(float2*, int, int) {}
-  __device__ inline f32x4 apply(f32x4 acc, float2, int) const { return acc; }
-};
+__device__ __forceinline__ void lgkm_wait0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
-// Which residual row feeds GEMM row m (MODE 0: row m; 1: noise row m of the
-// step; 2: last real row of sequence m).
+// Keeps a value's consumers after the preceding wait.
+__device__ __forceinline__ void pin(u32x4& v) { asm volatile("" : "+v"(v)); }
+
+// s_waitcnt with vmcnt = N and the other counters left alone (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Which A row feeds GEMM row m (MODE 0: row m; 1: noise row m of the step;
+// 2: last real row of sequence m).
 template <int MODE>
 __device__ inline int map_row(int m, const KfStepGeom& g) {
   if constexpr (MODE == 1) return (m / g.k) * g.R + g.nr + (m % g.k);
@@ -253,194 +264,103 @@ __device__ inline int map_row(int m, const KfStepGeom& g) {
   else return m;
 }
 
-// LayerNorm folded into the GEMM.  For a row x (fp32 residual stream) with
-// mean mu and rstd = 1 / sqrt(var + 1e-5), gain g and shift beta:
-//   sum_k W[n][k] LN(x)_k = rstd * (sum_k W[n][k] g_k v_k - delta * c1[n]) + c2[n],
-// with v = x - x_ref (x_ref = the row's first element: keeps the MFMA operand
-// centred), delta = mu - x_ref, c1 = W g and c2 = W beta precomputed at weight
-// load.  The operand staged in LDS is g * v in the compute dtype; the loader
-// accumulates sum v and sum v^2 of its rows over the whole K loop (the
-// workgroup sees every column of its rows), so no statistics pass is needed.
-template <typename T, int BM, int MODE>
-struct ANorm {
-  static constexpr int L = BM * KCH / 256;
-  static constexpr int CH = 16 / (int)sizeof(T);  // elements per staged chunk
-  static constexpr int XW = CH / 4;               // 16-byte fp32 words per chunk
-  static constexpr bool kNorm = true;
-  static constexpr int kRegs = 4 * (L * XW + XW);
-  struct Stage {
-    u32x4 x[L][XW];
-    u32x4 g[XW];
-  };
-  const float* X;
-  int ldx;
-  int M;
-  const float* gain;
+// A operand: a compute-dtype matrix [arows][lda], rows picked by map_row.
+// With NORM, the GEMM applies the LayerNorm of each A row through the folded
+// weights: W' = W diag(g) (scaled at weight load), c1 = W' 1, c2 = W beta, so
+//   LN(x) W^T = rstd * (x W'^T - mu * c1) + c2,
+// where mu and rstd = 1 / sqrt(var + 1e-5) come from the A tile itself: the
+// workgroup stages every column of its rows, and the statistics are summed
+// from LDS as the K loop passes.
+struct GemmA {
+  const void* A;
+  int lda;
+  int arows;
   const float* c1;
   const float* c2;
   KfStepGeom g;
-  float xref[L], s1[L], s2[L];
-
-  __device__ void init(int m0, int tid) {
-#pragma unroll
-    for (int i = 0; i < L; ++i) {
-      const int gr = m0 + (tid + i * 256) / KCH;
-      const int rr = gr < M ? gr : M - 1;
-      xref[i] = X[(size_t)map_row<MODE>(rr, g) * ldx];
-      s1[i] = 0.f;
-      s2[i] = 0.f;
-    }
-  }
-  __device__ void load(Stage& st, int m0, int k0, int tid) const {
-#pragma unroll
-    for (int i = 0; i < L; ++i) {
-      const int c = tid + i * 256, gr = m0 + c / KCH;
-      const int rr = gr < M ? gr : M - 1;
-      const float* p = X + (size_t)map_row<MODE>(rr, g) * ldx + k0 + (c % KCH) * CH;
-#pragma unroll
-      for (int w = 0; w < XW; ++w) st.x[i][w] = gload16(p + 4 * w);
-    }
-    const float* gp = gain + k0 + (tid % KCH) * CH;  // same column chunk for every i
-#pragma unroll
-    for (int w = 0; w < XW; ++w) st.g[w] = gload16(gp + 4 * w);
-  }
-  __device__ void store(const Stage& st, u32x4* __restrict__ lds, int tid) {
-#pragma unroll
-    for (int i = 0; i < L; ++i) {
-      const int c = tid + i * 256;
-      u32x4 out;
-      if constexpr (sizeof(T) == 2) {
-#pragma unroll
-        for (int w = 0; w < XW; ++w)
-#pragma unroll
-          for (int e = 0; e < 4; e += 2) {
-            const float v0 = __uint_as_float(st.x[i][w][e]) - xref[i];
-            const float v1 = __uint_as_float(st.x[i][w][e + 1]) - xref[i];
-            s1[i] += v0 + v1;
-            s2[i] += v0 * v0 + v1 * v1;
-            const bf16 b0 = (bf16)(v0 * __uint_as_float(st.g[w][e]));
-            const bf16 b1 = (bf16)(v1 * __uint_as_float(st.g[w][e + 1]));
-            out[w * 2 + e / 2] = (uint32_t)__builtin_bit_cast(uint16_t, b0) |
-                                 ((uint32_t)__builtin_bit_cast(uint16_t, b1) << 16);
-          }
-      } else {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float v = __uint_as_float(st.x[i][0][e]) - xref[i];
-          s1[i] += v;
-          s2[i] += v * v;
-          out[e] = __float_as_uint(v * __uint_as_float(st.g[0][e]));
-        }
-      }
-      lds[swz(c / KCH, c % KCH)] = out;
-    }
-  }
-  // Row statistics to LDS: stat[row] = (delta, rstd).
-  __device__ void finish(float2* stat, int K, int tid) {
-#pragma unroll
-    for (int i = 0; i < L; ++i) {
-      float a = s1[i], b = s2[i];
-#pragma unroll
-      for (int off = 1; off < KCH; off <<= 1) {
-        a += __shfl_xor(a, off, 64);
-        b += __shfl_xor(b, off, 64);
-      }
-      if ((tid % KCH) == 0) {
-        const float delta = a / (float)K;
-        const float var = fmaxf(b / (float)K - delta * delta, 0.f);
-        stat[(tid + i * 256) / KCH] = make_float2(delta, 1.0f / sqrtf(var + 1e-5f));
-      }
-    }
-  }
-  __device__ inline f32x4 apply(f32x4 acc, float2 st, int n) const {
-    f32x4 r;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) r[i] = st.y * (acc[i] - st.x * c1[n + i]) + c2[n + i];
-    return r;
-  }
 };
 
-// One K slab of this wavefront's TN x TM block of 16x16 tiles.
-template <typename T, int TM, int TN>
-__device__ __forceinline__ void mma_slab(f32x4 (&acc)[TN][TM], const u32x4* __restrict__ la,
-                                         const u32x4* __restrict__ lw, int arow, int wrow,
-                                         int lane) {
-#pragma unroll
-  for (int s = 0; s < KCH / 4; ++s) {
-    u32x4 af[TN], bfr[TM];
-    const int ch = s * 4 + (lane >> 4);
-#pragma unroll
-    for (int tn = 0; tn < TN; ++tn) af[tn] = lw[swz(wrow + tn * 16, ch)];
-#pragma unroll
-    for (int tm = 0; tm < TM; ++tm) bfr[tm] = la[swz(arow + tm * 16, ch)];
-#pragma unroll
-    for (int tn = 0; tn < TN; ++tn)
-#pragma unroll
-      for (int tm = 0; tm < TM; ++tm) Mfma<T>::mma(af[tn], bfr[tm], acc[tn][tm]);
-  }
-}
-
-template <int L, typename T>
-__device__ __forceinline__ void gload_w(u32x4 (&r)[L], const T* __restrict__ base, int ld, int row0,
-                                        int nrows, int k0, int tid) {
-  constexpr int CH = 16 / (int)sizeof(T);
-#ifdef KF_GEMM_BUFLOAD
-  const __amdgpu_buffer_rsrc_t rs = make_rsrc(base, (uint32_t)((size_t)nrows * ld * sizeof(T)));
-#endif
-#pragma unroll
-  for (int i = 0; i < L; ++i) {
-    const int c = tid + i * 256, gr = row0 + c / KCH;
-    const int rr = gr < nrows ? gr : nrows - 1;
-#ifdef KF_GEMM_BUFLOAD
-    r[i] = bload16(rs, (uint32_t)(((size_t)rr * ld + k0 + (c % KCH) * CH) * sizeof(T)));
-#else
-    r[i] = gload16(base + (size_t)rr * ld + k0 + (c % KCH) * CH);
-#endif
-  }
-}
-
-template <int L>
-__device__ __forceinline__ void sstore_w(const u32x4 (&r)[L], u32x4* __restrict__ lds, int tid) {
-#pragma unroll
-  for (int i = 0; i < L; ++i) {
-    const int c = tid + i * 256;
-    lds[swz(c / KCH, c % KCH)] = r[i];
-  }
-}
-
 // ---------------------------------------------------------------- kernel
-// Ring of S register stages over the K slabs (S divides the slab count): the
-// prologue issues slabs 0..S-1; slab kt is stored to LDS buffer kt & 1 (last
-// read by slab kt - 2, which every wavefront finished before the barrier of
-// slab kt - 1), then its registers are refilled with slab kt + S, so S slabs
-// are always in flight.  The last trip is peeled and issues no loads.
-// Scheduling barriers keep each slab's loads in issue order, so the wait
-// before a slab's LDS store covers only that slab.
-template <typename T, int BM, int BN, int WM, int WN, int S, class AL, class Ep>
+// S-stage LDS ring.  At K step kt the kernel waits for its own loads of
+// stage kt, meets the other wavefronts at a barrier (after which every load of
+// stage kt has landed and every read of stage kt - 1 is done), issues the loads
+// of step kt + S - 1 into the buffer that stage kt - 1 used, and multiplies
+// stage kt.  Each wavefront loads 8 rows (one 128-byte slab each) per
+// instruction: BM / 32 A instructions and BN / 32 W instructions per stage.
+template <typename T, int BM, int BN, int WM, int WN, int S, int MODE, bool NORM, class Ep>
 __global__ void __launch_bounds__(256)
-    gemm_kernel(AL al, const T* __restrict__ W, int ldw, int M, int N, int K, Ep ep) {
+    gemm_kernel(GemmA ga, const T* __restrict__ W, int ldw, int M, int N, int K, Ep ep) {
   constexpr int CH = 16 / (int)sizeof(T);  // elements per 16-byte chunk
   constexpr int BK = KCH * CH;             // K per slab
   constexpr int MW = BM / WM, NW = BN / WN;
   constexpr int TM = MW / 16, TN = NW / 16;
-  constexpr int LW = BN * KCH / 256;
+  constexpr int PA = BM / 32, PW = BN / 32, PER = PA + PW;
+  constexpr int LS = NORM ? BM * KCH / 256 : 1;  // statistics chunks per thread
+  constexpr int ROWB = KCH * 16;                 // bytes per staged row
   static_assert(WM * WN == 4, "four wavefronts");
   static_assert(MW % 16 == 0 && NW % 16 == 0, "16x16 MFMA tiles");
-  static_assert((BM * KCH) % 256 == 0 && (BN * KCH) % 256 == 0, "whole chunks per thread");
-  static_assert(S % 2 == 0, "even ring depth (LDS buffer parity)");
+  static_assert(BM % 32 == 0 && BN % 32 == 0, "whole DMA instructions per wavefront");
+  static_assert(S >= 2 && S <= 4, "ring depth");
 
-  __shared__ u32x4 sA[2][BM * KCH];
-  __shared__ u32x4 sW[2][BN * KCH];
-  __shared__ float2 sStat[AL::kNorm ? BM : 1];
+  __shared__ u32x4 sbuf[S][(BM + BN) * KCH];
+  __shared__ float2 sStat[NORM ? BM : 1];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   const int gm = (M + BM - 1) / BM, gn = (N + BN - 1) / BN;
   const int tile = xcd_tile(blockIdx.x, gm * gn);
   const int m0 = (tile % gm) * BM, n0 = (tile / gm) * BN;
+  const int nk = K / BK;
 
-  AL a = al;
-  a.init(m0, tid);
+  const T* A = static_cast<const T*>(ga.A);
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(A, (uint32_t)((size_t)ga.arows * ga.lda * sizeof(T)));
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(W, (uint32_t)((size_t)N * ldw * sizeof(T)));
+
+  // DMA sources at k = 0.  Lane l of a load covers row r0 + l / 8 and LDS
+  // slot l % 8, which holds chunk (l % 8) ^ ((r >> 1) & 7) of the row: the
+  // swizzled layout of swz().  Rows past the end re-read the last row: such a
+  // row only feeds its own output row, which is never stored.
+  uint32_t aoff[PA], woff[PW];
+#pragma unroll
+  for (int j = 0; j < PA; ++j) {
+    const int r = wave * 8 + 32 * j + lane / 8, c = (lane & 7) ^ ((r >> 1) & 7);
+    const int gr = m0 + r < M ? m0 + r : M - 1;
+    aoff[j] = (uint32_t)(((size_t)map_row<MODE>(gr, ga.g) * ga.lda + c * CH) * sizeof(T));
+  }
+#pragma unroll
+  for (int j = 0; j < PW; ++j) {
+    const int r = wave * 8 + 32 * j + lane / 8, c = (lane & 7) ^ ((r >> 1) & 7);
+    const int gr = n0 + r < N ? n0 + r : N - 1;
+    woff[j] = (uint32_t)(((size_t)gr * ldw + c * CH) * sizeof(T));
+  }
+  auto issue = [&](int stage, int kt) {
+    const uint32_t so = (uint32_t)(kt * BK * (int)sizeof(T));
+#pragma unroll
+    for (int j = 0; j < PA; ++j) dma16(ra, aoff[j], so, &sbuf[stage][(wave * 8 + 32 * j) * KCH]);
+#pragma unroll
+    for (int j = 0; j < PW; ++j)
+      dma16(rw, woff[j], so, &sbuf[stage][(BM + wave * 8 + 32 * j) * KCH]);
+  };
+
+  // LDS read offsets within a stage.  Every row a lane reads is congruent to
+  // lane % 16 modulo 16, so one swizzle key serves all of them.
+  const int key = (lane & 15) >> 1;
+  uint32_t rdA[2], rdW[2];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int ch = (s * 4 + (lane >> 4)) ^ key;
+    rdA[s] = (uint32_t)(((wm * MW + (lane & 15)) * KCH + ch) * 16);
+    rdW[s] = (uint32_t)(((BM + wn * NW + (lane & 15)) * KCH + ch) * 16);
+  }
+  uint32_t rdS[LS];
+  float s1[LS], s2[LS];
+#pragma unroll
+  for (int q = 0; q < LS; ++q) {
+    const int c = tid + q * 256;
+    rdS[q] = (uint32_t)(swz(c / KCH, c % KCH) * 16);
+    s1[q] = 0.f;
+    s2[q] = 0.f;
+  }
 
   f32x4 acc[TN][TM];
 #pragma unroll
@@ -448,41 +368,117 @@ __global__ void __launch_bounds__(256)
 #pragma unroll
     for (int y = 0; y < TM; ++y) acc[x][y] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int arow = wm * MW + (lane & 15), wrow = wn * NW + (lane & 15);
-  const int trips = K / (BK * S);
-
-  typename AL::Stage sa[S];
-  u32x4 rw[S][LW];
+  // Column constants of this lane's output columns (bias; folded-LayerNorm
+  // sums), loaded now so that the epilogue does not wait on memory.
+  f32x4 pb[TN], p1[TN], p2[TN];
 #pragma unroll
-  for (int i = 0; i < S; ++i) {
-    a.load(sa[i], m0, i * BK, tid);
-    gload_w<LW>(rw[i], W, ldw, n0, N, i * BK, tid);
-    __builtin_amdgcn_sched_barrier(0);
+  for (int tn = 0; tn < TN; ++tn) {
+    const int n = n0 + wn * NW + tn * 16 + 4 * (lane >> 4);
+    const int nc = n < N ? n : 0;
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+    pb[tn] = ep.bias ? *reinterpret_cast<const f32x4*>(ep.bias + nc) : z;
+    p1[tn] = NORM ? *reinterpret_cast<const f32x4*>(ga.c1 + nc) : z;
+    p2[tn] = NORM ? *reinterpret_cast<const f32x4*>(ga.c2 + nc) : z;
   }
-  for (int t = 0; t + 1 < trips; ++t) {
+
+  auto compute = [&](int stage) {
+    const uint32_t sb = lds_addr(&sbuf[stage][0]);
+    u32x4 af[2][TN], bv[2][TM], xs[LS];
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) af[s][tn] = ds_read16(sb + rdW[s] + tn * 16 * ROWB);
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm) bv[s][tm] = ds_read16(sb + rdA[s] + tm * 16 * ROWB);
+    }
+    if constexpr (NORM) {
+#pragma unroll
+      for (int q = 0; q < LS; ++q) xs[q] = ds_read16(sb + rdS[q]);
+    }
+    lgkm_wait0();
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) pin(af[s][tn]);
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm) pin(bv[s][tm]);
+    }
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm) Mfma<T>::mma(af[s][tn], bv[s][tm], acc[tn][tm]);
+    if constexpr (NORM) {
+#pragma unroll
+      for (int q = 0; q < LS; ++q) {
+        pin(xs[q]);
+        // The words are named one by one: bit-casting xs[q][w] with an
+        // unrolled index w has been compiled to read word 0 every time.
+        const uint32_t xw[4] = {xs[q].x, xs[q].y, xs[q].z, xs[q].w};
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          if constexpr (sizeof(T) == 2) {  // v_dot2: two products and the sum per instruction
+            const bf16x2 x2 = __builtin_bit_cast(bf16x2, xw[w]);
+            s1[q] = __builtin_amdgcn_fdot2_f32_bf16(x2, bf16x2{(bf16)1.0f, (bf16)1.0f}, s1[q], false);
+            s2[q] = __builtin_amdgcn_fdot2_f32_bf16(x2, x2, s2[q], false);
+          } else {
+            const float v = __uint_as_float(xw[w]);
+            s1[q] += v;
+            s2[q] += v * v;
+          }
+        }
+      }
+    }
+  };
+
+#pragma unroll
+  for (int i = 0; i < S - 1; ++i)
+    if (i < nk) issue(i, i);
+  for (int kt0 = 0; kt0 < nk; kt0 += S) {
 #pragma unroll
     for (int i = 0; i < S; ++i) {
-      const int kn = (t * S + i + S) * BK;
-      a.store(sa[i], sA[i & 1], tid);
-      sstore_w<LW>(rw[i], sW[i & 1], tid);
-      __syncthreads();
-      a.load(sa[i], m0, kn, tid);
-      gload_w<LW>(rw[i], W, ldw, n0, N, kn, tid);
-      __builtin_amdgcn_sched_barrier(0);
-      mma_slab<T, TM, TN>(acc, sA[i & 1], sW[i & 1], arow, wrow, lane);
+      const int kt = kt0 + i;
+      if (kt < nk) {
+        if (kt + S - 2 < nk) vm_wait<(S - 2) * PER>();
+        else vm_wait<0>();
+        __builtin_amdgcn_s_barrier();
+        if (kt + S - 1 < nk) issue((i + S - 1) % S, kt + S - 1);
+        compute(i);
+      }
     }
   }
+
+  if constexpr (NORM) {
 #pragma unroll
-  for (int i = 0; i < S; ++i) {
-    a.store(sa[i], sA[i & 1], tid);
-    sstore_w<LW>(rw[i], sW[i & 1], tid);
+    for (int q = 0; q < LS; ++q) {
+      float a = s1[q], b = s2[q];
+#pragma unroll
+      for (int off = 1; off < KCH; off <<= 1) {
+        a += __shfl_xor(a, off, 64);
+        b += __shfl_xor(b, off, 64);
+      }
+      if ((tid % KCH) == 0) {
+        const float mu = a / (float)K;
+        const float var = fmaxf(b / (float)K - mu * mu, 0.f);
+        sStat[(tid + q * 256) / KCH] = make_float2(mu, 1.0f / sqrtf(var + 1e-5f));
+      }
+    }
     __syncthreads();
-    mma_slab<T, TM, TN>(acc, sA[i & 1], sW[i & 1], arow, wrow, lane);
   }
-  if constexpr (AL::kNorm) {
-    a.finish(sStat, K, tid);
-    __syncthreads();
-  }
+  // Folded LayerNorm (if any) and bias for 16x16 tile (tn, row ml).
+  auto apply = [&](f32x4 v, int ml, int tn) -> f32x4 {
+    f32x4 r;
+    if constexpr (NORM) {
+      const float2 st = sStat[ml];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) r[i] = st.y * (v[i] - st.x * p1[tn][i]) + p2[tn][i] + pb[tn][i];
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) r[i] = v[i] + pb[tn][i];
+    }
+    return r;
+  };
 
   if constexpr (!IsHead<Ep>::value) {
 #pragma unroll
@@ -491,7 +487,7 @@ __global__ void __launch_bounds__(256)
       for (int tm = 0; tm < TM; ++tm) {
         const int n = n0 + wn * NW + tn * 16 + 4 * (lane >> 4);
         const int ml = wm * MW + tm * 16 + (lane & 15), m = m0 + ml;
-        if (m < M && n < N) ep.store4(m, n, a.apply(acc[tn][tm], sStat[AL::kNorm ? ml : 0], n));
+        if (m < M && n < N) ep.store4(m, n, apply(acc[tn][tm], ml, tn));
       }
   } else {
     // Row-wise argmax over this tile's columns: lane-local, then across the
@@ -502,13 +498,12 @@ __global__ void __launch_bounds__(256)
     for (int tm = 0; tm < TM; ++tm) {
       const int mloc = wm * MW + tm * 16 + (lane & 15);
       const int m = m0 + mloc;
-      const float2 st = sStat[AL::kNorm ? mloc : 0];
       float bv = -INFINITY;
       int bi = 0x7fffffff;
 #pragma unroll
       for (int tn = 0; tn < TN; ++tn) {
         const int n = n0 + wn * NW + tn * 16 + 4 * (lane >> 4);
-        const f32x4 v = a.apply(acc[tn][tm], st, n);
+        const f32x4 v = apply(acc[tn][tm], mloc, tn);
 #pragma unroll
         for (int i = 0; i < 4; ++i)
           if (n + i < ep.V && v[i] > bv) { bv = v[i]; bi = n + i; }
@@ -549,106 +544,51 @@ __global__ void __launch_bounds__(256)
   }
 }
 
-// Ring depth: the deepest of {12, 6, 2} that divides the slab count and keeps
-// the staged slabs within 192 registers per thread (deeper rings are not even
-// instantiated for tiles whose stages would not fit).
-template <typename T, int BM, int BN, int WM, int WN, class AL, class Ep>
-hipError_t launch_gemm(const AL& al, const T* W, int ldw, int M, int N, int K, const Ep& ep,
+template <typename T, int BM, int BN, int WM, int WN, int S, int MODE, bool NORM, class Ep>
+hipError_t launch_tile(const GemmA& ga, const T* W, int ldw, int M, int N, int K, const Ep& ep,
                        hipStream_t s) {
-  constexpr int BK = KCH * 16 / (int)sizeof(T);
-  constexpr int LW = BN * KCH / 256;
-  constexpr int per = AL::kRegs + 4 * LW;
   const int tiles = ((N + BN - 1) / BN) * ((M + BM - 1) / BM);
-  const int nk = K / BK;
-  if constexpr (12 * per <= 192) {
-    if (nk % 12 == 0) {
-      hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN, 12, AL, Ep>), dim3(tiles), dim3(256), 0,
-                         s, al, W, ldw, M, N, K, ep);
-      return hipGetLastError();
-    }
-  }
-  if constexpr (6 * per <= 192) {
-    if (nk % 6 == 0) {
-      hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN, 6, AL, Ep>), dim3(tiles), dim3(256), 0, s,
-                         al, W, ldw, M, N, K, ep);
-      return hipGetLastError();
-    }
-  }
-  hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN, 2, AL, Ep>), dim3(tiles), dim3(256), 0, s, al,
-                     W, ldw, M, N, K, ep);
+  hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN, S, MODE, NORM, Ep>), dim3(tiles), dim3(256),
+                     0, s, ga, W, ldw, M, N, K, ep);
   return hipGetLastError();
 }
 
-// Loader arguments independent of the tile shape; launch() instantiates the
-// loader for the chosen tile.
-template <typename T>
-struct PlainArgs {
-  const T* A;
-  int lda, M;
-  template <int BM, int BN, int WM, int WN, class Ep>
-  hipError_t launch(const T* W, int ldw, int Mr, int N, int K, const Ep& ep, hipStream_t s) const {
-    APlain<T, BM> al;
-    al.A = A;
-    al.lda = lda;
-    al.M = M;
-    return launch_gemm<T, BM, BN, WM, WN>(al, W, ldw, Mr, N, K, ep, s);
-  }
-};
-
-template <typename T, int MODE>
-struct NormArgs {
-  const float* X;
-  int ldx, M;
-  const float* gain;
-  const float* c1;
-  const float* c2;
-  KfStepGeom g;
-  template <int BM, int BN, int WM, int WN, class Ep>
-  hipError_t launch(const T* W, int ldw, int Mr, int N, int K, const Ep& ep, hipStream_t s) const {
-    ANorm<T, BM, MODE> al;
-    al.X = X;
-    al.ldx = ldx;
-    al.M = M;
-    al.gain = gain;
-    al.c1 = c1;
-    al.c2 = c2;
-    al.g = g;
-    return launch_gemm<T, BM, BN, WM, WN>(al, W, ldw, Mr, N, K, ep, s);
-  }
-};
-
 inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
-// Tile choice: the largest tile that still gives at least one workgroup per
-// CU (256), else the smallest tile.
-template <typename T, class ALP, class Ep>
-hipError_t dispatch(const ALP& alp, const T* W, int ldw, int M, int N, int K, const Ep& ep,
+// Tile choice: the largest tile that still gives about one workgroup per CU.
+template <typename T, int MODE, bool NORM, class Ep>
+hipError_t dispatch(const GemmA& ga, const T* W, int M, int N, int K, const Ep& ep,
                     hipStream_t s) {
   if (M <= 0 || N <= 0) return hipSuccess;
   constexpr int kFill = 256;
   if (cdiv(M, 128) * cdiv(N, 128) >= kFill)
-    return alp.template launch<128, 128, 2, 2>(W, ldw, M, N, K, ep, s);
+    return launch_tile<T, 128, 128, 2, 2, 2, MODE, NORM>(ga, W, K, M, N, K, ep, s);
   if (cdiv(M, 64) * cdiv(N, 128) >= kFill)
-    return alp.template launch<64, 128, 2, 2>(W, ldw, M, N, K, ep, s);
-  if (cdiv(M, 64) * cdiv(N, 64) >= kFill)
-    return alp.template launch<64, 64, 2, 2>(W, ldw, M, N, K, ep, s);
-  if (cdiv(M, 32) * cdiv(N, 64) >= kFill)
-    return alp.template launch<32, 64, 2, 2>(W, ldw, M, N, K, ep, s);
-  return alp.template launch<32, 32, 2, 2>(W, ldw, M, N, K, ep, s);
+    return launch_tile<T, 64, 128, 2, 2, 3, MODE, NORM>(ga, W, K, M, N, K, ep, s);
+  if (cdiv(M, 64) * cdiv(N, 64) >= kFill * 3 / 4)
+    return launch_tile<T, 64, 64, 2, 2, 3, MODE, NORM>(ga, W, K, M, N, K, ep, s);
+  if (cdiv(M, 32) * cdiv(N, 64) >= kFill * 3 / 4)
+    return launch_tile<T, 32, 64, 2, 2, 4, MODE, NORM>(ga, W, K, M, N, K, ep, s);
+  return launch_tile<T, 32, 32, 2, 2, 4, MODE, NORM>(ga, W, K, M, N, K, ep, s);
 }
 
-// c1[n] = sum_k W[n][k] g[k], c2[n] = sum_k W[n][k] beta[k]: one wavefront per
-// output column, fixed summation order.
+// LayerNorm folding at weight load, one wavefront per output row n:
+//   Wout[n][k] = W[n][k] g[k] (rounded to T), c1[n] = sum_k Wout[n][k],
+//   c2[n] = sum_k W[n][k] beta[k].
+// c1 sums the rounded weights, so the mean term cancels exactly against the
+// MFMA products.  Wout may be W itself.
 template <typename T>
 __global__ void __launch_bounds__(256)
-    ln_fold_kernel(const T* __restrict__ W, const float* __restrict__ g,
+    ln_fold_kernel(const T* W, T* Wout, const float* __restrict__ g,
                    const float* __restrict__ beta, int N, int K, float* c1, float* c2) {
   const int n = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (n >= N) return;
   float a = 0.f, b = 0.f;
   for (int k = lane; k < K; k += 64) {
     const float w = to_f(W[(size_t)n * K + k]);
-    a += w * g[k];
+    const T ws = from_f<T>(w * g[k]);
+    Wout[(size_t)n * K + k] = ws;
+    a += to_f(ws);
     b += w * beta[k];
   }
 #pragma unroll
@@ -668,62 +608,64 @@ template <typename T>
 hipError_t gemm_bias(const T* A, const T* W, int M, int N, int K, const float* bias, Act act,
                      T* out, int ldo, hipStream_t s) {
   EpBias<T> ep{out, ldo, bias, act == Act::Gelu ? 1 : 0};
-  return dispatch<T>(PlainArgs<T>{A, K, M}, W, K, M, N, K, ep, s);
+  return dispatch<T, 0, false>(GemmA{A, K, M, nullptr, nullptr, KfStepGeom{}}, W, M, N, K, ep, s);
 }
 
 template <typename T>
 hipError_t gemm_residual(const T* A, const T* W, int M, int N, int K, const float* bias, float* X,
-                         hipStream_t s) {
-  EpResidual ep{X, N, bias};
-  return dispatch<T>(PlainArgs<T>{A, K, M}, W, K, M, N, K, ep, s);
+                         T* Xh, hipStream_t s) {
+  EpResidual<T> ep{X, Xh, N, bias};
+  return dispatch<T, 0, false>(GemmA{A, K, M, nullptr, nullptr, KfStepGeom{}}, W, M, N, K, ep, s);
 }
 
 template <typename T>
 hipError_t gemm_noise_out(const T* A, const T* W, int M, int d, int K, const float* bias,
-                          const T* pos, float* X, KfStepGeom g, const KfDevState* st,
+                          const T* pos, float* X, T* Xh, KfStepGeom g, const KfDevState* st,
                           hipStream_t s) {
-  EpNoiseOut<T> ep{X, bias, pos, st, g, d};
-  return dispatch<T>(PlainArgs<T>{A, K, M}, W, K, M, d, K, ep, s);
+  EpNoiseOut<T> ep{X, Xh, bias, pos, st, g, d};
+  return dispatch<T, 0, false>(GemmA{A, K, M, nullptr, nullptr, KfStepGeom{}}, W, M, d, K, ep, s);
 }
 
 template <typename T>
-hipError_t gemm_qkv_ln(const float* X, const LnFold& ln, const T* W, int M, int d,
-                       const float* bias, T* Q, T* kv, KfStepGeom g, KfKvGeom kg, int layer,
-                       const KfDevState* st, hipStream_t s) {
+hipError_t gemm_qkv_ln(const T* Xh, const LnFold& ln, const T* W, int M, int d, const float* bias,
+                       T* Q, T* kv, KfStepGeom g, KfKvGeom kg, int layer, const KfDevState* st,
+                       hipStream_t s) {
   EpQKV<T> ep{Q, kv, bias, st, g, kg, layer};
-  NormArgs<T, 0> na{X, d, M, ln.gain, ln.c1, ln.c2, g};
-  return dispatch<T>(na, W, d, M, 3 * d, d, ep, s);
+  return dispatch<T, 0, true>(GemmA{Xh, d, M, ln.c1, ln.c2, g}, W, M, 3 * d, d, ep, s);
 }
 
 template <typename T>
-hipError_t gemm_up_ln(const float* X, const LnFold& ln, const T* W, int M, int N, int d,
+hipError_t gemm_up_ln(const T* Xh, const LnFold& ln, const T* W, int M, int N, int d,
                       const float* bias, T* out, hipStream_t s) {
   EpBias<T> ep{out, N, bias, 1};
-  NormArgs<T, 0> na{X, d, M, ln.gain, ln.c1, ln.c2, KfStepGeom{}};
-  return dispatch<T>(na, W, d, M, N, d, ep, s);
+  return dispatch<T, 0, true>(GemmA{Xh, d, M, ln.c1, ln.c2, KfStepGeom{}}, W, M, N, d, ep, s);
 }
 
 template <typename T>
-hipError_t gemm_head_ln(const float* X, const LnFold& ln, const T* W, int M, int Vpad, int V,
-                        int d, int gather, KfStepGeom g, float* pval, int* pidx, float* logits,
+hipError_t gemm_head_ln(const T* Xh, const LnFold& ln, const T* W, int M, int Vpad, int V, int d,
+                        int gather, KfStepGeom g, float* pval, int* pidx, float* logits,
                         hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  EpHead ep{pval, pidx, logits, V, Vpad / kHeadTileN};
-  auto go = [&](auto na) {
-    if (M <= 32) return na.template launch<32, kHeadTileN, 1, 4>(W, d, M, Vpad, d, ep, s);
-    if (M <= 512) return na.template launch<64, kHeadTileN, 2, 2>(W, d, M, Vpad, d, ep, s);
-    return na.template launch<128, kHeadTileN, 2, 2>(W, d, M, Vpad, d, ep, s);
+  EpHead ep{nullptr, pval, pidx, logits, V, Vpad / kHeadTileN};
+  const GemmA ga{Xh, d, g.B * g.R, ln.c1, ln.c2, g};
+  auto go = [&](auto mode) {
+    constexpr int MODE = decltype(mode)::value;
+    if (M <= 32)
+      return launch_tile<T, 32, kHeadTileN, 1, 4, 3, MODE, true>(ga, W, d, M, Vpad, d, ep, s);
+    if (M <= 512)
+      return launch_tile<T, 64, kHeadTileN, 2, 2, 3, MODE, true>(ga, W, d, M, Vpad, d, ep, s);
+    return launch_tile<T, 128, kHeadTileN, 2, 2, 2, MODE, true>(ga, W, d, M, Vpad, d, ep, s);
   };
-  if (gather == 2) return go(NormArgs<T, 2>{X, d, M, ln.gain, ln.c1, ln.c2, g});
-  return go(NormArgs<T, 1>{X, d, M, ln.gain, ln.c1, ln.c2, g});
+  if (gather == 2) return go(std::integral_constant<int, 2>{});
+  return go(std::integral_constant<int, 1>{});
 }
 
 template <typename T>
-hipError_t launch_ln_fold(const T* W, const float* g, const float* beta, int N, int K, float* c1,
-                          float* c2, hipStream_t s) {
+hipError_t launch_ln_fold(const T* W, T* Wout, const float* g, const float* beta, int N, int K,
+                          float* c1, float* c2, hipStream_t s) {
   if (N <= 0) return hipSuccess;
-  hipLaunchKernelGGL(ln_fold_kernel<T>, dim3((N + 3) / 4), dim3(256), 0, s, W, g, beta, N, K, c1,
-                     c2);
+  hipLaunchKernelGGL(ln_fold_kernel<T>, dim3((N + 3) / 4), dim3(256), 0, s, W, Wout, g, beta, N, K,
+                     c1, c2);
   return hipGetLastError();
 }
 
@@ -731,19 +673,19 @@ hipError_t launch_ln_fold(const T* W, const float* g, const float* beta, int N, 
   template hipError_t gemm_bias<T>(const T*, const T*, int, int, int, const float*, Act, T*, int, \
                                    hipStream_t);                                                   \
   template hipError_t gemm_residual<T>(const T*, const T*, int, int, int, const float*, float*,   \
-                                       hipStream_t);                                               \
+                                       T*, hipStream_t);                                           \
   template hipError_t gemm_noise_out<T>(const T*, const T*, int, int, int, const float*,          \
-                                        const T*, float*, KfStepGeom, const KfDevState*,           \
+                                        const T*, float*, T*, KfStepGeom, const KfDevState*,       \
                                         hipStream_t);                                              \
-  template hipError_t gemm_qkv_ln<T>(const float*, const LnFold&, const T*, int, int,             \
-                                     const float*, T*, T*, KfStepGeom, KfKvGeom, int,              \
-                                     const KfDevState*, hipStream_t);                              \
-  template hipError_t gemm_up_ln<T>(const float*, const LnFold&, const T*, int, int, int,         \
+  template hipError_t gemm_qkv_ln<T>(const T*, const LnFold&, const T*, int, int, const float*,   \
+                                     T*, T*, KfStepGeom, KfKvGeom, int, const KfDevState*,         \
+                                     hipStream_t);                                                 \
+  template hipError_t gemm_up_ln<T>(const T*, const LnFold&, const T*, int, int, int,             \
                                     const float*, T*, hipStream_t);                                \
-  template hipError_t gemm_head_ln<T>(const float*, const LnFold&, const T*, int, int, int, int,  \
-                                      int, KfStepGeom, float*, int*, float*, hipStream_t);         \
-  template hipError_t launch_ln_fold<T>(const T*, const float*, const float*, int, int, float*,   \
-                                        float*, hipStream_t);
+  template hipError_t gemm_head_ln<T>(const T*, const LnFold&, const T*, int, int, int, int, int, \
+                                      KfStepGeom, float*, int*, float*, hipStream_t);              \
+  template hipError_t launch_ln_fold<T>(const T*, T*, const float*, const float*, int, int,       \
+                                        float*, float*, hipStream_t);
 KF_INST(float)
 KF_INST(bf16)
 #undef KF_INST

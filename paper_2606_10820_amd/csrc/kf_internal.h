@@ -76,7 +76,7 @@ enum class Act { None = 0, Gelu = 1 };
 
 // Real-row embedding: X[b*R + i] = tok[toks[b*tok_stride + i]] + pos[C + i], i < nr.
 template <typename T>
-hipError_t launch_embed_real(float* X, const T* tok, const T* pos, const int32_t* toks,
+hipError_t launch_embed_real(float* X, T* Xh, const T* tok, const T* pos, const int32_t* toks,
                              int tok_stride, KfStepGeom g, int d, int V, KfDevState* st,
                              hipStream_t s);
 
@@ -97,40 +97,44 @@ hipError_t launch_attention(const T* Q, const T* kv, T* O, const KfDevState* st,
 template <typename T>
 hipError_t gemm_bias(const T* A, const T* W, int M, int N, int K, const float* bias, Act act,
                      T* out, int ldo, hipStream_t s);
+// Residual update X[M][N] += C + bias; with a 16-bit T the updated rows are
+// also written to Xh (the compute-dtype copy of the residual stream; for fp32,
+// Xh aliases X and is not written).
 template <typename T>
 hipError_t gemm_residual(const T* A, const T* W, int M, int N, int K, const float* bias, float* X,
-                         hipStream_t s);
-// LayerNorm folded into a GEMM (gain, shift and the precomputed per-column
-// sums c1 = W.gain, c2 = W.shift).  A rows are read from the fp32 residual
-// stream X [rows][d].
+                         T* Xh, hipStream_t s);
+// LayerNorm folded into a GEMM whose weights were scaled by the gain at load
+// (W' = W diag(gain)): c1 = W' 1 and c2 = W shift.  A rows come from the
+// compute-dtype residual copy Xh [rows][d]; each row's mean and variance are
+// taken from the rows as staged by the GEMM.
 struct LnFold {
-  const float* gain;
   const float* c1;
   const float* c2;
 };
 template <typename T>
-hipError_t gemm_qkv_ln(const float* X, const LnFold& ln, const T* W, int M, int d,
-                       const float* bias, T* Q, T* kv, KfStepGeom g, KfKvGeom kg, int layer,
-                       const KfDevState* st, hipStream_t s);
+hipError_t gemm_qkv_ln(const T* Xh, const LnFold& ln, const T* W, int M, int d, const float* bias,
+                       T* Q, T* kv, KfStepGeom g, KfKvGeom kg, int layer, const KfDevState* st,
+                       hipStream_t s);
 template <typename T>
-hipError_t gemm_up_ln(const float* X, const LnFold& ln, const T* W, int M, int N, int d,
+hipError_t gemm_up_ln(const T* Xh, const LnFold& ln, const T* W, int M, int N, int d,
                       const float* bias, T* out, hipStream_t s);
 template <typename T>
 hipError_t gemm_noise_out(const T* A, const T* W, int M, int d, int K, const float* bias,
-                          const T* pos, float* X, KfStepGeom g, const KfDevState* st,
+                          const T* pos, float* X, T* Xh, KfStepGeom g, const KfDevState* st,
                           hipStream_t s);
 // Head over the final LayerNorm of the selected rows (gather: 1 = noise rows
 // of the step, 2 = last real row per sequence): per (row, 128-column tile) the
 // maximum and its lowest column index into pval/pidx [M][Vpad/128]; columns
 // >= V are excluded.  When logits is not null the fp32 logits [M][V] are
-// written as well.
+// written as well.  W is the gain-scaled token table [Vpad][d].
 template <typename T>
-hipError_t gemm_head_ln(const float* X, const LnFold& ln, const T* W, int M, int Vpad, int V,
-                        int d, int gather, KfStepGeom g, float* pval, int* pidx, float* logits,
+hipError_t gemm_head_ln(const T* Xh, const LnFold& ln, const T* W, int M, int Vpad, int V, int d,
+                        int gather, KfStepGeom g, float* pval, int* pidx, float* logits,
                         hipStream_t s);
-// c1 = W gain and c2 = W shift for a folded LayerNorm, W [N][K].
+// Fold a LayerNorm into the GEMM that consumes it: Wout = W diag(gain) in T,
+// c1 = Wout 1, c2 = W shift; W [N][K], Wout may alias W.
 template <typename T>
-hipError_t launch_ln_fold(const T* W, const float* gain, const float* shift, int N, int K,
+hipError_t launch_ln_fold(const T* W, T* Wout, const float* gain, const float* shift, int N, int K,
                           float* c1, float* c2, hipStream_t s);
 constexpr int kHeadTileN = 128;
 

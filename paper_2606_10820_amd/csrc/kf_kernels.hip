@@ -29,7 +29,8 @@ __device__ inline float wave_sum(float v) {
 // Real rows (Appendix C.1, Embed): token table row plus learned position.
 template <typename T>
 __global__ void __launch_bounds__(256)
-    embed_real_kernel(float* __restrict__ X, const T* __restrict__ tok, const T* __restrict__ pos,
+    embed_real_kernel(float* __restrict__ X, T* __restrict__ Xh, const T* __restrict__ tok,
+                      const T* __restrict__ pos,
                       const int32_t* __restrict__ toks, int tok_stride, KfStepGeom g, int d, int V,
                       KfDevState* st) {
   const int r = blockIdx.x;
@@ -43,7 +44,12 @@ __global__ void __launch_bounds__(256)
   float* x = X + ((size_t)b * g.R + i) * d;
   const T* te = tok + (size_t)t * d;
   const T* pe = pos + (size_t)(C + i) * d;
-  for (int e = threadIdx.x; e < d; e += blockDim.x) x[e] = to_f(te[e]) + to_f(pe[e]);
+  T* xh = Xh + ((size_t)b * g.R + i) * d;
+  for (int e = threadIdx.x; e < d; e += blockDim.x) {
+    const float v = to_f(te[e]) + to_f(pe[e]);
+    x[e] = v;
+    if constexpr (sizeof(T) == 2) xh[e] = from_f<T>(v);
+  }
 }
 
 // ------------------------------------------------------- noise sinusoid
@@ -445,11 +451,11 @@ inline unsigned grid_for(size_t n, unsigned block) {
 
 // ------------------------------------------------------------ launchers
 template <typename T>
-hipError_t launch_embed_real(float* X, const T* tok, const T* pos, const int32_t* toks,
+hipError_t launch_embed_real(float* X, T* Xh, const T* tok, const T* pos, const int32_t* toks,
                              int tok_stride, KfStepGeom g, int d, int V, KfDevState* st,
                              hipStream_t s) {
   if (g.nr <= 0 || g.B <= 0) return hipSuccess;
-  hipLaunchKernelGGL(embed_real_kernel<T>, dim3(g.B * g.nr), dim3(256), 0, s, X, tok, pos, toks,
+  hipLaunchKernelGGL(embed_real_kernel<T>, dim3(g.B * g.nr), dim3(256), 0, s, X, Xh, tok, pos, toks,
                      tok_stride, g, d, V, st);
   return hipGetLastError();
 }
@@ -561,7 +567,7 @@ hipError_t launch_copy_f32(const float* src, float* dst, size_t n, hipStream_t s
 hipError_t launch_zero_i32(int* dst, size_t n, hipStream_t s) { return launch_zero<int>(dst, n, s); }
 
 #define KF_INST(T)                                                                                  \
-  template hipError_t launch_embed_real<T>(float*, const T*, const T*, const int32_t*, int,        \
+  template hipError_t launch_embed_real<T>(float*, T*, const T*, const T*, const int32_t*, int,    \
                                            KfStepGeom, int, int, KfDevState*, hipStream_t);         \
   template hipError_t launch_noise_sinusoid<T>(T*, const float*, uint64_t, const double*,          \
                                                KfStepGeom, int, const KfDevState*, float*,          \
