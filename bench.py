@@ -68,13 +68,13 @@ def step_costs(cfg: S.ModelConfig, B: int, nr: int, k: int, C: int) -> dict:
         add("noise", 4 * d * d * es + Mk * 4 * d * es + Mk * d * (4 + es), 2 * Mk * d * 4 * d)
     visible = sum(C + i + 1 for i in range(R))  # keys seen by the R queries of a sequence
     for _ in range(L):
-        add("norm", 2 * M * d * (4 + es), 0)
+        # LayerNorm is folded into the GEMM that consumes it: its bytes are the
+        # GEMM's activation read, counted there.
         add("qkv", 3 * d * d * es + M * d * es + M * 3 * d * es, 2 * M * 3 * d * d)
         add("attn", B * (C + R) * 2 * d * es + 2 * M * d * es, 4 * B * visible * d)
         add("oproj", d * d * es + M * d * es + 2 * M * d * 4, 2 * M * d * d)
         add("mlp_up", f * d * es + M * d * es + M * f * es, 2 * M * f * d)
         add("mlp_down", d * f * es + M * f * es + 2 * M * d * 4, 2 * M * d * f)
-    add("norm", Mh * d * (4 + es), 0)
     add("head", V * d * es + Mh * d * es, 2 * Mh * V * d)
     add("select", Mh * 8, 0)
     return c
@@ -112,6 +112,9 @@ def parse():
     ap.add_argument("--k", type=int, default=None)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-ar", action="store_true", help="skip the k=1 AR baseline")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the OpenWebText-shaped batch sweep and k comparison")
+    ap.add_argument("--sweep-batches", default="1,16,64,256,512")
     ap.add_argument("--cpu-blocks", type=int, default=8,
                     help="decode blocks per sequence in the CPU oracle sample")
     ap.add_argument("--summarize", metavar="DIR", default=None,
@@ -200,6 +203,81 @@ def summarize(root: str) -> None:
         wm = np.mean(wv) if wv else float("nan")
         print(f"| {k[0]} | {k[1]} | {len(fv or wv)} | {fm:.1f} | {wm:.1f} | "
               f"{fm * 1024 * (f_scale or 1) / 1e6:.2f} | {wm * 1024 * (w_scale or 1) / 1e6:.2f} |")
+
+
+def step_roof_ms(costs, dtype) -> float:
+    by = sum(v[0] for v in costs.values())
+    fl = sum(v[1] for v in costs.values())
+    return max(by / (PEAK_HBM_GBS * 1e9), fl / (PEAK_MFMA_TFLOPS[dtype] * 1e12)) * 1e3
+
+
+def time_calls(fn, reps):
+    import torch
+    fn()  # warm-up (also captures the decode-step graph)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        fn()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) / reps
+
+
+def owt_sweep(batches, stream):
+    """OpenWebText-shaped model (12 layers, d=768, vocab 50257, context 1024,
+    bf16), prompt 128 Zipf(1.1) tokens, generation to the full context (896 new
+    tokens): k=4 against the k=1 AR baseline per batch size, and k in {1, 2, 4}
+    (plus AR) at batch 32.  Each figure is whole-generate throughput with its
+    step-level roofline fraction t_roof / t_meas."""
+    import torch
+    from paper_2606_10820_amd import binding as Bd
+    w = S.WORKLOADS["owt"]
+    cfg = w["cfg"]
+    N, L, seed = w["N"], w["L"], 2
+    log("[bench] sweep: generating OWT-shaped weights")
+    blob = S.pack_blob(cfg, S.make_weights(cfg, seed=0))
+    dev = torch.device("cuda:0")
+
+    def ctx(B):
+        kc = Bd.make_config(cfg.n_layer, cfg.d_model, cfg.n_head, cfg.d_mlp, cfg.vocab,
+                            cfg.n_ctx, cfg.dtype, B, 4, N, 0)
+        kf = Bd.KForcing(kc, device="cuda:0", stream=stream)
+        kf.load_weights(blob)
+        return kf
+
+    def run(kf, B, k, reps):
+        prompt = torch.as_tensor(S.make_prompts(w["prompts"], 1, B, N, cfg.vocab), device=dev)
+        out = torch.empty((B, L), dtype=torch.int32, device=dev)
+        if k == 0:
+            dt = time_calls(lambda: kf.generate_ar(prompt, L, seed, out=out), reps)
+            roof = step_roof_ms(generate_ar_costs(cfg, B, N, L), cfg.dtype)
+        else:
+            dt = time_calls(lambda: kf.generate(prompt, L, k, seed, out=out), reps)
+            roof = step_roof_ms(generate_costs(cfg, B, N, L, k), cfg.dtype)
+        return {"tokens_s": round(B * L / dt, 1), "ms_per_generate": round(dt * 1e3, 3),
+                "roofline_ms": round(roof, 3), "roofline_frac": round(roof / (dt * 1e3), 4)}
+
+    rows = []
+    for B in batches:
+        kf = ctx(B)
+        r4 = run(kf, B, 4, 2)
+        r1 = run(kf, B, 0, 1)
+        rows.append({"batch": B, "k4": r4, "ar_k1": r1,
+                     "speedup_k4_vs_ar": round(r4["tokens_s"] / r1["tokens_s"], 3)})
+        log(f"[bench] sweep B={B}: k=4 {r4['tokens_s']:,.0f} tok/s "
+            f"({r4['roofline_frac']:.1%} of step roofline), AR {r1['tokens_s']:,.0f} tok/s, "
+            f"x{rows[-1]['speedup_k4_vs_ar']:.2f}")
+        del kf
+        torch.cuda.empty_cache()
+    B = w["B"]
+    kf = ctx(B)
+    ks = {f"k{k}": run(kf, B, k, 2) for k in (1, 2, 4)}
+    ks["ar_k1"] = run(kf, B, 0, 1)
+    log("[bench] OWT B=%d: " % B + ", ".join(f"{n} {v['tokens_s']:,.0f} tok/s" for n, v in ks.items()))
+    del kf
+    torch.cuda.empty_cache()
+    return {"workload": (f"OWT-shaped: {cfg.n_layer} layers, d={cfg.d_model}, vocab {cfg.vocab}, "
+                         f"context {cfg.n_ctx}, prompt {N} Zipf(1.1), {L} new tokens, bf16"),
+            "by_batch": rows, "k_at_batch": {"batch": B, **ks}}
 
 
 def main():
@@ -322,6 +400,9 @@ def main():
                                  "ms_per_step": round(dt_ar / ar_steps * 1e3, 4),
                                  "passes": L, "speedup_k_vs_ar": round(value / v_ar, 3)}
         log(f"[bench] AR k=1: {v_ar:,.0f} tokens/s -> speedup {value / v_ar:.2f}x")
+
+    if not a.no_sweep:
+        res["owt_sweep"] = owt_sweep([int(x) for x in a.sweep_batches.split(",") if x], stream)
 
     if not a.no_cpu:
         log("[bench] CPU oracle sample ...")

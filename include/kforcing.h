@@ -64,6 +64,10 @@ typedef struct kf_config {
   int max_prompt; /* longest prompt N given to a prefill call */
   unsigned flags; /* KF_FLAG_* */
 } kf_config;
+/* A config is also rejected when the rows of its largest step,
+ * max_batch * (max(max_prompt, max_k) + max_k), times max(d_mlp, 4 d_model)
+ * compute-dtype elements (or times d_model fp32 elements) reach 2 GiB: the
+ * GEMMs address their operands with 32-bit byte ranges. */
 
 /* Opaque per-stream context. */
 typedef struct kf_ctx kf_ctx;

@@ -42,8 +42,8 @@ struct Plan {
   size_t head_c1 = 0, head_c2 = 0, head_w = 0;  // folded final norm; gain-scaled token table
   std::vector<LayerOff> layer;
   size_t kv = 0, kv_bytes = 0;
-  size_t X = 0, Xh = 0, A = 0, Q = 0, O = 0, Hm = 0, noise = 0, pval = 0, pidx = 0, logits = 0, dstate = 0,
-         pend = 0;
+  size_t X = 0, Xh = 0, lnst = 0, A = 0, Q = 0, O = 0, Hm = 0, noise = 0, pval = 0, pidx = 0;
+  size_t logits = 0, dstate = 0, pend = 0;
   size_t total = 0;
 };
 
@@ -66,6 +66,13 @@ bool config_ok(const kf_config& c, std::string* why) {
   if (c.max_k < 1 || c.max_k > c.n_ctx) return bad("max_k must be in [1, n_ctx]");
   if (c.max_prompt < 1 || c.max_prompt > c.n_ctx) return bad("max_prompt must be in [1, n_ctx]");
   if (c.flags & ~KF_FLAG_DEBUG_LOGITS) return bad("unknown flag bits");
+  // GEMM operands are addressed through buffer descriptors with 32-bit byte
+  // ranges: the largest activation matrix of a step must stay below 2 GiB.
+  const long long es = c.dtype == KF_BF16 ? 2 : 4;
+  const long long rows = (long long)c.max_batch * ((c.max_prompt > c.max_k ? c.max_prompt : c.max_k) + c.max_k);
+  const long long width = c.d_mlp > 4 * c.d_model ? c.d_mlp : 4 * c.d_model;
+  if (rows * width * es >= (1LL << 31) || rows * c.d_model * 4 >= (1LL << 31))
+    return bad("max_batch * (max(max_prompt, max_k) + max_k) rows too large for one step");
   return true;
 }
 
@@ -123,6 +130,7 @@ void make_plan(const kf_config& c, Plan& p) {
   const size_t R = p.rows_max, Hw = f > 4 * d ? f : 4 * d;
   p.X = take(R * d * 4);
   p.Xh = es == 2 ? take(R * d * es) : p.X;
+  p.lnst = take(R * (d / 16) * 8);  // LayerNorm partial sums of the residual rows
   p.A = take(R * d * es);
   p.Q = take(R * d * es);
   p.O = take(R * d * es);
@@ -261,6 +269,7 @@ int run_step(kf_ctx* c, const StepIn& in) {
   KfDevState* st = reinterpret_cast<KfDevState*>(base + p.dstate);
   float* X = reinterpret_cast<float*>(base + p.X);
   T* Xh = reinterpret_cast<T*>(base + p.Xh);  // compute-dtype residual copy (X itself for fp32)
+  float2* lnst = reinterpret_cast<float2*>(base + p.lnst);
   T* A = reinterpret_cast<T*>(base + p.A);  // noise sinusoid staging
   T* Q = reinterpret_cast<T*>(base + p.Q);
   T* O = reinterpret_cast<T*>(base + p.O);
@@ -279,7 +288,7 @@ int run_step(kf_ctx* c, const StepIn& in) {
   if (in.reset) KF_HIP(c, kf::launch_zero_i32(reinterpret_cast<int*>(st), 1, s));
   if (in.nr > 0)
     KF_LAUNCH(c, KF_KC_EMBED,
-              kf::launch_embed_real<T>(X, Xh, tok, pos, in.toks, in.tok_stride, g, d, V, st, s));
+              kf::launch_embed_real<T>(X, Xh, lnst, tok, pos, in.toks, in.tok_stride, g, d, V, st, s));
   if (in.k > 0) {
     const int Mk = in.B * in.k;
     float* urec = reinterpret_cast<float*>(base + p.noise);
@@ -290,23 +299,23 @@ int run_step(kf_ctx* c, const StepIn& in) {
     KF_LAUNCH(c, KF_KC_NOISE,
               kf::gemm_bias<T>(A, W(p.nw1), Mk, 4 * d, d, F(p.nb1), kf::Act::Gelu, Hm, 4 * d, s));
     KF_LAUNCH(c, KF_KC_NOISE,
-              kf::gemm_noise_out<T>(Hm, W(p.nw2), Mk, d, 4 * d, F(p.nb2), pos, X, Xh, g, st, s));
+              kf::gemm_noise_out<T>(Hm, W(p.nw2), Mk, d, 4 * d, F(p.nb2), pos, X, Xh, lnst, g, st, s));
   }
   for (int l = 0; l < cf.n_layer; ++l) {
     const LayerOff& y = p.layer[l];
-    const kf::LnFold ln1{F(y.qkv_c1), F(y.qkv_c2)};
-    const kf::LnFold ln2{F(y.up_c1), F(y.up_c2)};
+    const kf::LnFold ln1{F(y.qkv_c1), F(y.qkv_c2), lnst};
+    const kf::LnFold ln2{F(y.up_c1), F(y.up_c2), lnst};
     KF_LAUNCH(c, KF_KC_QKV,
               kf::gemm_qkv_ln<T>(Xh, ln1, W(y.wqkv), M, d, F(y.bqkv), Q, kv, g, kg, l, st, s));
     KF_LAUNCH(c, KF_KC_ATTN, kf::launch_attention<T>(Q, kv, O, st, g, kg, l, s));
-    KF_LAUNCH(c, KF_KC_OPROJ, kf::gemm_residual<T>(O, W(y.wo), M, d, d, F(y.bo), X, Xh, s));
+    KF_LAUNCH(c, KF_KC_OPROJ, kf::gemm_residual<T>(O, W(y.wo), M, d, d, F(y.bo), X, Xh, lnst, s));
     KF_LAUNCH(c, KF_KC_MLP_UP, kf::gemm_up_ln<T>(Xh, ln2, W(y.w1), M, f, d, F(y.b1), Hm, s));
-    KF_LAUNCH(c, KF_KC_MLP_DOWN, kf::gemm_residual<T>(Hm, W(y.w2), M, d, f, F(y.b2), X, Xh, s));
+    KF_LAUNCH(c, KF_KC_MLP_DOWN, kf::gemm_residual<T>(Hm, W(y.w2), M, d, f, F(y.b2), X, Xh, lnst, s));
   }
   const bool ar = in.k == 0;
   const int Mh = ar ? in.B : in.B * in.k;
   float* logits = (ar || debug) ? reinterpret_cast<float*>(base + p.logits) : nullptr;
-  const kf::LnFold lnf{F(p.head_c1), F(p.head_c2)};
+  const kf::LnFold lnf{F(p.head_c1), F(p.head_c2), lnst};
   KF_LAUNCH(c, KF_KC_HEAD,
             kf::gemm_head_ln<T>(Xh, lnf, W(p.head_w), Mh, p.Vpad, V, d, ar ? 2 : 1, g,
                                 reinterpret_cast<float*>(base + p.pval),

@@ -68,7 +68,11 @@ struct Mfma<float> {
 // ------------------------------------------------------------ epilogues
 // store4(m, n, v): v holds C[m][n .. n+3] with the bias already added (the
 // kernel loads each lane's bias columns before its K loop); N is a multiple
-// of 4.
+// of 4.  Epilogues that write the residual stream (kStats) return the four
+// values written and name their stream row (srow); the kernel then writes the
+// LayerNorm partial sums of every 16-column group of that row to lnst
+// [rows][ldx / 16] as (sum x, sum x^2), which the next LayerNorm-folded GEMM
+// reads instead of recomputing row statistics.
 
 // Four consecutive values to T memory in one store.
 template <typename T>
@@ -90,11 +94,13 @@ struct EpBias {
   int ldo;
   const float* bias;
   int gelu;
-  __device__ inline void store4(int m, int n, f32x4 v) const {
+  static constexpr bool kStats = false;
+  __device__ inline f32x4 store4(int m, int n, f32x4 v) const {
     float x[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) x[i] = gelu ? gelu_f(v[i]) : v[i];
     put4(out + (size_t)m * ldo + n, x[0], x[1], x[2], x[3]);
+    return v;
   }
 };
 
@@ -107,7 +113,11 @@ struct EpResidual {
   T* Xh;
   int ldx;
   const float* bias;
-  __device__ inline void store4(int m, int n, f32x4 v) const {
+  float2* lnst;
+  static constexpr bool kStats = true;
+  __device__ inline int srow(int m) const { return m; }
+  __device__ inline int cols() const { return ldx; }
+  __device__ inline f32x4 store4(int m, int n, f32x4 v) const {
     float4* p = reinterpret_cast<float4*>(X + (size_t)m * ldx + n);
     float4 x = *p;
     x.x += v[0];
@@ -116,6 +126,7 @@ struct EpResidual {
     x.w += v[3];
     *p = x;
     if constexpr (sizeof(T) == 2) put4(Xh + (size_t)m * ldx + n, x.x, x.y, x.z, x.w);
+    return f32x4{x.x, x.y, x.z, x.w};
   }
 };
 
@@ -131,12 +142,13 @@ struct EpQKV {
   KfStepGeom g;
   KfKvGeom kg;
   int layer;
-  __device__ inline void store4(int m, int n, f32x4 v) const {
+  static constexpr bool kStats = false;
+  __device__ inline f32x4 store4(int m, int n, f32x4 v) const {
     const int d = kg.H * kg.dh;
     const int which = n / d, c = n - which * d;
     if (which == 0) {
       put4(Q + (size_t)m * d + c, v[0], v[1], v[2], v[3]);
-      return;
+      return v;
     }
     const int b = m / g.R, i = m - b * g.R;
     const int h = c / kg.dh, e = c - h * kg.dh;
@@ -148,6 +160,7 @@ struct EpQKV {
 #pragma unroll
       for (int r = 0; r < 4; ++r) base[(size_t)(e + r) * kg.T + slot] = from_f<T>(v[r]);
     }
+    return v;
   }
 };
 
@@ -162,21 +175,30 @@ struct EpNoiseOut {
   const KfDevState* st;
   KfStepGeom g;
   int d;
-  __device__ inline void store4(int m, int n, f32x4 v) const {
-    const int b = m / g.k, j = m - b * g.k;
+  float2* lnst;
+  static constexpr bool kStats = true;
+  __device__ inline int cols() const { return d; }
+  __device__ inline int srow(int m) const {
+    const int b = m / g.k;
+    return b * g.R + g.nr + (m - b * g.k);
+  }
+  __device__ inline f32x4 store4(int m, int n, f32x4 v) const {
+    const int j = m % g.k;
     const int p = st->C + g.nr + j;
-    const size_t row = (size_t)b * g.R + g.nr + j;
+    const size_t row = (size_t)srow(m);
     const T* pe = pos + (size_t)p * d + n;
     float x[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) x[i] = v[i] + to_f(pe[i]);
     *reinterpret_cast<float4*>(X + row * d + n) = make_float4(x[0], x[1], x[2], x[3]);
     if constexpr (sizeof(T) == 2) put4(Xh + row * d + n, x[0], x[1], x[2], x[3]);
+    return f32x4{x[0], x[1], x[2], x[3]};
   }
 };
 
 // Head: no store; per-tile argmax partials (and optional fp32 logits).
 struct EpHead {
+  static constexpr bool kStats = false;
   const float* bias;  // always null: the tied head has no bias
   float* pval;
   int* pidx;
@@ -202,13 +224,23 @@ struct IsHead<EpHead> {
 constexpr int KCH = 8;
 __device__ inline int swz(int r, int c) { return r * KCH + (c ^ ((r >> 1) & 7)); }
 
-// Workgroups are dealt to the eight XCDs round-robin by linear id; give each
-// XCD a contiguous run of tiles (M fastest) so that the workgroups sharing a
-// weight strip share one L2.
-__device__ inline int xcd_tile(int lin, int total) {
+// Workgroups are dealt to the eight XCDs round-robin by linear id.  Each XCD
+// gets a contiguous run of the tile order, and the order walks the grid in
+// column groups of kGroupN weight tiles (M fastest inside a group): the
+// workgroups an XCD runs together then cover a compact block of rows and
+// columns, so both operand strips stay in that XCD's L2 instead of every
+// XCD streaming all of A once per weight strip.
+constexpr int kGroupN = 4;
+__device__ inline void tile_coords(int lin, int gm, int gn, int& tm, int& tn) {
+  const int total = gm * gn;
   const int q = total >> 3, r = total & 7;
   const int x = lin & 7, j = lin >> 3;
-  return x * q + (x < r ? x : r) + j;
+  const int t = x * q + (x < r ? x : r) + j;  // this XCD's run of the order
+  const int grp = t / (gm * kGroupN), first = grp * kGroupN;
+  const int width = gn - first < kGroupN ? gn - first : kGroupN;
+  const int u = t - grp * gm * kGroupN;
+  tm = u / width;
+  tn = first + u % width;
 }
 
 // ------------------------------------------------------------ memory ops
@@ -268,25 +300,24 @@ __device__ inline int map_row(int m, const KfStepGeom& g) {
 // With NORM, the GEMM applies the LayerNorm of each A row through the folded
 // weights: W' = W diag(g) (scaled at weight load), c1 = W' 1, c2 = W beta, so
 //   LN(x) W^T = rstd * (x W'^T - mu * c1) + c2,
-// where mu and rstd = 1 / sqrt(var + 1e-5) come from the A tile itself: the
-// workgroup stages every column of its rows, and the statistics are summed
-// from LDS as the K loop passes.
+// where mu and rstd = 1 / sqrt(var + 1e-5) come from the row's partial sums
+// lnst [arows][K / 16] (sum x, sum x^2 per 16 columns of the fp32 residual
+// row), written by the kernel that produced the row.
 struct GemmA {
   const void* A;
   int lda;
   int arows;
   const float* c1;
   const float* c2;
+  const float2* lnst;
   KfStepGeom g;
 };
 
 // ---------------------------------------------------------------- kernel
-// S-stage LDS ring.  At K step kt the kernel waits for its own loads of
-// stage kt, meets the other wavefronts at a barrier (after which every load of
-// stage kt has landed and every read of stage kt - 1 is done), issues the loads
-// of step kt + S - 1 into the buffer that stage kt - 1 used, and multiplies
-// stage kt.  Each wavefront loads 8 rows (one 128-byte slab each) per
-// instruction: BM / 32 A instructions and BN / 32 W instructions per stage.
+// S-stage LDS ring fed by direct-to-LDS loads, with a register double buffer
+// of MFMA operands (pipeline described at the K loop).  Each wavefront loads
+// 8 rows (one 128-byte slab each) per instruction: BM / 32 A instructions and
+// BN / 32 W instructions per stage.
 template <typename T, int BM, int BN, int WM, int WN, int S, int MODE, bool NORM, class Ep>
 __global__ void __launch_bounds__(256)
     gemm_kernel(GemmA ga, const T* __restrict__ W, int ldw, int M, int N, int K, Ep ep) {
@@ -295,7 +326,6 @@ __global__ void __launch_bounds__(256)
   constexpr int MW = BM / WM, NW = BN / WN;
   constexpr int TM = MW / 16, TN = NW / 16;
   constexpr int PA = BM / 32, PW = BN / 32, PER = PA + PW;
-  constexpr int LS = NORM ? BM * KCH / 256 : 1;  // statistics chunks per thread
   constexpr int ROWB = KCH * 16;                 // bytes per staged row
   static_assert(WM * WN == 4, "four wavefronts");
   static_assert(MW % 16 == 0 && NW % 16 == 0, "16x16 MFMA tiles");
@@ -308,8 +338,9 @@ __global__ void __launch_bounds__(256)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   const int gm = (M + BM - 1) / BM, gn = (N + BN - 1) / BN;
-  const int tile = xcd_tile(blockIdx.x, gm * gn);
-  const int m0 = (tile % gm) * BM, n0 = (tile / gm) * BN;
+  int tmi, tni;
+  tile_coords(blockIdx.x, gm, gn, tmi, tni);
+  const int m0 = tmi * BM, n0 = tni * BN;
   const int nk = K / BK;
 
   const T* A = static_cast<const T*>(ga.A);
@@ -352,16 +383,6 @@ __global__ void __launch_bounds__(256)
     rdA[s] = (uint32_t)(((wm * MW + (lane & 15)) * KCH + ch) * 16);
     rdW[s] = (uint32_t)(((BM + wn * NW + (lane & 15)) * KCH + ch) * 16);
   }
-  uint32_t rdS[LS];
-  float s1[LS], s2[LS];
-#pragma unroll
-  for (int q = 0; q < LS; ++q) {
-    const int c = tid + q * 256;
-    rdS[q] = (uint32_t)(swz(c / KCH, c % KCH) * 16);
-    s1[q] = 0.f;
-    s2[q] = 0.f;
-  }
-
   f32x4 acc[TN][TM];
 #pragma unroll
   for (int x = 0; x < TN; ++x)
@@ -381,91 +402,117 @@ __global__ void __launch_bounds__(256)
     p2[tn] = NORM ? *reinterpret_cast<const f32x4*>(ga.c2 + nc) : z;
   }
 
-  auto compute = [&](int stage) {
-    const uint32_t sb = lds_addr(&sbuf[stage][0]);
-    u32x4 af[2][TN], bv[2][TM], xs[LS];
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-#pragma unroll
-      for (int tn = 0; tn < TN; ++tn) af[s][tn] = ds_read16(sb + rdW[s] + tn * 16 * ROWB);
-#pragma unroll
-      for (int tm = 0; tm < TM; ++tm) bv[s][tm] = ds_read16(sb + rdA[s] + tm * 16 * ROWB);
-    }
-    if constexpr (NORM) {
-#pragma unroll
-      for (int q = 0; q < LS; ++q) xs[q] = ds_read16(sb + rdS[q]);
-    }
-    lgkm_wait0();
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-#pragma unroll
-      for (int tn = 0; tn < TN; ++tn) pin(af[s][tn]);
-#pragma unroll
-      for (int tm = 0; tm < TM; ++tm) pin(bv[s][tm]);
-    }
-#pragma unroll
-    for (int s = 0; s < 2; ++s)
-#pragma unroll
-      for (int tn = 0; tn < TN; ++tn)
-#pragma unroll
-        for (int tm = 0; tm < TM; ++tm) Mfma<T>::mma(af[s][tn], bv[s][tm], acc[tn][tm]);
-    if constexpr (NORM) {
-#pragma unroll
-      for (int q = 0; q < LS; ++q) {
-        pin(xs[q]);
-        // The words are named one by one: bit-casting xs[q][w] with an
-        // unrolled index w has been compiled to read word 0 every time.
-        const uint32_t xw[4] = {xs[q].x, xs[q].y, xs[q].z, xs[q].w};
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          if constexpr (sizeof(T) == 2) {  // v_dot2: two products and the sum per instruction
-            const bf16x2 x2 = __builtin_bit_cast(bf16x2, xw[w]);
-            s1[q] = __builtin_amdgcn_fdot2_f32_bf16(x2, bf16x2{(bf16)1.0f, (bf16)1.0f}, s1[q], false);
-            s2[q] = __builtin_amdgcn_fdot2_f32_bf16(x2, x2, s2[q], false);
-          } else {
-            const float v = __uint_as_float(xw[w]);
-            s1[q] += v;
-            s2[q] += v * v;
-          }
-        }
-      }
-    }
+  // One 32-wide K slice (half a slab) of this wavefront's operands.
+  struct Slice {
+    u32x4 a[TN];  // weight rows (MFMA "A")
+    u32x4 b[TM];  // activation rows (MFMA "B")
   };
-
+  auto read_slice = [&](int stage, int s, Slice& f) {
+    const uint32_t sb = lds_addr(&sbuf[stage][0]);
 #pragma unroll
-  for (int i = 0; i < S - 1; ++i)
+    for (int tn = 0; tn < TN; ++tn) f.a[tn] = ds_read16(sb + rdW[s] + tn * 16 * ROWB);
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) f.b[tm] = ds_read16(sb + rdA[s] + tm * 16 * ROWB);
+  };
+  auto pin_slice = [&](Slice& f) {
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) pin(f.a[tn]);
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) pin(f.b[tm]);
+  };
+  auto mma_slice = [&](const Slice& f) {
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm) Mfma<T>::mma(f.a[tn], f.b[tm], acc[tn][tm]);
+  };
+  // Software pipeline over K steps (one 64-wide slab per step, two slices):
+  //   [slice 0 of step kt is in registers]
+  //   read slice 1 of step kt; MFMAs of slice 0
+  //   wait for the reads; wait for this wavefront's loads of stage kt + 1
+  //   barrier: stage kt + 1 has landed, every read of stage kt is done
+  //   load step kt + S into stage kt's buffer; read slice 0 of step kt + 1
+  //   MFMAs of slice 1 of step kt; wait for the reads
+  // so LDS reads always run under MFMAs, and S stages are loading at a time.
+  // Folded LayerNorm: each row's mean and rstd from its partial sums.  The
+  // partials are loaded before the operand loads are issued (so waiting for
+  // them does not wait for the operands) and reduced by the TPR consecutive
+  // lanes that share a row.
+  constexpr int TPR = NORM ? 256 / BM : 1;
+  constexpr int PMAX = 12;  // float4 loads (two partials each) per lane, unrolled
+  float4 part[PMAX];
+  const int parts4 = K / 32;  // float4 words per row
+  const float4* prow = nullptr;
+  if constexpr (NORM) {
+    const int r = tid / TPR, gr = m0 + r < M ? m0 + r : M - 1;
+    prow = reinterpret_cast<const float4*>(ga.lnst + (size_t)map_row<MODE>(gr, ga.g) * (K / 16));
+#pragma unroll
+    for (int j = 0; j < PMAX; ++j) {
+      const int w = (tid % TPR) + j * TPR;
+      part[j] = w < parts4 ? prow[w] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  }
+  Slice f0, f1;
+#pragma unroll
+  for (int i = 0; i < S; ++i)
     if (i < nk) issue(i, i);
+  if constexpr (NORM) {
+    float a = 0.f, b = 0.f;
+#pragma unroll
+    for (int j = 0; j < PMAX; ++j) {
+      a += part[j].x + part[j].z;
+      b += part[j].y + part[j].w;
+    }
+    for (int w = (tid % TPR) + PMAX * TPR; w < parts4; w += TPR) {  // wide rows only
+      const float4 v = prow[w];
+      a += v.x + v.z;
+      b += v.y + v.w;
+    }
+#pragma unroll
+    for (int off = 1; off < TPR; off <<= 1) {
+      a += __shfl_xor(a, off, 64);
+      b += __shfl_xor(b, off, 64);
+    }
+    if (tid % TPR == 0) {
+      const float mu = a / (float)K;
+      const float var = fmaxf(b / (float)K - mu * mu, 0.f);
+      sStat[tid / TPR] = make_float2(mu, 1.0f / sqrtf(var + 1e-5f));
+    }
+  }
+  if (nk > S - 1) vm_wait<(S - 1) * PER>();
+  else vm_wait<0>();
+  lgkm_wait0();  // sStat written before the barrier publishes it
+  __builtin_amdgcn_s_barrier();
+  read_slice(0, 0, f0);
+  lgkm_wait0();
+  pin_slice(f0);
   for (int kt0 = 0; kt0 < nk; kt0 += S) {
 #pragma unroll
     for (int i = 0; i < S; ++i) {
       const int kt = kt0 + i;
       if (kt < nk) {
-        if (kt + S - 2 < nk) vm_wait<(S - 2) * PER>();
-        else vm_wait<0>();
-        __builtin_amdgcn_s_barrier();
-        if (kt + S - 1 < nk) issue((i + S - 1) % S, kt + S - 1);
-        compute(i);
+        read_slice(i, 1, f1);
+        __builtin_amdgcn_sched_barrier(0);  // the reads issue first,
+        mma_slice(f0);                       // the MFMAs run under them,
+        __builtin_amdgcn_sched_barrier(0);  // and only then the wait
+        lgkm_wait0();
+        pin_slice(f1);
+        if (kt + 1 < nk) {
+          if (kt + S - 1 < nk) vm_wait<(S - 2) * PER>();
+          else vm_wait<0>();
+          __builtin_amdgcn_s_barrier();
+          if (kt + S < nk) issue(i, kt + S);
+          read_slice((i + 1) % S, 0, f0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        mma_slice(f1);
+        __builtin_amdgcn_sched_barrier(0);
+        lgkm_wait0();
+        pin_slice(f0);
       }
     }
   }
 
-  if constexpr (NORM) {
-#pragma unroll
-    for (int q = 0; q < LS; ++q) {
-      float a = s1[q], b = s2[q];
-#pragma unroll
-      for (int off = 1; off < KCH; off <<= 1) {
-        a += __shfl_xor(a, off, 64);
-        b += __shfl_xor(b, off, 64);
-      }
-      if ((tid % KCH) == 0) {
-        const float mu = a / (float)K;
-        const float var = fmaxf(b / (float)K - mu * mu, 0.f);
-        sStat[(tid + q * 256) / KCH] = make_float2(mu, 1.0f / sqrtf(var + 1e-5f));
-      }
-    }
-    __syncthreads();
-  }
   // Folded LayerNorm (if any) and bias for 16x16 tile (tn, row ml).
   auto apply = [&](f32x4 v, int ml, int tn) -> f32x4 {
     f32x4 r;
@@ -487,7 +534,20 @@ __global__ void __launch_bounds__(256)
       for (int tm = 0; tm < TM; ++tm) {
         const int n = n0 + wn * NW + tn * 16 + 4 * (lane >> 4);
         const int ml = wm * MW + tm * 16 + (lane & 15), m = m0 + ml;
-        if (m < M && n < N) ep.store4(m, n, apply(acc[tn][tm], ml, tn));
+        const bool live = m < M && n < N;
+        f32x4 x = {0.f, 0.f, 0.f, 0.f};
+        if (live) x = ep.store4(m, n, apply(acc[tn][tm], ml, tn));
+        if constexpr (Ep::kStats) {
+          // the four lane groups hold the 16 columns of this tile's row m
+          float a = x[0] + x[1] + x[2] + x[3];
+          float b = x[0] * x[0] + x[1] * x[1] + x[2] * x[2] + x[3] * x[3];
+          a += __shfl_xor(a, 16, 64);
+          b += __shfl_xor(b, 16, 64);
+          a += __shfl_xor(a, 32, 64);
+          b += __shfl_xor(b, 32, 64);
+          if (live && (lane >> 4) == 0)
+            ep.lnst[(size_t)ep.srow(m) * (ep.cols() / 16) + n / 16] = make_float2(a, b);
+        }
       }
   } else {
     // Row-wise argmax over this tile's columns: lane-local, then across the
@@ -608,22 +668,25 @@ template <typename T>
 hipError_t gemm_bias(const T* A, const T* W, int M, int N, int K, const float* bias, Act act,
                      T* out, int ldo, hipStream_t s) {
   EpBias<T> ep{out, ldo, bias, act == Act::Gelu ? 1 : 0};
-  return dispatch<T, 0, false>(GemmA{A, K, M, nullptr, nullptr, KfStepGeom{}}, W, M, N, K, ep, s);
+  return dispatch<T, 0, false>(GemmA{A, K, M, nullptr, nullptr, nullptr, KfStepGeom{}}, W, M, N, K,
+                               ep, s);
 }
 
 template <typename T>
 hipError_t gemm_residual(const T* A, const T* W, int M, int N, int K, const float* bias, float* X,
-                         T* Xh, hipStream_t s) {
-  EpResidual<T> ep{X, Xh, N, bias};
-  return dispatch<T, 0, false>(GemmA{A, K, M, nullptr, nullptr, KfStepGeom{}}, W, M, N, K, ep, s);
+                         T* Xh, float2* lnst, hipStream_t s) {
+  EpResidual<T> ep{X, Xh, N, bias, lnst};
+  return dispatch<T, 0, false>(GemmA{A, K, M, nullptr, nullptr, nullptr, KfStepGeom{}}, W, M, N, K,
+                               ep, s);
 }
 
 template <typename T>
 hipError_t gemm_noise_out(const T* A, const T* W, int M, int d, int K, const float* bias,
-                          const T* pos, float* X, T* Xh, KfStepGeom g, const KfDevState* st,
-                          hipStream_t s) {
-  EpNoiseOut<T> ep{X, Xh, bias, pos, st, g, d};
-  return dispatch<T, 0, false>(GemmA{A, K, M, nullptr, nullptr, KfStepGeom{}}, W, M, d, K, ep, s);
+                          const T* pos, float* X, T* Xh, float2* lnst, KfStepGeom g,
+                          const KfDevState* st, hipStream_t s) {
+  EpNoiseOut<T> ep{X, Xh, bias, pos, st, g, d, lnst};
+  return dispatch<T, 0, false>(GemmA{A, K, M, nullptr, nullptr, nullptr, KfStepGeom{}}, W, M, d, K,
+                               ep, s);
 }
 
 template <typename T>
@@ -631,14 +694,15 @@ hipError_t gemm_qkv_ln(const T* Xh, const LnFold& ln, const T* W, int M, int d, 
                        T* Q, T* kv, KfStepGeom g, KfKvGeom kg, int layer, const KfDevState* st,
                        hipStream_t s) {
   EpQKV<T> ep{Q, kv, bias, st, g, kg, layer};
-  return dispatch<T, 0, true>(GemmA{Xh, d, M, ln.c1, ln.c2, g}, W, M, 3 * d, d, ep, s);
+  return dispatch<T, 0, true>(GemmA{Xh, d, M, ln.c1, ln.c2, ln.lnst, g}, W, M, 3 * d, d, ep, s);
 }
 
 template <typename T>
 hipError_t gemm_up_ln(const T* Xh, const LnFold& ln, const T* W, int M, int N, int d,
                       const float* bias, T* out, hipStream_t s) {
   EpBias<T> ep{out, N, bias, 1};
-  return dispatch<T, 0, true>(GemmA{Xh, d, M, ln.c1, ln.c2, KfStepGeom{}}, W, M, N, d, ep, s);
+  return dispatch<T, 0, true>(GemmA{Xh, d, M, ln.c1, ln.c2, ln.lnst, KfStepGeom{}}, W, M, N, d, ep,
+                              s);
 }
 
 template <typename T>
@@ -647,7 +711,7 @@ hipError_t gemm_head_ln(const T* Xh, const LnFold& ln, const T* W, int M, int Vp
                         hipStream_t s) {
   if (M <= 0) return hipSuccess;
   EpHead ep{nullptr, pval, pidx, logits, V, Vpad / kHeadTileN};
-  const GemmA ga{Xh, d, g.B * g.R, ln.c1, ln.c2, g};
+  const GemmA ga{Xh, d, g.B * g.R, ln.c1, ln.c2, ln.lnst, g};
   auto go = [&](auto mode) {
     constexpr int MODE = decltype(mode)::value;
     if (M <= 32)
@@ -673,10 +737,10 @@ hipError_t launch_ln_fold(const T* W, T* Wout, const float* g, const float* beta
   template hipError_t gemm_bias<T>(const T*, const T*, int, int, int, const float*, Act, T*, int, \
                                    hipStream_t);                                                   \
   template hipError_t gemm_residual<T>(const T*, const T*, int, int, int, const float*, float*,   \
-                                       T*, hipStream_t);                                           \
+                                       T*, float2*, hipStream_t);                                  \
   template hipError_t gemm_noise_out<T>(const T*, const T*, int, int, int, const float*,          \
-                                        const T*, float*, T*, KfStepGeom, const KfDevState*,       \
-                                        hipStream_t);                                              \
+                                        const T*, float*, T*, float2*, KfStepGeom,                 \
+                                        const KfDevState*, hipStream_t);                           \
   template hipError_t gemm_qkv_ln<T>(const T*, const LnFold&, const T*, int, int, const float*,   \
                                      T*, T*, KfStepGeom, KfKvGeom, int, const KfDevState*,         \
                                      hipStream_t);                                                 \

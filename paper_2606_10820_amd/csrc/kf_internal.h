@@ -74,11 +74,12 @@ namespace kf {
 
 enum class Act { None = 0, Gelu = 1 };
 
-// Real-row embedding: X[b*R + i] = tok[toks[b*tok_stride + i]] + pos[C + i], i < nr.
+// Real-row embedding: X[b*R + i] = tok[toks[b*tok_stride + i]] + pos[C + i], i < nr,
+// with its compute-dtype copy Xh and LayerNorm partial sums lnst (see gemm_residual).
 template <typename T>
-hipError_t launch_embed_real(float* X, T* Xh, const T* tok, const T* pos, const int32_t* toks,
-                             int tok_stride, KfStepGeom g, int d, int V, KfDevState* st,
-                             hipStream_t s);
+hipError_t launch_embed_real(float* X, T* Xh, float2* lnst, const T* tok, const T* pos,
+                             const int32_t* toks, int tok_stride, KfStepGeom g, int d, int V,
+                             KfDevState* st, hipStream_t s);
 
 // Sinusoid of each noise row's u into S [B*k][d]; u from noise [B*k] or, when
 // noise is null, from the device Philox stream at positions C + nr + j.
@@ -99,17 +100,20 @@ hipError_t gemm_bias(const T* A, const T* W, int M, int N, int K, const float* b
                      T* out, int ldo, hipStream_t s);
 // Residual update X[M][N] += C + bias; with a 16-bit T the updated rows are
 // also written to Xh (the compute-dtype copy of the residual stream; for fp32,
-// Xh aliases X and is not written).
+// Xh aliases X and is not written).  Every writer of the residual stream also
+// writes lnst [rows][N / 16]: (sum x, sum x^2) over each 16 columns of the
+// updated row, the input of the next folded LayerNorm.
 template <typename T>
 hipError_t gemm_residual(const T* A, const T* W, int M, int N, int K, const float* bias, float* X,
-                         T* Xh, hipStream_t s);
+                         T* Xh, float2* lnst, hipStream_t s);
 // LayerNorm folded into a GEMM whose weights were scaled by the gain at load
 // (W' = W diag(gain)): c1 = W' 1 and c2 = W shift.  A rows come from the
-// compute-dtype residual copy Xh [rows][d]; each row's mean and variance are
-// taken from the rows as staged by the GEMM.
+// compute-dtype residual copy Xh [rows][d]; each row's mean and variance come
+// from its partial sums in lnst.
 struct LnFold {
   const float* c1;
   const float* c2;
+  const float2* lnst;  // partial row sums of the residual stream (see gemm_residual)
 };
 template <typename T>
 hipError_t gemm_qkv_ln(const T* Xh, const LnFold& ln, const T* W, int M, int d, const float* bias,
@@ -120,8 +124,8 @@ hipError_t gemm_up_ln(const T* Xh, const LnFold& ln, const T* W, int M, int N, i
                       const float* bias, T* out, hipStream_t s);
 template <typename T>
 hipError_t gemm_noise_out(const T* A, const T* W, int M, int d, int K, const float* bias,
-                          const T* pos, float* X, T* Xh, KfStepGeom g, const KfDevState* st,
-                          hipStream_t s);
+                          const T* pos, float* X, T* Xh, float2* lnst, KfStepGeom g,
+                          const KfDevState* st, hipStream_t s);
 // Head over the final LayerNorm of the selected rows (gather: 1 = noise rows
 // of the step, 2 = last real row per sequence): per (row, 128-column tile) the
 // maximum and its lowest column index into pval/pidx [M][Vpad/128]; columns

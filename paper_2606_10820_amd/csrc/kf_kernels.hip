@@ -29,8 +29,8 @@ __device__ inline float wave_sum(float v) {
 // Real rows (Appendix C.1, Embed): token table row plus learned position.
 template <typename T>
 __global__ void __launch_bounds__(256)
-    embed_real_kernel(float* __restrict__ X, T* __restrict__ Xh, const T* __restrict__ tok,
-                      const T* __restrict__ pos,
+    embed_real_kernel(float* __restrict__ X, T* __restrict__ Xh, float2* __restrict__ lnst,
+                      const T* __restrict__ tok, const T* __restrict__ pos,
                       const int32_t* __restrict__ toks, int tok_stride, KfStepGeom g, int d, int V,
                       KfDevState* st) {
   const int r = blockIdx.x;
@@ -41,14 +41,25 @@ __global__ void __launch_bounds__(256)
     if (threadIdx.x == 0) atomicOr(&st->err, 1);
     t = 0;
   }
-  float* x = X + ((size_t)b * g.R + i) * d;
+  const size_t row = (size_t)b * g.R + i;
+  float* x = X + row * d;
   const T* te = tok + (size_t)t * d;
   const T* pe = pos + (size_t)(C + i) * d;
-  T* xh = Xh + ((size_t)b * g.R + i) * d;
-  for (int e = threadIdx.x; e < d; e += blockDim.x) {
-    const float v = to_f(te[e]) + to_f(pe[e]);
-    x[e] = v;
-    if constexpr (sizeof(T) == 2) xh[e] = from_f<T>(v);
+  T* xh = Xh + row * d;
+  // one thread per 16 columns (d <= 2048): the row and its LayerNorm partials
+  const int grp = threadIdx.x;
+  if (grp < d / 16) {
+    float a = 0.f, q = 0.f;
+#pragma unroll
+    for (int c = 0; c < 16; ++c) {
+      const int e = grp * 16 + c;
+      const float v = to_f(te[e]) + to_f(pe[e]);
+      x[e] = v;
+      if constexpr (sizeof(T) == 2) xh[e] = from_f<T>(v);
+      a += v;
+      q += v * v;
+    }
+    lnst[row * (d / 16) + grp] = make_float2(a, q);
   }
 }
 
@@ -451,11 +462,11 @@ inline unsigned grid_for(size_t n, unsigned block) {
 
 // ------------------------------------------------------------ launchers
 template <typename T>
-hipError_t launch_embed_real(float* X, T* Xh, const T* tok, const T* pos, const int32_t* toks,
-                             int tok_stride, KfStepGeom g, int d, int V, KfDevState* st,
-                             hipStream_t s) {
+hipError_t launch_embed_real(float* X, T* Xh, float2* lnst, const T* tok, const T* pos,
+                             const int32_t* toks, int tok_stride, KfStepGeom g, int d, int V,
+                             KfDevState* st, hipStream_t s) {
   if (g.nr <= 0 || g.B <= 0) return hipSuccess;
-  hipLaunchKernelGGL(embed_real_kernel<T>, dim3(g.B * g.nr), dim3(256), 0, s, X, Xh, tok, pos, toks,
+  hipLaunchKernelGGL(embed_real_kernel<T>, dim3(g.B * g.nr), dim3(256), 0, s, X, Xh, lnst, tok, pos, toks,
                      tok_stride, g, d, V, st);
   return hipGetLastError();
 }
@@ -567,8 +578,9 @@ hipError_t launch_copy_f32(const float* src, float* dst, size_t n, hipStream_t s
 hipError_t launch_zero_i32(int* dst, size_t n, hipStream_t s) { return launch_zero<int>(dst, n, s); }
 
 #define KF_INST(T)                                                                                  \
-  template hipError_t launch_embed_real<T>(float*, T*, const T*, const T*, const int32_t*, int,    \
-                                           KfStepGeom, int, int, KfDevState*, hipStream_t);         \
+  template hipError_t launch_embed_real<T>(float*, T*, float2*, const T*, const T*,               \
+                                           const int32_t*, int, KfStepGeom, int, int, KfDevState*, \
+                                           hipStream_t);                                            \
   template hipError_t launch_noise_sinusoid<T>(T*, const float*, uint64_t, const double*,          \
                                                KfStepGeom, int, const KfDevState*, float*,          \
                                                hipStream_t);                                        \

@@ -61,6 +61,7 @@ def test_strerror(L):
     dict(n_layer=0), dict(d_model=100), dict(n_head=3), dict(d_model=256, n_head=1),
     dict(d_mlp=100), dict(vocab=1), dict(n_ctx=100), dict(dtype=7), dict(max_batch=0), dict(max_k=0),
     dict(max_k=1000), dict(max_prompt=0), dict(flags=8),
+    dict(max_batch=65535, max_prompt=128, d_mlp=4096),
 ])
 def test_bad_config_rejected(L, bad):
     cfg = _cfg(**bad)
