@@ -66,25 +66,44 @@ struct Mfma<float> {
 };
 
 // ------------------------------------------------------------ epilogues
-// store4(m, n, v): v holds C[m][n .. n+3] with the bias already added (the
-// kernel loads each lane's bias columns before its K loop); N is a multiple
-// of 4.  Epilogues that write the residual stream (kStats) return the four
-// values written and name their stream row (srow); the kernel then writes the
-// LayerNorm partial sums of every 16-column group of that row to lnst
-// [rows][ldx / 16] as (sum x, sum x^2), which the next LayerNorm-folded GEMM
-// reads instead of recomputing row statistics.
-
-// Four consecutive values to T memory in one store.
+// store8(m, n, v): v holds C[m][n .. n+7] with the bias (and a folded
+// LayerNorm) already applied; n is a multiple of 8.  The kernel stages each
+// tile through LDS so that consecutive lanes store consecutive 8-column chunks
+// of a row.  Epilogues that write the residual stream (kStats) leave in v the
+// eight values written and name their stream row (srow); the kernel then
+// writes the LayerNorm partial sums of every 16-column group of that row to
+// lnst [rows][cols() / 16] as (sum x, sum x^2), which the next
+// LayerNorm-folded GEMM reads instead of recomputing row statistics.
+// Eight consecutive values to T memory (16-byte aligned for bf16: one store).
 template <typename T>
-__device__ inline void put4(T* p, float a, float b, float c, float d) {
+__device__ inline void put8(T* p, const float (&v)[8]) {
   if constexpr (sizeof(T) == 2) {
-    const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (bf16)a) |
-                        ((uint32_t)__builtin_bit_cast(uint16_t, (bf16)b) << 16);
-    const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (bf16)c) |
-                        ((uint32_t)__builtin_bit_cast(uint16_t, (bf16)d) << 16);
-    *reinterpret_cast<uint2*>(p) = make_uint2(lo, hi);
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      w[i] = (uint32_t)__builtin_bit_cast(uint16_t, (bf16)v[2 * i]) |
+             ((uint32_t)__builtin_bit_cast(uint16_t, (bf16)v[2 * i + 1]) << 16);
+    *reinterpret_cast<uint4*>(p) = make_uint4(w[0], w[1], w[2], w[3]);
   } else {
-    *reinterpret_cast<float4*>(p) = make_float4(a, b, c, d);
+    reinterpret_cast<float4*>(p)[0] = make_float4(v[0], v[1], v[2], v[3]);
+    reinterpret_cast<float4*>(p)[1] = make_float4(v[4], v[5], v[6], v[7]);
+  }
+}
+
+template <typename T>
+__device__ inline void get8(const T* p, float (&v)[8]) {
+  if constexpr (sizeof(T) == 2) {
+    const uint4 q = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = __uint_as_float(w[i] << 16);
+      v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+  } else {
+    const float4 a = reinterpret_cast<const float4*>(p)[0], b = reinterpret_cast<const float4*>(p)[1];
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
   }
 }
 
@@ -95,12 +114,12 @@ struct EpBias {
   const float* bias;
   int gelu;
   static constexpr bool kStats = false;
-  __device__ inline f32x4 store4(int m, int n, f32x4 v) const {
-    float x[4];
+  __device__ inline void store8(int m, int n, float (&v)[8]) const {
+    if (gelu) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) x[i] = gelu ? gelu_f(v[i]) : v[i];
-    put4(out + (size_t)m * ldo + n, x[0], x[1], x[2], x[3]);
-    return v;
+      for (int i = 0; i < 8; ++i) v[i] = gelu_f(v[i]);
+    }
+    put8(out + (size_t)m * ldo + n, v);
   }
 };
 
@@ -117,22 +136,21 @@ struct EpResidual {
   static constexpr bool kStats = true;
   __device__ inline int srow(int m) const { return m; }
   __device__ inline int cols() const { return ldx; }
-  __device__ inline f32x4 store4(int m, int n, f32x4 v) const {
-    float4* p = reinterpret_cast<float4*>(X + (size_t)m * ldx + n);
-    float4 x = *p;
-    x.x += v[0];
-    x.y += v[1];
-    x.z += v[2];
-    x.w += v[3];
-    *p = x;
-    if constexpr (sizeof(T) == 2) put4(Xh + (size_t)m * ldx + n, x.x, x.y, x.z, x.w);
-    return f32x4{x.x, x.y, x.z, x.w};
+  __device__ inline void store8(int m, int n, float (&v)[8]) const {
+    float* p = X + (size_t)m * ldx + n;
+    float x[8];
+    get8(p, x);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] += x[i];
+    put8(p, v);
+    if constexpr (sizeof(T) == 2) put8(Xh + (size_t)m * ldx + n, v);
   }
 };
 
 // QKV projection: q goes to Q [M][d]; k and v of row (b, i) go straight into
 // the KV cache slot C + i of sequence b (the KV append of the step).  Keys are
-// stored [slot][d_head] and values transposed, [d_head][slot], per head.
+// stored [slot][d_head] and values transposed, [d_head][slot], per head.  An
+// 8-column chunk never straddles q/k/v or two heads (d_head >= 32).
 template <typename T>
 struct EpQKV {
   T* Q;
@@ -143,24 +161,23 @@ struct EpQKV {
   KfKvGeom kg;
   int layer;
   static constexpr bool kStats = false;
-  __device__ inline f32x4 store4(int m, int n, f32x4 v) const {
+  __device__ inline void store8(int m, int n, float (&v)[8]) const {
     const int d = kg.H * kg.dh;
     const int which = n / d, c = n - which * d;
     if (which == 0) {
-      put4(Q + (size_t)m * d + c, v[0], v[1], v[2], v[3]);
-      return v;
+      put8(Q + (size_t)m * d + c, v);
+      return;
     }
     const int b = m / g.R, i = m - b * g.R;
     const int h = c / kg.dh, e = c - h * kg.dh;
     const int slot = st->C + i;
     T* base = kv + (size_t)b * kg.seq_stride() + kg.head_off(layer, which - 1, h);
     if (which == 1) {  // keys: [slot][dh]
-      put4(base + (size_t)slot * kg.dh + e, v[0], v[1], v[2], v[3]);
+      put8(base + (size_t)slot * kg.dh + e, v);
     } else {           // values, transposed: [dh][slot]
 #pragma unroll
-      for (int r = 0; r < 4; ++r) base[(size_t)(e + r) * kg.T + slot] = from_f<T>(v[r]);
+      for (int r = 0; r < 8; ++r) base[(size_t)(e + r) * kg.T + slot] = from_f<T>(v[r]);
     }
-    return v;
   }
 };
 
@@ -182,17 +199,15 @@ struct EpNoiseOut {
     const int b = m / g.k;
     return b * g.R + g.nr + (m - b * g.k);
   }
-  __device__ inline f32x4 store4(int m, int n, f32x4 v) const {
-    const int j = m % g.k;
-    const int p = st->C + g.nr + j;
+  __device__ inline void store8(int m, int n, float (&v)[8]) const {
+    const int p = st->C + g.nr + m % g.k;
     const size_t row = (size_t)srow(m);
-    const T* pe = pos + (size_t)p * d + n;
-    float x[4];
+    float pe[8];
+    get8(pos + (size_t)p * d + n, pe);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) x[i] = v[i] + to_f(pe[i]);
-    *reinterpret_cast<float4*>(X + row * d + n) = make_float4(x[0], x[1], x[2], x[3]);
-    if constexpr (sizeof(T) == 2) put4(Xh + row * d + n, x[0], x[1], x[2], x[3]);
-    return f32x4{x[0], x[1], x[2], x[3]};
+    for (int i = 0; i < 8; ++i) v[i] += pe[i];
+    put8(X + row * d + n, v);
+    if constexpr (sizeof(T) == 2) put8(Xh + row * d + n, v);
   }
 };
 
@@ -330,7 +345,8 @@ __global__ void __launch_bounds__(256)
   static_assert(WM * WN == 4, "four wavefronts");
   static_assert(MW % 16 == 0 && NW % 16 == 0, "16x16 MFMA tiles");
   static_assert(BM % 32 == 0 && BN % 32 == 0, "whole DMA instructions per wavefront");
-  static_assert(S >= 2 && S <= 4, "ring depth");
+  static_assert(S >= 2 && S <= 8, "ring depth");
+  static_assert((S - 1) * (BM / 32 + BN / 32) < 64, "vmcnt range");
 
   __shared__ u32x4 sbuf[S][(BM + BN) * KCH];
   __shared__ float2 sStat[NORM ? BM : 1];
@@ -528,27 +544,60 @@ __global__ void __launch_bounds__(256)
   };
 
   if constexpr (!IsHead<Ep>::value) {
+    // Stores through LDS: one wavefront row band (MW rows) at a time is
+    // written to the free ring as fp32 rows padded by 16 bytes (the 16 lanes
+    // of a column write then hit distinct banks) and read back as 8-column
+    // row chunks, consecutive lanes taking consecutive chunks.
+    constexpr int SROW = BN + 4;  // fp32 words per staged row
+    constexpr int CPR = BN / 8;   // chunks per row
+    static_assert(MW * SROW * 4 <= S * (BM + BN) * KCH * 16, "staging fits the ring");
+    static_assert((MW * CPR) % 64 == 0, "whole wavefronts per chunk pass");
+    float* stage = reinterpret_cast<float*>(&sbuf[0][0]);
+    __syncthreads();  // every wavefront is done reading the ring
 #pragma unroll
-    for (int tn = 0; tn < TN; ++tn)
+    for (int pass = 0; pass < WM; ++pass) {
+      if (wm == pass) {
 #pragma unroll
-      for (int tm = 0; tm < TM; ++tm) {
-        const int n = n0 + wn * NW + tn * 16 + 4 * (lane >> 4);
-        const int ml = wm * MW + tm * 16 + (lane & 15), m = m0 + ml;
-        const bool live = m < M && n < N;
-        f32x4 x = {0.f, 0.f, 0.f, 0.f};
-        if (live) x = ep.store4(m, n, apply(acc[tn][tm], ml, tn));
-        if constexpr (Ep::kStats) {
-          // the four lane groups hold the 16 columns of this tile's row m
-          float a = x[0] + x[1] + x[2] + x[3];
-          float b = x[0] * x[0] + x[1] * x[1] + x[2] * x[2] + x[3] * x[3];
-          a += __shfl_xor(a, 16, 64);
-          b += __shfl_xor(b, 16, 64);
-          a += __shfl_xor(a, 32, 64);
-          b += __shfl_xor(b, 32, 64);
-          if (live && (lane >> 4) == 0)
-            ep.lnst[(size_t)ep.srow(m) * (ep.cols() / 16) + n / 16] = make_float2(a, b);
+        for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+          for (int tm = 0; tm < TM; ++tm) {
+            const int ml = wm * MW + tm * 16 + (lane & 15);
+            const f32x4 r = apply(acc[tn][tm], ml, tn);
+            float* q = stage + (tm * 16 + (lane & 15)) * SROW + wn * NW + tn * 16 + 4 * (lane >> 4);
+            *reinterpret_cast<float4*>(q) = make_float4(r[0], r[1], r[2], r[3]);
+          }
+      }
+      __syncthreads();
+#pragma unroll
+      for (int c0 = 0; c0 < MW * CPR; c0 += 256) {
+        const int c = c0 + tid;
+        if (c0 + 256 <= MW * CPR || c < MW * CPR) {
+          const int rr = c / CPR, cc = c % CPR;
+          const int m = m0 + pass * MW + rr, n = n0 + cc * 8;
+          const bool live = m < M && n < N;
+          float v[8];
+          const float4 lo = *reinterpret_cast<const float4*>(stage + rr * SROW + cc * 8);
+          const float4 hi = *reinterpret_cast<const float4*>(stage + rr * SROW + cc * 8 + 4);
+          v[0] = lo.x; v[1] = lo.y; v[2] = lo.z; v[3] = lo.w;
+          v[4] = hi.x; v[5] = hi.y; v[6] = hi.z; v[7] = hi.w;
+          if (live) ep.store8(m, n, v);
+          if constexpr (Ep::kStats) {
+            // chunks 2j and 2j + 1 of a row (lanes c, c ^ 1) form 16-column group j
+            float a = 0.f, b = 0.f;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+              a += v[i];
+              b += v[i] * v[i];
+            }
+            a += __shfl_xor(a, 1, 64);
+            b += __shfl_xor(b, 1, 64);
+            if (live && (cc & 1) == 0)
+              ep.lnst[(size_t)ep.srow(m) * (ep.cols() / 16) + n / 16] = make_float2(a, b);
+          }
         }
       }
+      __syncthreads();  // the next band reuses the staging rows
+    }
   } else {
     // Row-wise argmax over this tile's columns: lane-local, then across the
     // four lane groups holding the same row, then across the WN wavefronts.
@@ -735,17 +784,17 @@ hipError_t launch_ln_fold(const T* W, T* Wout, const float* g, const float* beta
 
 #define KF_INST(T)                                                                                 \
   template hipError_t gemm_bias<T>(const T*, const T*, int, int, int, const float*, Act, T*, int, \
-                                   hipStream_t);                                                   \
+                                   hipStream_t);                                 \
   template hipError_t gemm_residual<T>(const T*, const T*, int, int, int, const float*, float*,   \
-                                       T*, float2*, hipStream_t);                                  \
+                                       T*, float2*, hipStream_t);                \
   template hipError_t gemm_noise_out<T>(const T*, const T*, int, int, int, const float*,          \
                                         const T*, float*, T*, float2*, KfStepGeom,                 \
-                                        const KfDevState*, hipStream_t);                           \
+                                        const KfDevState*, hipStream_t);         \
   template hipError_t gemm_qkv_ln<T>(const T*, const LnFold&, const T*, int, int, const float*,   \
                                      T*, T*, KfStepGeom, KfKvGeom, int, const KfDevState*,         \
-                                     hipStream_t);                                                 \
+                                     hipStream_t);                               \
   template hipError_t gemm_up_ln<T>(const T*, const LnFold&, const T*, int, int, int,             \
-                                    const float*, T*, hipStream_t);                                \
+                                    const float*, T*, hipStream_t);              \
   template hipError_t gemm_head_ln<T>(const T*, const LnFold&, const T*, int, int, int, int, int, \
                                       KfStepGeom, float*, int*, float*, hipStream_t);              \
   template hipError_t launch_ln_fold<T>(const T*, T*, const float*, const float*, int, int,       \
