@@ -24,6 +24,13 @@ constexpr int kHeaderInts = 16;
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Attention key-split workspace: partial states for up to 8192 (sequence,
+// head, query row, split) entries (the launcher splits only grids of fewer
+// than 256 workgroups, into at most 512 in total).
+constexpr int kAttnEntries = 8192;
+// Split-K GEMM workspace (fp32 parts of the plain GEMMs of small steps).
+constexpr size_t kSplitBytes = (size_t)8 << 20;
+
 // ------------------------------------------------------------ memory plan
 struct LayerOff {
   size_t ln1_g, ln1_b, wqkv, bqkv, wo, bo, ln2_g, ln2_b, w1, b1, w2, b2;
@@ -44,6 +51,8 @@ struct Plan {
   size_t kv = 0, kv_bytes = 0;
   size_t X = 0, Xh = 0, lnst = 0, A = 0, Q = 0, O = 0, Hm = 0, noise = 0, pval = 0, pidx = 0;
   size_t logits = 0, dstate = 0, pend = 0;
+  size_t att_m = 0, att_l = 0, att_o = 0;  // attention key-split partial states
+  size_t split_part = 0;                   // split-K GEMM parts
   size_t total = 0;
 };
 
@@ -141,6 +150,10 @@ void make_plan(const kf_config& c, Plan& p) {
   p.logits = take((size_t)p.logit_rows * c.vocab * 4);
   p.dstate = take(sizeof(KfDevState));
   p.pend = take((size_t)c.max_batch * c.max_k * 4);
+  p.att_m = take((size_t)kAttnEntries * 4);
+  p.att_l = take((size_t)kAttnEntries * 4);
+  p.att_o = take((size_t)kAttnEntries * (d / c.n_head) * 4);
+  p.split_part = take(kSplitBytes);
   p.total = off;
 }
 
@@ -270,6 +283,10 @@ int run_step(kf_ctx* c, const StepIn& in) {
   float* X = reinterpret_cast<float*>(base + p.X);
   T* Xh = reinterpret_cast<T*>(base + p.Xh);  // compute-dtype residual copy (X itself for fp32)
   float2* lnst = reinterpret_cast<float2*>(base + p.lnst);
+  const kf::AttnSplit asp{reinterpret_cast<float*>(base + p.att_m),
+                          reinterpret_cast<float*>(base + p.att_l),
+                          reinterpret_cast<float*>(base + p.att_o), kAttnEntries, 1};
+  const kf::SplitWs sws{reinterpret_cast<float*>(base + p.split_part), kSplitBytes};
   T* A = reinterpret_cast<T*>(base + p.A);  // noise sinusoid staging
   T* Q = reinterpret_cast<T*>(base + p.Q);
   T* O = reinterpret_cast<T*>(base + p.O);
@@ -297,9 +314,9 @@ int run_step(kf_ctx* c, const StepIn& in) {
                                            reinterpret_cast<const double*>(base + p.omega), g, d,
                                            st, urec, s));
     KF_LAUNCH(c, KF_KC_NOISE,
-              kf::gemm_bias<T>(A, W(p.nw1), Mk, 4 * d, d, F(p.nb1), kf::Act::Gelu, Hm, 4 * d, s));
+              kf::gemm_bias<T>(A, W(p.nw1), Mk, 4 * d, d, F(p.nb1), kf::Act::Gelu, Hm, 4 * d, &sws, s));
     KF_LAUNCH(c, KF_KC_NOISE,
-              kf::gemm_noise_out<T>(Hm, W(p.nw2), Mk, d, 4 * d, F(p.nb2), pos, X, Xh, lnst, g, st, s));
+              kf::gemm_noise_out<T>(Hm, W(p.nw2), Mk, d, 4 * d, F(p.nb2), pos, X, Xh, lnst, g, st, &sws, s));
   }
   for (int l = 0; l < cf.n_layer; ++l) {
     const LayerOff& y = p.layer[l];
@@ -307,10 +324,10 @@ int run_step(kf_ctx* c, const StepIn& in) {
     const kf::LnFold ln2{F(y.up_c1), F(y.up_c2), lnst};
     KF_LAUNCH(c, KF_KC_QKV,
               kf::gemm_qkv_ln<T>(Xh, ln1, W(y.wqkv), M, d, F(y.bqkv), Q, kv, g, kg, l, st, s));
-    KF_LAUNCH(c, KF_KC_ATTN, kf::launch_attention<T>(Q, kv, O, st, g, kg, l, s));
-    KF_LAUNCH(c, KF_KC_OPROJ, kf::gemm_residual<T>(O, W(y.wo), M, d, d, F(y.bo), X, Xh, lnst, s));
+    KF_LAUNCH(c, KF_KC_ATTN, kf::launch_attention<T>(Q, kv, O, st, g, kg, l, asp, s));
+    KF_LAUNCH(c, KF_KC_OPROJ, kf::gemm_residual<T>(O, W(y.wo), M, d, d, F(y.bo), X, Xh, lnst, &sws, s));
     KF_LAUNCH(c, KF_KC_MLP_UP, kf::gemm_up_ln<T>(Xh, ln2, W(y.w1), M, f, d, F(y.b1), Hm, s));
-    KF_LAUNCH(c, KF_KC_MLP_DOWN, kf::gemm_residual<T>(Hm, W(y.w2), M, d, f, F(y.b2), X, Xh, lnst, s));
+    KF_LAUNCH(c, KF_KC_MLP_DOWN, kf::gemm_residual<T>(Hm, W(y.w2), M, d, f, F(y.b2), X, Xh, lnst, &sws, s));
   }
   const bool ar = in.k == 0;
   const int Mh = ar ? in.B : in.B * in.k;

@@ -211,6 +211,19 @@ struct EpNoiseOut {
   }
 };
 
+// One K split of a split-K GEMM: fp32 C rows to part [M][ldp] (the kernel
+// moves part to its split's slice); the bias and the GEMM's real epilogue run
+// in splitk_reduce_kernel.
+struct EpPartial {
+  float* part;
+  int ldp;
+  const float* bias;  // always null: added by the reduction
+  static constexpr bool kStats = false;
+  __device__ inline void store8(int m, int n, float (&v)[8]) const {
+    put8(part + (size_t)m * ldp + n, v);
+  }
+};
+
 // Head: no store; per-tile argmax partials (and optional fp32 logits).
 struct EpHead {
   static constexpr bool kStats = false;
@@ -335,7 +348,8 @@ struct GemmA {
 // BN / 32 W instructions per stage.
 template <typename T, int BM, int BN, int WM, int WN, int S, int MODE, bool NORM, class Ep>
 __global__ void __launch_bounds__(256)
-    gemm_kernel(GemmA ga, const T* __restrict__ W, int ldw, int M, int N, int K, Ep ep) {
+    gemm_kernel(GemmA ga, const T* __restrict__ W, int ldw, int M, int N, int K, Ep ep,
+                int ksplit) {
   constexpr int CH = 16 / (int)sizeof(T);  // elements per 16-byte chunk
   constexpr int BK = KCH * CH;             // K per slab
   constexpr int MW = BM / WM, NW = BN / WN;
@@ -354,10 +368,15 @@ __global__ void __launch_bounds__(256)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   const int gm = (M + BM - 1) / BM, gn = (N + BN - 1) / BN;
+  // ksplit > 1 only with EpPartial: workgroup (tile, split) takes K steps
+  // [split * nk, (split + 1) * nk) and writes its own slice of the parts.
+  const int split = (int)blockIdx.x % ksplit;
   int tmi, tni;
-  tile_coords(blockIdx.x, gm, gn, tmi, tni);
+  tile_coords((int)blockIdx.x / ksplit, gm, gn, tmi, tni);
   const int m0 = tmi * BM, n0 = tni * BN;
-  const int nk = K / BK;
+  const int nk = K / BK / ksplit;
+  const int kbeg = split * nk;
+  if constexpr (std::is_same<Ep, EpPartial>::value) ep.part += (size_t)split * M * ep.ldp;
 
   const T* A = static_cast<const T*>(ga.A);
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(A, (uint32_t)((size_t)ga.arows * ga.lda * sizeof(T)));
@@ -381,7 +400,7 @@ __global__ void __launch_bounds__(256)
     woff[j] = (uint32_t)(((size_t)gr * ldw + c * CH) * sizeof(T));
   }
   auto issue = [&](int stage, int kt) {
-    const uint32_t so = (uint32_t)(kt * BK * (int)sizeof(T));
+    const uint32_t so = (uint32_t)((kbeg + kt) * BK * (int)sizeof(T));
 #pragma unroll
     for (int j = 0; j < PA; ++j) dma16(ra, aoff[j], so, &sbuf[stage][(wave * 8 + 32 * j) * KCH]);
 #pragma unroll
@@ -655,10 +674,78 @@ __global__ void __launch_bounds__(256)
 
 template <typename T, int BM, int BN, int WM, int WN, int S, int MODE, bool NORM, class Ep>
 hipError_t launch_tile(const GemmA& ga, const T* W, int ldw, int M, int N, int K, const Ep& ep,
-                       hipStream_t s) {
+                       hipStream_t s, int ksplit = 1) {
   const int tiles = ((N + BN - 1) / BN) * ((M + BM - 1) / BM);
-  hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN, S, MODE, NORM, Ep>), dim3(tiles), dim3(256),
-                     0, s, ga, W, ldw, M, N, K, ep);
+  hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN, S, MODE, NORM, Ep>), dim3(tiles * ksplit),
+                     dim3(256), 0, s, ga, W, ldw, M, N, K, ep, ksplit);
+  return hipGetLastError();
+}
+
+// Reduction of a split-K GEMM: C = sum of the parts in split order, plus the
+// bias, through the GEMM's epilogue (and its LayerNorm partial sums).  One
+// thread per 8-column chunk of a row.
+template <class Ep>
+__global__ void __launch_bounds__(128)
+    splitk_reduce_kernel(const float* __restrict__ part, int splits, int M, int N, Ep ep) {
+  constexpr int SMAX = 16;
+  const int m = blockIdx.x, c = blockIdx.y * 128 + threadIdx.x, n = c * 8;
+  const bool live = n < N;
+  float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (live) {
+    float x[SMAX][8];
+#pragma unroll
+    for (int sp = 0; sp < SMAX; ++sp)
+      if (sp < splits) get8(part + ((size_t)sp * M + m) * N + n, x[sp]);
+#pragma unroll
+    for (int sp = 0; sp < SMAX; ++sp)
+      if (sp < splits) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] += x[sp][i];
+      }
+    if (ep.bias) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] += ep.bias[n + i];
+    }
+    ep.store8(m, n, v);
+  }
+  if constexpr (Ep::kStats) {
+    float a = 0.f, b = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      a += v[i];
+      b += v[i] * v[i];
+    }
+    a += __shfl_xor(a, 1, 64);
+    b += __shfl_xor(b, 1, 64);
+    if (live && (c & 1) == 0) ep.lnst[(size_t)ep.srow(m) * (ep.cols() / 16) + n / 16] = make_float2(a, b);
+  }
+}
+
+// A GEMM without a folded LayerNorm whose grid cannot fill the chip is run as
+// K splits (up to 16, at least two K steps each, about 320 workgroups in all)
+// into the fp32 workspace, then reduced.
+template <typename T, int BM, int BN, int WM, int WN, int S, class Ep>
+hipError_t launch_plain(const GemmA& ga, const T* W, int M, int N, int K, const Ep& ep,
+                        hipStream_t s, const SplitWs* ws) {
+  const int tiles = ((N + BN - 1) / BN) * ((M + BM - 1) / BM);
+  constexpr int BK = KCH * 16 / (int)sizeof(T);
+  const int nk = K / BK;
+  int ks = 1;
+  if (ws && ws->part && tiles < 128) {
+    for (int c : {16, 12, 8, 6, 4, 3, 2}) {
+      if (nk % c == 0 && nk / c >= 2 && tiles * c <= 320 &&
+          (size_t)c * M * N * sizeof(float) <= ws->bytes) {
+        ks = c;
+        break;
+      }
+    }
+  }
+  if (ks == 1) return launch_tile<T, BM, BN, WM, WN, S, 0, false>(ga, W, K, M, N, K, ep, s);
+  const EpPartial pe{ws->part, N, nullptr};
+  hipError_t e = launch_tile<T, BM, BN, WM, WN, S, 0, false>(ga, W, K, M, N, K, pe, s, ks);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(splitk_reduce_kernel<Ep>, dim3(M, (N / 8 + 127) / 128), dim3(128), 0, s,
+                     ws->part, ks, M, N, ep);
   return hipGetLastError();
 }
 
@@ -666,19 +753,31 @@ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 // Tile choice: the largest tile that still gives about one workgroup per CU.
 template <typename T, int MODE, bool NORM, class Ep>
-hipError_t dispatch(const GemmA& ga, const T* W, int M, int N, int K, const Ep& ep,
-                    hipStream_t s) {
+hipError_t dispatch(const GemmA& ga, const T* W, int M, int N, int K, const Ep& ep, hipStream_t s,
+                    const SplitWs* ws = nullptr) {
   if (M <= 0 || N <= 0) return hipSuccess;
   constexpr int kFill = 256;
-  if (cdiv(M, 128) * cdiv(N, 128) >= kFill)
-    return launch_tile<T, 128, 128, 2, 2, 2, MODE, NORM>(ga, W, K, M, N, K, ep, s);
-  if (cdiv(M, 64) * cdiv(N, 128) >= kFill)
-    return launch_tile<T, 64, 128, 2, 2, 3, MODE, NORM>(ga, W, K, M, N, K, ep, s);
-  if (cdiv(M, 64) * cdiv(N, 64) >= kFill * 3 / 4)
-    return launch_tile<T, 64, 64, 2, 2, 3, MODE, NORM>(ga, W, K, M, N, K, ep, s);
-  if (cdiv(M, 32) * cdiv(N, 64) >= kFill * 3 / 4)
-    return launch_tile<T, 32, 64, 2, 2, 4, MODE, NORM>(ga, W, K, M, N, K, ep, s);
-  return launch_tile<T, 32, 32, 2, 2, 4, MODE, NORM>(ga, W, K, M, N, K, ep, s);
+  if constexpr (!NORM && MODE == 0) {
+    if (cdiv(M, 128) * cdiv(N, 128) >= kFill)
+      return launch_plain<T, 128, 128, 2, 2, 2>(ga, W, M, N, K, ep, s, ws);
+    if (cdiv(M, 64) * cdiv(N, 128) >= kFill)
+      return launch_plain<T, 64, 128, 2, 2, 3>(ga, W, M, N, K, ep, s, ws);
+    if (cdiv(M, 64) * cdiv(N, 64) >= kFill * 3 / 4)
+      return launch_plain<T, 64, 64, 2, 2, 3>(ga, W, M, N, K, ep, s, ws);
+    if (cdiv(M, 32) * cdiv(N, 64) >= kFill * 3 / 4)
+      return launch_plain<T, 32, 64, 2, 2, 4>(ga, W, M, N, K, ep, s, ws);
+    return launch_plain<T, 32, 32, 2, 2, 4>(ga, W, M, N, K, ep, s, ws);
+  } else {
+    if (cdiv(M, 128) * cdiv(N, 128) >= kFill)
+      return launch_tile<T, 128, 128, 2, 2, 2, MODE, NORM>(ga, W, K, M, N, K, ep, s);
+    if (cdiv(M, 64) * cdiv(N, 128) >= kFill)
+      return launch_tile<T, 64, 128, 2, 2, 3, MODE, NORM>(ga, W, K, M, N, K, ep, s);
+    if (cdiv(M, 64) * cdiv(N, 64) >= kFill * 3 / 4)
+      return launch_tile<T, 64, 64, 2, 2, 3, MODE, NORM>(ga, W, K, M, N, K, ep, s);
+    if (cdiv(M, 32) * cdiv(N, 64) >= kFill * 3 / 4)
+      return launch_tile<T, 32, 64, 2, 2, 4, MODE, NORM>(ga, W, K, M, N, K, ep, s);
+    return launch_tile<T, 32, 32, 2, 2, 4, MODE, NORM>(ga, W, K, M, N, K, ep, s);
+  }
 }
 
 // LayerNorm folding at weight load, one wavefront per output row n:
@@ -715,27 +814,27 @@ __global__ void __launch_bounds__(256)
 
 template <typename T>
 hipError_t gemm_bias(const T* A, const T* W, int M, int N, int K, const float* bias, Act act,
-                     T* out, int ldo, hipStream_t s) {
+                     T* out, int ldo, const SplitWs* ws, hipStream_t s) {
   EpBias<T> ep{out, ldo, bias, act == Act::Gelu ? 1 : 0};
   return dispatch<T, 0, false>(GemmA{A, K, M, nullptr, nullptr, nullptr, KfStepGeom{}}, W, M, N, K,
-                               ep, s);
+                               ep, s, ws);
 }
 
 template <typename T>
 hipError_t gemm_residual(const T* A, const T* W, int M, int N, int K, const float* bias, float* X,
-                         T* Xh, float2* lnst, hipStream_t s) {
+                         T* Xh, float2* lnst, const SplitWs* ws, hipStream_t s) {
   EpResidual<T> ep{X, Xh, N, bias, lnst};
   return dispatch<T, 0, false>(GemmA{A, K, M, nullptr, nullptr, nullptr, KfStepGeom{}}, W, M, N, K,
-                               ep, s);
+                               ep, s, ws);
 }
 
 template <typename T>
 hipError_t gemm_noise_out(const T* A, const T* W, int M, int d, int K, const float* bias,
                           const T* pos, float* X, T* Xh, float2* lnst, KfStepGeom g,
-                          const KfDevState* st, hipStream_t s) {
+                          const KfDevState* st, const SplitWs* ws, hipStream_t s) {
   EpNoiseOut<T> ep{X, Xh, bias, pos, st, g, d, lnst};
   return dispatch<T, 0, false>(GemmA{A, K, M, nullptr, nullptr, nullptr, KfStepGeom{}}, W, M, d, K,
-                               ep, s);
+                               ep, s, ws);
 }
 
 template <typename T>
@@ -784,17 +883,17 @@ hipError_t launch_ln_fold(const T* W, T* Wout, const float* g, const float* beta
 
 #define KF_INST(T)                                                                                 \
   template hipError_t gemm_bias<T>(const T*, const T*, int, int, int, const float*, Act, T*, int, \
-                                   hipStream_t);                                 \
+                                   const SplitWs*, hipStream_t);                                   \
   template hipError_t gemm_residual<T>(const T*, const T*, int, int, int, const float*, float*,   \
-                                       T*, float2*, hipStream_t);                \
+                                       T*, float2*, const SplitWs*, hipStream_t);                  \
   template hipError_t gemm_noise_out<T>(const T*, const T*, int, int, int, const float*,          \
                                         const T*, float*, T*, float2*, KfStepGeom,                 \
-                                        const KfDevState*, hipStream_t);         \
+                                        const KfDevState*, const SplitWs*, hipStream_t);           \
   template hipError_t gemm_qkv_ln<T>(const T*, const LnFold&, const T*, int, int, const float*,   \
                                      T*, T*, KfStepGeom, KfKvGeom, int, const KfDevState*,         \
-                                     hipStream_t);                               \
+                                     hipStream_t);                                                 \
   template hipError_t gemm_up_ln<T>(const T*, const LnFold&, const T*, int, int, int,             \
-                                    const float*, T*, hipStream_t);              \
+                                    const float*, T*, hipStream_t);                                \
   template hipError_t gemm_head_ln<T>(const T*, const LnFold&, const T*, int, int, int, int, int, \
                                       KfStepGeom, float*, int*, float*, hipStream_t);              \
   template hipError_t launch_ln_fold<T>(const T*, T*, const float*, const float*, int, int,       \

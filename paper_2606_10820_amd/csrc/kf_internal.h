@@ -74,6 +74,13 @@ namespace kf {
 
 enum class Act { None = 0, Gelu = 1 };
 
+// fp32 workspace of the split-K GEMMs (plain GEMMs whose grids cannot fill the
+// chip run as K splits into it, then a reduction); null part: no split.
+struct SplitWs {
+  float* part;
+  size_t bytes;
+};
+
 // Real-row embedding: X[b*R + i] = tok[toks[b*tok_stride + i]] + pos[C + i], i < nr,
 // with its compute-dtype copy Xh and LayerNorm partial sums lnst (see gemm_residual).
 template <typename T>
@@ -89,15 +96,25 @@ hipError_t launch_noise_sinusoid(T* S, const float* noise, uint64_t seed, const 
                                  KfStepGeom g, int d, const KfDevState* st, float* u_out,
                                  hipStream_t s);
 
+// Key-split workspace of the attention: per (sequence, head, query row, split)
+// entry the running max m, the sum l and the unnormalised output o[d_head]
+// (fp32).  ns is chosen by the launcher (1 = no split).
+struct AttnSplit {
+  float* m;
+  float* l;
+  float* o;
+  int entries;  // capacity in entries
+  int ns;
+};
 // Block attention over the KV cache for every (sequence, head, query block).
 template <typename T>
 hipError_t launch_attention(const T* Q, const T* kv, T* O, const KfDevState* st, KfStepGeom g,
-                            KfKvGeom kg, int layer, hipStream_t s);
+                            KfKvGeom kg, int layer, const AttnSplit& ws, hipStream_t s);
 
 // GEMM family: C = epilogue(A[M][K] . W[N][K]^T), fp32 accumulation.
 template <typename T>
 hipError_t gemm_bias(const T* A, const T* W, int M, int N, int K, const float* bias, Act act,
-                     T* out, int ldo, hipStream_t s);
+                     T* out, int ldo, const SplitWs* ws, hipStream_t s);
 // Residual update X[M][N] += C + bias; with a 16-bit T the updated rows are
 // also written to Xh (the compute-dtype copy of the residual stream; for fp32,
 // Xh aliases X and is not written).  Every writer of the residual stream also
@@ -105,7 +122,7 @@ hipError_t gemm_bias(const T* A, const T* W, int M, int N, int K, const float* b
 // updated row, the input of the next folded LayerNorm.
 template <typename T>
 hipError_t gemm_residual(const T* A, const T* W, int M, int N, int K, const float* bias, float* X,
-                         T* Xh, float2* lnst, hipStream_t s);
+                         T* Xh, float2* lnst, const SplitWs* ws, hipStream_t s);
 // LayerNorm folded into a GEMM whose weights were scaled by the gain at load
 // (W' = W diag(gain)): c1 = W' 1 and c2 = W shift.  A rows come from the
 // compute-dtype residual copy Xh [rows][d]; each row's mean and variance come
@@ -125,7 +142,7 @@ hipError_t gemm_up_ln(const T* Xh, const LnFold& ln, const T* W, int M, int N, i
 template <typename T>
 hipError_t gemm_noise_out(const T* A, const T* W, int M, int d, int K, const float* bias,
                           const T* pos, float* X, T* Xh, float2* lnst, KfStepGeom g,
-                          const KfDevState* st, hipStream_t s);
+                          const KfDevState* st, const SplitWs* ws, hipStream_t s);
 // Head over the final LayerNorm of the selected rows (gather: 1 = noise rows
 // of the step, 2 = last real row per sequence): per (row, 128-column tile) the
 // maximum and its lowest column index into pval/pidx [M][Vpad/128]; columns

@@ -185,8 +185,9 @@ __global__ void __launch_bounds__(256)
 }
 
 // Block attention on MFMA (bf16).  One workgroup per (sequence, head, block of
-// 16 query rows); its four wavefronts take 32-key tiles round-robin and merge
-// their online-softmax states through LDS at the end.
+// 16 query rows, key split); its four wavefronts take 32-key tiles of the
+// split's key range round-robin and merge their online-softmax states through
+// LDS at the end.
 //   S^T = K Q^T   with v_mfma_f32_16x16x32_bf16: A = 16 keys x 32 d_head,
 //                 B = 32 d_head x 16 queries.  MFMA row i of key group grp is
 //                 key 8*(i/4) + 4*grp + i%4 of the tile, so the output rows a
@@ -194,6 +195,11 @@ __global__ void __launch_bounds__(256)
 //   O^T += V^T P^T  A = 16 d_head x 32 keys read straight from the transposed
 //                 value cache (8 consecutive slots = one 16-byte load), B = the
 //                 lane's own 8 probabilities -- no data exchange between lanes.
+// Each wavefront loads the K and V fragments of its next tile before working
+// on the current one.  With ns > 1 key splits (grids too small to fill the
+// chip), every split writes its unnormalised state (max m, sum l, o) for the
+// combine kernel; the split count depends only on the shapes, not on the
+// context length, so a captured step replays unchanged as C grows.
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
@@ -205,17 +211,20 @@ template <int DH>
 __global__ void __launch_bounds__(256)
     attention_mfma_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ kv,
                           bf16* __restrict__ O, const KfDevState* st, KfStepGeom g, KfKvGeom kg,
-                          int layer, float scale) {
+                          int layer, float scale, AttnSplit sp) {
   constexpr int QB = 16, KT = 32, NDC = DH / 32, NDB = DH / 16;
   const int H = kg.H, T = kg.T, d = H * DH;
   const int nqb = (g.R + QB - 1) / QB;
-  const int qb = blockIdx.x % nqb, bh = blockIdx.x / nqb;
+  const int split = blockIdx.x % sp.ns, rest = blockIdx.x / sp.ns;
+  const int qb = rest % nqb, bh = rest / nqb;
   const int b = bh / H, h = bh % H;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int gq = lane >> 4, lq = lane & 15;
   const int C = st->C;
   const int q0 = qb * QB, nq = min(QB, g.R - q0);
   const int nkeys = C + q0 + nq;
+  const int chunk = ((nkeys + sp.ns - 1) / sp.ns + KT - 1) / KT * KT;
+  const int ks = split * chunk, ke = min(nkeys, ks + chunk);
   const bf16* Kb = kv + (size_t)b * kg.seq_stride() + kg.head_off(layer, 0, h);
   const bf16* Vt = kv + (size_t)b * kg.seq_stride() + kg.head_off(layer, 1, h);
 
@@ -231,17 +240,43 @@ __global__ void __launch_bounds__(256)
 #pragma unroll
   for (int i = 0; i < NDB; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  for (int t0 = w * KT; t0 < nkeys; t0 += 4 * KT) {
+  struct Frag {
+    bf16x8_t k[2][NDC];
+    bf16x8_t v[NDB];
+  };
+  // K rows past the end read the last key (then zeroed); value slots past the
+  // end are zeroed (their probability is 0, and 0 * a stale NaN would not be).
+  auto load = [&](int t0, Frag& f) {
+#pragma unroll
+    for (int grp = 0; grp < 2; ++grp) {
+      const int key = t0 + 8 * (lq >> 2) + 4 * grp + (lq & 3);
+      const int kc = key < nkeys ? key : nkeys - 1;
+#pragma unroll
+      for (int c = 0; c < NDC; ++c) {
+        const bf16x8_t x = load8(Kb + (size_t)kc * DH + c * 32 + 8 * gq);
+        f.k[grp][c] = key < nkeys ? x : zero8;
+      }
+    }
+    const int kb = t0 + 8 * gq;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      const bf16* vp = Vt + (size_t)(db * 16 + lq) * T + kb;
+      if (kb + 8 <= nkeys) {
+        f.v[db] = load8(vp);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) f.v[db][e] = (kb + e < nkeys) ? vp[e] : (bf16)0.f;
+      }
+    }
+  };
+  auto tile = [&](int t0, const Frag& f) {
     f32x4_t s[2];
 #pragma unroll
     for (int grp = 0; grp < 2; ++grp) {
-      const int key = t0 + 8 * (lq >> 2) + 4 * grp + (lq & 3);  // MFMA row lq of group grp
       s[grp] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int c = 0; c < NDC; ++c) {
-        bf16x8_t kf = key < nkeys ? load8(Kb + (size_t)key * DH + c * 32 + 8 * gq) : zero8;
-        s[grp] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[c], s[grp], 0, 0, 0);
-      }
+      for (int c = 0; c < NDC; ++c)
+        s[grp] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.k[grp][c], qf[c], s[grp], 0, 0, 0);
     }
     // this lane: query lq, keys t0 + 8*gq + 4*grp + r
     float p[8];
@@ -272,20 +307,26 @@ __global__ void __launch_bounds__(256)
     psum += __shfl_xor(psum, 32, 64);
     l_run = l_run * alpha + psum;
     m_run = m_new;
-    const int kb = t0 + 8 * gq;
 #pragma unroll
     for (int db = 0; db < NDB; ++db) {
-      const bf16* vp = Vt + (size_t)(db * 16 + lq) * T + kb;
-      bf16x8_t vf;
-      if (kb + 8 <= nkeys) {
-        vf = load8(vp);
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) vf[e] = (kb + e < nkeys) ? vp[e] : (bf16)0.f;
-      }
       o[db] *= alpha;
-      o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[db], 0, 0, 0);
+      o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.v[db], pf, o[db], 0, 0, 0);
     }
+  };
+
+  Frag fa, fb;
+  int t0 = ks + w * KT;
+  if (t0 < ke) load(t0, fa);
+  while (t0 < ke) {  // ping-pong: the next tile loads while this one computes
+    int tn = t0 + 4 * KT;
+    if (tn < ke) load(tn, fb);
+    tile(t0, fa);
+    t0 = tn;
+    if (t0 >= ke) break;
+    tn = t0 + 4 * KT;
+    if (tn < ke) load(tn, fa);
+    tile(t0, fb);
+    t0 = tn;
   }
 
   // merge the four wavefronts' partial states
@@ -312,16 +353,64 @@ __global__ void __launch_bounds__(256)
       f[i] = (sm[i][q] == -INFINITY) ? 0.f : __expf(sm[i][q] - M);
       den += f[i] * sl[i][q];
     }
-    const float inv = 1.0f / den;
-    bf16* orow = O + ((size_t)b * g.R + q0 + q) * d + h * DH + e0;
+    if (sp.ns == 1) {
+      const float inv = 1.0f / den;
+      bf16* orow = O + ((size_t)b * g.R + q0 + q) * d + h * DH + e0;
 #pragma unroll
-    for (int e = 0; e < EPT; ++e) {
-      float acc = 0.f;
+      for (int e = 0; e < EPT; ++e) {
+        float acc = 0.f;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) acc += f[i] * so[i][q][e0 + e];
-      orow[e] = (bf16)(acc * inv);
+        for (int i = 0; i < 4; ++i) acc += f[i] * so[i][q][e0 + e];
+        orow[e] = (bf16)(acc * inv);
+      }
+    } else {
+      const size_t ent = (((size_t)b * H + h) * g.R + q0 + q) * sp.ns + split;
+      if (e0 == 0) {
+        sp.m[ent] = M;
+        sp.l[ent] = den;
+      }
+      float* orow = sp.o + ent * DH + e0;
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) {
+        float acc = 0.f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc += f[i] * so[i][q][e0 + e];
+        orow[e] = acc;
+      }
     }
   }
+}
+
+// Merge of the key splits: O = sum_s f_s o_s / sum_s f_s l_s with
+// f_s = exp(m_s - max m), splits taken in order.  One block of DH threads per
+// (query row, head); the split loop is unrolled to its bound (16) so that all
+// loads are in flight together.
+template <int DH>
+__global__ void __launch_bounds__(DH)
+    attention_combine_kernel(bf16* __restrict__ O, KfStepGeom g, int H, AttnSplit sp) {
+  constexpr int NSMAX = 16;
+  const int h = blockIdx.x % H, row = blockIdx.x / H;
+  const int b = row / g.R, i = row - b * g.R, e = threadIdx.x;
+  const size_t base = (((size_t)b * H + h) * g.R + i) * sp.ns;
+  float ms[NSMAX], ls[NSMAX], os[NSMAX];
+#pragma unroll
+  for (int s = 0; s < NSMAX; ++s) {
+    const bool on = s < sp.ns;
+    ms[s] = on ? sp.m[base + s] : -INFINITY;
+    ls[s] = on ? sp.l[base + s] : 0.f;
+    os[s] = on ? sp.o[(base + s) * DH + e] : 0.f;
+  }
+  float M = -INFINITY;
+#pragma unroll
+  for (int s = 0; s < NSMAX; ++s) M = fmaxf(M, ms[s]);
+  float den = 0.f, acc = 0.f;
+#pragma unroll
+  for (int s = 0; s < NSMAX; ++s) {
+    const float f = ms[s] == -INFINITY ? 0.f : __expf(ms[s] - M);
+    den += f * ls[s];
+    acc += f * os[s];
+  }
+  O[(size_t)row * H * DH + h * DH + e] = (bf16)(acc / den);
 }
 
 // ------------------------------------------------------- token selection
@@ -483,23 +572,45 @@ hipError_t launch_noise_sinusoid(T* S, const float* noise, uint64_t seed, const 
 
 template <typename T>
 hipError_t launch_attention(const T* Q, const T* kv, T* O, const KfDevState* st, KfStepGeom g,
-                            KfKvGeom kg, int layer, hipStream_t s) {
+                            KfKvGeom kg, int layer, const AttnSplit& ws, hipStream_t s) {
   if (g.B <= 0 || g.R <= 0) return hipSuccess;
   const float scale = 1.0f / sqrtf((float)kg.dh);
   if constexpr (sizeof(T) == 2) {
-    dim3 grid(g.B * kg.H * ((g.R + 15) / 16));
+    // key splits: enough workgroups for ~512 in flight, each split at least
+    // 128 keys of the full context, within the partial-state workspace
+    const int base = g.B * kg.H * ((g.R + 15) / 16);
+    int ns = 1;
+    if (ws.o && base < 256) {
+      ns = 512 / base;
+      ns = ns < kg.T / 128 ? ns : kg.T / 128;
+      ns = ns < 16 ? ns : 16;
+      while (ns > 1 && (long long)g.B * kg.H * g.R * ns > ws.entries) --ns;
+      if (ns < 1) ns = 1;
+    }
+    AttnSplit sp = ws;
+    sp.ns = ns;
+    dim3 grid(base * ns);
     switch (kg.dh) {
       case 32:
         hipLaunchKernelGGL(attention_mfma_kernel<32>, grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
-                           layer, scale);
+                           layer, scale, sp);
+        if (ns > 1)
+          hipLaunchKernelGGL(attention_combine_kernel<32>, dim3(g.B * g.R * kg.H), dim3(32), 0, s,
+                             O, g, kg.H, sp);
         break;
       case 64:
         hipLaunchKernelGGL(attention_mfma_kernel<64>, grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
-                           layer, scale);
+                           layer, scale, sp);
+        if (ns > 1)
+          hipLaunchKernelGGL(attention_combine_kernel<64>, dim3(g.B * g.R * kg.H), dim3(64), 0, s,
+                             O, g, kg.H, sp);
         break;
       case 128:
         hipLaunchKernelGGL(attention_mfma_kernel<128>, grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
-                           layer, scale);
+                           layer, scale, sp);
+        if (ns > 1)
+          hipLaunchKernelGGL(attention_combine_kernel<128>, dim3(g.B * g.R * kg.H), dim3(128), 0, s,
+                             O, g, kg.H, sp);
         break;
       default:
         return hipErrorInvalidValue;
@@ -585,7 +696,7 @@ hipError_t launch_zero_i32(int* dst, size_t n, hipStream_t s) { return launch_ze
                                                KfStepGeom, int, const KfDevState*, float*,          \
                                                hipStream_t);                                        \
   template hipError_t launch_attention<T>(const T*, const T*, T*, const KfDevState*, KfStepGeom,   \
-                                          KfKvGeom, int, hipStream_t);                              \
+                                          KfKvGeom, int, const AttnSplit&, hipStream_t);            \
   template hipError_t launch_convert<T>(const float*, T*, size_t, hipStream_t);                    \
   template hipError_t launch_zero<T>(T*, size_t, hipStream_t);
 KF_INST(float)
