@@ -120,6 +120,8 @@ def parse():
     ap.add_argument("--summarize", metavar="DIR", default=None,
                     help="print a markdown summary of rocprofv3 CSV output under DIR "
                          "(kernel stats, and FETCH_SIZE / WRITE_SIZE counter runs) and exit")
+    ap.add_argument("--write-traffic", metavar="JSON", default=None,
+                    help="with --summarize: also store the per-class traffic for bench.py")
     return ap.parse_args()
 
 
@@ -159,8 +161,53 @@ def _short(name: str) -> str:
     return n.split("(")[0]
 
 
-def summarize(root: str) -> None:
-    """Markdown summary of rocprofv3 --stats / --pmc CSV output (no GPU needed)."""
+KERNEL_SOURCES = os.path.join(ROOT, "paper_2606_10820_amd", "csrc")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_lm1b_b64_k4.json")
+
+
+def kernel_source_hash() -> str:
+    """sha256 over the library's kernel sources: counter figures taken from an
+    older build are not reported."""
+    import hashlib
+    h = hashlib.sha256()
+    for fn in sorted(os.listdir(KERNEL_SOURCES)):
+        with open(os.path.join(KERNEL_SOURCES, fn), "rb") as f:
+            h.update(fn.encode() + b"\0" + f.read())
+    return h.hexdigest()
+
+
+def kernel_class(name: str, state: dict):
+    """Kernel class of one dispatch, from its name and the launch order of a
+    step: out-proj and MLP-down share one GEMM instantiation and alternate;
+    a split-K part belongs to the reduction that follows it."""
+    if "embed_real_kernel" in name:
+        return "embed"
+    if "noise_sinusoid_kernel" in name or "EpNoiseOut" in name:
+        return "noise"
+    if "attention_mfma_kernel" in name or "attention_combine_kernel" in name:
+        return "attn"
+    if "EpQKV" in name:
+        return "qkv"
+    if "EpHead" in name:
+        return "head"
+    if any(k in name for k in ("argmax_select_kernel", "icdf_select_kernel", "commit_kernel")):
+        return "select"
+    if "EpPartial" in name:
+        return "pending"
+    if "EpResidual" in name:
+        if "splitk_reduce" in name or "gemm_kernel" in name:
+            role = "oproj" if state.get("residual", 0) % 2 == 0 else "mlp_down"
+            state["residual"] = state.get("residual", 0) + 1
+            return role
+    if "EpBias" in name:
+        return "mlp_up" if "Lb1E" in name else "noise"
+    return None
+
+
+def summarize(root: str, write_json: str = None) -> None:
+    """Markdown summary of rocprofv3 --stats / --pmc CSV output (no GPU needed),
+    with HBM traffic per kernel class; write_json stores the per-launch class
+    traffic for bench.py."""
     import csv
     import glob
     stats = glob.glob(os.path.join(root, "**", "*_kernel_stats.csv"), recursive=True)
@@ -173,11 +220,13 @@ def summarize(root: str) -> None:
             print(f"| {_short(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
                   f"{float(r['MinNs']) / 1e3:.2f} | {float(r['TotalDurationNs']) / tot * 100:.1f}% |")
         print()
-    pmc = {}
+    pmc, seq = {}, {}
     for path in glob.glob(os.path.join(root, "**", "*_counter_collection.csv"), recursive=True):
         for r in csv.DictReader(open(path)):
             key = (_short(r["Kernel_Name"]), int(r["Grid_Size"]))
             pmc.setdefault(r["Counter_Name"], {}).setdefault(key, []).append(float(r["Counter_Value"]))
+            seq.setdefault(r["Counter_Name"], []).append(
+                (int(r["Dispatch_Id"]), r["Kernel_Name"], float(r["Counter_Value"])))
     if not pmc:
         return
     # calibration: fp32 -> bf16 weight conversion of the token table reads 4n, writes 2n bytes
@@ -203,6 +252,57 @@ def summarize(root: str) -> None:
         wm = np.mean(wv) if wv else float("nan")
         print(f"| {k[0]} | {k[1]} | {len(fv or wv)} | {fm:.1f} | {wm:.1f} | "
               f"{fm * 1024 * (f_scale or 1) / 1e6:.2f} | {wm * 1024 * (w_scale or 1) / 1e6:.2f} |")
+    # per kernel class: scaled bytes per class launch (a class launch may run a
+    # helper kernel too: split-K reduction, attention combine)
+    cls = {}
+    for counter, scale in (("FETCH_SIZE", f_scale), ("WRITE_SIZE", w_scale)):
+        state, pending = {}, 0.0
+        for _, name, v in sorted(seq.get(counter, [])):
+            c = kernel_class(name, state)
+            b = v * 1024 * (scale or 1.0)
+            if c is None:
+                continue
+            if c == "pending":
+                pending += b
+                continue
+            e = cls.setdefault(c, {"launches": {}, "bytes": {}})
+            e["bytes"][counter] = e["bytes"].get(counter, 0.0) + b + pending
+            pending = 0.0
+            helper = "attention_combine" in name or "splitk_reduce" in name
+            if not helper:
+                e["launches"][counter] = e["launches"].get(counter, 0) + 1
+    print("\n| class | launches | MB read / launch | MB written / launch |\n|---|---|---|---|")
+    out = {}
+    for c, e in sorted(cls.items()):
+        n = e["launches"].get("FETCH_SIZE") or e["launches"].get("WRITE_SIZE") or 1
+        rd = e["bytes"].get("FETCH_SIZE", float("nan")) / n
+        wr = e["bytes"].get("WRITE_SIZE", float("nan")) / max(e["launches"].get("WRITE_SIZE", n), 1)
+        print(f"| {c} | {n} | {rd / 1e6:.2f} | {wr / 1e6:.2f} |")
+        out[c] = {"launches": n, "read_bytes_per_launch": rd, "write_bytes_per_launch": wr}
+    if write_json:
+        with open(write_json, "w") as f:
+            json.dump({"workload": "lm1b B=64 k=4 (bench.py defaults)",
+                       "source_sha256": kernel_source_hash(),
+                       "calibration": {"kernel": cal[0] if cal else None,
+                                       "fetch_scale": f_scale, "write_scale": w_scale},
+                       "classes": out}, f, indent=1)
+            f.write("\n")
+
+
+def load_traffic(dom: str, workload: str, B: int, k: int):
+    """Per-launch HBM bytes of class dom from the committed counter summary,
+    or None when the summary is for another workload or an older build."""
+    if workload != "lm1b" or B != S.WORKLOADS["lm1b"]["B"] or k != S.WORKLOADS["lm1b"]["k"]:
+        return None
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("source_sha256") != kernel_source_hash() or dom not in t.get("classes", {}):
+        return None
+    c = t["classes"][dom]
+    return c["read_bytes_per_launch"] + c["write_bytes_per_launch"]
 
 
 def step_roof_ms(costs, dtype) -> float:
@@ -283,7 +383,7 @@ def owt_sweep(batches, stream):
 def main():
     a = parse()
     if a.summarize:
-        summarize(a.summarize)
+        summarize(a.summarize, a.write_traffic)
         return
     if a.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {a.gpus}); the decode path "
@@ -363,7 +463,9 @@ def main():
         roof = {"bound": "hbm", "achieved": by / (dom_ms * 1e-3) / 1e9, "peak": PEAK_HBM_GBS,
                 "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = None
+    # HBM bytes per launch of the class from rocprofv3 FETCH_SIZE / WRITE_SIZE
+    # (calibrated), when taken on this build of the kernels
+    roof["traffic"] = load_traffic(dom, a.workload, B, k)
     roof["kernel_class"] = dom
     roof["launches"] = dom_n
     roof["avg_launch_us"] = dom_ms * 1e3 / max(dom_n, 1)
