@@ -676,7 +676,7 @@ template <typename T, int BM, int BN, int WM, int WN, int S, int MODE, bool NORM
 hipError_t launch_tile(const GemmA& ga, const T* W, int ldw, int M, int N, int K, const Ep& ep,
                        hipStream_t s, int ksplit = 1) {
   const int tiles = ((N + BN - 1) / BN) * ((M + BM - 1) / BM);
-  hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN, S, MODE, NORM, Ep>), dim3(tiles * ksplit),
+  launch((gemm_kernel<T, BM, BN, WM, WN, S, MODE, NORM, Ep>), dim3(tiles * ksplit),
                      dim3(256), 0, s, ga, W, ldw, M, N, K, ep, ksplit);
   return hipGetLastError();
 }
@@ -744,7 +744,7 @@ hipError_t launch_plain(const GemmA& ga, const T* W, int M, int N, int K, const 
   const EpPartial pe{ws->part, N, nullptr};
   hipError_t e = launch_tile<T, BM, BN, WM, WN, S, 0, false>(ga, W, K, M, N, K, pe, s, ks);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(splitk_reduce_kernel<Ep>, dim3(M, (N / 8 + 127) / 128), dim3(128), 0, s,
+  launch(splitk_reduce_kernel<Ep>, dim3(M, (N / 8 + 127) / 128), dim3(128), 0, s,
                      ws->part, ks, M, N, ep);
   return hipGetLastError();
 }
@@ -876,7 +876,7 @@ template <typename T>
 hipError_t launch_ln_fold(const T* W, T* Wout, const float* g, const float* beta, int N, int K,
                           float* c1, float* c2, hipStream_t s) {
   if (N <= 0) return hipSuccess;
-  hipLaunchKernelGGL(ln_fold_kernel<T>, dim3((N + 3) / 4), dim3(256), 0, s, W, Wout, g, beta, N, K,
+  launch(ln_fold_kernel<T>, dim3((N + 3) / 4), dim3(256), 0, s, W, Wout, g, beta, N, K,
                      c1, c2);
   return hipGetLastError();
 }

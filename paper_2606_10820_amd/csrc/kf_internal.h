@@ -1,6 +1,7 @@
 // kf_internal.h -- internal declarations shared by the library's HIP sources.
 // Not part of the public ABI (include/kforcing.h is).
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -71,6 +72,27 @@ __host__ __device__ inline float kf_noise_u(uint64_t seed, int b, int p) {
 // ------------------------------------------------------------ launchers
 // All return hipGetLastError() of their launch (hipSuccess when nothing ran).
 namespace kf {
+
+// Kernel timing.  While a kernel class is being timed the host points
+// launch_timer at an event pair: the first kernel of the launcher records
+// `start` on its own dispatch and every kernel records `stop`, so the interval
+// is exactly the launcher's kernels (no event packets between them).
+struct LaunchTimer {
+  hipEvent_t start, stop;
+  bool started;
+};
+extern thread_local LaunchTimer* launch_timer;
+
+template <typename F, typename... Args>
+inline void launch(F kernel, dim3 grid, dim3 block, uint32_t shmem, hipStream_t s, Args... args) {
+  if (LaunchTimer* t = launch_timer) {
+    hipExtLaunchKernelGGL(kernel, grid, block, shmem, s, t->started ? nullptr : t->start, t->stop,
+                          0u, args...);
+    t->started = true;
+  } else {
+    hipLaunchKernelGGL(kernel, grid, block, shmem, s, args...);
+  }
+}
 
 enum class Act { None = 0, Gelu = 1 };
 

@@ -555,7 +555,7 @@ hipError_t launch_embed_real(float* X, T* Xh, float2* lnst, const T* tok, const 
                              const int32_t* toks, int tok_stride, KfStepGeom g, int d, int V,
                              KfDevState* st, hipStream_t s) {
   if (g.nr <= 0 || g.B <= 0) return hipSuccess;
-  hipLaunchKernelGGL(embed_real_kernel<T>, dim3(g.B * g.nr), dim3(256), 0, s, X, Xh, lnst, tok, pos, toks,
+  launch(embed_real_kernel<T>, dim3(g.B * g.nr), dim3(256), 0, s, X, Xh, lnst, tok, pos, toks,
                      tok_stride, g, d, V, st);
   return hipGetLastError();
 }
@@ -565,7 +565,7 @@ hipError_t launch_noise_sinusoid(T* S, const float* noise, uint64_t seed, const 
                                  KfStepGeom g, int d, const KfDevState* st, float* u_out,
                                  hipStream_t s) {
   if (g.k <= 0 || g.B <= 0) return hipSuccess;
-  hipLaunchKernelGGL(noise_sinusoid_kernel<T>, dim3(g.B * g.k), dim3(256), 0, s, S, noise, seed,
+  launch(noise_sinusoid_kernel<T>, dim3(g.B * g.k), dim3(256), 0, s, S, noise, seed,
                      omega, g, d, st, u_out);
   return hipGetLastError();
 }
@@ -592,24 +592,24 @@ hipError_t launch_attention(const T* Q, const T* kv, T* O, const KfDevState* st,
     dim3 grid(base * ns);
     switch (kg.dh) {
       case 32:
-        hipLaunchKernelGGL(attention_mfma_kernel<32>, grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
+        launch(attention_mfma_kernel<32>, grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
                            layer, scale, sp);
         if (ns > 1)
-          hipLaunchKernelGGL(attention_combine_kernel<32>, dim3(g.B * g.R * kg.H), dim3(32), 0, s,
+          launch(attention_combine_kernel<32>, dim3(g.B * g.R * kg.H), dim3(32), 0, s,
                              O, g, kg.H, sp);
         break;
       case 64:
-        hipLaunchKernelGGL(attention_mfma_kernel<64>, grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
+        launch(attention_mfma_kernel<64>, grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
                            layer, scale, sp);
         if (ns > 1)
-          hipLaunchKernelGGL(attention_combine_kernel<64>, dim3(g.B * g.R * kg.H), dim3(64), 0, s,
+          launch(attention_combine_kernel<64>, dim3(g.B * g.R * kg.H), dim3(64), 0, s,
                              O, g, kg.H, sp);
         break;
       case 128:
-        hipLaunchKernelGGL(attention_mfma_kernel<128>, grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
+        launch(attention_mfma_kernel<128>, grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
                            layer, scale, sp);
         if (ns > 1)
-          hipLaunchKernelGGL(attention_combine_kernel<128>, dim3(g.B * g.R * kg.H), dim3(128), 0, s,
+          launch(attention_combine_kernel<128>, dim3(g.B * g.R * kg.H), dim3(128), 0, s,
                              O, g, kg.H, sp);
         break;
       default:
@@ -620,15 +620,15 @@ hipError_t launch_attention(const T* Q, const T* kv, T* O, const KfDevState* st,
   dim3 grid(g.B * kg.H, (g.R + 15) / 16);
   switch (kg.dh) {
     case 32:
-      hipLaunchKernelGGL((attention_kernel<T, 32>), grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
+      launch((attention_kernel<T, 32>), grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
                          layer, scale);
       break;
     case 64:
-      hipLaunchKernelGGL((attention_kernel<T, 64>), grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
+      launch((attention_kernel<T, 64>), grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
                          layer, scale);
       break;
     case 128:
-      hipLaunchKernelGGL((attention_kernel<T, 128>), grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
+      launch((attention_kernel<T, 128>), grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
                          layer, scale);
       break;
     default:
@@ -641,7 +641,7 @@ hipError_t launch_argmax_select(const float* pval, const int* pidx, int n_tiles,
                                 const KfDevState* st, KfOutDesc od, hipStream_t s) {
   int rows = g.B * g.k;
   if (rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(argmax_select_kernel, dim3((rows + 3) / 4), dim3(256), 0, s, pval, pidx,
+  launch(argmax_select_kernel, dim3((rows + 3) / 4), dim3(256), 0, s, pval, pidx,
                      n_tiles, g, st, od);
   return hipGetLastError();
 }
@@ -649,19 +649,19 @@ hipError_t launch_argmax_select(const float* pval, const int* pidx, int n_tiles,
 hipError_t launch_icdf_select(const float* logits, int V, const float* u_in, uint64_t seed,
                               KfStepGeom g, const KfDevState* st, KfOutDesc od, hipStream_t s) {
   if (g.B <= 0) return hipSuccess;
-  hipLaunchKernelGGL(icdf_select_kernel, dim3(g.B), dim3(1024), 0, s, logits, V, u_in, seed, g, st,
+  launch(icdf_select_kernel, dim3(g.B), dim3(1024), 0, s, logits, V, u_in, seed, g, st,
                      od);
   return hipGetLastError();
 }
 
 hipError_t launch_commit(KfDevState* st, int nr, hipStream_t s) {
-  hipLaunchKernelGGL(commit_kernel, dim3(1), dim3(64), 0, s, st, nr);
+  launch(commit_kernel, dim3(1), dim3(64), 0, s, st, nr);
   return hipGetLastError();
 }
 
 hipError_t launch_fill_noise(float* out, uint64_t seed, int B, int p0, int n, hipStream_t s) {
   if (B <= 0 || n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(fill_noise_kernel, dim3((B * n + 255) / 256), dim3(256), 0, s, out, seed, B,
+  launch(fill_noise_kernel, dim3((B * n + 255) / 256), dim3(256), 0, s, out, seed, B,
                      p0, n);
   return hipGetLastError();
 }
@@ -669,20 +669,20 @@ hipError_t launch_fill_noise(float* out, uint64_t seed, int B, int p0, int n, hi
 template <typename T>
 hipError_t launch_convert(const float* src, T* dst, size_t n, hipStream_t s) {
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(convert_kernel<T>, dim3(grid_for(n, 256)), dim3(256), 0, s, src, dst, n);
+  launch(convert_kernel<T>, dim3(grid_for(n, 256)), dim3(256), 0, s, src, dst, n);
   return hipGetLastError();
 }
 
 template <typename T>
 hipError_t launch_zero(T* dst, size_t n, hipStream_t s) {
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(zero_kernel<T>, dim3(grid_for(n, 256)), dim3(256), 0, s, dst, n);
+  launch(zero_kernel<T>, dim3(grid_for(n, 256)), dim3(256), 0, s, dst, n);
   return hipGetLastError();
 }
 
 hipError_t launch_copy_f32(const float* src, float* dst, size_t n, hipStream_t s) {
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(copy_f32_kernel, dim3(grid_for(n, 256)), dim3(256), 0, s, src, dst, n);
+  launch(copy_f32_kernel, dim3(grid_for(n, 256)), dim3(256), 0, s, src, dst, n);
   return hipGetLastError();
 }
 
