@@ -178,3 +178,26 @@ def test_large_backbone_prefill_decode():
     prompt = S.prompts_zipf(1, B, N, LARGE.vocab)
     st = _blocks(kf, _model(LARGE), prompt, [k, k], seed=2, tol=TOL[1], rows=[0, 1])
     _log(f"large bf16 parity: {st}")
+
+
+def test_owt_batch512_decode():
+    """The largest sweep batch on the OWT-shaped model: batch 512 with a
+    16-token prompt, so the prefill runs 10240 body rows and each decode block
+    4096 (the 128x128 GEMM tiles) and 2048 head rows; prefill and two decode
+    blocks, sequences 0, 257 and 511."""
+    B, N, k = 512, 16, 4
+    kf = _ctx(OWT, B, k, N)
+    prompt = S.prompts_zipf(1, B, N, OWT.vocab)
+    st = _blocks(kf, _model(OWT), prompt, [k, k, k], seed=3, tol=TOL[1], rows=[0, 257, B - 1])
+    _log(f"owt bf16 B=512 parity: {st}")
+
+
+def test_large_backbone_batch256():
+    """The 24-layer backbone (d = 1024, 16 heads, MLP 4096) at its batch of 256
+    with a 16-token prompt: prefill (5120 rows) and one decode block (2048
+    rows), sequences 0 and 255."""
+    B, N, k = 256, 16, 4
+    kf = _ctx(LARGE, B, k, N)
+    prompt = S.prompts_zipf(1, B, N, LARGE.vocab)
+    st = _blocks(kf, _model(LARGE), prompt, [k, k], seed=4, tol=TOL[1], rows=[0, B - 1])
+    _log(f"large bf16 B=256 parity: {st}")
