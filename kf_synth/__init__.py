@@ -145,6 +145,7 @@ class ModelConfig:
     vocab: int
     n_ctx: int
     dtype: int  # DTYPE_FP32 or DTYPE_BF16
+    temperature: bool = False  # temperature-conditioned noise encoder
 
     @property
     def d_head(self) -> int:
@@ -177,6 +178,8 @@ def tensor_table(cfg: ModelConfig) -> List[Tuple[str, Tuple[int, ...]]]:
             (f"l{l}.w_2", (d, f)), (f"l{l}.b_2", (d,)),
         ]
     t += [("lnf_g", (d,)), ("lnf_b", (d,))]
+    if cfg.temperature:  # tau sinusoid -> Linear(d, d) -> GELU -> Linear(d, d)
+        t += [("temp_w1", (d, d)), ("temp_b1", (d,)), ("temp_w2", (d, d)), ("temp_b2", (d,))]
     return t
 
 
@@ -184,10 +187,14 @@ def n_params(cfg: ModelConfig) -> int:
     return int(sum(int(np.prod(s)) for _, s in tensor_table(cfg)))
 
 
+BLOB_FLAG_TEMPERATURE = 1  # header word 9: the temperature encoder's tensors follow lnf_b
+
+
 def header(cfg: ModelConfig) -> np.ndarray:
     h = np.zeros(HEADER_INTS, dtype=np.int32)
-    h[:9] = [BLOB_MAGIC, BLOB_VERSION, cfg.n_layer, cfg.d_model, cfg.n_head,
-             cfg.d_mlp, cfg.vocab, cfg.n_ctx, cfg.dtype]
+    h[:10] = [BLOB_MAGIC, BLOB_VERSION, cfg.n_layer, cfg.d_model, cfg.n_head,
+              cfg.d_mlp, cfg.vocab, cfg.n_ctx, cfg.dtype,
+              BLOB_FLAG_TEMPERATURE if cfg.temperature else 0]
     return h
 
 

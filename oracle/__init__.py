@@ -64,6 +64,8 @@ def lib():
             f = getattr(L, "orc_seq_new" + sfx); f.restype = P; f.argtypes = [P]
             f = getattr(L, "orc_seq_free" + sfx); f.restype = None; f.argtypes = [P]
             f = getattr(L, "orc_seq_len" + sfx); f.restype = ctypes.c_int; f.argtypes = [P]
+            f = getattr(L, "orc_seq_set_temperature" + sfx); f.restype = ctypes.c_int
+            f.argtypes = [P, ctypes.c_double]
             f = getattr(L, "orc_seq_kv" + sfx); f.restype = None
             f.argtypes = [P, ctypes.c_int, ctypes.c_int, dp]
             f = getattr(L, "orc_step" + sfx); f.restype = ctypes.c_int
@@ -141,6 +143,11 @@ class Seq:
     @property
     def C(self) -> int:
         return _f("orc_seq_len", self.model.prec)(self.h)
+
+    def set_temperature(self, tau: float) -> None:
+        """Temperature conditioning of this sequence's later noise rows."""
+        if _f("orc_seq_set_temperature", self.model.prec)(self.h, float(tau)) < 0:
+            raise ValueError("oracle: the model has no temperature encoder")
 
     def kv(self, layer: int, which: int) -> np.ndarray:
         out = np.zeros((self.C, self.model.d), np.float64)
@@ -337,6 +344,7 @@ def parse_blob(blob: np.ndarray) -> Tuple[dict, dict]:
     blob = np.asarray(blob, np.float32)
     hdr = blob[:16].view(np.int32)
     L, d, H, f, V, T, dt = (int(x) for x in hdr[2:9])
+    temp = bool(int(hdr[9]) & 1)
     shapes = [("tok", (V, d)), ("pos", (T, d)), ("nw1", (4 * d, d)), ("nb1", (4 * d,)),
               ("nw2", (d, 4 * d)), ("nb2", (d,))]
     for l in range(L):
@@ -345,6 +353,8 @@ def parse_blob(blob: np.ndarray) -> Tuple[dict, dict]:
                    (f"{l}.ln2_g", (d,)), (f"{l}.ln2_b", (d,)), (f"{l}.w1", (f, d)),
                    (f"{l}.b1", (f,)), (f"{l}.w2", (d, f)), (f"{l}.b2", (d,))]
     shapes += [("lnf_g", (d,)), ("lnf_b", (d,))]
+    if temp:
+        shapes += [("tw1", (d, d)), ("tb1", (d,)), ("tw2", (d, d)), ("tb2", (d,))]
     W = {}
     off = 16
     for name, shp in shapes:
@@ -355,7 +365,7 @@ def parse_blob(blob: np.ndarray) -> Tuple[dict, dict]:
         W[name] = a.astype(np.float64).reshape(shp)
         off += n
     assert off == blob.size
-    return dict(L=L, d=d, H=H, f=f, V=V, T=T), W
+    return dict(L=L, d=d, H=H, f=f, V=V, T=T, temperature=temp), W
 
 
 def _np_ln(x, g, b):
@@ -376,10 +386,11 @@ def _np_sinusoid(u, d):
 
 
 def dense_forward(cfg: dict, W: dict, rows: List[Tuple[str, float]], positions: Sequence[int],
-                  mask: np.ndarray) -> np.ndarray:
+                  mask: np.ndarray, tau: float = None) -> np.ndarray:
     """Whole-sequence forward with an explicit boolean mask[q, key]; returns logits per row.
 
-    rows[i] is ("tok", id) or ("noise", u)."""
+    rows[i] is ("tok", id) or ("noise", u); tau (temperature models) conditions
+    every noise row with W_t2 GELU(W_t1 sin(tau) + b_t1) + b_t2."""
     d, H = cfg["d"], cfg["H"]
     dh = d // H
     n = len(rows)
@@ -393,6 +404,9 @@ def dense_forward(cfg: dict, W: dict, rows: List[Tuple[str, float]], positions: 
         E = _np_sinusoid([rows[i][1] for i in noi_idx], d)
         Hn = _np_gelu(E @ W["nw1"].T + W["nb1"])
         X[noi_idx] = Hn @ W["nw2"].T + W["nb2"]
+        if cfg.get("temperature"):
+            Et = _np_sinusoid([tau], d)[0]
+            X[noi_idx] += _np_gelu(Et @ W["tw1"].T + W["tb1"]) @ W["tw2"].T + W["tb2"]
     X = X + W["pos"][pos]
     neg = np.where(mask, 0.0, -np.inf)
     for l in range(cfg["L"]):

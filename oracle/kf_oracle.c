@@ -35,7 +35,14 @@
  *   - noise MLP: Linear(d -> 4d), GELU, Linear(4d -> d); no token embedding
  *     on noise rows;
  *   - weights: 2-D tensors are rounded to bf16 (round-to-nearest-even) for
- *     bf16 models, 1-D tensors stay as given.
+ *     bf16 models, 1-D tensors stay as given;
+ *   - temperature conditioning (Sec. 3.3 "Temperature-controlled generation",
+ *     Appendix C.2 "Temperature control at inference"): a model whose blob
+ *     carries the temperature encoder maps each sequence's tau through the
+ *     same sinusoid and Linear(d -> d), GELU, Linear(d -> d), and adds the
+ *     result to every noise row of that sequence.  With the noise MLP this
+ *     gives the encoder 10 d^2 + 7 d parameters (5.9 M at d = 768, the size
+ *     the paper's model table lists for the noise encoder).
  */
 #include <math.h>
 #include <stdint.h>
@@ -54,14 +61,16 @@
 
 #define ORC_MAGIC 0x4B465731
 #define ORC_HDR 16
+#define ORC_FLAG_TEMPERATURE 1 /* header word 9 */
 
 typedef struct {
   REAL *ln1_g, *ln1_b, *wqkv, *bqkv, *wo, *bo, *ln2_g, *ln2_b, *w1, *b1, *w2, *b2;
 } orc_layer;
 
 typedef struct {
-  int L, d, H, f, V, T, dtype;
+  int L, d, H, f, V, T, dtype, temp;
   REAL *tok, *pos, *nw1, *nb1, *nw2, *nb2, *lnf_g, *lnf_b;
+  REAL *tw1, *tb1, *tw2, *tb2; /* temperature encoder (temp != 0) */
   orc_layer *layer;
   REAL *store;
 } orc_model;
@@ -70,6 +79,7 @@ typedef struct {
   const orc_model *m;
   int C;        /* committed context length */
   REAL *K, *Vc; /* [L][T][d] committed keys / values */
+  REAL *temb;   /* [d] temperature embedding added to noise rows, or NULL */
 } orc_seq;
 
 /* ---------------------------------------------------------------- helpers */
@@ -165,9 +175,12 @@ static long model_params(int L, int d, int f, int V, int T) {
   return (long)V * d + (long)T * d + 4L * d * d + 4L * d + 4L * d * d + d + L * per + 2L * d;
 }
 
+static long temp_params(int d) { return 2L * d * d + 2L * d; }
+
 long SYM(orc_blob_floats)(const int32_t *hdr) {
   if (hdr[0] != ORC_MAGIC) return -1;
-  return ORC_HDR + model_params(hdr[2], hdr[3], hdr[5], hdr[6], hdr[7]);
+  return ORC_HDR + model_params(hdr[2], hdr[3], hdr[5], hdr[6], hdr[7]) +
+         ((hdr[9] & ORC_FLAG_TEMPERATURE) ? temp_params(hdr[3]) : 0);
 }
 
 /* Copy n floats into REAL storage, rounding to bf16 when asked. */
@@ -188,10 +201,12 @@ orc_model *SYM(orc_model_new)(const float *blob, long n_floats) {
   if (hdr[0] != ORC_MAGIC || hdr[1] != 1) return NULL;
   int L = hdr[2], d = hdr[3], H = hdr[4], f = hdr[5], V = hdr[6], T = hdr[7], dt = hdr[8];
   if (L < 1 || d < 2 || H < 1 || d % H || d % 2 || f < 1 || V < 1 || T < 1) return NULL;
-  long np = model_params(L, d, f, V, T);
+  if (hdr[9] & ~ORC_FLAG_TEMPERATURE) return NULL;
+  const int temp = (hdr[9] & ORC_FLAG_TEMPERATURE) != 0;
+  long np = model_params(L, d, f, V, T) + (temp ? temp_params(d) : 0);
   if (n_floats != ORC_HDR + np) return NULL;
   orc_model *m = (orc_model *)calloc(1, sizeof(orc_model));
-  m->L = L; m->d = d; m->H = H; m->f = f; m->V = V; m->T = T; m->dtype = dt;
+  m->L = L; m->d = d; m->H = H; m->f = f; m->V = V; m->T = T; m->dtype = dt; m->temp = temp;
   m->store = (REAL *)malloc(sizeof(REAL) * (size_t)np);
   m->layer = (orc_layer *)calloc((size_t)L, sizeof(orc_layer));
   REAL *cur = m->store;
@@ -220,6 +235,12 @@ orc_model *SYM(orc_model_new)(const float *blob, long n_floats) {
   }
   m->lnf_g = take(&cur, &src, d, 0);
   m->lnf_b = take(&cur, &src, d, 0);
+  if (temp) {
+    m->tw1 = take(&cur, &src, (long)d * d, mb);
+    m->tb1 = take(&cur, &src, d, 0);
+    m->tw2 = take(&cur, &src, (long)d * d, mb);
+    m->tb2 = take(&cur, &src, d, 0);
+  }
   return m;
 }
 
@@ -244,7 +265,27 @@ void SYM(orc_seq_free)(orc_seq *s) {
   if (!s) return;
   free(s->K);
   free(s->Vc);
+  free(s->temb);
   free(s);
+}
+
+/* Temperature of the sequence: its embedding W_t2 GELU(W_t1 sin(tau) + b_t1) + b_t2
+ * is added to every later noise row.  -1 when the model has no temperature
+ * encoder. */
+int SYM(orc_seq_set_temperature)(orc_seq *s, double tau) {
+  const orc_model *m = s->m;
+  if (!m->temp) return -1;
+  const int d = m->d;
+  REAL *e = (REAL *)malloc(sizeof(REAL) * (size_t)d);
+  REAL *h = (REAL *)malloc(sizeof(REAL) * (size_t)d);
+  if (!s->temb) s->temb = (REAL *)malloc(sizeof(REAL) * (size_t)d);
+  sinusoid(tau, d, e);
+  linear(e, m->tw1, m->tb1, d, d, h);
+  for (int i = 0; i < d; ++i) h[i] = gelu(h[i]);
+  linear(h, m->tw2, m->tb2, d, d, s->temb);
+  free(e);
+  free(h);
+  return 0;
 }
 
 int SYM(orc_seq_len)(const orc_seq *s) { return s->C; }
@@ -276,6 +317,7 @@ int SYM(orc_step)(orc_seq *s, int nr, const int32_t *toks, int k, const double *
   const int C = s->C, n = nr + k;
   if (nr < 0 || k < 0 || n < 1 || C + n > m->T) return -1;
   if (k == 0 && nr < 1) return -1;
+  if (k > 0 && m->temp && !s->temb) return -1; /* the model needs each sequence's tau */
   for (int i = 0; i < nr; ++i)
     if (toks[i] < 0 || toks[i] >= V) return -1;
 
@@ -306,6 +348,8 @@ int SYM(orc_step)(orc_seq *s, int nr, const int32_t *toks, int k, const double *
       for (int i = 0; i < 4 * d; ++i) Y[i] = gelu(Y[i]);
       linear(Y, m->nw2, m->nb2, 4 * d, d, Z);
       for (int i = 0; i < d; ++i) x[i] = Z[i] + pe[i];
+      if (s->temb)
+        for (int i = 0; i < d; ++i) x[i] += s->temb[i];
     }
   }
 

@@ -536,3 +536,123 @@ def test_bad_arguments_rejected(small):
     with pytest.raises(ValueError):
         s.step(list(range(60)), [0.1] * 5)   # past n_ctx
     assert s.C == 0
+
+
+# ----------------------------------------------------- temperature encoder
+# Sec. 3.3 "Temperature-controlled generation" and Appendix C.2 "Temperature
+# control at inference": the noise encoder also receives tau.  Reading: tau
+# goes through the same sinusoid and its own Linear(d, d), GELU, Linear(d, d),
+# and the result is added to every noise row of the sequence.
+
+SMALL_T = S.ModelConfig(2, 64, 4, 128, 96, 64, S.DTYPE_FP32, temperature=True)
+
+
+@pytest.fixture(scope="module")
+def small_t():
+    blob = _blob(SMALL_T)
+    return blob, O.Model(blob)
+
+
+def _encoder_count():
+    for line in open(os.path.join(GOLD, "paper_counts.txt")):
+        w = line.split()
+        if w and w[0] == "encoder":
+            return int(w[1]), float(w[2])
+    raise AssertionError("no encoder line")
+
+
+def test_temperature_encoder_size():
+    """Model table (Appendix D): the noise encoder, with the noise and
+    temperature embeddings, has ~5.9 M parameters at d = 768.  The reading
+    (noise MLP d -> 4d -> d plus a temperature MLP d -> d -> d) gives
+    10 d^2 + 7 d = 5.90 M; feeding [sin(u), sin(tau)] to one MLP would give
+    7.1 M and a temperature embedding without its own MLP 4.7 M."""
+    d, pm = _encoder_count()
+    cfg = S.ModelConfig(12, d, 12, 4 * d, 30522, 128, S.DTYPE_BF16, temperature=True)
+    enc = sum(int(np.prod(s)) for n, s in S.tensor_table(cfg) if n.startswith(("noise_", "temp_")))
+    assert enc == 10 * d * d + 7 * d
+    assert abs(enc / 1e6 - pm) / pm < 0.01, enc
+
+
+def test_temperature_required_for_noise_rows(small_t):
+    """A temperature-conditioned model needs each sequence's tau before it can
+    embed noise rows; AR steps (no noise rows) do not."""
+    _, m = small_t
+    s = m.seq()
+    with pytest.raises(ValueError):
+        s.step([1, 2, 3], [0.5, 0.25])
+    s.step([1, 2, 3], [])  # AR step: fine
+    with pytest.raises(ValueError):
+        O.Model(_blob(SMALL)).seq().set_temperature(0.5)
+
+
+def test_temperature_zero_encoder_is_unconditioned():
+    """With the temperature MLP's output layer zero, every tau leaves the model
+    exactly the unconditioned one."""
+    W = S.make_weights(SMALL_T, seed=0, random_affine=True)
+    W["temp_w2"][:] = 0.0
+    W["temp_b2"][:] = 0.0
+    mt = O.Model(S.pack_blob(SMALL_T, W))
+    mu = O.Model(S.pack_blob(SMALL, {k: v for k, v in W.items() if not k.startswith("temp_")}))
+    x, u = [5, 9, 1, 40], [0.3, 0.7, 0.05]
+    lu, _ = mu.seq().step(x, u)
+    for tau in (0.01, 0.5, 1.0):
+        s = mt.seq()
+        s.set_temperature(tau)
+        lt, _ = s.step(x, u)
+        assert np.array_equal(lt, lu)
+
+
+def test_temperature_is_a_per_sequence_noise_bias(small_t):
+    """The temperature enters only as a vector added to the sequence's noise
+    rows: an unconditioned model whose noise-MLP output bias absorbs that vector
+    gives the same outputs, prefill and decode, while real rows (and so the
+    committed cache) are untouched."""
+    blob, m = small_t
+    cfg, Wp = O.parse_blob(blob)
+    d, tau = cfg["d"], 0.42
+    h = d // 2
+    a = 1000.0 * tau * 10000.0 ** (-np.arange(h) / h)
+    e = np.concatenate([np.cos(a), np.sin(a)])
+    z = Wp["tw1"] @ e + Wp["tb1"]
+    z = 0.5 * z * (1.0 + np.tanh(np.sqrt(2.0 / np.pi) * (z + 0.044715 * z ** 3)))
+    temb = Wp["tw2"] @ z + Wp["tb2"]
+    # the unconditioned model with the folded bias, through the fp64 numpy
+    # forward (a blob would round the folded bias to fp32)
+    W = S.make_weights(SMALL_T, seed=0, random_affine=True)
+    cfg_u, Wu_p = O.parse_blob(S.pack_blob(SMALL, {k: v for k, v in W.items() if not k.startswith("temp_")}))
+    Wu_p["nb2"] = Wp["nb2"] + temb
+    x, uu = [3, 17, 8, 60, 2], [0.11, 0.83, 0.5]
+    s = m.seq()
+    s.set_temperature(tau)
+    lt, _ = s.step(x, uu)
+    n = len(x) + len(uu)
+    mask = np.tril(np.ones((n, n), bool))
+    rows = [("tok", t) for t in x] + [("noise", q) for q in uu]
+    ref = O.dense_forward(cfg_u, Wu_p, rows, list(range(n)), mask)[len(x):]
+    assert np.max(np.abs(lt - ref)) <= 1e-10 * np.abs(ref).max()
+
+
+def test_temperature_brute_force(small_t):
+    """(e) with temperature: the numpy dense SingleForward of a
+    temperature-conditioned model equals the oracle's prefills group by group,
+    and different tau give different outputs."""
+    blob, m = small_t
+    cfg, W = O.parse_blob(blob)
+    rng = np.random.default_rng(11)
+    N, k, tau = 5, 3, 0.3
+    x = [int(t) for t in rng.integers(0, cfg["V"], N)]
+    zz = rng.random((N, k))
+    M, pos, _ = O.single_forward_layout(N, k)
+    rows = [("tok", t) for t in x] + [("noise", float(zz[t, j])) for t in range(N) for j in range(k)]
+    dense = O.dense_forward(cfg, W, rows, pos, M, tau=tau)
+    for t in range(1, N + 1):
+        s = m.seq()
+        s.set_temperature(tau)
+        lg, _ = s.step(x[:t], zz[t - 1])
+        ref = dense[N + (t - 1) * k:N + t * k]
+        assert np.max(np.abs(lg - ref)) <= 1e-10 * np.abs(ref).max(), t
+    s = m.seq()
+    s.set_temperature(0.9)
+    lg9, _ = s.step(x, zz[N - 1])
+    assert np.max(np.abs(lg9 - dense[N + (N - 1) * k:])) > 1e-3 * np.abs(lg9).max()
