@@ -50,6 +50,9 @@ extern "C" {
 
 #define KF_FLAG_DEBUG_LOGITS 1u /* reserve room for, and record, the fp32 head logits of
                                    the most recent step (kf_debug_logits) */
+#define KF_FLAG_TEMPERATURE 2u  /* the model has a temperature-conditioned noise encoder
+                                   (its weight blob carries the encoder, header word 9 = 1);
+                                   see kf_set_temperature */
 
 typedef struct kf_config {
   int n_layer;    /* Transformer blocks */
@@ -92,8 +95,10 @@ int kf_bind_state(kf_ctx *ctx, void *dev_ptr, size_t bytes);
  * W1 [4d][d], b1 [4d], W2 [d][4d], b2 [d], then per layer: ln1 gain, ln1
  * shift [d], W_qkv [3d][d], b_qkv [3d], W_o [d][d], b_o [d], ln2 gain, ln2
  * shift [d], W_1 [d_mlp][d], b_1 [d_mlp], W_2 [d][d_mlp], b_2 [d]; finally
- * the final-norm gain and shift [d].  Matrices are [out][in].  For KF_BF16
- * the 2-D tensors are rounded to bf16 (round to nearest even) on load.
+ * the final-norm gain and shift [d]; with KF_FLAG_TEMPERATURE, then the
+ * temperature encoder W_t1 [d][d], b_t1 [d], W_t2 [d][d], b_t2 [d].  Matrices
+ * are [out][in].  For KF_BF16 the 2-D tensors are rounded to bf16 (round to
+ * nearest even) on load.
  * blob_is_device: 0 = host pointer (copied synchronously), 1 = device
  * pointer (converted on the stream).  The header must match the config. */
 int kf_load_weights(kf_ctx *ctx, const void *blob, size_t bytes, int blob_is_device);
@@ -124,6 +129,18 @@ int kf_decode_block(kf_ctx *ctx, int B, int k, const float *noise, int32_t *out)
  * L == 0 launches nothing. */
 int kf_generate(kf_ctx *ctx, int B, int N, const int32_t *prompt, int L, int k, uint64_t seed,
                 int32_t *out);
+
+/* Temperature-controlled generation (Sec. 3.3; Appendix C.2, temperature
+ * control at inference): tau [B] (device memory, read during the call) sets the
+ * temperature of sequences 0..B-1.  Each tau goes through the noise sinusoid
+ * and the encoder's Linear(d, d), GELU, Linear(d, d); the resulting vector is
+ * added to every later noise row of that sequence until the next call (the
+ * weights are reloaded, or the temperature is set again).  Requires
+ * KF_FLAG_TEMPERATURE (else KF_ESTATE) and loaded weights; 1 <= B <= max_batch.
+ * With the flag, kf_prefill, kf_decode_block and kf_generate for B sequences
+ * return KF_ESTATE until the temperature of at least B sequences is set; the
+ * AR calls have no noise rows and do not need it. */
+int kf_set_temperature(kf_ctx *ctx, const float *tau, int B);
 
 /* Autoregressive baseline (the AR teacher's decoding, Sec. 4; inverse-CDF map
  * of Appendix B: the smallest token id m with F_m > u, F the CDF of the

@@ -19,6 +19,7 @@ _LIB_PATH = os.path.join(_PKG, "libkforcing.so")
 KF_OK, KF_EINVAL, KF_ESTATE, KF_ECTX, KF_ENOMEM, KF_EHIP = 0, -1, -2, -3, -4, -5
 KF_FP32, KF_BF16 = 0, 1
 KF_FLAG_DEBUG_LOGITS = 1
+KF_FLAG_TEMPERATURE = 2
 KF_KC_NAMES = ["embed", "noise", "norm", "qkv", "attn", "oproj", "mlp_up", "mlp_down", "head",
                "select"]
 KF_TIMING_ALL = (1 << len(KF_KC_NAMES)) - 1
@@ -70,6 +71,7 @@ def lib():
         "kf_generate_ar": (I, [P, I, I, P, I, U64, P]),
         "kf_debug_logits": (I, [P, P, SZ]),
         "kf_fill_noise": (I, [P, U64, I, I, I, P]),
+        "kf_set_temperature": (I, [P, P, I]),
         "kf_get_state": (I, [P, IP, IP, IP]),
         "kf_device_errors": (I, [P, IP]),
         "kf_set_graphs": (I, [P, I]),
@@ -210,6 +212,12 @@ class KForcing:
                                device=self.device)
         self._check(self.L.kf_debug_logits(self.h, self._p(out), out.numel()))
         return out
+
+    def set_temperature(self, tau):
+        """Per-sequence temperatures tau [B] (temperature-conditioned models)."""
+        t = self._f32(tau).reshape(-1)
+        self._check(self.L.kf_set_temperature(self.h, self._p(t), int(t.numel())))
+        self.torch.cuda.synchronize(self.device)  # t is read during the call's kernels
 
     def fill_noise(self, seed: int, B: int, p0: int, n: int):
         out = self.torch.empty((B, n), dtype=self.torch.float32, device=self.device)

@@ -21,6 +21,7 @@ namespace {
 
 constexpr int32_t kMagic = 0x4B465731;
 constexpr int kHeaderInts = 16;
+constexpr int32_t kBlobTemperature = 1;  // header word 9: temperature encoder present
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
@@ -47,6 +48,8 @@ struct Plan {
   size_t wbegin = 0, wend = 0;
   size_t tok = 0, pos = 0, nw1 = 0, nb1 = 0, nw2 = 0, nb2 = 0, omega = 0, lnf_g = 0, lnf_b = 0;
   size_t head_c1 = 0, head_c2 = 0, head_w = 0;  // folded final norm; gain-scaled token table
+  size_t tw1 = 0, tb1 = 0, tw2 = 0, tb2 = 0;     // temperature encoder (KF_FLAG_TEMPERATURE)
+  size_t temb = 0;                              // per-sequence temperature embedding [max_batch][d]
   std::vector<LayerOff> layer;
   size_t kv = 0, kv_bytes = 0;
   size_t X = 0, Xh = 0, lnst = 0, A = 0, Q = 0, O = 0, Hm = 0, noise = 0, pval = 0, pidx = 0;
@@ -74,7 +77,7 @@ bool config_ok(const kf_config& c, std::string* why) {
   if (c.max_batch < 1 || c.max_batch > 65535) return bad("max_batch must be in [1, 65535]");
   if (c.max_k < 1 || c.max_k > c.n_ctx) return bad("max_k must be in [1, n_ctx]");
   if (c.max_prompt < 1 || c.max_prompt > c.n_ctx) return bad("max_prompt must be in [1, n_ctx]");
-  if (c.flags & ~KF_FLAG_DEBUG_LOGITS) return bad("unknown flag bits");
+  if (c.flags & ~(KF_FLAG_DEBUG_LOGITS | KF_FLAG_TEMPERATURE)) return bad("unknown flag bits");
   // GEMM operands are addressed through buffer descriptors with 32-bit byte
   // ranges: the largest activation matrix of a step must stay below 2 GiB.
   const long long es = c.dtype == KF_BF16 ? 2 : 4;
@@ -133,11 +136,18 @@ void make_plan(const kf_config& c, Plan& p) {
   p.head_c1 = take((size_t)p.Vpad * 4);
   p.head_c2 = take((size_t)p.Vpad * 4);
   p.head_w = take((size_t)p.Vpad * d * es);
+  if (c.flags & KF_FLAG_TEMPERATURE) {
+    p.tw1 = take(d * d * es);
+    p.tb1 = take(d * 4);
+    p.tw2 = take(d * d * es);
+    p.tb2 = take(d * 4);
+  }
   p.wend = off;
   p.kv_bytes = (size_t)c.max_batch * L * 2 * T * d * es;
   p.kv = take(p.kv_bytes);
   const size_t R = p.rows_max, Hw = f > 4 * d ? f : 4 * d;
   p.X = take(R * d * 4);
+  p.temb = (c.flags & KF_FLAG_TEMPERATURE) ? take((size_t)c.max_batch * d * es) : 0;
   p.Xh = es == 2 ? take(R * d * es) : p.X;
   p.lnst = take(R * (d / 16) * 8);  // LayerNorm partial sums of the residual rows
   p.A = take(R * d * es);
@@ -178,6 +188,7 @@ struct kf_ctx {
   // sequence state (host mirror of the device state)
   bool live = false;
   int B = 0, C = 0, pending = 0;
+  int temp_B = 0;  // sequences whose temperature embedding is set (kf_set_temperature)
   int last_head_rows = 0;
   bool last_logits = false;
   std::string err;
@@ -291,6 +302,7 @@ int run_step(kf_ctx* c, const StepIn& in) {
   float* X = reinterpret_cast<float*>(base + p.X);
   T* Xh = reinterpret_cast<T*>(base + p.Xh);  // compute-dtype residual copy (X itself for fp32)
   float2* lnst = reinterpret_cast<float2*>(base + p.lnst);
+  const T* temb = (cf.flags & KF_FLAG_TEMPERATURE) ? reinterpret_cast<const T*>(base + p.temb) : nullptr;
   const kf::AttnSplit asp{reinterpret_cast<float*>(base + p.att_m),
                           reinterpret_cast<float*>(base + p.att_l),
                           reinterpret_cast<float*>(base + p.att_o), kAttnEntries, 1};
@@ -324,7 +336,8 @@ int run_step(kf_ctx* c, const StepIn& in) {
     KF_LAUNCH(c, KF_KC_NOISE,
               kf::gemm_bias<T>(A, W(p.nw1), Mk, 4 * d, d, F(p.nb1), kf::Act::Gelu, Hm, 4 * d, &sws, s));
     KF_LAUNCH(c, KF_KC_NOISE,
-              kf::gemm_noise_out<T>(Hm, W(p.nw2), Mk, d, 4 * d, F(p.nb2), pos, X, Xh, lnst, g, st, &sws, s));
+              kf::gemm_noise_out<T>(Hm, W(p.nw2), Mk, d, 4 * d, F(p.nb2), pos, temb, X, Xh, lnst, g,
+                                    st, &sws, s));
   }
   for (int l = 0; l < cf.n_layer; ++l) {
     const LayerOff& y = p.layer[l];
@@ -366,6 +379,15 @@ int step(kf_ctx* c, const StepIn& in) {
 int ready(kf_ctx* c) {
   if (!c->base) return fail(c, KF_ESTATE, "no state buffer bound (kf_bind_state)");
   if (!c->weights) return fail(c, KF_ESTATE, "no weights loaded (kf_load_weights)");
+  return KF_OK;
+}
+
+// A temperature-conditioned model embeds noise rows only for sequences whose
+// temperature has been set.
+int temp_ready(kf_ctx* c, int B) {
+  if ((c->cfg.flags & KF_FLAG_TEMPERATURE) && c->temp_B < B)
+    return fail(c, KF_ESTATE, "temperature set for %d sequences, the step has %d (kf_set_temperature)",
+                c->temp_B, B);
   return KF_OK;
 }
 
@@ -451,6 +473,28 @@ int repeat_step(kf_ctx* c, const StepIn& in, int count, int adv, int N, int L) {
   return KF_OK;
 }
 
+// Temperature embeddings of sequences 0..B-1: tau through the noise sinusoid,
+// then Linear(d, d), GELU, Linear(d, d), into temb [b][d].
+template <typename T>
+int run_temperature(kf_ctx* c, const float* tau, int B) {
+  const Plan& p = c->plan;
+  char* base = c->base;
+  const int d = c->cfg.d_model;
+  hipStream_t s = c->stream;
+  T* A = reinterpret_cast<T*>(base + p.A);
+  T* Hm = reinterpret_cast<T*>(base + p.Hm);
+  T* temb = reinterpret_cast<T*>(base + p.temb);
+  auto F = [&](size_t o) { return reinterpret_cast<const float*>(base + o); };
+  auto W = [&](size_t o) { return reinterpret_cast<const T*>(base + o); };
+  const KfStepGeom g{B, 1, 0, 1};  // one "noise row" per sequence, u = tau[b]
+  KF_HIP(c, kf::launch_noise_sinusoid<T>(A, tau, 0, reinterpret_cast<const double*>(base + p.omega), g,
+                                         d, reinterpret_cast<const KfDevState*>(base + p.dstate),
+                                         nullptr, s));
+  KF_HIP(c, kf::gemm_bias<T>(A, W(p.tw1), B, d, d, F(p.tb1), kf::Act::Gelu, Hm, d, nullptr, s));
+  KF_HIP(c, kf::gemm_bias<T>(Hm, W(p.tw2), B, d, d, F(p.tb2), kf::Act::None, temb, d, nullptr, s));
+  return KF_OK;
+}
+
 }  // namespace
 
 // ==================================================================== ABI
@@ -524,9 +568,10 @@ int kf_load_weights(kf_ctx* c, const void* blob, size_t bytes, int blob_is_devic
   const Plan& p = c->plan;
   drop_graph(c);
   const size_t d = cf.d_model, f = cf.d_mlp, V = cf.vocab, T = cf.n_ctx, L = cf.n_layer;
+  const bool temp = (cf.flags & KF_FLAG_TEMPERATURE) != 0;
   const size_t n_params = V * d + T * d + 8 * d * d + 4 * d + d +
                           L * (2 * d + 3 * d * d + 3 * d + d * d + d + 2 * d + f * d + f + d * f + d) +
-                          2 * d;
+                          2 * d + (temp ? 2 * d * d + 2 * d : 0);
   if (bytes != (kHeaderInts + n_params) * 4)
     return fail(c, KF_EINVAL, "blob has %zu bytes, %zu expected for this config", bytes,
                 (kHeaderInts + n_params) * 4);
@@ -535,8 +580,9 @@ int kf_load_weights(kf_ctx* c, const void* blob, size_t bytes, int blob_is_devic
     KF_HIP(c, hipMemcpy(hdr, blob, sizeof hdr, hipMemcpyDeviceToHost));
   else
     memcpy(hdr, blob, sizeof hdr);
-  const int32_t want[9] = {kMagic, 1, cf.n_layer, cf.d_model, cf.n_head, cf.d_mlp, cf.vocab, cf.n_ctx, cf.dtype};
-  for (int i = 0; i < 9; ++i)
+  const int32_t want[10] = {kMagic, 1, cf.n_layer, cf.d_model, cf.n_head, cf.d_mlp, cf.vocab,
+                            cf.n_ctx, cf.dtype, temp ? kBlobTemperature : 0};
+  for (int i = 0; i < 10; ++i)
     if (hdr[i] != want[i]) return fail(c, KF_EINVAL, "blob header word %d is %d, expected %d", i, hdr[i], want[i]);
 
   // Destination of each tensor in blob order: (offset, count, is_matrix).
@@ -565,6 +611,12 @@ int kf_load_weights(kf_ctx* c, const void* blob, size_t bytes, int blob_is_devic
   }
   dst.push_back({p.lnf_g, d, false});
   dst.push_back({p.lnf_b, d, false});
+  if (temp) {
+    dst.push_back({p.tw1, d * d, true});
+    dst.push_back({p.tb1, d, false});
+    dst.push_back({p.tw2, d * d, true});
+    dst.push_back({p.tb2, d, false});
+  }
 
   // sinusoid frequencies omega_i = 10000^(-i/(d/2)) for the noise encoder
   std::vector<double> omega(d / 2);
@@ -616,6 +668,22 @@ int kf_load_weights(kf_ctx* c, const void* blob, size_t bytes, int blob_is_devic
   KF_HIP(c, hipStreamSynchronize(c->stream));
   c->weights = true;
   c->live = false;
+  c->temp_B = 0;
+  return KF_OK;
+}
+
+int kf_set_temperature(kf_ctx* c, const float* tau, int B) {
+  if (!c) return KF_EINVAL;
+  const kf_config& cf = c->cfg;
+  if (!(cf.flags & KF_FLAG_TEMPERATURE))
+    return fail(c, KF_ESTATE, "the config has no temperature encoder (KF_FLAG_TEMPERATURE)");
+  if (B < 1 || B > cf.max_batch) return fail(c, KF_EINVAL, "B=%d outside [1, %d]", B, cf.max_batch);
+  if (!tau) return fail(c, KF_EINVAL, "null pointer argument");
+  int r = ready(c);
+  if (r) return r;
+  r = cf.dtype == KF_BF16 ? run_temperature<bf16>(c, tau, B) : run_temperature<float>(c, tau, B);
+  if (r) return r;
+  c->temp_B = B;
   return KF_OK;
 }
 
@@ -628,6 +696,8 @@ int kf_prefill(kf_ctx* c, int B, int N, const int32_t* prompt, int k, const floa
   if (!noise || !out || (N > 0 && !prompt)) return fail(c, KF_EINVAL, "null pointer argument");
   if (N + k > cf.n_ctx) return fail(c, KF_ECTX, "N + k = %d exceeds n_ctx = %d", N + k, cf.n_ctx);
   int r = ready(c);
+  if (r) return r;
+  r = temp_ready(c, B);
   if (r) return r;
   StepIn in{B, N, k, prompt, N, noise, nullptr, 0, out_desc(c, out, k, -1), true};
   r = step(c, in);
@@ -645,6 +715,8 @@ int kf_decode_block(kf_ctx* c, int B, int k, const float* noise, int32_t* out) {
   if (k < 1 || k > cf.max_k) return fail(c, KF_EINVAL, "k=%d outside [1, %d]", k, cf.max_k);
   if (!noise || !out) return fail(c, KF_EINVAL, "null pointer argument");
   int r = ready(c);
+  if (r) return r;
+  r = temp_ready(c, B);
   if (r) return r;
   if (!c->live) return fail(c, KF_ESTATE, "decode before prefill");
   if (B != c->B) return fail(c, KF_ESTATE, "B=%d differs from the prefill's B=%d", B, c->B);
@@ -668,6 +740,8 @@ int kf_generate(kf_ctx* c, int B, int N, const int32_t* prompt, int L, int k, ui
   if (L > 0 && (!out || (N > 0 && !prompt))) return fail(c, KF_EINVAL, "null pointer argument");
   if (N + L > cf.n_ctx) return fail(c, KF_ECTX, "N + L = %d exceeds n_ctx = %d", N + L, cf.n_ctx);
   int r = ready(c);
+  if (r) return r;
+  r = temp_ready(c, B);
   if (r) return r;
   if (L == 0) return KF_OK;
   StepIn in{B, N, k, prompt, N, nullptr, nullptr, seed, out_desc(c, out, L, N), true};

@@ -182,13 +182,15 @@ struct EpQKV {
 };
 
 // Second noise-MLP layer: noise row m = (b, j) lands in residual row
-// b*R + nr + j with its learned position C + nr + j added.
+// b*R + nr + j with its learned position C + nr + j added, and, for a
+// temperature-conditioned model, sequence b's temperature embedding.
 template <typename T>
 struct EpNoiseOut {
   float* X;
   T* Xh;
   const float* bias;
   const T* pos;
+  const T* temb;  // per-sequence temperature embedding [B][d], or null
   const KfDevState* st;
   KfStepGeom g;
   int d;
@@ -206,6 +208,11 @@ struct EpNoiseOut {
     get8(pos + (size_t)p * d + n, pe);
 #pragma unroll
     for (int i = 0; i < 8; ++i) v[i] += pe[i];
+    if (temb) {
+      get8(temb + (size_t)(m / g.k) * d + n, pe);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] += pe[i];
+    }
     put8(X + row * d + n, v);
     if constexpr (sizeof(T) == 2) put8(Xh + row * d + n, v);
   }
@@ -830,9 +837,9 @@ hipError_t gemm_residual(const T* A, const T* W, int M, int N, int K, const floa
 
 template <typename T>
 hipError_t gemm_noise_out(const T* A, const T* W, int M, int d, int K, const float* bias,
-                          const T* pos, float* X, T* Xh, float2* lnst, KfStepGeom g,
-                          const KfDevState* st, const SplitWs* ws, hipStream_t s) {
-  EpNoiseOut<T> ep{X, Xh, bias, pos, st, g, d, lnst};
+                          const T* pos, const T* temb, float* X, T* Xh, float2* lnst,
+                          KfStepGeom g, const KfDevState* st, const SplitWs* ws, hipStream_t s) {
+  EpNoiseOut<T> ep{X, Xh, bias, pos, temb, st, g, d, lnst};
   return dispatch<T, 0, false>(GemmA{A, K, M, nullptr, nullptr, nullptr, KfStepGeom{}}, W, M, d, K,
                                ep, s, ws);
 }
@@ -887,7 +894,7 @@ hipError_t launch_ln_fold(const T* W, T* Wout, const float* g, const float* beta
   template hipError_t gemm_residual<T>(const T*, const T*, int, int, int, const float*, float*,   \
                                        T*, float2*, const SplitWs*, hipStream_t);                  \
   template hipError_t gemm_noise_out<T>(const T*, const T*, int, int, int, const float*,          \
-                                        const T*, float*, T*, float2*, KfStepGeom,                 \
+                                        const T*, const T*, float*, T*, float2*, KfStepGeom,       \
                                         const KfDevState*, const SplitWs*, hipStream_t);           \
   template hipError_t gemm_qkv_ln<T>(const T*, const LnFold&, const T*, int, int, const float*,   \
                                      T*, T*, KfStepGeom, KfKvGeom, int, const KfDevState*,         \

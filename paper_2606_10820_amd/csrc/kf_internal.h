@@ -163,8 +163,8 @@ hipError_t gemm_up_ln(const T* Xh, const LnFold& ln, const T* W, int M, int N, i
                       const float* bias, T* out, hipStream_t s);
 template <typename T>
 hipError_t gemm_noise_out(const T* A, const T* W, int M, int d, int K, const float* bias,
-                          const T* pos, float* X, T* Xh, float2* lnst, KfStepGeom g,
-                          const KfDevState* st, const SplitWs* ws, hipStream_t s);
+                          const T* pos, const T* temb, float* X, T* Xh, float2* lnst,
+                          KfStepGeom g, const KfDevState* st, const SplitWs* ws, hipStream_t s);
 // Head over the final LayerNorm of the selected rows (gather: 1 = noise rows
 // of the step, 2 = last real row per sequence): per (row, 128-column tile) the
 // maximum and its lowest column index into pval/pidx [M][Vpad/128]; columns

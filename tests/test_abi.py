@@ -2,6 +2,7 @@
 declared in include/kforcing.h, and rejects bad arguments before touching a
 device (each rejection leaves the context's state unchanged)."""
 import ctypes
+import dataclasses
 import os
 import re
 import subprocess
@@ -128,6 +129,35 @@ def test_state_machine_without_device(L):
     C, p, B = ctypes.c_int(-1), ctypes.c_int(-1), ctypes.c_int(-1)
     assert L.kf_get_state(h, ctypes.byref(C), ctypes.byref(p), ctypes.byref(B)) == Bd.KF_OK
     assert (C.value, p.value, B.value) == (0, 0, 0)
+    L.kf_destroy(h)
+
+
+def test_temperature_entry_point_checks(L):
+    P = ctypes.c_void_p
+    fake = P(0x10000)  # never dereferenced: every call below fails validation first
+    plain = _ctx(L, _cfg())
+    assert L.kf_set_temperature(plain, fake, 2) == Bd.KF_ESTATE  # no temperature encoder
+    L.kf_destroy(plain)
+    cfg = _cfg(flags=Bd.KF_FLAG_TEMPERATURE)
+    assert L.kf_state_bytes(ctypes.byref(cfg)) > L.kf_state_bytes(ctypes.byref(_cfg()))
+    h = _ctx(L, cfg)
+    assert L.kf_set_temperature(h, None, 2) == Bd.KF_EINVAL
+    assert L.kf_set_temperature(h, fake, 0) == Bd.KF_EINVAL
+    assert L.kf_set_temperature(h, fake, 9) == Bd.KF_EINVAL
+    assert L.kf_set_temperature(h, fake, 2) == Bd.KF_ESTATE  # no state buffer yet
+    need = L.kf_state_bytes(ctypes.byref(cfg))
+    assert L.kf_bind_state(h, fake, need) == Bd.KF_OK
+    assert L.kf_set_temperature(h, fake, 2) == Bd.KF_ESTATE  # no weights yet
+    # blobs with and without the encoder are told apart before any copy
+    toy = S.WORKLOADS["toy"]["cfg"]
+    plain_blob = S.pack_blob(toy, S.make_weights(toy))
+    assert L.kf_load_weights(h, P(plain_blob.ctypes.data), plain_blob.nbytes, 0) == Bd.KF_EINVAL
+    toy_t = dataclasses.replace(toy, temperature=True)
+    t_blob = S.pack_blob(toy_t, S.make_weights(toy_t))
+    bad = t_blob.copy()
+    bad[:16].view(np.int32)[9] = 0
+    assert L.kf_load_weights(h, P(bad.ctypes.data), bad.nbytes, 0) == Bd.KF_EINVAL
+    assert b"header word 9" in L.kf_last_error(h)
     L.kf_destroy(h)
 
 
