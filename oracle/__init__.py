@@ -508,3 +508,30 @@ def generate_batched(model: Model, prompt: np.ndarray, L: int, k: int, seed: int
         pending = np.stack([argmax(logits[b]) for b in range(B)])
         out[:, p - N:p - N + k] = pending
     return out
+
+
+def masked_attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, mask: np.ndarray,
+                     scale: float) -> np.ndarray:
+    """Attention with an explicit boolean mask, the plain definition in fp64:
+    per (batch, head), O = softmax(scale * Q K^T over the visible keys) V.
+    Q [B][H][nq][dh], K and V [B][H][nk][dh], mask [nq][nk]; every query row
+    must see at least one key."""
+    Q, K, V = (np.asarray(a, np.float64) for a in (Q, K, V))
+    assert mask.shape == (Q.shape[2], K.shape[2]) and mask.any(axis=1).all()
+    S = np.einsum("bhqd,bhkd->bhqk", Q, K) * scale
+    S = np.where(mask[None, None], S, -np.inf)
+    S = S - S.max(axis=-1, keepdims=True)
+    P = np.exp(S)
+    P /= P.sum(axis=-1, keepdims=True)
+    return np.einsum("bhqk,bhkd->bhqd", P, V)
+
+
+def training_mask(kind: str, N: int, k: int) -> np.ndarray:
+    """Query x key mask of the training attention calls (Appendix C.2):
+    "single" = M_S over all N + Nk tokens; "double" = M_D, the Future-1 and
+    Future-2 query rows over the N + 2Nk context, Future-1, Future-2 keys."""
+    if kind == "single":
+        return single_forward_layout(N, k)[0]
+    if kind == "double":
+        return double_forward_layout(N, k)[0][N:]
+    raise ValueError(kind)

@@ -656,3 +656,38 @@ def test_temperature_brute_force(small_t):
     s.set_temperature(0.9)
     lg9, _ = s.step(x, zz[N - 1])
     assert np.max(np.abs(lg9 - dense[N + (N - 1) * k:])) > 1e-3 * np.abs(lg9).max()
+
+
+# ------------------------------------------- training-mask attention (C.2)
+
+def test_masked_attention_definition():
+    """The plain masked attention: a row with one visible key returns that
+    key's value; equal scores average the visible values; each row agrees with
+    the C oracle's own single-query attention over the visible keys."""
+    rng = np.random.default_rng(21)
+    B, H, nq, nk, dh = 1, 2, 6, 9, 8
+    Q, K, V = rng.standard_normal((B, H, nq, dh)), rng.standard_normal((B, H, nk, dh)), rng.standard_normal((B, H, nk, dh))
+    mask = rng.random((nq, nk)) < 0.5
+    mask[:, 0] = True
+    mask[0] = False
+    mask[0, 3] = True
+    Om = O.masked_attention(Q, K, V, mask, 0.37)
+    assert np.allclose(Om[:, :, 0], V[:, :, 3], rtol=0, atol=1e-15)
+    Oq = O.masked_attention(np.zeros_like(Q), K, V, mask, 1.0)
+    for r in range(nq):
+        assert np.allclose(Oq[0, 0, r], V[0, 0, mask[r]].mean(axis=0), atol=1e-14)
+    for h in range(H):  # the C oracle's attend scales by 1/sqrt(dh) itself
+        for r in range(nq):
+            idx = np.flatnonzero(mask[r])
+            o, _ = O.attend(Q[0, h, r] * 0.37 * math.sqrt(dh), K[0, h, idx], V[0, h, idx])
+            assert np.allclose(Om[0, h, r], o, atol=1e-12)
+
+
+def test_training_masks_nnz():
+    """The masks the training attention uses have the Appendix C.2 sizes:
+    |M_S| over all rows, and the Future-2 rows of M_D."""
+    for N, k in [(5, 3), (7, 1), (4, 4), (9, 2)]:
+        assert int(O.training_mask("single", N, k).sum()) == O.nnz_single(N, k)
+        Md = O.training_mask("double", N, k)
+        assert Md.shape == (2 * N * k, N + 2 * N * k)
+        assert int(Md[N * k:].sum()) == O.nnz_double(N, k)
