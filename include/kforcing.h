@@ -201,6 +201,35 @@ int kf_device_errors(kf_ctx *ctx, int *flags);
 int kf_set_timing(kf_ctx *ctx, int class_mask);
 int kf_kernel_time(kf_ctx *ctx, int kernel_class, double *total_ms, int *launches);
 
+/* ------------------------------------------- attention of the training masks
+ * Block-sparse attention under the masks that train K-Forcing (Appendix C.2),
+ * for N context tokens and k tokens per context position, 0-based group
+ * t = 0..N-1 and in-group index j = 0..k-1:
+ *   KF_MASK_SINGLE (SingleForward M_S): queries = keys = [context N | noise N*k];
+ *     context row i sees context 0..i; noise row N + t*k + j sees context
+ *     0..t and noise N + t*k .. N + t*k + j.
+ *   KF_MASK_DOUBLE (DoubleForward M_D, its Future-1 and Future-2 query rows):
+ *     queries [F1 N*k | F2 N*k], keys [context N | F1 N*k | F2 N*k];
+ *     F1 row t*k + j sees context 0..t and F1 keys of group t up to j;
+ *     F2 row N*k + t*k + j sees context 0..t, all k F1 keys of group t and F2
+ *     keys of group t up to j.
+ * O = softmax(scale * Q K^T + mask) V per (sequence, head), fp32 softmax.
+ *   Q, O: bf16 [B][H][rows][d_head]; K, V: bf16 [B][H][keys][d_head]; device
+ *   pointers, 16-byte aligned, owned by the caller; O must not overlap the
+ *   inputs.  rows = N + N*k (single) or 2*N*k (double); keys = N + N*k
+ *   (single) or N + 2*N*k (double).  d_head in {32, 64, 128}.
+ *   Work is enqueued on hip_stream (null: the default stream); nothing is
+ *   allocated.  B, H or N equal to 0 is an empty problem (KF_OK, nothing
+ *   launched, pointers unchecked).
+ * Returns KF_EINVAL for an unknown mask, k < 1, a negative size, an unsupported
+ * d_head, a non-finite scale, a null or misaligned pointer, or a problem whose
+ * per-head element count or workgroup count reaches 2^31; KF_EHIP when the
+ * launch fails.  There is no context, hence no kf_last_error() message. */
+#define KF_MASK_SINGLE 0
+#define KF_MASK_DOUBLE 1
+int kf_training_attention(void *hip_stream, int mask, int B, int H, int N, int k, int d_head,
+                          const void *Q, const void *K, const void *V, void *O, float scale);
+
 /* Release host resources (device memory belongs to the caller). */
 void kf_destroy(kf_ctx *ctx);
 

@@ -6,7 +6,8 @@ inputs that both the HIP path and the CPU oracle consume:
 * model weights  (Gaussian N(0, std) via Box-Muller, optionally random affine
   parameters for tests),
 * prompt token ids (uniform over the vocabulary, or truncated Zipf(s)),
-* noise blocks u in [0, 1) handed to an explicit decode call.
+* noise blocks u in [0, 1) handed to an explicit decode call,
+* query/key/value tensors of the training-mask attention (bfloat16 values).
 
 Every random word comes from the counter-based generator Philox4x32-10
 (Salmon, Moraes, Dror and Shaw, "Parallel random numbers: as easy as 1, 2, 3",
@@ -22,6 +23,10 @@ schedule 0x9E3779B9 / 0xBB67AE85.  Counters and streams:
 
 The noise rule lets k = 1, 2, 4 and the autoregressive baseline consume the
 same u for the same emitted position.
+
+Attention inputs are many (up to ~10^9 values at a training batch), so they
+come from numpy's PCG64 instead, seeded with (seed, 3, b, h) per sequence and
+head, so that any one (b, h) slice can be drawn again on its own.
 """
 from __future__ import annotations
 
@@ -260,3 +265,37 @@ def make_prompts(kind: str, seed: int, B: int, N: int, V: int) -> np.ndarray:
 
 def describe(cfg: ModelConfig) -> str:
     return json.dumps(dataclasses.asdict(cfg))
+
+
+# ---------------------------------------------------------------------------
+# Attention inputs of the training masks
+# ---------------------------------------------------------------------------
+
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    """float32 values rounded to the nearest bfloat16 (ties to even), as float32."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    u = (u + (np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1)))) & np.uint32(0xFFFF0000)
+    return u.view(np.float32)
+
+
+def attention_inputs(seed: int, b: int, h: int, rows: int, keys: int, dh: int,
+                     std: float = 1.0) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Q [rows][dh], K [keys][dh], V [keys][dh] of sequence b, head h:
+    N(0, std^2) draws (PCG64 seeded with (seed, 3, b, h)) rounded to bfloat16."""
+    g = np.random.default_rng([seed, STREAM_NOISE + 1, b, h])
+    q = g.standard_normal((rows, dh), dtype=np.float32) * np.float32(std)
+    k = g.standard_normal((keys, dh), dtype=np.float32) * np.float32(std)
+    v = g.standard_normal((keys, dh), dtype=np.float32)
+    return round_bf16(q), round_bf16(k), round_bf16(v)
+
+
+def attention_batch(seed: int, B: int, H: int, rows: int, keys: int, dh: int,
+                    std: float = 1.0) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """attention_inputs stacked to [B][H][rows or keys][dh]."""
+    q = np.empty((B, H, rows, dh), np.float32)
+    k = np.empty((B, H, keys, dh), np.float32)
+    v = np.empty((B, H, keys, dh), np.float32)
+    for b in range(B):
+        for h in range(H):
+            q[b, h], k[b, h], v[b, h] = attention_inputs(seed, b, h, rows, keys, dh, std)
+    return q, k, v

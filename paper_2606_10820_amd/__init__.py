@@ -6,5 +6,6 @@ argument marshalling only.  PyTorch supplies device memory and the stream.
 """
 from .binding import (  # noqa: F401
     KF_BF16, KF_EHIP, KF_ECTX, KF_EINVAL, KF_ENOMEM, KF_ESTATE, KF_FLAG_DEBUG_LOGITS, KF_FP32,
-    KF_KC_NAMES, KF_OK, KfConfig, KfError, KForcing, lib, lib_path,
+    KF_KC_NAMES, KF_MASK_DOUBLE, KF_MASK_SINGLE, KF_OK, KfConfig, KfError, KForcing, lib,
+    lib_path, training_attention, training_attention_shapes,
 )

@@ -20,6 +20,7 @@ KF_OK, KF_EINVAL, KF_ESTATE, KF_ECTX, KF_ENOMEM, KF_EHIP = 0, -1, -2, -3, -4, -5
 KF_FP32, KF_BF16 = 0, 1
 KF_FLAG_DEBUG_LOGITS = 1
 KF_FLAG_TEMPERATURE = 2
+KF_MASK_SINGLE, KF_MASK_DOUBLE = 0, 1
 KF_KC_NAMES = ["embed", "noise", "norm", "qkv", "attn", "oproj", "mlp_up", "mlp_down", "head",
                "select"]
 KF_TIMING_ALL = (1 << len(KF_KC_NAMES)) - 1
@@ -80,6 +81,7 @@ def lib():
         "kf_destroy": (None, [P]),
         "kf_last_error": (ctypes.c_char_p, [P]),
         "kf_strerror": (ctypes.c_char_p, [I]),
+        "kf_training_attention": (I, [P, I, I, I, I, I, I, P, P, P, P, ctypes.c_float]),
     }
     for name, (res, args) in sigs.items():
         f = getattr(L, name)
@@ -245,3 +247,51 @@ class KForcing:
         ms, n = ctypes.c_double(), ctypes.c_int()
         self._check(self.L.kf_kernel_time(self.h, cls, ctypes.byref(ms), ctypes.byref(n)))
         return ms.value, n.value
+
+
+def training_attention_shapes(mask: int, N: int, k: int):
+    """(query rows, keys) of one sequence under a training mask."""
+    if mask == KF_MASK_SINGLE:
+        return N + N * k, N + N * k
+    return 2 * N * k, N + 2 * N * k
+
+
+def training_attention_entries(mask: int, N: int, k: int) -> int:
+    """Visible (query, key) pairs of one sequence under a training mask: the
+    algorithmic work (4 * d_head flops each) of kf_training_attention."""
+    ctx = N * (N + 1) // 2                      # context rows, causal
+    noise = k * N * (N + 1) // 2 + N * k * (k + 1) // 2   # staircase + in-group causal
+    if mask == KF_MASK_SINGLE:
+        return ctx + noise
+    # Future-1 rows as the noise rows above; Future-2 rows add all k Future-1 keys
+    return 2 * noise + N * k * k
+
+
+def training_attention(mask: int, q, k_, v, N: int, k: int, scale: Optional[float] = None,
+                       out=None, stream=None):
+    """Attention of the training masks (kf_training_attention).
+
+    q [B][H][rows][dh], k_/v [B][H][keys][dh]: contiguous bf16 device tensors.
+    Returns out (allocated like q when None).  The call is asynchronous on
+    `stream` (default: torch's current stream)."""
+    import torch
+    B, H, rows, dh = q.shape
+    if (rows, k_.shape[2]) != training_attention_shapes(mask, N, k):
+        raise ValueError("q/k rows do not match the mask's layout")
+    for t in (q, k_, v):
+        if t.dtype != torch.bfloat16 or not t.is_contiguous() or not t.is_cuda:
+            raise ValueError("q, k, v must be contiguous bf16 device tensors")
+    if k_.shape != v.shape or k_.shape[:2] != (B, H) or k_.shape[3] != dh:
+        raise ValueError("k and v must be [B][H][keys][dh] like q")
+    if out is None:
+        out = torch.empty_like(q)
+    if scale is None:
+        scale = dh ** -0.5
+    s = stream if stream is not None else torch.cuda.current_stream(q.device)
+    rc = lib().kf_training_attention(
+        ctypes.c_void_p(s.cuda_stream), mask, B, H, N, k, dh, ctypes.c_void_p(q.data_ptr()),
+        ctypes.c_void_p(k_.data_ptr()), ctypes.c_void_p(v.data_ptr()),
+        ctypes.c_void_p(out.data_ptr()), float(scale))
+    if rc != KF_OK:
+        raise KfError(rc, lib().kf_strerror(rc).decode())
+    return out

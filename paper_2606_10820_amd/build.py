@@ -15,7 +15,7 @@ CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libkforcing.so")
 BUILD_DIR = os.path.join(PKG, "_build")
 
-SOURCES = ["kf_api.cpp", "kf_kernels.hip", "kf_gemm.hip"]
+SOURCES = ["kf_api.cpp", "kf_kernels.hip", "kf_gemm.hip", "kf_blockattn.hip"]
 HEADERS = ["kf_internal.h"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

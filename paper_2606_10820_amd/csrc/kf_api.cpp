@@ -885,4 +885,27 @@ int kf_kernel_time(kf_ctx* c, int cls, double* total_ms, int* launches) {
   return KF_OK;
 }
 
+int kf_training_attention(void* hip_stream, int mask, int B, int H, int N, int k, int d_head,
+                          const void* Q, const void* K, const void* V, void* O, float scale) {
+  if (mask != KF_MASK_SINGLE && mask != KF_MASK_DOUBLE) return KF_EINVAL;
+  if (B < 0 || H < 0 || N < 0 || k < 1) return KF_EINVAL;
+  if (d_head != 32 && d_head != 64 && d_head != 128) return KF_EINVAL;
+  if (!isfinite(scale)) return KF_EINVAL;
+  if (B == 0 || H == 0 || N == 0) return KF_OK;
+  const void* ptrs[4] = {Q, K, V, O};
+  for (const void* q : ptrs)
+    if (!q || (reinterpret_cast<uintptr_t>(q) & 15)) return KF_EINVAL;
+  const int64_t nk = (int64_t)N * k;
+  const int64_t rows = mask == KF_MASK_SINGLE ? N + nk : 2 * nk;
+  const int64_t keys = mask == KF_MASK_SINGLE ? N + nk : N + 2 * nk;
+  const int64_t lim = (int64_t)1 << 31;
+  if (keys * d_head >= lim || (int64_t)B * H >= lim || (int64_t)B * H * ((rows + 63) / 64) >= lim)
+    return KF_EINVAL;
+  const hipError_t e = kf::launch_training_attention(
+      mask, B, H, N, k, d_head, static_cast<const bf16*>(Q), static_cast<const bf16*>(K),
+      static_cast<const bf16*>(V), static_cast<bf16*>(O), scale,
+      static_cast<hipStream_t>(hip_stream));
+  return e == hipSuccess ? KF_OK : KF_EHIP;
+}
+
 }  // extern "C"

@@ -206,4 +206,13 @@ hipError_t launch_zero(T* dst, size_t n, hipStream_t s);
 hipError_t launch_copy_f32(const float* src, float* dst, size_t n, hipStream_t s);
 hipError_t launch_zero_i32(int* dst, size_t n, hipStream_t s);
 
+// Attention under a training mask (KF_MASK_SINGLE / KF_MASK_DOUBLE of
+// include/kforcing.h): Q [B*H][rows][dh], K, V [B*H][keys][dh], O like Q, bf16;
+// dh in {32, 64, 128}.  rows and keys as given by the two helpers.
+int training_attention_rows(int mask, int N, int k);
+int training_attention_keys(int mask, int N, int k);
+hipError_t launch_training_attention(int mask, int B, int H, int N, int k, int dh, const bf16* Q,
+                                     const bf16* K, const bf16* V, bf16* O, float scale,
+                                     hipStream_t s);
+
 }  // namespace kf

@@ -161,6 +161,48 @@ def test_temperature_entry_point_checks(L):
     L.kf_destroy(h)
 
 
+def test_training_attention_argument_checks(L):
+    P = ctypes.c_void_p
+    a = P(0x10000)  # 16-byte aligned, never dereferenced: each call fails validation first
+    ok = dict(mask=0, B=2, H=3, N=8, k=4, dh=64)
+
+    def call(**kw):
+        x = dict(ok, **kw)
+        ptrs = kw.get("ptrs", (a, a, a, a))
+        return L.kf_training_attention(None, x["mask"], x["B"], x["H"], x["N"], x["k"], x["dh"],
+                                       *ptrs, kw.get("scale", 0.125))
+
+    assert call(mask=2) == Bd.KF_EINVAL
+    assert call(mask=-1) == Bd.KF_EINVAL
+    assert call(k=0) == Bd.KF_EINVAL
+    assert call(B=-1) == Bd.KF_EINVAL
+    assert call(N=-3) == Bd.KF_EINVAL
+    for dh in (0, 16, 48, 96, 256):
+        assert call(dh=dh) == Bd.KF_EINVAL
+    assert call(scale=float("inf")) == Bd.KF_EINVAL
+    assert call(scale=float("nan")) == Bd.KF_EINVAL
+    assert call(ptrs=(a, None, a, a)) == Bd.KF_EINVAL
+    assert call(ptrs=(a, a, P(0x10008), a)) == Bd.KF_EINVAL  # misaligned
+    # per-head keys * d_head must stay below 2^31: N + 2Nk = 2^25 + ... keys at d_head 64
+    assert call(mask=1, N=1 << 22, k=4) == Bd.KF_EINVAL
+    # empty problems succeed without touching the (null) pointers or a device
+    for mask in (0, 1):
+        assert call(mask=mask, B=0, ptrs=(None,) * 4) == Bd.KF_OK
+        assert call(mask=mask, N=0, ptrs=(None,) * 4) == Bd.KF_OK
+        assert call(mask=mask, H=0, ptrs=(None,) * 4) == Bd.KF_OK
+
+
+def test_training_attention_shapes():
+    import oracle as O
+    assert Bd.training_attention_shapes(Bd.KF_MASK_SINGLE, 5, 3) == (20, 20)
+    assert Bd.training_attention_shapes(Bd.KF_MASK_DOUBLE, 5, 3) == (30, 35)
+    for N, k in [(1, 1), (5, 3), (17, 4), (9, 8)]:
+        for mask, kind in ((Bd.KF_MASK_SINGLE, "single"), (Bd.KF_MASK_DOUBLE, "double")):
+            M = O.training_mask(kind, N, k)
+            assert M.shape == Bd.training_attention_shapes(mask, N, k)
+            assert Bd.training_attention_entries(mask, N, k) == int(M.sum())
+
+
 def test_null_context(L):
     assert L.kf_prefill(None, 1, 1, None, 1, None, None) == Bd.KF_EINVAL
     assert L.kf_create(None, None, None) == Bd.KF_EINVAL
