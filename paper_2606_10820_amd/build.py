@@ -16,7 +16,7 @@ OUT = os.path.join(PKG, "libkforcing.so")
 BUILD_DIR = os.path.join(PKG, "_build")
 
 SOURCES = ["kf_api.cpp", "kf_kernels.hip", "kf_gemm.hip", "kf_blockattn.hip"]
-HEADERS = ["kf_internal.h"]
+HEADERS = ["kf_internal.h", "kf_lds.h"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
@@ -29,9 +29,15 @@ FLAGS = [
 ]
 
 
+# Per-source flags.  The training attention rescales its MFMA accumulators
+# with VALU code inside the key loop; its inline-asm LDS reads would otherwise
+# make the compiler keep the accumulators in AGPRs and copy them every tile.
+SOURCE_FLAGS = {"kf_blockattn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-    cmd = [HIPCC] + FLAGS + ["-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC] + FLAGS + SOURCE_FLAGS.get(src, []) + ["-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")

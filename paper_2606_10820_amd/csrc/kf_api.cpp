@@ -14,7 +14,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/kforcing.h"
+#include "kforcing.h"
 #include "kf_internal.h"
 
 namespace {

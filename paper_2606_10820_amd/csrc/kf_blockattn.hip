@@ -13,23 +13,30 @@
 // Every query row therefore sees at most three key intervals, one in each of
 // the disjoint key regions (context, first noise block, second noise block).
 // A workgroup owns 64 consecutive query rows (16 per wavefront) and walks only
-// the union of their intervals, region by region, in 64-key tiles staged in
-// LDS and shared by its four wavefronts.  A wavefront skips a tile that misses
-// all of its rows and applies the per-element mask only on tiles that are not
-// fully visible to all of them.  The work is O(|M|), not O((N + Nk)^2).
+// the union of their intervals, region by region, in 64-key tiles that travel
+// from HBM straight into an S-stage LDS ring (buffer loads with the lds
+// modifier; keys past the interval read as zero) and are shared by its four
+// wavefronts.  A wavefront skips a tile that misses all of its rows and
+// applies the per-element mask only on tiles that are not fully visible to
+// all of them.  The work is O(|M|), not O((N + Nk)^2).
 //
 //   S^T = K Q^T on v_mfma_f32_16x16x32_bf16, keys as the A operand; a lane
 //   ends up with query lq and keys 16g + 4gq + r (g, r = 0..3).
-//   Online softmax in fp32 (base 2, the scale folded into the exponent).
+//   Online softmax in fp32, base 2 with the scale folded into one FMA; the
+//   running maximum is raised only when it grows by more than 2^8.
 //   O^T += V^T P^T: the lane's probabilities of key blocks 2c and 2c+1 are the
-//   B operand of chunk c directly; the value tile is stored transposed in LDS
-//   with its key slots permuted to the same order, so that each A operand is
-//   one 16-byte LDS read.
+//   B operand of chunk c directly, and the A operand comes from the natural
+//   [key][d_head] value tile through transposing LDS reads (ds_read_b64_tr_b16)
+//   whose row addresses put keys in that same order.
 #include <limits.h>
 #include <math.h>
 
-#include "../../include/kforcing.h"
+#include <type_traits>
+#include <utility>
+
+#include "kforcing.h"
 #include "kf_internal.h"
+#include "kf_lds.h"
 
 namespace kf {
 namespace {
@@ -82,92 +89,97 @@ __device__ inline Intervals row_intervals(int mask, int N, int k, int row) {
 // a[s] for a runtime s in 0..2 without indexing a register array
 __device__ inline int pick(const int (&a)[3], int s) { return s == 0 ? a[0] : (s == 1 ? a[1] : a[2]); }
 
-// LDS key slot of the 4-key group kg (keys 4kg..4kg+3 of a tile) in the
-// transposed value tile: key 16g' + 4gq' + r of a 32-key chunk sits at slot
-// 8gq' + 4g' + r, the order in which a lane holds its probabilities.
-__device__ inline int v_slot(int kg) { return 32 * (kg >> 3) + 8 * (kg & 3) + 4 * ((kg >> 2) & 1); }
+template <int... I, typename F>
+__device__ inline void static_for_impl(std::integer_sequence<int, I...>, F&& f) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ inline void static_for(F&& f) {
+  static_for_impl(std::make_integer_sequence<int, N>{}, f);
+}
 
-template <int DH>
-struct TileRegs {
-  static constexpr int NK = DH / 32;                  // 16-byte key chunks per thread
-  static constexpr int NV = (4 * DH + 255) / 256;     // 4x4 value blocks per thread
-  uint4 k[NK];
-  uint2 v[NV][4];
+// Cross-lane reductions over the four 16-lane groups (lanes l, l^16, l^32, l^48)
+// with the gfx950 permlane swaps (VALU, no LDS traffic).
+__device__ inline float max_xor16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ inline float max_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+// max of three without the NaN-quieting copies that fmaxf adds (scores are
+// finite or -inf here)
+__device__ inline float max3(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
+// Tile geometry.  A stage holds the K tile then the V tile, each [64 keys]
+// [DH] bf16 in natural layout with 16-byte chunks permuted within each row:
+// logical chunk c of key row r sits at chunk c ^ swz(r).  swz makes both
+// readers conflict-free: the K reads (16 consecutive rows, one logical chunk)
+// and the transposing V reads (8 consecutive rows, two adjacent chunks).
+template <int DH, int S_>
+struct Geo {
+  static constexpr int ROWB = DH * 2;           // bytes per key row
+  static constexpr int TILEB = kKT * ROWB;      // bytes of one K or V tile
+  static constexpr int SEGW = TILEB / 1024 / 4; // 1 KB DMA segments per wavefront per tensor
+  static constexpr int NCH = DH / 8;            // 16-byte chunks per row
+  static constexpr int RP = 128 / DH;           // rows per 256 bytes (the 64 LDS banks)
+  static constexpr int S = S_;                  // pipeline stages
+  static constexpr int PER = 2 * SEGW;          // DMA instructions per wavefront per tile
+  static constexpr int STAGEB = 2 * TILEB;
 };
 
-// Global -> registers: keys t0..t0+63 of K and V ([key][DH] per head); keys at
-// or past end read as zero.
 template <int DH>
-__device__ inline void load_tile(TileRegs<DH>& r, const bf16* Kh, const bf16* Vh, int t0, int end,
-                                 int tid) {
-#pragma unroll
-  for (int i = 0; i < TileRegs<DH>::NK; ++i) {
-    const int c = tid + 256 * i, key = t0 + c / (DH / 8), col = (c % (DH / 8)) * 8;
-    r.k[i] = key < end ? *reinterpret_cast<const uint4*>(Kh + (size_t)key * DH + col)
-                       : make_uint4(0, 0, 0, 0);
-  }
-#pragma unroll
-  for (int i = 0; i < TileRegs<DH>::NV; ++i) {
-    const int c = tid + 256 * i, kg = c & 15, cg = c >> 4;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int key = t0 + 4 * kg + e;
-      r.v[i][e] = (c < 4 * DH && key < end)
-                      ? *reinterpret_cast<const uint2*>(Vh + (size_t)key * DH + 4 * cg)
-                      : make_uint2(0, 0);
-    }
-  }
+__device__ inline int swz(int r) {
+  constexpr int NCH = DH / 8, RP = 128 / DH;
+  const int m = (r / RP) % NCH;
+  return ((m & (NCH / 2 - 1)) << 1) | (m / (NCH / 2));
 }
 
-// Registers -> LDS: keys as [key][DH + 8]; values transposed, [DH][64 + 8]
-// with permuted key slots (v_slot).
-template <int DH>
-__device__ inline void store_tile(const TileRegs<DH>& r, bf16* sK, bf16* sV, int tid) {
-  constexpr int KLD = DH + 8, VLD = kKT + 8;
-#pragma unroll
-  for (int i = 0; i < TileRegs<DH>::NK; ++i) {
-    const int c = tid + 256 * i, key = c / (DH / 8), col = (c % (DH / 8)) * 8;
-    *reinterpret_cast<uint4*>(sK + key * KLD + col) = r.k[i];
-  }
-#pragma unroll
-  for (int i = 0; i < TileRegs<DH>::NV; ++i) {
-    const int c = tid + 256 * i, kg = c & 15, cg = c >> 4;
-    if (c < 4 * DH) {
-      const uint2* x = r.v[i];
-      bf16* dst = sV + (4 * cg) * VLD + v_slot(kg);
-      // column e of the 4x4 block (keys 4kg..4kg+3, d_head 4cg..4cg+3)
-      const uint2 c0 = make_uint2((x[0].x & 0xffffu) | (x[1].x << 16), (x[2].x & 0xffffu) | (x[3].x << 16));
-      const uint2 c1 = make_uint2((x[0].x >> 16) | (x[1].x & 0xffff0000u), (x[2].x >> 16) | (x[3].x & 0xffff0000u));
-      const uint2 c2 = make_uint2((x[0].y & 0xffffu) | (x[1].y << 16), (x[2].y & 0xffffu) | (x[3].y << 16));
-      const uint2 c3 = make_uint2((x[0].y >> 16) | (x[1].y & 0xffff0000u), (x[2].y >> 16) | (x[3].y & 0xffff0000u));
-      *reinterpret_cast<uint2*>(dst) = c0;
-      *reinterpret_cast<uint2*>(dst + VLD) = c1;
-      *reinterpret_cast<uint2*>(dst + 2 * VLD) = c2;
-      *reinterpret_cast<uint2*>(dst + 3 * VLD) = c3;
-    }
-  }
-}
-
-template <int DH>
+template <int DH, int S>
 __global__ void __launch_bounds__(256)
     training_attention_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
                               const bf16* __restrict__ V, bf16* __restrict__ O, int mask, int N,
-                              int k, int nq, int nk, int BH, float scale_log2) {
-  constexpr int NDC = DH / 32, NDB = DH / 16, KLD = DH + 8, VLD = kKT + 8;
-  __shared__ __attribute__((aligned(16))) bf16 sK[2][kKT * KLD];
-  __shared__ __attribute__((aligned(16))) bf16 sV[2][DH * VLD];
+                              int k, int nq, int nk, int BH, float c2) {
+  using G = Geo<DH, S>;
+  constexpr int NDC = DH / 32, NDB = DH / 16;
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[S * G::STAGEB];
 
-  // heaviest query blocks (latest rows) of every head first; consecutive
-  // workgroups take consecutive heads
+  // Work order: workgroups are dealt to the 8 XCDs round-robin, so XCD x
+  // runs the workgroups x, x + 8, ...; it is given a contiguous run of the
+  // (head, query block) list, head by head with the heaviest blocks (latest
+  // rows) first, so that the query blocks of one head share its keys and
+  // values through that XCD's L2.
   const int nqb = (nq + kQB - 1) / kQB;
-  const int qb = nqb - 1 - (int)(blockIdx.x / BH);
-  const size_t bh = blockIdx.x % BH;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, gq = lane >> 4, lq = lane & 15;
+  const int total = BH * nqb, x8 = blockIdx.x & 7, j8 = blockIdx.x >> 3;
+  const int t8 = x8 * (total >> 3) + min(x8, total & 7) + j8;
+  const int qb = nqb - 1 - t8 % nqb;
+  const size_t bh = t8 / nqb;
+  const int tid = threadIdx.x, lane = tid & 63, gq = lane >> 4, lq = lane & 15;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int q0 = qb * kQB;
   const bf16* Kh = K + bh * (size_t)nk * DH;
   const bf16* Vh = V + bh * (size_t)nk * DH;
 
+  // this lane's query row and its Q fragment (MFMA B operand: d_head 32c + 8gq..+7)
+  const int row = q0 + 16 * w + lq;
+  const bool valid = row < nq;
+  bf16x8_t qf[NDC];
+  {
+    const bf16* qrow = Q + (bh * nq + (valid ? row : 0)) * DH + 8 * gq;
+#pragma unroll
+    for (int c = 0; c < NDC; ++c)
+      qf[c] = valid ? __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(qrow + 32 * c))
+                    : bf16x8_t{};
+  }
+  vm_wait<0>();
+
   // key ranges of the workgroup: per region, the union over its 64 rows
+  // (an empty region has lo = hi = 0 and no tiles)
   int lo[3], hi[3], nt[3];
   {
     const Intervals v = q0 + lane < nq ? row_intervals(mask, N, k, q0 + lane) : no_intervals();
@@ -180,17 +192,15 @@ __global__ void __launch_bounds__(256)
         a = min(a, __shfl_xor(a, off, 64));
         b = max(b, __shfl_xor(b, off, 64));
       }
-      lo[s] = a;
-      hi[s] = b;
-      nt[s] = b > a ? (b - a + kKT - 1) / kKT : 0;
+      lo[s] = __builtin_amdgcn_readfirstlane(b > a ? a : 0);
+      hi[s] = __builtin_amdgcn_readfirstlane(b > a ? b : 0);
+      nt[s] = (hi[s] - lo[s] + kKT - 1) / kKT;
     }
   }
   const int ntiles = nt[0] + nt[1] + nt[2];
 
-  // this lane's query row; the wavefront's union (wlo, whi) and intersection
-  // (ilo, ihi) of its 16 rows' intervals per region
-  const int row = q0 + 16 * w + lq;
-  const bool valid = row < nq;
+  // the wavefront's union (wlo, whi) and intersection (ilo, ihi) of its 16
+  // rows' intervals per region
   const Intervals iv = valid ? row_intervals(mask, N, k, row) : no_intervals();
   int wlo[3], whi[3], ilo[3], ihi[3];
 #pragma unroll
@@ -206,120 +216,171 @@ __global__ void __launch_bounds__(256)
       c = max(c, __shfl_xor(c, off, 64));
       d = min(d, __shfl_xor(d, off, 64));
     }
-    wlo[s] = a;
-    whi[s] = b;
-    ilo[s] = c;
-    ihi[s] = d;
+    wlo[s] = __builtin_amdgcn_readfirstlane(a);
+    whi[s] = __builtin_amdgcn_readfirstlane(b);
+    ilo[s] = __builtin_amdgcn_readfirstlane(c);
+    ihi[s] = __builtin_amdgcn_readfirstlane(d);
   }
 
-  const bf16x8_t zero8 = {};
-  bf16x8_t qf[NDC];
-  {
-    const bf16* qrow = Q + (bh * nq + (valid ? row : 0)) * DH + 8 * gq;
+  // Tiles in order: region 0, 1, 2, each from its union's first key in steps
+  // of 64; tile ti lies in region (ti >= b1) + (ti >= b2).  Tiles past the
+  // last one load nothing.
+  const int b1 = nt[0], b2 = nt[0] + nt[1];
+  const int dt1 = lo[1] - lo[0] - kKT * b1, dt2 = lo[2] - lo[1] - kKT * nt[1];
+  const int de1 = hi[1] - hi[0], de2 = hi[2] - hi[1];
+  auto tile_t0 = [&](int ti) { return lo[0] + kKT * ti + (ti >= b1 ? dt1 : 0) + (ti >= b2 ? dt2 : 0); };
+  auto tile_end = [&](int ti) { return hi[0] + (ti >= b1 ? de1 : 0) + (ti >= b2 ? de2 : 0); };
+
+  // DMA: segment w + 4i of a tile is LDS bytes [1024 (w + 4i), +1024); lane L
+  // fills 16 of them, the chunk that the swizzle puts there
+  uint32_t voff[G::SEGW];
 #pragma unroll
-    for (int c = 0; c < NDC; ++c)
-      qf[c] = valid ? __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(qrow + 32 * c))
-                    : zero8;
+  for (int i = 0; i < G::SEGW; ++i) {
+    const int byte = (w + 4 * i) * 1024 + 16 * lane;
+    const int r = byte / G::ROWB, pc = (byte % G::ROWB) / 16;
+    voff[i] = r * G::ROWB + ((pc ^ swz<DH>(r)) * 16);
   }
-
-  // tile ti -> (region s, first key t0)
-  auto tile = [&](int ti, int& s, int& t0) {
-    s = ti < nt[0] ? 0 : (ti < nt[0] + nt[1] ? 1 : 2);
-    const int first = s == 0 ? 0 : (s == 1 ? nt[0] : nt[0] + nt[1]);
-    t0 = pick(lo, s) + (ti - first) * kKT;
+  auto issue = [&](int ti, int stage) {
+    const bool live = ti < ntiles;
+    const int t0 = live ? tile_t0(ti) : 0;
+    const int rows = live ? min(tile_end(ti) - t0, kKT) : 0;
+    const __amdgpu_buffer_rsrc_t rk = make_rsrc(Kh + (size_t)t0 * DH, rows * G::ROWB);
+    const __amdgpu_buffer_rsrc_t rv = make_rsrc(Vh + (size_t)t0 * DH, rows * G::ROWB);
+    unsigned char* st = smem + stage * G::STAGEB;
+#pragma unroll
+    for (int i = 0; i < G::SEGW; ++i) dma16(rk, voff[i], 0, st + (w + 4 * i) * 1024);
+#pragma unroll
+    for (int i = 0; i < G::SEGW; ++i) dma16(rv, voff[i], 0, st + G::TILEB + (w + 4 * i) * 1024);
   };
 
-  float m_run = -INFINITY, l_run = 0.f;
-  f32x4_t o[NDB];
+  // LDS read offsets of this lane within a tile.  K (MFMA A of S^T): key row
+  // 16g + lq, logical chunk 4c + gq.  V (transposing reads, MFMA A of O^T):
+  // key row 32c + 4gq + lq/4 (+16 for the upper half of the k-slots), d_head
+  // 16db + 4 (lq % 4), i.e. logical chunk 2db + (lq % 4) / 2, byte 8 (lq % 2).
+  uint32_t kofs[NDC], vofs[NDB];
+#pragma unroll
+  for (int c = 0; c < NDC; ++c) kofs[c] = lq * G::ROWB + (((4 * c + gq) ^ swz<DH>(lq)) * 16);
+  {
+    const int r = 4 * gq + (lq >> 2);
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+      vofs[db] = r * G::ROWB + (((2 * db + ((lq & 3) >> 1)) ^ swz<DH>(r)) * 16) + (lq & 1) * 8;
+  }
+
+  // running max (log2 units); o = unnormalised O^T; ls = the row sums of P,
+  // formed by the MFMA against a block of ones (every element of ls is the
+  // sum of this lane's query row, over the bf16 probabilities that o uses)
+  float m_run = -INFINITY;
+  f32x4_t o[NDB], ls = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int i = 0; i < NDB; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const bf16x8_t ones = {1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f};
 
-  TileRegs<DH> regs;
-  {
-    int s, t0;
-    tile(0, s, t0);
-    load_tile<DH>(regs, Kh, Vh, t0, pick(hi, s), tid);
-    store_tile<DH>(regs, sK[0], sV[0], tid);
-  }
-  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < S - 1; ++j) issue(j, j);
+  // per-region values of the current tile's region, updated where a region starts
+  int cwlo = 0, cwhi = 0, cilo = 0, cihi = 0, rlo = 0, rhi = 0;
 
   for (int ti = 0; ti < ntiles; ++ti) {
-    const int cur = ti & 1;
-    int s, t0;
-    tile(ti, s, t0);
-    if (ti + 1 < ntiles) {
-      int s1, t1;
-      tile(ti + 1, s1, t1);
-      load_tile<DH>(regs, Kh, Vh, t1, pick(hi, s1), tid);
+    vm_wait<(S - 2) * G::PER>();  // this wavefront's part of tile ti has landed
+    __builtin_amdgcn_s_barrier();  // ... and everyone's; stage (ti - 1) % S is free
+    issue(ti + S - 1, (ti + S - 1) % S);
+    if (ti == 0 || ti == b1 || ti == b2) {
+      const int rs = (ti >= b1) + (ti >= b2);
+      cwlo = pick(wlo, rs);
+      cwhi = pick(whi, rs);
+      cilo = pick(ilo, rs);
+      cihi = pick(ihi, rs);
+      rlo = pick(iv.lo, rs);
+      rhi = pick(iv.hi, rs);
     }
-    if (t0 < pick(whi, s) && t0 + kKT > pick(wlo, s)) {
-      const bf16* kb = sK[cur];
-      const bf16* vb = sV[cur];
-      f32x4_t sc[4];
+    const int t0 = tile_t0(ti);
+    if (t0 >= cwhi || t0 + kKT <= cwlo) continue;  // no row of this wavefront
+
+    const uint32_t kb = lds_addr(smem + (ti % S) * G::STAGEB), vb = kb + G::TILEB;
+    // S^T = K Q^T: lane holds query lq, keys 16g + 4gq + r
+    u32x4 a[4][NDC];
+    static_for<4>([&](auto g) {
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        sc[g] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int c = 0; c < NDC; ++c) a[g][c] = ds_read16_off<g * 16 * G::ROWB>(kb + kofs[c]);
+    });
+    lgkm_wait0();
+    // value fragments of all 64 keys, in flight during the S MFMAs and the softmax
+    u32x2 va[2][NDB], vc[2][NDB];
+    static_for<2>([&](auto c) {
+      static_for<NDB>([&](auto db) {
+        va[c][db] = ds_read_tr16_off<c * 32 * G::ROWB>(vb + vofs[db]);
+        vc[c][db] = ds_read_tr16_off<c * 32 * G::ROWB + 16 * G::ROWB>(vb + vofs[db]);
+      });
+    });
+    f32x4_t sc[4];
 #pragma unroll
-        for (int c = 0; c < NDC; ++c) {
-          const bf16x8_t a =
-              *reinterpret_cast<const bf16x8_t*>(kb + (16 * g + lq) * KLD + 32 * c + 8 * gq);
-          sc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[c], sc[g], 0, 0, 0);
-        }
+    for (int g = 0; g < 4; ++g) {
+      sc[g] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < NDC; ++c) {
+        pin(a[g][c]);
+        sc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a[g][c]),
+                                                        qf[c], sc[g], 0, 0, 0);
       }
-      // a tile serves its region's interval only (its last keys may spill
-      // into the next region, which has tiles of its own)
-      const bool full = t0 >= pick(ilo, s) && t0 + kKT <= pick(ihi, s);
-      const int rlo = pick(iv.lo, s), rhi = pick(iv.hi, s);
-      float x[16];
-      float tmax = -INFINITY;
+    }
+
+    // mask: a tile serves its own region's interval only (its last keys may
+    // spill into the next region, which has tiles of its own)
+    if (!(t0 >= cilo && t0 + kKT <= cihi)) {
+      const unsigned width = rhi > rlo ? (unsigned)(rhi - rlo) : 0u;
+      const int base = t0 + 4 * gq - rlo;
 #pragma unroll
       for (int g = 0; g < 4; ++g)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int key = t0 + 16 * g + 4 * gq + r;
-          float v = sc[g][r] * scale_log2;
-          if (!full && (key < rlo || key >= rhi)) v = -INFINITY;
-          x[4 * g + r] = v;
-          tmax = fmaxf(tmax, v);
-        }
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-      const float m_new = fmaxf(m_run, tmax);
-      const float ref = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = __builtin_amdgcn_exp2f(m_run - ref);
-      float psum = 0.f;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        x[i] = __builtin_amdgcn_exp2f(x[i] - ref);
-        psum += x[i];
-      }
-      l_run = l_run * alpha + psum;
-      m_run = m_new;
+        for (int r = 0; r < 4; ++r)
+          if ((unsigned)(base + 16 * g + r) >= width) sc[g][r] = -INFINITY;
+    }
+    float mx = max3(max3(sc[0][0], sc[0][1], sc[0][2]), max3(sc[0][3], sc[1][0], sc[1][1]),
+                    max3(sc[1][2], sc[1][3], sc[2][0]));
+    mx = max3(mx, max3(sc[2][1], sc[2][2], sc[2][3]), max3(sc[3][0], sc[3][1], sc[3][2]));
+    mx = max3(mx, sc[3][3], sc[3][3]);
+    mx = max_xor32(max_xor16(mx)) * c2;
+    // rescale only when the row maximum grows by more than 2^8: probabilities
+    // stay below 256, and the same reference serves numerator and denominator
+    const bool grow = mx > m_run + 8.f;
+    if (__builtin_amdgcn_ballot_w64(grow)) {
+      const float mn = grow ? mx : m_run;
+      const float alpha = __builtin_amdgcn_exp2f(m_run - mn);
+      ls *= alpha;
 #pragma unroll
       for (int db = 0; db < NDB; ++db) o[db] *= alpha;
-#pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        bf16x8_t pf;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) pf[i] = (bf16)x[8 * c + i];
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) {
-          const bf16x8_t a =
-              *reinterpret_cast<const bf16x8_t*>(vb + (16 * db + lq) * VLD + 32 * c + 8 * gq);
-          o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pf, o[db], 0, 0, 0);
-        }
-      }
+      m_run = mn;
     }
-    if (ti + 1 < ntiles) store_tile<DH>(regs, sK[cur ^ 1], sV[cur ^ 1], tid);
-    __syncthreads();
+    const float mref = m_run == -INFINITY ? 0.f : m_run;
+    bf16x8_t pf[2];
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        pf[g >> 1][4 * (g & 1) + r] = (bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(sc[g][r], c2, -mref));
+      }
+
+    ls = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[0], ls, 0, 0, 0);
+    ls = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[1], ls, 0, 0, 0);
+    // O^T += V^T P^T, keys 0..31 then 32..63
+    lgkm_wait0();
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        pin(va[c][db]);
+        pin(vc[c][db]);
+        const u32x4 x = {va[c][db].x, va[c][db].y, vc[c][db].x, vc[c][db].y};
+        o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, x), pf[c],
+                                                        o[db], 0, 0, 0);
+      }
   }
+  vm_wait<0>();  // tail loads of nonexistent tiles
 
   // lane: query lq, d_head 16db + 4gq + r
-  float l = l_run;
-  l += __shfl_xor(l, 16, 64);
-  l += __shfl_xor(l, 32, 64);
   if (valid) {
-    const float inv = 1.0f / l;
+    const float inv = 1.0f / ls[0];
     bf16* orow = O + (bh * nq + row) * DH + 4 * gq;
 #pragma unroll
     for (int db = 0; db < NDB; ++db) {
@@ -350,19 +411,19 @@ hipError_t launch_training_attention(int mask, int B, int H, int N, int k, int d
   const int nk = training_attention_keys(mask, N, k);
   const int BH = B * H;
   const dim3 grid((unsigned)BH * ((nq + kQB - 1) / kQB));
-  const float sl2 = scale * 1.4426950408889634f;
+  const float c2 = scale * 1.4426950408889634f;  // scale * log2(e)
   switch (dh) {
     case 32:
-      launch(training_attention_kernel<32>, grid, dim3(256), 0, s, Q, K, V, O, mask, N, k, nq, nk,
-             BH, sl2);
+      launch(training_attention_kernel<32, 3>, grid, dim3(256), 0, s, Q, K, V, O, mask, N, k, nq,
+             nk, BH, c2);
       break;
     case 64:
-      launch(training_attention_kernel<64>, grid, dim3(256), 0, s, Q, K, V, O, mask, N, k, nq, nk,
-             BH, sl2);
+      launch(training_attention_kernel<64, 2>, grid, dim3(256), 0, s, Q, K, V, O, mask, N, k, nq,
+             nk, BH, c2);
       break;
     case 128:
-      launch(training_attention_kernel<128>, grid, dim3(256), 0, s, Q, K, V, O, mask, N, k, nq,
-             nk, BH, sl2);
+      launch(training_attention_kernel<128, 2>, grid, dim3(256), 0, s, Q, K, V, O, mask, N, k, nq,
+             nk, BH, c2);
       break;
     default:
       return hipErrorInvalidValue;

@@ -18,6 +18,7 @@
 #include <type_traits>
 
 #include "kf_internal.h"
+#include "kf_lds.h"
 
 namespace kf {
 namespace {
@@ -25,7 +26,6 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));  // one 16-byte chunk
 
 __device__ inline float to_f(float x) { return x; }
 __device__ inline float to_f(bf16 x) { return (float)x; }
@@ -276,50 +276,6 @@ __device__ inline void tile_coords(int lin, int gm, int gn, int& tm, int& tn) {
   const int u = t - grp * gm * kGroupN;
   tm = u / width;
   tn = first + u % width;
-}
-
-// ------------------------------------------------------------ memory ops
-// Operand tiles travel from global memory straight into LDS (buffer loads
-// with the lds modifier: no register staging).  The compiler cannot track
-// those LDS writes against ordinary LDS reads and would wait for every
-// outstanding load before each read, which serialises the pipeline; so the
-// kernel reads its tiles with explicit ds_read_b128 instructions and manages
-// both counters itself: vmcnt before the barrier that publishes a stage,
-// lgkmcnt before the MFMAs that consume the reads.
-typedef __attribute__((address_space(3))) void* lds_ptr;
-
-__device__ inline uint32_t lds_addr(const void* p) {
-  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
-}
-
-__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
-                                           0x00020000);
-}
-
-// 16 bytes per lane, global byte offset voff + soff, into LDS at dst + 16 * lane
-// (dst is uniform across the wavefront).
-__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff,
-                                      void* dst) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr)dst, 16, voff, soff, 0, 0);
-}
-
-__device__ __forceinline__ u32x4 ds_read16(uint32_t addr) {
-  u32x4 v;
-  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr) : "memory");
-  return v;
-}
-
-__device__ __forceinline__ void lgkm_wait0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
-
-// Keeps a value's consumers after the preceding wait.
-__device__ __forceinline__ void pin(u32x4& v) { asm volatile("" : "+v"(v)); }
-
-// s_waitcnt with vmcnt = N and the other counters left alone (gfx9 encoding).
-template <int N>
-__device__ __forceinline__ void vm_wait() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
 // Which A row feeds GEMM row m (MODE 0: row m; 1: noise row m of the step;
