@@ -86,6 +86,46 @@ __device__ inline Intervals row_intervals(int mask, int N, int k, int row) {
   return v;
 }
 
+// Union [ulo, uhi) and intersection [ilo, ihi) per region of the intervals
+// of query rows [a, b) (a < b <= rows).  Within each part of the query rows
+// (single: context, noise; double: Future-1, Future-2) every endpoint is a
+// non-decreasing function of the row and a region is either empty for all
+// rows of the part or for none, so the first and last row of each part
+// decide.  An empty union is [0, 0); an empty intersection has ilo > ihi.
+__device__ inline void row_bounds(int mask, int N, int k, int a, int b, int (&ulo)[3],
+                                  int (&uhi)[3], int (&ilo)[3], int (&ihi)[3]) {
+  const int split = mask == KF_MASK_SINGLE ? N : N * k;
+#pragma unroll
+  for (int s = 0; s < 3; ++s) {
+    ulo[s] = INT_MAX;
+    uhi[s] = INT_MIN;
+    ilo[s] = INT_MIN;
+    ihi[s] = INT_MAX;
+  }
+  const int pa[2] = {a, max(a, split)}, pb[2] = {min(b, split), b};
+#pragma unroll
+  for (int part = 0; part < 2; ++part) {
+    if (pa[part] >= pb[part]) continue;
+    const Intervals f = row_intervals(mask, N, k, pa[part]);
+    const Intervals l = row_intervals(mask, N, k, pb[part] - 1);
+#pragma unroll
+    for (int s = 0; s < 3; ++s) {
+      if (f.lo[s] < f.hi[s]) {
+        ulo[s] = min(ulo[s], f.lo[s]);
+        uhi[s] = max(uhi[s], l.hi[s]);
+        ilo[s] = max(ilo[s], l.lo[s]);
+        ihi[s] = min(ihi[s], f.hi[s]);
+      } else {
+        ilo[s] = INT_MAX;
+        ihi[s] = INT_MIN;
+      }
+    }
+  }
+#pragma unroll
+  for (int s = 0; s < 3; ++s)
+    if (ulo[s] >= uhi[s]) ulo[s] = uhi[s] = 0;
+}
+
 // a[s] for a runtime s in 0..2 without indexing a register array
 __device__ inline int pick(const int (&a)[3], int s) { return s == 0 ? a[0] : (s == 1 ? a[1] : a[2]); }
 
@@ -140,6 +180,40 @@ __device__ inline int swz(int r) {
   return ((m & (NCH / 2 - 1)) << 1) | (m / (NCH / 2));
 }
 
+// Scalar geometry of one work item -- a head and a 64-row query block: the
+// workgroup's key ranges as a tile sequence.  Tiles run over region 0, 1, 2,
+// each from its union's first key in steps of 64; tile ti lies in region
+// (ti >= b1) + (ti >= b2).
+struct Item {
+  int bh, q0, ntiles, b1, b2, lo0, dt1, dt2, hi0, de1, de2;
+  __device__ int t0(int ti) const {
+    return lo0 + kKT * ti + (ti >= b1 ? dt1 : 0) + (ti >= b2 ? dt2 : 0);
+  }
+  __device__ int end(int ti) const { return hi0 + (ti >= b1 ? de1 : 0) + (ti >= b2 ? de2 : 0); }
+};
+
+// Item t of the (head, query block) list: head t / nqb, its blocks heaviest
+// (latest rows) first.
+__device__ inline Item make_item(int t, int nqb, int mask, int N, int k, int nq) {
+  Item it;
+  it.bh = t / nqb;
+  it.q0 = (nqb - 1 - (t - it.bh * nqb)) * kQB;
+  int lo[3], hi[3], ilo[3], ihi[3], nt[3];
+  row_bounds(mask, N, k, it.q0, min(it.q0 + kQB, nq), lo, hi, ilo, ihi);
+#pragma unroll
+  for (int s = 0; s < 3; ++s) nt[s] = (hi[s] - lo[s] + kKT - 1) / kKT;
+  it.ntiles = nt[0] + nt[1] + nt[2];
+  it.b1 = nt[0];
+  it.b2 = nt[0] + nt[1];
+  it.lo0 = lo[0];
+  it.dt1 = lo[1] - lo[0] - kKT * nt[0];
+  it.dt2 = lo[2] - lo[1] - kKT * nt[1];
+  it.hi0 = hi[0];
+  it.de1 = hi[1] - hi[0];
+  it.de2 = hi[2] - hi[1];
+  return it;
+}
+
 template <int DH, int S>
 __global__ void __launch_bounds__(256)
     training_attention_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
@@ -149,87 +223,15 @@ __global__ void __launch_bounds__(256)
   constexpr int NDC = DH / 32, NDB = DH / 16;
   __shared__ __attribute__((aligned(1024))) unsigned char smem[S * G::STAGEB];
 
-  // Work order: workgroups are dealt to the 8 XCDs round-robin, so XCD x
-  // runs the workgroups x, x + 8, ...; it is given a contiguous run of the
-  // (head, query block) list, head by head with the heaviest blocks (latest
-  // rows) first, so that the query blocks of one head share its keys and
-  // values through that XCD's L2.
-  const int nqb = (nq + kQB - 1) / kQB;
-  const int total = BH * nqb, x8 = blockIdx.x & 7, j8 = blockIdx.x >> 3;
-  const int t8 = x8 * (total >> 3) + min(x8, total & 7) + j8;
-  const int qb = nqb - 1 - t8 % nqb;
-  const size_t bh = t8 / nqb;
+  // Work order.  Workgroups are dealt to the 8 XCDs round-robin, so XCD x runs
+  // workgroups x, x + 8, ...  Each XCD is given a contiguous run of the item
+  // list (whole heads, one after another), so that the query blocks of one
+  // head share its keys and values through that XCD's L2.
+  const int nqb = (nq + kQB - 1) / kQB, total = BH * nqb;
+  const int x8 = blockIdx.x & 7, j8 = blockIdx.x >> 3;
+  const Item C = make_item(x8 * (total >> 3) + min(x8, total & 7) + j8, nqb, mask, N, k, nq);
   const int tid = threadIdx.x, lane = tid & 63, gq = lane >> 4, lq = lane & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int q0 = qb * kQB;
-  const bf16* Kh = K + bh * (size_t)nk * DH;
-  const bf16* Vh = V + bh * (size_t)nk * DH;
-
-  // this lane's query row and its Q fragment (MFMA B operand: d_head 32c + 8gq..+7)
-  const int row = q0 + 16 * w + lq;
-  const bool valid = row < nq;
-  bf16x8_t qf[NDC];
-  {
-    const bf16* qrow = Q + (bh * nq + (valid ? row : 0)) * DH + 8 * gq;
-#pragma unroll
-    for (int c = 0; c < NDC; ++c)
-      qf[c] = valid ? __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(qrow + 32 * c))
-                    : bf16x8_t{};
-  }
-  vm_wait<0>();
-
-  // key ranges of the workgroup: per region, the union over its 64 rows
-  // (an empty region has lo = hi = 0 and no tiles)
-  int lo[3], hi[3], nt[3];
-  {
-    const Intervals v = q0 + lane < nq ? row_intervals(mask, N, k, q0 + lane) : no_intervals();
-#pragma unroll
-    for (int s = 0; s < 3; ++s) {
-      const bool ne = v.lo[s] < v.hi[s];
-      int a = ne ? v.lo[s] : INT_MAX, b = ne ? v.hi[s] : 0;
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        a = min(a, __shfl_xor(a, off, 64));
-        b = max(b, __shfl_xor(b, off, 64));
-      }
-      lo[s] = __builtin_amdgcn_readfirstlane(b > a ? a : 0);
-      hi[s] = __builtin_amdgcn_readfirstlane(b > a ? b : 0);
-      nt[s] = (hi[s] - lo[s] + kKT - 1) / kKT;
-    }
-  }
-  const int ntiles = nt[0] + nt[1] + nt[2];
-
-  // the wavefront's union (wlo, whi) and intersection (ilo, ihi) of its 16
-  // rows' intervals per region
-  const Intervals iv = valid ? row_intervals(mask, N, k, row) : no_intervals();
-  int wlo[3], whi[3], ilo[3], ihi[3];
-#pragma unroll
-  for (int s = 0; s < 3; ++s) {
-    const bool ne = iv.lo[s] < iv.hi[s];
-    int a = ne ? iv.lo[s] : INT_MAX, b = ne ? iv.hi[s] : 0;
-    int c = valid ? (ne ? iv.lo[s] : INT_MAX) : INT_MIN;
-    int d = valid ? (ne ? iv.hi[s] : INT_MIN) : INT_MAX;
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) {
-      a = min(a, __shfl_xor(a, off, 64));
-      b = max(b, __shfl_xor(b, off, 64));
-      c = max(c, __shfl_xor(c, off, 64));
-      d = min(d, __shfl_xor(d, off, 64));
-    }
-    wlo[s] = __builtin_amdgcn_readfirstlane(a);
-    whi[s] = __builtin_amdgcn_readfirstlane(b);
-    ilo[s] = __builtin_amdgcn_readfirstlane(c);
-    ihi[s] = __builtin_amdgcn_readfirstlane(d);
-  }
-
-  // Tiles in order: region 0, 1, 2, each from its union's first key in steps
-  // of 64; tile ti lies in region (ti >= b1) + (ti >= b2).  Tiles past the
-  // last one load nothing.
-  const int b1 = nt[0], b2 = nt[0] + nt[1];
-  const int dt1 = lo[1] - lo[0] - kKT * b1, dt2 = lo[2] - lo[1] - kKT * nt[1];
-  const int de1 = hi[1] - hi[0], de2 = hi[2] - hi[1];
-  auto tile_t0 = [&](int ti) { return lo[0] + kKT * ti + (ti >= b1 ? dt1 : 0) + (ti >= b2 ? dt2 : 0); };
-  auto tile_end = [&](int ti) { return hi[0] + (ti >= b1 ? de1 : 0) + (ti >= b2 ? de2 : 0); };
 
   // DMA: segment w + 4i of a tile is LDS bytes [1024 (w + 4i), +1024); lane L
   // fills 16 of them, the chunk that the swizzle puts there
@@ -240,19 +242,6 @@ __global__ void __launch_bounds__(256)
     const int r = byte / G::ROWB, pc = (byte % G::ROWB) / 16;
     voff[i] = r * G::ROWB + ((pc ^ swz<DH>(r)) * 16);
   }
-  auto issue = [&](int ti, int stage) {
-    const bool live = ti < ntiles;
-    const int t0 = live ? tile_t0(ti) : 0;
-    const int rows = live ? min(tile_end(ti) - t0, kKT) : 0;
-    const __amdgpu_buffer_rsrc_t rk = make_rsrc(Kh + (size_t)t0 * DH, rows * G::ROWB);
-    const __amdgpu_buffer_rsrc_t rv = make_rsrc(Vh + (size_t)t0 * DH, rows * G::ROWB);
-    unsigned char* st = smem + stage * G::STAGEB;
-#pragma unroll
-    for (int i = 0; i < G::SEGW; ++i) dma16(rk, voff[i], 0, st + (w + 4 * i) * 1024);
-#pragma unroll
-    for (int i = 0; i < G::SEGW; ++i) dma16(rv, voff[i], 0, st + G::TILEB + (w + 4 * i) * 1024);
-  };
-
   // LDS read offsets of this lane within a tile.  K (MFMA A of S^T): key row
   // 16g + lq, logical chunk 4c + gq.  V (transposing reads, MFMA A of O^T):
   // key row 32c + 4gq + lq/4 (+16 for the upper half of the k-slots), d_head
@@ -266,27 +255,59 @@ __global__ void __launch_bounds__(256)
     for (int db = 0; db < NDB; ++db)
       vofs[db] = r * G::ROWB + (((2 * db + ((lq & 3) >> 1)) ^ swz<DH>(r)) * 16) + (lq & 1) * 8;
   }
+  const bf16x8_t ones = {1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f};
 
-  // running max (log2 units); o = unnormalised O^T; ls = the row sums of P,
-  // formed by the MFMA against a block of ones (every element of ls is the
-  // sum of this lane's query row, over the bf16 probabilities that o uses)
+  // Tiles past the last one load nothing, so every wavefront issues the same
+  // number of loads per tile.
+  auto issue = [&](int ti, int stage) {
+    const bool live = ti < C.ntiles;
+    const int t0 = live ? C.t0(ti) : 0;
+    const int rows = live ? min(C.end(ti) - t0, kKT) : 0;
+    const size_t off = ((size_t)C.bh * nk + t0) * DH;
+    const __amdgpu_buffer_rsrc_t rk = make_rsrc(K + off, rows * G::ROWB);
+    const __amdgpu_buffer_rsrc_t rv = make_rsrc(V + off, rows * G::ROWB);
+    unsigned char* st = smem + stage * G::STAGEB;
+#pragma unroll
+    for (int i = 0; i < G::SEGW; ++i) dma16(rk, voff[i], 0, st + (w + 4 * i) * 1024);
+#pragma unroll
+    for (int i = 0; i < G::SEGW; ++i) dma16(rv, voff[i], 0, st + G::TILEB + (w + 4 * i) * 1024);
+  };
+#pragma unroll
+  for (int j = 0; j < S - 1; ++j) issue(j, j);
+
+  // this lane's query row, its Q fragment (MFMA B operand: d_head 32c + 8gq..+7)
+  // and intervals; the wavefront's union (wlo, whi) and intersection (ilo, ihi)
+  // of its 16 rows' intervals per region
+  const int row = C.q0 + 16 * w + lq;
+  const bool valid = row < nq;
+  bf16x8_t qf[NDC];
+  {
+    const bf16* qrow = Q + ((size_t)C.bh * nq + (valid ? row : 0)) * DH + 8 * gq;
+#pragma unroll
+    for (int c = 0; c < NDC; ++c)
+      qf[c] = valid ? __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(qrow + 32 * c))
+                    : bf16x8_t{};
+  }
+  int wlo[3] = {0, 0, 0}, whi[3] = {0, 0, 0}, ilo[3] = {1, 1, 1}, ihi[3] = {0, 0, 0};
+  if (C.q0 + 16 * w < nq)
+    row_bounds(mask, N, k, C.q0 + 16 * w, min(C.q0 + 16 * w + 16, nq), wlo, whi, ilo, ihi);
+  const Intervals iv = valid ? row_intervals(mask, N, k, row) : no_intervals();
+  // running max m (log2 units); o = the unnormalised O^T; ls = the row sums of
+  // P, formed by the MFMA against a block of ones (each element of ls is the
+  // sum of this lane's query row over the bf16 probabilities that o uses)
   float m_run = -INFINITY;
   f32x4_t o[NDB], ls = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int i = 0; i < NDB; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  const bf16x8_t ones = {1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f};
 
-#pragma unroll
-  for (int j = 0; j < S - 1; ++j) issue(j, j);
   // per-region values of the current tile's region, updated where a region starts
   int cwlo = 0, cwhi = 0, cilo = 0, cihi = 0, rlo = 0, rhi = 0;
-
-  for (int ti = 0; ti < ntiles; ++ti) {
+  for (int ti = 0; ti < C.ntiles; ++ti) {
     vm_wait<(S - 2) * G::PER>();  // this wavefront's part of tile ti has landed
     __builtin_amdgcn_s_barrier();  // ... and everyone's; stage (ti - 1) % S is free
     issue(ti + S - 1, (ti + S - 1) % S);
-    if (ti == 0 || ti == b1 || ti == b2) {
-      const int rs = (ti >= b1) + (ti >= b2);
+    if (ti == 0 || ti == C.b1 || ti == C.b2) {
+      const int rs = (ti >= C.b1) + (ti >= C.b2);
       cwlo = pick(wlo, rs);
       cwhi = pick(whi, rs);
       cilo = pick(ilo, rs);
@@ -294,94 +315,92 @@ __global__ void __launch_bounds__(256)
       rlo = pick(iv.lo, rs);
       rhi = pick(iv.hi, rs);
     }
-    const int t0 = tile_t0(ti);
-    if (t0 >= cwhi || t0 + kKT <= cwlo) continue;  // no row of this wavefront
-
-    const uint32_t kb = lds_addr(smem + (ti % S) * G::STAGEB), vb = kb + G::TILEB;
-    // S^T = K Q^T: lane holds query lq, keys 16g + 4gq + r
-    u32x4 a[4][NDC];
-    static_for<4>([&](auto g) {
+    const int t0 = C.t0(ti);
+    if (t0 < cwhi && t0 + kKT > cwlo) {  // some row of this wavefront sees the tile
+      const uint32_t kb = lds_addr(smem + (ti % S) * G::STAGEB), vb = kb + G::TILEB;
+      // S^T = K Q^T: lane holds query lq, keys 16g + 4gq + r
+      u32x4 a[4][NDC];
+      static_for<4>([&](auto gg) {
 #pragma unroll
-      for (int c = 0; c < NDC; ++c) a[g][c] = ds_read16_off<g * 16 * G::ROWB>(kb + kofs[c]);
-    });
-    lgkm_wait0();
-    // value fragments of all 64 keys, in flight during the S MFMAs and the softmax
-    u32x2 va[2][NDB], vc[2][NDB];
-    static_for<2>([&](auto c) {
-      static_for<NDB>([&](auto db) {
-        va[c][db] = ds_read_tr16_off<c * 32 * G::ROWB>(vb + vofs[db]);
-        vc[c][db] = ds_read_tr16_off<c * 32 * G::ROWB + 16 * G::ROWB>(vb + vofs[db]);
+        for (int c = 0; c < NDC; ++c) a[gg][c] = ds_read16_off<gg * 16 * G::ROWB>(kb + kofs[c]);
       });
-    });
-    f32x4_t sc[4];
+      lgkm_wait0();
+      // value fragments of all 64 keys, in flight during the S MFMAs and the softmax
+      u32x2 va[2][NDB], vc[2][NDB];
+      static_for<2>([&](auto c) {
+        static_for<NDB>([&](auto db) {
+          va[c][db] = ds_read_tr16_off<c * 32 * G::ROWB>(vb + vofs[db]);
+          vc[c][db] = ds_read_tr16_off<c * 32 * G::ROWB + 16 * G::ROWB>(vb + vofs[db]);
+        });
+      });
+      f32x4_t sc[4];
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      sc[g] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int gg = 0; gg < 4; ++gg) {
+        sc[gg] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int c = 0; c < NDC; ++c) {
-        pin(a[g][c]);
-        sc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a[g][c]),
-                                                        qf[c], sc[g], 0, 0, 0);
+        for (int c = 0; c < NDC; ++c) {
+          pin(a[gg][c]);
+          sc[gg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a[gg][c]),
+                                                           qf[c], sc[gg], 0, 0, 0);
+        }
       }
-    }
-
-    // mask: a tile serves its own region's interval only (its last keys may
-    // spill into the next region, which has tiles of its own)
-    if (!(t0 >= cilo && t0 + kKT <= cihi)) {
-      const unsigned width = rhi > rlo ? (unsigned)(rhi - rlo) : 0u;
-      const int base = t0 + 4 * gq - rlo;
+      // mask: a tile serves its own region's interval only (its last keys may
+      // spill into the next region, which has tiles of its own)
+      if (!(t0 >= cilo && t0 + kKT <= cihi)) {
+        const unsigned width = rhi > rlo ? (unsigned)(rhi - rlo) : 0u;
+        const int base = t0 + 4 * gq - rlo;
 #pragma unroll
-      for (int g = 0; g < 4; ++g)
+        for (int gg = 0; gg < 4; ++gg)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if ((unsigned)(base + 16 * gg + r) >= width) sc[gg][r] = -INFINITY;
+      }
+      float mx = max3(max3(sc[0][0], sc[0][1], sc[0][2]), max3(sc[0][3], sc[1][0], sc[1][1]),
+                      max3(sc[1][2], sc[1][3], sc[2][0]));
+      mx = max3(mx, max3(sc[2][1], sc[2][2], sc[2][3]), max3(sc[3][0], sc[3][1], sc[3][2]));
+      mx = max3(mx, sc[3][3], sc[3][3]);
+      mx = max_xor32(max_xor16(mx)) * c2;
+      // rescale only when the row maximum grows by more than 2^8: probabilities
+      // stay below 256, and the same reference serves numerator and denominator
+      const bool grow = mx > m_run + 8.f;
+      if (__builtin_amdgcn_ballot_w64(grow)) {
+        const float mn = grow ? mx : m_run;
+        const float alpha = __builtin_amdgcn_exp2f(m_run - mn);
+        ls *= alpha;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) o[db] *= alpha;
+        m_run = mn;
+      }
+      const float mref = m_run == -INFINITY ? 0.f : m_run;
+      bf16x8_t pf[2];
+#pragma unroll
+      for (int gg = 0; gg < 4; ++gg)
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          if ((unsigned)(base + 16 * g + r) >= width) sc[g][r] = -INFINITY;
+          pf[gg >> 1][4 * (gg & 1) + r] =
+              (bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(sc[gg][r], c2, -mref));
+      ls = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[0], ls, 0, 0, 0);
+      ls = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[1], ls, 0, 0, 0);
+      // O^T += V^T P^T, keys 0..31 then 32..63
+      lgkm_wait0();
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+          pin(va[c][db]);
+          pin(vc[c][db]);
+          const u32x4 x = {va[c][db].x, va[c][db].y, vc[c][db].x, vc[c][db].y};
+          o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, x), pf[c],
+                                                          o[db], 0, 0, 0);
+        }
     }
-    float mx = max3(max3(sc[0][0], sc[0][1], sc[0][2]), max3(sc[0][3], sc[1][0], sc[1][1]),
-                    max3(sc[1][2], sc[1][3], sc[2][0]));
-    mx = max3(mx, max3(sc[2][1], sc[2][2], sc[2][3]), max3(sc[3][0], sc[3][1], sc[3][2]));
-    mx = max3(mx, sc[3][3], sc[3][3]);
-    mx = max_xor32(max_xor16(mx)) * c2;
-    // rescale only when the row maximum grows by more than 2^8: probabilities
-    // stay below 256, and the same reference serves numerator and denominator
-    const bool grow = mx > m_run + 8.f;
-    if (__builtin_amdgcn_ballot_w64(grow)) {
-      const float mn = grow ? mx : m_run;
-      const float alpha = __builtin_amdgcn_exp2f(m_run - mn);
-      ls *= alpha;
-#pragma unroll
-      for (int db = 0; db < NDB; ++db) o[db] *= alpha;
-      m_run = mn;
-    }
-    const float mref = m_run == -INFINITY ? 0.f : m_run;
-    bf16x8_t pf[2];
-#pragma unroll
-    for (int g = 0; g < 4; ++g)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        pf[g >> 1][4 * (g & 1) + r] = (bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(sc[g][r], c2, -mref));
-      }
-
-    ls = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[0], ls, 0, 0, 0);
-    ls = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[1], ls, 0, 0, 0);
-    // O^T += V^T P^T, keys 0..31 then 32..63
-    lgkm_wait0();
-#pragma unroll
-    for (int c = 0; c < 2; ++c)
-#pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-        pin(va[c][db]);
-        pin(vc[c][db]);
-        const u32x4 x = {va[c][db].x, va[c][db].y, vc[c][db].x, vc[c][db].y};
-        o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, x), pf[c],
-                                                        o[db], 0, 0, 0);
-      }
   }
-  vm_wait<0>();  // tail loads of nonexistent tiles
+  vm_wait<0>();  // loads issued for tiles past the last one
 
   // lane: query lq, d_head 16db + 4gq + r
   if (valid) {
     const float inv = 1.0f / ls[0];
-    bf16* orow = O + (bh * nq + row) * DH + 4 * gq;
+    bf16* orow = O + ((size_t)C.bh * nq + row) * DH + 4 * gq;
 #pragma unroll
     for (int db = 0; db < NDB; ++db) {
       const bf16 e0 = (bf16)(o[db][0] * inv), e1 = (bf16)(o[db][1] * inv);
@@ -404,31 +423,32 @@ int training_attention_keys(int mask, int N, int k) {
   return mask == KF_MASK_SINGLE ? N + N * k : N + 2 * N * k;
 }
 
-hipError_t launch_training_attention(int mask, int B, int H, int N, int k, int dh, const bf16* Q,
-                                     const bf16* K, const bf16* V, bf16* O, float scale,
-                                     hipStream_t s) {
+namespace {
+
+template <int DH, int S>
+hipError_t launch_ta(int mask, int B, int H, int N, int k, const bf16* Q, const bf16* K,
+                     const bf16* V, bf16* O, float scale, hipStream_t s) {
   const int nq = training_attention_rows(mask, N, k);
   const int nk = training_attention_keys(mask, N, k);
   const int BH = B * H;
-  const dim3 grid((unsigned)BH * ((nq + kQB - 1) / kQB));
+  const dim3 grid((unsigned)((long long)BH * ((nq + kQB - 1) / kQB)));  // one workgroup per item
   const float c2 = scale * 1.4426950408889634f;  // scale * log2(e)
-  switch (dh) {
-    case 32:
-      launch(training_attention_kernel<32, 3>, grid, dim3(256), 0, s, Q, K, V, O, mask, N, k, nq,
-             nk, BH, c2);
-      break;
-    case 64:
-      launch(training_attention_kernel<64, 2>, grid, dim3(256), 0, s, Q, K, V, O, mask, N, k, nq,
-             nk, BH, c2);
-      break;
-    case 128:
-      launch(training_attention_kernel<128, 2>, grid, dim3(256), 0, s, Q, K, V, O, mask, N, k, nq,
-             nk, BH, c2);
-      break;
-    default:
-      return hipErrorInvalidValue;
-  }
+  launch(training_attention_kernel<DH, S>, grid, dim3(256), 0, s, Q, K, V, O, mask, N, k, nq, nk,
+         BH, c2);
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_training_attention(int mask, int B, int H, int N, int k, int dh, const bf16* Q,
+                                     const bf16* K, const bf16* V, bf16* O, float scale,
+                                     hipStream_t s) {
+  switch (dh) {
+    case 32: return launch_ta<32, 3>(mask, B, H, N, k, Q, K, V, O, scale, s);
+    case 64: return launch_ta<64, 2>(mask, B, H, N, k, Q, K, V, O, scale, s);
+    case 128: return launch_ta<128, 2>(mask, B, H, N, k, Q, K, V, O, scale, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace kf
