@@ -115,6 +115,10 @@ def parse():
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the OpenWebText-shaped batch sweep and k comparison")
     ap.add_argument("--sweep-batches", default="1,16,64,256,512")
+    ap.add_argument("--no-train-attn", action="store_true",
+                    help="skip the training-mask attention measurement")
+    ap.add_argument("--train-attn-only", action="store_true",
+                    help="measure only the training-mask attention and print its JSON")
     ap.add_argument("--cpu-blocks", type=int, default=8,
                     help="decode blocks per sequence in the CPU oracle sample")
     ap.add_argument("--summarize", metavar="DIR", default=None,
@@ -380,6 +384,50 @@ def owt_sweep(batches, stream):
             "by_batch": rows, "k_at_batch": {"batch": B, **ks}}
 
 
+def training_attention_bench(reps: int = 10):
+    """Block-sparse attention of the training masks (SingleForward M_S and
+    DoubleForward M_D, Appendix C.2) at one GPU's share of the paper's
+    training batch (global batch 512 over 8 GPUs: 64 sequences; 12 heads,
+    d_head 64, k = 4) for the OWT (N = 1024) and LM1B (N = 128) sequence
+    lengths.  Inputs are seeded N(0, 1) bf16 tensors.  Work counted: 4 d_head
+    flops per visible (query, key) pair, against the bf16 MFMA peak."""
+    import torch
+    from paper_2606_10820_amd import binding as Bd
+    dev = torch.device("cuda:0")
+    peak = PEAK_MFMA_TFLOPS[S.DTYPE_BF16]
+    cases = []
+    for name, (B, H, N, k, dh) in (("OWT", (64, 12, 1024, 4, 64)), ("LM1B", (64, 12, 128, 4, 64))):
+        for mask, mname in ((Bd.KF_MASK_SINGLE, "single"), (Bd.KF_MASK_DOUBLE, "double")):
+            rows, keys = Bd.training_attention_shapes(mask, N, k)
+            g = torch.Generator(device=dev)
+            g.manual_seed(1)
+            q = torch.randn((B, H, rows, dh), device=dev, generator=g).to(torch.bfloat16)
+            kk = torch.randn((B, H, keys, dh), device=dev, generator=g).to(torch.bfloat16)
+            v = torch.randn((B, H, keys, dh), device=dev, generator=g).to(torch.bfloat16)
+            out = torch.empty_like(q)
+            for _ in range(3):
+                Bd.training_attention(mask, q, kk, v, N, k, dh ** -0.5, out=out)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                Bd.training_attention(mask, q, kk, v, N, k, dh ** -0.5, out=out)
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / reps
+            ent = Bd.training_attention_entries(mask, N, k)
+            tf = 4.0 * ent * dh * B * H / (ms * 1e-3) / 1e12
+            cases.append({"workload": f"{name} training share: B={B}, H={H}, N={N}, k={k}, d_head={dh}",
+                          "mask": mname, "ms": round(ms, 4), "tflops": round(tf, 1),
+                          "frac": round(tf / peak, 4), "visible_pairs_per_head": ent,
+                          "dense_pairs_per_head": rows * keys})
+            log(f"[bench] training attention {name} {mname}: {ms:.3f} ms, {tf:.1f} TFLOP/s "
+                f"({tf / peak:.1%} of bf16 MFMA peak)")
+            del q, kk, v, out
+    torch.cuda.empty_cache()
+    return {"kernel": "kf_training_attention", "peak_tflops": peak,
+            "work": "4 * d_head flops per visible (query, key) pair", "cases": cases}
+
+
 def main():
     a = parse()
     if a.summarize:
@@ -391,6 +439,10 @@ def main():
         sys.exit(2)
     import torch
     from paper_2606_10820_amd import binding as Bd
+
+    if a.train_attn_only:
+        print(json.dumps(training_attention_bench(max(a.steps, 1))), flush=True)
+        return
 
     w = S.WORKLOADS[a.workload]
     cfg: S.ModelConfig = w["cfg"]
@@ -505,6 +557,9 @@ def main():
 
     if not a.no_sweep:
         res["owt_sweep"] = owt_sweep([int(x) for x in a.sweep_batches.split(",") if x], stream)
+
+    if not a.no_train_attn:
+        res["training_attention"] = training_attention_bench()
 
     if not a.no_cpu:
         log("[bench] CPU oracle sample ...")
