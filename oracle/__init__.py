@@ -13,7 +13,10 @@ Pieces:
     blocks, generation, full recompute, AR decoding), the oracle's own
     Philox4x32-10 for the noise of a generation run, and an independent numpy
     dense-mask forward pass used as a brute-force pin (SingleForward /
-    DoubleForward masks of Appendix C.2).
+    DoubleForward masks of Appendix C.2);
+  * the Stage-1 distillation targets of the AR teacher (temperature-scaled
+    inverse CDF at every position) and plain masked attention under the
+    training masks.
 """
 from __future__ import annotations
 
@@ -320,6 +323,41 @@ def generate_ar(model: Model, prompt: np.ndarray, L: int, seed: int,
             out[ri, p - N] = tok
             pending = [tok]
     return out
+
+
+def tempered_icdf(logits: np.ndarray, tau: float, u: float) -> int:
+    """The teacher's sampler of forward distillation (Appendix C.2, Stage-1
+    algorithm): the inverse-CDF map (strict convention) of softmax(logits / tau)
+    at u."""
+    return icdf(softmax(np.asarray(logits, np.float64) / float(tau)), u)
+
+
+def teacher_targets(model: Model, tokens: np.ndarray, tau: Sequence[float], u: np.ndarray,
+                    rows: Optional[Sequence[int]] = None):
+    """Stage-1 distillation targets (Appendix C.2, forward distillation, the
+    teacher's lines): an AR causal pass over each sequence's tokens; at
+    position p the target is tempered_icdf of the next-token logits at
+    u[b][p] with the sequence's temperature tau[b].
+
+    Returns (targets [len(rows), N], logits [len(rows), N, V])."""
+    tokens = np.asarray(tokens, np.int32)
+    u = np.asarray(u, np.float64)
+    B, N = tokens.shape
+    rows = list(range(B)) if rows is None else list(rows)
+    out = np.zeros((len(rows), N), np.int32)
+    lg = np.zeros((len(rows), N, model.V), np.float64)
+    for ri, b in enumerate(rows):
+        s = model.seq()
+        for p in range(N):
+            logits, _ = s.step([int(tokens[b, p])], [], commit=True)
+            lg[ri, p] = logits[0]
+            out[ri, p] = tempered_icdf(logits[0], float(tau[b]), float(u[b, p]))
+    return out, lg
+
+
+def tempered_margin(logits: np.ndarray, tau: float, u: float) -> float:
+    """Distance from u to the nearest CDF boundary of softmax(logits / tau)."""
+    return cdf_margin(np.asarray(logits, np.float64) / float(tau), u)
 
 
 def cdf_margin(logits: np.ndarray, u: float) -> float:

@@ -691,3 +691,58 @@ def test_training_masks_nnz():
         Md = O.training_mask("double", N, k)
         assert Md.shape == (2 * N * k, N + 2 * N * k)
         assert int(Md[N * k:].sum()) == O.nnz_double(N, k)
+
+
+# ------------------------------------ Stage-1 distillation targets (C.2)
+
+def test_tempered_icdf_closed_form():
+    """softmax(l / tau) of l = (0, ln 2, ln 3) is (1, 2, 3)^(1/tau) normalised;
+    the strict inverse CDF picks the first index whose CDF exceeds u."""
+    l = np.array([0.0, math.log(2.0), math.log(3.0)])
+    for tau in (0.5, 1.0, 2.0):
+        w = np.array([1.0, 2.0, 3.0]) ** (1.0 / tau)
+        F = np.cumsum(w) / w.sum()
+        for u in (0.0, 0.5 * F[0], F[0] - 1e-9, F[0] + 1e-9, 0.5 * (F[0] + F[1]),
+                  F[1] - 1e-9, F[1] + 1e-9, 0.999999):
+            expect = int(np.argmax(F > u))
+            assert O.tempered_icdf(l, tau, u) == expect, (tau, u)
+    # tau = 1 is the untempered sampler; tau = 0.5 squares the odds
+    assert O.tempered_icdf(l, 0.5, 1.0 / 14 + 1e-9) == 1
+    assert O.tempered_icdf(l, 0.5, 5.0 / 14 + 1e-9) == 2
+
+
+def test_tempered_icdf_limits():
+    """Low temperature is greedy decoding; very high temperature is uniform,
+    so the map becomes floor(u V)."""
+    rng = np.random.default_rng(3)
+    l = rng.normal(size=50)
+    V = l.size
+    for u in np.linspace(0.0, 0.999, 37):
+        assert O.tempered_icdf(l, 1e-3, float(u)) == int(np.argmax(l))
+        if abs(u * V - round(u * V)) > 1e-3:
+            assert O.tempered_icdf(l, 1e9, float(u)) == int(math.floor(u * V))
+
+
+def test_teacher_targets_brute_force(small):
+    """The teacher's logits at every position equal the independent numpy
+    dense causal forward over the prefix, and each target is the tempered
+    inverse CDF of them (rows with u near a CDF boundary are skipped)."""
+    blob, m = small
+    cfg, W = O.parse_blob(blob)
+    rng = np.random.default_rng(11)
+    B, N = 2, 7
+    tokens = rng.integers(0, SMALL.vocab, (B, N)).astype(np.int32)
+    tau = [0.7, 1.6]
+    u = rng.random((B, N))
+    tg, lg = O.teacher_targets(m, tokens, tau, u)
+    for b in range(B):
+        n = N
+        M = np.tril(np.ones((n, n), bool))
+        dense = O.dense_forward(cfg, W, [("tok", t) for t in tokens[b]], list(range(n)), M)
+        np.testing.assert_allclose(lg[b], dense, rtol=0, atol=1e-9)
+        for p in range(N):
+            z = dense[p] / tau[b]
+            q = np.exp(z - z.max())
+            F = np.cumsum(q / q.sum())
+            if np.min(np.abs(F - u[b, p])) > 1e-9:
+                assert tg[b, p] == int(np.argmax(F > u[b, p]))
