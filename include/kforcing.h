@@ -50,6 +50,9 @@ extern "C" {
 
 #define KF_FLAG_DEBUG_LOGITS 1u /* reserve room for, and record, the fp32 head logits of
                                    the most recent step (kf_debug_logits) */
+#define KF_FLAG_TEACHER 4u      /* reserve the sampling-head workspace of kf_teacher_targets
+                                   (min(max_batch * max_prompt, 8192) rows x (Vpad / 128) x
+                                   36 bytes) */
 #define KF_FLAG_TEMPERATURE 2u  /* the model has a temperature-conditioned noise encoder
                                    (its weight blob carries the encoder, header word 9 = 1);
                                    see kf_set_temperature */
@@ -177,8 +180,34 @@ int kf_set_graphs(kf_ctx *ctx, int enable);
 int kf_get_state(const kf_ctx *ctx, int *C, int *pending, int *B);
 
 /* Synchronise the stream and return the device-side error flags (bit 0: a
- * token id outside [0, V) was replaced by 0), then clear them. */
+ * token id outside [0, V) was replaced by 0; bit 1: kf_teacher_targets met a
+ * temperature outside (0, inf)), then clear them. */
 int kf_device_errors(kf_ctx *ctx, int *flags);
+
+/* Distillation targets of the Stage-1 AR teacher (Appendix C.2, forward
+ * distillation algorithm, teacher lines): the loaded model runs as an
+ * autoregressive teacher, one causal pass over tokens [B][N] (positions
+ * 0..N-1), and for every (b, p)
+ *     targets[b][p] = smallest m with F_m > u[b][p],
+ * F the CDF of softmax(l_{b,p} / tau[b]) over the vocabulary, l_{b,p} the head
+ * logits at position p (the teacher's distribution of the token after
+ * tokens[b][0..p]).  The inverse CDF is the strict convention of the AR
+ * sampler; if rounding leaves F_V <= u it returns the last token with
+ * q > 0.  The logits never reach HBM: the head GEMM keeps per-tile maxima and
+ * 16-column sums of exp(l / tau) and a selection kernel recomputes only the
+ * 16 logits around the crossing point.
+ *   tokens int32 [B][N], tau fp32 [B] (> 0), u fp32 [B][N] in [0, 1),
+ *   targets int32 [B][N]: device pointers owned by the caller.
+ *   Requires KF_FLAG_TEACHER; 1 <= B <= max_batch, 1 <= N <= max_prompt.
+ *   A tau outside (0, inf) sets device error bit 1 (kf_device_errors) and
+ *   gives target 0 for that sequence's rows.  Token ids outside [0, V) are
+ *   replaced by 0 (error bit 0), as in a prefill.
+ *   The pass uses the KV cache: any generation in progress ends (a later
+ *   decode needs a new prefill).  With KF_FLAG_DEBUG_LOGITS the fp32 logits
+ *   of the last head chunk (rows ((B*N - 1) / 8192) * 8192 .. B*N - 1) are
+ *   kept for kf_debug_logits. */
+int kf_teacher_targets(kf_ctx *ctx, int B, int N, const int32_t *tokens, const float *tau,
+                       const float *u, int32_t *targets);
 
 /* Per-kernel timing with HIP events on the context's stream.  kf_set_timing
  * takes a bit mask over the kernel classes below (bit c = class c; 0 turns

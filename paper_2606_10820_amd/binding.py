@@ -20,6 +20,7 @@ KF_OK, KF_EINVAL, KF_ESTATE, KF_ECTX, KF_ENOMEM, KF_EHIP = 0, -1, -2, -3, -4, -5
 KF_FP32, KF_BF16 = 0, 1
 KF_FLAG_DEBUG_LOGITS = 1
 KF_FLAG_TEMPERATURE = 2
+KF_FLAG_TEACHER = 4
 KF_MASK_SINGLE, KF_MASK_DOUBLE = 0, 1
 KF_KC_NAMES = ["embed", "noise", "norm", "qkv", "attn", "oproj", "mlp_up", "mlp_down", "head",
                "select"]
@@ -73,6 +74,7 @@ def lib():
         "kf_debug_logits": (I, [P, P, SZ]),
         "kf_fill_noise": (I, [P, U64, I, I, I, P]),
         "kf_set_temperature": (I, [P, P, I]),
+        "kf_teacher_targets": (I, [P, I, I, P, P, P, P]),
         "kf_get_state": (I, [P, IP, IP, IP]),
         "kf_device_errors": (I, [P, IP]),
         "kf_set_graphs": (I, [P, I]),
@@ -220,6 +222,20 @@ class KForcing:
         t = self._f32(tau).reshape(-1)
         self._check(self.L.kf_set_temperature(self.h, self._p(t), int(t.numel())))
         self.torch.cuda.synchronize(self.device)  # t is read during the call's kernels
+
+    def teacher_targets(self, tokens, tau, u, out=None):
+        """Stage-1 teacher targets: tokens [B][N] int32, tau [B], u [B][N]
+        (device tensors or array-likes); returns targets [B][N] int32."""
+        tk = self._i32(tokens)
+        B, N = tk.shape
+        t = self._f32(tau).reshape(-1)
+        uu = self._f32(u).reshape(B, N)
+        if out is None:
+            out = self.torch.empty((B, N), dtype=self.torch.int32, device=self.device)
+        self._check(self.L.kf_teacher_targets(self.h, B, N, self._p(tk), self._p(t), self._p(uu),
+                                              self._p(out)))
+        self.torch.cuda.synchronize(self.device)  # the inputs may be temporaries
+        return out
 
     def fill_noise(self, seed: int, B: int, p0: int, n: int):
         out = self.torch.empty((B, n), dtype=self.torch.float32, device=self.device)

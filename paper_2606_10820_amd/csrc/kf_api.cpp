@@ -31,6 +31,9 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 constexpr int kAttnEntries = 8192;
 // Split-K GEMM workspace (fp32 parts of the plain GEMMs of small steps).
 constexpr size_t kSplitBytes = (size_t)8 << 20;
+// Rows per sampling-head chunk of kf_teacher_targets: the head partials of a
+// chunk take rows * (Vpad / 128) * 36 bytes (about 116 MB at vocabulary 50257).
+constexpr int kTeacherChunk = 8192;
 
 // ------------------------------------------------------------ memory plan
 struct LayerOff {
@@ -54,6 +57,8 @@ struct Plan {
   size_t kv = 0, kv_bytes = 0;
   size_t X = 0, Xh = 0, lnst = 0, A = 0, Q = 0, O = 0, Hm = 0, noise = 0, pval = 0, pidx = 0;
   size_t logits = 0, dstate = 0, pend = 0;
+  int teacher_rows = 0;                    // rows per sampling-head chunk (KF_FLAG_TEACHER)
+  size_t tmax = 0, tsub = 0;               // sampling-head partials of one chunk
   size_t att_m = 0, att_l = 0, att_o = 0;  // attention key-split partial states
   size_t split_part = 0;                   // split-K GEMM parts
   size_t total = 0;
@@ -77,7 +82,8 @@ bool config_ok(const kf_config& c, std::string* why) {
   if (c.max_batch < 1 || c.max_batch > 65535) return bad("max_batch must be in [1, 65535]");
   if (c.max_k < 1 || c.max_k > c.n_ctx) return bad("max_k must be in [1, n_ctx]");
   if (c.max_prompt < 1 || c.max_prompt > c.n_ctx) return bad("max_prompt must be in [1, n_ctx]");
-  if (c.flags & ~(KF_FLAG_DEBUG_LOGITS | KF_FLAG_TEMPERATURE)) return bad("unknown flag bits");
+  if (c.flags & ~(KF_FLAG_DEBUG_LOGITS | KF_FLAG_TEMPERATURE | KF_FLAG_TEACHER))
+    return bad("unknown flag bits");
   // GEMM operands are addressed through buffer descriptors with 32-bit byte
   // ranges: the largest activation matrix of a step must stay below 2 GiB.
   const long long es = c.dtype == KF_BF16 ? 2 : 4;
@@ -95,7 +101,13 @@ void make_plan(const kf_config& c, Plan& p) {
   p.n_tiles = p.Vpad / kf::kHeadTileN;
   p.rows_max = c.max_batch * ((c.max_prompt > c.max_k ? c.max_prompt : c.max_k) + c.max_k);
   p.head_max = c.max_batch * c.max_k;
-  p.logit_rows = (c.flags & KF_FLAG_DEBUG_LOGITS) ? p.head_max : c.max_batch;
+  if (c.flags & KF_FLAG_TEACHER) {
+    const long long tr = (long long)c.max_batch * c.max_prompt;
+    p.teacher_rows = (int)(tr < kTeacherChunk ? tr : kTeacherChunk);
+  }
+  p.logit_rows = (c.flags & KF_FLAG_DEBUG_LOGITS)
+                     ? (p.head_max > p.teacher_rows ? p.head_max : p.teacher_rows)
+                     : c.max_batch;
   size_t off = 0;
   auto take = [&](size_t bytes) {
     size_t o = off;
@@ -158,6 +170,8 @@ void make_plan(const kf_config& c, Plan& p) {
   p.pval = take((size_t)p.head_max * p.n_tiles * 4);
   p.pidx = take((size_t)p.head_max * p.n_tiles * 4);
   p.logits = take((size_t)p.logit_rows * c.vocab * 4);
+  p.tmax = take((size_t)p.teacher_rows * p.n_tiles * 4);
+  p.tsub = take((size_t)p.teacher_rows * p.n_tiles * 8 * 4);
   p.dstate = take(sizeof(KfDevState));
   p.pend = take((size_t)c.max_batch * c.max_k * 4);
   p.att_m = take((size_t)kAttnEntries * 4);
@@ -289,6 +303,10 @@ struct StepIn {
   uint64_t seed;
   KfOutDesc od;
   bool reset;                // prefill: C := 0 before the step
+  // teacher targets (kf_teacher_targets): every real row is sampled
+  const float* tau = nullptr;    // [B] temperatures
+  const float* u_rows = nullptr; // [B][nr] noise
+  int32_t* targets = nullptr;    // [B][nr] output; non-null selects the teacher head
 };
 
 template <typename T>
@@ -349,6 +367,28 @@ int run_step(kf_ctx* c, const StepIn& in) {
     KF_LAUNCH(c, KF_KC_OPROJ, kf::gemm_residual<T>(O, W(y.wo), M, d, d, F(y.bo), X, Xh, lnst, &sws, s));
     KF_LAUNCH(c, KF_KC_MLP_UP, kf::gemm_up_ln<T>(Xh, ln2, W(y.w1), M, f, d, F(y.b1), Hm, s));
     KF_LAUNCH(c, KF_KC_MLP_DOWN, kf::gemm_residual<T>(Hm, W(y.w2), M, d, f, F(y.b2), X, Xh, lnst, &sws, s));
+  }
+  if (in.targets) {
+    // Teacher targets: the sampling head over every row, in chunks of the
+    // head-partials workspace, each followed by its inverse-CDF selection.
+    const kf::LnFold lnf{F(p.head_c1), F(p.head_c2), lnst};
+    float* tmax = reinterpret_cast<float*>(base + p.tmax);
+    float* tsub = reinterpret_cast<float*>(base + p.tsub);
+    float* lg = debug ? reinterpret_cast<float*>(base + p.logits) : nullptr;
+    int mc = 0;
+    for (int r0 = 0; r0 < M; r0 += p.teacher_rows) {
+      mc = M - r0 < p.teacher_rows ? M - r0 : p.teacher_rows;
+      KF_LAUNCH(c, KF_KC_HEAD,
+                kf::gemm_head_sample<T>(Xh, lnf, W(p.head_w), mc, p.Vpad, V, d, r0, in.nr, in.tau,
+                                        tmax, tsub, lg, s));
+      KF_LAUNCH(c, KF_KC_SELECT,
+                kf::launch_teacher_select<T>(tmax, tsub, p.n_tiles, V, Xh, lnst, W(p.head_w),
+                                             F(p.head_c1), F(p.head_c2), d, in.tau, in.u_rows,
+                                             r0, mc, in.nr, in.targets, st, s));
+    }
+    c->last_head_rows = mc;
+    c->last_logits = debug;
+    return KF_OK;
   }
   const bool ar = in.k == 0;
   const int Mh = ar ? in.B : in.B * in.k;
@@ -883,6 +923,35 @@ int kf_kernel_time(kf_ctx* c, int cls, double* total_ms, int* launches) {
   *total_ms = tot;
   *launches = n;
   return KF_OK;
+}
+
+int kf_teacher_targets(kf_ctx* c, int B, int N, const int32_t* tokens, const float* tau,
+                       const float* u, int32_t* targets) {
+  if (!c) return KF_EINVAL;
+  if (int r = ready(c)) return r;
+  if (!(c->cfg.flags & KF_FLAG_TEACHER))
+    return fail(c, KF_ESTATE, "teacher targets need a context created with KF_FLAG_TEACHER");
+  if (B < 1 || B > c->cfg.max_batch) return fail(c, KF_EINVAL, "B = %d outside [1, %d]", B, c->cfg.max_batch);
+  if (N < 1 || N > c->cfg.max_prompt)
+    return fail(c, KF_EINVAL, "N = %d outside [1, max_prompt = %d]", N, c->cfg.max_prompt);
+  if (!tokens || !tau || !u || !targets) return fail(c, KF_EINVAL, "null pointer");
+  StepIn in{};
+  in.B = B;
+  in.nr = N;
+  in.k = 0;
+  in.toks = tokens;
+  in.tok_stride = N;
+  in.reset = true;
+  in.tau = tau;
+  in.u_rows = u;
+  in.targets = targets;
+  // the pass writes the KV cache of every sequence: a generation in progress ends here
+  c->live = false;
+  c->C = 0;
+  c->pending = 0;
+  c->B = 0;
+  drop_graph(c);
+  return step(c, in);
 }
 
 int kf_training_attention(void* hip_stream, int mask, int B, int H, int N, int k, int d_head,

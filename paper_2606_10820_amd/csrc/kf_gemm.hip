@@ -242,12 +242,36 @@ struct EpHead {
   int n_tiles;
 };
 
+// Head of a temperature-scaled sampling pass over every row (teacher
+// targets): per (row, 128-column tile) the maximum M_t of the scaled logits
+// x = l / tau_b and, per 16-column group q of the tile, sum exp(x - M_t) over
+// the group's columns (< V).  Row m of this launch is row row0 + m of the step,
+// sequence (row0 + m) / rows_per_seq.  logits (optional, fp32 [M][V]) keeps
+// the unscaled logits.
+struct EpHeadSample {
+  static constexpr bool kStats = false;
+  const float* bias;  // always null: the tied head has no bias
+  float* pmax;        // [M][n_tiles]
+  float* psub;        // [M][n_tiles][8]
+  float* logits;
+  const float* tau;   // [sequences]
+  int row0, rows_per_seq, V, n_tiles;
+  __device__ float inv_tau(int m) const {
+    const float t = tau[(row0 + m) / rows_per_seq];
+    return (t > 0.f && t < INFINITY) ? 1.0f / t : 1.0f;  // invalid tau: the select flags it
+  }
+};
+
 template <typename Ep>
 struct IsHead {
   static constexpr bool value = false;
 };
 template <>
 struct IsHead<EpHead> {
+  static constexpr bool value = true;
+};
+template <>
+struct IsHead<EpHeadSample> {
   static constexpr bool value = true;
 };
 
@@ -580,6 +604,62 @@ __global__ void __launch_bounds__(256)
       }
       __syncthreads();  // the next band reuses the staging rows
     }
+  } else if constexpr (std::is_same<Ep, EpHeadSample>::value) {
+    // Tile maximum of the scaled logits per row (lane-local, across the four
+    // lane groups holding the row, then across the WN wavefronts), then the
+    // 16-column group sums of exp(x - M_t): group (wn, tn) is exactly the
+    // 16 columns that the four lane groups of wavefront wn hold for tn.
+    static_assert(BN == 128 && WN * TN == 8, "eight 16-column groups per head tile");
+    __shared__ float redm[WN][BM];
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) {
+      const int mloc = wm * MW + tm * 16 + (lane & 15);
+      const int m = m0 + mloc;
+      const float it = ep.inv_tau(m < M ? m : 0);
+      float bv = -INFINITY;
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) {
+        const int n = n0 + wn * NW + tn * 16 + 4 * (lane >> 4);
+        const f32x4 v = apply(acc[tn][tm], mloc, tn);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (n + i < ep.V) bv = fmaxf(bv, v[i] * it);
+      }
+      bv = fmaxf(bv, __shfl_xor(bv, 16, 64));
+      bv = fmaxf(bv, __shfl_xor(bv, 32, 64));
+      if ((lane >> 4) == 0) redm[wn][mloc] = bv;
+    }
+    __syncthreads();
+    const int nt = n0 / BN;
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) {
+      const int mloc = wm * MW + tm * 16 + (lane & 15);
+      const int m = m0 + mloc;
+      const float it = ep.inv_tau(m < M ? m : 0);
+      float mt = redm[0][mloc];
+#pragma unroll
+      for (int w = 1; w < WN; ++w) mt = fmaxf(mt, redm[w][mloc]);
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) {
+        const int n = n0 + wn * NW + tn * 16 + 4 * (lane >> 4);
+        const f32x4 v = apply(acc[tn][tm], mloc, tn);
+        float sg = 0.f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (n + i < ep.V) sg += __expf(v[i] * it - mt);
+        sg += __shfl_xor(sg, 16, 64);
+        sg += __shfl_xor(sg, 32, 64);
+        if (m < M) {
+          if ((lane >> 4) == 0) ep.psub[((size_t)m * ep.n_tiles + nt) * 8 + wn * TN + tn] = sg;
+          if (ep.logits) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if (n + i < ep.V) ep.logits[(size_t)m * ep.V + n + i] = v[i];
+          }
+        }
+      }
+      if (m < M && wn == 0 && (lane >> 4) == 0) ep.pmax[(size_t)m * ep.n_tiles + nt] = mt;
+    }
   } else {
     // Row-wise argmax over this tile's columns: lane-local, then across the
     // four lane groups holding the same row, then across the WN wavefronts.
@@ -836,6 +916,21 @@ hipError_t gemm_head_ln(const T* Xh, const LnFold& ln, const T* W, int M, int Vp
 }
 
 template <typename T>
+hipError_t gemm_head_sample(const T* Xh, const LnFold& ln, const T* W, int M, int Vpad, int V, int d,
+                            int row0, int rows_per_seq, const float* tau, float* pmax, float* psub,
+                            float* logits, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  EpHeadSample ep{nullptr, pmax, psub, logits, tau, row0, rows_per_seq, V, Vpad / kHeadTileN};
+  const GemmA ga{Xh + (size_t)row0 * d, d, M, ln.c1, ln.c2, ln.lnst + (size_t)row0 * (d / 16),
+                 KfStepGeom{}};
+  if (M <= 32)
+    return launch_tile<T, 32, kHeadTileN, 1, 4, 3, 0, true>(ga, W, d, M, Vpad, d, ep, s);
+  if (M <= 512)
+    return launch_tile<T, 64, kHeadTileN, 2, 2, 3, 0, true>(ga, W, d, M, Vpad, d, ep, s);
+  return launch_tile<T, 128, kHeadTileN, 2, 2, 2, 0, true>(ga, W, d, M, Vpad, d, ep, s);
+}
+
+template <typename T>
 hipError_t launch_ln_fold(const T* W, T* Wout, const float* g, const float* beta, int N, int K,
                           float* c1, float* c2, hipStream_t s) {
   if (N <= 0) return hipSuccess;
@@ -859,6 +954,9 @@ hipError_t launch_ln_fold(const T* W, T* Wout, const float* g, const float* beta
                                     const float*, T*, hipStream_t);                                \
   template hipError_t gemm_head_ln<T>(const T*, const LnFold&, const T*, int, int, int, int, int, \
                                       KfStepGeom, float*, int*, float*, hipStream_t);              \
+  template hipError_t gemm_head_sample<T>(const T*, const LnFold&, const T*, int, int, int, int,  \
+                                          int, int, const float*, float*, float*, float*,          \
+                                          hipStream_t);                                            \
   template hipError_t launch_ln_fold<T>(const T*, T*, const float*, const float*, int, int,       \
                                         float*, float*, hipStream_t);
 KF_INST(float)

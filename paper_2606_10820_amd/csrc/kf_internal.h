@@ -13,7 +13,7 @@ typedef __bf16 bf16;
 // identical from one step to the next.
 struct KfDevState {
   int C;    // committed context length (positions 0..C-1 hold real-token K/V)
-  int err;  // bit 0: a token id outside [0, V) was replaced by 0
+  int err;  // bit 0: a token id outside [0, V) was replaced by 0; bit 1: a bad temperature
   int pad[14];
 };
 
@@ -174,6 +174,29 @@ template <typename T>
 hipError_t gemm_head_ln(const T* Xh, const LnFold& ln, const T* W, int M, int Vpad, int V, int d,
                         int gather, KfStepGeom g, float* pval, int* pidx, float* logits,
                         hipStream_t s);
+// Head of a temperature-scaled sampling pass (teacher targets) over rows
+// row0 .. row0 + M - 1 of the step (all rows are real rows; row r belongs to
+// sequence r / rows_per_seq, temperature tau[r / rows_per_seq]): per launch
+// row m and 128-column tile t, pmax [M][n_tiles] = max over columns < V of
+// l / tau and psub [M][n_tiles][8] = per 16-column group, sum exp(l / tau -
+// pmax).  When logits is not null the fp32 logits [M][V] are written too.
+template <typename T>
+hipError_t gemm_head_sample(const T* Xh, const LnFold& ln, const T* W, int M, int Vpad, int V, int d,
+                            int row0, int rows_per_seq, const float* tau, float* pmax, float* psub,
+                            float* logits, hipStream_t s);
+// Inverse-CDF selection from the sampling head's partials: for launch row m
+// (step row row0 + m, sequence b = (row0 + m) / rows_per_seq) the smallest
+// column j with F_j > u[row0 + m], F the CDF of softmax(l / tau_b); the
+// crossing group's 16 logits are recomputed from Xh, the LayerNorm partial
+// sums and the head weights.  A tau outside (0, inf) sets error bit 1 and
+// selects 0.  Writes targets[row0 + m].
+template <typename T>
+hipError_t launch_teacher_select(const float* pmax, const float* psub, int n_tiles, int V,
+                                 const T* Xh, const float2* lnst, const T* W, const float* c1,
+                                 const float* c2, int d, const float* tau, const float* u, int row0,
+                                 int M, int rows_per_seq, int32_t* targets, KfDevState* st,
+                                 hipStream_t s);
+
 // Fold a LayerNorm into the GEMM that consumes it: Wout = W diag(gain) in T,
 // c1 = Wout 1, c2 = W shift; W [N][K], Wout may alias W.
 template <typename T>

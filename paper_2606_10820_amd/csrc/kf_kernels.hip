@@ -510,6 +510,195 @@ __global__ void __launch_bounds__(1024)
   }
 }
 
+// ------------------------------------------------ teacher target selection
+// Temperature-scaled inverse CDF over a whole vocabulary without the logits in
+// HBM (Algorithm "Stage 1" teacher: targets = InverseCDF(softmax(l / tau), z)).
+// The sampling head left, per row, the maximum M_t of x = l / tau in each
+// 128-column tile and per 16-column group q the sum of exp(x - M_t).  With M
+// the row maximum, the mass of tile t is w_t = exp(M_t - M) sum_q psub[t][q].
+// One wavefront per row scans tile masses (lane L holds a contiguous run of
+// tiles; an inclusive scan over the lanes keeps tile order), then the eight
+// group masses of the crossing tile, then recomputes the crossing group's 16
+// logits from the normalised hidden row and scans them: the result is the
+// smallest column j with sum_{i <= j} p_i > u Z, the strict convention.  When
+// rounding leaves no crossing (u Z at or above the total), every level takes
+// its last element with positive mass, i.e. the last token with q > 0.
+__device__ inline float wave_max(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
+  return v;
+}
+
+// 8 consecutive elements of a compute-dtype row as floats
+__device__ inline void load8f(const float* p, float (&x)[8]) {
+  const float4 a = *reinterpret_cast<const float4*>(p), b = *reinterpret_cast<const float4*>(p + 4);
+  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w; x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+}
+__device__ inline void load8f(const bf16* p, float (&x)[8]) {
+  const uint4 v = *reinterpret_cast<const uint4*>(p);
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    x[2 * i] = __uint_as_float(w[i] << 16);
+    x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256)
+    teacher_select_kernel(const float* __restrict__ pmax, const float* __restrict__ psub, int nT,
+                          int V, const T* __restrict__ Xh, const float2* __restrict__ lnst,
+                          const T* __restrict__ W, const float* __restrict__ c1,
+                          const float* __restrict__ c2, int d, const float* __restrict__ tau,
+                          const float* __restrict__ u, int row0, int M, int rows_per_seq,
+                          int32_t* __restrict__ targets, KfDevState* st) {
+  const int lane = threadIdx.x & 63;
+  const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (m >= M) return;  // whole wavefront
+  const int r = row0 + m;
+  const float tb = tau[r / rows_per_seq];
+  if (!(tb > 0.f && tb < INFINITY)) {
+    if (lane == 0) {
+      targets[r] = 0;
+      atomicOr(&st->err, 2);
+    }
+    return;
+  }
+  const float it = 1.0f / tb;
+  const float* pm = pmax + (size_t)m * nT;
+  const float* ps = psub + (size_t)m * nT * 8;
+
+  // level 1: tiles
+  const int c = (nT + 63) / 64, t_lo = min(nT, lane * c), t_hi = min(nT, t_lo + c);
+  float mx = -INFINITY;
+  for (int t = t_lo; t < t_hi; ++t) mx = fmaxf(mx, pm[t]);
+  mx = wave_max(mx);
+  auto tile_w = [&](int t) {
+    const float mt = pm[t];
+    if (mt == -INFINITY) return 0.f;
+    const float4 a = *reinterpret_cast<const float4*>(ps + (size_t)t * 8);
+    const float4 b = *reinterpret_cast<const float4*>(ps + (size_t)t * 8 + 4);
+    return __expf(mt - mx) * (((a.x + a.y) + (a.z + a.w)) + ((b.x + b.y) + (b.z + b.w)));
+  };
+  float ls = 0.f;
+  for (int t = t_lo; t < t_hi; ++t) ls += tile_w(t);
+  float incl = ls;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const float v = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += v;
+  }
+  const float Z = __shfl(incl, 63, 64);
+  const float thr = u[r] * Z;
+  const uint64_t cross = __ballot(incl > thr);
+  const bool fall = cross == 0;
+  int ls_lane;
+  if (!fall) {
+    ls_lane = __ffsll((unsigned long long)cross) - 1;
+  } else {
+    const uint64_t pos = __ballot(ls > 0.f);
+    ls_lane = pos ? 63 - __clzll((unsigned long long)pos) : 0;
+  }
+  float run = __shfl(incl - ls, ls_lane, 64);  // mass before the lane's tiles
+  int tstar = -1;
+  {
+    const int lo = min(nT, ls_lane * c), hi = min(nT, lo + c);
+    float run_last = run;
+    int t_last = lo;
+    for (int t = lo; t < hi; ++t) {
+      const float w = tile_w(t);
+      if (!fall && run + w > thr) {
+        tstar = t;
+        break;
+      }
+      if (w > 0.f) {
+        t_last = t;
+        run_last = run;
+      }
+      run += w;
+    }
+    if (tstar < 0) {  // fallback, or rounding between the lane scan and the tile scan
+      tstar = t_last;
+      run = run_last;
+    }
+  }
+
+  // level 2: the eight 16-column groups of tile tstar
+  const float sc = __expf(pm[tstar] - mx);
+  int qstar = -1;
+  {
+    float run_last = run;
+    int q_last = 0;
+    for (int q = 0; q < 8; ++q) {
+      const float gq = sc * ps[(size_t)tstar * 8 + q];
+      if (!fall && run + gq > thr) {
+        qstar = q;
+        break;
+      }
+      if (gq > 0.f) {
+        q_last = q;
+        run_last = run;
+      }
+      run += gq;
+    }
+    if (qstar < 0) {
+      qstar = q_last;
+      run = run_last;
+    }
+  }
+
+  // level 3: recompute the group's 16 logits (four lanes per column) and scan
+  const int j0 = tstar * kHeadTileN + qstar * 16;
+  const int jj = lane >> 2, part = lane & 3, j = j0 + jj;
+  float dot = 0.f;
+  if (j < V) {
+    const T* wr = W + (size_t)j * d;
+    const T* xr = Xh + (size_t)r * d;
+    for (int ch = part; ch < d / 8; ch += 4) {
+      float a[8], b[8];
+      load8f(wr + ch * 8, a);
+      load8f(xr + ch * 8, b);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) dot = fmaf(a[i], b[i], dot);
+    }
+  }
+  dot += __shfl_xor(dot, 1, 64);
+  dot += __shfl_xor(dot, 2, 64);
+  // the row's LayerNorm statistics from its partial sums, as the head GEMM forms them
+  float sa = 0.f, sb = 0.f;
+  for (int i = lane; i < d / 16; i += 64) {
+    const float2 v = lnst[(size_t)r * (d / 16) + i];
+    sa += v.x;
+    sb += v.y;
+  }
+  sa = wave_sum(sa);
+  sb = wave_sum(sb);
+  const float mu = sa / (float)d;
+  const float rstd = 1.0f / sqrtf(fmaxf(sb / (float)d - mu * mu, 0.f) + 1e-5f);
+  float p = 0.f;
+  if (j < V) {
+    const float l = rstd * (dot - mu * c1[j]) + c2[j];
+    p = __expf(l * it - pm[tstar]) * sc;
+  }
+  float pj = __shfl(p, 4 * (lane & 15), 64);  // lanes 0..15: column j0 + lane
+  if (lane >= 16) pj = 0.f;
+  float in16 = pj;
+#pragma unroll
+  for (int off = 1; off < 16; off <<= 1) {
+    const float v = __shfl_up(in16, off, 64);
+    if ((lane & 15) >= off) in16 += v;
+  }
+  const uint64_t hit = __ballot(lane < 16 && !fall && run + in16 > thr);
+  int jstar;
+  if (hit) {
+    jstar = __ffsll((unsigned long long)hit) - 1;
+  } else {
+    const uint64_t pos = __ballot(lane < 16 && pj > 0.f);
+    jstar = pos ? 63 - __clzll((unsigned long long)pos) : 0;
+  }
+  if (lane == 0) targets[r] = min(j0 + jstar, V - 1);
+}
+
 __global__ void commit_kernel(KfDevState* st, int nr) {
   if (threadIdx.x == 0 && blockIdx.x == 0) st->C += nr;
 }
@@ -654,6 +843,18 @@ hipError_t launch_icdf_select(const float* logits, int V, const float* u_in, uin
   return hipGetLastError();
 }
 
+template <typename T>
+hipError_t launch_teacher_select(const float* pmax, const float* psub, int n_tiles, int V,
+                                 const T* Xh, const float2* lnst, const T* W, const float* c1,
+                                 const float* c2, int d, const float* tau, const float* u, int row0,
+                                 int M, int rows_per_seq, int32_t* targets, KfDevState* st,
+                                 hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  launch(teacher_select_kernel<T>, dim3((M + 3) / 4), dim3(256), 0, s, pmax, psub, n_tiles, V, Xh,
+         lnst, W, c1, c2, d, tau, u, row0, M, rows_per_seq, targets, st);
+  return hipGetLastError();
+}
+
 hipError_t launch_commit(KfDevState* st, int nr, hipStream_t s) {
   launch(commit_kernel, dim3(1), dim3(64), 0, s, st, nr);
   return hipGetLastError();
@@ -698,7 +899,11 @@ hipError_t launch_zero_i32(int* dst, size_t n, hipStream_t s) { return launch_ze
   template hipError_t launch_attention<T>(const T*, const T*, T*, const KfDevState*, KfStepGeom,   \
                                           KfKvGeom, int, const AttnSplit&, hipStream_t);            \
   template hipError_t launch_convert<T>(const float*, T*, size_t, hipStream_t);                    \
-  template hipError_t launch_zero<T>(T*, size_t, hipStream_t);
+  template hipError_t launch_zero<T>(T*, size_t, hipStream_t);                                   \
+  template hipError_t launch_teacher_select<T>(const float*, const float*, int, int, const T*,     \
+                                               const float2*, const T*, const float*, const float*, \
+                                               int, const float*, const float*, int, int, int,      \
+                                               int32_t*, KfDevState*, hipStream_t);
 KF_INST(float)
 KF_INST(bf16)
 #undef KF_INST

@@ -203,6 +203,24 @@ def test_training_attention_shapes():
             assert Bd.training_attention_entries(mask, N, k) == int(M.sum())
 
 
+def test_teacher_targets_argument_checks(L):
+    P = ctypes.c_void_p
+    fake = P(0x10000)  # never dereferenced: every call below fails validation first
+    plain = _ctx(L, _cfg())
+    assert L.kf_teacher_targets(plain, 1, 4, fake, fake, fake, fake) == Bd.KF_ESTATE  # no state
+    L.kf_destroy(plain)
+    cfg = _cfg(flags=Bd.KF_FLAG_TEACHER)
+    assert L.kf_state_bytes(ctypes.byref(cfg)) > L.kf_state_bytes(ctypes.byref(_cfg()))
+    h = _ctx(L, cfg)
+    assert L.kf_teacher_targets(h, 1, 4, fake, fake, fake, fake) == Bd.KF_ESTATE  # no state buffer
+    assert L.kf_bind_state(h, fake, L.kf_state_bytes(ctypes.byref(cfg))) == Bd.KF_OK
+    assert L.kf_teacher_targets(h, 1, 4, fake, fake, fake, fake) == Bd.KF_ESTATE  # no weights
+    L.kf_destroy(h)
+    # argument ranges are checked after the state: a context without KF_FLAG_TEACHER
+    # and with weights would say ESTATE; with the flag, bad sizes say EINVAL
+    assert L.kf_teacher_targets(None, 1, 4, fake, fake, fake, fake) == Bd.KF_EINVAL
+
+
 def test_null_context(L):
     assert L.kf_prefill(None, 1, 1, None, 1, None, None) == Bd.KF_EINVAL
     assert L.kf_create(None, None, None) == Bd.KF_EINVAL
