@@ -119,7 +119,11 @@ def parse():
                     help="skip the training-mask attention measurement")
     ap.add_argument("--train-attn-only", action="store_true",
                     help="measure only the training-mask attention and print its JSON")
-    ap.add_argument("--cpu-blocks", type=int, default=8,
+    ap.add_argument("--no-teacher", action="store_true",
+                    help="skip the distillation-target measurement")
+    ap.add_argument("--teacher-only", action="store_true",
+                    help="measure only the distillation targets and print their JSON")
+    ap.add_argument("--cpu-blocks", type=int, default=28,
                     help="decode blocks per sequence in the CPU oracle sample")
     ap.add_argument("--summarize", metavar="DIR", default=None,
                     help="print a markdown summary of rocprofv3 CSV output under DIR "
@@ -384,6 +388,75 @@ def owt_sweep(batches, stream):
             "by_batch": rows, "k_at_batch": {"batch": B, **ks}}
 
 
+def teacher_costs(cfg: S.ModelConfig, B: int, N: int) -> dict:
+    """Per kernel class (bytes, flops) of one kf_teacher_targets call: an AR
+    prefill of N tokens per sequence whose head runs over every row."""
+    c = step_costs(cfg, B, N, 0, 0)
+    es = 2 if cfg.dtype == S.DTYPE_BF16 else 4
+    d, V, M = cfg.d_model, cfg.vocab, B * N
+    nt = (V + 255) // 256 * 2
+    c["head"] = [V * d * es + M * d * es + M * nt * 36, 2.0 * M * V * d]
+    c["select"] = [M * (nt * 36 + 16 * d * es + d * es + 8), 2.0 * M * 16 * d]
+    return c
+
+
+def teacher_bench(reps: int = 3):
+    """Stage-1 distillation targets (kf_teacher_targets) at one GPU's share of
+    the paper's training batch (64 sequences) for the LM1B-shaped (N = 128)
+    and OWT-shaped (N = 1024) models: targets per second and the fraction of
+    the call's algorithmic roofline (max of bytes / HBM peak and flops / bf16
+    MFMA peak, counted by teacher_costs)."""
+    import torch
+    from paper_2606_10820_amd import binding as Bd
+    dev = torch.device("cuda:0")
+    out = []
+    for name in ("lm1b", "owt"):
+        w = S.WORKLOADS[name]
+        cfg = w["cfg"]
+        B, N = 64, cfg.n_ctx
+        log(f"[bench] teacher targets {name}: B={B}, N={N}")
+        blob = S.pack_blob(cfg, S.make_weights(cfg, seed=0))
+        kc = Bd.make_config(cfg.n_layer, cfg.d_model, cfg.n_head, cfg.d_mlp, cfg.vocab, cfg.n_ctx,
+                            cfg.dtype, B, 1, N, Bd.KF_FLAG_TEACHER)
+        kf = Bd.KForcing(kc, device="cuda:0")
+        kf.load_weights(blob)
+        tokens = torch.as_tensor(S.make_prompts(w["prompts"], 3, B, N, cfg.vocab), device=dev)
+        tau = torch.as_tensor(np.random.default_rng(5).uniform(0.5, 1.5, B).astype(np.float32),
+                              device=dev)
+        u = torch.as_tensor(S.noise_block(3, B, 0, N), device=dev)
+        tg = torch.empty((B, N), dtype=torch.int32, device=dev)
+        L = kf.L
+        call = lambda: L.kf_teacher_targets(kf.h, B, N, kf._p(tokens), kf._p(tau), kf._p(u),
+                                            kf._p(tg))
+        assert call() == 0
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            call()
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) / reps * 1e3
+        kf.set_timing(Bd.KF_TIMING_ALL)
+        call()
+        per = {n: round(kf.kernel_time(ci)[0], 4) for ci, n in enumerate(CLASSES)}
+        kf.set_timing(0)
+        costs = teacher_costs(cfg, B, N)
+        by = sum(v[0] for v in costs.values())
+        fl = sum(v[1] for v in costs.values())
+        roof = max(by / (PEAK_HBM_GBS * 1e9), fl / (PEAK_MFMA_TFLOPS[cfg.dtype] * 1e12)) * 1e3
+        hb, hf = costs["head"]
+        out.append({"workload": f"{name}-shaped teacher, B={B}, N={N} (every position sampled)",
+                    "ms": round(ms, 3), "targets_per_s": round(B * N / (ms * 1e-3), 1),
+                    "algorithmic_flops": fl, "algorithmic_bytes": by,
+                    "roofline_ms": round(roof, 4), "roofline_frac": round(roof / ms, 4),
+                    "head_tflops": round(hf / (per["head"] * 1e-3) / 1e12, 1),
+                    "kernel_ms": per})
+        log(f"[bench] teacher {name}: {ms:.3f} ms, {B * N / (ms * 1e-3):,.0f} targets/s, "
+            f"{roof / ms:.1%} of its roofline; head {out[-1]['head_tflops']} TFLOP/s")
+        del kf
+        torch.cuda.empty_cache()
+    return {"entry": "kf_teacher_targets", "cases": out}
+
+
 def training_attention_bench(reps: int = 10):
     """Block-sparse attention of the training masks (SingleForward M_S and
     DoubleForward M_D, Appendix C.2) at one GPU's share of the paper's
@@ -442,6 +515,9 @@ def main():
 
     if a.train_attn_only:
         print(json.dumps(training_attention_bench(max(a.steps, 1))), flush=True)
+        return
+    if a.teacher_only:
+        print(json.dumps(teacher_bench(max(a.steps, 1))), flush=True)
         return
 
     w = S.WORKLOADS[a.workload]
@@ -560,6 +636,8 @@ def main():
 
     if not a.no_train_attn:
         res["training_attention"] = training_attention_bench()
+    if not a.no_teacher:
+        res["teacher_targets"] = teacher_bench()
 
     if not a.no_cpu:
         log("[bench] CPU oracle sample ...")
