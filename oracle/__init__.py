@@ -15,8 +15,9 @@ Pieces:
     dense-mask forward pass used as a brute-force pin (SingleForward /
     DoubleForward masks of Appendix C.2);
   * the Stage-1 distillation targets of the AR teacher (temperature-scaled
-    inverse CDF at every position) and plain masked attention under the
-    training masks.
+    inverse CDF at every position), the Stage-2 self-forcing targets (two
+    dense-mask passes of a K-Forcing teacher) and plain masked attention
+    under the training masks.
 """
 from __future__ import annotations
 
@@ -562,6 +563,41 @@ def masked_attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, mask: np.ndarr
     P = np.exp(S)
     P /= P.sum(axis=-1, keepdims=True)
     return np.einsum("bhqk,bhkd->bhqd", P, V)
+
+
+def selfforcing_targets(cfg: dict, W: dict, tokens: np.ndarray, k: int, z1: np.ndarray,
+                        z2: np.ndarray, tau: Optional[Sequence[float]] = None,
+                        x1_forced: Optional[np.ndarray] = None):
+    """Stage-2 self-forcing targets (Appendix C.2, self-forcing distillation,
+    the teacher's lines) with the dense masks.  Per sequence b:
+      round 1: SingleForward over [context | noise z1[b]]; x1 = argmax of
+               each noise row (group t, token j);
+      round 2: DoubleForward over [context | Future-1 tokens | Future-2 noise
+               z2[b]]; x2 = argmax of each Future-2 row.
+    Future-1 carries x1, or x1_forced[b] when given (teacher forcing).
+    Returns x1, x2 [B][N][k] and the logits of both rounds' noise rows
+    [B][N*k][V]."""
+    tokens = np.asarray(tokens)
+    B, N = tokens.shape
+    z1 = np.asarray(z1, np.float64).reshape(B, N * k)
+    z2 = np.asarray(z2, np.float64).reshape(B, N * k)
+    MS, posS, _ = single_forward_layout(N, k)
+    MD, posD = double_forward_layout(N, k)
+    x1 = np.zeros((B, N * k), np.int32)
+    x2 = np.zeros((B, N * k), np.int32)
+    l1 = np.zeros((B, N * k, cfg["V"]))
+    l2 = np.zeros((B, N * k, cfg["V"]))
+    for b in range(B):
+        tb = None if tau is None else float(tau[b])
+        ctx = [("tok", int(t)) for t in tokens[b]]
+        rows = ctx + [("noise", float(z)) for z in z1[b]]
+        l1[b] = dense_forward(cfg, W, rows, posS, MS, tau=tb)[N:]
+        x1[b] = argmax(l1[b])
+        f1 = x1[b] if x1_forced is None else np.asarray(x1_forced[b]).reshape(-1)
+        rows = ctx + [("tok", int(t)) for t in f1] + [("noise", float(z)) for z in z2[b]]
+        l2[b] = dense_forward(cfg, W, rows, posD, MD, tau=tb)[N + N * k:]
+        x2[b] = argmax(l2[b])
+    return x1.reshape(B, N, k), x2.reshape(B, N, k), l1, l2
 
 
 def training_mask(kind: str, N: int, k: int) -> np.ndarray:

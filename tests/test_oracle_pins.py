@@ -746,3 +746,49 @@ def test_teacher_targets_brute_force(small):
             F = np.cumsum(q / q.sum())
             if np.min(np.abs(F - u[b, p])) > 1e-9:
                 assert tg[b, p] == int(np.argmax(F > u[b, p]))
+
+
+# ------------------------------------ Stage-2 self-forcing targets (C.2)
+
+def test_selfforcing_targets_equal_decode_steps(small):
+    """The teacher rollout's round-1 group t equals a K-Forcing prefill over
+    the first t+1 context tokens with noise z1[t] (C oracle, cached steps),
+    and its round-2 group t equals the decode step that follows with x1[t]
+    as the real rows and z2[t] as the noise: the DoubleForward window is one
+    decode step (Appendix C.2), here across every group of a sequence."""
+    blob, m = small
+    cfg, W = O.parse_blob(blob)
+    rng = np.random.default_rng(13)
+    B, N, k = 2, 5, 3
+    tokens = rng.integers(0, SMALL.vocab, (B, N)).astype(np.int32)
+    z1 = rng.random((B, N, k))
+    z2 = rng.random((B, N, k))
+    x1, x2, l1, l2 = O.selfforcing_targets(cfg, W, tokens, k, z1, z2)
+    for b in range(B):
+        for t in range(N):
+            s, lg, toks = O.prefill(m, list(tokens[b, :t + 1]), list(z1[b, t]))
+            np.testing.assert_allclose(l1[b, t * k:(t + 1) * k], lg, rtol=0, atol=1e-9)
+            assert list(toks) == list(x1[b, t])
+            lg2, toks2 = O.decode(s, list(x1[b, t]), list(z2[b, t]))
+            np.testing.assert_allclose(l2[b, t * k:(t + 1) * k], lg2, rtol=0, atol=1e-9)
+            assert list(toks2) == list(x2[b, t])
+
+
+def test_selfforcing_teacher_forcing_changes_only_round_two(small):
+    """Forcing other Future-1 tokens leaves round 1 alone and changes the
+    Future-2 logits of exactly the groups whose Future-1 tokens changed."""
+    blob, m = small
+    cfg, W = O.parse_blob(blob)
+    rng = np.random.default_rng(14)
+    B, N, k = 1, 4, 2
+    tokens = rng.integers(0, SMALL.vocab, (B, N)).astype(np.int32)
+    z1, z2 = rng.random((B, N, k)), rng.random((B, N, k))
+    x1, x2, l1, l2 = O.selfforcing_targets(cfg, W, tokens, k, z1, z2)
+    forced = x1.copy()
+    forced[0, 2, 1] = (forced[0, 2, 1] + 1) % SMALL.vocab
+    f1, f2, g1, g2 = O.selfforcing_targets(cfg, W, tokens, k, z1, z2, x1_forced=forced)
+    np.testing.assert_array_equal(f1, x1)
+    np.testing.assert_allclose(g1, l1, rtol=0, atol=0)
+    for t in range(N):
+        same = np.allclose(g2[0, t * k:(t + 1) * k], l2[0, t * k:(t + 1) * k], rtol=0, atol=1e-12)
+        assert same == (t != 2), t
