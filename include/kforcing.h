@@ -53,6 +53,10 @@ extern "C" {
 #define KF_FLAG_TEACHER 4u      /* reserve the sampling-head workspace of kf_teacher_targets
                                    (min(max_batch * max_prompt, 8192) rows x (Vpad / 128) x
                                    36 bytes) */
+#define KF_FLAG_ROLLOUT 8u      /* reserve the workspace of kf_selfforcing_targets: residual
+                                   rows for 2 * max_batch * max_prompt * max_k rows and
+                                   n_layer x 2 x max_batch x n_head x max_prompt (1 + 2 max_k)
+                                   x d_head elements of keys and values */
 #define KF_FLAG_TEMPERATURE 2u  /* the model has a temperature-conditioned noise encoder
                                    (its weight blob carries the encoder, header word 9 = 1);
                                    see kf_set_temperature */
@@ -208,6 +212,27 @@ int kf_device_errors(kf_ctx *ctx, int *flags);
  *   kept for kf_debug_logits. */
 int kf_teacher_targets(kf_ctx *ctx, int B, int N, const int32_t *tokens, const float *tau,
                        const float *u, int32_t *targets);
+
+/* Stage-2 self-forcing targets (Appendix C.2, self-forcing distillation, the
+ * teacher's lines): the loaded K-Forcing model is the teacher with window k.
+ * Round 1 is one SingleForward pass over the N context tokens and, after
+ * each context position t = 0..N-1, k noise rows z1[b][t][0..k) (noise j of
+ * group t at position t + 1 + j, the position of the token it stands for);
+ * x1[b][t][j] is the argmax of noise row (t, j).  Round 2 is one
+ * DoubleForward pass: Future-1 rows carry x1 as tokens (positions t + 1 + j),
+ * Future-2 rows carry the noise z2 (positions t + 1 + k + j), both attending
+ * to round 1's context keys under M_D; x2[b][t][j] is the argmax of Future-2
+ * row (t, j).  The 2k targets of context position t are [x1[b][t] ; x2[b][t]].
+ *   tokens int32 [B][N]; z1, z2 fp32 [B][N][k] in [0, 1); x1, x2 int32
+ *   [B][N][k]: device pointers owned by the caller.
+ *   Requires KF_FLAG_ROLLOUT and a bf16 model; 1 <= B <= max_batch,
+ *   1 <= N <= max_prompt, 1 <= k <= max_k, N + 2k <= n_ctx (else KF_ECTX).
+ *   A temperature-conditioned model uses the temperatures of
+ *   kf_set_temperature for both rounds.  The call ends any generation in
+ *   progress.  With KF_FLAG_DEBUG_LOGITS, the fp32 logits of the Future-2
+ *   rows (B*N*k rows, in x2 order) are kept for kf_debug_logits. */
+int kf_selfforcing_targets(kf_ctx *ctx, int B, int N, int k, const int32_t *tokens,
+                           const float *z1, const float *z2, int32_t *x1, int32_t *x2);
 
 /* Per-kernel timing with HIP events on the context's stream.  kf_set_timing
  * takes a bit mask over the kernel classes below (bit c = class c; 0 turns

@@ -21,6 +21,7 @@ KF_FP32, KF_BF16 = 0, 1
 KF_FLAG_DEBUG_LOGITS = 1
 KF_FLAG_TEMPERATURE = 2
 KF_FLAG_TEACHER = 4
+KF_FLAG_ROLLOUT = 8
 KF_MASK_SINGLE, KF_MASK_DOUBLE = 0, 1
 KF_KC_NAMES = ["embed", "noise", "norm", "qkv", "attn", "oproj", "mlp_up", "mlp_down", "head",
                "select"]
@@ -75,6 +76,7 @@ def lib():
         "kf_fill_noise": (I, [P, U64, I, I, I, P]),
         "kf_set_temperature": (I, [P, P, I]),
         "kf_teacher_targets": (I, [P, I, I, P, P, P, P]),
+        "kf_selfforcing_targets": (I, [P, I, I, I, P, P, P, P, P]),
         "kf_get_state": (I, [P, IP, IP, IP]),
         "kf_device_errors": (I, [P, IP]),
         "kf_set_graphs": (I, [P, I]),
@@ -236,6 +238,20 @@ class KForcing:
                                               self._p(out)))
         self.torch.cuda.synchronize(self.device)  # the inputs may be temporaries
         return out
+
+    def selfforcing_targets(self, tokens, k: int, z1, z2):
+        """Stage-2 teacher rollout: tokens [B][N], z1/z2 [B][N][k]; returns (x1, x2),
+        each int32 [B][N][k]."""
+        tk = self._i32(tokens)
+        B, N = tk.shape
+        a = self._f32(z1).reshape(B, N, k)
+        b = self._f32(z2).reshape(B, N, k)
+        x1 = self.torch.empty((B, N, k), dtype=self.torch.int32, device=self.device)
+        x2 = self.torch.empty((B, N, k), dtype=self.torch.int32, device=self.device)
+        self._check(self.L.kf_selfforcing_targets(self.h, B, N, k, self._p(tk), self._p(a),
+                                                  self._p(b), self._p(x1), self._p(x2)))
+        self.torch.cuda.synchronize(self.device)  # the inputs may be temporaries
+        return x1, x2
 
     def fill_noise(self, seed: int, B: int, p0: int, n: int):
         out = self.torch.empty((B, n), dtype=self.torch.float32, device=self.device)

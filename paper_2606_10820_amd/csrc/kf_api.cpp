@@ -58,6 +58,7 @@ struct Plan {
   size_t X = 0, Xh = 0, lnst = 0, A = 0, Q = 0, O = 0, Hm = 0, noise = 0, pval = 0, pidx = 0;
   size_t logits = 0, dstate = 0, pend = 0;
   int teacher_rows = 0;                    // rows per sampling-head chunk (KF_FLAG_TEACHER)
+  size_t roll_kv = 0;                      // per-layer K/V of the teacher rollout (KF_FLAG_ROLLOUT)
   size_t tmax = 0, tsub = 0;               // sampling-head partials of one chunk
   size_t att_m = 0, att_l = 0, att_o = 0;  // attention key-split partial states
   size_t split_part = 0;                   // split-K GEMM parts
@@ -82,12 +83,16 @@ bool config_ok(const kf_config& c, std::string* why) {
   if (c.max_batch < 1 || c.max_batch > 65535) return bad("max_batch must be in [1, 65535]");
   if (c.max_k < 1 || c.max_k > c.n_ctx) return bad("max_k must be in [1, n_ctx]");
   if (c.max_prompt < 1 || c.max_prompt > c.n_ctx) return bad("max_prompt must be in [1, n_ctx]");
-  if (c.flags & ~(KF_FLAG_DEBUG_LOGITS | KF_FLAG_TEMPERATURE | KF_FLAG_TEACHER))
+  if (c.flags & ~(KF_FLAG_DEBUG_LOGITS | KF_FLAG_TEMPERATURE | KF_FLAG_TEACHER | KF_FLAG_ROLLOUT))
     return bad("unknown flag bits");
   // GEMM operands are addressed through buffer descriptors with 32-bit byte
   // ranges: the largest activation matrix of a step must stay below 2 GiB.
   const long long es = c.dtype == KF_BF16 ? 2 : 4;
-  const long long rows = (long long)c.max_batch * ((c.max_prompt > c.max_k ? c.max_prompt : c.max_k) + c.max_k);
+  long long rows = (long long)c.max_batch * ((c.max_prompt > c.max_k ? c.max_prompt : c.max_k) + c.max_k);
+  if (c.flags & KF_FLAG_ROLLOUT) {
+    const long long r2 = 2LL * c.max_batch * c.max_prompt * c.max_k;  // DoubleForward rows
+    if (r2 > rows) rows = r2;
+  }
   const long long width = c.d_mlp > 4 * c.d_model ? c.d_mlp : 4 * c.d_model;
   if (rows * width * es >= (1LL << 31) || rows * c.d_model * 4 >= (1LL << 31))
     return bad("max_batch * (max(max_prompt, max_k) + max_k) rows too large for one step");
@@ -101,6 +106,11 @@ void make_plan(const kf_config& c, Plan& p) {
   p.n_tiles = p.Vpad / kf::kHeadTileN;
   p.rows_max = c.max_batch * ((c.max_prompt > c.max_k ? c.max_prompt : c.max_k) + c.max_k);
   p.head_max = c.max_batch * c.max_k;
+  if (c.flags & KF_FLAG_ROLLOUT) {
+    const int r2 = 2 * c.max_batch * c.max_prompt * c.max_k;
+    if (r2 > p.rows_max) p.rows_max = r2;
+    if (c.max_batch * c.max_prompt * c.max_k > p.head_max) p.head_max = c.max_batch * c.max_prompt * c.max_k;
+  }
   if (c.flags & KF_FLAG_TEACHER) {
     const long long tr = (long long)c.max_batch * c.max_prompt;
     p.teacher_rows = (int)(tr < kTeacherChunk ? tr : kTeacherChunk);
@@ -170,6 +180,9 @@ void make_plan(const kf_config& c, Plan& p) {
   p.pval = take((size_t)p.head_max * p.n_tiles * 4);
   p.pidx = take((size_t)p.head_max * p.n_tiles * 4);
   p.logits = take((size_t)p.logit_rows * c.vocab * 4);
+  if (c.flags & KF_FLAG_ROLLOUT)
+    p.roll_kv = take(L * 2 * (size_t)c.max_batch * c.n_head *
+                     ((size_t)c.max_prompt * (1 + 2 * (size_t)c.max_k)) * (d / c.n_head) * es);
   p.tmax = take((size_t)p.teacher_rows * p.n_tiles * 4);
   p.tsub = take((size_t)p.teacher_rows * p.n_tiles * 8 * 4);
   p.dstate = take(sizeof(KfDevState));
@@ -409,6 +422,117 @@ int run_step(kf_ctx* c, const StepIn& in) {
   KF_LAUNCH(c, KF_KC_SELECT, kf::launch_commit(st, in.nr, s));
   c->last_head_rows = Mh;
   c->last_logits = logits != nullptr;
+  return KF_OK;
+}
+
+// Stage-2 self-forcing teacher rollout (Appendix C.2): round 1 is a
+// SingleForward pass over [context N | noise N*k] rows per sequence, its
+// noise rows' argmax giving x1; round 2 a DoubleForward pass over
+// [Future-1 N*k | Future-2 N*k] rows (x1 as tokens, then fresh noise) that
+// attends to round 1's context keys, its Future-2 argmax giving x2.  Each
+// layer's keys and values live in one buffer [B][H][N + 2Nk][dh]:
+// [context | noise of round 1, then Future-1 | Future-2].
+template <typename T>
+int run_rollout(kf_ctx* c, int B, int N, int k, const int32_t* tokens, const float* z1,
+                const float* z2, int32_t* x1, int32_t* x2) {
+  const Plan& p = c->plan;
+  char* base = c->base;
+  const kf_config& cf = c->cfg;
+  const int d = cf.d_model, f = cf.d_mlp, V = cf.vocab, H = cf.n_head, dh = d / H;
+  hipStream_t s = c->stream;
+  KfDevState* st = reinterpret_cast<KfDevState*>(base + p.dstate);
+  float* X = reinterpret_cast<float*>(base + p.X);
+  T* Xh = reinterpret_cast<T*>(base + p.Xh);
+  float2* lnst = reinterpret_cast<float2*>(base + p.lnst);
+  const T* temb = (cf.flags & KF_FLAG_TEMPERATURE) ? reinterpret_cast<const T*>(base + p.temb) : nullptr;
+  const kf::SplitWs sws{reinterpret_cast<float*>(base + p.split_part), kSplitBytes};
+  T* A = reinterpret_cast<T*>(base + p.A);
+  T* Q = reinterpret_cast<T*>(base + p.Q);
+  T* O = reinterpret_cast<T*>(base + p.O);
+  T* Hm = reinterpret_cast<T*>(base + p.Hm);
+  const T* tok = reinterpret_cast<const T*>(base + p.tok);
+  const T* pos = reinterpret_cast<const T*>(base + p.pos);
+  auto F = [&](size_t o) { return reinterpret_cast<const float*>(base + o); };
+  auto W = [&](size_t o) { return reinterpret_cast<const T*>(base + o); };
+  const int ldk = N * (1 + 2 * k), nk = N * k;
+  const size_t kvl = (size_t)B * H * ldk * dh;  // elements of one layer's K (or V)
+  T* kvb = reinterpret_cast<T*>(base + p.roll_kv);
+  const bool debug = (cf.flags & KF_FLAG_DEBUG_LOGITS) != 0;
+  float* logits = debug ? reinterpret_cast<float*>(base + p.logits) : nullptr;
+
+  auto noise = [&](const float* z, int n, int off, int shift) -> int {
+    const KfStepGeom gz{B * N, k, 0, k};  // one noise group of k per (sequence, position)
+    KF_LAUNCH(c, KF_KC_NOISE,
+              kf::launch_noise_sinusoid<T>(A, z, 0, reinterpret_cast<const double*>(base + p.omega),
+                                           gz, d, st, nullptr, s));
+    KF_LAUNCH(c, KF_KC_NOISE,
+              kf::gemm_bias<T>(A, W(p.nw1), B * nk, 4 * d, d, F(p.nb1), kf::Act::Gelu, Hm, 4 * d,
+                               &sws, s));
+    KF_LAUNCH(c, KF_KC_NOISE,
+              kf::gemm_seq_noise_out<T>(Hm, W(p.nw2), B * nk, d, 4 * d, F(p.nb2), pos, temb, X, Xh,
+                                        lnst, n, off, N, k, shift, &sws, s));
+    return KF_OK;
+  };
+  auto body = [&](int n, int koff, int mask) -> int {
+    const int M = B * n;
+    for (int l = 0; l < cf.n_layer; ++l) {
+      const LayerOff& y = p.layer[l];
+      const kf::LnFold ln1{F(y.qkv_c1), F(y.qkv_c2), lnst};
+      const kf::LnFold ln2{F(y.up_c1), F(y.up_c2), lnst};
+      T* Kl = kvb + (size_t)l * 2 * kvl;
+      T* Vl = Kl + kvl;
+      KF_LAUNCH(c, KF_KC_QKV,
+                kf::gemm_qkv_seq<T>(Xh, ln1, W(y.wqkv), M, d, F(y.bqkv), Q, Kl, Vl, n, ldk, koff, H, s));
+      KF_LAUNCH(c, KF_KC_ATTN,
+                kf::launch_training_attention_seq(mask, B, H, N, k, dh, reinterpret_cast<const bf16*>(Q),
+                                                  reinterpret_cast<const bf16*>(Kl),
+                                                  reinterpret_cast<const bf16*>(Vl), ldk,
+                                                  reinterpret_cast<bf16*>(O), 1.0f / sqrtf((float)dh), s));
+      KF_LAUNCH(c, KF_KC_OPROJ, kf::gemm_residual<T>(O, W(y.wo), M, d, d, F(y.bo), X, Xh, lnst, &sws, s));
+      KF_LAUNCH(c, KF_KC_MLP_UP, kf::gemm_up_ln<T>(Xh, ln2, W(y.w1), M, f, d, F(y.b1), Hm, s));
+      KF_LAUNCH(c, KF_KC_MLP_DOWN,
+                kf::gemm_residual<T>(Hm, W(y.w2), M, d, f, F(y.b2), X, Xh, lnst, &sws, s));
+    }
+    return KF_OK;
+  };
+  auto head = [&](int n, int off, int32_t* out) -> int {
+    const KfStepGeom gh{B, n, off, nk};  // head rows: the nk rows after `off` of each sequence
+    const kf::LnFold lnf{F(p.head_c1), F(p.head_c2), lnst};
+    KF_LAUNCH(c, KF_KC_HEAD,
+              kf::gemm_head_ln<T>(Xh, lnf, W(p.head_w), B * nk, p.Vpad, V, d, 1, gh,
+                                  reinterpret_cast<float*>(base + p.pval),
+                                  reinterpret_cast<int*>(base + p.pidx), logits, s));
+    KfOutDesc od;
+    od.out = out;
+    od.stride = nk;
+    od.gen_base = -1;
+    od.pend = nullptr;
+    od.pend_stride = 0;
+    KF_LAUNCH(c, KF_KC_SELECT,
+              kf::launch_argmax_select(reinterpret_cast<const float*>(base + p.pval),
+                                       reinterpret_cast<const int*>(base + p.pidx), p.n_tiles, gh,
+                                       st, od, s));
+    return KF_OK;
+  };
+
+  KF_HIP(c, kf::launch_zero_i32(reinterpret_cast<int*>(st), 1, s));  // C = 0: context positions 0..N-1
+  // round 1: SingleForward over [context | noise z1]
+  const int n1 = N + nk;
+  KF_LAUNCH(c, KF_KC_EMBED,
+            kf::launch_embed_real<T>(X, Xh, lnst, tok, pos, tokens, N, KfStepGeom{B, n1, N, 0}, d, V,
+                                     st, s));
+  if (int r = noise(z1, n1, N, 1)) return r;
+  if (int r = body(n1, 0, KF_MASK_SINGLE)) return r;
+  if (int r = head(n1, N, x1)) return r;
+  // round 2: DoubleForward over [Future-1 = x1 | Future-2 = noise z2]
+  const int n2 = 2 * nk;
+  KF_LAUNCH(c, KF_KC_EMBED,
+            kf::launch_embed_group<T>(X, Xh, lnst, tok, pos, x1, B, N, k, n2, 0, 1, d, V, st, s));
+  if (int r = noise(z2, n2, nk, 1 + k)) return r;
+  if (int r = body(n2, N, KF_MASK_DOUBLE)) return r;
+  if (int r = head(n2, nk, x2)) return r;
+  c->last_head_rows = B * nk;
+  c->last_logits = debug;
   return KF_OK;
 }
 
@@ -952,6 +1076,31 @@ int kf_teacher_targets(kf_ctx* c, int B, int N, const int32_t* tokens, const flo
   c->B = 0;
   drop_graph(c);
   return step(c, in);
+}
+
+int kf_selfforcing_targets(kf_ctx* c, int B, int N, int k, const int32_t* tokens, const float* z1,
+                           const float* z2, int32_t* x1, int32_t* x2) {
+  if (!c) return KF_EINVAL;
+  if (int r = ready(c)) return r;
+  const kf_config& cf = c->cfg;
+  if (!(cf.flags & KF_FLAG_ROLLOUT))
+    return fail(c, KF_ESTATE, "the teacher rollout needs a context created with KF_FLAG_ROLLOUT");
+  if (cf.dtype != KF_BF16) return fail(c, KF_EINVAL, "the teacher rollout runs bf16 models only");
+  if (B < 1 || B > cf.max_batch) return fail(c, KF_EINVAL, "B = %d outside [1, %d]", B, cf.max_batch);
+  if (N < 1 || N > cf.max_prompt)
+    return fail(c, KF_EINVAL, "N = %d outside [1, max_prompt = %d]", N, cf.max_prompt);
+  if (k < 1 || k > cf.max_k) return fail(c, KF_EINVAL, "k = %d outside [1, max_k = %d]", k, cf.max_k);
+  if (N + 2 * k > cf.n_ctx)
+    return fail(c, KF_ECTX, "N + 2k = %d exceeds n_ctx = %d", N + 2 * k, cf.n_ctx);
+  if (!tokens || !z1 || !z2 || !x1 || !x2) return fail(c, KF_EINVAL, "null pointer");
+  if (int r = temp_ready(c, B)) return r;
+  // the rollout uses the step workspace and the device state: a generation in progress ends
+  c->live = false;
+  c->C = 0;
+  c->pending = 0;
+  c->B = 0;
+  drop_graph(c);
+  return run_rollout<bf16>(c, B, N, k, tokens, z1, z2, x1, x2);
 }
 
 int kf_training_attention(void* hip_stream, int mask, int B, int H, int N, int k, int d_head,

@@ -218,7 +218,7 @@ template <int DH, int S>
 __global__ void __launch_bounds__(256)
     training_attention_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
                               const bf16* __restrict__ V, bf16* __restrict__ O, int mask, int N,
-                              int k, int nq, int nk, int BH, float c2) {
+                              int k, int nq, int ldk, int H, int BH, int o_inter, float c2) {
   using G = Geo<DH, S>;
   constexpr int NDC = DH / 32, NDB = DH / 16;
   __shared__ __attribute__((aligned(1024))) unsigned char smem[S * G::STAGEB];
@@ -263,7 +263,7 @@ __global__ void __launch_bounds__(256)
     const bool live = ti < C.ntiles;
     const int t0 = live ? C.t0(ti) : 0;
     const int rows = live ? min(C.end(ti) - t0, kKT) : 0;
-    const size_t off = ((size_t)C.bh * nk + t0) * DH;
+    const size_t off = ((size_t)C.bh * ldk + t0) * DH;
     const __amdgpu_buffer_rsrc_t rk = make_rsrc(K + off, rows * G::ROWB);
     const __amdgpu_buffer_rsrc_t rv = make_rsrc(V + off, rows * G::ROWB);
     unsigned char* st = smem + stage * G::STAGEB;
@@ -400,7 +400,10 @@ __global__ void __launch_bounds__(256)
   // lane: query lq, d_head 16db + 4gq + r
   if (valid) {
     const float inv = 1.0f / ls[0];
-    bf16* orow = O + ((size_t)C.bh * nq + row) * DH + 4 * gq;
+    // O: [B][H][nq][DH], or [B][nq][H][DH] (rows of a residual stream) with o_inter
+    const int ob = C.bh / H, oh = C.bh - ob * H;
+    bf16* orow = O + (o_inter ? (((size_t)ob * nq + row) * H + oh) * DH
+                              : ((size_t)C.bh * nq + row) * DH) + 4 * gq;
 #pragma unroll
     for (int db = 0; db < NDB; ++db) {
       const bf16 e0 = (bf16)(o[db][0] * inv), e1 = (bf16)(o[db][1] * inv);
@@ -427,15 +430,24 @@ namespace {
 
 template <int DH, int S>
 hipError_t launch_ta(int mask, int B, int H, int N, int k, const bf16* Q, const bf16* K,
-                     const bf16* V, bf16* O, float scale, hipStream_t s) {
+                     const bf16* V, int ldk, bf16* O, int o_inter, float scale, hipStream_t s) {
   const int nq = training_attention_rows(mask, N, k);
-  const int nk = training_attention_keys(mask, N, k);
   const int BH = B * H;
   const dim3 grid((unsigned)((long long)BH * ((nq + kQB - 1) / kQB)));  // one workgroup per item
   const float c2 = scale * 1.4426950408889634f;  // scale * log2(e)
-  launch(training_attention_kernel<DH, S>, grid, dim3(256), 0, s, Q, K, V, O, mask, N, k, nq, nk,
-         BH, c2);
+  launch(training_attention_kernel<DH, S>, grid, dim3(256), 0, s, Q, K, V, O, mask, N, k, nq, ldk,
+         H, BH, o_inter, c2);
   return hipGetLastError();
+}
+
+hipError_t launch_ta_dh(int mask, int B, int H, int N, int k, int dh, const bf16* Q, const bf16* K,
+                        const bf16* V, int ldk, bf16* O, int o_inter, float scale, hipStream_t s) {
+  switch (dh) {
+    case 32: return launch_ta<32, 3>(mask, B, H, N, k, Q, K, V, ldk, O, o_inter, scale, s);
+    case 64: return launch_ta<64, 2>(mask, B, H, N, k, Q, K, V, ldk, O, o_inter, scale, s);
+    case 128: return launch_ta<128, 2>(mask, B, H, N, k, Q, K, V, ldk, O, o_inter, scale, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace
@@ -443,12 +455,14 @@ hipError_t launch_ta(int mask, int B, int H, int N, int k, const bf16* Q, const 
 hipError_t launch_training_attention(int mask, int B, int H, int N, int k, int dh, const bf16* Q,
                                      const bf16* K, const bf16* V, bf16* O, float scale,
                                      hipStream_t s) {
-  switch (dh) {
-    case 32: return launch_ta<32, 3>(mask, B, H, N, k, Q, K, V, O, scale, s);
-    case 64: return launch_ta<64, 2>(mask, B, H, N, k, Q, K, V, O, scale, s);
-    case 128: return launch_ta<128, 2>(mask, B, H, N, k, Q, K, V, O, scale, s);
-    default: return hipErrorInvalidValue;
-  }
+  return launch_ta_dh(mask, B, H, N, k, dh, Q, K, V, training_attention_keys(mask, N, k), O, 0,
+                      scale, s);
+}
+
+hipError_t launch_training_attention_seq(int mask, int B, int H, int N, int k, int dh, const bf16* Q,
+                                         const bf16* K, const bf16* V, int ldk, bf16* O,
+                                         float scale, hipStream_t s) {
+  return launch_ta_dh(mask, B, H, N, k, dh, Q, K, V, ldk, O, 1, scale, s);
 }
 
 }  // namespace kf

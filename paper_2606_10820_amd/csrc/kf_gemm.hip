@@ -218,6 +218,63 @@ struct EpNoiseOut {
   }
 };
 
+// Q, K, V of a whole-sequence forward (the K-Forcing teacher rollout): GEMM
+// row m = (b, i), i < n, in the layouts of the training-mask attention: Q
+// [B][H][n][dh]; K and V [B][H][ldk][dh], row i at key koff + i.
+template <typename T>
+struct EpQKVSeq {
+  T* Q;
+  T* K;
+  T* V;
+  const float* bias;
+  int n, ldk, koff, H, dh;
+  static constexpr bool kStats = false;
+  __device__ inline void store8(int m, int c, float (&v)[8]) const {
+    const int d = H * dh, which = c / d, cc = c - which * d, h = cc / dh, e = cc - h * dh;
+    const int b = m / n, i = m - b * n;
+    const size_t bh = (size_t)b * H + h;
+    if (which == 0) put8(Q + (bh * n + i) * dh + e, v);
+    else put8((which == 1 ? K : V) + (bh * ldk + koff + i) * dh + e, v);
+  }
+};
+
+// Second noise-MLP layer of a whole-sequence forward: noise row m = (b, t, j)
+// (N groups of k per sequence) lands in residual row b*n + off + t*k + j with
+// the learned position t + shift + j added (the position of the token the
+// row stands for) and, for a temperature-conditioned model, sequence b's
+// temperature embedding.
+template <typename T>
+struct EpSeqNoise {
+  float* X;
+  T* Xh;
+  const float* bias;
+  const T* pos;
+  const T* temb;  // [B][d] or null
+  int n, off, N, k, shift, d;
+  float2* lnst;
+  static constexpr bool kStats = true;
+  __device__ inline int cols() const { return d; }
+  __device__ inline int srow(int m) const {
+    const int nk = N * k, b = m / nk;
+    return b * n + off + (m - b * nk);
+  }
+  __device__ inline void store8(int m, int c, float (&v)[8]) const {
+    const int nk = N * k, b = m / nk, q = m - b * nk, t = q / k, j = q - t * k;
+    const size_t row = (size_t)srow(m);
+    float pe[8];
+    get8(pos + (size_t)(t + shift + j) * d + c, pe);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] += pe[i];
+    if (temb) {
+      get8(temb + (size_t)b * d + c, pe);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] += pe[i];
+    }
+    put8(X + row * d + c, v);
+    if constexpr (sizeof(T) == 2) put8(Xh + row * d + c, v);
+  }
+};
+
 // One K split of a split-K GEMM: fp32 C rows to part [M][ldp] (the kernel
 // moves part to its split's slice); the bias and the GEMM's real epilogue run
 // in splitk_reduce_kernel.
@@ -916,6 +973,23 @@ hipError_t gemm_head_ln(const T* Xh, const LnFold& ln, const T* W, int M, int Vp
 }
 
 template <typename T>
+hipError_t gemm_qkv_seq(const T* Xh, const LnFold& ln, const T* W, int M, int d, const float* bias,
+                        T* Q, T* K, T* V, int n, int ldk, int koff, int H, hipStream_t s) {
+  EpQKVSeq<T> ep{Q, K, V, bias, n, ldk, koff, H, d / H};
+  return dispatch<T, 0, true>(GemmA{Xh, d, M, ln.c1, ln.c2, ln.lnst, KfStepGeom{}}, W, M, 3 * d, d,
+                              ep, s);
+}
+
+template <typename T>
+hipError_t gemm_seq_noise_out(const T* A, const T* W, int M, int d, int K, const float* bias,
+                              const T* pos, const T* temb, float* X, T* Xh, float2* lnst, int n,
+                              int off, int N, int k, int shift, const SplitWs* ws, hipStream_t s) {
+  EpSeqNoise<T> ep{X, Xh, bias, pos, temb, n, off, N, k, shift, d, lnst};
+  return dispatch<T, 0, false>(GemmA{A, K, M, nullptr, nullptr, nullptr, KfStepGeom{}}, W, M, d, K,
+                               ep, s, ws);
+}
+
+template <typename T>
 hipError_t gemm_head_sample(const T* Xh, const LnFold& ln, const T* W, int M, int Vpad, int V, int d,
                             int row0, int rows_per_seq, const float* tau, float* pmax, float* psub,
                             float* logits, hipStream_t s) {
@@ -954,6 +1028,11 @@ hipError_t launch_ln_fold(const T* W, T* Wout, const float* g, const float* beta
                                     const float*, T*, hipStream_t);                                \
   template hipError_t gemm_head_ln<T>(const T*, const LnFold&, const T*, int, int, int, int, int, \
                                       KfStepGeom, float*, int*, float*, hipStream_t);              \
+  template hipError_t gemm_qkv_seq<T>(const T*, const LnFold&, const T*, int, int, const float*,  \
+                                      T*, T*, T*, int, int, int, int, hipStream_t);                \
+  template hipError_t gemm_seq_noise_out<T>(const T*, const T*, int, int, int, const float*,      \
+                                            const T*, const T*, float*, T*, float2*, int, int, int, \
+                                            int, int, const SplitWs*, hipStream_t);                \
   template hipError_t gemm_head_sample<T>(const T*, const LnFold&, const T*, int, int, int, int,  \
                                           int, int, const float*, float*, float*, float*,          \
                                           hipStream_t);                                            \

@@ -197,6 +197,25 @@ hipError_t launch_teacher_select(const float* pmax, const float* psub, int n_til
                                  int M, int rows_per_seq, int32_t* targets, KfDevState* st,
                                  hipStream_t s);
 
+// Whole-sequence forward of the teacher rollout (SingleForward / DoubleForward
+// passes).  Rows of sequence b are residual rows b*n .. b*n + n - 1.
+//   gemm_qkv_seq: LayerNorm-folded QKV; Q to [B][H][n][dh], K and V to
+//     [B][H][ldk][dh] at keys koff + i.
+//   gemm_seq_noise_out: second noise-MLP layer; noise row (b, t, j) of N groups
+//     of k to residual row b*n + off + t*k + j, position t + shift + j.
+//   launch_embed_group: token rows (b, t, j) likewise, tokens [B][N*k].
+template <typename T>
+hipError_t gemm_qkv_seq(const T* Xh, const LnFold& ln, const T* W, int M, int d, const float* bias,
+                        T* Q, T* K, T* V, int n, int ldk, int koff, int H, hipStream_t s);
+template <typename T>
+hipError_t gemm_seq_noise_out(const T* A, const T* W, int M, int d, int K, const float* bias,
+                              const T* pos, const T* temb, float* X, T* Xh, float2* lnst, int n,
+                              int off, int N, int k, int shift, const SplitWs* ws, hipStream_t s);
+template <typename T>
+hipError_t launch_embed_group(float* X, T* Xh, float2* lnst, const T* tok, const T* pos,
+                              const int32_t* toks, int B, int N, int k, int n, int off, int shift,
+                              int d, int V, KfDevState* st, hipStream_t s);
+
 // Fold a LayerNorm into the GEMM that consumes it: Wout = W diag(gain) in T,
 // c1 = Wout 1, c2 = W shift; W [N][K], Wout may alias W.
 template <typename T>
@@ -237,5 +256,10 @@ int training_attention_keys(int mask, int N, int k);
 hipError_t launch_training_attention(int mask, int B, int H, int N, int k, int dh, const bf16* Q,
                                      const bf16* K, const bf16* V, bf16* O, float scale,
                                      hipStream_t s);
+// The same with K, V holding ldk keys per head and O written as the rows of a
+// residual stream, [B][rows][H][dh].
+hipError_t launch_training_attention_seq(int mask, int B, int H, int N, int k, int dh, const bf16* Q,
+                                         const bf16* K, const bf16* V, int ldk, bf16* O,
+                                         float scale, hipStream_t s);
 
 }  // namespace kf

@@ -444,7 +444,7 @@ __global__ void __launch_bounds__(256)
     const int b = m / g.k, j = m % g.k;
     if (bi == 0x7fffffff) bi = 0;
     od.out[out_index(od, st->C, g.nr, b, j)] = bi;
-    od.pend[(size_t)b * od.pend_stride + j] = bi;
+    if (od.pend) od.pend[(size_t)b * od.pend_stride + j] = bi;
   }
 }
 
@@ -507,6 +507,42 @@ __global__ void __launch_bounds__(1024)
     }
     od.out[out_index(od, C, g.nr, b, 0)] = tok;
     od.pend[(size_t)b * od.pend_stride] = tok;
+  }
+}
+
+// Token rows of a whole-sequence forward laid out as N groups of k (the
+// Future-1 rows of DoubleForward): row (b, t, j) takes token toks[b][t*k + j]
+// at position t + shift + j into residual row b*n + off + t*k + j, with its
+// LayerNorm partial sums, as embed_real_kernel does for a step's real rows.
+template <typename T>
+__global__ void __launch_bounds__(256)
+    embed_group_kernel(float* __restrict__ X, T* __restrict__ Xh, float2* __restrict__ lnst,
+                       const T* __restrict__ tok, const T* __restrict__ pos,
+                       const int32_t* __restrict__ toks, int N, int k, int n, int off, int shift,
+                       int d, int V, KfDevState* st) {
+  const int r = blockIdx.x, nk = N * k;
+  const int b = r / nk, q = r - b * nk, t = q / k, j = q - t * k;
+  int tk = toks[(size_t)b * nk + q];
+  if (tk < 0 || tk >= V) {
+    if (threadIdx.x == 0) atomicOr(&st->err, 1);
+    tk = 0;
+  }
+  const size_t row = (size_t)b * n + off + q;
+  const T* te = tok + (size_t)tk * d;
+  const T* pe = pos + (size_t)(t + shift + j) * d;
+  const int grp = threadIdx.x;
+  if (grp < d / 16) {
+    float a = 0.f, sq = 0.f;
+#pragma unroll
+    for (int c = 0; c < 16; ++c) {
+      const int e = grp * 16 + c;
+      const float v = to_f(te[e]) + to_f(pe[e]);
+      X[row * d + e] = v;
+      if constexpr (sizeof(T) == 2) Xh[row * d + e] = from_f<T>(v);
+      a += v;
+      sq += v * v;
+    }
+    lnst[row * (d / 16) + grp] = make_float2(a, sq);
   }
 }
 
@@ -844,6 +880,16 @@ hipError_t launch_icdf_select(const float* logits, int V, const float* u_in, uin
 }
 
 template <typename T>
+hipError_t launch_embed_group(float* X, T* Xh, float2* lnst, const T* tok, const T* pos,
+                              const int32_t* toks, int B, int N, int k, int n, int off, int shift,
+                              int d, int V, KfDevState* st, hipStream_t s) {
+  if (B * N * k <= 0) return hipSuccess;
+  launch(embed_group_kernel<T>, dim3(B * N * k), dim3(256), 0, s, X, Xh, lnst, tok, pos, toks, N,
+         k, n, off, shift, d, V, st);
+  return hipGetLastError();
+}
+
+template <typename T>
 hipError_t launch_teacher_select(const float* pmax, const float* psub, int n_tiles, int V,
                                  const T* Xh, const float2* lnst, const T* W, const float* c1,
                                  const float* c2, int d, const float* tau, const float* u, int row0,
@@ -900,6 +946,9 @@ hipError_t launch_zero_i32(int* dst, size_t n, hipStream_t s) { return launch_ze
                                           KfKvGeom, int, const AttnSplit&, hipStream_t);            \
   template hipError_t launch_convert<T>(const float*, T*, size_t, hipStream_t);                    \
   template hipError_t launch_zero<T>(T*, size_t, hipStream_t);                                   \
+  template hipError_t launch_embed_group<T>(float*, T*, float2*, const T*, const T*,              \
+                                            const int32_t*, int, int, int, int, int, int, int, int, \
+                                            KfDevState*, hipStream_t);                              \
   template hipError_t launch_teacher_select<T>(const float*, const float*, int, int, const T*,     \
                                                const float2*, const T*, const float*, const float*, \
                                                int, const float*, const float*, int, int, int,      \
