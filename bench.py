@@ -123,6 +123,10 @@ def parse():
                     help="skip the distillation-target measurement")
     ap.add_argument("--teacher-only", action="store_true",
                     help="measure only the distillation targets and print their JSON")
+    ap.add_argument("--no-rollout", action="store_true",
+                    help="skip the self-forcing target measurement")
+    ap.add_argument("--rollout-only", action="store_true",
+                    help="measure only the self-forcing targets and print their JSON")
     ap.add_argument("--cpu-blocks", type=int, default=28,
                     help="decode blocks per sequence in the CPU oracle sample")
     ap.add_argument("--summarize", metavar="DIR", default=None,
@@ -457,6 +461,84 @@ def teacher_bench(reps: int = 3):
     return {"entry": "kf_teacher_targets", "cases": out}
 
 
+def rollout_costs(cfg: S.ModelConfig, B: int, N: int, k: int):
+    """(bytes, flops) of one kf_selfforcing_targets call: per round, the body
+    GEMMs over its rows, the block-sparse attention over its visible pairs,
+    the noise MLP over N*k rows and the head over N*k rows (the step formulas
+    of step_costs applied to the rounds' row counts)."""
+    es = 2 if cfg.dtype == S.DTYPE_BF16 else 4
+    d, f, V, L = cfg.d_model, cfg.d_mlp, cfg.vocab, cfg.n_layer
+    nk = N * k
+    ctx = N * (N + 1) // 2
+    noise = k * N * (N + 1) // 2 + nk * (k + 1) // 2
+    rounds = ((N + nk, ctx + noise, N + nk), (2 * nk, 2 * noise + nk * k, N + 2 * nk))
+    by = fl = 0.0
+    for rows, pairs, keys in rounds:
+        M = B * rows
+        fl += L * (2.0 * M * (4 * d * d + 2 * d * f) + 4.0 * d * B * pairs)
+        by += L * ((4 * d * d + 2 * d * f) * es + M * (6 * d * es + 2 * f * es + 4 * d * 4)
+                   + B * keys * 2 * d * es)
+        fl += 2.0 * B * nk * (8 * d * d) + 2.0 * B * nk * V * d
+        by += 8 * d * d * es + V * d * es + B * nk * (6 * d * es + 8)
+    return by, fl
+
+
+def rollout_bench(reps: int = 2):
+    """Stage-2 self-forcing targets (kf_selfforcing_targets), teacher window
+    k = 2 (the PFLM(2) -> PFLM(4) stage), 64 sequences of the LM1B-shaped
+    (N = 128 - 2k) and OWT-shaped (N = 1024 - 2k) models: targets per second
+    (2k per context position) and the call's roofline fraction."""
+    import torch
+    from paper_2606_10820_amd import binding as Bd
+    dev = torch.device("cuda:0")
+    out = []
+    k = 2
+    for name in ("lm1b", "owt"):
+        w = S.WORKLOADS[name]
+        cfg = w["cfg"]
+        B, N = 64, cfg.n_ctx - 2 * k
+        log(f"[bench] self-forcing targets {name}: B={B}, N={N}, k={k}")
+        blob = S.pack_blob(cfg, S.make_weights(cfg, seed=0))
+        kc = Bd.make_config(cfg.n_layer, cfg.d_model, cfg.n_head, cfg.d_mlp, cfg.vocab, cfg.n_ctx,
+                            cfg.dtype, B, k, N, Bd.KF_FLAG_ROLLOUT)
+        kf = Bd.KForcing(kc, device="cuda:0")
+        kf.load_weights(blob)
+        tokens = torch.as_tensor(S.make_prompts(w["prompts"], 3, B, N, cfg.vocab), device=dev)
+        g = torch.Generator(device=dev)
+        g.manual_seed(7)
+        z1 = torch.rand((B, N, k), device=dev, generator=g)
+        z2 = torch.rand((B, N, k), device=dev, generator=g)
+        x1 = torch.empty((B, N, k), dtype=torch.int32, device=dev)
+        x2 = torch.empty_like(x1)
+        L = kf.L
+        call = lambda: L.kf_selfforcing_targets(kf.h, B, N, k, kf._p(tokens), kf._p(z1),
+                                                kf._p(z2), kf._p(x1), kf._p(x2))
+        assert call() == 0
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            call()
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) / reps * 1e3
+        kf.set_timing(Bd.KF_TIMING_ALL)
+        call()
+        per = {n: round(kf.kernel_time(ci)[0], 4) for ci, n in enumerate(CLASSES)}
+        kf.set_timing(0)
+        by, fl = rollout_costs(cfg, B, N, k)
+        roof = max(by / (PEAK_HBM_GBS * 1e9), fl / (PEAK_MFMA_TFLOPS[cfg.dtype] * 1e12)) * 1e3
+        out.append({"workload": f"{name}-shaped teacher, B={B}, N={N}, k={k} (2k targets per position)",
+                    "ms": round(ms, 3), "targets_per_s": round(B * N * 2 * k / (ms * 1e-3), 1),
+                    "algorithmic_flops": fl, "algorithmic_bytes": by,
+                    "tflops": round(fl / (ms * 1e-3) / 1e12, 1),
+                    "roofline_ms": round(roof, 4), "roofline_frac": round(roof / ms, 4),
+                    "kernel_ms": per})
+        log(f"[bench] self-forcing {name}: {ms:.2f} ms, {B * N * 2 * k / (ms * 1e-3):,.0f} targets/s, "
+            f"{fl / (ms * 1e-3) / 1e12:.0f} TFLOP/s, {roof / ms:.1%} of its roofline")
+        del kf
+        torch.cuda.empty_cache()
+    return {"entry": "kf_selfforcing_targets", "cases": out}
+
+
 def training_attention_bench(reps: int = 10):
     """Block-sparse attention of the training masks (SingleForward M_S and
     DoubleForward M_D, Appendix C.2) at one GPU's share of the paper's
@@ -518,6 +600,9 @@ def main():
         return
     if a.teacher_only:
         print(json.dumps(teacher_bench(max(a.steps, 1))), flush=True)
+        return
+    if a.rollout_only:
+        print(json.dumps(rollout_bench(max(a.steps, 1))), flush=True)
         return
 
     w = S.WORKLOADS[a.workload]
@@ -638,6 +723,8 @@ def main():
         res["training_attention"] = training_attention_bench()
     if not a.no_teacher:
         res["teacher_targets"] = teacher_bench()
+    if not a.no_rollout:
+        res["selfforcing_targets"] = rollout_bench()
 
     if not a.no_cpu:
         log("[bench] CPU oracle sample ...")

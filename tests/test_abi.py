@@ -61,8 +61,10 @@ def test_strerror(L):
 @pytest.mark.parametrize("bad", [
     dict(n_layer=0), dict(d_model=100), dict(n_head=3), dict(d_model=256, n_head=1),
     dict(d_mlp=100), dict(vocab=1), dict(n_ctx=100), dict(dtype=7), dict(max_batch=0), dict(max_k=0),
-    dict(max_k=1000), dict(max_prompt=0), dict(flags=8),
+    dict(max_k=1000), dict(max_prompt=0), dict(flags=16),
     dict(max_batch=65535, max_prompt=128, d_mlp=4096),
+    # the teacher rollout's DoubleForward rows (2 * max_batch * max_prompt * max_k) count too
+    dict(flags=8, max_batch=4096, max_prompt=128),
 ])
 def test_bad_config_rejected(L, bad):
     cfg = _cfg(**bad)
@@ -219,6 +221,20 @@ def test_teacher_targets_argument_checks(L):
     # argument ranges are checked after the state: a context without KF_FLAG_TEACHER
     # and with weights would say ESTATE; with the flag, bad sizes say EINVAL
     assert L.kf_teacher_targets(None, 1, 4, fake, fake, fake, fake) == Bd.KF_EINVAL
+
+
+def test_selfforcing_argument_checks(L):
+    P = ctypes.c_void_p
+    fake = P(0x10000)  # never dereferenced: every call below fails validation first
+    plain = _ctx(L, _cfg())
+    assert L.kf_selfforcing_targets(plain, 1, 4, 2, fake, fake, fake, fake, fake) == Bd.KF_ESTATE
+    L.kf_destroy(plain)
+    cfg = _cfg(flags=Bd.KF_FLAG_ROLLOUT)
+    assert L.kf_state_bytes(ctypes.byref(cfg)) > L.kf_state_bytes(ctypes.byref(_cfg()))
+    h = _ctx(L, cfg)
+    assert L.kf_selfforcing_targets(h, 1, 4, 2, fake, fake, fake, fake, fake) == Bd.KF_ESTATE
+    L.kf_destroy(h)
+    assert L.kf_selfforcing_targets(None, 1, 4, 2, fake, fake, fake, fake, fake) == Bd.KF_EINVAL
 
 
 def test_null_context(L):
