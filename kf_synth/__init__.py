@@ -151,6 +151,7 @@ class ModelConfig:
     n_ctx: int
     dtype: int  # DTYPE_FP32 or DTYPE_BF16
     temperature: bool = False  # temperature-conditioned noise encoder
+    rms_rope: bool = False     # RMSNorm + rotary positions (no learned positions)
 
     @property
     def d_head(self) -> int:
@@ -193,13 +194,15 @@ def n_params(cfg: ModelConfig) -> int:
 
 
 BLOB_FLAG_TEMPERATURE = 1  # header word 9: the temperature encoder's tensors follow lnf_b
+BLOB_FLAG_RMS_ROPE = 2     # header word 9: RMSNorm + rotary positions (pos and norm shifts unused)
 
 
 def header(cfg: ModelConfig) -> np.ndarray:
     h = np.zeros(HEADER_INTS, dtype=np.int32)
     h[:10] = [BLOB_MAGIC, BLOB_VERSION, cfg.n_layer, cfg.d_model, cfg.n_head,
               cfg.d_mlp, cfg.vocab, cfg.n_ctx, cfg.dtype,
-              BLOB_FLAG_TEMPERATURE if cfg.temperature else 0]
+              (BLOB_FLAG_TEMPERATURE if cfg.temperature else 0)
+              | (BLOB_FLAG_RMS_ROPE if cfg.rms_rope else 0)]
     return h
 
 
@@ -214,7 +217,9 @@ def make_weights(cfg: ModelConfig, seed: int = 0, std: float = 0.02,
     for ti, (name, shape) in enumerate(tensor_table(cfg)):
         n = int(np.prod(shape))
         base = name.split(".")[-1]
-        if len(shape) == 2:
+        if cfg.rms_rope and (name == "pos_emb" or (base.endswith("_b") and base.startswith("ln"))):
+            arr = np.zeros(n, np.float32)  # a rotary RMSNorm model has neither
+        elif len(shape) == 2:
             arr = normal(seed, ti, n, std)
         elif base.endswith("_g"):
             arr = (np.ones(n, np.float32) if not random_affine

@@ -85,6 +85,10 @@ def lib():
             f = getattr(L, "orc_gelu" + sfx); f.restype = ctypes.c_double; f.argtypes = [ctypes.c_double]
             f = getattr(L, "orc_layernorm" + sfx); f.restype = None
             f.argtypes = [dp, dp, dp, ctypes.c_int, dp]
+            f = getattr(L, "orc_rmsnorm" + sfx); f.restype = None
+            f.argtypes = [dp, dp, ctypes.c_int, dp]
+            f = getattr(L, "orc_rope" + sfx); f.restype = None
+            f.argtypes = [dp, ctypes.c_int, ctypes.c_int, ctypes.c_int]
             f = getattr(L, "orc_sinusoid" + sfx); f.restype = None
             f.argtypes = [ctypes.c_double, ctypes.c_int, dp]
             f = getattr(L, "orc_attend" + sfx); f.restype = ctypes.c_double
@@ -196,6 +200,21 @@ def icdf(q: Sequence[float], z: float) -> int:
     """Inverse-CDF map with the strict-inequality convention of Appendix B."""
     q = np.ascontiguousarray(np.asarray(q, np.float64))
     return int(_f("orc_icdf", "f64")(_dp(q), q.size, float(z)))
+
+
+def rmsnorm(x, g, prec: str = "f64") -> np.ndarray:
+    x = np.ascontiguousarray(x, np.float64)
+    g = np.ascontiguousarray(g, np.float64)
+    y = np.zeros_like(x)
+    _f("orc_rmsnorm", prec)(_dp(x), _dp(g), x.size, _dp(y))
+    return y
+
+
+def rope(x, H: int, dh: int, p: int, prec: str = "f64") -> np.ndarray:
+    """The oracle's rotary map of one row x [H*dh] at position p."""
+    y = np.ascontiguousarray(np.array(x, np.float64))
+    _f("orc_rope", prec)(_dp(y), H, dh, int(p))
+    return y
 
 
 def gelu(x: float, prec: str = "f64") -> float:
@@ -384,6 +403,7 @@ def parse_blob(blob: np.ndarray) -> Tuple[dict, dict]:
     hdr = blob[:16].view(np.int32)
     L, d, H, f, V, T, dt = (int(x) for x in hdr[2:9])
     temp = bool(int(hdr[9]) & 1)
+    rope = bool(int(hdr[9]) & 2)
     shapes = [("tok", (V, d)), ("pos", (T, d)), ("nw1", (4 * d, d)), ("nb1", (4 * d,)),
               ("nw2", (d, 4 * d)), ("nb2", (d,))]
     for l in range(L):
@@ -404,13 +424,34 @@ def parse_blob(blob: np.ndarray) -> Tuple[dict, dict]:
         W[name] = a.astype(np.float64).reshape(shp)
         off += n
     assert off == blob.size
-    return dict(L=L, d=d, H=H, f=f, V=V, T=T, temperature=temp), W
+    return dict(L=L, d=d, H=H, f=f, V=V, T=T, temperature=temp, rms_rope=rope), W
 
 
 def _np_ln(x, g, b):
     mu = x.mean(-1, keepdims=True)
     var = ((x - mu) ** 2).mean(-1, keepdims=True)
     return (x - mu) / np.sqrt(var + 1e-5) * g + b
+
+
+def _np_rms(x, g):
+    return x / np.sqrt((x * x).mean(-1, keepdims=True) + 1e-5) * g
+
+
+def _np_rope(x, positions, H, dh):
+    """RoFormer rotary map on rows x [n][H*dh] at the given positions: in each
+    head, pairs (2i, 2i+1), i < d_rot/2, d_rot = min(64, dh), turned by
+    p * 10000^(-2i/d_rot)."""
+    x = np.array(x, np.float64)
+    dr = min(64, dh)
+    i = np.arange(dr // 2)
+    ang = np.asarray(positions, np.float64)[:, None] * 10000.0 ** (-2.0 * i / dr)[None, :]
+    c, s = np.cos(ang), np.sin(ang)
+    for h in range(H):
+        x0 = x[:, h * dh + 2 * i].copy()
+        x1 = x[:, h * dh + 2 * i + 1].copy()
+        x[:, h * dh + 2 * i] = x0 * c - x1 * s
+        x[:, h * dh + 2 * i + 1] = x0 * s + x1 * c
+    return x
 
 
 def _np_gelu(x):
@@ -446,12 +487,17 @@ def dense_forward(cfg: dict, W: dict, rows: List[Tuple[str, float]], positions: 
         if cfg.get("temperature"):
             Et = _np_sinusoid([tau], d)[0]
             X[noi_idx] += _np_gelu(Et @ W["tw1"].T + W["tb1"]) @ W["tw2"].T + W["tb2"]
-    X = X + W["pos"][pos]
+    rope = cfg.get("rms_rope", False)
+    nrm = (lambda x, g, b: _np_rms(x, g)) if rope else _np_ln
+    if not rope:
+        X = X + W["pos"][pos]
     neg = np.where(mask, 0.0, -np.inf)
     for l in range(cfg["L"]):
-        A = _np_ln(X, W[f"{l}.ln1_g"], W[f"{l}.ln1_b"])
+        A = nrm(X, W[f"{l}.ln1_g"], W[f"{l}.ln1_b"])
         QKV = A @ W[f"{l}.wqkv"].T + W[f"{l}.bqkv"]
         Q, K, Vv = QKV[:, :d], QKV[:, d:2 * d], QKV[:, 2 * d:]
+        if rope:
+            Q, K = _np_rope(Q, pos, H, dh), _np_rope(K, pos, H, dh)
         O = np.zeros((n, d))
         for h in range(H):
             sl = slice(h * dh, (h + 1) * dh)
@@ -461,9 +507,9 @@ def dense_forward(cfg: dict, W: dict, rows: List[Tuple[str, float]], positions: 
             P = P / P.sum(axis=1, keepdims=True)
             O[:, sl] = P @ Vv[:, sl]
         X = X + O @ W[f"{l}.wo"].T + W[f"{l}.bo"]
-        A = _np_ln(X, W[f"{l}.ln2_g"], W[f"{l}.ln2_b"])
+        A = nrm(X, W[f"{l}.ln2_g"], W[f"{l}.ln2_b"])
         X = X + _np_gelu(A @ W[f"{l}.w1"].T + W[f"{l}.b1"]) @ W[f"{l}.w2"].T + W[f"{l}.b2"]
-    return _np_ln(X, W["lnf_g"], W["lnf_b"]) @ W["tok"].T
+    return nrm(X, W["lnf_g"], W["lnf_b"]) @ W["tok"].T
 
 
 def single_forward_layout(N: int, k: int):

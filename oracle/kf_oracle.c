@@ -36,6 +36,13 @@
  *     on noise rows;
  *   - weights: 2-D tensors are rounded to bf16 (round-to-nearest-even) for
  *     bf16 models, 1-D tensors stay as given;
+ *   - the paper's own backbone (Appendix D model table: RMSNorm pre-norm,
+ *     RoPE with d_rot = 64), for blobs whose header word 9 has bit 1 set:
+ *     every norm is RMSNorm x / sqrt(mean(x^2) + 1e-5) * g (the shift
+ *     tensors are ignored), there are no learned positions (the position
+ *     table is ignored), and q and k of every row are rotated at the row's
+ *     position p by RoFormer's rotary map on the first d_rot = min(64, d_head)
+ *     dimensions of each head: pairs (2i, 2i+1) turned by p * 10000^(-2i/d_rot);
  *   - temperature conditioning (Sec. 3.3 "Temperature-controlled generation",
  *     Appendix C.2 "Temperature control at inference"): a model whose blob
  *     carries the temperature encoder maps each sequence's tau through the
@@ -62,13 +69,14 @@
 #define ORC_MAGIC 0x4B465731
 #define ORC_HDR 16
 #define ORC_FLAG_TEMPERATURE 1 /* header word 9 */
+#define ORC_FLAG_RMS_ROPE 2    /* header word 9: RMSNorm + rotary positions */
 
 typedef struct {
   REAL *ln1_g, *ln1_b, *wqkv, *bqkv, *wo, *bo, *ln2_g, *ln2_b, *w1, *b1, *w2, *b2;
 } orc_layer;
 
 typedef struct {
-  int L, d, H, f, V, T, dtype, temp;
+  int L, d, H, f, V, T, dtype, temp, rope;
   REAL *tok, *pos, *nw1, *nb1, *nw2, *nb2, *lnf_g, *lnf_b;
   REAL *tw1, *tb1, *tw2, *tb2; /* temperature encoder (temp != 0) */
   orc_layer *layer;
@@ -115,6 +123,36 @@ static void layernorm(const REAL *x, const REAL *g, const REAL *b, int d, REAL *
   var /= d;
   REAL r = (REAL)1 / (REAL)sqrt((double)(var + (REAL)1e-5));
   for (int i = 0; i < d; ++i) y[i] = (x[i] - mean) * r * g[i] + b[i];
+}
+
+/* RMSNorm: x / sqrt(mean(x^2) + 1e-5) * g. */
+static void rmsnorm(const REAL *x, const REAL *g, int d, REAL *y) {
+  REAL ms = 0;
+  for (int i = 0; i < d; ++i) ms += x[i] * x[i];
+  ms /= d;
+  REAL r = (REAL)1 / (REAL)sqrt((double)(ms + (REAL)1e-5));
+  for (int i = 0; i < d; ++i) y[i] = x[i] * r * g[i];
+}
+
+/* The model's pre-norm: LayerNorm, or RMSNorm for the rotary backbone. */
+static void norm(const orc_model *m, const REAL *x, const REAL *g, const REAL *b, REAL *y) {
+  if (m->rope) rmsnorm(x, g, m->d, y);
+  else layernorm(x, g, b, m->d, y);
+}
+
+/* Rotary positions (RoFormer): in each head of x [H][dh], the pairs
+ * (2i, 2i+1), i < d_rot/2, turned by the angle p * 10000^(-2i/d_rot). */
+static void rope(REAL *x, int H, int dh, int p) {
+  const int dr = dh < 64 ? dh : 64;
+  for (int h = 0; h < H; ++h)
+    for (int i = 0; i < dr / 2; ++i) {
+      const double a = (double)p * pow(10000.0, -2.0 * i / (double)dr);
+      const double c = cos(a), sn = sin(a);
+      REAL *e = x + (size_t)h * dh + 2 * i;
+      const double x0 = (double)e[0], x1 = (double)e[1];
+      e[0] = (REAL)(x0 * c - x1 * sn);
+      e[1] = (REAL)(x0 * sn + x1 * c);
+    }
 }
 
 /* GELU, tanh form: 0.5 x (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3))). */
@@ -201,12 +239,13 @@ orc_model *SYM(orc_model_new)(const float *blob, long n_floats) {
   if (hdr[0] != ORC_MAGIC || hdr[1] != 1) return NULL;
   int L = hdr[2], d = hdr[3], H = hdr[4], f = hdr[5], V = hdr[6], T = hdr[7], dt = hdr[8];
   if (L < 1 || d < 2 || H < 1 || d % H || d % 2 || f < 1 || V < 1 || T < 1) return NULL;
-  if (hdr[9] & ~ORC_FLAG_TEMPERATURE) return NULL;
+  if (hdr[9] & ~(ORC_FLAG_TEMPERATURE | ORC_FLAG_RMS_ROPE)) return NULL;
   const int temp = (hdr[9] & ORC_FLAG_TEMPERATURE) != 0;
   long np = model_params(L, d, f, V, T) + (temp ? temp_params(d) : 0);
   if (n_floats != ORC_HDR + np) return NULL;
   orc_model *m = (orc_model *)calloc(1, sizeof(orc_model));
   m->L = L; m->d = d; m->H = H; m->f = f; m->V = V; m->T = T; m->dtype = dt; m->temp = temp;
+  m->rope = (hdr[9] & ORC_FLAG_RMS_ROPE) != 0;
   m->store = (REAL *)malloc(sizeof(REAL) * (size_t)np);
   m->layer = (orc_layer *)calloc((size_t)L, sizeof(orc_layer));
   REAL *cur = m->store;
@@ -341,13 +380,13 @@ int SYM(orc_step)(orc_seq *s, int nr, const int32_t *toks, int k, const double *
     const REAL *pe = m->pos + (size_t)(C + r) * d;
     if (r < nr) {
       const REAL *te = m->tok + (size_t)toks[r] * d;
-      for (int i = 0; i < d; ++i) x[i] = te[i] + pe[i];
+      for (int i = 0; i < d; ++i) x[i] = te[i] + (m->rope ? (REAL)0 : pe[i]);
     } else {
       sinusoid(u[r - nr], d, A);
       linear(A, m->nw1, m->nb1, d, 4 * d, Y);
       for (int i = 0; i < 4 * d; ++i) Y[i] = gelu(Y[i]);
       linear(Y, m->nw2, m->nb2, 4 * d, d, Z);
-      for (int i = 0; i < d; ++i) x[i] = Z[i] + pe[i];
+      for (int i = 0; i < d; ++i) x[i] = Z[i] + (m->rope ? (REAL)0 : pe[i]);
       if (s->temb)
         for (int i = 0; i < d; ++i) x[i] += s->temb[i];
     }
@@ -360,8 +399,12 @@ int SYM(orc_step)(orc_seq *s, int nr, const int32_t *toks, int k, const double *
     const REAL *kc = s->K + (size_t)l * m->T * d, *vc = s->Vc + (size_t)l * m->T * d;
     /* q, k, v of every new row */
     for (int r = 0; r < n; ++r) {
-      layernorm(X + (size_t)r * d, y->ln1_g, y->ln1_b, d, A);
+      norm(m, X + (size_t)r * d, y->ln1_g, y->ln1_b, A);
       linear(A, y->wqkv, y->bqkv, d, 3 * d, QKV);
+      if (m->rope) { /* row r sits at position C + r */
+        rope(QKV, H, dh, C + r);
+        rope(QKV + d, H, dh, C + r);
+      }
       memcpy(Q + (size_t)r * d, QKV, sizeof(REAL) * d);
       memcpy(kn + (size_t)r * d, QKV + d, sizeof(REAL) * d);
       memcpy(vn + (size_t)r * d, QKV + 2 * d, sizeof(REAL) * d);
@@ -384,7 +427,7 @@ int SYM(orc_step)(orc_seq *s, int nr, const int32_t *toks, int k, const double *
       REAL *x = X + (size_t)r * d;
       linear(O + (size_t)r * d, y->wo, y->bo, d, d, Z);
       for (int i = 0; i < d; ++i) x[i] += Z[i];
-      layernorm(x, y->ln2_g, y->ln2_b, d, A);
+      norm(m, x, y->ln2_g, y->ln2_b, A);
       linear(A, y->w1, y->b1, d, f, Y);
       for (int i = 0; i < f; ++i) Y[i] = gelu(Y[i]);
       linear(Y, y->w2, y->b2, f, d, Z);
@@ -400,7 +443,7 @@ int SYM(orc_step)(orc_seq *s, int nr, const int32_t *toks, int k, const double *
   int r0 = k > 0 ? nr : nr - 1;
   if (logits) {
     for (int j = 0; j < nh; ++j) {
-      layernorm(X + (size_t)(r0 + j) * d, m->lnf_g, m->lnf_b, d, A);
+      norm(m, X + (size_t)(r0 + j) * d, m->lnf_g, m->lnf_b, A);
       for (int v = 0; v < V; ++v) {
         const REAL *w = m->tok + (size_t)v * d;
         REAL sc = 0;
@@ -486,6 +529,22 @@ double SYM(orc_softmax)(const double *logits, int V, double *q) {
 /* ---------------------------------------------- component entry points */
 
 double SYM(orc_gelu)(double x) { return (double)gelu((REAL)x); }
+
+void SYM(orc_rmsnorm)(const double *x, const double *g, int d, double *y) {
+  REAL *xr = (REAL *)malloc(sizeof(REAL) * 3 * (size_t)d);
+  for (int i = 0; i < d; ++i) { xr[i] = (REAL)x[i]; xr[d + i] = (REAL)g[i]; }
+  rmsnorm(xr, xr + d, d, xr + 2 * d);
+  for (int i = 0; i < d; ++i) y[i] = (double)xr[2 * d + i];
+  free(xr);
+}
+
+void SYM(orc_rope)(double *x, int H, int dh, int p) {
+  REAL *xr = (REAL *)malloc(sizeof(REAL) * (size_t)H * dh);
+  for (int i = 0; i < H * dh; ++i) xr[i] = (REAL)x[i];
+  rope(xr, H, dh, p);
+  for (int i = 0; i < H * dh; ++i) x[i] = (double)xr[i];
+  free(xr);
+}
 
 void SYM(orc_layernorm)(const double *x, const double *g, const double *b, int d, double *y) {
   REAL *xr = (REAL *)calloc(3 * (size_t)d, sizeof(REAL)), *yr = (REAL *)calloc((size_t)d, sizeof(REAL));

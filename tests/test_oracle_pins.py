@@ -792,3 +792,69 @@ def test_selfforcing_teacher_forcing_changes_only_round_two(small):
     for t in range(N):
         same = np.allclose(g2[0, t * k:(t + 1) * k], l2[0, t * k:(t + 1) * k], rtol=0, atol=1e-12)
         assert same == (t != 2), t
+
+
+# ------------------------- the paper's backbone: RMSNorm + rotary positions
+
+def test_rmsnorm_closed_form():
+    """RMSNorm of (3, 4) with gain (1, 2): mean square 12.5."""
+    r = 1.0 / math.sqrt(12.5 + 1e-5)
+    np.testing.assert_allclose(O.rmsnorm([3.0, 4.0], [1.0, 2.0]), [3 * r, 8 * r], rtol=1e-15)
+    # scale invariance: RMSNorm(c x) = RMSNorm(x) up to the epsilon
+    x = np.random.default_rng(0).normal(size=32)
+    np.testing.assert_allclose(O.rmsnorm(1e3 * x, np.ones(32)), O.rmsnorm(x, np.ones(32)),
+                               rtol=1e-5)
+
+
+def test_rope_closed_form_and_relative_positions():
+    """RoFormer's rotary map: pair 0 turns by p radians, pair i by
+    p * 10000^(-2i/64); position 0 is the identity; norms are kept; and the
+    score of a query at m and a key at n depends on n - m only."""
+    H, dh = 2, 64
+    e0 = np.zeros(H * dh)
+    e0[0] = 1.0
+    for p in (0, 1, 7, 100):
+        y = O.rope(e0, H, dh, p)
+        assert abs(y[0] - math.cos(p)) < 1e-14 and abs(y[1] - math.sin(p)) < 1e-14
+    e = np.zeros(H * dh)
+    e[dh + 10] = 1.0  # head 1, pair 5
+    y = O.rope(e, H, dh, 3)
+    a = 3 * 10000.0 ** (-10.0 / 64)
+    assert abs(y[dh + 10] - math.cos(a)) < 1e-14 and abs(y[dh + 11] - math.sin(a)) < 1e-14
+    rng = np.random.default_rng(1)
+    q, k = rng.normal(size=H * dh), rng.normal(size=H * dh)
+    np.testing.assert_allclose(O.rope(q, H, dh, 0), q, rtol=0, atol=0)
+    np.testing.assert_allclose(np.linalg.norm(O.rope(q, H, dh, 37)), np.linalg.norm(q), rtol=1e-14)
+    for m, n, sft in ((3, 9, 5), (20, 2, 11)):
+        for h in range(H):
+            sl = slice(h * dh, (h + 1) * dh)
+            a = O.rope(q, H, dh, m)[sl] @ O.rope(k, H, dh, n)[sl]
+            b = O.rope(q, H, dh, m + sft)[sl] @ O.rope(k, H, dh, n + sft)[sl]
+            assert abs(a - b) < 1e-12 * (1 + abs(a))
+    # d_rot = 64 < d_head = 128: dimensions 64.. are left alone
+    x = rng.normal(size=128)
+    np.testing.assert_allclose(O.rope(x, 1, 128, 9)[64:], x[64:], rtol=0, atol=0)
+
+
+def test_rms_rope_backbone_brute_force():
+    """(e) for the paper's backbone: the C oracle's cached steps (prefill and
+    decode with noise rows, RMSNorm, rotary q/k at each row's position) equal
+    the independent numpy dense SingleForward / DoubleForward passes."""
+    cfg = S.ModelConfig(2, 64, 4, 128, 96, 64, S.DTYPE_FP32, rms_rope=True)
+    blob = _blob(cfg, seed=12)
+    m = O.Model(blob)
+    N, k = 5, 2
+    rng = np.random.default_rng(15)
+    c, W, x, outs = _check_single_forward(blob, m, N, k, rng)
+    assert c["rms_rope"]
+    z2 = rng.random((N, k))
+    MD, pos = O.double_forward_layout(N, k)
+    rows = [("tok", t) for t in x]
+    rows += [("tok", outs[t][1][j]) for t in range(1, N + 1) for j in range(k)]
+    rows += [("noise", float(z2[t - 1, j])) for t in range(1, N + 1) for j in range(k)]
+    dense = O.dense_forward(c, W, rows, pos, MD)
+    for t in range(1, N + 1):
+        s, _ = outs[t]
+        lg, _ = O.decode(s, outs[t][1], z2[t - 1])
+        ref = dense[N + N * k + (t - 1) * k:N + N * k + t * k]
+        assert np.max(np.abs(lg - ref)) <= 1e-10 * np.abs(ref).max()
