@@ -57,8 +57,14 @@ extern "C" {
                                    rows for 2 * max_batch * max_prompt * max_k rows and
                                    n_layer x 2 x max_batch x n_head x max_prompt (1 + 2 max_k)
                                    x d_head elements of keys and values */
+#define KF_FLAG_RMS_ROPE 16u    /* the paper's backbone (Appendix D model table): RMSNorm
+                                   pre-norm and rotary positions (RoFormer pairs (2i, 2i+1)
+                                   over d_rot = min(64, d_head), angle p 10000^(-2i/d_rot)),
+                                   no learned positions; the blob has header word 9 bit 1
+                                   set and still carries the position table and the norm
+                                   shifts, which are ignored */
 #define KF_FLAG_TEMPERATURE 2u  /* the model has a temperature-conditioned noise encoder
-                                   (its weight blob carries the encoder, header word 9 = 1);
+                                   (its weight blob carries the encoder, header word 9 bit 0);
                                    see kf_set_temperature */
 
 typedef struct kf_config {

@@ -22,6 +22,7 @@ KF_FLAG_DEBUG_LOGITS = 1
 KF_FLAG_TEMPERATURE = 2
 KF_FLAG_TEACHER = 4
 KF_FLAG_ROLLOUT = 8
+KF_FLAG_RMS_ROPE = 16
 KF_MASK_SINGLE, KF_MASK_DOUBLE = 0, 1
 KF_KC_NAMES = ["embed", "noise", "norm", "qkv", "attn", "oproj", "mlp_up", "mlp_down", "head",
                "select"]

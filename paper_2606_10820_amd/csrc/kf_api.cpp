@@ -22,6 +22,7 @@ namespace {
 constexpr int32_t kMagic = 0x4B465731;
 constexpr int kHeaderInts = 16;
 constexpr int32_t kBlobTemperature = 1;  // header word 9: temperature encoder present
+constexpr int32_t kBlobRmsRope = 2;      // header word 9: RMSNorm + rotary positions
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
@@ -52,6 +53,7 @@ struct Plan {
   size_t tok = 0, pos = 0, nw1 = 0, nb1 = 0, nw2 = 0, nb2 = 0, omega = 0, lnf_g = 0, lnf_b = 0;
   size_t head_c1 = 0, head_c2 = 0, head_w = 0;  // folded final norm; gain-scaled token table
   size_t tw1 = 0, tb1 = 0, tw2 = 0, tb2 = 0;     // temperature encoder (KF_FLAG_TEMPERATURE)
+  size_t rope = 0;                              // rotary table [n_ctx][d_rot/2] (KF_FLAG_RMS_ROPE)
   size_t temb = 0;                              // per-sequence temperature embedding [max_batch][d]
   std::vector<LayerOff> layer;
   size_t kv = 0, kv_bytes = 0;
@@ -83,7 +85,8 @@ bool config_ok(const kf_config& c, std::string* why) {
   if (c.max_batch < 1 || c.max_batch > 65535) return bad("max_batch must be in [1, 65535]");
   if (c.max_k < 1 || c.max_k > c.n_ctx) return bad("max_k must be in [1, n_ctx]");
   if (c.max_prompt < 1 || c.max_prompt > c.n_ctx) return bad("max_prompt must be in [1, n_ctx]");
-  if (c.flags & ~(KF_FLAG_DEBUG_LOGITS | KF_FLAG_TEMPERATURE | KF_FLAG_TEACHER | KF_FLAG_ROLLOUT))
+  if (c.flags & ~(KF_FLAG_DEBUG_LOGITS | KF_FLAG_TEMPERATURE | KF_FLAG_TEACHER | KF_FLAG_ROLLOUT |
+                  KF_FLAG_RMS_ROPE))
     return bad("unknown flag bits");
   // GEMM operands are addressed through buffer descriptors with 32-bit byte
   // ranges: the largest activation matrix of a step must stay below 2 GiB.
@@ -158,6 +161,7 @@ void make_plan(const kf_config& c, Plan& p) {
   p.head_c1 = take((size_t)p.Vpad * 4);
   p.head_c2 = take((size_t)p.Vpad * 4);
   p.head_w = take((size_t)p.Vpad * d * es);
+  if (c.flags & KF_FLAG_RMS_ROPE) p.rope = take(T * 32 * sizeof(float2));
   if (c.flags & KF_FLAG_TEMPERATURE) {
     p.tw1 = take(d * d * es);
     p.tb1 = take(d * 4);
@@ -352,6 +356,8 @@ int run_step(kf_ctx* c, const StepIn& in) {
   KfKvGeom kg{cf.n_layer, cf.n_head, cf.n_ctx, d / cf.n_head};
   const int M = in.B * g.R;
   const bool debug = (cf.flags & KF_FLAG_DEBUG_LOGITS) != 0;
+  const int rms = (cf.flags & KF_FLAG_RMS_ROPE) ? 1 : 0;
+  const float2* rope = rms ? reinterpret_cast<const float2*>(base + p.rope) : nullptr;
 
   if (in.reset) KF_HIP(c, kf::launch_zero_i32(reinterpret_cast<int*>(st), 1, s));
   if (in.nr > 0)
@@ -372,10 +378,10 @@ int run_step(kf_ctx* c, const StepIn& in) {
   }
   for (int l = 0; l < cf.n_layer; ++l) {
     const LayerOff& y = p.layer[l];
-    const kf::LnFold ln1{F(y.qkv_c1), F(y.qkv_c2), lnst};
-    const kf::LnFold ln2{F(y.up_c1), F(y.up_c2), lnst};
+    const kf::LnFold ln1{F(y.qkv_c1), F(y.qkv_c2), lnst, rms};
+    const kf::LnFold ln2{F(y.up_c1), F(y.up_c2), lnst, rms};
     KF_LAUNCH(c, KF_KC_QKV,
-              kf::gemm_qkv_ln<T>(Xh, ln1, W(y.wqkv), M, d, F(y.bqkv), Q, kv, g, kg, l, st, s));
+              kf::gemm_qkv_ln<T>(Xh, ln1, W(y.wqkv), M, d, F(y.bqkv), Q, kv, g, kg, l, st, rope, s));
     KF_LAUNCH(c, KF_KC_ATTN, kf::launch_attention<T>(Q, kv, O, st, g, kg, l, asp, s));
     KF_LAUNCH(c, KF_KC_OPROJ, kf::gemm_residual<T>(O, W(y.wo), M, d, d, F(y.bo), X, Xh, lnst, &sws, s));
     KF_LAUNCH(c, KF_KC_MLP_UP, kf::gemm_up_ln<T>(Xh, ln2, W(y.w1), M, f, d, F(y.b1), Hm, s));
@@ -384,7 +390,7 @@ int run_step(kf_ctx* c, const StepIn& in) {
   if (in.targets) {
     // Teacher targets: the sampling head over every row, in chunks of the
     // head-partials workspace, each followed by its inverse-CDF selection.
-    const kf::LnFold lnf{F(p.head_c1), F(p.head_c2), lnst};
+    const kf::LnFold lnf{F(p.head_c1), F(p.head_c2), lnst, rms};
     float* tmax = reinterpret_cast<float*>(base + p.tmax);
     float* tsub = reinterpret_cast<float*>(base + p.tsub);
     float* lg = debug ? reinterpret_cast<float*>(base + p.logits) : nullptr;
@@ -396,7 +402,7 @@ int run_step(kf_ctx* c, const StepIn& in) {
                                         tmax, tsub, lg, s));
       KF_LAUNCH(c, KF_KC_SELECT,
                 kf::launch_teacher_select<T>(tmax, tsub, p.n_tiles, V, Xh, lnst, W(p.head_w),
-                                             F(p.head_c1), F(p.head_c2), d, in.tau, in.u_rows,
+                                             F(p.head_c1), F(p.head_c2), rms, d, in.tau, in.u_rows,
                                              r0, mc, in.nr, in.targets, st, s));
     }
     c->last_head_rows = mc;
@@ -406,7 +412,7 @@ int run_step(kf_ctx* c, const StepIn& in) {
   const bool ar = in.k == 0;
   const int Mh = ar ? in.B : in.B * in.k;
   float* logits = (ar || debug) ? reinterpret_cast<float*>(base + p.logits) : nullptr;
-  const kf::LnFold lnf{F(p.head_c1), F(p.head_c2), lnst};
+  const kf::LnFold lnf{F(p.head_c1), F(p.head_c2), lnst, rms};
   KF_LAUNCH(c, KF_KC_HEAD,
             kf::gemm_head_ln<T>(Xh, lnf, W(p.head_w), Mh, p.Vpad, V, d, ar ? 2 : 1, g,
                                 reinterpret_cast<float*>(base + p.pval),
@@ -459,6 +465,8 @@ int run_rollout(kf_ctx* c, int B, int N, int k, const int32_t* tokens, const flo
   T* kvb = reinterpret_cast<T*>(base + p.roll_kv);
   const bool debug = (cf.flags & KF_FLAG_DEBUG_LOGITS) != 0;
   float* logits = debug ? reinterpret_cast<float*>(base + p.logits) : nullptr;
+  const int rms = (cf.flags & KF_FLAG_RMS_ROPE) ? 1 : 0;
+  const float2* rope = rms ? reinterpret_cast<const float2*>(base + p.rope) : nullptr;
 
   auto noise = [&](const float* z, int n, int off, int shift) -> int {
     const KfStepGeom gz{B * N, k, 0, k};  // one noise group of k per (sequence, position)
@@ -475,14 +483,16 @@ int run_rollout(kf_ctx* c, int B, int N, int k, const int32_t* tokens, const flo
   };
   auto body = [&](int n, int koff, int mask) -> int {
     const int M = B * n;
+    const int round = mask == KF_MASK_SINGLE ? 1 : 2;
     for (int l = 0; l < cf.n_layer; ++l) {
       const LayerOff& y = p.layer[l];
-      const kf::LnFold ln1{F(y.qkv_c1), F(y.qkv_c2), lnst};
-      const kf::LnFold ln2{F(y.up_c1), F(y.up_c2), lnst};
+      const kf::LnFold ln1{F(y.qkv_c1), F(y.qkv_c2), lnst, rms};
+      const kf::LnFold ln2{F(y.up_c1), F(y.up_c2), lnst, rms};
       T* Kl = kvb + (size_t)l * 2 * kvl;
       T* Vl = Kl + kvl;
       KF_LAUNCH(c, KF_KC_QKV,
-                kf::gemm_qkv_seq<T>(Xh, ln1, W(y.wqkv), M, d, F(y.bqkv), Q, Kl, Vl, n, ldk, koff, H, s));
+                kf::gemm_qkv_seq<T>(Xh, ln1, W(y.wqkv), M, d, F(y.bqkv), Q, Kl, Vl, n, ldk, koff, H,
+                                    N, k, round, rope, s));
       KF_LAUNCH(c, KF_KC_ATTN,
                 kf::launch_training_attention_seq(mask, B, H, N, k, dh, reinterpret_cast<const bf16*>(Q),
                                                   reinterpret_cast<const bf16*>(Kl),
@@ -497,7 +507,7 @@ int run_rollout(kf_ctx* c, int B, int N, int k, const int32_t* tokens, const flo
   };
   auto head = [&](int n, int off, int32_t* out) -> int {
     const KfStepGeom gh{B, n, off, nk};  // head rows: the nk rows after `off` of each sequence
-    const kf::LnFold lnf{F(p.head_c1), F(p.head_c2), lnst};
+    const kf::LnFold lnf{F(p.head_c1), F(p.head_c2), lnst, rms};
     KF_LAUNCH(c, KF_KC_HEAD,
               kf::gemm_head_ln<T>(Xh, lnf, W(p.head_w), B * nk, p.Vpad, V, d, 1, gh,
                                   reinterpret_cast<float*>(base + p.pval),
@@ -733,6 +743,7 @@ int kf_load_weights(kf_ctx* c, const void* blob, size_t bytes, int blob_is_devic
   drop_graph(c);
   const size_t d = cf.d_model, f = cf.d_mlp, V = cf.vocab, T = cf.n_ctx, L = cf.n_layer;
   const bool temp = (cf.flags & KF_FLAG_TEMPERATURE) != 0;
+  const bool rmsr = (cf.flags & KF_FLAG_RMS_ROPE) != 0;
   const size_t n_params = V * d + T * d + 8 * d * d + 4 * d + d +
                           L * (2 * d + 3 * d * d + 3 * d + d * d + d + 2 * d + f * d + f + d * f + d) +
                           2 * d + (temp ? 2 * d * d + 2 * d : 0);
@@ -745,15 +756,18 @@ int kf_load_weights(kf_ctx* c, const void* blob, size_t bytes, int blob_is_devic
   else
     memcpy(hdr, blob, sizeof hdr);
   const int32_t want[10] = {kMagic, 1, cf.n_layer, cf.d_model, cf.n_head, cf.d_mlp, cf.vocab,
-                            cf.n_ctx, cf.dtype, temp ? kBlobTemperature : 0};
+                            cf.n_ctx, cf.dtype,
+                            (temp ? kBlobTemperature : 0) | (rmsr ? kBlobRmsRope : 0)};
   for (int i = 0; i < 10; ++i)
     if (hdr[i] != want[i]) return fail(c, KF_EINVAL, "blob header word %d is %d, expected %d", i, hdr[i], want[i]);
 
-  // Destination of each tensor in blob order: (offset, count, is_matrix).
-  struct Dst { size_t off, n; bool mat; };
+  // Destination of each tensor in blob order: (offset, count, is_matrix,
+  // unused).  The rotary RMSNorm backbone has no learned positions and no
+  // norm shifts: those tensors are skipped and their regions hold zeros.
+  struct Dst { size_t off, n; bool mat, unused; };
   std::vector<Dst> dst;
-  dst.push_back({p.tok, V * d, true});
-  dst.push_back({p.pos, T * d, true});
+  dst.push_back({p.tok, V * d, true, false});
+  dst.push_back({p.pos, T * d, true, rmsr});
   dst.push_back({p.nw1, 4 * d * d, true});
   dst.push_back({p.nb1, 4 * d, false});
   dst.push_back({p.nw2, 4 * d * d, true});
@@ -761,20 +775,20 @@ int kf_load_weights(kf_ctx* c, const void* blob, size_t bytes, int blob_is_devic
   for (size_t l = 0; l < L; ++l) {
     const LayerOff& y = p.layer[l];
     dst.push_back({y.ln1_g, d, false});
-    dst.push_back({y.ln1_b, d, false});
+    dst.push_back({y.ln1_b, d, false, rmsr});
     dst.push_back({y.wqkv, 3 * d * d, true});
     dst.push_back({y.bqkv, 3 * d, false});
     dst.push_back({y.wo, d * d, true});
     dst.push_back({y.bo, d, false});
     dst.push_back({y.ln2_g, d, false});
-    dst.push_back({y.ln2_b, d, false});
+    dst.push_back({y.ln2_b, d, false, rmsr});
     dst.push_back({y.w1, f * d, true});
     dst.push_back({y.b1, f, false});
     dst.push_back({y.w2, d * f, true});
     dst.push_back({y.b2, d, false});
   }
   dst.push_back({p.lnf_g, d, false});
-  dst.push_back({p.lnf_b, d, false});
+  dst.push_back({p.lnf_b, d, false, rmsr});
   if (temp) {
     dst.push_back({p.tw1, d * d, true});
     dst.push_back({p.tb1, d, false});
@@ -785,6 +799,17 @@ int kf_load_weights(kf_ctx* c, const void* blob, size_t bytes, int blob_is_devic
   // sinusoid frequencies omega_i = 10000^(-i/(d/2)) for the noise encoder
   std::vector<double> omega(d / 2);
   for (size_t i = 0; i < d / 2; ++i) omega[i] = pow(10000.0, -(double)i / (double)(d / 2));
+  // rotary table: position p, pair i < d_rot/2 -> (cos, sin) of p 10000^(-2i/d_rot)
+  std::vector<float2> rope_cs;
+  if (rmsr) {
+    const int dh = cf.d_model / cf.n_head, dr = dh < 64 ? dh : 64;
+    rope_cs.assign(T * 32, make_float2(0.f, 0.f));
+    for (size_t q = 0; q < T; ++q)
+      for (int i = 0; i < dr / 2; ++i) {
+        const double a = (double)q * pow(10000.0, -2.0 * i / (double)dr);
+        rope_cs[q * (dr / 2) + i] = make_float2((float)cos(a), (float)sin(a));
+      }
+  }
 
   const bool bf = cf.dtype == KF_BF16;
   if (!blob_is_device) {
@@ -792,7 +817,8 @@ int kf_load_weights(kf_ctx* c, const void* blob, size_t bytes, int blob_is_devic
     const float* src = static_cast<const float*>(blob) + kHeaderInts;
     for (const Dst& t : dst) {
       uint8_t* o = img.data() + (t.off - p.wbegin);
-      if (t.mat && bf) {
+      if (t.unused) {  // stays zero
+      } else if (t.mat && bf) {
         uint16_t* h = reinterpret_cast<uint16_t*>(o);
         for (size_t i = 0; i < t.n; ++i) h[i] = f32_to_bf16_rne(src[i]);
       } else {
@@ -801,6 +827,7 @@ int kf_load_weights(kf_ctx* c, const void* blob, size_t bytes, int blob_is_devic
       src += t.n;
     }
     memcpy(img.data() + (p.omega - p.wbegin), omega.data(), omega.size() * 8);
+    if (rmsr) memcpy(img.data() + (p.rope - p.wbegin), rope_cs.data(), rope_cs.size() * sizeof(float2));
     KF_HIP(c, hipMemcpyAsync(c->base + p.wbegin, img.data(), img.size(), hipMemcpyHostToDevice, c->stream));
     KF_HIP(c, hipStreamSynchronize(c->stream));
   } else {
@@ -813,13 +840,22 @@ int kf_load_weights(kf_ctx* c, const void* blob, size_t bytes, int blob_is_devic
       KF_HIP(c, kf::launch_zero<float>(reinterpret_cast<float*>(c->base + p.tok) + V * d, pad, c->stream));
     }
     for (const Dst& t : dst) {
-      if (t.mat && bf)
+      if (t.unused && t.mat && bf)
+        KF_HIP(c, kf::launch_zero<bf16>(reinterpret_cast<bf16*>(c->base + t.off), t.n, c->stream));
+      else if (t.unused && t.mat)
+        KF_HIP(c, kf::launch_zero<float>(reinterpret_cast<float*>(c->base + t.off), t.n, c->stream));
+      else if (t.unused)
+        KF_HIP(c, kf::launch_zero<float>(reinterpret_cast<float*>(c->base + t.off), t.n, c->stream));
+      else if (t.mat && bf)
         KF_HIP(c, kf::launch_convert<bf16>(src, reinterpret_cast<bf16*>(c->base + t.off), t.n, c->stream));
       else
         KF_HIP(c, kf::launch_copy_f32(src, reinterpret_cast<float*>(c->base + t.off), t.n, c->stream));
       src += t.n;
     }
     KF_HIP(c, hipMemcpyAsync(c->base + p.omega, omega.data(), omega.size() * 8, hipMemcpyHostToDevice, c->stream));
+    if (rmsr)
+      KF_HIP(c, hipMemcpyAsync(c->base + p.rope, rope_cs.data(), rope_cs.size() * sizeof(float2),
+                               hipMemcpyHostToDevice, c->stream));
     KF_HIP(c, hipStreamSynchronize(c->stream));
   }
   {

@@ -151,6 +151,22 @@ struct EpResidual {
 // the KV cache slot C + i of sequence b (the KV append of the step).  Keys are
 // stored [slot][d_head] and values transposed, [d_head][slot], per head.  An
 // 8-column chunk never straddles q/k/v or two heads (d_head >= 32).
+// Rotary positions (RoFormer) on 8 consecutive columns e..e+7 of one head
+// (e even): pairs (e + 2r, e + 2r + 1) with pair index i = e/2 + r < d_rot/2
+// turn by the table angle of position p (cs [n_ctx][d_rot/2] = cos, sin).
+__device__ inline void rotate8(float (&v)[8], const float2* cs, int dr, int p, int e) {
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int i = e / 2 + r;
+    if (2 * i < dr) {
+      const float2 t = cs[(size_t)p * (dr / 2) + i];
+      const float x0 = v[2 * r], x1 = v[2 * r + 1];
+      v[2 * r] = x0 * t.x - x1 * t.y;
+      v[2 * r + 1] = x0 * t.y + x1 * t.x;
+    }
+  }
+}
+
 template <typename T>
 struct EpQKV {
   T* Q;
@@ -160,10 +176,15 @@ struct EpQKV {
   KfStepGeom g;
   KfKvGeom kg;
   int layer;
+  const float2* rope;  // rotary table, or null
   static constexpr bool kStats = false;
   __device__ inline void store8(int m, int n, float (&v)[8]) const {
     const int d = kg.H * kg.dh;
     const int which = n / d, c = n - which * d;
+    if (rope && which < 2) {
+      const int i = m - (m / g.R) * g.R;
+      rotate8(v, rope, kg.dh < 64 ? kg.dh : 64, st->C + i, c % kg.dh);
+    }
     if (which == 0) {
       put8(Q + (size_t)m * d + c, v);
       return;
@@ -228,11 +249,28 @@ struct EpQKVSeq {
   T* V;
   const float* bias;
   int n, ldk, koff, H, dh;
+  int N, k, round;     // the round's row layout (positions of its rows)
+  const float2* rope;  // rotary table, or null
   static constexpr bool kStats = false;
+  __device__ inline int position(int i) const {
+    const int nk = N * k;
+    int q, base;
+    if (round == 1) {
+      if (i < N) return i;
+      q = i - N;
+      base = 1;
+    } else {
+      q = i < nk ? i : i - nk;
+      base = i < nk ? 1 : 1 + k;
+    }
+    const int t = q / k;
+    return t + base + (q - t * k);
+  }
   __device__ inline void store8(int m, int c, float (&v)[8]) const {
     const int d = H * dh, which = c / d, cc = c - which * d, h = cc / dh, e = cc - h * dh;
     const int b = m / n, i = m - b * n;
     const size_t bh = (size_t)b * H + h;
+    if (rope && which < 2) rotate8(v, rope, dh < 64 ? dh : 64, position(i), e);
     if (which == 0) put8(Q + (bh * n + i) * dh + e, v);
     else put8((which == 1 ? K : V) + (bh * ldk + koff + i) * dh + e, v);
   }
@@ -383,6 +421,7 @@ struct GemmA {
   const float* c2;
   const float2* lnst;
   KfStepGeom g;
+  int rms;  // RMSNorm statistics (mu = 0)
 };
 
 // ---------------------------------------------------------------- kernel
@@ -553,8 +592,8 @@ __global__ void __launch_bounds__(256)
       b += __shfl_xor(b, off, 64);
     }
     if (tid % TPR == 0) {
-      const float mu = a / (float)K;
-      const float var = fmaxf(b / (float)K - mu * mu, 0.f);
+      const float mu = ga.rms ? 0.f : a / (float)K;
+      const float var = ga.rms ? b / (float)K : fmaxf(b / (float)K - mu * mu, 0.f);
       sStat[tid / TPR] = make_float2(mu, 1.0f / sqrtf(var + 1e-5f));
     }
   }
@@ -940,16 +979,16 @@ hipError_t gemm_noise_out(const T* A, const T* W, int M, int d, int K, const flo
 template <typename T>
 hipError_t gemm_qkv_ln(const T* Xh, const LnFold& ln, const T* W, int M, int d, const float* bias,
                        T* Q, T* kv, KfStepGeom g, KfKvGeom kg, int layer, const KfDevState* st,
-                       hipStream_t s) {
-  EpQKV<T> ep{Q, kv, bias, st, g, kg, layer};
-  return dispatch<T, 0, true>(GemmA{Xh, d, M, ln.c1, ln.c2, ln.lnst, g}, W, M, 3 * d, d, ep, s);
+                       const float2* rope, hipStream_t s) {
+  EpQKV<T> ep{Q, kv, bias, st, g, kg, layer, rope};
+  return dispatch<T, 0, true>(GemmA{Xh, d, M, ln.c1, ln.c2, ln.lnst, g, ln.rms}, W, M, 3 * d, d, ep, s);
 }
 
 template <typename T>
 hipError_t gemm_up_ln(const T* Xh, const LnFold& ln, const T* W, int M, int N, int d,
                       const float* bias, T* out, hipStream_t s) {
   EpBias<T> ep{out, N, bias, 1};
-  return dispatch<T, 0, true>(GemmA{Xh, d, M, ln.c1, ln.c2, ln.lnst, KfStepGeom{}}, W, M, N, d, ep,
+  return dispatch<T, 0, true>(GemmA{Xh, d, M, ln.c1, ln.c2, ln.lnst, KfStepGeom{}, ln.rms}, W, M, N, d, ep,
                               s);
 }
 
@@ -959,7 +998,7 @@ hipError_t gemm_head_ln(const T* Xh, const LnFold& ln, const T* W, int M, int Vp
                         hipStream_t s) {
   if (M <= 0) return hipSuccess;
   EpHead ep{nullptr, pval, pidx, logits, V, Vpad / kHeadTileN};
-  const GemmA ga{Xh, d, g.B * g.R, ln.c1, ln.c2, ln.lnst, g};
+  const GemmA ga{Xh, d, g.B * g.R, ln.c1, ln.c2, ln.lnst, g, ln.rms};
   auto go = [&](auto mode) {
     constexpr int MODE = decltype(mode)::value;
     if (M <= 32)
@@ -974,9 +1013,10 @@ hipError_t gemm_head_ln(const T* Xh, const LnFold& ln, const T* W, int M, int Vp
 
 template <typename T>
 hipError_t gemm_qkv_seq(const T* Xh, const LnFold& ln, const T* W, int M, int d, const float* bias,
-                        T* Q, T* K, T* V, int n, int ldk, int koff, int H, hipStream_t s) {
-  EpQKVSeq<T> ep{Q, K, V, bias, n, ldk, koff, H, d / H};
-  return dispatch<T, 0, true>(GemmA{Xh, d, M, ln.c1, ln.c2, ln.lnst, KfStepGeom{}}, W, M, 3 * d, d,
+                        T* Q, T* K, T* V, int n, int ldk, int koff, int H, int N, int k, int round,
+                        const float2* rope, hipStream_t s) {
+  EpQKVSeq<T> ep{Q, K, V, bias, n, ldk, koff, H, d / H, N, k, round, rope};
+  return dispatch<T, 0, true>(GemmA{Xh, d, M, ln.c1, ln.c2, ln.lnst, KfStepGeom{}, ln.rms}, W, M, 3 * d, d,
                               ep, s);
 }
 
@@ -996,7 +1036,7 @@ hipError_t gemm_head_sample(const T* Xh, const LnFold& ln, const T* W, int M, in
   if (M <= 0) return hipSuccess;
   EpHeadSample ep{nullptr, pmax, psub, logits, tau, row0, rows_per_seq, V, Vpad / kHeadTileN};
   const GemmA ga{Xh + (size_t)row0 * d, d, M, ln.c1, ln.c2, ln.lnst + (size_t)row0 * (d / 16),
-                 KfStepGeom{}};
+                 KfStepGeom{}, ln.rms};
   if (M <= 32)
     return launch_tile<T, 32, kHeadTileN, 1, 4, 3, 0, true>(ga, W, d, M, Vpad, d, ep, s);
   if (M <= 512)
@@ -1023,13 +1063,14 @@ hipError_t launch_ln_fold(const T* W, T* Wout, const float* g, const float* beta
                                         const KfDevState*, const SplitWs*, hipStream_t);           \
   template hipError_t gemm_qkv_ln<T>(const T*, const LnFold&, const T*, int, int, const float*,   \
                                      T*, T*, KfStepGeom, KfKvGeom, int, const KfDevState*,         \
-                                     hipStream_t);                                                 \
+                                     const float2*, hipStream_t);                                  \
   template hipError_t gemm_up_ln<T>(const T*, const LnFold&, const T*, int, int, int,             \
                                     const float*, T*, hipStream_t);                                \
   template hipError_t gemm_head_ln<T>(const T*, const LnFold&, const T*, int, int, int, int, int, \
                                       KfStepGeom, float*, int*, float*, hipStream_t);              \
   template hipError_t gemm_qkv_seq<T>(const T*, const LnFold&, const T*, int, int, const float*,  \
-                                      T*, T*, T*, int, int, int, int, hipStream_t);                \
+                                      T*, T*, T*, int, int, int, int, int, int, int,               \
+                                      const float2*, hipStream_t);                                 \
   template hipError_t gemm_seq_noise_out<T>(const T*, const T*, int, int, int, const float*,      \
                                             const T*, const T*, float*, T*, float2*, int, int, int, \
                                             int, int, const SplitWs*, hipStream_t);                \

@@ -153,11 +153,14 @@ struct LnFold {
   const float* c1;
   const float* c2;
   const float2* lnst;  // partial row sums of the residual stream (see gemm_residual)
+  int rms;             // RMSNorm: no mean (mu = 0, rstd from the mean square)
 };
+// rope (optional): rotary table [n_ctx][d_rot/2] (cos, sin) with d_rot =
+// min(64, d_head); when set, Q and K are rotated at each row's position C + i.
 template <typename T>
 hipError_t gemm_qkv_ln(const T* Xh, const LnFold& ln, const T* W, int M, int d, const float* bias,
                        T* Q, T* kv, KfStepGeom g, KfKvGeom kg, int layer, const KfDevState* st,
-                       hipStream_t s);
+                       const float2* rope, hipStream_t s);
 template <typename T>
 hipError_t gemm_up_ln(const T* Xh, const LnFold& ln, const T* W, int M, int N, int d,
                       const float* bias, T* out, hipStream_t s);
@@ -193,8 +196,8 @@ hipError_t gemm_head_sample(const T* Xh, const LnFold& ln, const T* W, int M, in
 template <typename T>
 hipError_t launch_teacher_select(const float* pmax, const float* psub, int n_tiles, int V,
                                  const T* Xh, const float2* lnst, const T* W, const float* c1,
-                                 const float* c2, int d, const float* tau, const float* u, int row0,
-                                 int M, int rows_per_seq, int32_t* targets, KfDevState* st,
+                                 const float* c2, int rms, int d, const float* tau, const float* u,
+                                 int row0, int M, int rows_per_seq, int32_t* targets, KfDevState* st,
                                  hipStream_t s);
 
 // Whole-sequence forward of the teacher rollout (SingleForward / DoubleForward
@@ -204,9 +207,13 @@ hipError_t launch_teacher_select(const float* pmax, const float* psub, int n_til
 //   gemm_seq_noise_out: second noise-MLP layer; noise row (b, t, j) of N groups
 //     of k to residual row b*n + off + t*k + j, position t + shift + j.
 //   launch_embed_group: token rows (b, t, j) likewise, tokens [B][N*k].
+// With rope set, Q and K rows are rotated at their positions in the round's
+// layout (round 1: context i, then noise (t, j) at t + 1 + j; round 2:
+// Future-1 (t, j) at t + 1 + j, then Future-2 at t + 1 + k + j).
 template <typename T>
 hipError_t gemm_qkv_seq(const T* Xh, const LnFold& ln, const T* W, int M, int d, const float* bias,
-                        T* Q, T* K, T* V, int n, int ldk, int koff, int H, hipStream_t s);
+                        T* Q, T* K, T* V, int n, int ldk, int koff, int H, int N, int k, int round,
+                        const float2* rope, hipStream_t s);
 template <typename T>
 hipError_t gemm_seq_noise_out(const T* A, const T* W, int M, int d, int K, const float* bias,
                               const T* pos, const T* temb, float* X, T* Xh, float2* lnst, int n,

@@ -585,7 +585,7 @@ __global__ void __launch_bounds__(256)
     teacher_select_kernel(const float* __restrict__ pmax, const float* __restrict__ psub, int nT,
                           int V, const T* __restrict__ Xh, const float2* __restrict__ lnst,
                           const T* __restrict__ W, const float* __restrict__ c1,
-                          const float* __restrict__ c2, int d, const float* __restrict__ tau,
+                          const float* __restrict__ c2, int rms, int d, const float* __restrict__ tau,
                           const float* __restrict__ u, int row0, int M, int rows_per_seq,
                           int32_t* __restrict__ targets, KfDevState* st) {
   const int lane = threadIdx.x & 63;
@@ -709,8 +709,9 @@ __global__ void __launch_bounds__(256)
   }
   sa = wave_sum(sa);
   sb = wave_sum(sb);
-  const float mu = sa / (float)d;
-  const float rstd = 1.0f / sqrtf(fmaxf(sb / (float)d - mu * mu, 0.f) + 1e-5f);
+  const float mu = rms ? 0.f : sa / (float)d;
+  const float rstd =
+      1.0f / sqrtf((rms ? sb / (float)d : fmaxf(sb / (float)d - mu * mu, 0.f)) + 1e-5f);
   float p = 0.f;
   if (j < V) {
     const float l = rstd * (dot - mu * c1[j]) + c2[j];
@@ -892,12 +893,12 @@ hipError_t launch_embed_group(float* X, T* Xh, float2* lnst, const T* tok, const
 template <typename T>
 hipError_t launch_teacher_select(const float* pmax, const float* psub, int n_tiles, int V,
                                  const T* Xh, const float2* lnst, const T* W, const float* c1,
-                                 const float* c2, int d, const float* tau, const float* u, int row0,
-                                 int M, int rows_per_seq, int32_t* targets, KfDevState* st,
+                                 const float* c2, int rms, int d, const float* tau, const float* u,
+                                 int row0, int M, int rows_per_seq, int32_t* targets, KfDevState* st,
                                  hipStream_t s) {
   if (M <= 0) return hipSuccess;
   launch(teacher_select_kernel<T>, dim3((M + 3) / 4), dim3(256), 0, s, pmax, psub, n_tiles, V, Xh,
-         lnst, W, c1, c2, d, tau, u, row0, M, rows_per_seq, targets, st);
+         lnst, W, c1, c2, rms, d, tau, u, row0, M, rows_per_seq, targets, st);
   return hipGetLastError();
 }
 
@@ -951,7 +952,7 @@ hipError_t launch_zero_i32(int* dst, size_t n, hipStream_t s) { return launch_ze
                                             KfDevState*, hipStream_t);                              \
   template hipError_t launch_teacher_select<T>(const float*, const float*, int, int, const T*,     \
                                                const float2*, const T*, const float*, const float*, \
-                                               int, const float*, const float*, int, int, int,      \
+                                               int, int, const float*, const float*, int, int, int, \
                                                int32_t*, KfDevState*, hipStream_t);
 KF_INST(float)
 KF_INST(bf16)

@@ -61,7 +61,7 @@ def test_strerror(L):
 @pytest.mark.parametrize("bad", [
     dict(n_layer=0), dict(d_model=100), dict(n_head=3), dict(d_model=256, n_head=1),
     dict(d_mlp=100), dict(vocab=1), dict(n_ctx=100), dict(dtype=7), dict(max_batch=0), dict(max_k=0),
-    dict(max_k=1000), dict(max_prompt=0), dict(flags=16),
+    dict(max_k=1000), dict(max_prompt=0), dict(flags=32),
     dict(max_batch=65535, max_prompt=128, d_mlp=4096),
     # the teacher rollout's DoubleForward rows (2 * max_batch * max_prompt * max_k) count too
     dict(flags=8, max_batch=4096, max_prompt=128),
@@ -81,6 +81,9 @@ def test_state_bytes_covers_kv_cache(L):
     assert n > kv + weights
     big = _cfg(dtype=Bd.KF_BF16, flags=Bd.KF_FLAG_DEBUG_LOGITS)
     assert L.kf_state_bytes(ctypes.byref(big)) > L.kf_state_bytes(ctypes.byref(_cfg(dtype=Bd.KF_BF16)))
+    # the rotary backbone keeps a cos/sin table of n_ctx x 32 float2 beside the weights
+    rr = _cfg(flags=Bd.KF_FLAG_RMS_ROPE)
+    assert L.kf_state_bytes(ctypes.byref(rr)) >= n + 128 * 32 * 8
 
 
 def test_state_machine_without_device(L):

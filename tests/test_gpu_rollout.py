@@ -35,6 +35,8 @@ def _ctx(cfg, blob, B, N, k):
     flags = Bd.KF_FLAG_ROLLOUT | Bd.KF_FLAG_DEBUG_LOGITS
     if cfg.temperature:
         flags |= Bd.KF_FLAG_TEMPERATURE
+    if cfg.rms_rope:
+        flags |= Bd.KF_FLAG_RMS_ROPE
     c = Bd.make_config(cfg.n_layer, cfg.d_model, cfg.n_head, cfg.d_mlp, cfg.vocab, cfg.n_ctx,
                        cfg.dtype, B, k, N, flags)
     kf = Bd.KForcing(c)

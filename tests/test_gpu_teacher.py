@@ -35,6 +35,8 @@ def _ctx(cfg, blob, max_batch, max_prompt, debug=True):
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     flags = Bd.KF_FLAG_TEACHER | (Bd.KF_FLAG_DEBUG_LOGITS if debug else 0)
+    if cfg.rms_rope:
+        flags |= Bd.KF_FLAG_RMS_ROPE
     c = Bd.make_config(cfg.n_layer, cfg.d_model, cfg.n_head, cfg.d_mlp, cfg.vocab, cfg.n_ctx,
                        cfg.dtype, max_batch, 1, max_prompt, flags)
     kf = Bd.KForcing(c)
