@@ -20,6 +20,7 @@ timed on a bounded sample on the host.
 from __future__ import annotations
 
 import argparse
+import ctypes
 import json
 import os
 import sys
@@ -115,6 +116,10 @@ def parse():
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the OpenWebText-shaped batch sweep and k comparison")
     ap.add_argument("--sweep-batches", default="1,16,64,256,512")
+    ap.add_argument("--no-serving", action="store_true",
+                    help="skip the continuous-batching run")
+    ap.add_argument("--serving-only", action="store_true",
+                    help="only the continuous-batching run (one JSON line)")
     ap.add_argument("--no-train-attn", action="store_true",
                     help="skip the training-mask attention measurement")
     ap.add_argument("--train-attn-only", action="store_true",
@@ -539,6 +544,94 @@ def rollout_bench(reps: int = 2):
     return {"entry": "kf_selfforcing_targets", "cases": out}
 
 
+def serving_bench(stream, reps: int = 2):
+    """Continuous batching (kf_serve_*) on the LM1B-shaped model: 128 sequences
+    (prompt 16 Zipf tokens, 112 new tokens each, k = 4) through 64 slots.
+    Sequences arrive in waves of 16 every 7 steps; a finished sequence is
+    released and the next waiting one is admitted into its slot at the
+    following step.  Tokens per second over the whole run, host calls
+    included, beside the lock-step kf_generate of the same sequences."""
+    import torch
+    from paper_2606_10820_amd import binding as Bd
+    w = S.WORKLOADS["lm1b"]
+    cfg = w["cfg"]
+    slots_n, n_seq, N, L, k = 64, 128, w["N"], w["L"] - w["L"] % 4, 4
+    dev = torch.device("cuda:0")
+    blob = S.pack_blob(cfg, S.make_weights(cfg, seed=0))
+    kc = Bd.make_config(cfg.n_layer, cfg.d_model, cfg.n_head, cfg.d_mlp, cfg.vocab, cfg.n_ctx,
+                        cfg.dtype, slots_n, k, N, Bd.KF_FLAG_SERVING)
+    kf = Bd.KForcing(kc, device="cuda:0", stream=stream)
+    kf.load_weights(blob)
+    prompts = torch.as_tensor(S.make_prompts(w["prompts"], 5, n_seq, N, cfg.vocab), device=dev)
+    g = torch.Generator(device=dev)
+    g.manual_seed(11)
+    noise = torch.rand((4096, slots_n, k), device=dev, generator=g)
+    out = torch.empty((slots_n, k), dtype=torch.int32, device=dev)
+    L_ = kf.L
+    passes = L // k
+
+    def run():
+        nxt, done, tick = 0, 0, 0
+        age = {}                      # slot -> passes done
+        free = list(range(slots_n))
+        calls = rows = 0
+        while done < n_seq:
+            # arrivals: waves of 16 every 7 steps; a freed slot takes the next waiting sequence
+            arrived = min(n_seq, 16 * (tick // 7 + 1))
+            take = min(len(free), arrived - nxt)
+            new = []
+            if take > 0:
+                new = [free.pop() for _ in range(take)]
+                arr = np.asarray(new, np.int32)
+                rc = L_.kf_serve_admit(kf.h, take, arr.ctypes.data_as(ctypes.c_void_p), N,
+                                       kf._p(prompts[nxt:nxt + take]), k,
+                                       kf._p(noise[tick % 4096]), kf._p(out))
+                assert rc == 0, kf.L.kf_last_error(kf.h)
+                nxt += take
+                calls += 1
+                rows += take
+                for q in new:
+                    age[q] = 1
+            live = [q for q in age if q not in new]  # the admitted made their first pass
+            if live:
+                arr = np.asarray(live, np.int32)
+                rc = L_.kf_serve_step(kf.h, len(live), arr.ctypes.data_as(ctypes.c_void_p), k,
+                                      kf._p(noise[(tick + 1) % 4096]), kf._p(out))
+                assert rc == 0, kf.L.kf_last_error(kf.h)
+                calls += 1
+                rows += len(live)
+                for q in live:
+                    age[q] += 1
+            fin = [q for q in age if age[q] >= passes]
+            if fin:
+                arr = np.asarray(fin, np.int32)
+                assert L_.kf_serve_release(kf.h, len(fin), arr.ctypes.data_as(ctypes.c_void_p)) == 0
+                for q in fin:
+                    del age[q]
+                    free.append(q)
+                done += len(fin)
+            tick += 1
+        return tick, calls, rows
+
+    run()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        ticks, calls, rows = run()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) / reps * 1e3
+    toks = n_seq * L
+    res = {"workload": (f"lm1b-shaped, {n_seq} sequences (prompt {N}, {L} new tokens, k={k}) "
+                        f"through {slots_n} slots, arrivals of 16 every 7 steps"),
+           "ms": round(ms, 3), "tokens_per_s": round(toks / (ms * 1e-3), 1),
+           "steps": ticks, "calls": calls, "sequence_passes": rows}
+    log(f"[bench] serving: {ms:.2f} ms for {toks} tokens -> {toks / (ms * 1e-3):,.0f} tokens/s "
+        f"({ticks} steps, {calls} calls)")
+    del kf
+    torch.cuda.empty_cache()
+    return res
+
+
 def training_attention_bench(reps: int = 10):
     """Block-sparse attention of the training masks (SingleForward M_S and
     DoubleForward M_D, Appendix C.2) at one GPU's share of the paper's
@@ -603,6 +696,11 @@ def main():
         return
     if a.rollout_only:
         print(json.dumps(rollout_bench(max(a.steps, 1))), flush=True)
+        return
+    if a.serving_only:
+        st = torch.cuda.Stream(device=torch.device("cuda:0"))
+        torch.cuda.set_stream(st)
+        print(json.dumps(serving_bench(st, max(a.steps, 1))), flush=True)
         return
 
     w = S.WORKLOADS[a.workload]
@@ -718,6 +816,10 @@ def main():
 
     if not a.no_sweep:
         res["owt_sweep"] = owt_sweep([int(x) for x in a.sweep_batches.split(",") if x], stream)
+
+    if not a.no_serving:
+        res["serving"] = serving_bench(stream)
+        res["serving"]["lockstep_tokens_per_s"] = round(value, 1)
 
     if not a.no_train_attn:
         res["training_attention"] = training_attention_bench()

@@ -63,6 +63,8 @@ extern "C" {
                                    no learned positions; the blob has header word 9 bit 1
                                    set and still carries the position table and the norm
                                    shifts, which are ignored */
+#define KF_FLAG_SERVING 32u     /* continuous batching over a paged KV cache: the
+                                   kf_serve_* calls, a page table and per-slot state */
 #define KF_FLAG_TEMPERATURE 2u  /* the model has a temperature-conditioned noise encoder
                                    (its weight blob carries the encoder, header word 9 bit 0);
                                    see kf_set_temperature */
@@ -79,6 +81,8 @@ typedef struct kf_config {
   int max_k;      /* largest window k any call may use (k <= max_k) */
   int max_prompt; /* longest prompt N given to a prefill call */
   unsigned flags; /* KF_FLAG_* */
+  int kv_pages;   /* KV pool size in pages of 128 positions (KF_FLAG_SERVING only);
+                     0 = max_batch * ceil(n_ctx / 128), every slot can reach n_ctx */
 } kf_config;
 /* A config is also rejected when the rows of its largest step,
  * max_batch * (max(max_prompt, max_k) + max_k), times max(d_mlp, 4 d_model)
@@ -93,8 +97,11 @@ typedef struct kf_ctx kf_ctx;
 int kf_create(const kf_config *cfg, void *hip_stream, kf_ctx **out);
 
 /* Device bytes the caller must provide for cfg: packed weights, the KV cache
- * ([max_batch][n_layer][K,V][n_head][n_ctx][d_head]) and the workspace.
- * Returns 0 for an invalid cfg. */
+ * and the workspace.  The KV cache is a pool of pages of 128 positions of one
+ * sequence, each [n_layer][K,V][n_head][128 * d_head] compute-dtype elements
+ * (keys slot-major, values transposed); the pool holds kv_pages pages, or
+ * max_batch * ceil(n_ctx / 128) when kv_pages is 0.  Returns 0 for an invalid
+ * cfg. */
 size_t kf_state_bytes(const kf_config *cfg);
 
 /* Hand the context a device buffer of at least kf_state_bytes() bytes,
@@ -289,6 +296,47 @@ int kf_kernel_time(kf_ctx *ctx, int kernel_class, double *total_ms, int *launche
 #define KF_MASK_DOUBLE 1
 int kf_training_attention(void *hip_stream, int mask, int B, int H, int N, int k, int d_head,
                           const void *Q, const void *K, const void *V, void *O, float scale);
+
+/* ----------------------------------------------------- continuous batching
+ * Serving of independent sequences that start and end at different steps
+ * (the decode of Appendix C.1 per sequence, batched): a context created with
+ * KF_FLAG_SERVING has max_batch sequence slots, each with its own committed
+ * length C and pending tokens, over a pool of KV pages (kv_pages) handed out
+ * as sequences grow and returned when they are released.  Every sequence
+ * computes exactly what kf_prefill / kf_decode_block compute for it alone.
+ * Slot lists are host arrays of distinct ids in [0, max_batch); the row order
+ * of prompts, noise and out follows the list.  Calls of this group end a
+ * lock-step generation in progress; the lock-step calls (kf_prefill,
+ * kf_generate, the AR calls, kf_teacher_targets) release every slot.
+ * A temperature-conditioned model uses the temperature of each slot's index
+ * (kf_set_temperature sets slots 0..B-1).
+ *
+ * kf_serve_admit: start n sequences in free slots: prompt rows prompts [n][N]
+ * (device, positions 0..N-1) and k noise rows noise [n][k] (device), one
+ * causal pass, argmax tokens -> out [n][k] (device), pending; C = N.
+ * 0 <= N <= max_prompt, 1 <= k <= max_k, N + k <= n_ctx (else KF_ECTX).
+ * KF_ESTATE if a slot is in use; KF_ENOMEM (nothing changes) if the pool
+ * lacks the ceil((N + k) / 128) pages per sequence.
+ *
+ * kf_serve_step: one decode block for the n listed slots, which must hold
+ * sequences with equal pending counts p: pending tokens at positions
+ * C..C+p-1 and noise [n][k] rows after them; out [n][k] becomes the slots'
+ * pending tokens and C += p.  Per slot C + p + k <= n_ctx (else KF_ECTX);
+ * KF_ENOMEM (nothing changes) when the pool cannot cover positions
+ * 0..C+p+k-1 of every listed slot.  Slots not listed are untouched.
+ *
+ * kf_serve_release: end the sequences in the listed slots and return their
+ * pages (KF_ESTATE, nothing changes, if one holds no sequence).
+ *
+ * kf_serve_state: C, pending count and pages of a slot (C = -1 if free).
+ * kf_serve_pages: free and total pages of the pool. */
+int kf_serve_admit(kf_ctx *ctx, int n, const int32_t *slots, int N, const int32_t *prompts, int k,
+                   const float *noise, int32_t *out);
+int kf_serve_step(kf_ctx *ctx, int n, const int32_t *slots, int k, const float *noise,
+                  int32_t *out);
+int kf_serve_release(kf_ctx *ctx, int n, const int32_t *slots);
+int kf_serve_state(const kf_ctx *ctx, int slot, int *C, int *pending, int *pages);
+int kf_serve_pages(const kf_ctx *ctx, int *free_pages, int *total);
 
 /* Release host resources (device memory belongs to the caller). */
 void kf_destroy(kf_ctx *ctx);

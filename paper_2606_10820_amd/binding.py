@@ -23,6 +23,8 @@ KF_FLAG_TEMPERATURE = 2
 KF_FLAG_TEACHER = 4
 KF_FLAG_ROLLOUT = 8
 KF_FLAG_RMS_ROPE = 16
+KF_FLAG_SERVING = 32
+KF_PAGE = 128  # positions per KV page
 KF_MASK_SINGLE, KF_MASK_DOUBLE = 0, 1
 KF_KC_NAMES = ["embed", "noise", "norm", "qkv", "attn", "oproj", "mlp_up", "mlp_down", "head",
                "select"]
@@ -36,7 +38,7 @@ class KfConfig(ctypes.Structure):
         ("n_layer", ctypes.c_int), ("d_model", ctypes.c_int), ("n_head", ctypes.c_int),
         ("d_mlp", ctypes.c_int), ("vocab", ctypes.c_int), ("n_ctx", ctypes.c_int),
         ("dtype", ctypes.c_int), ("max_batch", ctypes.c_int), ("max_k", ctypes.c_int),
-        ("max_prompt", ctypes.c_int), ("flags", ctypes.c_uint),
+        ("max_prompt", ctypes.c_int), ("flags", ctypes.c_uint), ("kv_pages", ctypes.c_int),
     ]
 
 
@@ -87,6 +89,11 @@ def lib():
         "kf_last_error": (ctypes.c_char_p, [P]),
         "kf_strerror": (ctypes.c_char_p, [I]),
         "kf_training_attention": (I, [P, I, I, I, I, I, I, P, P, P, P, ctypes.c_float]),
+        "kf_serve_admit": (I, [P, I, P, I, P, I, P, P]),
+        "kf_serve_step": (I, [P, I, P, I, P, P]),
+        "kf_serve_release": (I, [P, I, P]),
+        "kf_serve_state": (I, [P, I, IP, IP, IP]),
+        "kf_serve_pages": (I, [P, IP, IP]),
     }
     for name, (res, args) in sigs.items():
         f = getattr(L, name)
@@ -97,9 +104,9 @@ def lib():
 
 
 def make_config(n_layer, d_model, n_head, d_mlp, vocab, n_ctx, dtype, max_batch, max_k,
-                max_prompt, flags=0) -> KfConfig:
+                max_prompt, flags=0, kv_pages=0) -> KfConfig:
     return KfConfig(n_layer, d_model, n_head, d_mlp, vocab, n_ctx, dtype, max_batch, max_k,
-                    max_prompt, flags)
+                    max_prompt, flags, kv_pages)
 
 
 class KForcing:
@@ -253,6 +260,50 @@ class KForcing:
                                                   self._p(b), self._p(x1), self._p(x2)))
         self.torch.cuda.synchronize(self.device)  # the inputs may be temporaries
         return x1, x2
+
+    # -- continuous batching (KF_FLAG_SERVING) ---------------------------
+    @staticmethod
+    def _slots(slots):
+        import numpy as np
+        arr = np.ascontiguousarray(slots, dtype=np.int32)
+        return arr, ctypes.c_void_p(arr.ctypes.data)
+
+    def serve_admit(self, slots, prompts, k: int, noise, out=None):
+        """Start len(slots) sequences: prompts [n][N], noise [n][k] -> out [n][k]."""
+        arr, sp = self._slots(slots)
+        prompts = self._i32(prompts).reshape(len(arr), -1)
+        noise = self._f32(noise)
+        n, N = prompts.shape
+        if out is None:
+            out = self.torch.empty((n, k), dtype=self.torch.int32, device=self.device)
+        self._check(self.L.kf_serve_admit(self.h, n, sp, N, self._p(prompts), k, self._p(noise),
+                                          self._p(out)))
+        return out
+
+    def serve_step(self, slots, noise, out=None):
+        """One decode block for the listed slots: noise [n][k] -> out [n][k]."""
+        arr, sp = self._slots(slots)
+        noise = self._f32(noise)
+        n, k = noise.shape
+        if out is None:
+            out = self.torch.empty((n, k), dtype=self.torch.int32, device=self.device)
+        self._check(self.L.kf_serve_step(self.h, n, sp, k, self._p(noise), self._p(out)))
+        return out
+
+    def serve_release(self, slots):
+        arr, sp = self._slots(slots)
+        self._check(self.L.kf_serve_release(self.h, len(arr), sp))
+
+    def serve_state(self, slot: int):
+        C, p, g = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+        self._check(self.L.kf_serve_state(self.h, slot, ctypes.byref(C), ctypes.byref(p),
+                                          ctypes.byref(g)))
+        return C.value, p.value, g.value
+
+    def serve_pages(self):
+        f, t = ctypes.c_int(), ctypes.c_int()
+        self._check(self.L.kf_serve_pages(self.h, ctypes.byref(f), ctypes.byref(t)))
+        return f.value, t.value
 
     def fill_noise(self, seed: int, B: int, p0: int, n: int):
         out = self.torch.empty((B, n), dtype=self.torch.float32, device=self.device)

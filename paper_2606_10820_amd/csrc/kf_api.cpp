@@ -56,7 +56,13 @@ struct Plan {
   size_t rope = 0;                              // rotary table [n_ctx][d_rot/2] (KF_FLAG_RMS_ROPE)
   size_t temb = 0;                              // per-sequence temperature embedding [max_batch][d]
   std::vector<LayerOff> layer;
+  int Tp = 0;           // per-sequence KV capacity rounded up to whole pages
+  int npp = 0;          // pages per sequence (Tp / kPage)
+  int n_pages = 0;      // pages in the KV pool
+  size_t page_bytes = 0;
   size_t kv = 0, kv_bytes = 0;
+  size_t meta = 0;      // continuous batching: slot map [max_batch], committed lengths
+                        // [max_batch], page table [max_batch][npp] (int32)
   size_t X = 0, Xh = 0, lnst = 0, A = 0, Q = 0, O = 0, Hm = 0, noise = 0, pval = 0, pidx = 0;
   size_t logits = 0, dstate = 0, pend = 0;
   int teacher_rows = 0;                    // rows per sampling-head chunk (KF_FLAG_TEACHER)
@@ -86,8 +92,12 @@ bool config_ok(const kf_config& c, std::string* why) {
   if (c.max_k < 1 || c.max_k > c.n_ctx) return bad("max_k must be in [1, n_ctx]");
   if (c.max_prompt < 1 || c.max_prompt > c.n_ctx) return bad("max_prompt must be in [1, n_ctx]");
   if (c.flags & ~(KF_FLAG_DEBUG_LOGITS | KF_FLAG_TEMPERATURE | KF_FLAG_TEACHER | KF_FLAG_ROLLOUT |
-                  KF_FLAG_RMS_ROPE))
+                  KF_FLAG_RMS_ROPE | KF_FLAG_SERVING))
     return bad("unknown flag bits");
+  if (c.kv_pages < 0) return bad("kv_pages must be >= 0");
+  if (c.kv_pages > 0 && !(c.flags & KF_FLAG_SERVING)) return bad("kv_pages needs KF_FLAG_SERVING");
+  if ((long long)c.max_batch * ((c.n_ctx + kPage - 1) / kPage) > (1 << 24))
+    return bad("max_batch * pages per sequence must stay below 2^24");
   // GEMM operands are addressed through buffer descriptors with 32-bit byte
   // ranges: the largest activation matrix of a step must stay below 2 GiB.
   const long long es = c.dtype == KF_BF16 ? 2 : 4;
@@ -169,8 +179,13 @@ void make_plan(const kf_config& c, Plan& p) {
     p.tb2 = take(d * 4);
   }
   p.wend = off;
-  p.kv_bytes = (size_t)c.max_batch * L * 2 * T * d * es;
+  p.Tp = (c.n_ctx + kPage - 1) / kPage * kPage;
+  p.npp = p.Tp / kPage;
+  p.page_bytes = L * 2 * d * kPage * es;
+  p.n_pages = c.kv_pages > 0 ? c.kv_pages : c.max_batch * p.npp;
+  p.kv_bytes = (size_t)p.n_pages * p.page_bytes;
   p.kv = take(p.kv_bytes);
+  if (c.flags & KF_FLAG_SERVING) p.meta = take((size_t)c.max_batch * (2 + p.npp) * 4);
   const size_t R = p.rows_max, Hw = f > 4 * d ? f : 4 * d;
   p.X = take(R * d * 4);
   p.temb = (c.flags & KF_FLAG_TEMPERATURE) ? take((size_t)c.max_batch * d * es) : 0;
@@ -220,6 +235,16 @@ struct kf_ctx {
   bool live = false;
   int B = 0, C = 0, pending = 0;
   int temp_B = 0;  // sequences whose temperature embedding is set (kf_set_temperature)
+  // continuous batching (KF_FLAG_SERVING): sequence slots and the page pool
+  struct Slot {
+    bool live = false;
+    int C = 0, pending = 0;
+    std::vector<int> pages;  // page ids of positions 0, 128, 256, ...
+  };
+  std::vector<Slot> slots;
+  std::vector<int> free_pages;  // stack of unused page ids
+  int serving = 0;              // live slots
+  std::vector<int> map_dev;     // the slot map last written to the device
   int last_head_rows = 0;
   bool last_logits = false;
   std::string err;
@@ -313,7 +338,7 @@ int ev_end(kf_ctx* c) {
 // Inputs of one step.
 struct StepIn {
   int B, nr, k;              // sequences, real rows, noise rows (k == 0: AR step)
-  const int32_t* toks;       // real-row tokens [B][tok_stride]
+  const int32_t* toks;       // real-row tokens [B][tok_stride] (or [slots][..], see serve)
   int tok_stride;
   const float* noise;        // [B][k] or null (device Philox)
   const float* u_ar;         // AR: [B] or null (device Philox)
@@ -324,6 +349,11 @@ struct StepIn {
   const float* tau = nullptr;    // [B] temperatures
   const float* u_rows = nullptr; // [B][nr] noise
   int32_t* targets = nullptr;    // [B][nr] output; non-null selects the teacher head
+  // continuous batching: step sequence b is the slot in the device slot map,
+  // with its own committed length and pages; toks are then indexed by slot
+  // when toks_by_slot (the pending-token buffer)
+  bool serve = false;
+  bool toks_by_slot = false;
 };
 
 template <typename T>
@@ -353,16 +383,24 @@ int run_step(kf_ctx* c, const StepIn& in) {
   auto W = [&](size_t o) { return reinterpret_cast<const T*>(base + o); };
 
   KfStepGeom g{in.B, in.nr + in.k, in.nr, in.k};
-  KfKvGeom kg{cf.n_layer, cf.n_head, cf.n_ctx, d / cf.n_head};
+  KfKvGeom kg{cf.n_layer, cf.n_head, p.Tp, d / cf.n_head};
+  if (in.serve) {
+    int* meta = reinterpret_cast<int*>(base + p.meta);
+    g.map = meta;
+    g.cs = meta + cf.max_batch;
+    kg.ptab = meta + 2 * cf.max_batch;
+  }
   const int M = in.B * g.R;
   const bool debug = (cf.flags & KF_FLAG_DEBUG_LOGITS) != 0;
   const int rms = (cf.flags & KF_FLAG_RMS_ROPE) ? 1 : 0;
   const float2* rope = rms ? reinterpret_cast<const float2*>(base + p.rope) : nullptr;
 
-  if (in.reset) KF_HIP(c, kf::launch_zero_i32(reinterpret_cast<int*>(st), 1, s));
+  if (in.reset && in.serve) KF_HIP(c, kf::launch_seq_reset(g, s));
+  else if (in.reset) KF_HIP(c, kf::launch_zero_i32(reinterpret_cast<int*>(st), 1, s));
   if (in.nr > 0)
     KF_LAUNCH(c, KF_KC_EMBED,
-              kf::launch_embed_real<T>(X, Xh, lnst, tok, pos, in.toks, in.tok_stride, g, d, V, st, s));
+              kf::launch_embed_real<T>(X, Xh, lnst, tok, pos, in.toks, in.tok_stride,
+                                       in.toks_by_slot ? 1 : 0, g, d, V, st, s));
   if (in.k > 0) {
     const int Mk = in.B * in.k;
     float* urec = reinterpret_cast<float*>(base + p.noise);
@@ -425,7 +463,7 @@ int run_step(kf_ctx* c, const StepIn& in) {
   else
     KF_LAUNCH(c, KF_KC_SELECT,
               kf::launch_icdf_select(logits, V, in.u_ar, in.seed, g, st, in.od, s));
-  KF_LAUNCH(c, KF_KC_SELECT, kf::launch_commit(st, in.nr, s));
+  KF_LAUNCH(c, KF_KC_SELECT, kf::launch_commit(st, g, in.nr, s));
   c->last_head_rows = Mh;
   c->last_logits = logits != nullptr;
   return KF_OK;
@@ -529,7 +567,7 @@ int run_rollout(kf_ctx* c, int B, int N, int k, const int32_t* tokens, const flo
   // round 1: SingleForward over [context | noise z1]
   const int n1 = N + nk;
   KF_LAUNCH(c, KF_KC_EMBED,
-            kf::launch_embed_real<T>(X, Xh, lnst, tok, pos, tokens, N, KfStepGeom{B, n1, N, 0}, d, V,
+            kf::launch_embed_real<T>(X, Xh, lnst, tok, pos, tokens, N, 0, KfStepGeom{B, n1, N, 0}, d, V,
                                      st, s));
   if (int r = noise(z1, n1, N, 1)) return r;
   if (int r = body(n1, 0, KF_MASK_SINGLE)) return r;
@@ -669,6 +707,105 @@ int run_temperature(kf_ctx* c, const float* tau, int B) {
   return KF_OK;
 }
 
+// ------------------------------------------------------ continuous batching
+// Host side of the paged KV pool: a stack of free page ids and, per sequence
+// slot, the pages that hold its positions 0, 128, 256, ...  The device copy of
+// the page table and of the step's slot map is kept current through scatter
+// launches (the values travel in the launch arguments).
+
+void serve_reset(kf_ctx* c) {
+  c->slots.assign(c->cfg.max_batch, kf_ctx::Slot{});
+  c->free_pages.resize(c->plan.n_pages);
+  for (int i = 0; i < c->plan.n_pages; ++i) c->free_pages[i] = c->plan.n_pages - 1 - i;
+  c->serving = 0;
+  c->map_dev.clear();
+}
+
+// Lock-step calls address sequence b's pages b * npp + j directly: they end
+// every served sequence, and need B whole sequences' worth of pages.
+int lockstep_begin(kf_ctx* c, int B) {
+  if ((long long)B * c->plan.npp > c->plan.n_pages)
+    return fail(c, KF_EINVAL, "B=%d sequences of %d pages exceed the KV pool of %d pages", B,
+                c->plan.npp, c->plan.n_pages);
+  if (c->serving) serve_reset(c);
+  return KF_OK;
+}
+
+struct ScatterBatch {
+  kf_ctx* c;
+  int* dst;
+  kf::KfScatter u{};
+  int add(int idx, int val) {
+    u.idx[u.n] = idx;
+    u.val[u.n] = val;
+    if (++u.n == kf::kScatterMax) return flush();
+    return KF_OK;
+  }
+  int flush() {
+    if (u.n == 0) return KF_OK;
+    KF_HIP(c, kf::launch_scatter_i32(dst, u, c->stream));
+    u.n = 0;
+    return KF_OK;
+  }
+};
+
+// Check the slot list of a serving call: distinct ids in [0, max_batch).
+int check_slots(kf_ctx* c, int n, const int32_t* slots) {
+  if (n < 1 || n > c->cfg.max_batch)
+    return fail(c, KF_EINVAL, "n=%d outside [1, %d]", n, c->cfg.max_batch);
+  if (!slots) return fail(c, KF_EINVAL, "null slot list");
+  std::vector<char> seen(c->cfg.max_batch, 0);
+  for (int b = 0; b < n; ++b) {
+    const int q = slots[b];
+    if (q < 0 || q >= c->cfg.max_batch) return fail(c, KF_EINVAL, "slot %d outside [0, %d)", q, c->cfg.max_batch);
+    if (seen[q]) return fail(c, KF_EINVAL, "slot %d appears twice", q);
+    seen[q] = 1;
+  }
+  return KF_OK;
+}
+
+// Give each slot of the step the pages that cover positions [0, upto[b]),
+// all or nothing, and send the new page-table entries and the slot map to the
+// device.  On failure nothing changes.
+int serve_prepare(kf_ctx* c, int n, const int32_t* slots, const std::vector<int>& upto) {
+  const Plan& p = c->plan;
+  int need = 0;
+  for (int b = 0; b < n; ++b) {
+    const int want = (upto[b] + kPage - 1) / kPage;
+    const int have = (int)c->slots[slots[b]].pages.size();
+    if (want > have) need += want - have;
+  }
+  if (need > (int)c->free_pages.size())
+    return fail(c, KF_ENOMEM, "the step needs %d more KV pages, %zu of %d are free", need,
+                c->free_pages.size(), p.n_pages);
+  ScatterBatch sb{c, reinterpret_cast<int*>(c->base + p.meta)};
+  for (int b = 0; b < n; ++b) {
+    kf_ctx::Slot& sl = c->slots[slots[b]];
+    const int want = (upto[b] + kPage - 1) / kPage;
+    while ((int)sl.pages.size() < want) {
+      const int pg = c->free_pages.back();
+      c->free_pages.pop_back();
+      const int j = (int)sl.pages.size();
+      sl.pages.push_back(pg);
+      if (int r = sb.add(2 * c->cfg.max_batch + slots[b] * p.npp + j, pg)) return r;
+    }
+  }
+  if ((int)c->map_dev.size() < n) c->map_dev.resize(n, -1);
+  for (int b = 0; b < n; ++b)
+    if (c->map_dev[b] != slots[b]) {
+      if (int r = sb.add(b, slots[b])) return r;
+      c->map_dev[b] = slots[b];
+    }
+  return sb.flush();
+}
+
+void serve_free(kf_ctx* c, int q) {
+  kf_ctx::Slot& sl = c->slots[q];
+  for (int pg : sl.pages) c->free_pages.push_back(pg);
+  sl = kf_ctx::Slot{};
+  --c->serving;
+}
+
 }  // namespace
 
 // ==================================================================== ABI
@@ -730,6 +867,7 @@ int kf_bind_state(kf_ctx* c, void* dev_ptr, size_t bytes) {
   c->weights = false;
   c->live = false;
   c->B = c->C = c->pending = 0;
+  serve_reset(c);
   return KF_OK;
 }
 
@@ -899,6 +1037,7 @@ int kf_prefill(kf_ctx* c, int B, int N, const int32_t* prompt, int k, const floa
   if (r) return r;
   r = temp_ready(c, B);
   if (r) return r;
+  if ((r = lockstep_begin(c, B))) return r;
   StepIn in{B, N, k, prompt, N, noise, nullptr, 0, out_desc(c, out, k, -1), true};
   r = step(c, in);
   if (r) return r;
@@ -944,6 +1083,7 @@ int kf_generate(kf_ctx* c, int B, int N, const int32_t* prompt, int L, int k, ui
   r = temp_ready(c, B);
   if (r) return r;
   if (L == 0) return KF_OK;
+  if ((r = lockstep_begin(c, B))) return r;
   StepIn in{B, N, k, prompt, N, nullptr, nullptr, seed, out_desc(c, out, L, N), true};
   r = step(c, in);
   if (r) return r;
@@ -964,6 +1104,7 @@ int kf_prefill_ar(kf_ctx* c, int B, int N, const int32_t* prompt, const float* u
   if (N + 1 > cf.n_ctx) return fail(c, KF_ECTX, "N + 1 = %d exceeds n_ctx = %d", N + 1, cf.n_ctx);
   int r = ready(c);
   if (r) return r;
+  if ((r = lockstep_begin(c, B))) return r;
   StepIn in{B, N, 0, prompt, N, nullptr, u, 0, out_desc(c, out, 1, -1), true};
   r = step(c, in);
   if (r) return r;
@@ -1003,6 +1144,7 @@ int kf_generate_ar(kf_ctx* c, int B, int N, const int32_t* prompt, int L, uint64
   int r = ready(c);
   if (r) return r;
   if (L == 0) return KF_OK;
+  if ((r = lockstep_begin(c, B))) return r;
   StepIn in{B, N, 0, prompt, N, nullptr, nullptr, seed, out_desc(c, out, L, N), true};
   r = step(c, in);
   if (r) return r;
@@ -1105,6 +1247,7 @@ int kf_teacher_targets(kf_ctx* c, int B, int N, const int32_t* tokens, const flo
   in.tau = tau;
   in.u_rows = u;
   in.targets = targets;
+  if (int r = lockstep_begin(c, B)) return r;
   // the pass writes the KV cache of every sequence: a generation in progress ends here
   c->live = false;
   c->C = 0;
@@ -1137,6 +1280,113 @@ int kf_selfforcing_targets(kf_ctx* c, int B, int N, int k, const int32_t* tokens
   c->B = 0;
   drop_graph(c);
   return run_rollout<bf16>(c, B, N, k, tokens, z1, z2, x1, x2);
+}
+
+// ------------------------------------------------------ continuous batching
+int kf_serve_admit(kf_ctx* c, int n, const int32_t* slots, int N, const int32_t* prompts, int k,
+                   const float* noise, int32_t* out) {
+  if (!c) return KF_EINVAL;
+  const kf_config& cf = c->cfg;
+  if (!(cf.flags & KF_FLAG_SERVING)) return fail(c, KF_ESTATE, "serving calls need KF_FLAG_SERVING");
+  if (int r = check_slots(c, n, slots)) return r;
+  if (N < 0 || N > cf.max_prompt) return fail(c, KF_EINVAL, "N=%d outside [0, %d]", N, cf.max_prompt);
+  if (k < 1 || k > cf.max_k) return fail(c, KF_EINVAL, "k=%d outside [1, %d]", k, cf.max_k);
+  if (!noise || !out || (N > 0 && !prompts)) return fail(c, KF_EINVAL, "null pointer argument");
+  if (N + k > cf.n_ctx) return fail(c, KF_ECTX, "N + k = %d exceeds n_ctx = %d", N + k, cf.n_ctx);
+  if (int r = ready(c)) return r;
+  int top = 0;
+  for (int b = 0; b < n; ++b) {
+    if (c->slots.size() != (size_t)cf.max_batch || c->slots[slots[b]].live)
+      return fail(c, KF_ESTATE, "slot %d is in use (kf_serve_release it first)", slots[b]);
+    top = slots[b] + 1 > top ? slots[b] + 1 : top;
+  }
+  if (int r = temp_ready(c, top)) return r;
+  // admission writes pages the lock-step calls address directly
+  c->live = false;
+  c->B = c->C = c->pending = 0;
+  drop_graph(c);
+  std::vector<int> upto(n, N + k);
+  if (int r = serve_prepare(c, n, slots, upto)) return r;
+  StepIn in{n, N, k, prompts, N, noise, nullptr, 0, out_desc(c, out, k, -1), true};
+  in.serve = true;
+  for (int b = 0; b < n; ++b) {
+    kf_ctx::Slot& sl = c->slots[slots[b]];
+    sl.live = true;
+    sl.C = N;
+    sl.pending = k;
+    ++c->serving;
+  }
+  const int r = step(c, in);
+  if (r)
+    for (int b = 0; b < n; ++b) serve_free(c, slots[b]);
+  return r;
+}
+
+int kf_serve_step(kf_ctx* c, int n, const int32_t* slots, int k, const float* noise, int32_t* out) {
+  if (!c) return KF_EINVAL;
+  const kf_config& cf = c->cfg;
+  if (!(cf.flags & KF_FLAG_SERVING)) return fail(c, KF_ESTATE, "serving calls need KF_FLAG_SERVING");
+  if (int r = check_slots(c, n, slots)) return r;
+  if (k < 1 || k > cf.max_k) return fail(c, KF_EINVAL, "k=%d outside [1, %d]", k, cf.max_k);
+  if (!noise || !out) return fail(c, KF_EINVAL, "null pointer argument");
+  if (int r = ready(c)) return r;
+  if (c->slots.size() != (size_t)cf.max_batch) return fail(c, KF_ESTATE, "no sequence admitted");
+  int top = 0, nr = -1;
+  std::vector<int> upto(n);
+  for (int b = 0; b < n; ++b) {
+    const kf_ctx::Slot& sl = c->slots[slots[b]];
+    if (!sl.live) return fail(c, KF_ESTATE, "slot %d holds no sequence", slots[b]);
+    if (nr >= 0 && sl.pending != nr)
+      return fail(c, KF_EINVAL, "slots of one step must have equal pending counts (%d, %d)", nr,
+                  sl.pending);
+    nr = sl.pending;
+    if (sl.C + sl.pending + k > cf.n_ctx)
+      return fail(c, KF_ECTX, "slot %d: C + pending + k = %d exceeds n_ctx = %d", slots[b],
+                  sl.C + sl.pending + k, cf.n_ctx);
+    upto[b] = sl.C + sl.pending + k;
+    top = slots[b] + 1 > top ? slots[b] + 1 : top;
+  }
+  if (int r = temp_ready(c, top)) return r;
+  if (int r = serve_prepare(c, n, slots, upto)) return r;
+  StepIn in{n, nr, k, pend_ptr(c), cf.max_k, noise, nullptr, 0, out_desc(c, out, k, -1), false};
+  in.serve = true;
+  in.toks_by_slot = true;
+  if (int r = step(c, in)) return r;
+  for (int b = 0; b < n; ++b) {
+    kf_ctx::Slot& sl = c->slots[slots[b]];
+    sl.C += sl.pending;
+    sl.pending = k;
+  }
+  return KF_OK;
+}
+
+int kf_serve_release(kf_ctx* c, int n, const int32_t* slots) {
+  if (!c) return KF_EINVAL;
+  if (!(c->cfg.flags & KF_FLAG_SERVING)) return fail(c, KF_ESTATE, "serving calls need KF_FLAG_SERVING");
+  if (int r = check_slots(c, n, slots)) return r;
+  for (int b = 0; b < n; ++b)
+    if (c->slots.size() != (size_t)c->cfg.max_batch || !c->slots[slots[b]].live)
+      return fail(c, KF_ESTATE, "slot %d holds no sequence", slots[b]);
+  for (int b = 0; b < n; ++b) serve_free(c, slots[b]);
+  return KF_OK;
+}
+
+int kf_serve_state(const kf_ctx* c, int slot, int* C, int* pending, int* pages) {
+  if (!c) return KF_EINVAL;
+  if (slot < 0 || slot >= c->cfg.max_batch) return KF_EINVAL;
+  const bool on = c->slots.size() == (size_t)c->cfg.max_batch && c->slots[slot].live;
+  if (C) *C = on ? c->slots[slot].C : -1;
+  if (pending) *pending = on ? c->slots[slot].pending : 0;
+  if (pages) *pages = on ? (int)c->slots[slot].pages.size() : 0;
+  return KF_OK;
+}
+
+int kf_serve_pages(const kf_ctx* c, int* free_pages, int* total) {
+  if (!c) return KF_EINVAL;
+  if (free_pages)
+    *free_pages = c->slots.size() == (size_t)c->cfg.max_batch ? (int)c->free_pages.size() : c->plan.n_pages;
+  if (total) *total = c->plan.n_pages;
+  return KF_OK;
 }
 
 int kf_training_attention(void* hip_stream, int mask, int B, int H, int N, int k, int d_head,

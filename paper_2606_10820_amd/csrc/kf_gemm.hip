@@ -148,9 +148,9 @@ struct EpResidual {
 };
 
 // QKV projection: q goes to Q [M][d]; k and v of row (b, i) go straight into
-// the KV cache slot C + i of sequence b (the KV append of the step).  Keys are
-// stored [slot][d_head] and values transposed, [d_head][slot], per head.  An
-// 8-column chunk never straddles q/k/v or two heads (d_head >= 32).
+// cache slot C_b + i of sequence b (the KV append of the step), in the page
+// that holds it: keys [slot][d_head] and values transposed, [d_head][slot], per
+// head.  An 8-column chunk never straddles q/k/v or two heads (d_head >= 32).
 // Rotary positions (RoFormer) on 8 consecutive columns e..e+7 of one head
 // (e even): pairs (e + 2r, e + 2r + 1) with pair index i = e/2 + r < d_rot/2
 // turn by the table angle of position p (cs [n_ctx][d_rot/2] = cos, sin).
@@ -181,37 +181,38 @@ struct EpQKV {
   __device__ inline void store8(int m, int n, float (&v)[8]) const {
     const int d = kg.H * kg.dh;
     const int which = n / d, c = n - which * d;
-    if (rope && which < 2) {
-      const int i = m - (m / g.R) * g.R;
-      rotate8(v, rope, kg.dh < 64 ? kg.dh : 64, st->C + i, c % kg.dh);
-    }
-    if (which == 0) {
+    if (which == 0 && !rope) {
       put8(Q + (size_t)m * d + c, v);
       return;
     }
     const int b = m / g.R, i = m - b * g.R;
-    const int h = c / kg.dh, e = c - h * kg.dh;
-    const int slot = st->C + i;
-    T* base = kv + (size_t)b * kg.seq_stride() + kg.head_off(layer, which - 1, h);
+    const int slot = g.ctx(st, b) + i;  // this row's position and cache slot
+    if (rope && which < 2) rotate8(v, rope, kg.dh < 64 ? kg.dh : 64, slot, c % kg.dh);
+    if (which == 0) {
+      put8(Q + (size_t)m * d + c, v);
+      return;
+    }
+    const int h = c / kg.dh, e = c - h * kg.dh, r0 = (unsigned)slot % kPage;
+    T* base = kv + kg.page_base(g.slot(b), slot) + kg.head_off(layer, which - 1, h);
     if (which == 1) {  // keys: [slot][dh]
-      put8(base + (size_t)slot * kg.dh + e, v);
+      put8(base + (size_t)r0 * kg.dh + e, v);
     } else {           // values, transposed: [dh][slot]
 #pragma unroll
-      for (int r = 0; r < 8; ++r) base[(size_t)(e + r) * kg.T + slot] = from_f<T>(v[r]);
+      for (int r = 0; r < 8; ++r) base[(size_t)(e + r) * kPage + r0] = from_f<T>(v[r]);
     }
   }
 };
 
 // Second noise-MLP layer: noise row m = (b, j) lands in residual row
-// b*R + nr + j with its learned position C + nr + j added, and, for a
-// temperature-conditioned model, sequence b's temperature embedding.
+// b*R + nr + j with its learned position C_b + nr + j added, and, for a
+// temperature-conditioned model, the temperature embedding of b's slot.
 template <typename T>
 struct EpNoiseOut {
   float* X;
   T* Xh;
   const float* bias;
   const T* pos;
-  const T* temb;  // per-sequence temperature embedding [B][d], or null
+  const T* temb;  // per-slot temperature embedding [slots][d], or null
   const KfDevState* st;
   KfStepGeom g;
   int d;
@@ -223,14 +224,15 @@ struct EpNoiseOut {
     return b * g.R + g.nr + (m - b * g.k);
   }
   __device__ inline void store8(int m, int n, float (&v)[8]) const {
-    const int p = st->C + g.nr + m % g.k;
+    const int b = m / g.k;
+    const int p = g.ctx(st, b) + g.nr + (m - b * g.k);
     const size_t row = (size_t)srow(m);
     float pe[8];
     get8(pos + (size_t)p * d + n, pe);
 #pragma unroll
     for (int i = 0; i < 8; ++i) v[i] += pe[i];
     if (temb) {
-      get8(temb + (size_t)(m / g.k) * d + n, pe);
+      get8(temb + (size_t)g.slot(b) * d + n, pe);
 #pragma unroll
       for (int i = 0; i < 8; ++i) v[i] += pe[i];
     }

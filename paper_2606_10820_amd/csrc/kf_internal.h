@@ -23,23 +23,47 @@ struct KfOutDesc {
   int stride;      // per-sequence stride of out (elements)
   int gen_base;    // >= 0: generation run, element index = emitted position - gen_base
                    // <  0: element index = head row index within the sequence
-  int32_t* pend;   // pending-token buffer [B][pend_stride] for the next step
+  int32_t* pend;   // pending-token buffer [slots][pend_stride] for the next step
   int pend_stride;
 };
 
 // Geometry of one step: B sequences, R = nr + k rows each (nr real rows, then
 // k noise rows), row (b, i) stored at index b * R + i.
+//
+// Lock-step batches (map == null): step sequence b is sequence slot b and every
+// sequence has the committed length KfDevState::C.  Continuous batching
+// (map != null): step sequence b is slot map[b], whose committed length is
+// cs[map[b]]; the slot picks its KV pages, pending tokens and temperature.
 struct KfStepGeom {
   int B, R, nr, k;
+  const int* map = nullptr;  // [B] sequence slots of the step, or null
+  int* cs = nullptr;         // [slots] committed lengths (with map), or null
+  __device__ inline int slot(int b) const { return map ? map[b] : b; }
+  __device__ inline int ctx(const KfDevState* st, int b) const { return map ? cs[map[b]] : st->C; }
 };
 
-// Geometry of the KV cache: [B][L][2][H][T * dh] elements; per head the keys
-// are [T][dh] (slot-major) and the values [dh][T] (transposed).
+// Geometry of the KV cache, in pages of kPage = 128 slots of one sequence.  A
+// page holds every layer: [L][2][H][128 * dh] elements, per head the keys
+// [128][dh] (slot-major) and the values [dh][128] (transposed).  Slot s of
+// sequence slot q lives in page ptab[q * (T / 128) + s / 128]; without a page
+// table (lock-step batches) sequence q owns pages q * (T / 128) onwards.  T is
+// the per-sequence capacity rounded up to a whole page.  (128-slot rows of
+// transposed values made the KV append of the QKV epilogue measurably faster
+// than 64-slot rows.)
+constexpr int kPage = 128;
 struct KfKvGeom {
   int L, H, T, dh;
-  __host__ __device__ size_t seq_stride() const { return (size_t)L * 2 * H * T * dh; }
-  __host__ __device__ size_t head_off(int layer, int which, int h) const {
-    return (((size_t)layer * 2 + which) * H + h) * (size_t)T * dh;
+  const int* ptab = nullptr;  // [slots][T / kPage] page ids, or null
+  __host__ __device__ unsigned page_elems() const { return (unsigned)(L * 2 * H * kPage * dh); }
+  // Offset of (layer, K or V, head) within a page (a page has < 2^31 elements).
+  __host__ __device__ unsigned head_off(int layer, int which, int h) const {
+    return (unsigned)(((layer * 2 + which) * H + h) * (kPage * dh));
+  }
+  // First element of the page holding slot s of sequence slot q.
+  __device__ inline size_t page_base(int q, int s) const {
+    const unsigned np = (unsigned)T / kPage, j = (unsigned)s / kPage;
+    const unsigned pg = ptab ? (unsigned)ptab[q * np + j] : q * np + j;
+    return (size_t)pg * page_elems();
   }
 };
 
@@ -103,15 +127,16 @@ struct SplitWs {
   size_t bytes;
 };
 
-// Real-row embedding: X[b*R + i] = tok[toks[b*tok_stride + i]] + pos[C + i], i < nr,
-// with its compute-dtype copy Xh and LayerNorm partial sums lnst (see gemm_residual).
+// Real-row embedding: X[b*R + i] = tok[toks[q*tok_stride + i]] + pos[C_b + i], i < nr,
+// with its compute-dtype copy Xh and LayerNorm partial sums lnst (see gemm_residual);
+// q = b, or the step's sequence slot when toks_by_slot (the pending-token buffer).
 template <typename T>
 hipError_t launch_embed_real(float* X, T* Xh, float2* lnst, const T* tok, const T* pos,
-                             const int32_t* toks, int tok_stride, KfStepGeom g, int d, int V,
-                             KfDevState* st, hipStream_t s);
+                             const int32_t* toks, int tok_stride, int toks_by_slot, KfStepGeom g,
+                             int d, int V, KfDevState* st, hipStream_t s);
 
 // Sinusoid of each noise row's u into S [B*k][d]; u from noise [B*k] or, when
-// noise is null, from the device Philox stream at positions C + nr + j.
+// noise is null, from the device Philox stream at positions C_b + nr + j.
 // The u actually used are written to u_out [B*k] when it is not null.
 template <typename T>
 hipError_t launch_noise_sinusoid(T* S, const float* noise, uint64_t seed, const double* omega,
@@ -241,8 +266,21 @@ hipError_t launch_argmax_select(const float* pval, const int* pidx, int n_tiles,
 hipError_t launch_icdf_select(const float* logits, int V, const float* u_in, uint64_t seed,
                               KfStepGeom g, const KfDevState* st, KfOutDesc od, hipStream_t s);
 
-// C += nr (end of step).
-hipError_t launch_commit(KfDevState* st, int nr, hipStream_t s);
+// C += nr (end of step): KfDevState::C, or with g.map the committed length of
+// each of the step's sequence slots.
+hipError_t launch_commit(KfDevState* st, KfStepGeom g, int nr, hipStream_t s);
+// Committed length 0 for each of the step's sequence slots (g.map required).
+hipError_t launch_seq_reset(KfStepGeom g, hipStream_t s);
+
+// Small host-to-device updates carried in the launch arguments (copied at
+// launch, so the host may reuse its arrays at once): dst[idx[i]] = val[i].
+constexpr int kScatterMax = 240;
+struct KfScatter {
+  int n;
+  int idx[kScatterMax];
+  int val[kScatterMax];
+};
+hipError_t launch_scatter_i32(int* dst, const KfScatter& u, hipStream_t s);
 
 // Device Philox noise for n positions starting at p0, [B][n].
 hipError_t launch_fill_noise(float* out, uint64_t seed, int B, int p0, int n, hipStream_t s);

@@ -31,12 +31,12 @@ template <typename T>
 __global__ void __launch_bounds__(256)
     embed_real_kernel(float* __restrict__ X, T* __restrict__ Xh, float2* __restrict__ lnst,
                       const T* __restrict__ tok, const T* __restrict__ pos,
-                      const int32_t* __restrict__ toks, int tok_stride, KfStepGeom g, int d, int V,
-                      KfDevState* st) {
+                      const int32_t* __restrict__ toks, int tok_stride, int toks_by_slot,
+                      KfStepGeom g, int d, int V, KfDevState* st) {
   const int r = blockIdx.x;
   const int b = r / g.nr, i = r % g.nr;
-  const int C = st->C;
-  int t = toks[(size_t)b * tok_stride + i];
+  const int C = g.ctx(st, b);
+  int t = toks[(size_t)(toks_by_slot ? g.slot(b) : b) * tok_stride + i];
   if (t < 0 || t >= V) {
     if (threadIdx.x == 0) atomicOr(&st->err, 1);
     t = 0;
@@ -74,7 +74,7 @@ __global__ void __launch_bounds__(256)
                           const KfDevState* st, float* __restrict__ u_out) {
   const int m = blockIdx.x;
   const int b = m / g.k, j = m % g.k;
-  float u = noise ? noise[m] : kf_noise_u(seed, b, st->C + g.nr + j);
+  float u = noise ? noise[m] : kf_noise_u(seed, g.slot(b), g.ctx(st, b) + g.nr + j);
   if (u_out && threadIdx.x == 0) u_out[m] = u;
   const int h = d / 2;
   const double su = 1000.0 * (double)u;
@@ -104,10 +104,8 @@ __global__ void __launch_bounds__(256)
   const int b = blockIdx.x / H, h = blockIdx.x % H;
   const int q0 = blockIdx.y * QB;
   const int nq = min(QB, g.R - q0);
-  const int C = st->C;
+  const int C = g.ctx(st, b), seq = g.slot(b);
   const int nkeys = C + q0 + nq;
-  const T* Kb = kv + (size_t)b * kg.seq_stride() + kg.head_off(layer, 0, h);
-  const T* Vb = kv + (size_t)b * kg.seq_stride() + kg.head_off(layer, 1, h);
 
   __shared__ float sQ[QB][DH];
   __shared__ float sK[KT][DH + 1];
@@ -126,14 +124,19 @@ __global__ void __launch_bounds__(256)
 #pragma unroll
   for (int c = 0; c < EPT; ++c) o[c] = 0.f;
 
+  static_assert(kPage % KT == 0, "a key tile lies in one KV page");
   for (int kt0 = 0; kt0 < nkeys; kt0 += KT) {
+    const T* page = kv + kg.page_base(seq, kt0);
+    const T* Kb = page + kg.head_off(layer, 0, h);
+    const T* Vb = page + kg.head_off(layer, 1, h);
+    const int p0 = kt0 % kPage;
     __syncthreads();
     for (int idx = tid; idx < KT * DH; idx += 256) {
       int kk = idx / DH, e = idx % DH, slot = kt0 + kk;
       float kx = 0.f, vx = 0.f;
       if (slot < nkeys) {
-        kx = to_f(Kb[(size_t)slot * DH + e]);
-        vx = to_f(Vb[(size_t)e * kg.T + slot]);
+        kx = to_f(Kb[(size_t)(p0 + kk) * DH + e]);
+        vx = to_f(Vb[(size_t)e * kPage + p0 + kk]);
       }
       sK[kk][e] = kx;
       sV[kk][e] = vx;
@@ -213,20 +216,18 @@ __global__ void __launch_bounds__(256)
                           bf16* __restrict__ O, const KfDevState* st, KfStepGeom g, KfKvGeom kg,
                           int layer, float scale, AttnSplit sp) {
   constexpr int QB = 16, KT = 32, NDC = DH / 32, NDB = DH / 16;
-  const int H = kg.H, T = kg.T, d = H * DH;
+  const int H = kg.H, d = H * DH;
   const int nqb = (g.R + QB - 1) / QB;
   const int split = blockIdx.x % sp.ns, rest = blockIdx.x / sp.ns;
   const int qb = rest % nqb, bh = rest / nqb;
   const int b = bh / H, h = bh % H;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int gq = lane >> 4, lq = lane & 15;
-  const int C = st->C;
+  const int C = g.ctx(st, b), seq = g.slot(b);
   const int q0 = qb * QB, nq = min(QB, g.R - q0);
   const int nkeys = C + q0 + nq;
   const int chunk = ((nkeys + sp.ns - 1) / sp.ns + KT - 1) / KT * KT;
   const int ks = split * chunk, ke = min(nkeys, ks + chunk);
-  const bf16* Kb = kv + (size_t)b * kg.seq_stride() + kg.head_off(layer, 0, h);
-  const bf16* Vt = kv + (size_t)b * kg.seq_stride() + kg.head_off(layer, 1, h);
 
   const bf16x8_t zero8 = {};
   bf16x8_t qf[NDC];
@@ -244,13 +245,20 @@ __global__ void __launch_bounds__(256)
     bf16x8_t k[2][NDC];
     bf16x8_t v[NDB];
   };
+  // A tile starts at a multiple of 32 keys, so it lies in one KV page, and so
+  // does the last key nkeys - 1 >= t0 that stands in for keys past the end.
   // K rows past the end read the last key (then zeroed); value slots past the
   // end are zeroed (their probability is 0, and 0 * a stale NaN would not be).
+  static_assert(kPage % KT == 0, "tiles do not straddle KV pages");
   auto load = [&](int t0, Frag& f) {
+    const bf16* page = kv + kg.page_base(seq, t0);
+    const bf16* Kb = page + kg.head_off(layer, 0, h);
+    const bf16* Vt = page + kg.head_off(layer, 1, h);
+    const int pbase = t0 - t0 % kPage;
 #pragma unroll
     for (int grp = 0; grp < 2; ++grp) {
       const int key = t0 + 8 * (lq >> 2) + 4 * grp + (lq & 3);
-      const int kc = key < nkeys ? key : nkeys - 1;
+      const int kc = (key < nkeys ? key : nkeys - 1) - pbase;
 #pragma unroll
       for (int c = 0; c < NDC; ++c) {
         const bf16x8_t x = load8(Kb + (size_t)kc * DH + c * 32 + 8 * gq);
@@ -260,7 +268,7 @@ __global__ void __launch_bounds__(256)
     const int kb = t0 + 8 * gq;
 #pragma unroll
     for (int db = 0; db < NDB; ++db) {
-      const bf16* vp = Vt + (size_t)(db * 16 + lq) * T + kb;
+      const bf16* vp = Vt + (size_t)(db * 16 + lq) * kPage + (kb - pbase);
       if (kb + 8 <= nkeys) {
         f.v[db] = load8(vp);
       } else {
@@ -443,8 +451,8 @@ __global__ void __launch_bounds__(256)
   if (lane == 0) {
     const int b = m / g.k, j = m % g.k;
     if (bi == 0x7fffffff) bi = 0;
-    od.out[out_index(od, st->C, g.nr, b, j)] = bi;
-    if (od.pend) od.pend[(size_t)b * od.pend_stride + j] = bi;
+    od.out[out_index(od, g.ctx(st, b), g.nr, b, j)] = bi;
+    if (od.pend) od.pend[(size_t)g.slot(b) * od.pend_stride + j] = bi;
   }
 }
 
@@ -459,8 +467,8 @@ __global__ void __launch_bounds__(1024)
   __shared__ int found;
   const int b = blockIdx.x, t = threadIdx.x;
   const float* l = logits + (size_t)b * V;
-  const int C = st->C;
-  const float u = u_in ? u_in[b] : kf_noise_u(seed, b, C + g.nr);
+  const int C = g.ctx(st, b);
+  const float u = u_in ? u_in[b] : kf_noise_u(seed, g.slot(b), C + g.nr);
   const int chunk = (V + 1023) / 1024;
   const int lo = min(V, t * chunk), hi = min(V, lo + chunk);
   float mx = -INFINITY;
@@ -506,7 +514,7 @@ __global__ void __launch_bounds__(1024)
         if (expf(l[i] - mx) > 0.f) { tok = i; break; }
     }
     od.out[out_index(od, C, g.nr, b, 0)] = tok;
-    od.pend[(size_t)b * od.pend_stride] = tok;
+    od.pend[(size_t)g.slot(b) * od.pend_stride] = tok;
   }
 }
 
@@ -736,8 +744,26 @@ __global__ void __launch_bounds__(256)
   if (lane == 0) targets[r] = min(j0 + jstar, V - 1);
 }
 
-__global__ void commit_kernel(KfDevState* st, int nr) {
-  if (threadIdx.x == 0 && blockIdx.x == 0) st->C += nr;
+// End of step: the real rows' K/V become context (C += nr), for the batch or
+// for each sequence slot of the step.
+__global__ void commit_kernel(KfDevState* st, KfStepGeom g, int nr) {
+  if (!g.map) {
+    if (threadIdx.x == 0 && blockIdx.x == 0) st->C += nr;
+    return;
+  }
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b < g.B) g.cs[g.map[b]] += nr;
+}
+
+__global__ void scatter_i32_kernel(int* dst, KfScatter u) {
+  const int i = threadIdx.x;
+  if (i < u.n) dst[u.idx[i]] = u.val[i];
+}
+
+// Admission of new sequences: their slots start from an empty context.
+__global__ void seq_reset_kernel(KfStepGeom g) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b < g.B) g.cs[g.map[b]] = 0;
 }
 
 __global__ void fill_noise_kernel(float* out, uint64_t seed, int B, int p0, int n) {
@@ -778,11 +804,11 @@ inline unsigned grid_for(size_t n, unsigned block) {
 // ------------------------------------------------------------ launchers
 template <typename T>
 hipError_t launch_embed_real(float* X, T* Xh, float2* lnst, const T* tok, const T* pos,
-                             const int32_t* toks, int tok_stride, KfStepGeom g, int d, int V,
-                             KfDevState* st, hipStream_t s) {
+                             const int32_t* toks, int tok_stride, int toks_by_slot, KfStepGeom g,
+                             int d, int V, KfDevState* st, hipStream_t s) {
   if (g.nr <= 0 || g.B <= 0) return hipSuccess;
   launch(embed_real_kernel<T>, dim3(g.B * g.nr), dim3(256), 0, s, X, Xh, lnst, tok, pos, toks,
-                     tok_stride, g, d, V, st);
+                     tok_stride, toks_by_slot, g, d, V, st);
   return hipGetLastError();
 }
 
@@ -902,8 +928,21 @@ hipError_t launch_teacher_select(const float* pmax, const float* psub, int n_til
   return hipGetLastError();
 }
 
-hipError_t launch_commit(KfDevState* st, int nr, hipStream_t s) {
-  launch(commit_kernel, dim3(1), dim3(64), 0, s, st, nr);
+hipError_t launch_commit(KfDevState* st, KfStepGeom g, int nr, hipStream_t s) {
+  launch(commit_kernel, dim3(g.map ? (g.B + 255) / 256 : 1), dim3(256), 0, s, st, g, nr);
+  return hipGetLastError();
+}
+
+hipError_t launch_scatter_i32(int* dst, const KfScatter& u, hipStream_t s) {
+  if (u.n <= 0) return hipSuccess;
+  if (u.n > kScatterMax) return hipErrorInvalidValue;
+  launch(scatter_i32_kernel, dim3(1), dim3(256), 0, s, dst, u);
+  return hipGetLastError();
+}
+
+hipError_t launch_seq_reset(KfStepGeom g, hipStream_t s) {
+  if (!g.map || g.B <= 0) return hipSuccess;
+  launch(seq_reset_kernel, dim3((g.B + 255) / 256), dim3(256), 0, s, g);
   return hipGetLastError();
 }
 
@@ -938,8 +977,8 @@ hipError_t launch_zero_i32(int* dst, size_t n, hipStream_t s) { return launch_ze
 
 #define KF_INST(T)                                                                                  \
   template hipError_t launch_embed_real<T>(float*, T*, float2*, const T*, const T*,               \
-                                           const int32_t*, int, KfStepGeom, int, int, KfDevState*, \
-                                           hipStream_t);                                            \
+                                           const int32_t*, int, int, KfStepGeom, int, int,         \
+                                           KfDevState*, hipStream_t);                               \
   template hipError_t launch_noise_sinusoid<T>(T*, const float*, uint64_t, const double*,          \
                                                KfStepGeom, int, const KfDevState*, float*,          \
                                                hipStream_t);                                        \

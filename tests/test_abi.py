@@ -61,7 +61,8 @@ def test_strerror(L):
 @pytest.mark.parametrize("bad", [
     dict(n_layer=0), dict(d_model=100), dict(n_head=3), dict(d_model=256, n_head=1),
     dict(d_mlp=100), dict(vocab=1), dict(n_ctx=100), dict(dtype=7), dict(max_batch=0), dict(max_k=0),
-    dict(max_k=1000), dict(max_prompt=0), dict(flags=32),
+    dict(max_k=1000), dict(max_prompt=0), dict(flags=64),
+    dict(kv_pages=-1), dict(kv_pages=8),  # a page pool needs KF_FLAG_SERVING
     dict(max_batch=65535, max_prompt=128, d_mlp=4096),
     # the teacher rollout's DoubleForward rows (2 * max_batch * max_prompt * max_k) count too
     dict(flags=8, max_batch=4096, max_prompt=128),
@@ -238,6 +239,48 @@ def test_selfforcing_argument_checks(L):
     assert L.kf_selfforcing_targets(h, 1, 4, 2, fake, fake, fake, fake, fake) == Bd.KF_ESTATE
     L.kf_destroy(h)
     assert L.kf_selfforcing_targets(None, 1, 4, 2, fake, fake, fake, fake, fake) == Bd.KF_EINVAL
+
+
+def test_serving_state_bytes_and_checks(L):
+    """The KV pool of a serving context is kv_pages pages of 64 positions x
+    n_layer x 2 x d_model elements; serving calls check their arguments before
+    touching any device memory."""
+    dense = _cfg(flags=Bd.KF_FLAG_SERVING, n_ctx=256)
+    small = _cfg(flags=Bd.KF_FLAG_SERVING, n_ctx=256, kv_pages=5)
+    page = Bd.KF_PAGE * 2 * 2 * 128 * 4  # positions x layers x (K, V) x d_model x fp32
+    nd, ns = L.kf_state_bytes(ctypes.byref(dense)), L.kf_state_bytes(ctypes.byref(small))
+    assert nd - ns >= (8 * 2 - 5) * page - 4096
+    assert nd - ns <= (8 * 2 - 5) * page + 4096
+    h = _ctx(L, small)
+    P = ctypes.c_void_p
+    fake = P(0x10000)
+    one = (ctypes.c_int32 * 1)(3)
+    two = (ctypes.c_int32 * 2)(1, 1)
+    bad = (ctypes.c_int32 * 1)(8)
+    # argument checks come first (no state bound yet)
+    assert L.kf_serve_admit(h, 0, one, 4, fake, 2, fake, fake) == Bd.KF_EINVAL
+    assert L.kf_serve_admit(h, 2, two, 4, fake, 2, fake, fake) == Bd.KF_EINVAL  # repeated slot
+    assert L.kf_serve_admit(h, 1, bad, 4, fake, 2, fake, fake) == Bd.KF_EINVAL  # slot >= max_batch
+    assert L.kf_serve_admit(h, 1, None, 4, fake, 2, fake, fake) == Bd.KF_EINVAL
+    assert L.kf_serve_admit(h, 1, one, 33, fake, 2, fake, fake) == Bd.KF_EINVAL  # N > max_prompt
+    assert L.kf_serve_admit(h, 1, one, 4, fake, 5, fake, fake) == Bd.KF_EINVAL   # k > max_k
+    assert L.kf_serve_admit(h, 1, one, 4, fake, 2, None, fake) == Bd.KF_EINVAL
+    assert L.kf_serve_step(h, 1, one, 0, fake, fake) == Bd.KF_EINVAL
+    assert L.kf_serve_admit(h, 1, one, 4, fake, 2, fake, fake) == Bd.KF_ESTATE   # nothing bound
+    assert L.kf_serve_release(h, 1, one) == Bd.KF_ESTATE
+    C, pend, pg = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+    assert L.kf_serve_state(h, 3, ctypes.byref(C), ctypes.byref(pend), ctypes.byref(pg)) == Bd.KF_OK
+    assert (C.value, pend.value, pg.value) == (-1, 0, 0)
+    assert L.kf_serve_state(h, 8, None, None, None) == Bd.KF_EINVAL
+    fr, tot = ctypes.c_int(), ctypes.c_int()
+    assert L.kf_serve_pages(h, ctypes.byref(fr), ctypes.byref(tot)) == Bd.KF_OK
+    assert (fr.value, tot.value) == (5, 5)
+    L.kf_destroy(h)
+    # a context without the flag refuses the serving calls
+    h = _ctx(L, _cfg())
+    assert L.kf_serve_admit(h, 1, one, 4, fake, 2, fake, fake) == Bd.KF_ESTATE
+    assert L.kf_serve_step(h, 1, one, 2, fake, fake) == Bd.KF_ESTATE
+    L.kf_destroy(h)
 
 
 def test_null_context(L):
