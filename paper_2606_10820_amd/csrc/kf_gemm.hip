@@ -167,6 +167,38 @@ __device__ inline void rotate8(float (&v)[8], const float2* cs, int dr, int p, i
   }
 }
 
+// A run of len <= 4 consecutive elements starting at p, whose element 0 sits
+// a elements into an aligned group of 4: the widest aligned stores.
+template <typename T>
+__device__ inline void put_run4(T* p, int a, const float* v, int len) {
+  static_assert(kVBlk == 4, "runs of one value block");
+  if constexpr (sizeof(T) == 2) {
+    auto pair = [&](int j) {
+      return (uint32_t)__builtin_bit_cast(uint16_t, (bf16)v[j]) |
+             ((uint32_t)__builtin_bit_cast(uint16_t, (bf16)v[j + 1]) << 16);
+    };
+    if (len == 4) {  // a == 0: one 8-byte store
+      *reinterpret_cast<uint2*>(p) = make_uint2(pair(0), pair(2));
+      return;
+    }
+    for (int j = 0; j < len;) {
+      if (((a + j) & 1) == 0 && j + 1 < len) {
+        *reinterpret_cast<uint32_t*>(p + j) = pair(j);
+        j += 2;
+      } else {
+        p[j] = (bf16)v[j];
+        ++j;
+      }
+    }
+  } else {
+    if (len == 4) {
+      *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+      return;
+    }
+    for (int j = 0; j < len; ++j) p[j] = v[j];
+  }
+}
+
 template <typename T>
 struct EpQKV {
   T* Q;
@@ -196,11 +228,39 @@ struct EpQKV {
     T* base = kv + kg.page_base(g.slot(b), slot) + kg.head_off(layer, which - 1, h);
     if (which == 1) {  // keys: [slot][dh]
       put8(base + (size_t)r0 * kg.dh + e, v);
-    } else {           // values, transposed: [dh][slot]
+    } else {           // values, transposed in 8-slot blocks
 #pragma unroll
-      for (int r = 0; r < 8; ++r) base[(size_t)(e + r) * kPage + r0] = from_f<T>(v[r]);
+      for (int r = 0; r < 8; ++r) base[KfKvGeom::vt_off(slot, e + r, kg.dh)] = from_f<T>(v[r]);
     }
   }
+  // Value tiles (column_tile) are stored by column: v holds rows m..m+7 (those
+  // < M) of value column n.  Rows that are consecutive slots of one sequence
+  // within one value block are one contiguous run, and consecutive lanes hold
+  // consecutive value rows, whose runs are adjacent.
+  __device__ inline bool column_tile(int n0) const { return n0 >= 2 * kg.H * kg.dh; }
+  __device__ inline void store_col8(int m, int n, const float (&v)[8], int M) const {
+    const int c = n - 2 * kg.H * kg.dh, h = c / kg.dh, e = c - h * kg.dh;
+    const unsigned ho = kg.head_off(layer, 1, h);
+    for (int r = 0; r < 8 && m + r < M;) {
+      const int b = (m + r) / g.R, i = (m + r) - b * g.R;
+      const int slot = g.ctx(st, b) + i, a = slot % kVBlk;
+      int len = kVBlk - a;
+      len = len < 8 - r ? len : 8 - r;
+      len = len < M - (m + r) ? len : M - (m + r);
+      len = len < g.R - i ? len : g.R - i;
+      put_run4(kv + kg.page_base(g.slot(b), slot) + ho + KfKvGeom::vt_off(slot, e, kg.dh), a, v + r,
+               len);
+      r += len;
+    }
+  }
+};
+template <typename Ep>
+struct HasColumns {
+  static constexpr bool value = false;
+};
+template <typename T>
+struct HasColumns<EpQKV<T>> {
+  static constexpr bool value = true;
 };
 
 // Second noise-MLP layer: noise row m = (b, j) lands in residual row
@@ -672,9 +732,25 @@ __global__ void __launch_bounds__(256)
           }
       }
       __syncthreads();
+      bool by_column = false;
+      if constexpr (HasColumns<Ep>::value) by_column = ep.column_tile(n0);
 #pragma unroll
       for (int c0 = 0; c0 < MW * CPR; c0 += 256) {
         const int c = c0 + tid;
+        if constexpr (HasColumns<Ep>::value) {
+          if (by_column) {  // 8 consecutive rows of one column per lane
+            static_assert(MW % 8 == 0, "whole 8-row groups per band");
+            if (c0 + 256 <= MW * CPR || c < MW * CPR) {
+              const int cg = c / BN, cl = c % BN;
+              const int m = m0 + pass * MW + cg * 8, n = n0 + cl;
+              float v[8];
+#pragma unroll
+              for (int r = 0; r < 8; ++r) v[r] = stage[(cg * 8 + r) * SROW + cl];
+              if (m < M && n < N) ep.store_col8(m, n, v, M);
+            }
+            continue;
+          }
+        }
         if (c0 + 256 <= MW * CPR || c < MW * CPR) {
           const int rr = c / CPR, cc = c % CPR;
           const int m = m0 + pass * MW + rr, n = n0 + cc * 8;

@@ -44,13 +44,19 @@ struct KfStepGeom {
 
 // Geometry of the KV cache, in pages of kPage = 128 slots of one sequence.  A
 // page holds every layer: [L][2][H][128 * dh] elements, per head the keys
-// [128][dh] (slot-major) and the values [dh][128] (transposed).  Slot s of
+// [128][dh] (slot-major) and the values transposed in blocks of kVBlk = 4
+// slots, [32][dh][4]: the 4 slots of a block are contiguous for each value
+// row, and consecutive value rows of a block are adjacent, so the rows a step
+// appends (positions advance by whole blocks) are written as lane-contiguous
+// runs.  8 consecutive slots of a value row (one P.V operand fragment) are
+// two 4-slot pieces.  Slot s of
 // sequence slot q lives in page ptab[q * (T / 128) + s / 128]; without a page
 // table (lock-step batches) sequence q owns pages q * (T / 128) onwards.  T is
 // the per-sequence capacity rounded up to a whole page.  (128-slot rows of
 // transposed values made the KV append of the QKV epilogue measurably faster
 // than 64-slot rows.)
 constexpr int kPage = 128;
+constexpr int kVBlk = 4;
 struct KfKvGeom {
   int L, H, T, dh;
   const int* ptab = nullptr;  // [slots][T / kPage] page ids, or null
@@ -58,6 +64,10 @@ struct KfKvGeom {
   // Offset of (layer, K or V, head) within a page (a page has < 2^31 elements).
   __host__ __device__ unsigned head_off(int layer, int which, int h) const {
     return (unsigned)(((layer * 2 + which) * H + h) * (kPage * dh));
+  }
+  // Offset of value (slot s, row e) within a head's value blocks.
+  __host__ __device__ static unsigned vt_off(int s, int e, int dh) {
+    return (unsigned)(((s % kPage) / kVBlk) * (dh * kVBlk) + e * kVBlk + (s % kVBlk));
   }
   // First element of the page holding slot s of sequence slot q.
   __device__ inline size_t page_base(int q, int s) const {

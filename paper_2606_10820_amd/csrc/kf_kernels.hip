@@ -136,7 +136,7 @@ __global__ void __launch_bounds__(256)
       float kx = 0.f, vx = 0.f;
       if (slot < nkeys) {
         kx = to_f(Kb[(size_t)(p0 + kk) * DH + e]);
-        vx = to_f(Vb[(size_t)e * kPage + p0 + kk]);
+        vx = to_f(Vb[KfKvGeom::vt_off(p0 + kk, e, DH)]);
       }
       sK[kk][e] = kx;
       sV[kk][e] = vx;
@@ -268,12 +268,16 @@ __global__ void __launch_bounds__(256)
     const int kb = t0 + 8 * gq;
 #pragma unroll
     for (int db = 0; db < NDB; ++db) {
-      const bf16* vp = Vt + (size_t)(db * 16 + lq) * kPage + (kb - pbase);
+      // slots kb..kb+3 and kb+4..kb+7: two value blocks
+      const bf16* vp = Vt + KfKvGeom::vt_off(kb - pbase, db * 16 + lq, DH);
+      const bf16* vq = Vt + KfKvGeom::vt_off(kb + 4 - pbase, db * 16 + lq, DH);
       if (kb + 8 <= nkeys) {
-        f.v[db] = load8(vp);
+        const uint2 lo = *reinterpret_cast<const uint2*>(vp), hi = *reinterpret_cast<const uint2*>(vq);
+        f.v[db] = __builtin_bit_cast(bf16x8_t, make_uint4(lo.x, lo.y, hi.x, hi.y));
       } else {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) f.v[db][e] = (kb + e < nkeys) ? vp[e] : (bf16)0.f;
+        for (int e = 0; e < 8; ++e)
+          f.v[db][e] = (kb + e < nkeys) ? (e < 4 ? vp[e] : vq[e - 4]) : (bf16)0.f;
       }
     }
   };
