@@ -414,13 +414,35 @@ int run_step(kf_ctx* c, const StepIn& in) {
               kf::gemm_noise_out<T>(Hm, W(p.nw2), Mk, d, 4 * d, F(p.nb2), pos, temb, X, Xh, lnst, g,
                                     st, &sws, s));
   }
+  // The teacher pass of a 16-bit model (causal attention over whole sequences,
+  // nothing decoded after it) runs its attention through the block kernel of
+  // the training masks: SingleForward with no noise rows is the causal mask.
+  // Q goes to [B][H][N][d_head] and K, V to two such buffers in the KV cache
+  // memory, which the pass does not otherwise use.
+  const bool seq_attn = in.targets && sizeof(T) == 2;
+  const int H = cf.n_head, dh = d / cf.n_head;
   for (int l = 0; l < cf.n_layer; ++l) {
     const LayerOff& y = p.layer[l];
     const kf::LnFold ln1{F(y.qkv_c1), F(y.qkv_c2), lnst, rms};
     const kf::LnFold ln2{F(y.up_c1), F(y.up_c2), lnst, rms};
-    KF_LAUNCH(c, KF_KC_QKV,
-              kf::gemm_qkv_ln<T>(Xh, ln1, W(y.wqkv), M, d, F(y.bqkv), Q, kv, g, kg, l, st, rope, s));
-    KF_LAUNCH(c, KF_KC_ATTN, kf::launch_attention<T>(Q, kv, O, st, g, kg, l, asp, s));
+    if constexpr (sizeof(T) == 2) {
+      if (seq_attn) {
+        const int n = in.nr;
+        T* Kl = kv;
+        T* Vl = kv + (size_t)in.B * n * d;
+        KF_LAUNCH(c, KF_KC_QKV,
+                  kf::gemm_qkv_seq<T>(Xh, ln1, W(y.wqkv), M, d, F(y.bqkv), Q, Kl, Vl, n, n, 0, H,
+                                      n, 0, 1, rope, s));
+        KF_LAUNCH(c, KF_KC_ATTN,
+                  kf::launch_training_attention_seq(KF_MASK_SINGLE, in.B, H, n, 0, dh, Q, Kl, Vl,
+                                                    n, O, 1.0f / sqrtf((float)dh), s));
+      }
+    }
+    if (!seq_attn) {
+      KF_LAUNCH(c, KF_KC_QKV,
+                kf::gemm_qkv_ln<T>(Xh, ln1, W(y.wqkv), M, d, F(y.bqkv), Q, kv, g, kg, l, st, rope, s));
+      KF_LAUNCH(c, KF_KC_ATTN, kf::launch_attention<T>(Q, kv, O, st, g, kg, l, asp, s));
+    }
     KF_LAUNCH(c, KF_KC_OPROJ, kf::gemm_residual<T>(O, W(y.wo), M, d, d, F(y.bo), X, Xh, lnst, &sws, s));
     KF_LAUNCH(c, KF_KC_MLP_UP, kf::gemm_up_ln<T>(Xh, ln2, W(y.w1), M, f, d, F(y.b1), Hm, s));
     KF_LAUNCH(c, KF_KC_MLP_DOWN, kf::gemm_residual<T>(Hm, W(y.w2), M, d, f, F(y.b2), X, Xh, lnst, &sws, s));

@@ -210,8 +210,8 @@ __device__ inline bf16x8_t load8(const bf16* p) {
   return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(p));
 }
 
-template <int DH>
-__global__ void __launch_bounds__(256)
+template <int DH, int NW = 4>
+__global__ void __launch_bounds__(64 * NW)
     attention_mfma_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ kv,
                           bf16* __restrict__ O, const KfDevState* st, KfStepGeom g, KfKvGeom kg,
                           int layer, float scale, AttnSplit sp) {
@@ -330,20 +330,20 @@ __global__ void __launch_bounds__(256)
   int t0 = ks + w * KT;
   if (t0 < ke) load(t0, fa);
   while (t0 < ke) {  // ping-pong: the next tile loads while this one computes
-    int tn = t0 + 4 * KT;
+    int tn = t0 + NW * KT;
     if (tn < ke) load(tn, fb);
     tile(t0, fa);
     t0 = tn;
     if (t0 >= ke) break;
-    tn = t0 + 4 * KT;
+    tn = t0 + NW * KT;
     if (tn < ke) load(tn, fa);
     tile(t0, fb);
     t0 = tn;
   }
 
-  // merge the four wavefronts' partial states
-  __shared__ float sm[4][QB], sl[4][QB];
-  __shared__ float so[4][QB][DH + 1];
+  // merge the wavefronts' partial states
+  __shared__ float sm[NW][QB], sl[NW][QB];
+  __shared__ float so[NW][QB][DH + 1];
   if (gq == 0) {
     sm[w][lq] = m_run;
     sl[w][lq] = l_run;
@@ -353,15 +353,15 @@ __global__ void __launch_bounds__(256)
 #pragma unroll
     for (int r = 0; r < 4; ++r) so[w][lq][db * 16 + 4 * gq + r] = o[db][r];
   __syncthreads();
-  constexpr int EPT = DH / 16;
-  const int q = threadIdx.x >> 4, e0 = (threadIdx.x & 15) * EPT;
+  constexpr int TPQ = 64 * NW / QB, EPT = DH / TPQ;  // threads per query row, elements each
+  const int q = threadIdx.x / TPQ, e0 = (threadIdx.x % TPQ) * EPT;
   if (q < nq) {
     float M = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) M = fmaxf(M, sm[i][q]);
-    float f[4], den = 0.f;
+    for (int i = 0; i < NW; ++i) M = fmaxf(M, sm[i][q]);
+    float f[NW], den = 0.f;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < NW; ++i) {
       f[i] = (sm[i][q] == -INFINITY) ? 0.f : __expf(sm[i][q] - M);
       den += f[i] * sl[i][q];
     }
@@ -372,7 +372,7 @@ __global__ void __launch_bounds__(256)
       for (int e = 0; e < EPT; ++e) {
         float acc = 0.f;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) acc += f[i] * so[i][q][e0 + e];
+        for (int i = 0; i < NW; ++i) acc += f[i] * so[i][q][e0 + e];
         orow[e] = (bf16)(acc * inv);
       }
     } else {
@@ -386,7 +386,7 @@ __global__ void __launch_bounds__(256)
       for (int e = 0; e < EPT; ++e) {
         float acc = 0.f;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) acc += f[i] * so[i][q][e0 + e];
+        for (int i = 0; i < NW; ++i) acc += f[i] * so[i][q][e0 + e];
         orow[e] = acc;
       }
     }

@@ -183,6 +183,26 @@ def test_rms_rope_teacher_targets():
     assert kf.device_errors() == 0
 
 
+def test_rms_rope_teacher_targets_bf16():
+    """Stage-1 targets on a bf16 rotary model (d_head 128): the teacher pass of
+    a 16-bit model attends through the block kernel of the training masks."""
+    from tests import test_gpu_teacher as T
+    cfg = S.ModelConfig(2, 256, 2, 512, 1024, 128, S.DTYPE_BF16, rms_rope=True)
+    blob = _blob(cfg, 6)
+    B, N = 3, 70
+    tau = [float(np.float32(t)) for t in (0.7, 1.0, 1.6)]
+    tokens, u = T._inputs(cfg, B, N, 26)
+    kf = T._ctx(cfg, blob, B, N)
+    tg = T._run(kf, tokens, tau, u)
+    gl = kf.debug_logits(B * N).cpu().numpy().astype(np.float64)
+    otg, olg = O.teacher_targets(O.Model(blob), tokens, tau, u)
+    rel = T._check_logits(gl, olg.reshape(B * N, -1), TOL[1], "rms/rope bf16 teacher")
+    ex = T._check_gpu_logits(gl, tg.reshape(-1), np.repeat(tau, N), u.reshape(-1),
+                             "rms/rope bf16 teacher")
+    _log(f"rms/rope bf16 teacher: max logit rel err {rel:.2e}; near-boundary rows {ex}")
+    assert kf.device_errors() == 0
+
+
 @pytest.mark.parametrize("cfg", [
     S.ModelConfig(2, 128, 4, 512, 1024, 128, S.DTYPE_BF16, rms_rope=True),
     S.ModelConfig(2, 256, 2, 512, 1024, 128, S.DTYPE_BF16, rms_rope=True),
