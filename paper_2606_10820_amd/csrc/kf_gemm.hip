@@ -948,9 +948,11 @@ hipError_t launch_plain(const GemmA& ga, const T* W, int M, int N, int K, const 
   constexpr int BK = KCH * 16 / (int)sizeof(T);
   const int nk = K / BK;
   int ks = 1;
-  if (ws && ws->part && tiles < 128) {
+  // Long-K grids of up to one workgroup per CU split too (in two): at
+  // M = 512, K = 3072 that measured 8 % faster, reduction included.
+  if (ws && ws->part && (tiles < 128 || (tiles < 256 && nk >= 24))) {
     for (int c : {16, 12, 8, 6, 4, 3, 2}) {
-      if (nk % c == 0 && nk / c >= 2 && tiles * c <= 320 &&
+      if (nk % c == 0 && nk / c >= 2 && tiles * c <= (tiles < 128 ? 320 : 2 * tiles) &&
           (size_t)c * M * N * sizeof(float) <= ws->bytes) {
         ks = c;
         break;
