@@ -283,10 +283,11 @@ def summarize(root: str, write_json: str = None) -> None:
                 pending += b
                 continue
             e = cls.setdefault(c, {"launches": {}, "bytes": {}})
+            split = pending > 0.0  # the reduction of a split-K launch
             e["bytes"][counter] = e["bytes"].get(counter, 0.0) + b + pending
             pending = 0.0
             helper = "attention_combine" in name or "splitk_reduce" in name
-            if not helper:
+            if not helper or split:
                 e["launches"][counter] = e["launches"].get(counter, 0) + 1
     print("\n| class | launches | MB read / launch | MB written / launch |\n|---|---|---|---|")
     out = {}
