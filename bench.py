@@ -116,6 +116,10 @@ def parse():
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the OpenWebText-shaped batch sweep and k comparison")
     ap.add_argument("--sweep-batches", default="1,16,64,256,512")
+    ap.add_argument("--no-large", action="store_true",
+                    help="skip the 24-layer backbone at batch 256")
+    ap.add_argument("--large-only", action="store_true",
+                    help="only the 24-layer backbone at batch 256 (one JSON line)")
     ap.add_argument("--no-serving", action="store_true",
                     help="skip the continuous-batching run")
     ap.add_argument("--serving-only", action="store_true",
@@ -633,6 +637,61 @@ def serving_bench(stream, reps: int = 2):
     return res
 
 
+def large_bench(stream, reps: int = 2):
+    """The 24-layer backbone (d 1024, 16 heads, MLP 4096, vocab 50257, context
+    1024, bf16): 256 sequences, prompt 256 Zipf(1.1) tokens, 768 new tokens at
+    k = 4 (192 passes).  Tokens/s, the step roofline fraction, and the body
+    GEMMs' MFMA rate (algorithmic flops of each class over its HIP-event time;
+    at M = 2048 rows per decode pass these GEMMs are MFMA-bound)."""
+    import torch
+    from paper_2606_10820_amd import binding as Bd
+    w = S.WORKLOADS["large"]
+    cfg = w["cfg"]
+    B, N, k = w["B"], w["N"], w["k"]
+    L = w["L"] - w["L"] % k
+    dev = torch.device("cuda:0")
+    log(f"[bench] large backbone: generating weights ({S.n_params(cfg) / 1e6:.1f} M params)")
+    blob = S.pack_blob(cfg, S.make_weights(cfg, seed=0))
+    kc = Bd.make_config(cfg.n_layer, cfg.d_model, cfg.n_head, cfg.d_mlp, cfg.vocab, cfg.n_ctx,
+                        cfg.dtype, B, k, N, 0)
+    kf = Bd.KForcing(kc, device="cuda:0", stream=stream)
+    kf.load_weights(blob)
+    prompt = torch.as_tensor(S.make_prompts(w["prompts"], 1, B, N, cfg.vocab), device=dev)
+    out = torch.empty((B, L), dtype=torch.int32, device=dev)
+    run = lambda: kf.generate(prompt, L, k, 2, out=out)
+    run()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        run()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) / reps * 1e3
+    kf.set_timing(Bd.KF_TIMING_ALL)
+    run()
+    per = {n: kf.kernel_time(ci)[0] for ci, n in enumerate(CLASSES)}
+    kf.set_timing(0)
+    costs = generate_costs(cfg, B, N, L, k)
+    roof = step_roof_ms(costs, cfg.dtype)
+    gemm = {n: round(costs[n][1] / (per[n] * 1e-3) / 1e12, 1)
+            for n in ("qkv", "oproj", "mlp_up", "mlp_down", "head") if per[n] > 0}
+    fl = sum(costs[n][1] for n in ("qkv", "oproj", "mlp_up", "mlp_down"))
+    tms = sum(per[n] for n in ("qkv", "oproj", "mlp_up", "mlp_down"))
+    res = {"workload": (f"large backbone: {cfg.n_layer} layers, d={cfg.d_model}, {cfg.n_head} heads, "
+                        f"MLP {cfg.d_mlp}, vocab {cfg.vocab}, context {cfg.n_ctx}; batch {B}, "
+                        f"prompt {N}, k={k}, {L} new tokens"),
+           "ms_per_generate": round(ms, 2), "tokens_per_s": round(B * L / (ms * 1e-3), 1),
+           "roofline_ms": round(roof, 3), "roofline_frac": round(roof / ms, 4),
+           "gemm_tflops_by_class": gemm,
+           "body_gemm_tflops": round(fl / (tms * 1e-3) / 1e12, 1),
+           "body_gemm_mfma_frac": round(fl / (tms * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS[cfg.dtype], 4),
+           "kernel_ms_per_generate": {n: round(v, 3) for n, v in per.items()}}
+    log(f"[bench] large backbone: {ms:.1f} ms per generate, {B * L / (ms * 1e-3):,.0f} tokens/s, "
+        f"{roof / ms:.1%} of the step roofline; body GEMMs {res['body_gemm_tflops']} TFLOP/s")
+    del kf
+    torch.cuda.empty_cache()
+    return res
+
+
 def training_attention_bench(reps: int = 10):
     """Block-sparse attention of the training masks (SingleForward M_S and
     DoubleForward M_D, Appendix C.2) at one GPU's share of the paper's
@@ -697,6 +756,11 @@ def main():
         return
     if a.rollout_only:
         print(json.dumps(rollout_bench(max(a.steps, 1))), flush=True)
+        return
+    if a.large_only:
+        st = torch.cuda.Stream(device=torch.device("cuda:0"))
+        torch.cuda.set_stream(st)
+        print(json.dumps(large_bench(st, max(a.steps, 1))), flush=True)
         return
     if a.serving_only:
         st = torch.cuda.Stream(device=torch.device("cuda:0"))
@@ -817,6 +881,9 @@ def main():
 
     if not a.no_sweep:
         res["owt_sweep"] = owt_sweep([int(x) for x in a.sweep_batches.split(",") if x], stream)
+
+    if not a.no_large:
+        res["large_backbone"] = large_bench(stream)
 
     if not a.no_serving:
         res["serving"] = serving_bench(stream)
