@@ -189,8 +189,11 @@ int kf_fill_noise(kf_ctx *ctx, uint64_t seed, int B, int p0, int n, float *out);
  * HIP graph per argument set (default on).  Every launch of a decode block
  * reads the context length from device memory, so a captured block replays
  * unchanged; the instantiated graph is kept on the context until the
- * arguments, the state buffer or the weights change.  Used only on a non-null
- * stream and while kernel timing is off; results are identical either way. */
+ * arguments, the state buffer or the weights change.  kf_serve_step likewise
+ * replays one graph per (sequences, pending count, k), up to 16 of them, with
+ * noise and tokens copied through fixed device buffers around the replay.
+ * Used only on a non-null stream and while kernel timing is off; results are
+ * identical either way. */
 int kf_set_graphs(kf_ctx *ctx, int enable);
 
 /* Host view of the sequence state: committed length C, pending count, B. */

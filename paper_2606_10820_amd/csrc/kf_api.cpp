@@ -32,6 +32,8 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 constexpr int kAttnEntries = 8192;
 // Split-K GEMM workspace (fp32 parts of the plain GEMMs of small steps).
 constexpr size_t kSplitBytes = (size_t)8 << 20;
+// Captured served steps kept per context (one per (sequences, pending, k)).
+constexpr size_t kServeGraphs = 16;
 // Rows per sampling-head chunk of kf_teacher_targets: the head partials of a
 // chunk take rows * (Vpad / 128) * 36 bytes (about 116 MB at vocabulary 50257).
 constexpr int kTeacherChunk = 8192;
@@ -63,6 +65,7 @@ struct Plan {
   size_t kv = 0, kv_bytes = 0;
   size_t meta = 0;      // continuous batching: slot map [max_batch], committed lengths
                         // [max_batch], page table [max_batch][npp] (int32)
+  size_t serve_noise = 0, serve_out = 0;  // fixed [max_batch][max_k] buffers of graph-replayed steps
   size_t X = 0, Xh = 0, lnst = 0, A = 0, Q = 0, O = 0, Hm = 0, noise = 0, pval = 0, pidx = 0;
   size_t logits = 0, dstate = 0, pend = 0;
   int teacher_rows = 0;                    // rows per sampling-head chunk (KF_FLAG_TEACHER)
@@ -185,7 +188,11 @@ void make_plan(const kf_config& c, Plan& p) {
   p.n_pages = c.kv_pages > 0 ? c.kv_pages : c.max_batch * p.npp;
   p.kv_bytes = (size_t)p.n_pages * p.page_bytes;
   p.kv = take(p.kv_bytes);
-  if (c.flags & KF_FLAG_SERVING) p.meta = take((size_t)c.max_batch * (2 + p.npp) * 4);
+  if (c.flags & KF_FLAG_SERVING) {
+    p.meta = take((size_t)c.max_batch * (2 + p.npp) * 4);
+    p.serve_noise = take((size_t)c.max_batch * c.max_k * 4);
+    p.serve_out = take((size_t)c.max_batch * c.max_k * 4);
+  }
   const size_t R = p.rows_max, Hw = f > 4 * d ? f : 4 * d;
   p.X = take(R * d * 4);
   p.temb = (c.flags & KF_FLAG_TEMPERATURE) ? take((size_t)c.max_batch * d * es) : 0;
@@ -245,6 +252,12 @@ struct kf_ctx {
   std::vector<int> free_pages;  // stack of unused page ids
   int serving = 0;              // live slots
   std::vector<int> map_dev;     // the slot map last written to the device
+  // captured served steps, by (sequences, pending rows, noise rows); most recent last
+  struct ServeGraph {
+    int n, nr, k;
+    hipGraphExec_t exec;
+  };
+  std::vector<ServeGraph> sgraphs;
   int last_head_rows = 0;
   bool last_logits = false;
   std::string err;
@@ -664,6 +677,11 @@ void drop_graph(kf_ctx* c) {
   c->gexec = nullptr;
 }
 
+void drop_serve_graphs(kf_ctx* c) {
+  for (auto& g : c->sgraphs) (void)hipGraphExecDestroy(g.exec);
+  c->sgraphs.clear();
+}
+
 // Run `count` identical steps and advance the host view of C by `adv` after
 // each.  Every launch of such a step reads C from device memory, so one
 // captured step replays unchanged; the instantiated graph is cached on the
@@ -870,6 +888,7 @@ int kf_create(const kf_config* cfg, void* hip_stream, kf_ctx** out) {
 void kf_destroy(kf_ctx* c) {
   if (!c) return;
   drop_graph(c);
+  drop_serve_graphs(c);
   for (auto& e : c->evs) {
     (void)hipEventDestroy(e.a);
     (void)hipEventDestroy(e.b);
@@ -884,6 +903,7 @@ int kf_bind_state(kf_ctx* c, void* dev_ptr, size_t bytes) {
   if (bytes < c->plan.total)
     return fail(c, KF_ENOMEM, "state buffer has %zu bytes, %zu needed", bytes, c->plan.total);
   drop_graph(c);
+  drop_serve_graphs(c);
   c->base = static_cast<char*>(dev_ptr);
   c->bytes = bytes;
   c->weights = false;
@@ -1219,7 +1239,10 @@ int kf_device_errors(kf_ctx* c, int* flags) {
 int kf_set_graphs(kf_ctx* c, int enable) {
   if (!c) return KF_EINVAL;
   c->graphs = enable != 0;
-  if (!c->graphs) drop_graph(c);
+  if (!c->graphs) {
+    drop_graph(c);
+    drop_serve_graphs(c);
+  }
   return KF_OK;
 }
 
@@ -1370,10 +1393,55 @@ int kf_serve_step(kf_ctx* c, int n, const int32_t* slots, int k, const float* no
   }
   if (int r = temp_ready(c, top)) return r;
   if (int r = serve_prepare(c, n, slots, upto)) return r;
-  StepIn in{n, nr, k, pend_ptr(c), cf.max_k, noise, nullptr, 0, out_desc(c, out, k, -1), false};
+  // On a real stream with timing off, the step replays a graph captured for
+  // (n, nr, k): every launch reads the slot map, the committed lengths, the
+  // page table and the pending tokens from device memory, and noise and tokens
+  // pass through fixed buffers, copied in and out around the replay.
+  const bool replay = c->graphs && c->stream != nullptr && !c->timing;
+  float* sn = replay ? reinterpret_cast<float*>(c->base + c->plan.serve_noise) : nullptr;
+  int32_t* so = replay ? reinterpret_cast<int32_t*>(c->base + c->plan.serve_out) : nullptr;
+  StepIn in{n, nr, k, pend_ptr(c), cf.max_k, replay ? sn : noise, nullptr, 0,
+            out_desc(c, replay ? so : out, k, -1), false};
   in.serve = true;
   in.toks_by_slot = true;
-  if (int r = step(c, in)) return r;
+  if (!replay) {
+    if (int r = step(c, in)) return r;
+  } else {
+    const size_t bytes = (size_t)n * k * 4;
+    KF_HIP(c, hipMemcpyAsync(sn, noise, bytes, hipMemcpyDeviceToDevice, c->stream));
+    hipGraphExec_t exec = nullptr;
+    for (size_t i = 0; i < c->sgraphs.size(); ++i)
+      if (c->sgraphs[i].n == n && c->sgraphs[i].nr == nr && c->sgraphs[i].k == k) {
+        kf_ctx::ServeGraph g = c->sgraphs[i];
+        c->sgraphs.erase(c->sgraphs.begin() + i);
+        c->sgraphs.push_back(g);
+        exec = g.exec;
+        break;
+      }
+    if (!exec) {
+      KF_HIP(c, hipStreamBeginCapture(c->stream, hipStreamCaptureModeRelaxed));
+      int r = step(c, in);
+      hipGraph_t gr = nullptr;
+      hipError_t e = hipStreamEndCapture(c->stream, &gr);
+      if (r) {
+        if (e == hipSuccess && gr) (void)hipGraphDestroy(gr);
+        return r;
+      }
+      if (e != hipSuccess) return hip_fail(c, e, "hipStreamEndCapture");
+      e = hipGraphInstantiate(&exec, gr, nullptr, nullptr, 0);
+      (void)hipGraphDestroy(gr);
+      if (e != hipSuccess) return hip_fail(c, e, "hipGraphInstantiate");
+      if (c->sgraphs.size() == kServeGraphs) {
+        (void)hipGraphExecDestroy(c->sgraphs.front().exec);
+        c->sgraphs.erase(c->sgraphs.begin());
+      }
+      c->sgraphs.push_back({n, nr, k, exec});
+    }
+    KF_HIP(c, hipGraphLaunch(exec, c->stream));
+    KF_HIP(c, hipMemcpyAsync(out, so, bytes, hipMemcpyDeviceToDevice, c->stream));
+    c->last_head_rows = n * k;  // as the step itself records
+    c->last_logits = (cf.flags & KF_FLAG_DEBUG_LOGITS) != 0;
+  }
   for (int b = 0; b < n; ++b) {
     kf_ctx::Slot& sl = c->slots[slots[b]];
     sl.C += sl.pending;

@@ -217,3 +217,46 @@ def test_serving_lm1b_bf16():
         sv.rng.shuffle(order)
         sv.step(order, 4)
     _log(f"serving lm1b bf16: {merge(sv.stats)}")
+
+
+def test_serving_graph_replay_matches_direct():
+    """On a real stream, served steps replay one captured graph per (sequences,
+    pending count, k); tokens and logits equal the direct launches through a
+    churn of admissions, steps in changing orders and releases."""
+    from paper_2606_10820_amd import binding as Bd
+    cfg = S.ModelConfig(2, 128, 4, 512, 1024, 256, S.DTYPE_BF16)
+    blob = S.pack_blob(cfg, S.make_weights(cfg, seed=7, random_affine=True))
+    stream = torch.cuda.Stream()
+    res = {}
+    with torch.cuda.stream(stream):
+        for graphs in (False, True):
+            c = Bd.make_config(cfg.n_layer, cfg.d_model, cfg.n_head, cfg.d_mlp, cfg.vocab,
+                               cfg.n_ctx, cfg.dtype, 6, 4, 40,
+                               Bd.KF_FLAG_DEBUG_LOGITS | Bd.KF_FLAG_SERVING)
+            kf = Bd.KForcing(c, stream=stream)
+            kf.load_weights(blob)
+            kf.set_graphs(graphs)
+            rng = np.random.default_rng(3)
+            outs = []
+
+            def step(slots, k):
+                u = rng.random((len(slots), k)).astype(np.float32)
+                outs.append(kf.serve_step(slots, u).cpu().numpy())
+                outs.append(kf.debug_logits(len(slots) * k).cpu().numpy())
+
+            kf.serve_admit([0, 3], rng.integers(0, cfg.vocab, (2, 30)).astype(np.int32), 4,
+                           rng.random((2, 4)).astype(np.float32))
+            for it in range(5):
+                step([0, 3] if it % 2 else [3, 0], 4)
+            kf.serve_admit([5], rng.integers(0, cfg.vocab, (1, 12)).astype(np.int32), 4,
+                           rng.random((1, 4)).astype(np.float32))
+            for it in range(4):
+                step([5, 0, 3], 4)
+            kf.serve_release([0])
+            for it in range(3):
+                step([3, 5], 4)
+            stream.synchronize()
+            res[graphs] = outs
+    assert len(res[False]) == len(res[True])
+    for a, b in zip(res[False], res[True]):
+        np.testing.assert_array_equal(a, b)
