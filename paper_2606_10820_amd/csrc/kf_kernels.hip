@@ -188,16 +188,18 @@ __global__ void __launch_bounds__(256)
 }
 
 // Block attention on MFMA (bf16).  One workgroup per (sequence, head, block of
-// 16 query rows, key split); its four wavefronts take 32-key tiles of the
-// split's key range round-robin and merge their online-softmax states through
-// LDS at the end.
+// 16 query rows, key split); its NW wavefronts (four in the library: measured
+// best from 64 keys up, and within 6 % of two waves at 16 keys) take 32-key
+// tiles of the split's key range round-robin and merge their online-softmax
+// states through LDS at the end.
 //   S^T = K Q^T   with v_mfma_f32_16x16x32_bf16: A = 16 keys x 32 d_head,
 //                 B = 32 d_head x 16 queries.  MFMA row i of key group grp is
 //                 key 8*(i/4) + 4*grp + i%4 of the tile, so the output rows a
 //                 lane holds (4 per group, 2 groups) are 8 consecutive keys.
 //   O^T += V^T P^T  A = 16 d_head x 32 keys read straight from the transposed
-//                 value cache (8 consecutive slots = one 16-byte load), B = the
-//                 lane's own 8 probabilities -- no data exchange between lanes.
+//                 value blocks (8 consecutive slots of a value row = two 8-byte
+//                 loads), B = the lane's own 8 probabilities -- no data
+//                 exchange between lanes.
 // Each wavefront loads the K and V fragments of its next tile before working
 // on the current one.  With ns > 1 key splits (grids too small to fill the
 // chip), every split writes its unnormalised state (max m, sum l, o) for the

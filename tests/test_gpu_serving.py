@@ -219,6 +219,23 @@ def test_serving_lm1b_bf16():
     _log(f"serving lm1b bf16: {merge(sv.stats)}")
 
 
+def test_serving_bf16_dh128_pages():
+    """bf16 model with d_head 128 (MFMA attention at its widest head, value
+    blocks of 128 rows): sequences cross a page boundary (position 128) while
+    slots are stepped in changing orders."""
+    cfg = S.ModelConfig(2, 256, 2, 512, 1024, 256, S.DTYPE_BF16)
+    blob = S.pack_blob(cfg, S.make_weights(cfg, seed=8, random_affine=True))
+    kf = _ctx(cfg, blob, 4, 4, 120)
+    sv = Served(kf, O.Model(blob), TOL[1], np.random.default_rng(15))
+    sv.admit([2, 0], 110, 4, cfg.vocab)
+    sv.admit([3], 9, 4, cfg.vocab)
+    for it in range(6):
+        sv.step([0, 2] if it % 2 else [2, 0], 4)
+    assert sv.C[0] > 128 and sv.C[2] > 128
+    sv.step([3], 4)
+    _log(f"serving bf16 d_head 128: {merge(sv.stats)}")
+
+
 def test_serving_graph_replay_matches_direct():
     """On a real stream, served steps replay one captured graph per (sequences,
     pending count, k); tokens and logits equal the direct launches through a
