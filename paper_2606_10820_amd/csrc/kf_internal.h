@@ -48,13 +48,12 @@ struct KfStepGeom {
 // slots, [32][dh][4]: the 4 slots of a block are contiguous for each value
 // row, and consecutive value rows of a block are adjacent, so the rows a step
 // appends (positions advance by whole blocks) are written as lane-contiguous
-// runs.  8 consecutive slots of a value row (one P.V operand fragment) are
-// two 4-slot pieces.  Slot s of
-// sequence slot q lives in page ptab[q * (T / 128) + s / 128]; without a page
-// table (lock-step batches) sequence q owns pages q * (T / 128) onwards.  T is
-// the per-sequence capacity rounded up to a whole page.  (128-slot rows of
-// transposed values made the KV append of the QKV epilogue measurably faster
-// than 64-slot rows.)
+// runs; 8 consecutive slots of a value row (one P.V operand fragment) are two
+// 4-slot pieces.  Slot s of sequence slot q lives in page
+// ptab[q * (T / 128) + s / 128]; without a page table (lock-step batches)
+// sequence q owns pages q * (T / 128) onwards.  T is the per-sequence capacity
+// rounded up to a whole page.  (Pages of 128 rather than 64 slots measured
+// faster in the QKV epilogue's KV append.)
 constexpr int kPage = 128;
 constexpr int kVBlk = 4;
 struct KfKvGeom {
