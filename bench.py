@@ -187,13 +187,19 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_lm1b_b64_k4.json")
 
 
 def kernel_source_hash() -> str:
-    """sha256 over the library's kernel sources: counter figures taken from an
-    older build are not reported."""
+    """sha256 over the library's sources with comments and whitespace removed:
+    counter figures taken from different code are not reported (an edit of a
+    comment does not change the kernels)."""
     import hashlib
+    import re
     h = hashlib.sha256()
     for fn in sorted(os.listdir(KERNEL_SOURCES)):
-        with open(os.path.join(KERNEL_SOURCES, fn), "rb") as f:
-            h.update(fn.encode() + b"\0" + f.read())
+        with open(os.path.join(KERNEL_SOURCES, fn), encoding="utf-8") as f:
+            src = f.read()
+        src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+        src = re.sub(r"//[^\n]*", " ", src)
+        src = " ".join(src.split())
+        h.update(fn.encode() + b"\0" + src.encode())
     return h.hexdigest()
 
 
