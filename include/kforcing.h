@@ -40,7 +40,9 @@ extern "C" {
 #define KF_EINVAL (-1) /* bad argument: k < 1, k > max_k, B out of range, null pointer, L % k != 0 ... */
 #define KF_ESTATE (-2) /* no state bound, no weights loaded, decode before prefill, B mismatch */
 #define KF_ECTX (-3)   /* the step would run past n_ctx positions */
-#define KF_ENOMEM (-4) /* the bound state buffer is smaller than kf_state_bytes() */
+#define KF_ENOMEM (-4) /* out of memory: the bound state buffer is smaller than
+                          * kf_state_bytes(), the serving KV page pool cannot cover
+                          * a call, or kf_create could not allocate the context */
 #define KF_EHIP (-5)   /* a HIP runtime call failed (message from hipGetErrorString) */
 
 /* ---------------------------------------------------------- configuration */

@@ -857,7 +857,7 @@ const char* kf_strerror(int code) {
     case KF_EINVAL: return "invalid argument";
     case KF_ESTATE: return "invalid state";
     case KF_ECTX: return "context length exceeded";
-    case KF_ENOMEM: return "state buffer too small";
+    case KF_ENOMEM: return "out of memory (state buffer or KV page pool)";
     case KF_EHIP: return "HIP runtime error";
     default: return "unknown error";
   }
