@@ -704,7 +704,9 @@ def training_attention_bench(reps: int = 10):
     training batch (global batch 512 over 8 GPUs: 64 sequences; 12 heads,
     d_head 64, k = 4) for the OWT (N = 1024) and LM1B (N = 128) sequence
     lengths.  Inputs are seeded N(0, 1) bf16 tensors.  Work counted: 4 d_head
-    flops per visible (query, key) pair, against the bf16 MFMA peak."""
+    flops per visible (query, key) pair, against the bf16 MFMA peak; bytes:
+    Q, K, V read and O written once, against the HBM peak.  The roofline time
+    is the larger of the two."""
     import torch
     from paper_2606_10820_amd import binding as Bd
     dev = torch.device("cuda:0")
@@ -729,17 +731,26 @@ def training_attention_bench(reps: int = 10):
             torch.cuda.synchronize()
             ms = e0.elapsed_time(e1) / reps
             ent = Bd.training_attention_entries(mask, N, k)
-            tf = 4.0 * ent * dh * B * H / (ms * 1e-3) / 1e12
+            fl = 4.0 * ent * dh * B * H
+            tf = fl / (ms * 1e-3) / 1e12
+            by = 2.0 * B * H * dh * (2 * rows + 2 * keys)
+            t_mem, t_fl = by / (PEAK_HBM_GBS * 1e9) * 1e3, fl / (peak * 1e12) * 1e3
+            roof = max(t_mem, t_fl)
             cases.append({"workload": f"{name} training share: B={B}, H={H}, N={N}, k={k}, d_head={dh}",
                           "mask": mname, "ms": round(ms, 4), "tflops": round(tf, 1),
-                          "frac": round(tf / peak, 4), "visible_pairs_per_head": ent,
+                          "frac": round(tf / peak, 4), "hbm_bytes": by,
+                          "gbs": round(by / (ms * 1e-3) / 1e9, 1),
+                          "roofline_ms": round(roof, 4), "bound": "hbm" if t_mem >= t_fl else "mfma",
+                          "roofline_frac": round(roof / ms, 4), "visible_pairs_per_head": ent,
                           "dense_pairs_per_head": rows * keys})
             log(f"[bench] training attention {name} {mname}: {ms:.3f} ms, {tf:.1f} TFLOP/s "
-                f"({tf / peak:.1%} of bf16 MFMA peak)")
+                f"({tf / peak:.1%} of bf16 MFMA peak), {by / (ms * 1e-3) / 1e9:.0f} GB/s; "
+                f"{roof / ms:.1%} of its roofline ({'HBM' if t_mem >= t_fl else 'MFMA'}-bound)")
             del q, kk, v, out
     torch.cuda.empty_cache()
-    return {"kernel": "kf_training_attention", "peak_tflops": peak,
-            "work": "4 * d_head flops per visible (query, key) pair", "cases": cases}
+    return {"kernel": "kf_training_attention", "peak_tflops": peak, "peak_gbs": PEAK_HBM_GBS,
+            "work": "4 * d_head flops per visible (query, key) pair; Q, K, V, O once each",
+            "cases": cases}
 
 
 def main():
