@@ -42,7 +42,9 @@ namespace kf {
 namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
 
 constexpr int kQB = 64;  // query rows per workgroup
 constexpr int kKT = 64;  // keys per tile
@@ -60,13 +62,19 @@ __device__ inline Intervals no_intervals() {
   return v;
 }
 
-__device__ inline Intervals row_intervals(int mask, int N, int k, int row) {
+// q / k for 0 <= q with q * k < 2^32, from km = ceil(2^32 / k) (km = 0 for
+// k = 1): the rounded-up reciprocal errs by less than one in q / k there.
+__device__ inline int div_k(int q, uint32_t km) {
+  return km ? (int)__umulhi((uint32_t)q, km) : q;
+}
+
+__device__ inline Intervals row_intervals(int mask, int N, int k, uint32_t km, int row) {
   Intervals v = no_intervals();
   if (mask == KF_MASK_SINGLE) {
     if (row < N) {
       v.hi[0] = row + 1;
     } else {
-      const int q = row - N, t = q / k, j = q - t * k;
+      const int q = row - N, t = div_k(q, km), j = q - t * k;
       v.hi[0] = t + 1;
       v.lo[1] = N + t * k;
       v.hi[1] = N + t * k + j + 1;
@@ -74,7 +82,7 @@ __device__ inline Intervals row_intervals(int mask, int N, int k, int row) {
   } else {
     const int nk1 = N * k;
     const bool f2 = row >= nk1;
-    const int q = f2 ? row - nk1 : row, t = q / k, j = q - t * k;
+    const int q = f2 ? row - nk1 : row, t = div_k(q, km), j = q - t * k;
     v.hi[0] = t + 1;
     v.lo[1] = N + t * k;
     v.hi[1] = f2 ? N + (t + 1) * k : N + t * k + j + 1;
@@ -92,7 +100,7 @@ __device__ inline Intervals row_intervals(int mask, int N, int k, int row) {
 // non-decreasing function of the row and a region is either empty for all
 // rows of the part or for none, so the first and last row of each part
 // decide.  An empty union is [0, 0); an empty intersection has ilo > ihi.
-__device__ inline void row_bounds(int mask, int N, int k, int a, int b, int (&ulo)[3],
+__device__ inline void row_bounds(int mask, int N, int k, uint32_t km, int a, int b, int (&ulo)[3],
                                   int (&uhi)[3], int (&ilo)[3], int (&ihi)[3]) {
   const int split = mask == KF_MASK_SINGLE ? N : N * k;
 #pragma unroll
@@ -106,8 +114,8 @@ __device__ inline void row_bounds(int mask, int N, int k, int a, int b, int (&ul
 #pragma unroll
   for (int part = 0; part < 2; ++part) {
     if (pa[part] >= pb[part]) continue;
-    const Intervals f = row_intervals(mask, N, k, pa[part]);
-    const Intervals l = row_intervals(mask, N, k, pb[part] - 1);
+    const Intervals f = row_intervals(mask, N, k, km, pa[part]);
+    const Intervals l = row_intervals(mask, N, k, km, pb[part] - 1);
 #pragma unroll
     for (int s = 0; s < 3; ++s) {
       if (f.lo[s] < f.hi[s]) {
@@ -140,13 +148,19 @@ __device__ inline void static_for(F&& f) {
 
 // Cross-lane reductions over the four 16-lane groups (lanes l, l^16, l^32, l^48)
 // with the gfx950 permlane swaps (VALU, no LDS traffic).
+// (scores are finite or -inf, so no NaN-quieting copies: plain v_max_f32)
+__device__ inline float max2(float a, float b) {
+  float r;
+  asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
 __device__ inline float max_xor16(float x) {
   const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  return max2(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 __device__ inline float max_xor32(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  return max2(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 // max of three without the NaN-quieting copies that fmaxf adds (scores are
 // finite or -inf here)
@@ -194,12 +208,12 @@ struct Item {
 
 // Item t of the (head, query block) list: head t / nqb, its blocks heaviest
 // (latest rows) first.
-__device__ inline Item make_item(int t, int nqb, int mask, int N, int k, int nq) {
+__device__ inline Item make_item(int t, int nqb, int mask, int N, int k, uint32_t km, int nq) {
   Item it;
   it.bh = t / nqb;
   it.q0 = (nqb - 1 - (t - it.bh * nqb)) * kQB;
   int lo[3], hi[3], ilo[3], ihi[3], nt[3];
-  row_bounds(mask, N, k, it.q0, min(it.q0 + kQB, nq), lo, hi, ilo, ihi);
+  row_bounds(mask, N, k, km, it.q0, min(it.q0 + kQB, nq), lo, hi, ilo, ihi);
 #pragma unroll
   for (int s = 0; s < 3; ++s) nt[s] = (hi[s] - lo[s] + kKT - 1) / kKT;
   it.ntiles = nt[0] + nt[1] + nt[2];
@@ -218,7 +232,8 @@ template <int DH, int S>
 __global__ void __launch_bounds__(256)
     training_attention_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
                               const bf16* __restrict__ V, bf16* __restrict__ O, int mask, int N,
-                              int k, int nq, int ldk, int H, int BH, int o_inter, float c2) {
+                              int k, uint32_t km, int nq, int ldk, int H, int BH, int o_inter,
+                              float c2) {
   using G = Geo<DH, S>;
   constexpr int NDC = DH / 32, NDB = DH / 16;
   __shared__ __attribute__((aligned(1024))) unsigned char smem[S * G::STAGEB];
@@ -229,7 +244,7 @@ __global__ void __launch_bounds__(256)
   // head share its keys and values through that XCD's L2.
   const int nqb = (nq + kQB - 1) / kQB, total = BH * nqb;
   const int x8 = blockIdx.x & 7, j8 = blockIdx.x >> 3;
-  const Item C = make_item(x8 * (total >> 3) + min(x8, total & 7) + j8, nqb, mask, N, k, nq);
+  const Item C = make_item(x8 * (total >> 3) + min(x8, total & 7) + j8, nqb, mask, N, k, km, nq);
   const int tid = threadIdx.x, lane = tid & 63, gq = lane >> 4, lq = lane & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
 
@@ -290,8 +305,8 @@ __global__ void __launch_bounds__(256)
   }
   int wlo[3] = {0, 0, 0}, whi[3] = {0, 0, 0}, ilo[3] = {1, 1, 1}, ihi[3] = {0, 0, 0};
   if (C.q0 + 16 * w < nq)
-    row_bounds(mask, N, k, C.q0 + 16 * w, min(C.q0 + 16 * w + 16, nq), wlo, whi, ilo, ihi);
-  const Intervals iv = valid ? row_intervals(mask, N, k, row) : no_intervals();
+    row_bounds(mask, N, k, km, C.q0 + 16 * w, min(C.q0 + 16 * w + 16, nq), wlo, whi, ilo, ihi);
+  const Intervals iv = valid ? row_intervals(mask, N, k, km, row) : no_intervals();
   // running max m (log2 units); o = the unnormalised O^T; ls = the row sums of
   // P, formed by the MFMA against a block of ones (each element of ls is the
   // sum of this lane's query row over the bf16 probabilities that o uses)
@@ -399,20 +414,17 @@ __global__ void __launch_bounds__(256)
 
   // lane: query lq, d_head 16db + 4gq + r
   if (valid) {
-    const float inv = 1.0f / ls[0];
+    const float inv = __builtin_amdgcn_rcpf(ls[0]);  // ls >= 1: the row maximum's term
     // O: [B][H][nq][DH], or [B][nq][H][DH] (rows of a residual stream) with o_inter
     const int ob = C.bh / H, oh = C.bh - ob * H;
     bf16* orow = O + (o_inter ? (((size_t)ob * nq + row) * H + oh) * DH
                               : ((size_t)C.bh * nq + row) * DH) + 4 * gq;
 #pragma unroll
     for (int db = 0; db < NDB; ++db) {
-      const bf16 e0 = (bf16)(o[db][0] * inv), e1 = (bf16)(o[db][1] * inv);
-      const bf16 e2 = (bf16)(o[db][2] * inv), e3 = (bf16)(o[db][3] * inv);
-      const uint32_t w0 = (uint32_t)__builtin_bit_cast(uint16_t, e0) |
-                          ((uint32_t)__builtin_bit_cast(uint16_t, e1) << 16);
-      const uint32_t w1 = (uint32_t)__builtin_bit_cast(uint16_t, e2) |
-                          ((uint32_t)__builtin_bit_cast(uint16_t, e3) << 16);
-      *reinterpret_cast<uint2*>(orow + 16 * db) = make_uint2(w0, w1);
+      const f32x2_t lo = {o[db][0] * inv, o[db][1] * inv}, hi = {o[db][2] * inv, o[db][3] * inv};
+      *reinterpret_cast<uint2*>(orow + 16 * db) =
+          make_uint2(__builtin_bit_cast(uint32_t, __builtin_convertvector(lo, bf16x2_t)),
+                     __builtin_bit_cast(uint32_t, __builtin_convertvector(hi, bf16x2_t)));
     }
   }
 }
@@ -435,8 +447,11 @@ hipError_t launch_ta(int mask, int B, int H, int N, int k, const bf16* Q, const 
   const int BH = B * H;
   const dim3 grid((unsigned)((long long)BH * ((nq + kQB - 1) / kQB)));  // one workgroup per item
   const float c2 = scale * 1.4426950408889634f;  // scale * log2(e)
-  launch(training_attention_kernel<DH, S>, grid, dim3(256), 0, s, Q, K, V, O, mask, N, k, nq, ldk,
-         H, BH, o_inter, c2);
+  // q / k in the kernel by the rounded-up reciprocal: exact while q * k < 2^32
+  if ((long long)nq * (k > 1 ? k : 1) >= (1LL << 32)) return hipErrorInvalidValue;
+  const uint32_t km = k > 1 ? (uint32_t)(((1ULL << 32) + k - 1) / k) : 0u;
+  launch(training_attention_kernel<DH, S>, grid, dim3(256), 0, s, Q, K, V, O, mask, N, k, km, nq,
+         ldk, H, BH, o_inter, c2);
   return hipGetLastError();
 }
 

@@ -53,8 +53,9 @@ def _check(got, ref, where):
 
 
 # (mask, B, H, N, k, d_head, std): ragged row counts (not multiples of the
-# 64-row workgroup), k = 1 (one token per group), N = 1, every d_head, and
-# peaked softmax rows (std 2: scores ~ N(0, 16))
+# 64-row workgroup), k = 1 (one token per group), odd k = 5 (the kernel's
+# division of row indices by k), N = 1, every d_head, and peaked softmax rows
+# (std 2: scores ~ N(0, 16))
 CASES = [
     (0, 2, 3, 37, 3, 64, 1.0),
     (1, 2, 3, 37, 3, 64, 1.0),
@@ -68,6 +69,10 @@ CASES = [
     (1, 1, 3, 129, 2, 64, 2.0),
     (0, 1, 1, 200, 4, 64, 1.0),
     (1, 1, 1, 200, 4, 64, 1.0),
+    (0, 1, 2, 70, 5, 64, 1.0),
+    (1, 1, 2, 70, 5, 64, 1.0),
+    (0, 1, 2, 90, 1, 64, 1.0),
+    (1, 1, 2, 90, 1, 64, 1.0),
 ]
 
 
