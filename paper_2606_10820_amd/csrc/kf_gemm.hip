@@ -90,6 +90,24 @@ __device__ inline void put8(T* p, const float (&v)[8]) {
   }
 }
 
+// put8 for the KV append: a nontemporal store (the cache is streamed, not
+// reused from the caches; see the decode attention's loads).
+typedef unsigned int u32x4s_t __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2s_t __attribute__((ext_vector_type(2)));
+template <typename T>
+__device__ inline void put8_stream(T* p, const float (&v)[8]) {
+  if constexpr (sizeof(T) == 2) {
+    u32x4s_t w;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      w[i] = (uint32_t)__builtin_bit_cast(uint16_t, (bf16)v[2 * i]) |
+             ((uint32_t)__builtin_bit_cast(uint16_t, (bf16)v[2 * i + 1]) << 16);
+    __builtin_nontemporal_store(w, reinterpret_cast<u32x4s_t*>(p));
+  } else {
+    put8(p, v);
+  }
+}
+
 template <typename T>
 __device__ inline void get8(const T* p, float (&v)[8]) {
   if constexpr (sizeof(T) == 2) {
@@ -177,8 +195,9 @@ __device__ inline void put_run4(T* p, int a, const float* v, int len) {
       return (uint32_t)__builtin_bit_cast(uint16_t, (bf16)v[j]) |
              ((uint32_t)__builtin_bit_cast(uint16_t, (bf16)v[j + 1]) << 16);
     };
-    if (len == 4) {  // a == 0: one 8-byte store
-      *reinterpret_cast<uint2*>(p) = make_uint2(pair(0), pair(2));
+    if (len == 4) {  // a == 0: one 8-byte store, nontemporal (see put8_stream)
+      const u32x2s_t w = {pair(0), pair(2)};
+      __builtin_nontemporal_store(w, reinterpret_cast<u32x2s_t*>(p));
       return;
     }
     for (int j = 0; j < len;) {
@@ -227,7 +246,7 @@ struct EpQKV {
     const int h = c / kg.dh, e = c - h * kg.dh, r0 = (unsigned)slot % kPage;
     T* base = kv + kg.page_base(g.slot(b), slot) + kg.head_off(layer, which - 1, h);
     if (which == 1) {  // keys: [slot][dh]
-      put8(base + (size_t)r0 * kg.dh + e, v);
+      put8_stream(base + (size_t)r0 * kg.dh + e, v);
     } else {           // values, transposed in 8-slot blocks
 #pragma unroll
       for (int r = 0; r < 8; ++r) base[KfKvGeom::vt_off(slot, e + r, kg.dh)] = from_f<T>(v[r]);

@@ -207,9 +207,22 @@ __global__ void __launch_bounds__(256)
 // context length, so a captured step replays unchanged as C grows.
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 
 __device__ inline bf16x8_t load8(const bf16* p) {
   return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(p));
+}
+// KV-cache reads are nontemporal: a decode pass streams every sequence's cache
+// once, and keeping it from displacing other lines leaves the weights
+// resident in the last-level cache from one pass to the next (measured 5 %
+// faster per generate at both decode workloads).
+__device__ inline bf16x8_t load8_stream(const bf16* p) {
+  return __builtin_bit_cast(bf16x8_t, __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p)));
+}
+__device__ inline uint2 load4_stream(const bf16* p) {
+  const u32x2_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(p));
+  return make_uint2(v.x, v.y);
 }
 
 template <int DH, int NW = 4>
@@ -263,7 +276,7 @@ __global__ void __launch_bounds__(64 * NW)
       const int kc = (key < nkeys ? key : nkeys - 1) - pbase;
 #pragma unroll
       for (int c = 0; c < NDC; ++c) {
-        const bf16x8_t x = load8(Kb + (size_t)kc * DH + c * 32 + 8 * gq);
+        const bf16x8_t x = load8_stream(Kb + (size_t)kc * DH + c * 32 + 8 * gq);
         f.k[grp][c] = key < nkeys ? x : zero8;
       }
     }
@@ -274,7 +287,7 @@ __global__ void __launch_bounds__(64 * NW)
       const bf16* vp = Vt + KfKvGeom::vt_off(kb - pbase, db * 16 + lq, DH);
       const bf16* vq = Vt + KfKvGeom::vt_off(kb + 4 - pbase, db * 16 + lq, DH);
       if (kb + 8 <= nkeys) {
-        const uint2 lo = *reinterpret_cast<const uint2*>(vp), hi = *reinterpret_cast<const uint2*>(vq);
+        const uint2 lo = load4_stream(vp), hi = load4_stream(vq);
         f.v[db] = __builtin_bit_cast(bf16x8_t, make_uint4(lo.x, lo.y, hi.x, hi.y));
       } else {
 #pragma unroll
