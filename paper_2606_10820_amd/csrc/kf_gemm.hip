@@ -155,15 +155,23 @@ struct EpResidual {
   __device__ inline int srow(int m) const { return m; }
   __device__ inline int cols() const { return ldx; }
   __device__ inline void store8(int m, int n, float (&v)[8]) const {
-    float* p = X + (size_t)m * ldx + n;
     float x[8];
-    get8(p, x);
+    pre8(m, n, x);
+    store8_pre(m, n, v, x);
+  }
+  // The same in two halves, for kernels that load the old values early.
+  __device__ inline void pre8(int m, int n, float (&x)[8]) const { get8(X + (size_t)m * ldx + n, x); }
+  __device__ inline void store8_pre(int m, int n, float (&v)[8], const float (&x)[8]) const {
 #pragma unroll
     for (int i = 0; i < 8; ++i) v[i] += x[i];
-    put8(p, v);
+    put8(X + (size_t)m * ldx + n, v);
     if constexpr (sizeof(T) == 2) put8(Xh + (size_t)m * ldx + n, v);
   }
 };
+template <class Ep>
+struct HasPre : std::false_type {};
+template <typename T>
+struct HasPre<EpResidual<T>> : std::true_type {};
 
 // QKV projection: q goes to Q [M][d]; k and v of row (b, i) go straight into
 // cache slot C_b + i of sequence b (the KV append of the step), in the page
@@ -908,6 +916,183 @@ __global__ void __launch_bounds__(256)
   }
 }
 
+// ------------------------------------------------------- skinny GEMM
+// Steps of at most 16 rows (decode blocks of one to four sequences, the AR
+// baseline at small batch) do little arithmetic per weight byte, and the tiled
+// kernel's K loop then runs at the latency of its LDS ring and barriers.  Here
+// one workgroup takes 16 output columns and its KW wavefronts split K: each
+// wavefront streams its K range of the 16 weight rows and of the (at most 16)
+// activation rows from memory straight into MFMA operands (16-byte chunks, the
+// same chunk-to-k assignment on both sides, U K steps of loads in flight, no
+// LDS and no barrier in the loop).  The wavefronts' partial sums meet in LDS
+// in wavefront order, and the 16 x 16 tile goes through the folded LayerNorm,
+// the bias and the same epilogues as the tiled kernel.
+template <typename T, int KW, int MODE, bool NORM, class Ep>
+__global__ void __launch_bounds__(64 * KW)
+    gemm_skinny_kernel(GemmA ga, const T* __restrict__ W, int ldw, int M, int N, int K, Ep ep) {
+  static_assert(sizeof(T) == 2, "16-bit operands (one 16x16x32 MFMA per K step)");
+  static_assert(KW >= 4, "at least one thread per tile element");
+  constexpr int U = 8;  // 32-wide K steps per batch of loads
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r = lane & 15, q = lane >> 4;
+  const int n0 = blockIdx.x * 16;
+  const int kw = K / KW, steps = kw / 32;
+  const T* A = static_cast<const T*>(ga.A);
+
+  // Folded LayerNorm: the row partial sums of the 16 rows (16 threads per
+  // row) are loaded first and reduced once the operand loads are in flight,
+  // so both wait on one memory round trip.
+  constexpr int PS = 4;  // partial sums per thread held in registers (K <= 1024)
+  __shared__ float2 sStat[16];
+  float2 ps[PS];
+  const float2* pr = nullptr;
+  if constexpr (NORM) {
+    if (tid < 256) {
+      pr = ga.lnst + (size_t)map_row<MODE>((tid >> 4) < M ? (tid >> 4) : M - 1, ga.g) * (K / 16);
+#pragma unroll
+      for (int i = 0; i < PS; ++i) {
+        const int w = (tid & 15) + 16 * i;
+        ps[i] = w < K / 16 ? pr[w] : make_float2(0.f, 0.f);
+      }
+    }
+  }
+  // A residual-stream epilogue's old values are loaded now as well.
+  const int sm = (lane >> 1) & 15, scc = lane & 1, sn = n0 + 8 * scc;
+  const bool slive = wave == 0 && lane < 32 && sm < M && sn < N;
+  float pre[8];
+  if constexpr (HasPre<Ep>::value) {
+    if (slive) ep.pre8(sm, sn, pre);
+  }
+
+  // Lane (r, q) feeds weight row n0 + r and activation row r, elements
+  // 8q .. 8q + 7 of each 32-wide K step.  Rows past the end re-read the last
+  // row: their outputs are never stored.
+  const int wrow = n0 + r < N ? n0 + r : N - 1;
+  const int arow = map_row<MODE>(r < M ? r : M - 1, ga.g);
+  const u32x4* pw = reinterpret_cast<const u32x4*>(W + (size_t)wrow * ldw + wave * kw + 8 * q);
+  const u32x4* pa = reinterpret_cast<const u32x4*>(A + (size_t)arow * ga.lda + wave * kw + 8 * q);
+  const u32x4 z = {0u, 0u, 0u, 0u};
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  u32x4 wa[U], xa[U];
+#pragma unroll
+  for (int i = 0; i < U; ++i) {
+    wa[i] = i < steps ? pw[4 * i] : z;
+    xa[i] = i < steps ? pa[4 * i] : z;
+  }
+  if constexpr (NORM) {
+    if (tid < 256) {
+      float a = 0.f, b = 0.f;
+#pragma unroll
+      for (int i = 0; i < PS; ++i) {
+        a += ps[i].x;
+        b += ps[i].y;
+      }
+      for (int w = (tid & 15) + 16 * PS; w < K / 16; w += 16) {  // K > 1024 only
+        const float2 v = pr[w];
+        a += v.x;
+        b += v.y;
+      }
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) {
+        a += __shfl_xor(a, off, 64);
+        b += __shfl_xor(b, off, 64);
+      }
+      if ((tid & 15) == 0) {
+        const float mu = ga.rms ? 0.f : a / (float)K;
+        const float var = ga.rms ? b / (float)K : fmaxf(b / (float)K - mu * mu, 0.f);
+        sStat[tid >> 4] = make_float2(mu, 1.0f / sqrtf(var + 1e-5f));
+      }
+    }
+  }
+  for (int s = 0; s < steps; s += U) {
+    u32x4 wb[U], xb[U];
+#pragma unroll
+    for (int i = 0; i < U; ++i) {
+      const int t = s + U + i;
+      wb[i] = t < steps ? pw[4 * t] : z;
+      xb[i] = t < steps ? pa[4 * t] : z;
+    }
+#pragma unroll
+    for (int i = 0; i < U; ++i)
+      if (s + i < steps) Mfma<T>::mma(wa[i], xa[i], acc);
+#pragma unroll
+    for (int i = 0; i < U; ++i) {
+      wa[i] = wb[i];
+      xa[i] = xb[i];
+    }
+  }
+
+  // This lane holds row r, columns 4q .. 4q + 3 of its wavefront's K range.
+  constexpr int SR = 20;  // padded row of the 16 x 16 tile, in floats
+  __shared__ __align__(16) float sred[KW][16 * SR];
+  __shared__ float sout[16 * SR];
+  *reinterpret_cast<float4*>(&sred[wave][r * SR + 4 * q]) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+  __syncthreads();
+  if (tid < 256) {  // one tile element per thread: sum over K ranges, norm, bias
+    const int m = tid >> 4, c = tid & 15, n = n0 + c < N ? n0 + c : N - 1;
+    float v = 0.f;
+#pragma unroll
+    for (int w = 0; w < KW; ++w) v += sred[w][m * SR + c];
+    const float pb = ep.bias ? ep.bias[n] : 0.f;
+    if constexpr (NORM) {
+      const float2 st = sStat[m];
+      v = st.y * (v - st.x * ga.c1[n]) + ga.c2[n] + pb;
+    } else {
+      v = v + pb;
+    }
+    sout[m * SR + c] = v;
+  }
+  __syncthreads();
+  if (wave != 0) return;
+  if constexpr (HasColumns<Ep>::value) {
+    if (ep.column_tile(n0)) {  // 8 consecutive rows of one column per lane
+      const int cg = lane >> 4, cl = lane & 15;
+      const int m = 8 * cg, n = n0 + cl;
+      if (lane < 32 && m < M && n < N) {
+        float v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = sout[(m + i) * SR + cl];
+        ep.store_col8(m, n, v, M);
+      }
+      return;
+    }
+  }
+  const int m = sm, cc = scc, n = sn;
+  const bool live = slive;
+  float v[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = sout[m * SR + 8 * cc + i];
+  if constexpr (HasPre<Ep>::value) {
+    if (live) ep.store8_pre(m, n, v, pre);
+  } else {
+    if (live) ep.store8(m, n, v);
+  }
+  if constexpr (Ep::kStats) {
+    // chunks 0 and 1 of a row (lanes 2j, 2j + 1) form its 16-column group
+    float a = 0.f, b = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      a += v[i];
+      b += v[i] * v[i];
+    }
+    a += __shfl_xor(a, 1, 64);
+    b += __shfl_xor(b, 1, 64);
+    if (live && cc == 0) ep.lnst[(size_t)ep.srow(m) * (ep.cols() / 16) + n / 16] = make_float2(a, b);
+  }
+}
+
+template <typename T, int MODE, bool NORM, class Ep>
+hipError_t launch_skinny(const GemmA& ga, const T* W, int M, int N, int K, const Ep& ep,
+                         hipStream_t s) {
+  if (K % 256 == 0 && K >= 2048)
+    launch((gemm_skinny_kernel<T, 8, MODE, NORM, Ep>), dim3(N / 16), dim3(512), 0, s, ga, W, K, M,
+           N, K, ep);
+  else
+    launch((gemm_skinny_kernel<T, 4, MODE, NORM, Ep>), dim3(N / 16), dim3(256), 0, s, ga, W, K, M,
+           N, K, ep);
+  return hipGetLastError();
+}
+
 template <typename T, int BM, int BN, int WM, int WN, int S, int MODE, bool NORM, class Ep>
 hipError_t launch_tile(const GemmA& ga, const T* W, int ldw, int M, int N, int K, const Ep& ep,
                        hipStream_t s, int ksplit = 1) {
@@ -989,11 +1174,18 @@ hipError_t launch_plain(const GemmA& ga, const T* W, int M, int N, int K, const 
 
 inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
+// Steps of at most this many rows run the skinny kernel (16-bit operands).
+constexpr int kSkinnyRows = 16;
+
 // Tile choice: the largest tile that still gives about one workgroup per CU.
 template <typename T, int MODE, bool NORM, class Ep>
 hipError_t dispatch(const GemmA& ga, const T* W, int M, int N, int K, const Ep& ep, hipStream_t s,
                     const SplitWs* ws = nullptr) {
   if (M <= 0 || N <= 0) return hipSuccess;
+  if constexpr (sizeof(T) == 2) {
+    if (M <= kSkinnyRows && N % 16 == 0 && K % 128 == 0)
+      return launch_skinny<T, MODE, NORM>(ga, W, M, N, K, ep, s);
+  }
   constexpr int kFill = 256;
   if constexpr (!NORM && MODE == 0) {
     if (cdiv(M, 128) * cdiv(N, 128) >= kFill)

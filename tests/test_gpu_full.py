@@ -130,13 +130,15 @@ def test_lm1b_fp32_tokens():
     _log(f"lm1b fp32 parity: {st}")
 
 
-def test_lm1b_bf16_ar_baseline():
-    """AR baseline at the LM1B shape: logits within 2e-2 of the oracle."""
-    B, N = 64, 16
+@pytest.mark.parametrize("B", [64, 13, 1])
+def test_lm1b_bf16_ar_baseline(B):
+    """AR baseline at the LM1B shape: logits within 2e-2 of the oracle.  At 13
+    and 1 sequences every body GEMM has at most 16 rows (the skinny kernel)."""
+    N = 16
     kf = _ctx(LM1B, B, 4, N)
     prompt = S.prompts_zipf(1, B, N, LM1B.vocab)
     model = _model(LM1B)
-    rows = [0, B - 1]
+    rows = sorted({0, B - 1})
     seqs = {b: model.seq() for b in rows}
     pend = {b: list(prompt[b]) for b in rows}
     worst = 0.0
@@ -152,7 +154,7 @@ def test_lm1b_bf16_ar_baseline():
             worst = max(worst, rel)
             assert rel <= TOL[1]
             pend[b] = [int(toks[b])]
-    _log(f"lm1b AR logit rel err {worst:.3e}")
+    _log(f"lm1b AR B={B} logit rel err {worst:.3e}")
 
 
 OWT = S.WORKLOADS["owt"]["cfg"]
@@ -166,6 +168,17 @@ def test_owt_shape_prefill_decode():
     prompt = S.prompts_zipf(1, B, N, OWT.vocab)
     st = _blocks(kf, _model(OWT), prompt, [k, k], seed=2, tol=TOL[1], rows=[0, B - 1])
     _log(f"owt bf16 parity: {st}")
+
+
+def test_owt_batch1_decode():
+    """One sequence on the OWT-shaped model (the skinny GEMMs: 8 body rows and
+    4 head rows per k = 4 block): prefill of a 128-token prompt, three blocks
+    at k = 4, then blocks at k = 2 and k = 1 (12, 6 and 3 body rows)."""
+    B, N = 1, 128
+    kf = _ctx(OWT, B, 4, N)
+    prompt = S.prompts_zipf(1, B, N, OWT.vocab)
+    st = _blocks(kf, _model(OWT), prompt, [4, 4, 4, 2, 1], seed=4, tol=TOL[1], rows=[0])
+    _log(f"owt bf16 B=1 parity: {st}")
 
 
 LARGE = S.WORKLOADS["large"]["cfg"]
