@@ -227,7 +227,7 @@ def kernel_class(name: str, state: dict):
     if "EpPartial" in name:
         return "pending"
     if "EpResidual" in name:
-        if "splitk_reduce" in name or "gemm_kernel" in name:
+        if "splitk_reduce" in name or "gemm_kernel" in name or "gemm_skinny_kernel" in name:
             role = "oproj" if state.get("residual", 0) % 2 == 0 else "mlp_down"
             state["residual"] = state.get("residual", 0) + 1
             return role

@@ -189,9 +189,10 @@ __global__ void __launch_bounds__(256)
 
 // Block attention on MFMA (bf16).  One workgroup per (sequence, head, block of
 // 16 query rows, key split); its NW wavefronts (four in the library: measured
-// best from 64 keys up, and within 6 % of two waves at 16 keys) take 32-key
-// tiles of the split's key range round-robin and merge their online-softmax
-// states through LDS at the end.
+// best from 64 keys up, and within 6 % of two waves at 16 keys; eight for
+// mid-size decode grids, see kWideMin) take 32-key tiles of the split's key
+// range round-robin and merge their online-softmax states through LDS at the
+// end.
 //   S^T = K Q^T   with v_mfma_f32_16x16x32_bf16: A = 16 keys x 32 d_head,
 //                 B = 32 d_head x 16 queries.  MFMA row i of key group grp is
 //                 key 8*(i/4) + 4*grp + i%4 of the tile, so the output rows a
@@ -841,6 +842,15 @@ hipError_t launch_noise_sinusoid(T* S, const float* noise, uint64_t seed, const 
   return hipGetLastError();
 }
 
+// Decode grids of 64 to 255 query blocks at d_head 64 (batch 6 to 21 at 12
+// heads) run one workgroup of eight wavefronts per block instead of key
+// splits of four-wavefront workgroups and their merge kernel: measured on the
+// OWT-shaped model at batch 16, attention 43.2 -> 31.0 ms per generate (the
+// generate 139.6 -> 130.5 ms).  Smaller grids keep the splits (batch 1 lost
+// 4 % with eight wavefronts and no split), and grids of 256 blocks and more
+// keep four wavefronts (batch 64 lost 9 %, batch 256 15 % with eight).
+constexpr int kWideMin = 64;
+
 template <typename T>
 hipError_t launch_attention(const T* Q, const T* kv, T* O, const KfDevState* st, KfStepGeom g,
                             KfKvGeom kg, int layer, const AttnSplit& ws, hipStream_t s) {
@@ -870,6 +880,13 @@ hipError_t launch_attention(const T* Q, const T* kv, T* O, const KfDevState* st,
                              O, g, kg.H, sp);
         break;
       case 64:
+        if (ns > 1 && base >= kWideMin) {  // eight wavefronts, no key split
+          sp.ns = 1;
+          launch((attention_mfma_kernel<64, 8>), dim3(base), dim3(512), 0, s, Q, kv, O, st, g, kg,
+                 layer, scale, sp);
+          ns = 1;
+          break;
+        }
         launch(attention_mfma_kernel<64>, grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
                            layer, scale, sp);
         if (ns > 1)

@@ -181,6 +181,17 @@ def test_owt_batch1_decode():
     _log(f"owt bf16 B=1 parity: {st}")
 
 
+def test_owt_batch16_decode():
+    """The sweep's batch 16 on the OWT-shaped model: decode attention runs 192
+    query blocks of eight wavefronts with no key split (prefill: 960 blocks of
+    four); prompt 64, prefill and two blocks at k = 4, sequences 0 and 15."""
+    B, N, k = 16, 64, 4
+    kf = _ctx(OWT, B, k, N)
+    prompt = S.prompts_zipf(1, B, N, OWT.vocab)
+    st = _blocks(kf, _model(OWT), prompt, [k, k, k], seed=6, tol=TOL[1], rows=[0, B - 1])
+    _log(f"owt bf16 B=16 parity: {st}")
+
+
 LARGE = S.WORKLOADS["large"]["cfg"]
 
 
