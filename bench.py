@@ -177,6 +177,12 @@ def _short(name: str) -> str:
         ep = re.search(r"NS0_\d+(Ep\w+?)I|NS0_\d+(Ep\w+?)E", m.group(2))
         epn = (ep.group(1) or ep.group(2)) if ep else "?"
         return f"gemm {'x'.join(t[:2])} {epn}" + (" bf16" if "DF16b" in n else " f32")
+    if m and "gemm_skinny_kernel" in m.group(1):
+        t = re.findall(r"Li(\d+)E", m.group(2))
+        ep = re.search(r"NS0_\d+(Ep\w+?)I|NS0_\d+(Ep\w+?)E", m.group(2))
+        epn = (ep.group(1) or ep.group(2)) if ep else "?"
+        norm = "+LN " if "Lb1E" in m.group(2) else ""
+        return f"gemm skinny {t[0] if t else '?'}w {norm}{epn}" + (" bf16" if "DF16b" in n else " f32")
     if m:
         return m.group(1) + (" bf16" if "DF16b" in n else "")
     return n.split("(")[0]

@@ -923,8 +923,8 @@ __global__ void __launch_bounds__(256)
 // one workgroup takes 16 output columns and its KW wavefronts split K: each
 // wavefront streams its K range of the 16 weight rows and of the (at most 16)
 // activation rows from memory straight into MFMA operands (16-byte chunks, the
-// same chunk-to-k assignment on both sides, U K steps of loads in flight, no
-// LDS and no barrier in the loop).  The wavefronts' partial sums meet in LDS
+// same chunk-to-k assignment on both sides, up to 2U K steps of loads in
+// flight, no LDS and no barrier in the loop).  The wavefronts' partial sums meet in LDS
 // in wavefront order, and the 16 x 16 tile goes through the folded LayerNorm,
 // the bias and the same epilogues as the tiled kernel.
 template <typename T, int KW, int MODE, bool NORM, class Ep>
@@ -973,12 +973,24 @@ __global__ void __launch_bounds__(64 * KW)
   const u32x4* pa = reinterpret_cast<const u32x4*>(A + (size_t)arow * ga.lda + wave * kw + 8 * q);
   const u32x4 z = {0u, 0u, 0u, 0u};
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  u32x4 wa[U], xa[U];
+  // Two named load batches alternate (no register copies between them, which
+  // would wait for loads still in flight): batch B loads while batch A feeds
+  // the MFMAs, and the other way round.
+  u32x4 wa[U], xa[U], wb[U], xb[U];
+  auto load = [&](u32x4 (&w)[U], u32x4 (&x)[U], int s0) {
 #pragma unroll
-  for (int i = 0; i < U; ++i) {
-    wa[i] = i < steps ? pw[4 * i] : z;
-    xa[i] = i < steps ? pa[4 * i] : z;
-  }
+    for (int i = 0; i < U; ++i) {
+      const int t = s0 + i;
+      w[i] = t < steps ? pw[4 * t] : z;
+      x[i] = t < steps ? pa[4 * t] : z;
+    }
+  };
+  auto mma = [&](const u32x4 (&w)[U], const u32x4 (&x)[U], int s0) {
+#pragma unroll
+    for (int i = 0; i < U; ++i)
+      if (s0 + i < steps) Mfma<T>::mma(w[i], x[i], acc);
+  };
+  load(wa, xa, 0);
   if constexpr (NORM) {
     if (tid < 256) {
       float a = 0.f, b = 0.f;
@@ -1004,22 +1016,12 @@ __global__ void __launch_bounds__(64 * KW)
       }
     }
   }
-  for (int s = 0; s < steps; s += U) {
-    u32x4 wb[U], xb[U];
-#pragma unroll
-    for (int i = 0; i < U; ++i) {
-      const int t = s + U + i;
-      wb[i] = t < steps ? pw[4 * t] : z;
-      xb[i] = t < steps ? pa[4 * t] : z;
-    }
-#pragma unroll
-    for (int i = 0; i < U; ++i)
-      if (s + i < steps) Mfma<T>::mma(wa[i], xa[i], acc);
-#pragma unroll
-    for (int i = 0; i < U; ++i) {
-      wa[i] = wb[i];
-      xa[i] = xb[i];
-    }
+  for (int s = 0; s < steps; s += 2 * U) {
+    if (s + U < steps) load(wb, xb, s + U);
+    mma(wa, xa, s);
+    if (s + U >= steps) break;
+    if (s + 2 * U < steps) load(wa, xa, s + 2 * U);
+    mma(wb, xb, s + U);
   }
 
   // This lane holds row r, columns 4q .. 4q + 3 of its wavefront's K range.
