@@ -932,7 +932,7 @@ __global__ void __launch_bounds__(64 * KW)
     gemm_skinny_kernel(GemmA ga, const T* __restrict__ W, int ldw, int M, int N, int K, Ep ep) {
   static_assert(sizeof(T) == 2, "16-bit operands (one 16x16x32 MFMA per K step)");
   static_assert(KW >= 4, "at least one thread per tile element");
-  constexpr int U = 8;  // 32-wide K steps per batch of loads
+  constexpr int U = KW >= 16 ? 4 : 8;  // 32-wide K steps per batch of loads
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r = lane & 15, q = lane >> 4;
   const int n0 = blockIdx.x * 16;
@@ -956,7 +956,17 @@ __global__ void __launch_bounds__(64 * KW)
       }
     }
   }
-  // A residual-stream epilogue's old values are loaded now as well.
+  // The column constants of this thread's tile element (bias, folded-norm
+  // sums) and a residual-stream epilogue's old values are loaded now as well.
+  const int ec = tid & 15, en = n0 + ec < N ? n0 + ec : N - 1;
+  float e_pb = 0.f, e_c1 = 0.f, e_c2 = 0.f;
+  if (tid < 256) {
+    if (ep.bias) e_pb = ep.bias[en];
+    if constexpr (NORM) {
+      e_c1 = ga.c1[en];
+      e_c2 = ga.c2[en];
+    }
+  }
   const int sm = (lane >> 1) & 15, scc = lane & 1, sn = n0 + 8 * scc;
   const bool slive = wave == 0 && lane < 32 && sm < M && sn < N;
   float pre[8];
@@ -1031,16 +1041,15 @@ __global__ void __launch_bounds__(64 * KW)
   *reinterpret_cast<float4*>(&sred[wave][r * SR + 4 * q]) = make_float4(acc[0], acc[1], acc[2], acc[3]);
   __syncthreads();
   if (tid < 256) {  // one tile element per thread: sum over K ranges, norm, bias
-    const int m = tid >> 4, c = tid & 15, n = n0 + c < N ? n0 + c : N - 1;
+    const int m = tid >> 4, c = ec;
     float v = 0.f;
 #pragma unroll
     for (int w = 0; w < KW; ++w) v += sred[w][m * SR + c];
-    const float pb = ep.bias ? ep.bias[n] : 0.f;
     if constexpr (NORM) {
       const float2 st = sStat[m];
-      v = st.y * (v - st.x * ga.c1[n]) + ga.c2[n] + pb;
+      v = st.y * (v - st.x * e_c1) + e_c2 + e_pb;
     } else {
-      v = v + pb;
+      v = v + e_pb;
     }
     sout[m * SR + c] = v;
   }
@@ -1086,9 +1095,9 @@ __global__ void __launch_bounds__(64 * KW)
 template <typename T, int MODE, bool NORM, class Ep>
 hipError_t launch_skinny(const GemmA& ga, const T* W, int M, int N, int K, const Ep& ep,
                          hipStream_t s) {
-  if (K % 256 == 0 && K >= 2048)
-    launch((gemm_skinny_kernel<T, 8, MODE, NORM, Ep>), dim3(N / 16), dim3(512), 0, s, ga, W, K, M,
-           N, K, ep);
+  if (K % 512 == 0 && K >= 2048)  // long K (MLP-down): sixteen wavefronts of 6+ K steps
+    launch((gemm_skinny_kernel<T, 16, MODE, NORM, Ep>), dim3(N / 16), dim3(1024), 0, s, ga, W, K,
+           M, N, K, ep);
   else
     launch((gemm_skinny_kernel<T, 4, MODE, NORM, Ep>), dim3(N / 16), dim3(256), 0, s, ga, W, K, M,
            N, K, ep);
