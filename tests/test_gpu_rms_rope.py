@@ -100,15 +100,17 @@ def test_rms_rope_unused_tensors_ignored():
         np.testing.assert_array_equal(x, y)
 
 
-def test_lm1b_shape_rms_rope_bf16():
-    """LM1B-shaped bf16 rotary model (d_head 64): batch 8, prompt 16, prefill and
-    two decode blocks, sequences 0, 3 and 7."""
+@pytest.mark.parametrize("B", [8, 2])
+def test_lm1b_shape_rms_rope_bf16(B):
+    """LM1B-shaped bf16 rotary model (d_head 64): prompt 16, prefill and two
+    decode blocks; batch 8 (sequences 0, 3 and 7) and batch 2, whose 16-row
+    decode blocks run the skinny GEMMs (RMS statistics, rotary QKV epilogue)."""
     blob = _blob(LM1B_R, 0)
-    kf = _ctx(LM1B_R, blob, 8, 4, 16)
-    prompt = S.prompts_zipf(2, 8, 16, LM1B_R.vocab)
+    kf = _ctx(LM1B_R, blob, B, 4, 16)
+    prompt = S.prompts_zipf(2, B, 16, LM1B_R.vocab)
     st = _teacher_forced(kf, O.Model(blob), prompt, [4, 4, 4], seed=6, tol=TOL[1],
-                         rows=[0, 3, 7])
-    _log(f"lm1b rms/rope bf16: {st}")
+                         rows=sorted({0, B // 2 - 1, B - 1}))
+    _log(f"lm1b rms/rope bf16 B={B}: {st}")
 
 
 def test_rms_rope_generate():

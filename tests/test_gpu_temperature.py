@@ -97,12 +97,16 @@ def test_temperature_required_and_changeable():
     assert np.abs(la - lb).max() > 1e-4 * np.abs(la).max()
 
 
-def test_lm1b_shape_temperature_bf16():
-    """LM1B-shaped bf16 model with a temperature encoder: batch 8, prompt 16,
-    prefill and one decode block, sequences 0 and 7."""
+@pytest.mark.parametrize("B", [8, 2])
+def test_lm1b_shape_temperature_bf16(B):
+    """LM1B-shaped bf16 model with a temperature encoder: prompt 16, prefill and
+    one decode block, the first and last sequence; at batch 2 the decode block
+    (16 body rows, 8 noise rows) runs the skinny GEMMs, the temperature
+    embedding added in the second noise GEMM's epilogue."""
     blob = S.pack_blob(LM1B_T, S.make_weights(LM1B_T, seed=0, random_affine=True))
-    kf = _ctx(LM1B_T, blob, 8, 4, 16)
-    prompt = S.prompts_zipf(1, 8, 16, LM1B_T.vocab)
-    taus = np.linspace(0.01, 1.0, 8)
-    st = _teacher_forced(kf, O.Model(blob), prompt, taus, [4, 4], seed=5, tol=TOL[1], rows=[0, 7])
-    _log(f"lm1b temperature bf16 parity: {st}")
+    kf = _ctx(LM1B_T, blob, B, 4, 16)
+    prompt = S.prompts_zipf(1, B, 16, LM1B_T.vocab)
+    taus = np.linspace(0.01, 1.0, B)
+    st = _teacher_forced(kf, O.Model(blob), prompt, taus, [4, 4], seed=5, tol=TOL[1],
+                         rows=[0, B - 1])
+    _log(f"lm1b temperature bf16 B={B} parity: {st}")
