@@ -848,7 +848,8 @@ hipError_t launch_noise_sinusoid(T* S, const float* noise, uint64_t seed, const 
 // OWT-shaped model at batch 16, attention 43.2 -> 31.0 ms per generate (the
 // generate 139.6 -> 130.5 ms).  Smaller grids keep the splits (batch 1 lost
 // 4 % with eight wavefronts and no split), and grids of 256 blocks and more
-// keep four wavefronts (batch 64 lost 9 %, batch 256 15 % with eight).
+// keep four wavefronts (batch 24 and 32 lost 5 %, batch 64 9 %, batch 256
+// 15 % with eight).
 constexpr int kWideMin = 64;
 
 template <typename T>
