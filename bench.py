@@ -47,55 +47,94 @@ CLASSES = ["embed", "noise", "norm", "qkv", "attn", "oproj", "mlp_up", "mlp_down
 # --------------------------------------------------------------------------
 
 def step_costs(cfg: S.ModelConfig, B: int, nr: int, k: int, C: int) -> dict:
-    """Per kernel class: (bytes, flops) that one step must move / compute.
+    """Per kernel class: the algorithmic (bytes, flops) of one step with B
+    sequences, nr real rows and k noise rows per sequence over C committed
+    positions -- what the method itself must move or compute:
 
-    Bytes count every operand once: weights, activations in and out, the KV
-    cache rows each (sequence, head) attends to, the K/V rows written."""
+      bytes: the weights each class reads once, the cached K/V the attention
+             reads (C rows of 2 d elements per sequence and layer) and the K/V
+             the QKV GEMM appends (every new row);
+      flops: 2 M K N for each GEMM (M = B (nr + k) body rows, B k head rows, or
+             B for an AR step), the noise encoder's two GEMMs on the B k noise
+             rows, and 4 d per visible (query, key) pair of the attention.
+
+    Activations, the fp32 residual stream and partial results are an
+    implementation's own traffic and are not counted (operand_costs does)."""
     es = 2 if cfg.dtype == S.DTYPE_BF16 else 4
-    d, f, V, L, H = cfg.d_model, cfg.d_mlp, cfg.vocab, cfg.n_layer, cfg.n_head
+    d, f, V, L = cfg.d_model, cfg.d_mlp, cfg.vocab, cfg.n_layer
     R = nr + k
     M = B * R
-    Mk = B * k
-    Mh = Mk if k > 0 else B
+    Mh = B * k if k > 0 else B
     c = {n: [0.0, 0.0] for n in CLASSES}
 
     def add(n, by, fl):
         c[n][0] += by
         c[n][1] += fl
 
-    add("embed", B * nr * (2 * d * es + 4 * d), 0)
     if k > 0:
-        add("noise", Mk * d * es + 4 * d * d * es + Mk * 4 * d * es, 2 * Mk * 4 * d * d)
-        add("noise", 4 * d * d * es + Mk * 4 * d * es + Mk * d * (4 + es), 2 * Mk * d * 4 * d)
+        add("noise", 8 * d * d * es, 2 * B * k * 8 * d * d)
     visible = sum(C + i + 1 for i in range(R))  # keys seen by the R queries of a sequence
     for _ in range(L):
-        # LayerNorm is folded into the GEMM that consumes it: its bytes are the
-        # GEMM's activation read, counted there.
-        add("qkv", 3 * d * d * es + M * d * es + M * 3 * d * es, 2 * M * 3 * d * d)
-        add("attn", B * (C + R) * 2 * d * es + 2 * M * d * es, 4 * B * visible * d)
-        add("oproj", d * d * es + M * d * es + 2 * M * d * 4, 2 * M * d * d)
-        add("mlp_up", f * d * es + M * d * es + M * f * es, 2 * M * f * d)
-        add("mlp_down", d * f * es + M * f * es + 2 * M * d * 4, 2 * M * d * f)
-    add("head", V * d * es + Mh * d * es, 2 * Mh * V * d)
-    add("select", Mh * 8, 0)
+        add("qkv", 3 * d * d * es + B * R * 2 * d * es, 2 * M * 3 * d * d)
+        add("attn", B * C * 2 * d * es, 4 * B * visible * d)
+        add("oproj", d * d * es, 2 * M * d * d)
+        add("mlp_up", f * d * es, 2 * M * f * d)
+        add("mlp_down", d * f * es, 2 * M * d * f)
+    add("head", V * d * es, 2 * Mh * V * d)
     return c
 
 
-def generate_costs(cfg, B, N, L, k) -> dict:
+def operand_costs(cfg: S.ModelConfig, B: int, nr: int, k: int, C: int) -> dict:
+    """A diagnostic beside step_costs: bytes of every operand of this
+    implementation's kernels read or written once (weights, bf16 activations
+    in and out, the fp32 residual stream read and written by out-proj and
+    MLP-down, the cached rows each attention workgroup reads, Q and O).  Not a
+    roofline: the activations are the implementation's own traffic."""
+    es = 2 if cfg.dtype == S.DTYPE_BF16 else 4
+    d, f, V, L = cfg.d_model, cfg.d_mlp, cfg.vocab, cfg.n_layer
+    R = nr + k
+    M = B * R
+    Mk = B * k
+    Mh = Mk if k > 0 else B
+    c = {n: [0.0, 0.0] for n in CLASSES}
+
+    def add(n, by):
+        c[n][0] += by
+
+    add("embed", B * nr * (2 * d * es + 4 * d))
+    if k > 0:
+        add("noise", Mk * d * es + 4 * d * d * es + Mk * 4 * d * es)
+        add("noise", 4 * d * d * es + Mk * 4 * d * es + Mk * d * (4 + es))
+    for _ in range(L):
+        add("qkv", 3 * d * d * es + M * d * es + M * 3 * d * es)
+        add("attn", B * (C + R) * 2 * d * es + 2 * M * d * es)
+        add("oproj", d * d * es + M * d * es + 2 * M * d * 4)
+        add("mlp_up", f * d * es + M * d * es + M * f * es)
+        add("mlp_down", d * f * es + M * f * es + 2 * M * d * 4)
+    add("head", V * d * es + Mh * d * es)
+    add("select", Mh * 8)
+    return c
+
+
+def generate_costs(cfg, B, N, L, k, per_step=step_costs) -> dict:
+    """Summed per-class costs of a kf_generate call: the prefill (N prompt rows
+    + k noise rows, C = 0) and L/k - 1 decode blocks (k + k rows at
+    C = N, N + k, ...)."""
     tot = {n: [0.0, 0.0] for n in CLASSES}
     steps = [(N, k, 0)] + [(k, k, N + (s - 1) * k) for s in range(1, L // k)]
     for nr, kk, C in steps:
-        for n, (by, fl) in step_costs(cfg, B, nr, kk, C).items():
+        for n, (by, fl) in per_step(cfg, B, nr, kk, C).items():
             tot[n][0] += by
             tot[n][1] += fl
     return tot
 
 
-def generate_ar_costs(cfg, B, N, L) -> dict:
+def generate_ar_costs(cfg, B, N, L, per_step=step_costs) -> dict:
+    """Summed per-class costs of a kf_generate_ar call (one row per step)."""
     tot = {n: [0.0, 0.0] for n in CLASSES}
     steps = [(N, 0)] + [(1, N + s - 1) for s in range(1, L)]
     for nr, C in steps:
-        for n, (by, fl) in step_costs(cfg, B, nr, 0, C).items():
+        for n, (by, fl) in per_step(cfg, B, nr, 0, C).items():
             tot[n][0] += by
             tot[n][1] += fl
     return tot
@@ -115,7 +154,7 @@ def parse():
     ap.add_argument("--no-ar", action="store_true", help="skip the k=1 AR baseline")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the OpenWebText-shaped batch sweep and k comparison")
-    ap.add_argument("--sweep-batches", default="1,16,64,256,512")
+    ap.add_argument("--sweep-batches", default="1,16,32,64,256,512")
     ap.add_argument("--no-large", action="store_true",
                     help="skip the 24-layer backbone at batch 256")
     ap.add_argument("--large-only", action="store_true",
@@ -150,22 +189,101 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+def cpu_model_name() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(blob, prompt, k, seed, blocks):
-    """Oracle (fp32 instantiation, OpenMP over sequences) on a bounded sample."""
+    """The oracle's fp32 instantiation (the same loop nest as the parity
+    oracle, OpenMP over sequences) on bounded samples, on this host's cores:
+
+      value      -- the benchmark workload: one sequence per thread (up to the
+                    batch), prefill + `blocks` - 1 decode blocks at k;
+      one_thread -- the same with one thread on one sequence, 8 passes;
+      toy        -- the whole 2-layer toy workload (batch 4, 64 new tokens);
+      owt_k4_extrapolated -- the OWT-shaped model: 3 decode blocks at k = 4 at
+                    the mean context length of its generate (C = 572), on one
+                    copy per thread of a single sequence's context (built by an
+                    untimed prefill); tokens/s = sequences * k * 3 / time, an
+                    extrapolation of the whole generate from its mean step."""
+    import ctypes
     import oracle as O
     threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
     threads = max(1, min(threads, len(os.sched_getaffinity(0))))
     os.environ["OMP_NUM_THREADS"] = str(threads)
+    O.lib()
+    try:
+        gomp = ctypes.CDLL("libgomp.so.1")
+    except OSError:
+        gomp = None
+
+    def set_threads(n):
+        if gomp is not None:
+            gomp.omp_set_num_threads(n)
+
+    set_threads(threads)
     nseq = min(prompt.shape[0], threads)
     m = O.Model(blob, "f32")
     L = blocks * k
     t0 = time.perf_counter()
     O.generate_batched(m, prompt[:nseq], L, k, seed)
     dt = time.perf_counter() - t0
-    return {"value": nseq * L / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": (f"fp32 oracle loop nest, {nseq} sequences x {L} new tokens "
-                       f"(prefill + {blocks - 1} decode blocks at k={k}), {dt:.1f} s"),
-            "seconds": round(dt, 2)}
+    res = {"value": nseq * L / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+           "cpu": cpu_model_name(), "host_cpus": os.cpu_count(),
+           "sample": (f"fp32 oracle loop nest, {nseq} sequences x {L} new tokens "
+                      f"(prefill + {blocks - 1} decode blocks at k={k}), {dt:.1f} s"),
+           "seconds": round(dt, 2)}
+    # one thread, one sequence
+    set_threads(1)
+    L1 = 8 * k
+    t0 = time.perf_counter()
+    O.generate_batched(m, prompt[:1], L1, k, seed)
+    dt1 = time.perf_counter() - t0
+    res["one_thread"] = {"value": L1 / dt1, "unit": "tokens/s", "cores": 1,
+                         "sample": f"1 sequence x {L1} new tokens (prefill + 7 blocks), {dt1:.1f} s"}
+    set_threads(threads)
+    del m
+    # the toy workload end to end
+    tw = S.WORKLOADS["toy"]
+    tcfg = tw["cfg"]
+    tm = O.Model(S.pack_blob(tcfg, S.make_weights(tcfg, seed=0)), "f32")
+    tp = S.make_prompts(tw["prompts"], 1, tw["B"], tw["N"], tcfg.vocab)
+    t0 = time.perf_counter()
+    O.generate_batched(tm, tp, tw["L"], tw["k"], seed)
+    dtt = time.perf_counter() - t0
+    res["toy"] = {"value": tw["B"] * tw["L"] / dtt, "unit": "tokens/s", "cores": min(threads, tw["B"]),
+                  "sample": f"whole toy workload: {tw['B']} x {tw['L']} tokens at k={tw['k']}, "
+                            f"{dtt * 1e3:.0f} ms"}
+    # OWT-shaped k = 4: three decode blocks at C = 572
+    ow = S.WORKLOADS["owt"]
+    ocfg = ow["cfg"]
+    om = O.Model(owt_blob(), "f32")
+    C0, kk = 572, 4
+    op = S.make_prompts(ow["prompts"], 1, 1, C0 + kk, ocfg.vocab)[0]
+    base = om.seq()
+    t0 = time.perf_counter()
+    base.step(list(op[:C0]), [], commit=True)
+    t_pre = time.perf_counter() - t0
+    seqs = [base.copy() for _ in range(threads)]
+    pend = np.tile(op[C0:C0 + kk], (threads, 1))
+    t0 = time.perf_counter()
+    for st in range(3):
+        u = S.noise_block(seed, threads, C0 + (st + 1) * kk, kk)
+        pend = O.decode_batched(seqs, pend, kk, u)
+    dto = time.perf_counter() - t0
+    res["owt_k4_extrapolated"] = {
+        "value": threads * kk * 3 / dto, "unit": "tokens/s", "cores": threads,
+        "sample": (f"OWT-shaped fp32 oracle, {threads} sequences x 3 decode blocks at k={kk} "
+                   f"from C={C0} (the generate's mean context), {dto:.1f} s; context built by "
+                   f"an untimed {t_pre:.1f} s prefill; an extrapolation of the whole generate")}
+    return res
 
 
 def _short(name: str) -> str:
@@ -361,19 +479,31 @@ def time_calls(fn, reps):
     return (time.perf_counter() - t0) / reps
 
 
+_OWT_BLOB = {}
+
+
+def owt_blob():
+    """The OWT-shaped model's seeded weights (kept for the CPU baseline)."""
+    if "blob" not in _OWT_BLOB:
+        cfg = S.WORKLOADS["owt"]["cfg"]
+        log("[bench] generating OWT-shaped weights")
+        _OWT_BLOB["blob"] = S.pack_blob(cfg, S.make_weights(cfg, seed=0))
+    return _OWT_BLOB["blob"]
+
+
 def owt_sweep(batches, stream):
     """OpenWebText-shaped model (12 layers, d=768, vocab 50257, context 1024,
     bf16), prompt 128 Zipf(1.1) tokens, generation to the full context (896 new
-    tokens): k=4 against the k=1 AR baseline per batch size, and k in {1, 2, 4}
-    (plus AR) at batch 32.  Each figure is whole-generate throughput with its
-    step-level roofline fraction t_roof / t_meas."""
+    tokens): K-Forcing at k = 4, 2 and 1 and the k = 1 AR baseline at every
+    batch size.  Each figure is whole-generate throughput with its step-level
+    roofline fraction t_roof / t_meas (t_roof from step_costs: max of bytes /
+    HBM peak and flops / bf16 MFMA peak, summed over the generate's passes)."""
     import torch
     from paper_2606_10820_amd import binding as Bd
     w = S.WORKLOADS["owt"]
     cfg = w["cfg"]
     N, L, seed = w["N"], w["L"], 2
-    log("[bench] sweep: generating OWT-shaped weights")
-    blob = S.pack_blob(cfg, S.make_weights(cfg, seed=0))
+    blob = owt_blob()
     dev = torch.device("cuda:0")
 
     def ctx(B):
@@ -398,31 +528,31 @@ def owt_sweep(batches, stream):
     rows = []
     for B in batches:
         kf = ctx(B)
-        r4 = run(kf, B, 4, 2)
-        r1 = run(kf, B, 0, 1)
-        rows.append({"batch": B, "k4": r4, "ar_k1": r1,
-                     "speedup_k4_vs_ar": round(r4["tokens_s"] / r1["tokens_s"], 3)})
-        log(f"[bench] sweep B={B}: k=4 {r4['tokens_s']:,.0f} tok/s "
-            f"({r4['roofline_frac']:.1%} of step roofline), AR {r1['tokens_s']:,.0f} tok/s, "
-            f"x{rows[-1]['speedup_k4_vs_ar']:.2f}")
+        r = {"batch": B}
+        r["k4"] = run(kf, B, 4, 2)
+        r["k2"] = run(kf, B, 2, 1)
+        r["k1"] = run(kf, B, 1, 1)
+        r["ar_k1"] = run(kf, B, 0, 1)
+        for kk in ("k4", "k2", "k1"):
+            r[f"speedup_{kk}_vs_ar"] = round(r[kk]["tokens_s"] / r["ar_k1"]["tokens_s"], 3)
+        rows.append(r)
+        log(f"[bench] sweep B={B}: k=4 {r['k4']['tokens_s']:,.0f} tok/s "
+            f"({r['k4']['roofline_frac']:.1%} of step roofline), k=2 {r['k2']['tokens_s']:,.0f}, "
+            f"k=1 {r['k1']['tokens_s']:,.0f}, AR {r['ar_k1']['tokens_s']:,.0f} tok/s, "
+            f"k=4/AR x{r['speedup_k4_vs_ar']:.2f}")
         del kf
         torch.cuda.empty_cache()
-    B = w["B"]
-    kf = ctx(B)
-    ks = {f"k{k}": run(kf, B, k, 2) for k in (1, 2, 4)}
-    ks["ar_k1"] = run(kf, B, 0, 1)
-    log("[bench] OWT B=%d: " % B + ", ".join(f"{n} {v['tokens_s']:,.0f} tok/s" for n, v in ks.items()))
-    del kf
-    torch.cuda.empty_cache()
     return {"workload": (f"OWT-shaped: {cfg.n_layer} layers, d={cfg.d_model}, vocab {cfg.vocab}, "
                          f"context {cfg.n_ctx}, prompt {N} Zipf(1.1), {L} new tokens, bf16"),
-            "by_batch": rows, "k_at_batch": {"batch": B, **ks}}
+            "by_batch": rows}
 
 
 def teacher_costs(cfg: S.ModelConfig, B: int, N: int) -> dict:
     """Per kernel class (bytes, flops) of one kf_teacher_targets call: an AR
     prefill of N tokens per sequence whose head runs over every row."""
-    c = step_costs(cfg, B, N, 0, 0)
+    c = operand_costs(cfg, B, N, 0, 0)
+    for n, (_, fl) in step_costs(cfg, B, N, 0, 0).items():
+        c[n][1] = fl
     es = 2 if cfg.dtype == S.DTYPE_BF16 else 4
     d, V, M = cfg.d_model, cfg.vocab, B * N
     nt = (V + 255) // 256 * 2
@@ -848,6 +978,7 @@ def main():
         per[name] = (ms, n)
     kf.set_timing(0)
     costs = generate_costs(cfg, B, N, L, k)
+    opcosts = generate_costs(cfg, B, N, L, k, per_step=operand_costs)
     dom = max(CLASSES, key=lambda n: per[n][0])
     # the timed region again, with only the dominant class bracketed by events
     di = CLASSES.index(dom)
@@ -874,6 +1005,7 @@ def main():
     roof["launches"] = dom_n
     roof["avg_launch_us"] = dom_ms * 1e3 / max(dom_n, 1)
     roof["algorithmic_per_launch"] = {"bytes": by / max(dom_n, 1), "flops": fl / max(dom_n, 1)}
+    roof["operand_bytes_per_launch"] = opcosts[dom][0] * a.steps / max(dom_n, 1)
     gen_bytes = sum(v[0] for v in costs.values())
     gen_flops = sum(v[1] for v in costs.values())
     step_roof_ms = max(gen_bytes / (PEAK_HBM_GBS * 1e9), gen_flops / (peak_f * 1e12)) * 1e3
@@ -893,7 +1025,8 @@ def main():
         "step_roofline": {"generate_algorithmic_bytes": gen_bytes,
                           "generate_algorithmic_flops": gen_flops,
                           "roofline_ms": round(step_roof_ms, 4),
-                          "frac": round(step_roof_ms / ms_step, 4)},
+                          "frac": round(step_roof_ms / ms_step, 4),
+                          "generate_operand_bytes": sum(v[0] for v in opcosts.values())},
         "kernel_ms_per_generate": {n: round(per[n][0], 4) for n in CLASSES},
     }
 

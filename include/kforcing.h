@@ -110,7 +110,11 @@ size_t kf_state_bytes(const kf_config *cfg);
  * 256-byte aligned.  Re-binding discards weights and sequence state. */
 int kf_bind_state(kf_ctx *ctx, void *dev_ptr, size_t bytes);
 
-/* Load the weights from a flat blob: 16 int32 header words (magic 0x4B465731,
+/* Load the weights of the model the paper's model table defines (Appendix D:
+ * a causal Transformer backbone, its token and position embeddings, the
+ * noise encoder -- a sinusoid of u and a two-layer GELU MLP -- and, for a
+ * temperature-conditioned model, the temperature encoder; the head is tied
+ * to the token table) from a flat blob: 16 int32 header words (magic 0x4B465731,
  * version 1, n_layer, d_model, n_head, d_mlp, vocab, n_ctx, dtype, 7 zero
  * words) followed by every tensor as fp32 in a fixed order: token table
  * [V][d] (also the tied output head), position table [n_ctx][d], noise MLP
@@ -143,8 +147,10 @@ int kf_prefill(kf_ctx *ctx, int B, int N, const int32_t *prompt, int k, const fl
  * B must equal the prefill's B; k may change between calls; C+p+k <= n_ctx. */
 int kf_decode_block(kf_ctx *ctx, int B, int k, const float *noise, int32_t *out);
 
-/* Generate L new tokens per sequence (L % k == 0, N + L <= n_ctx): one
- * prefill and L/k - 1 decode blocks, with noise drawn on the device by
+/* The whole of Appendix C.1's algorithm "K-Forcing Inference with KV Cache"
+ * (its REQUIRE: prompt x_1..x_N, window k, generation length; its ENSURE: the
+ * generated tokens): generate L new tokens per sequence (L % k == 0,
+ * N + L <= n_ctx) as one prefill and L/k - 1 decode blocks, with noise drawn on the device by
  * Philox4x32-10 (key = seed, counter = (emitted position, sequence, 2, 0),
  * u = (word0 >> 8) * 2^-24).  out [B][L] holds positions N..N+L-1.  Leaves
  * the context decoded up to the last block (pending = last k tokens).

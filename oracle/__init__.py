@@ -68,6 +68,7 @@ def lib():
             f = getattr(L, "orc_seq_new" + sfx); f.restype = P; f.argtypes = [P]
             f = getattr(L, "orc_seq_free" + sfx); f.restype = None; f.argtypes = [P]
             f = getattr(L, "orc_seq_len" + sfx); f.restype = ctypes.c_int; f.argtypes = [P]
+            f = getattr(L, "orc_seq_copy" + sfx); f.restype = ctypes.c_int; f.argtypes = [P, P]
             f = getattr(L, "orc_seq_set_temperature" + sfx); f.restype = ctypes.c_int
             f.argtypes = [P, ctypes.c_double]
             f = getattr(L, "orc_seq_kv" + sfx); f.restype = None
@@ -151,6 +152,13 @@ class Seq:
     @property
     def C(self) -> int:
         return _f("orc_seq_len", self.model.prec)(self.h)
+
+    def copy(self) -> "Seq":
+        """A new sequence holding this one's committed context."""
+        s = Seq(self.model)
+        if _f("orc_seq_copy", self.model.prec)(s.h, self.h) < 0:
+            raise ValueError("oracle: sequence copy across models")
+        return s
 
     def set_temperature(self, tau: float) -> None:
         """Temperature conditioning of this sequence's later noise rows."""
@@ -571,6 +579,23 @@ def nnz_single(N: int, k: int) -> int:
 def nnz_double(N: int, k: int) -> int:
     """|M_D| closed form over the Future-2 queries (Appendix C.2)."""
     return k * N * (N + 1) // 2 + N * k * k + N * k * (k + 1) // 2
+
+
+def decode_batched(seqs: Sequence[Seq], pending: np.ndarray, k: int, u: np.ndarray) -> np.ndarray:
+    """One decode block over several sequences at once (one orc_step_batch
+    call, OpenMP over sequences): pending [B][nr] real rows, u [B][k] noise;
+    commits the real rows and returns the argmax tokens [B][k]."""
+    B = len(seqs)
+    model = seqs[0].model
+    arr = (ctypes.c_void_p * B)(*[s.h for s in seqs])
+    toks = np.ascontiguousarray(pending, np.int32).reshape(B, -1)
+    u = np.ascontiguousarray(u, np.float64).reshape(B, k)
+    logits = np.zeros((B, k, model.V), np.float64)
+    rc = _f("orc_step_batch", model.prec)(arr, B, toks.shape[1], _ip(toks), k, _dp(u), 1,
+                                         _dp(logits))
+    if rc < 0:
+        raise ValueError("oracle batched step rejected")
+    return np.stack([argmax(logits[b]) for b in range(B)])
 
 
 def generate_batched(model: Model, prompt: np.ndarray, L: int, k: int, seed: int) -> np.ndarray:

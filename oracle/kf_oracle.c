@@ -329,6 +329,26 @@ int SYM(orc_seq_set_temperature)(orc_seq *s, double tau) {
 
 int SYM(orc_seq_len)(const orc_seq *s) { return s->C; }
 
+/* Make dst hold src's committed context (keys, values, length, temperature
+ * embedding); both sequences must belong to the same model.  Returns -1 on a
+ * model mismatch. */
+int SYM(orc_seq_copy)(orc_seq *dst, const orc_seq *src) {
+  const orc_model *m = src->m;
+  if (dst->m != m) return -1;
+  size_t n = (size_t)m->L * m->T * m->d;
+  memcpy(dst->K, src->K, sizeof(REAL) * n);
+  memcpy(dst->Vc, src->Vc, sizeof(REAL) * n);
+  dst->C = src->C;
+  if (src->temb) {
+    if (!dst->temb) dst->temb = (REAL *)malloc(sizeof(REAL) * (size_t)m->d);
+    memcpy(dst->temb, src->temb, sizeof(REAL) * (size_t)m->d);
+  } else {
+    free(dst->temb);
+    dst->temb = NULL;
+  }
+  return 0;
+}
+
 /* Copy committed K or V of layer l, positions [0, C), into out[C][d] (as double). */
 void SYM(orc_seq_kv)(const orc_seq *s, int l, int which, double *out) {
   const orc_model *m = s->m;
@@ -360,36 +380,43 @@ int SYM(orc_step)(orc_seq *s, int nr, const int32_t *toks, int k, const double *
   for (int i = 0; i < nr; ++i)
     if (toks[i] < 0 || toks[i] >= V) return -1;
 
+  /* Rows are independent inside each loop below (a row's dot products, norm
+   * and attention read only earlier results), so the row loops run over
+   * OpenMP threads; every row is computed in the same order as a serial run,
+   * so the results do not depend on the thread count.  Called from inside
+   * orc_step_batch's parallel region, these regions are inactive (serial). */
   REAL *X = (REAL *)malloc(sizeof(REAL) * (size_t)n * d);
-  REAL *A = (REAL *)malloc(sizeof(REAL) * (size_t)d);
-  REAL *QKV = (REAL *)malloc(sizeof(REAL) * 3 * (size_t)d);
   REAL *Q = (REAL *)malloc(sizeof(REAL) * (size_t)n * d);
   REAL *Kn = (REAL *)malloc(sizeof(REAL) * (size_t)L * n * d);
   REAL *Vn = (REAL *)malloc(sizeof(REAL) * (size_t)L * n * d);
   REAL *O = (REAL *)malloc(sizeof(REAL) * (size_t)n * d);
-  REAL *Y = (REAL *)malloc(sizeof(REAL) * (size_t)(f > 4 * d ? f : 4 * d));
-  REAL *Z = (REAL *)malloc(sizeof(REAL) * (size_t)d);
-  REAL *P = (REAL *)malloc(sizeof(REAL) * (size_t)(C + n));
-  const REAL **kp = (const REAL **)malloc(sizeof(REAL *) * (size_t)(C + n));
-  const REAL **vp = (const REAL **)malloc(sizeof(REAL *) * (size_t)(C + n));
+  const size_t wide = (size_t)(f > 4 * d ? f : 4 * d);
   double dev = 0;
 
   /* Embedding (algorithm: Embed for real rows, NoiseEnc for noise rows). */
-  for (int r = 0; r < n; ++r) {
-    REAL *x = X + (size_t)r * d;
-    const REAL *pe = m->pos + (size_t)(C + r) * d;
-    if (r < nr) {
-      const REAL *te = m->tok + (size_t)toks[r] * d;
-      for (int i = 0; i < d; ++i) x[i] = te[i] + (m->rope ? (REAL)0 : pe[i]);
-    } else {
-      sinusoid(u[r - nr], d, A);
-      linear(A, m->nw1, m->nb1, d, 4 * d, Y);
-      for (int i = 0; i < 4 * d; ++i) Y[i] = gelu(Y[i]);
-      linear(Y, m->nw2, m->nb2, 4 * d, d, Z);
-      for (int i = 0; i < d; ++i) x[i] = Z[i] + (m->rope ? (REAL)0 : pe[i]);
-      if (s->temb)
-        for (int i = 0; i < d; ++i) x[i] += s->temb[i];
+#pragma omp parallel
+  {
+    REAL *A = (REAL *)malloc(sizeof(REAL) * (size_t)d);
+    REAL *Y = (REAL *)malloc(sizeof(REAL) * wide);
+    REAL *Z = (REAL *)malloc(sizeof(REAL) * (size_t)d);
+#pragma omp for schedule(static)
+    for (int r = 0; r < n; ++r) {
+      REAL *x = X + (size_t)r * d;
+      const REAL *pe = m->pos + (size_t)(C + r) * d;
+      if (r < nr) {
+        const REAL *te = m->tok + (size_t)toks[r] * d;
+        for (int i = 0; i < d; ++i) x[i] = te[i] + (m->rope ? (REAL)0 : pe[i]);
+      } else {
+        sinusoid(u[r - nr], d, A);
+        linear(A, m->nw1, m->nb1, d, 4 * d, Y);
+        for (int i = 0; i < 4 * d; ++i) Y[i] = gelu(Y[i]);
+        linear(Y, m->nw2, m->nb2, 4 * d, d, Z);
+        for (int i = 0; i < d; ++i) x[i] = Z[i] + (m->rope ? (REAL)0 : pe[i]);
+        if (s->temb)
+          for (int i = 0; i < d; ++i) x[i] += s->temb[i];
+      }
     }
+    free(A); free(Y); free(Z);
   }
 
   const REAL scale = (REAL)(1.0 / sqrt((double)dh));
@@ -398,40 +425,65 @@ int SYM(orc_step)(orc_seq *s, int nr, const int32_t *toks, int k, const double *
     REAL *kn = Kn + (size_t)l * n * d, *vn = Vn + (size_t)l * n * d;
     const REAL *kc = s->K + (size_t)l * m->T * d, *vc = s->Vc + (size_t)l * m->T * d;
     /* q, k, v of every new row */
-    for (int r = 0; r < n; ++r) {
-      norm(m, X + (size_t)r * d, y->ln1_g, y->ln1_b, A);
-      linear(A, y->wqkv, y->bqkv, d, 3 * d, QKV);
-      if (m->rope) { /* row r sits at position C + r */
-        rope(QKV, H, dh, C + r);
-        rope(QKV + d, H, dh, C + r);
+#pragma omp parallel
+    {
+      REAL *A = (REAL *)malloc(sizeof(REAL) * (size_t)d);
+      REAL *QKV = (REAL *)malloc(sizeof(REAL) * 3 * (size_t)d);
+#pragma omp for schedule(static)
+      for (int r = 0; r < n; ++r) {
+        norm(m, X + (size_t)r * d, y->ln1_g, y->ln1_b, A);
+        linear(A, y->wqkv, y->bqkv, d, 3 * d, QKV);
+        if (m->rope) { /* row r sits at position C + r */
+          rope(QKV, H, dh, C + r);
+          rope(QKV + d, H, dh, C + r);
+        }
+        memcpy(Q + (size_t)r * d, QKV, sizeof(REAL) * d);
+        memcpy(kn + (size_t)r * d, QKV + d, sizeof(REAL) * d);
+        memcpy(vn + (size_t)r * d, QKV + 2 * d, sizeof(REAL) * d);
       }
-      memcpy(Q + (size_t)r * d, QKV, sizeof(REAL) * d);
-      memcpy(kn + (size_t)r * d, QKV + d, sizeof(REAL) * d);
-      memcpy(vn + (size_t)r * d, QKV + 2 * d, sizeof(REAL) * d);
+      free(A); free(QKV);
     }
     /* causal attention: row r sees cache [0, C) then new rows [0, r] */
-    for (int r = 0; r < n; ++r) {
-      int nk = C + r + 1;
-      for (int h = 0; h < H; ++h) {
+#pragma omp parallel
+    {
+      REAL *P = (REAL *)malloc(sizeof(REAL) * (size_t)(C + n));
+      const REAL **kp = (const REAL **)malloc(sizeof(REAL *) * (size_t)(C + n));
+      const REAL **vp = (const REAL **)malloc(sizeof(REAL *) * (size_t)(C + n));
+      double tdev = 0;
+#pragma omp for schedule(dynamic, 1)
+      for (int rh = 0; rh < n * H; ++rh) {
+        const int r = rh / H, h = rh % H;
+        const int nk = C + r + 1;
         for (int t = 0; t < nk; ++t) {
           kp[t] = (t < C) ? kc + (size_t)t * d + h * dh : kn + (size_t)(t - C) * d + h * dh;
           vp[t] = (t < C) ? vc + (size_t)t * d + h * dh : vn + (size_t)(t - C) * d + h * dh;
         }
         REAL psum = attend(Q + (size_t)r * d + h * dh, kp, vp, nk, dh, scale, P, O + (size_t)r * d + h * dh);
         double dv = fabs((double)psum - 1.0);
-        if (dv > dev) dev = dv;
+        if (dv > tdev) tdev = dv;
       }
+#pragma omp critical
+      if (tdev > dev) dev = tdev;
+      free(P); free(kp); free(vp);
     }
     /* attention output projection + residual, then the MLP sub-block */
-    for (int r = 0; r < n; ++r) {
-      REAL *x = X + (size_t)r * d;
-      linear(O + (size_t)r * d, y->wo, y->bo, d, d, Z);
-      for (int i = 0; i < d; ++i) x[i] += Z[i];
-      norm(m, x, y->ln2_g, y->ln2_b, A);
-      linear(A, y->w1, y->b1, d, f, Y);
-      for (int i = 0; i < f; ++i) Y[i] = gelu(Y[i]);
-      linear(Y, y->w2, y->b2, f, d, Z);
-      for (int i = 0; i < d; ++i) x[i] += Z[i];
+#pragma omp parallel
+    {
+      REAL *A = (REAL *)malloc(sizeof(REAL) * (size_t)d);
+      REAL *Y = (REAL *)malloc(sizeof(REAL) * wide);
+      REAL *Z = (REAL *)malloc(sizeof(REAL) * (size_t)d);
+#pragma omp for schedule(static)
+      for (int r = 0; r < n; ++r) {
+        REAL *x = X + (size_t)r * d;
+        linear(O + (size_t)r * d, y->wo, y->bo, d, d, Z);
+        for (int i = 0; i < d; ++i) x[i] += Z[i];
+        norm(m, x, y->ln2_g, y->ln2_b, A);
+        linear(A, y->w1, y->b1, d, f, Y);
+        for (int i = 0; i < f; ++i) Y[i] = gelu(Y[i]);
+        linear(Y, y->w2, y->b2, f, d, Z);
+        for (int i = 0; i < d; ++i) x[i] += Z[i];
+      }
+      free(A); free(Y); free(Z);
     }
   }
 
@@ -442,8 +494,10 @@ int SYM(orc_step)(orc_seq *s, int nr, const int32_t *toks, int k, const double *
   int nh = k > 0 ? k : 1;
   int r0 = k > 0 ? nr : nr - 1;
   if (logits) {
+    REAL *A = (REAL *)malloc(sizeof(REAL) * (size_t)d);
     for (int j = 0; j < nh; ++j) {
       norm(m, X + (size_t)(r0 + j) * d, m->lnf_g, m->lnf_b, A);
+#pragma omp parallel for schedule(static)
       for (int v = 0; v < V; ++v) {
         const REAL *w = m->tok + (size_t)v * d;
         REAL sc = 0;
@@ -451,6 +505,7 @@ int SYM(orc_step)(orc_seq *s, int nr, const int32_t *toks, int k, const double *
         logits[(size_t)j * V + v] = (double)sc;
       }
     }
+    free(A);
   }
 
   /* cache commit: keep the real rows' K/V only */
@@ -464,8 +519,7 @@ int SYM(orc_step)(orc_seq *s, int nr, const int32_t *toks, int k, const double *
   }
   if (softmax_dev) *softmax_dev = dev;
 
-  free(X); free(A); free(QKV); free(Q); free(Kn); free(Vn); free(O); free(Y); free(Z); free(P);
-  free(kp); free(vp);
+  free(X); free(Q); free(Kn); free(Vn); free(O);
   return nh;
 }
 

@@ -46,3 +46,17 @@ def merge(stats: list) -> dict:
         for k in ("near", "near2", "mismatch_near"):
             out[k] += s[k]
     return out
+
+
+# Merged statistics of every parity configuration run in this session, by
+# name: the near-tie counts the tolerance rule exempts are part of the result
+# (tests/conftest.py prints them after the run and writes them to the JSON
+# file named by KF_PARITY_STATS, when set).
+RECORDED: dict = {}
+
+
+def report(name: str, stats: dict) -> dict:
+    """Print and record the merged statistics of one parity configuration."""
+    RECORDED[name] = dict(stats)
+    print(f"{name}: {stats}", flush=True)
+    return stats

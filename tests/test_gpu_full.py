@@ -18,7 +18,7 @@ import pytest
 
 import kf_synth as S
 import oracle as O
-from tests.parity_util import TOL, compare_head, merge
+from tests.parity_util import TOL, compare_head, merge, report
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
@@ -89,7 +89,7 @@ def test_lm1b_bf16_bench_configuration():
     kf = _ctx(LM1B, B, k, N)
     prompt = S.prompts_zipf(1, B, N, LM1B.vocab)
     st = _blocks(kf, _model(LM1B), prompt, [k, k, k], seed=2, tol=TOL[1], rows=[0, B - 1])
-    _log(f"lm1b bf16 B=64 parity: {st}")
+    report("lm1b bf16 B=64, prefill + 2 blocks", st)
 
 
 def test_lm1b_bf16_generate_last_block():
@@ -117,7 +117,7 @@ def test_lm1b_bf16_generate_last_block():
         ols = list(ex.map(last_block, rows))
     stats = [compare_head(gl[b], ol, out[b, L - k:], TOL[1], where=f"last block seq {b}")
              for b, ol in zip(rows, ols)]
-    _log(f"lm1b bf16 generate last-block parity: {merge(stats)}")
+    report("lm1b bf16 B=64 generate, last block (C=124)", merge(stats))
 
 
 def test_lm1b_fp32_tokens():
@@ -127,7 +127,7 @@ def test_lm1b_fp32_tokens():
     kf = _ctx(LM1B_F32, B, k, N)
     prompt = S.prompts_zipf(1, B, N, LM1B_F32.vocab)
     st = _blocks(kf, _model(LM1B_F32), prompt, [k, k], seed=2, tol=TOL[0], rows=[0, B - 1])
-    _log(f"lm1b fp32 parity: {st}")
+    report("lm1b fp32 B=4, prefill + 1 block", st)
 
 
 @pytest.mark.parametrize("B", [64, 13, 1])
@@ -167,7 +167,7 @@ def test_owt_shape_prefill_decode():
     kf = _ctx(OWT, B, k, N)
     prompt = S.prompts_zipf(1, B, N, OWT.vocab)
     st = _blocks(kf, _model(OWT), prompt, [k, k], seed=2, tol=TOL[1], rows=[0, B - 1])
-    _log(f"owt bf16 parity: {st}")
+    report("owt bf16 B=4, prompt 64, prefill + 1 block", st)
 
 
 def test_owt_batch1_decode():
@@ -178,7 +178,7 @@ def test_owt_batch1_decode():
     kf = _ctx(OWT, B, 4, N)
     prompt = S.prompts_zipf(1, B, N, OWT.vocab)
     st = _blocks(kf, _model(OWT), prompt, [4, 4, 4, 2, 1], seed=4, tol=TOL[1], rows=[0])
-    _log(f"owt bf16 B=1 parity: {st}")
+    report("owt bf16 B=1, prompt 128, k 4,4,4,2,1", st)
 
 
 def test_owt_batch16_decode():
@@ -189,7 +189,7 @@ def test_owt_batch16_decode():
     kf = _ctx(OWT, B, k, N)
     prompt = S.prompts_zipf(1, B, N, OWT.vocab)
     st = _blocks(kf, _model(OWT), prompt, [k, k, k], seed=6, tol=TOL[1], rows=[0, B - 1])
-    _log(f"owt bf16 B=16 parity: {st}")
+    report("owt bf16 B=16, prompt 64, prefill + 2 blocks", st)
 
 
 LARGE = S.WORKLOADS["large"]["cfg"]
@@ -201,7 +201,7 @@ def test_large_backbone_prefill_decode():
     kf = _ctx(LARGE, B, k, N)
     prompt = S.prompts_zipf(1, B, N, LARGE.vocab)
     st = _blocks(kf, _model(LARGE), prompt, [k, k], seed=2, tol=TOL[1], rows=[0, 1])
-    _log(f"large bf16 parity: {st}")
+    report("large bf16 B=2, prefill + 1 block", st)
 
 
 def test_owt_batch512_decode():
@@ -213,7 +213,7 @@ def test_owt_batch512_decode():
     kf = _ctx(OWT, B, k, N)
     prompt = S.prompts_zipf(1, B, N, OWT.vocab)
     st = _blocks(kf, _model(OWT), prompt, [k, k, k], seed=3, tol=TOL[1], rows=[0, 257, B - 1])
-    _log(f"owt bf16 B=512 parity: {st}")
+    report("owt bf16 B=512, prefill + 2 blocks", st)
 
 
 def test_large_backbone_batch256():
@@ -224,4 +224,4 @@ def test_large_backbone_batch256():
     kf = _ctx(LARGE, B, k, N)
     prompt = S.prompts_zipf(1, B, N, LARGE.vocab)
     st = _blocks(kf, _model(LARGE), prompt, [k, k], seed=4, tol=TOL[1], rows=[0, B - 1])
-    _log(f"large bf16 B=256 parity: {st}")
+    report("large bf16 B=256, prefill + 1 block", st)

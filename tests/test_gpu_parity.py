@@ -9,7 +9,7 @@ import pytest
 
 import kf_synth as S
 import oracle as O
-from tests.parity_util import TOL, compare_head, merge
+from tests.parity_util import TOL, compare_head, merge, report
 
 pytestmark = pytest.mark.gpu
 
@@ -90,7 +90,7 @@ def test_toy_prefill_and_decode(toy):
     kf = _ctx(TOY, 4, 4, 16, blob)
     prompt = S.prompts_uniform(1, 4, 16, TOY.vocab)
     st = run_teacher_forced(kf, model, prompt, [4] * 16, noise_seed=2, tol=TOL[0])
-    _log(f"toy fp32 parity: {st}")
+    report("toy fp32 B=4, prefill + 3 blocks", st)
     assert st["max_rel"] < 1e-4
 
 
@@ -114,7 +114,7 @@ def test_ragged_and_variable_k(toy):
     kf = _ctx(TOY, 5, 4, 40, blob)
     prompt = S.prompts_uniform(5, 3, 37, TOY.vocab)
     st = run_teacher_forced(kf, model, prompt, [3, 1, 4, 2, 4, 1, 1, 3], noise_seed=9, tol=TOL[0])
-    _log(f"ragged/variable-k parity: {st}")
+    report("toy fp32 ragged / variable k", st)
 
 
 def test_empty_prompt(toy):
@@ -123,7 +123,7 @@ def test_empty_prompt(toy):
     kf = _ctx(TOY, 2, 4, 16, blob)
     prompt = np.zeros((2, 0), np.int32)
     st = run_teacher_forced(kf, model, prompt, [4, 4, 2], noise_seed=4, tol=TOL[0])
-    _log(f"empty-prompt parity: {st}")
+    report("toy fp32 empty prompt", st)
 
 
 def test_fill_context_to_capacity(toy):
@@ -268,7 +268,7 @@ def test_toy_bf16(toy):
     kf = _ctx(TOY_BF16, 4, 4, 16, blob)
     prompt = S.prompts_uniform(1, 4, 16, TOY_BF16.vocab)
     st = run_teacher_forced(kf, model, prompt, [4] * 8, noise_seed=2, tol=TOL[1])
-    _log(f"toy bf16 parity: {st}")
+    report("toy bf16", st)
 
 
 def test_graph_replay_matches_direct(toy):

@@ -13,7 +13,7 @@ import pytest
 
 import kf_synth as S
 import oracle as O
-from tests.parity_util import TOL, compare_head, merge
+from tests.parity_util import TOL, compare_head, merge, report
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
@@ -72,7 +72,7 @@ def test_rms_rope_prefill_decode(cfg):
     _log(f"rms/rope dh={cfg.d_head} prefill + decode")
     st = _teacher_forced(kf, O.Model(blob), prompt, [4, 3, 1, 4, 2], seed=12, tol=TOL[0],
                          rows=range(3))
-    _log(f"rms/rope dh={cfg.d_head}: {st}")
+    report(f"rms/rope d_head {cfg.d_head}", st)
     assert kf.device_errors() == 0
 
 
@@ -110,7 +110,7 @@ def test_lm1b_shape_rms_rope_bf16(B):
     prompt = S.prompts_zipf(2, B, 16, LM1B_R.vocab)
     st = _teacher_forced(kf, O.Model(blob), prompt, [4, 4, 4], seed=6, tol=TOL[1],
                          rows=sorted({0, B // 2 - 1, B - 1}))
-    _log(f"lm1b rms/rope bf16 B={B}: {st}")
+    report(f"lm1b rms/rope bf16 B={B}", st)
 
 
 def test_rms_rope_generate():

@@ -16,7 +16,7 @@ import pytest
 
 import kf_synth as S
 import oracle as O
-from tests.parity_util import TOL, compare_head, merge
+from tests.parity_util import TOL, compare_head, merge, report
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
@@ -216,7 +216,7 @@ def test_serving_lm1b_bf16():
         order = [0, 1, 4, 6, 7]
         sv.rng.shuffle(order)
         sv.step(order, 4)
-    _log(f"serving lm1b bf16: {merge(sv.stats)}")
+    report("serving lm1b bf16", merge(sv.stats))
 
 
 def test_serving_bf16_dh128_pages():
@@ -233,7 +233,7 @@ def test_serving_bf16_dh128_pages():
         sv.step([0, 2] if it % 2 else [2, 0], 4)
     assert sv.C[0] > 128 and sv.C[2] > 128
     sv.step([3], 4)
-    _log(f"serving bf16 d_head 128: {merge(sv.stats)}")
+    report("serving bf16 d_head 128", merge(sv.stats))
 
 
 def test_serving_graph_replay_matches_direct():

@@ -9,7 +9,7 @@ import pytest
 
 import kf_synth as S
 import oracle as O
-from tests.parity_util import TOL, compare_head, merge
+from tests.parity_util import TOL, compare_head, merge, report
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
@@ -66,7 +66,7 @@ def test_toy_temperature_parity():
     prompt = S.prompts_uniform(1, 4, 16, TOY_T.vocab)
     st = _teacher_forced(kf, O.Model(blob), prompt, [0.05, 0.3, 0.7, 1.0], [4, 4, 2],
                          seed=9, tol=TOL[0], rows=range(4))
-    _log(f"toy temperature parity: {st}")
+    report("toy fp32 temperature", st)
 
 
 def test_temperature_required_and_changeable():
@@ -109,4 +109,4 @@ def test_lm1b_shape_temperature_bf16(B):
     taus = np.linspace(0.01, 1.0, B)
     st = _teacher_forced(kf, O.Model(blob), prompt, taus, [4, 4], seed=5, tol=TOL[1],
                          rows=[0, B - 1])
-    _log(f"lm1b temperature bf16 B={B} parity: {st}")
+    report(f"lm1b bf16 temperature B={B}", st)

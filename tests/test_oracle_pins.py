@@ -516,6 +516,41 @@ def test_generate_matches_manual_steps(small):
     assert list(toks[0]) == list(t) + list(t2)
 
 
+def test_generate_batched_equals_generate(toy):
+    """The batched driver (one orc_step_batch call per block, OpenMP over
+    sequences), which the CPU baseline times, emits exactly the tokens of
+    generate() on the toy workload, in both instantiations."""
+    blob, m = toy
+    w = S.WORKLOADS["toy"]
+    prompt = S.prompts_uniform(1, w["B"], w["N"], w["cfg"].vocab)
+    for model in (m, O.Model(blob, "f32")):
+        want, passes = O.generate(model, prompt, w["L"], w["k"], seed=9)
+        got = O.generate_batched(model, prompt, w["L"], w["k"], seed=9)
+        assert passes == w["L"] // w["k"]
+        assert np.array_equal(got, want)
+
+
+def test_step_independent_of_thread_count(toy):
+    """The row loops of a step run over OpenMP threads; each row is computed in
+    the same order whatever the thread count, so logits and the committed
+    cache are identical bit for bit with one thread and with several."""
+    import ctypes
+    _, m = toy
+    gomp = ctypes.CDLL("libgomp.so.1")
+    res = []
+    try:
+        for n in (1, 5):
+            gomp.omp_set_num_threads(n)
+            s = m.seq()
+            la, _ = s.step(list(range(37)), [0.25, 0.5, 0.75], commit=True)
+            lb, _ = s.step([3, 1, 4], [0.1, 0.9, 0.2], commit=True)
+            res.append((la, lb, s.kv(1, 0), s.kv(0, 1)))
+    finally:
+        gomp.omp_set_num_threads(os.cpu_count() or 1)
+    for x, y in zip(*res):
+        assert np.array_equal(x, y)
+
+
 def test_f32_instantiation_close(toy):
     """The fp32 instantiation (CPU timing) computes the same function."""
     blob, m = toy
