@@ -147,6 +147,29 @@ int kf_prefill(kf_ctx *ctx, int B, int N, const int32_t *prompt, int k, const fl
  * B must equal the prefill's B; k may change between calls; C+p+k <= n_ctx. */
 int kf_decode_block(kf_ctx *ctx, int B, int k, const float *noise, int32_t *out);
 
+/* kf_decode_block for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same decode block, bit for bit, with the step's partial results -- the
+ * attention key-split states, the split-K parts and the head's per-tile
+ * argmax partials -- held in a device array of the library instead of the
+ * state buffer's workspace.  The array is KF_NOALLOC_SCRATCH_BYTES (about
+ * 20 MiB), one copy per GPU the library runs on, kept until the process ends;
+ * its address is looked up once per GPU by kf_bind_state.  The call allocates
+ * nothing and needs nothing cleared (every partial result is written before it
+ * is read within the call).  Every call on one GPU shares that GPU's copy:
+ * calls that overlap on one GPU (several contexts or streams at once) race
+ * and must be serialised by the caller.
+ * Returns what kf_decode_block returns, plus KF_EINVAL when B * k *
+ * ceil(V / 128) exceeds KF_NOALLOC_HEAD_ENTRIES, and KF_EHIP when the array's
+ * address could not be found for the state buffer's GPU. */
+#define KF_NOALLOC_ATTN_ENTRIES 8192        /* attention key-split states, d_head <= 128 */
+#define KF_NOALLOC_SPLIT_BYTES (8u << 20)   /* split-K fp32 parts */
+#define KF_NOALLOC_HEAD_ENTRIES (1u << 20)  /* head argmax partials (value and index each) */
+#define KF_NOALLOC_SCRATCH_BYTES \
+  ((size_t)KF_NOALLOC_ATTN_ENTRIES * (2 + 128) * 4 + KF_NOALLOC_SPLIT_BYTES + \
+   (size_t)KF_NOALLOC_HEAD_ENTRIES * 8)
+int kf_decode_block_noalloc(kf_ctx *ctx, int B, int k, const float *noise, int32_t *out);
+
 /* The whole of Appendix C.1's algorithm "K-Forcing Inference with KV Cache"
  * (its REQUIRE: prompt x_1..x_N, window k, generation length; its ENSURE: the
  * generated tokens): generate L new tokens per sequence (L % k == 0,

@@ -71,6 +71,7 @@ def lib():
         "kf_load_weights": (I, [P, P, SZ, I]),
         "kf_prefill": (I, [P, I, I, P, I, P, P]),
         "kf_decode_block": (I, [P, I, I, P, P]),
+        "kf_decode_block_noalloc": (I, [P, I, I, P, P]),
         "kf_generate": (I, [P, I, I, P, I, I, U64, P]),
         "kf_prefill_ar": (I, [P, I, I, P, P, P]),
         "kf_decode_ar": (I, [P, I, P, P]),
@@ -186,6 +187,16 @@ class KForcing:
         if out is None:
             out = self.torch.empty((B, k), dtype=self.torch.int32, device=self.device)
         self._check(self.L.kf_decode_block(self.h, B, k, self._p(noise), self._p(out)))
+        return out
+
+    def decode_block_noalloc(self, noise, out=None):
+        """kf_decode_block with the step's partial results in the library's
+        device scratch (no allocation inside the call)."""
+        noise = self._f32(noise)
+        B, k = noise.shape
+        if out is None:
+            out = self.torch.empty((B, k), dtype=self.torch.int32, device=self.device)
+        self._check(self.L.kf_decode_block_noalloc(self.h, B, k, self._p(noise), self._p(out)))
         return out
 
     def generate(self, prompt, L: int, k: int, seed: int, out=None):

@@ -11,6 +11,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -270,6 +271,10 @@ struct kf_ctx {
   std::vector<Ev> evs;
   size_t ev_used = 0;
   bool ev_open = false;
+  // device scratch of kf_decode_block_noalloc on the state buffer's GPU (its
+  // address from hipGetSymbolAddress), or null with the reason in scratch_err
+  char* scratch = nullptr;
+  std::string scratch_err;
   // HIP-graph replay of the fixed-shape decode block of a generation run
   bool graphs = true;
   hipGraphExec_t gexec = nullptr;
@@ -348,6 +353,17 @@ int ev_end(kf_ctx* c) {
     if (e_ != hipSuccess) return hip_fail((ctx), e_, #expr);     \
   } while (0)
 
+// Partial-result buffers of one step (attention key-split states, split-K
+// parts, head argmax partials).
+struct Scratch {
+  float *att_m, *att_l, *att_o;
+  int att_entries;
+  float* split;
+  size_t split_bytes;
+  float* pval;
+  int* pidx;
+};
+
 // Inputs of one step.
 struct StepIn {
   int B, nr, k;              // sequences, real rows, noise rows (k == 0: AR step)
@@ -367,7 +383,11 @@ struct StepIn {
   // when toks_by_slot (the pending-token buffer)
   bool serve = false;
   bool toks_by_slot = false;
+  // kf_decode_block_noalloc: partial results in the library's device scratch
+  // instead of the state buffer's workspace
+  const Scratch* scr = nullptr;
 };
+
 
 template <typename T>
 int run_step(kf_ctx* c, const StepIn& in) {
@@ -381,10 +401,18 @@ int run_step(kf_ctx* c, const StepIn& in) {
   T* Xh = reinterpret_cast<T*>(base + p.Xh);  // compute-dtype residual copy (X itself for fp32)
   float2* lnst = reinterpret_cast<float2*>(base + p.lnst);
   const T* temb = (cf.flags & KF_FLAG_TEMPERATURE) ? reinterpret_cast<const T*>(base + p.temb) : nullptr;
-  const kf::AttnSplit asp{reinterpret_cast<float*>(base + p.att_m),
-                          reinterpret_cast<float*>(base + p.att_l),
-                          reinterpret_cast<float*>(base + p.att_o), kAttnEntries, 1};
-  const kf::SplitWs sws{reinterpret_cast<float*>(base + p.split_part), kSplitBytes};
+  kf::AttnSplit asp{reinterpret_cast<float*>(base + p.att_m),
+                    reinterpret_cast<float*>(base + p.att_l),
+                    reinterpret_cast<float*>(base + p.att_o), kAttnEntries, 1};
+  kf::SplitWs sws{reinterpret_cast<float*>(base + p.split_part), kSplitBytes};
+  float* pval = reinterpret_cast<float*>(base + p.pval);
+  int* pidx = reinterpret_cast<int*>(base + p.pidx);
+  if (in.scr) {
+    asp = kf::AttnSplit{in.scr->att_m, in.scr->att_l, in.scr->att_o, in.scr->att_entries, 1};
+    sws = kf::SplitWs{in.scr->split, in.scr->split_bytes};
+    pval = in.scr->pval;
+    pidx = in.scr->pidx;
+  }
   T* A = reinterpret_cast<T*>(base + p.A);  // noise sinusoid staging
   T* Q = reinterpret_cast<T*>(base + p.Q);
   T* O = reinterpret_cast<T*>(base + p.O);
@@ -487,14 +515,11 @@ int run_step(kf_ctx* c, const StepIn& in) {
   float* logits = (ar || debug) ? reinterpret_cast<float*>(base + p.logits) : nullptr;
   const kf::LnFold lnf{F(p.head_c1), F(p.head_c2), lnst, rms};
   KF_LAUNCH(c, KF_KC_HEAD,
-            kf::gemm_head_ln<T>(Xh, lnf, W(p.head_w), Mh, p.Vpad, V, d, ar ? 2 : 1, g,
-                                reinterpret_cast<float*>(base + p.pval),
-                                reinterpret_cast<int*>(base + p.pidx), logits, s));
+            kf::gemm_head_ln<T>(Xh, lnf, W(p.head_w), Mh, p.Vpad, V, d, ar ? 2 : 1, g, pval, pidx,
+                                logits, s));
   if (!ar)
     KF_LAUNCH(c, KF_KC_SELECT,
-              kf::launch_argmax_select(reinterpret_cast<const float*>(base + p.pval),
-                                       reinterpret_cast<const int*>(base + p.pidx), p.n_tiles, g,
-                                       st, in.od, s));
+              kf::launch_argmax_select(pval, pidx, p.n_tiles, g, st, in.od, s));
   else
     KF_LAUNCH(c, KF_KC_SELECT,
               kf::launch_icdf_select(logits, V, in.u_ar, in.seed, g, st, in.od, s));
@@ -851,6 +876,73 @@ void serve_free(kf_ctx* c, int q) {
 // ==================================================================== ABI
 extern "C" {
 
+// ------------------------------------------------ decode without allocation
+// The partial results of kf_decode_block_noalloc live in this file-scope
+// device array, one copy per GPU the library runs on, kept until the process
+// ends.  In host code its name is not a device address: each GPU's copy is
+// found once through hipGetSymbolAddress with that GPU current, and only that
+// address is used afterwards.  Regions (256-byte aligned): attention key-split
+// states m, l [entries] and o [entries][128]; split-K parts; head argmax
+// values and indices [entries] each.
+namespace {
+constexpr size_t kNaAttnM = 0;
+constexpr size_t kNaAttnL = kNaAttnM + (size_t)KF_NOALLOC_ATTN_ENTRIES * 4;
+constexpr size_t kNaAttnO = kNaAttnL + (size_t)KF_NOALLOC_ATTN_ENTRIES * 4;
+constexpr size_t kNaSplit = kNaAttnO + (size_t)KF_NOALLOC_ATTN_ENTRIES * 128 * 4;
+constexpr size_t kNaPval = kNaSplit + (size_t)KF_NOALLOC_SPLIT_BYTES;
+constexpr size_t kNaPidx = kNaPval + (size_t)KF_NOALLOC_HEAD_ENTRIES * 4;
+constexpr size_t kNaEnd = kNaPidx + (size_t)KF_NOALLOC_HEAD_ENTRIES * 4;
+static_assert(kNaEnd == KF_NOALLOC_SCRATCH_BYTES, "scratch layout");
+static_assert(kNaAttnL % 256 == 0 && kNaAttnO % 256 == 0 && kNaSplit % 256 == 0 &&
+                  kNaPval % 256 == 0 && kNaPidx % 256 == 0,
+              "aligned regions");
+}  // namespace
+
+static __device__ __align__(256) char scratch[KF_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char* g_scratch[kMaxDevices] = {};
+
+// Address of the scratch copy on the GPU that holds ctx's state buffer,
+// looked up once per GPU (with that GPU current).  A failure is kept in
+// scratch_err and reported by kf_decode_block_noalloc only.
+void find_scratch(kf_ctx* c) {
+  c->scratch = nullptr;
+  c->scratch_err.clear();
+  hipPointerAttribute_t at{};
+  hipError_t e = hipPointerGetAttributes(&at, c->base);
+  if (e != hipSuccess) {
+    c->scratch_err = std::string("hipPointerGetAttributes: ") + hipGetErrorString(e);
+    (void)hipGetLastError();  // not left for the launch checks of later calls
+    return;
+  }
+  const int dev = at.device;
+  if (dev < 0 || dev >= kMaxDevices) {
+    c->scratch_err = "state buffer on device " + std::to_string(dev) + ", beyond the scratch table";
+    return;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    int cur = -1;
+    e = hipGetDevice(&cur);
+    if (e == hipSuccess && cur != dev) e = hipSetDevice(dev);
+    void* ptr = nullptr;
+    if (e == hipSuccess) e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (cur >= 0 && cur != dev) (void)hipSetDevice(cur);
+    if (e != hipSuccess || !ptr) {
+      c->scratch_err = std::string("hipGetSymbolAddress(scratch): ") +
+                       (e != hipSuccess ? hipGetErrorString(e) : "null address");
+      (void)hipGetLastError();
+      return;
+    }
+    g_scratch[dev] = static_cast<char*>(ptr);
+  }
+  c->scratch = g_scratch[dev];
+}
+}  // namespace
+
 const char* kf_strerror(int code) {
   switch (code) {
     case KF_OK: return "ok";
@@ -910,6 +1002,7 @@ int kf_bind_state(kf_ctx* c, void* dev_ptr, size_t bytes) {
   c->live = false;
   c->B = c->C = c->pending = 0;
   serve_reset(c);
+  find_scratch(c);
   return KF_OK;
 }
 
@@ -1104,6 +1197,40 @@ int kf_decode_block(kf_ctx* c, int B, int k, const float* noise, int32_t* out) {
   if (c->C + c->pending + k > cf.n_ctx)
     return fail(c, KF_ECTX, "C + pending + k = %d exceeds n_ctx = %d", c->C + c->pending + k, cf.n_ctx);
   StepIn in{B, c->pending, k, pend_ptr(c), cf.max_k, noise, nullptr, 0, out_desc(c, out, k, -1), false};
+  r = step(c, in);
+  if (r) return r;
+  c->C += c->pending;
+  c->pending = k;
+  return KF_OK;
+}
+
+int kf_decode_block_noalloc(kf_ctx* c, int B, int k, const float* noise, int32_t* out) {
+  if (!c) return KF_EINVAL;
+  const kf_config& cf = c->cfg;
+  if (k < 1 || k > cf.max_k) return fail(c, KF_EINVAL, "k=%d outside [1, %d]", k, cf.max_k);
+  if (!noise || !out) return fail(c, KF_EINVAL, "null pointer argument");
+  const long long heads = (long long)B * k * c->plan.n_tiles;
+  if (heads > KF_NOALLOC_HEAD_ENTRIES)
+    return fail(c, KF_EINVAL,
+                "B*k*ceil(V/128) = %lld head partials exceed the device scratch maximum of %d "
+                "(KF_NOALLOC_HEAD_ENTRIES)",
+                heads, KF_NOALLOC_HEAD_ENTRIES);
+  int r = ready(c);
+  if (r) return r;
+  r = temp_ready(c, B);
+  if (r) return r;
+  if (!c->live) return fail(c, KF_ESTATE, "decode before prefill");
+  if (B != c->B) return fail(c, KF_ESTATE, "B=%d differs from the prefill's B=%d", B, c->B);
+  if (c->C + c->pending + k > cf.n_ctx)
+    return fail(c, KF_ECTX, "C + pending + k = %d exceeds n_ctx = %d", c->C + c->pending + k, cf.n_ctx);
+  if (!c->scratch) return fail(c, KF_EHIP, "device scratch unavailable: %s", c->scratch_err.c_str());
+  char* b = c->scratch;
+  const Scratch scr{reinterpret_cast<float*>(b + kNaAttnM), reinterpret_cast<float*>(b + kNaAttnL),
+                    reinterpret_cast<float*>(b + kNaAttnO), KF_NOALLOC_ATTN_ENTRIES,
+                    reinterpret_cast<float*>(b + kNaSplit), (size_t)KF_NOALLOC_SPLIT_BYTES,
+                    reinterpret_cast<float*>(b + kNaPval), reinterpret_cast<int*>(b + kNaPidx)};
+  StepIn in{B, c->pending, k, pend_ptr(c), cf.max_k, noise, nullptr, 0, out_desc(c, out, k, -1), false};
+  in.scr = &scr;
   r = step(c, in);
   if (r) return r;
   c->C += c->pending;

@@ -52,6 +52,19 @@ def test_every_declared_symbol_is_exported(L):
     assert set(names) <= exported, set(names) - exported
 
 
+def test_noalloc_decode_rejects_oversized_head(L):
+    """kf_decode_block_noalloc holds at most KF_NOALLOC_HEAD_ENTRIES head
+    partials (B * k * ceil(V / 128)) in its device scratch: a larger step is
+    rejected with a message naming the limit, before any state check."""
+    cfg = _cfg(d_model=64, n_head=1, d_mlp=64, vocab=1 << 20, max_batch=64, max_k=4)
+    h = _ctx(L, cfg)
+    fake = ctypes.c_void_p(0x10000)
+    assert L.kf_decode_block_noalloc(h, 33, 4, fake, fake) == Bd.KF_EINVAL  # 132 * 8192 > 2^20
+    assert b"KF_NOALLOC_HEAD_ENTRIES" in L.kf_last_error(h)
+    assert L.kf_decode_block_noalloc(h, 32, 4, fake, fake) == Bd.KF_ESTATE  # 128 * 8192 fits
+    L.kf_destroy(h)
+
+
 def test_strerror(L):
     assert L.kf_strerror(Bd.KF_OK) == b"ok"
     assert L.kf_strerror(Bd.KF_ECTX) == b"context length exceeded"
@@ -109,6 +122,9 @@ def test_state_machine_without_device(L):
     assert L.kf_prefill_ar(h, 2, 0, fake, fake, fake) == Bd.KF_EINVAL
     assert L.kf_generate_ar(h, 2, 4, fake, -1, 0, fake) == Bd.KF_EINVAL
     assert L.kf_decode_block(h, 2, 0, fake, fake) == Bd.KF_EINVAL
+    assert L.kf_decode_block_noalloc(h, 2, 2, fake, fake) == Bd.KF_ESTATE
+    assert L.kf_decode_block_noalloc(h, 2, 0, fake, fake) == Bd.KF_EINVAL
+    assert L.kf_decode_block_noalloc(h, 2, 2, None, fake) == Bd.KF_EINVAL
     assert L.kf_fill_noise(h, 0, 0, 0, 4, fake) == Bd.KF_EINVAL
     # binding: alignment and size
     need = L.kf_state_bytes(ctypes.byref(cfg))
