@@ -385,6 +385,39 @@ def summarize(root: str, write_json: str = None) -> None:
                 (int(r["Dispatch_Id"]), r["Kernel_Name"], float(r["Counter_Value"])))
     if not pmc:
         return
+    other = sorted(c for c in pmc if c not in ("FETCH_SIZE", "WRITE_SIZE"))
+    if other:
+        # mean per dispatch of every other counter, by kernel, and the MFMA busy
+        # fraction: SQ_VALU_MFMA_BUSY_CYCLES is summed over the 1024 SIMDs, so
+        # busy / 1024 / (kernel cycles) with the kernel's mean duration from a
+        # kernel trace in the same directory at the 2.4 GHz peak engine clock
+        durs = {}
+        for path in glob.glob(os.path.join(root, "**", "*_kernel_trace.csv"), recursive=True):
+            for r in csv.DictReader(open(path)):
+                if "Grid_Size" in r:
+                    grid = int(r["Grid_Size"])
+                else:
+                    grid = int(r["Grid_Size_X"]) * int(r["Grid_Size_Y"]) * int(r["Grid_Size_Z"])
+                key = (_short(r["Kernel_Name"]), grid)
+                durs.setdefault(key, []).append(float(r["End_Timestamp"]) - float(r["Start_Timestamp"]))
+        keys = sorted({k for c in other for k in pmc[c]},
+                      key=lambda k: -np.mean(pmc[other[0]].get(k, [0])))
+        print("| kernel | grid | dispatches | " + " | ".join(other) +
+              (" | mean us | MFMA busy |" if "SQ_VALU_MFMA_BUSY_CYCLES" in other else " |"))
+        print("|---|---|---|" + "---|" * len(other) +
+              ("---|---|" if "SQ_VALU_MFMA_BUSY_CYCLES" in other else ""))
+        for k in keys[:20]:
+            n = max(len(pmc[c].get(k, [])) for c in other)
+            vals = [np.mean(pmc[c][k]) if k in pmc[c] else float("nan") for c in other]
+            line = f"| {k[0]} | {k[1]} | {n} | " + " | ".join(f"{v:.4g}" for v in vals) + " |"
+            if "SQ_VALU_MFMA_BUSY_CYCLES" in other:
+                mb = np.mean(pmc["SQ_VALU_MFMA_BUSY_CYCLES"].get(k, [float("nan")]))
+                us = np.mean(durs[k]) / 1e3 if k in durs else float("nan")
+                line += f" {us:.2f} | {mb / 1024 / (us * 1e-6 * 2.4e9):.3f} |"
+            print(line)
+        print()
+    if "FETCH_SIZE" not in pmc and "WRITE_SIZE" not in pmc:
+        return
     # calibration: fp32 -> bf16 weight conversion of the token table reads 4n, writes 2n bytes
     conv = [k for k in pmc.get("FETCH_SIZE", {}) if k[0].startswith("convert_kernel")]
     cal = max(conv, key=lambda k: k[1]) if conv else None
