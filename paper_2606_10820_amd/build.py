@@ -16,7 +16,7 @@ OUT = os.path.join(PKG, "libkforcing.so")
 BUILD_DIR = os.path.join(PKG, "_build")
 
 SOURCES = ["kf_api.cpp", "kf_kernels.hip", "kf_gemm.hip", "kf_blockattn.hip"]
-HEADERS = ["kf_internal.h", "kf_lds.h"]
+HEADERS = ["kf_internal.h", "kf_lds.h", "kf_attn.h"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
