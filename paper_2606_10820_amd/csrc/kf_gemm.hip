@@ -664,27 +664,30 @@ __global__ void __launch_bounds__(256)
   for (int i = 0; i < S; ++i)
     if (i < nk) issue(i, i);
   if constexpr (NORM) {
-    float a = 0.f, b = 0.f;
+    // the row's mean from the group sums, then the merged squared deviations
+    float a = 0.f;
 #pragma unroll
-    for (int j = 0; j < PMAX; ++j) {
-      a += part[j].x + part[j].z;
-      b += part[j].y + part[j].w;
-    }
+    for (int j = 0; j < PMAX; ++j) a += part[j].x + part[j].z;
     for (int w = (tid % TPR) + PMAX * TPR; w < parts4; w += TPR) {  // wide rows only
       const float4 v = prow[w];
       a += v.x + v.z;
-      b += v.y + v.w;
     }
 #pragma unroll
-    for (int off = 1; off < TPR; off <<= 1) {
-      a += __shfl_xor(a, off, 64);
-      b += __shfl_xor(b, off, 64);
+    for (int off = 1; off < TPR; off <<= 1) a += __shfl_xor(a, off, 64);
+    const float mu = ga.rms ? 0.f : a / (float)K;
+    float b = 0.f;
+#pragma unroll
+    for (int j = 0; j < PMAX; ++j)
+      if ((tid % TPR) + j * TPR < parts4)
+        b += ln_group_sq(make_float2(part[j].x, part[j].y), mu) +
+             ln_group_sq(make_float2(part[j].z, part[j].w), mu);
+    for (int w = (tid % TPR) + PMAX * TPR; w < parts4; w += TPR) {
+      const float4 v = prow[w];
+      b += ln_group_sq(make_float2(v.x, v.y), mu) + ln_group_sq(make_float2(v.z, v.w), mu);
     }
-    if (tid % TPR == 0) {
-      const float mu = ga.rms ? 0.f : a / (float)K;
-      const float var = ga.rms ? b / (float)K : fmaxf(b / (float)K - mu * mu, 0.f);
-      sStat[tid / TPR] = make_float2(mu, 1.0f / sqrtf(var + 1e-5f));
-    }
+#pragma unroll
+    for (int off = 1; off < TPR; off <<= 1) b += __shfl_xor(b, off, 64);
+    if (tid % TPR == 0) sStat[tid / TPR] = make_float2(mu, 1.0f / sqrtf(b / (float)K + 1e-5f));
   }
   if (nk > S - 1) vm_wait<(S - 1) * PER>();
   else vm_wait<0>();
@@ -790,16 +793,8 @@ __global__ void __launch_bounds__(256)
           if (live) ep.store8(m, n, v);
           if constexpr (Ep::kStats) {
             // chunks 2j and 2j + 1 of a row (lanes c, c ^ 1) form 16-column group j
-            float a = 0.f, b = 0.f;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-              a += v[i];
-              b += v[i] * v[i];
-            }
-            a += __shfl_xor(a, 1, 64);
-            b += __shfl_xor(b, 1, 64);
-            if (live && (cc & 1) == 0)
-              ep.lnst[(size_t)ep.srow(m) * (ep.cols() / 16) + n / 16] = make_float2(a, b);
+            const float2 gs = ln_group16(v);
+            if (live && (cc & 1) == 0) ep.lnst[(size_t)ep.srow(m) * (ep.cols() / 16) + n / 16] = gs;
           }
         }
       }
@@ -1003,27 +998,22 @@ __global__ void __launch_bounds__(64 * KW)
   load(wa, xa, 0);
   if constexpr (NORM) {
     if (tid < 256) {
-      float a = 0.f, b = 0.f;
+      // the row's mean from the group sums, then the merged squared deviations
+      float a = 0.f;
 #pragma unroll
-      for (int i = 0; i < PS; ++i) {
-        a += ps[i].x;
-        b += ps[i].y;
-      }
-      for (int w = (tid & 15) + 16 * PS; w < K / 16; w += 16) {  // K > 1024 only
-        const float2 v = pr[w];
-        a += v.x;
-        b += v.y;
-      }
+      for (int i = 0; i < PS; ++i) a += ps[i].x;
+      for (int w = (tid & 15) + 16 * PS; w < K / 16; w += 16) a += pr[w].x;  // K > 1024 only
 #pragma unroll
-      for (int off = 1; off < 16; off <<= 1) {
-        a += __shfl_xor(a, off, 64);
-        b += __shfl_xor(b, off, 64);
-      }
-      if ((tid & 15) == 0) {
-        const float mu = ga.rms ? 0.f : a / (float)K;
-        const float var = ga.rms ? b / (float)K : fmaxf(b / (float)K - mu * mu, 0.f);
-        sStat[tid >> 4] = make_float2(mu, 1.0f / sqrtf(var + 1e-5f));
-      }
+      for (int off = 1; off < 16; off <<= 1) a += __shfl_xor(a, off, 64);
+      const float mu = ga.rms ? 0.f : a / (float)K;
+      float b = 0.f;
+#pragma unroll
+      for (int i = 0; i < PS; ++i)
+        if ((tid & 15) + 16 * i < K / 16) b += ln_group_sq(ps[i], mu);
+      for (int w = (tid & 15) + 16 * PS; w < K / 16; w += 16) b += ln_group_sq(pr[w], mu);
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) b += __shfl_xor(b, off, 64);
+      if ((tid & 15) == 0) sStat[tid >> 4] = make_float2(mu, 1.0f / sqrtf(b / (float)K + 1e-5f));
     }
   }
   for (int s = 0; s < steps; s += 2 * U) {
@@ -1080,15 +1070,8 @@ __global__ void __launch_bounds__(64 * KW)
   }
   if constexpr (Ep::kStats) {
     // chunks 0 and 1 of a row (lanes 2j, 2j + 1) form its 16-column group
-    float a = 0.f, b = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      a += v[i];
-      b += v[i] * v[i];
-    }
-    a += __shfl_xor(a, 1, 64);
-    b += __shfl_xor(b, 1, 64);
-    if (live && cc == 0) ep.lnst[(size_t)ep.srow(m) * (ep.cols() / 16) + n / 16] = make_float2(a, b);
+    const float2 gs = ln_group16(v);
+    if (live && cc == 0) ep.lnst[(size_t)ep.srow(m) * (ep.cols() / 16) + n / 16] = gs;
   }
 }
 
@@ -1141,15 +1124,8 @@ __global__ void __launch_bounds__(128)
     ep.store8(m, n, v);
   }
   if constexpr (Ep::kStats) {
-    float a = 0.f, b = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      a += v[i];
-      b += v[i] * v[i];
-    }
-    a += __shfl_xor(a, 1, 64);
-    b += __shfl_xor(b, 1, 64);
-    if (live && (c & 1) == 0) ep.lnst[(size_t)ep.srow(m) * (ep.cols() / 16) + n / 16] = make_float2(a, b);
+    const float2 gs = ln_group16(v);
+    if (live && (c & 1) == 0) ep.lnst[(size_t)ep.srow(m) * (ep.cols() / 16) + n / 16] = gs;
   }
 }
 

@@ -11,6 +11,49 @@ typedef __bf16 bf16;
 // Device-resident sequence state.  Kernels read the committed context length
 // C from here (never from a launch argument) so that a step's launches are
 // identical from one step to the next.
+// LayerNorm statistics of the residual stream, written by every kernel that
+// writes residual rows: per 16-column group of a row, (s, m2) = (the sum of
+// its 16 values, the sum of their squared deviations from the group mean
+// s / 16).  Consumers merge the groups of a row with the pairwise update of
+// Chan, Golub and LeVeque for equal counts: mean mu = (sum of s) / K and
+// K var = sum of (m2 + (s - 16 mu)^2 / 16), which has no E[x^2] - mu^2
+// cancellation when |mu| is large against the spread; with mu = 0 the same sum
+// is the row's sum of squares (RMSNorm).
+__host__ __device__ inline float ln_group_sq(float2 st, float mu) {
+  const float t = st.x - 16.0f * mu;
+  return st.y + t * t * (1.0f / 16.0f);
+}
+// (s, m2) of 16 values held 8 by this lane and 8 by lane ^ 1 (both lanes call).
+__device__ inline float2 ln_group16(const float (&v)[8]) {
+  float a = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) a += v[i];
+  a += __shfl_xor(a, 1, 64);
+  const float mean = a * (1.0f / 16.0f);
+  float m2 = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const float t = v[i] - mean;
+    m2 += t * t;
+  }
+  m2 += __shfl_xor(m2, 1, 64);
+  return make_float2(a, m2);
+}
+// (s, m2) of 16 values held by one thread.
+__device__ inline float2 ln_group16_one(const float (&v)[16]) {
+  float a = 0.f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) a += v[i];
+  const float mean = a * (1.0f / 16.0f);
+  float m2 = 0.f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const float t = v[i] - mean;
+    m2 += t * t;
+  }
+  return make_float2(a, m2);
+}
+
 struct KfDevState {
   int C;    // committed context length (positions 0..C-1 hold real-token K/V)
   int err;  // bit 0: a token id outside [0, V) was replaced by 0; bit 1: a bad temperature

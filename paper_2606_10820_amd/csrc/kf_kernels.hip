@@ -50,17 +50,15 @@ __global__ void __launch_bounds__(256)
   // one thread per 16 columns (d <= 2048): the row and its LayerNorm partials
   const int grp = threadIdx.x;
   if (grp < d / 16) {
-    float a = 0.f, q = 0.f;
+    float v[16];
 #pragma unroll
     for (int c = 0; c < 16; ++c) {
       const int e = grp * 16 + c;
-      const float v = to_f(te[e]) + to_f(pe[e]);
-      x[e] = v;
-      if constexpr (sizeof(T) == 2) xh[e] = from_f<T>(v);
-      a += v;
-      q += v * v;
+      v[c] = to_f(te[e]) + to_f(pe[e]);
+      x[e] = v[c];
+      if constexpr (sizeof(T) == 2) xh[e] = from_f<T>(v[c]);
     }
-    lnst[row * (d / 16) + grp] = make_float2(a, q);
+    lnst[row * (d / 16) + grp] = ln_group16_one(v);
   }
 }
 
@@ -352,17 +350,15 @@ __global__ void __launch_bounds__(256)
   const T* pe = pos + (size_t)(t + shift + j) * d;
   const int grp = threadIdx.x;
   if (grp < d / 16) {
-    float a = 0.f, sq = 0.f;
+    float v[16];
 #pragma unroll
     for (int c = 0; c < 16; ++c) {
       const int e = grp * 16 + c;
-      const float v = to_f(te[e]) + to_f(pe[e]);
-      X[row * d + e] = v;
-      if constexpr (sizeof(T) == 2) Xh[row * d + e] = from_f<T>(v);
-      a += v;
-      sq += v * v;
+      v[c] = to_f(te[e]) + to_f(pe[e]);
+      X[row * d + e] = v[c];
+      if constexpr (sizeof(T) == 2) Xh[row * d + e] = from_f<T>(v[c]);
     }
-    lnst[row * (d / 16) + grp] = make_float2(a, sq);
+    lnst[row * (d / 16) + grp] = ln_group16_one(v);
   }
 }
 
@@ -521,17 +517,14 @@ __global__ void __launch_bounds__(256)
   dot += __shfl_xor(dot, 1, 64);
   dot += __shfl_xor(dot, 2, 64);
   // the row's LayerNorm statistics from its partial sums, as the head GEMM forms them
-  float sa = 0.f, sb = 0.f;
-  for (int i = lane; i < d / 16; i += 64) {
-    const float2 v = lnst[(size_t)r * (d / 16) + i];
-    sa += v.x;
-    sb += v.y;
-  }
+  float sa = 0.f;
+  for (int i = lane; i < d / 16; i += 64) sa += lnst[(size_t)r * (d / 16) + i].x;
   sa = wave_sum(sa);
-  sb = wave_sum(sb);
   const float mu = rms ? 0.f : sa / (float)d;
-  const float rstd =
-      1.0f / sqrtf((rms ? sb / (float)d : fmaxf(sb / (float)d - mu * mu, 0.f)) + 1e-5f);
+  float sb = 0.f;
+  for (int i = lane; i < d / 16; i += 64) sb += ln_group_sq(lnst[(size_t)r * (d / 16) + i], mu);
+  sb = wave_sum(sb);
+  const float rstd = 1.0f / sqrtf(sb / (float)d + 1e-5f);
   float p = 0.f;
   if (j < V) {
     const float l = rstd * (dot - mu * c1[j]) + c2[j];

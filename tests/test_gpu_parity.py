@@ -90,8 +90,29 @@ def test_toy_prefill_and_decode(toy):
     kf = _ctx(TOY, 4, 4, 16, blob)
     prompt = S.prompts_uniform(1, 4, 16, TOY.vocab)
     st = run_teacher_forced(kf, model, prompt, [4] * 16, noise_seed=2, tol=TOL[0])
-    report("toy fp32 B=4, prefill + 3 blocks", st)
+    report("toy fp32 B=4, prefill + 15 blocks", st)
     assert st["max_rel"] < 1e-4
+
+
+def test_layernorm_rows_with_large_common_offset():
+    """Residual rows whose mean is far above their spread: the position table
+    carries +6 on every element, so every row entering the first LayerNorm
+    has mean ~6 and standard deviation ~0.03 (|mu| / sigma ~ 200).  The folded
+    LayerNorms merge centred per-16-column statistics, so the variance has no
+    E[x^2] - mu^2 cancellation (that form is off by a few per cent here), and
+    the fp32 model matches the oracle (two-pass LayerNorm in fp64) within 1e-4
+    at every block.  The fold itself, rstd (x W'^T - mu c1) + c2, still
+    subtracts two terms of size |mu| |w|, an error of about fp32 eps |mu| /
+    sigma relative (3e-5 here, 3e-4 at |mu| = 50)."""
+    _need_gpu()
+    W = S.make_weights(TOY, seed=0, random_affine=True)
+    W["pos_emb"] = W["pos_emb"] + np.float32(6.0)
+    blob = S.pack_blob(TOY, W)
+    model = O.Model(blob)
+    kf = _ctx(TOY, 4, 4, 16, blob)
+    prompt = S.prompts_uniform(1, 4, 16, TOY.vocab)
+    st = run_teacher_forced(kf, model, prompt, [4, 4, 4, 4], noise_seed=8, tol=TOL[0])
+    report("toy fp32 B=4, positions offset by +6", st)
 
 
 def test_toy_host_blob_equals_device_blob(toy):
