@@ -49,22 +49,24 @@ __device__ inline uint2 load4_stream(const bf16* p) {
   return make_uint2(v.x, v.y);
 }
 
-template <int DH, int NW>
-__device__ __forceinline__ void attention_block(const bf16* __restrict__ Q, const bf16* __restrict__ kv,
-                                                bf16* __restrict__ O, const KfDevState* st,
-                                                const KfStepGeom& g, const KfKvGeom& kg, int layer,
-                                                float scale, const AttnSplit& sp, int b, int h,
-                                                int qb, int split) {
-  constexpr int QB = 16, KT = 32, NDC = DH / 32, NDB = DH / 16;
-  const int H = kg.H, d = H * DH;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+// The online softmax of one wavefront over the key tiles t0 = first, first +
+// stride, ... < ke of (sequence b, head h) for the query rows q0 .. q0 + nq - 1
+// of the step (nq <= 16): on return the lane (query lq = lane & 15, group
+// gq = lane >> 4) holds the running maximum m_run and sum l_run of query lq
+// (the same in its four groups) and o[db][r] = the unnormalised output of
+// query lq at d_head index 16 db + 4 gq + r.
+template <int DH>
+__device__ __forceinline__ void attention_tiles(const bf16* __restrict__ Q, const bf16* __restrict__ kv,
+                                                const KfDevState* st, const KfStepGeom& g,
+                                                const KfKvGeom& kg, int layer, float scale, int b,
+                                                int h, int q0, int nq, int first, int stride, int ke,
+                                                float& m_run, float& l_run, f32x4_t (&o)[DH / 16]) {
+  constexpr int KT = 32, NDC = DH / 32, NDB = DH / 16;
+  const int d = kg.H * DH;
+  const int lane = threadIdx.x & 63;
   const int gq = lane >> 4, lq = lane & 15;
   const int C = g.ctx(st, b), seq = g.slot(b);
-  const int q0 = qb * QB, nq = min(QB, g.R - q0);
   const int nkeys = C + q0 + nq;
-  const int chunk = ((nkeys + sp.ns - 1) / sp.ns + KT - 1) / KT * KT;
-  const int ks = split * chunk, ke = min(nkeys, ks + chunk);
-
   const bf16x8_t zero8 = {};
   bf16x8_t qf[NDC];
   const bf16* qrow = Q + ((size_t)b * g.R + q0 + lq) * d + h * DH + 8 * gq;
@@ -72,8 +74,8 @@ __device__ __forceinline__ void attention_block(const bf16* __restrict__ Q, cons
   for (int c = 0; c < NDC; ++c) qf[c] = (lq < nq) ? load8(qrow + c * 32) : zero8;
   const int qslot = C + q0 + lq;
 
-  float m_run = -INFINITY, l_run = 0.f;
-  f32x4_t o[NDB];
+  m_run = -INFINITY;
+  l_run = 0.f;
 #pragma unroll
   for (int i = 0; i < NDB; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
@@ -163,19 +165,60 @@ __device__ __forceinline__ void attention_block(const bf16* __restrict__ Q, cons
   };
 
   Frag fa, fb;
-  int t0 = ks + w * KT;
+  int t0 = first;
   if (t0 < ke) load(t0, fa);
   while (t0 < ke) {  // ping-pong: the next tile loads while this one computes
-    int tn = t0 + NW * KT;
+    int tn = t0 + stride;
     if (tn < ke) load(tn, fb);
     tile(t0, fa);
     t0 = tn;
     if (t0 >= ke) break;
-    tn = t0 + NW * KT;
+    tn = t0 + stride;
     if (tn < ke) load(tn, fa);
     tile(t0, fb);
     t0 = tn;
   }
+}
+
+// Output rows of one wavefront that saw every key (attention_tiles over the
+// whole range): O[b][q0 + lq][h] = o / l_run, 4 consecutive elements per store.
+template <int DH>
+__device__ __forceinline__ void attention_wave_out(bf16* __restrict__ O, const KfStepGeom& g,
+                                                   const KfKvGeom& kg, int b, int h, int q0, int nq,
+                                                   float l_run, const f32x4_t (&o)[DH / 16]) {
+  const int lane = threadIdx.x & 63, gq = lane >> 4, lq = lane & 15;
+  if (lq >= nq) return;
+  const float inv = 1.0f / l_run;
+  bf16* orow = O + ((size_t)b * g.R + q0 + lq) * (kg.H * DH) + h * DH + 4 * gq;
+#pragma unroll
+  for (int db = 0; db < DH / 16; ++db) {
+    const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (bf16)(o[db][0] * inv)) |
+                        ((uint32_t)__builtin_bit_cast(uint16_t, (bf16)(o[db][1] * inv)) << 16);
+    const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (bf16)(o[db][2] * inv)) |
+                        ((uint32_t)__builtin_bit_cast(uint16_t, (bf16)(o[db][3] * inv)) << 16);
+    *reinterpret_cast<uint2*>(orow + db * 16) = make_uint2(lo, hi);
+  }
+}
+
+template <int DH, int NW>
+__device__ __forceinline__ void attention_block(const bf16* __restrict__ Q, const bf16* __restrict__ kv,
+                                                bf16* __restrict__ O, const KfDevState* st,
+                                                const KfStepGeom& g, const KfKvGeom& kg, int layer,
+                                                float scale, const AttnSplit& sp, int b, int h,
+                                                int qb, int split) {
+  constexpr int QB = 16, KT = 32, NDB = DH / 16;
+  const int H = kg.H, d = H * DH;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int gq = lane >> 4, lq = lane & 15;
+  const int C = g.ctx(st, b);
+  const int q0 = qb * QB, nq = min(QB, g.R - q0);
+  const int nkeys = C + q0 + nq;
+  const int chunk = ((nkeys + sp.ns - 1) / sp.ns + KT - 1) / KT * KT;
+  const int ks = split * chunk, ke = min(nkeys, ks + chunk);
+  float m_run, l_run;
+  f32x4_t o[NDB];
+  attention_tiles<DH>(Q, kv, st, g, kg, layer, scale, b, h, q0, nq, ks + w * KT, NW * KT, ke, m_run,
+                      l_run, o);
 
   // merge the wavefronts' partial states
   __shared__ float sm[NW][QB], sl[NW][QB];
