@@ -37,13 +37,23 @@ template <>
 __device__ inline bf16 from_f<bf16>(float x) { return (bf16)x; }
 
 // GELU, tanh form (GPT-2 style): 0.5 x (1 + tanh u) with u = c (x + 0.044715 x^3),
-// evaluated as x * sigmoid(2u) = x / (1 + exp(-2u)) (the same function; one
-// exponential and one fast division).  Saturates correctly at both ends:
-// exp(-2u) -> inf gives -0, exp(-2u) -> 0 gives x.
+// evaluated as x * sigmoid(2u) = x / (1 + exp(-2u)), the same function.  The
+// exponential is 2^z with z = -2u log2(e) = x (k0 + k1 x^2) (log2(e) folded into
+// the constants), and the quotient is x times the hardware reciprocal (about
+// 1 ulp): a full-precision division would cost ten instructions per element,
+// and the epilogue of a large GEMM is bound by this arithmetic.  Saturates
+// correctly at both ends: 2^z -> inf gives -0, 2^z -> 0 gives x.
 __device__ inline float gelu_f(float x) {
-  const float c = 0.7978845608028654f;
-  const float u = c * (x + 0.044715f * x * x * x);
-  return __fdividef(x, 1.0f + __expf(-2.0f * u));
+  constexpr float k0 = -2.0f * 0.7978845608028654f * 1.4426950408889634f;
+  constexpr float k1 = 0.044715f * k0;
+  const float z = x * fmaf(k1, x * x, k0);
+  return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(z));
+}
+
+// n / d for n >= 0 and a wave-uniform d > 0: a shift when d is a power of two
+// (head widths, rows per sequence at k = 1, 2, 4), else the integer division.
+__device__ inline int div_u(int n, int d) {
+  return (d & (d - 1)) == 0 ? n >> __builtin_ctz((unsigned)d) : n / d;
 }
 
 template <typename T>
@@ -239,19 +249,20 @@ struct EpQKV {
   static constexpr bool kStats = false;
   __device__ inline void store8(int m, int n, float (&v)[8]) const {
     const int d = kg.H * kg.dh;
-    const int which = n / d, c = n - which * d;
+    const int which = (n >= d) + (n >= 2 * d), c = n - which * d;  // n < 3d
     if (which == 0 && !rope) {
       put8(Q + (size_t)m * d + c, v);
       return;
     }
-    const int b = m / g.R, i = m - b * g.R;
+    const int b = div_u(m, g.R), i = m - b * g.R;
     const int slot = g.ctx(st, b) + i;  // this row's position and cache slot
-    if (rope && which < 2) rotate8(v, rope, kg.dh < 64 ? kg.dh : 64, slot, c % kg.dh);
+    const int h = div_u(c, kg.dh), e = c - h * kg.dh;
+    if (rope && which < 2) rotate8(v, rope, kg.dh < 64 ? kg.dh : 64, slot, e);
     if (which == 0) {
       put8(Q + (size_t)m * d + c, v);
       return;
     }
-    const int h = c / kg.dh, e = c - h * kg.dh, r0 = (unsigned)slot % kPage;
+    const int r0 = (unsigned)slot % kPage;
     T* base = kv + kg.page_base(g.slot(b), slot) + kg.head_off(layer, which - 1, h);
     if (which == 1) {  // keys: [slot][dh]
       put8_stream(base + (size_t)r0 * kg.dh + e, v);
@@ -265,19 +276,46 @@ struct EpQKV {
   // within one value block are one contiguous run, and consecutive lanes hold
   // consecutive value rows, whose runs are adjacent.
   __device__ inline bool column_tile(int n0) const { return n0 >= 2 * kg.H * kg.dh; }
+  //
+  // Every index into v is a compile-time constant (a run-time index would put
+  // v in scratch memory): each group of 4 rows is one aligned 4-slot block of
+  // one sequence (one 8-byte store) in the common case, else it is written as
+  // aligned pairs of slots and single slots.
+  __device__ inline T* vslot(int mr, int e, unsigned ho, int& i, int& slot) const {
+    const int b = div_u(mr, g.R);
+    i = mr - b * g.R;
+    slot = g.ctx(st, b) + i;
+    return kv + kg.page_base(g.slot(b), slot) + ho + KfKvGeom::vt_off(slot, e, kg.dh);
+  }
   __device__ inline void store_col8(int m, int n, const float (&v)[8], int M) const {
-    const int c = n - 2 * kg.H * kg.dh, h = c / kg.dh, e = c - h * kg.dh;
+    const int c = n - 2 * kg.H * kg.dh, h = div_u(c, kg.dh), e = c - h * kg.dh;
     const unsigned ho = kg.head_off(layer, 1, h);
-    for (int r = 0; r < 8 && m + r < M;) {
-      const int b = (m + r) / g.R, i = (m + r) - b * g.R;
-      const int slot = g.ctx(st, b) + i, a = slot % kVBlk;
-      int len = kVBlk - a;
-      len = len < 8 - r ? len : 8 - r;
-      len = len < M - (m + r) ? len : M - (m + r);
-      len = len < g.R - i ? len : g.R - i;
-      put_run4(kv + kg.page_base(g.slot(b), slot) + ho + KfKvGeom::vt_off(slot, e, kg.dh), a, v + r,
-               len);
-      r += len;
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int mq = m + 4 * q;
+      if (mq >= M) break;
+      int i, slot;
+      T* p = vslot(mq, e, ho, i, slot);
+      if ((slot & 3) == 0 && i + 4 <= g.R && mq + 4 <= M) {
+        put_run4(p, 0, &v[4 * q], 4);
+        continue;
+      }
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {  // rows mq + 2t, mq + 2t + 1
+        const int mt = mq + 2 * t;
+        if (mt >= M) break;
+        int it, st0;
+        T* pt = vslot(mt, e, ho, it, st0);
+        if ((st0 & 1) == 0 && it + 2 <= g.R && mt + 2 <= M) {
+          put_run4(pt, 0, &v[4 * q + 2 * t], 2);
+          continue;
+        }
+        *pt = from_f<T>(v[4 * q + 2 * t]);
+        if (mt + 1 < M) {
+          T* p1 = vslot(mt + 1, e, ho, it, st0);
+          *p1 = from_f<T>(v[4 * q + 2 * t + 1]);
+        }
+      }
     }
   }
 };
@@ -723,11 +761,17 @@ __global__ void __launch_bounds__(256)
     }
   }
 
-  // Folded LayerNorm (if any) and bias for 16x16 tile (tn, row ml).
-  auto apply = [&](f32x4 v, int ml, int tn) -> f32x4 {
+  // Folded LayerNorm (if any) and bias for 16x16 tile (tn, tm).  The row
+  // statistics of this lane's TM rows are read from LDS once, here.
+  float2 rst[NORM ? TM : 1];
+  if constexpr (NORM) {
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) rst[tm] = sStat[wm * MW + tm * 16 + (lane & 15)];
+  }
+  auto apply = [&](f32x4 v, int tm, int tn) -> f32x4 {
     f32x4 r;
     if constexpr (NORM) {
-      const float2 st = sStat[ml];
+      const float2 st = rst[tm];
 #pragma unroll
       for (int i = 0; i < 4; ++i) r[i] = st.y * (v[i] - st.x * p1[tn][i]) + p2[tn][i] + pb[tn][i];
     } else {
@@ -755,8 +799,7 @@ __global__ void __launch_bounds__(256)
         for (int tn = 0; tn < TN; ++tn)
 #pragma unroll
           for (int tm = 0; tm < TM; ++tm) {
-            const int ml = wm * MW + tm * 16 + (lane & 15);
-            const f32x4 r = apply(acc[tn][tm], ml, tn);
+            const f32x4 r = apply(acc[tn][tm], tm, tn);
             float* q = stage + (tm * 16 + (lane & 15)) * SROW + wn * NW + tn * 16 + 4 * (lane >> 4);
             *reinterpret_cast<float4*>(q) = make_float4(r[0], r[1], r[2], r[3]);
           }
@@ -816,7 +859,7 @@ __global__ void __launch_bounds__(256)
 #pragma unroll
       for (int tn = 0; tn < TN; ++tn) {
         const int n = n0 + wn * NW + tn * 16 + 4 * (lane >> 4);
-        const f32x4 v = apply(acc[tn][tm], mloc, tn);
+        const f32x4 v = apply(acc[tn][tm], tm, tn);
 #pragma unroll
         for (int i = 0; i < 4; ++i)
           if (n + i < ep.V) bv = fmaxf(bv, v[i] * it);
@@ -838,7 +881,7 @@ __global__ void __launch_bounds__(256)
 #pragma unroll
       for (int tn = 0; tn < TN; ++tn) {
         const int n = n0 + wn * NW + tn * 16 + 4 * (lane >> 4);
-        const f32x4 v = apply(acc[tn][tm], mloc, tn);
+        const f32x4 v = apply(acc[tn][tm], tm, tn);
         float sg = 0.f;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -870,7 +913,7 @@ __global__ void __launch_bounds__(256)
 #pragma unroll
       for (int tn = 0; tn < TN; ++tn) {
         const int n = n0 + wn * NW + tn * 16 + 4 * (lane >> 4);
-        const f32x4 v = apply(acc[tn][tm], mloc, tn);
+        const f32x4 v = apply(acc[tn][tm], tm, tn);
 #pragma unroll
         for (int i = 0; i < 4; ++i)
           if (n + i < ep.V && v[i] > bv) { bv = v[i]; bi = n + i; }
