@@ -684,29 +684,38 @@ __global__ void __launch_bounds__(256)
   // them does not wait for the operands) and reduced by the TPR consecutive
   // lanes that share a row.
   constexpr int TPR = NORM ? 256 / BM : 1;
-  constexpr int PMAX = 12;  // float4 loads (two partials each) per lane, unrolled
+  // float4 loads (two partials each) per lane, unrolled: whole rows up to
+  // K = 1024; wider rows finish in a loop.
+  constexpr int PMAX = NORM ? (32 / TPR > 0 ? 32 / TPR : 1) : 1;
   float4 part[PMAX];
   const int parts4 = K / 32;  // float4 words per row
   const float4* prow = nullptr;
+  // The prologue is straight-line code: the partial loads (indices clamped to
+  // the row, extra words masked below) and the first S stages are issued
+  // unconditionally, so the compiler's wait before the statistics covers the
+  // partials only.  Behind a branch it waits for every load in flight, the
+  // whole ring included.  A stage past this split's K range reads bytes that
+  // are never consumed (the buffer range returns zeros past its end), and it
+  // has landed before the first barrier.
   if constexpr (NORM) {
     const int r = tid / TPR, gr = m0 + r < M ? m0 + r : M - 1;
     prow = reinterpret_cast<const float4*>(ga.lnst + (size_t)map_row<MODE>(gr, ga.g) * (K / 16));
 #pragma unroll
     for (int j = 0; j < PMAX; ++j) {
       const int w = (tid % TPR) + j * TPR;
-      part[j] = w < parts4 ? prow[w] : make_float4(0.f, 0.f, 0.f, 0.f);
+      part[j] = prow[w < parts4 ? w : parts4 - 1];
     }
   }
   Slice f0, f1;
 #pragma unroll
-  for (int i = 0; i < S; ++i)
-    if (i < nk) issue(i, i);
+  for (int i = 0; i < S; ++i) issue(i, i);
   if constexpr (NORM) {
     // the row's mean from the group sums, then the merged squared deviations
     float a = 0.f;
 #pragma unroll
-    for (int j = 0; j < PMAX; ++j) a += part[j].x + part[j].z;
-    for (int w = (tid % TPR) + PMAX * TPR; w < parts4; w += TPR) {  // wide rows only
+    for (int j = 0; j < PMAX; ++j)
+      a += (tid % TPR) + j * TPR < parts4 ? part[j].x + part[j].z : 0.f;
+    for (int w = (tid % TPR) + PMAX * TPR; w < parts4; w += TPR) {  // K > 1024 only
       const float4 v = prow[w];
       a += v.x + v.z;
     }
@@ -715,10 +724,11 @@ __global__ void __launch_bounds__(256)
     const float mu = ga.rms ? 0.f : a / (float)K;
     float b = 0.f;
 #pragma unroll
-    for (int j = 0; j < PMAX; ++j)
-      if ((tid % TPR) + j * TPR < parts4)
-        b += ln_group_sq(make_float2(part[j].x, part[j].y), mu) +
-             ln_group_sq(make_float2(part[j].z, part[j].w), mu);
+    for (int j = 0; j < PMAX; ++j) {
+      const float q = ln_group_sq(make_float2(part[j].x, part[j].y), mu) +
+                      ln_group_sq(make_float2(part[j].z, part[j].w), mu);
+      b += (tid % TPR) + j * TPR < parts4 ? q : 0.f;
+    }
     for (int w = (tid % TPR) + PMAX * TPR; w < parts4; w += TPR) {
       const float4 v = prow[w];
       b += ln_group_sq(make_float2(v.x, v.y), mu) + ln_group_sq(make_float2(v.z, v.w), mu);
@@ -980,18 +990,20 @@ __global__ void __launch_bounds__(64 * KW)
   // Folded LayerNorm: the row partial sums of the 16 rows (16 threads per
   // row) are loaded first and reduced once the operand loads are in flight,
   // so both wait on one memory round trip.
+  // Every prologue load is unconditional, its index clamped into range (the
+  // extra values are masked where they are used): a load behind a branch makes
+  // the compiler wait for all loads in flight at the join.
   constexpr int PS = 4;  // partial sums per thread held in registers (K <= 1024)
   __shared__ float2 sStat[16];
   float2 ps[PS];
   const float2* pr = nullptr;
   if constexpr (NORM) {
-    if (tid < 256) {
-      pr = ga.lnst + (size_t)map_row<MODE>((tid >> 4) < M ? (tid >> 4) : M - 1, ga.g) * (K / 16);
+    const int pm = (tid >> 4) & 15;  // threads past 256 repeat rows 0..15; only the first 256 use them
+    pr = ga.lnst + (size_t)map_row<MODE>(pm < M ? pm : M - 1, ga.g) * (K / 16);
 #pragma unroll
-      for (int i = 0; i < PS; ++i) {
-        const int w = (tid & 15) + 16 * i;
-        ps[i] = w < K / 16 ? pr[w] : make_float2(0.f, 0.f);
-      }
+    for (int i = 0; i < PS; ++i) {
+      const int w = (tid & 15) + 16 * i;
+      ps[i] = pr[w < K / 16 ? w : K / 16 - 1];
     }
   }
   // The column constants of this thread's tile element (bias, folded-norm
@@ -1019,18 +1031,18 @@ __global__ void __launch_bounds__(64 * KW)
   const int arow = map_row<MODE>(r < M ? r : M - 1, ga.g);
   const u32x4* pw = reinterpret_cast<const u32x4*>(W + (size_t)wrow * ldw + wave * kw + 8 * q);
   const u32x4* pa = reinterpret_cast<const u32x4*>(A + (size_t)arow * ga.lda + wave * kw + 8 * q);
-  const u32x4 z = {0u, 0u, 0u, 0u};
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   // Two named load batches alternate (no register copies between them, which
   // would wait for loads still in flight): batch B loads while batch A feeds
   // the MFMAs, and the other way round.
   u32x4 wa[U], xa[U], wb[U], xb[U];
+  // Steps past the end re-load the last step (valid memory); mma() skips them.
   auto load = [&](u32x4 (&w)[U], u32x4 (&x)[U], int s0) {
 #pragma unroll
     for (int i = 0; i < U; ++i) {
-      const int t = s0 + i;
-      w[i] = t < steps ? pw[4 * t] : z;
-      x[i] = t < steps ? pa[4 * t] : z;
+      const int t = s0 + i < steps ? s0 + i : steps - 1;
+      w[i] = pw[4 * t];
+      x[i] = pa[4 * t];
     }
   };
   auto mma = [&](const u32x4 (&w)[U], const u32x4 (&x)[U], int s0) {
@@ -1044,15 +1056,14 @@ __global__ void __launch_bounds__(64 * KW)
       // the row's mean from the group sums, then the merged squared deviations
       float a = 0.f;
 #pragma unroll
-      for (int i = 0; i < PS; ++i) a += ps[i].x;
+      for (int i = 0; i < PS; ++i) a += (tid & 15) + 16 * i < K / 16 ? ps[i].x : 0.f;
       for (int w = (tid & 15) + 16 * PS; w < K / 16; w += 16) a += pr[w].x;  // K > 1024 only
 #pragma unroll
       for (int off = 1; off < 16; off <<= 1) a += __shfl_xor(a, off, 64);
       const float mu = ga.rms ? 0.f : a / (float)K;
       float b = 0.f;
 #pragma unroll
-      for (int i = 0; i < PS; ++i)
-        if ((tid & 15) + 16 * i < K / 16) b += ln_group_sq(ps[i], mu);
+      for (int i = 0; i < PS; ++i) b += (tid & 15) + 16 * i < K / 16 ? ln_group_sq(ps[i], mu) : 0.f;
       for (int w = (tid & 15) + 16 * PS; w < K / 16; w += 16) b += ln_group_sq(pr[w], mu);
 #pragma unroll
       for (int off = 1; off < 16; off <<= 1) b += __shfl_xor(b, off, 64);
