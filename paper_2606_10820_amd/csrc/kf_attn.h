@@ -1,6 +1,5 @@
 // kf_attn.h -- the bf16 block attention of one (sequence, head, block of 16
-// query rows, key split) on MFMA, shared by the decode attention kernel and
-// the fused small-step QKV + attention kernel.
+// query rows, key split) on MFMA, the body of the decode attention kernel.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <math.h>
@@ -44,9 +43,8 @@ __device__ inline bf16x8_t load8(const bf16* p) {
 __device__ inline bf16x8_t load8_stream(const bf16* p) {
   return __builtin_bit_cast(bf16x8_t, __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p)));
 }
-__device__ inline uint2 load4_stream(const bf16* p) {
-  const u32x2_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(p));
-  return make_uint2(v.x, v.y);
+__device__ inline u32x2_t load4_stream(const bf16* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(p));
 }
 
 // The online softmax of one wavefront over the key tiles t0 = first, first +
@@ -55,7 +53,11 @@ __device__ inline uint2 load4_stream(const bf16* p) {
 // gq = lane >> 4) holds the running maximum m_run and sum l_run of query lq
 // (the same in its four groups) and o[db][r] = the unnormalised output of
 // query lq at d_head index 16 db + 4 gq + r.
-template <int DH>
+// Where a tile's KV page comes from: PT 0, no page table (sequence q owns
+// pages q * np ...); PT 1, a page table of at most 64 pages per sequence, read
+// once into one register per lane; PT 2, a longer page table, read per tile.
+// The first two keep the tile loop free of dependent loads.
+template <int DH, int PT>
 __device__ __forceinline__ void attention_tiles(const bf16* __restrict__ Q, const bf16* __restrict__ kv,
                                                 const KfDevState* st, const KfStepGeom& g,
                                                 const KfKvGeom& kg, int layer, float scale, int b,
@@ -67,11 +69,16 @@ __device__ __forceinline__ void attention_tiles(const bf16* __restrict__ Q, cons
   const int gq = lane >> 4, lq = lane & 15;
   const int C = g.ctx(st, b), seq = g.slot(b);
   const int nkeys = C + q0 + nq;
-  const bf16x8_t zero8 = {};
+  // Every load is unconditional, at an address clamped into the sequence's
+  // pages, and the data past the end is masked where it is used: a select on
+  // loaded data, or a load behind a branch, makes the compiler wait for the
+  // loads in flight, and the next tile's loads would no longer overlap this
+  // tile's arithmetic.  Query rows past nq load row nq - 1 (their outputs are
+  // never stored).
   bf16x8_t qf[NDC];
-  const bf16* qrow = Q + ((size_t)b * g.R + q0 + lq) * d + h * DH + 8 * gq;
+  const bf16* qrow = Q + ((size_t)b * g.R + q0 + (lq < nq ? lq : nq - 1)) * d + h * DH + 8 * gq;
 #pragma unroll
-  for (int c = 0; c < NDC; ++c) qf[c] = (lq < nq) ? load8(qrow + c * 32) : zero8;
+  for (int c = 0; c < NDC; ++c) qf[c] = load8(qrow + c * 32);
   const int qslot = C + q0 + lq;
 
   m_run = -INFINITY;
@@ -79,17 +86,32 @@ __device__ __forceinline__ void attention_tiles(const bf16* __restrict__ Q, cons
 #pragma unroll
   for (int i = 0; i < NDB; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+  // The value fragment is kept as its two 8-byte halves and assembled in
+  // tile(): an assembly at load time is a register copy that waits for the
+  // load.
   struct Frag {
     bf16x8_t k[2][NDC];
-    bf16x8_t v[NDB];
+    u32x2_t vlo[NDB], vhi[NDB];
   };
   // A tile starts at a multiple of 32 keys, so it lies in one KV page, and so
-  // does the last key nkeys - 1 >= t0 that stands in for keys past the end.
-  // K rows past the end read the last key (then zeroed); value slots past the
-  // end are zeroed (their probability is 0, and 0 * a stale NaN would not be).
+  // does the last key nkeys - 1 >= t0 that stands in for keys past the end
+  // (their scores are masked to -inf).  Value slots past the end are read
+  // from the same page and zeroed in tile() (their probability is 0, and
+  // 0 * a stale NaN would not be).
   static_assert(kPage % KT == 0, "tiles do not straddle KV pages");
+  const unsigned np = (unsigned)kg.T / kPage;
+  unsigned pid = 0;
+  if constexpr (PT == 1) pid = (unsigned)kg.ptab[(size_t)seq * np + ((unsigned)lane < np ? lane : np - 1)];
+  auto page_of = [&](int t0) -> size_t {
+    const unsigned j = (unsigned)t0 / kPage;
+    unsigned pg;
+    if constexpr (PT == 0) pg = (unsigned)seq * np + j;
+    else if constexpr (PT == 1) pg = (unsigned)__builtin_amdgcn_readlane((int)pid, (int)j);
+    else pg = (unsigned)kg.ptab[(size_t)seq * np + j];
+    return (size_t)pg * kg.page_elems();
+  };
   auto load = [&](int t0, Frag& f) {
-    const bf16* page = kv + kg.page_base(seq, t0);
+    const bf16* page = kv + page_of(t0);
     const bf16* Kb = page + kg.head_off(layer, 0, h);
     const bf16* Vt = page + kg.head_off(layer, 1, h);
     const int pbase = t0 - t0 % kPage;
@@ -98,28 +120,29 @@ __device__ __forceinline__ void attention_tiles(const bf16* __restrict__ Q, cons
       const int key = t0 + 8 * (lq >> 2) + 4 * grp + (lq & 3);
       const int kc = (key < nkeys ? key : nkeys - 1) - pbase;
 #pragma unroll
-      for (int c = 0; c < NDC; ++c) {
-        const bf16x8_t x = load8_stream(Kb + (size_t)kc * DH + c * 32 + 8 * gq);
-        f.k[grp][c] = key < nkeys ? x : zero8;
-      }
+      for (int c = 0; c < NDC; ++c) f.k[grp][c] = load8_stream(Kb + (size_t)kc * DH + c * 32 + 8 * gq);
     }
     const int kb = t0 + 8 * gq;
 #pragma unroll
     for (int db = 0; db < NDB; ++db) {
-      // slots kb..kb+3 and kb+4..kb+7: two value blocks
-      const bf16* vp = Vt + KfKvGeom::vt_off(kb - pbase, db * 16 + lq, DH);
-      const bf16* vq = Vt + KfKvGeom::vt_off(kb + 4 - pbase, db * 16 + lq, DH);
-      if (kb + 8 <= nkeys) {
-        const uint2 lo = load4_stream(vp), hi = load4_stream(vq);
-        f.v[db] = __builtin_bit_cast(bf16x8_t, make_uint4(lo.x, lo.y, hi.x, hi.y));
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          f.v[db][e] = (kb + e < nkeys) ? (e < 4 ? vp[e] : vq[e - 4]) : (bf16)0.f;
-      }
+      // slots kb..kb+3 and kb+4..kb+7: two value blocks of this page
+      f.vlo[db] = load4_stream(Vt + KfKvGeom::vt_off(kb - pbase, db * 16 + lq, DH));
+      f.vhi[db] = load4_stream(Vt + KfKvGeom::vt_off(kb + 4 - pbase, db * 16 + lq, DH));
     }
   };
   auto tile = [&](int t0, const Frag& f) {
+    bf16x8_t v[NDB];
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+      v[db] = __builtin_bit_cast(bf16x8_t, u32x4_t{f.vlo[db].x, f.vlo[db].y, f.vhi[db].x, f.vhi[db].y});
+    if (t0 + KT > nkeys) {  // the ragged last tile: zero the value slots past the end
+      const int kb = t0 + 8 * gq;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (kb + e >= nkeys) v[db][e] = (bf16)0.f;
+    }
     f32x4_t s[2];
 #pragma unroll
     for (int grp = 0; grp < 2; ++grp) {
@@ -160,47 +183,35 @@ __device__ __forceinline__ void attention_tiles(const bf16* __restrict__ Q, cons
 #pragma unroll
     for (int db = 0; db < NDB; ++db) {
       o[db] *= alpha;
-      o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.v[db], pf, o[db], 0, 0, 0);
+      o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v[db], pf, o[db], 0, 0, 0);
     }
   };
 
+  // Ping-pong: the next tile loads while this one computes.  The last tile is
+  // peeled off (no prefetch), so the loop body has no branch around a load.
   Frag fa, fb;
   int t0 = first;
-  if (t0 < ke) load(t0, fa);
-  while (t0 < ke) {  // ping-pong: the next tile loads while this one computes
-    int tn = t0 + stride;
-    if (tn < ke) load(tn, fb);
+  if (t0 >= ke) return;
+  load(t0, fa);
+  while (true) {
+    if (t0 + stride >= ke) {
+      tile(t0, fa);
+      return;
+    }
+    load(t0 + stride, fb);
     tile(t0, fa);
-    t0 = tn;
-    if (t0 >= ke) break;
-    tn = t0 + stride;
-    if (tn < ke) load(tn, fa);
+    t0 += stride;
+    if (t0 + stride >= ke) {
+      tile(t0, fb);
+      return;
+    }
+    load(t0 + stride, fa);
     tile(t0, fb);
-    t0 = tn;
+    t0 += stride;
   }
 }
 
-// Output rows of one wavefront that saw every key (attention_tiles over the
-// whole range): O[b][q0 + lq][h] = o / l_run, 4 consecutive elements per store.
-template <int DH>
-__device__ __forceinline__ void attention_wave_out(bf16* __restrict__ O, const KfStepGeom& g,
-                                                   const KfKvGeom& kg, int b, int h, int q0, int nq,
-                                                   float l_run, const f32x4_t (&o)[DH / 16]) {
-  const int lane = threadIdx.x & 63, gq = lane >> 4, lq = lane & 15;
-  if (lq >= nq) return;
-  const float inv = 1.0f / l_run;
-  bf16* orow = O + ((size_t)b * g.R + q0 + lq) * (kg.H * DH) + h * DH + 4 * gq;
-#pragma unroll
-  for (int db = 0; db < DH / 16; ++db) {
-    const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (bf16)(o[db][0] * inv)) |
-                        ((uint32_t)__builtin_bit_cast(uint16_t, (bf16)(o[db][1] * inv)) << 16);
-    const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (bf16)(o[db][2] * inv)) |
-                        ((uint32_t)__builtin_bit_cast(uint16_t, (bf16)(o[db][3] * inv)) << 16);
-    *reinterpret_cast<uint2*>(orow + db * 16) = make_uint2(lo, hi);
-  }
-}
-
-template <int DH, int NW>
+template <int DH, int NW, int PT>
 __device__ __forceinline__ void attention_block(const bf16* __restrict__ Q, const bf16* __restrict__ kv,
                                                 bf16* __restrict__ O, const KfDevState* st,
                                                 const KfStepGeom& g, const KfKvGeom& kg, int layer,
@@ -217,8 +228,8 @@ __device__ __forceinline__ void attention_block(const bf16* __restrict__ Q, cons
   const int ks = split * chunk, ke = min(nkeys, ks + chunk);
   float m_run, l_run;
   f32x4_t o[NDB];
-  attention_tiles<DH>(Q, kv, st, g, kg, layer, scale, b, h, q0, nq, ks + w * KT, NW * KT, ke, m_run,
-                      l_run, o);
+  attention_tiles<DH, PT>(Q, kv, st, g, kg, layer, scale, b, h, q0, nq, ks + w * KT, NW * KT, ke,
+                          m_run, l_run, o);
 
   // merge the wavefronts' partial states
   __shared__ float sm[NW][QB], sl[NW][QB];

@@ -188,15 +188,37 @@ __global__ void __launch_bounds__(256)
 
 // Block attention on MFMA (bf16): one workgroup per (sequence, head, block of
 // 16 query rows, key split), the block computed by attention_block (kf_attn.h).
-template <int DH, int NW = 4>
-__global__ void __launch_bounds__(64 * NW)
+// PT selects where the KV pages come from (attention_tiles); each mode is its
+// own kernel, so the lock-step one carries no page-table registers.  Up to
+// d_head 64 the kernel is held to three wavefronts per SIMD (at most 168
+// registers, no spill): the double-buffered K and V fragments would otherwise
+// take it to two, and at large batch the KV stream needs the occupancy.
+template <int DH, int NW, int PT>
+__global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 64 ? 3 : 1)))
     attention_mfma_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ kv,
                           bf16* __restrict__ O, const KfDevState* st, KfStepGeom g, KfKvGeom kg,
                           int layer, float scale, AttnSplit sp) {
   const int nqb = (g.R + 15) / 16;
   const int split = blockIdx.x % sp.ns, rest = blockIdx.x / sp.ns;
   const int qb = rest % nqb, bh = rest / nqb;
-  attention_block<DH, NW>(Q, kv, O, st, g, kg, layer, scale, sp, bh / kg.H, bh % kg.H, qb, split);
+  attention_block<DH, NW, PT>(Q, kv, O, st, g, kg, layer, scale, sp, bh / kg.H, bh % kg.H, qb,
+                              split);
+}
+
+template <int DH, int NW>
+void launch_attention_mfma(dim3 grid, hipStream_t s, const bf16* Q, const bf16* kv, bf16* O,
+                           const KfDevState* st, const KfStepGeom& g, const KfKvGeom& kg, int layer,
+                           float scale, const AttnSplit& sp) {
+  const dim3 block(64 * NW);
+  if (!kg.ptab)
+    launch((attention_mfma_kernel<DH, NW, 0>), grid, block, 0, s, Q, kv, O, st, g, kg, layer,
+           scale, sp);
+  else if (kg.T <= 64 * kPage)
+    launch((attention_mfma_kernel<DH, NW, 1>), grid, block, 0, s, Q, kv, O, st, g, kg, layer,
+           scale, sp);
+  else
+    launch((attention_mfma_kernel<DH, NW, 2>), grid, block, 0, s, Q, kv, O, st, g, kg, layer,
+           scale, sp);
 }
 
 // Merge of the key splits: O = sum_s f_s o_s / sum_s f_s l_s with
@@ -659,8 +681,7 @@ hipError_t launch_attention(const T* Q, const T* kv, T* O, const KfDevState* st,
     dim3 grid(base * ns);
     switch (kg.dh) {
       case 32:
-        launch(attention_mfma_kernel<32>, grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
-                           layer, scale, sp);
+        launch_attention_mfma<32, 4>(grid, s, Q, kv, O, st, g, kg, layer, scale, sp);
         if (ns > 1)
           launch(attention_combine_kernel<32>, dim3(g.B * g.R * kg.H), dim3(32), 0, s,
                              O, g, kg.H, sp);
@@ -668,20 +689,17 @@ hipError_t launch_attention(const T* Q, const T* kv, T* O, const KfDevState* st,
       case 64:
         if (ns > 1 && base >= kWideMin) {  // eight wavefronts, no key split
           sp.ns = 1;
-          launch((attention_mfma_kernel<64, 8>), dim3(base), dim3(512), 0, s, Q, kv, O, st, g, kg,
-                 layer, scale, sp);
+          launch_attention_mfma<64, 8>(dim3(base), s, Q, kv, O, st, g, kg, layer, scale, sp);
           ns = 1;
           break;
         }
-        launch(attention_mfma_kernel<64>, grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
-                           layer, scale, sp);
+        launch_attention_mfma<64, 4>(grid, s, Q, kv, O, st, g, kg, layer, scale, sp);
         if (ns > 1)
           launch(attention_combine_kernel<64>, dim3(g.B * g.R * kg.H), dim3(64), 0, s,
                              O, g, kg.H, sp);
         break;
       case 128:
-        launch(attention_mfma_kernel<128>, grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
-                           layer, scale, sp);
+        launch_attention_mfma<128, 4>(grid, s, Q, kv, O, st, g, kg, layer, scale, sp);
         if (ns > 1)
           launch(attention_combine_kernel<128>, dim3(g.B * g.R * kg.H), dim3(128), 0, s,
                              O, g, kg.H, sp);
