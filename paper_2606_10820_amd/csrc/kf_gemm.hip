@@ -1152,35 +1152,57 @@ hipError_t launch_tile(const GemmA& ga, const T* W, int ldw, int M, int N, int K
 
 // Reduction of a split-K GEMM: C = sum of the parts in split order, plus the
 // bias, through the GEMM's epilogue (and its LayerNorm partial sums).  One
-// thread per 8-column chunk of a row.
-template <class Ep>
+// thread per 8-column chunk of a row.  The split count is a template
+// parameter so that every load (the parts, a residual epilogue's old row, the
+// bias) is issued before the first is waited for: one memory round trip.
+template <int NS, class Ep>
 __global__ void __launch_bounds__(128)
-    splitk_reduce_kernel(const float* __restrict__ part, int splits, int M, int N, Ep ep) {
-  constexpr int SMAX = 16;
+    splitk_reduce_kernel(const float* __restrict__ part, int M, int N, Ep ep) {
   const int m = blockIdx.x, c = blockIdx.y * 128 + threadIdx.x, n = c * 8;
   const bool live = n < N;
+  const int nc = live ? n : 0;  // past-the-end threads load column 0 and store nothing
+  float x[NS][8];
+#pragma unroll
+  for (int sp = 0; sp < NS; ++sp) get8(part + ((size_t)sp * M + m) * N + nc, x[sp]);
+  float pre[8];
+  if constexpr (HasPre<Ep>::value) ep.pre8(m, nc, pre);
+  float bv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (ep.bias) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) bv[i] = ep.bias[nc + i];
+  }
   float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int sp = 0; sp < NS; ++sp)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] += x[sp][i];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] += bv[i];
   if (live) {
-    float x[SMAX][8];
-#pragma unroll
-    for (int sp = 0; sp < SMAX; ++sp)
-      if (sp < splits) get8(part + ((size_t)sp * M + m) * N + n, x[sp]);
-#pragma unroll
-    for (int sp = 0; sp < SMAX; ++sp)
-      if (sp < splits) {
-#pragma unroll
-        for (int i = 0; i < 8; ++i) v[i] += x[sp][i];
-      }
-    if (ep.bias) {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] += ep.bias[n + i];
-    }
-    ep.store8(m, n, v);
+    if constexpr (HasPre<Ep>::value) ep.store8_pre(m, n, v, pre);
+    else ep.store8(m, n, v);
   }
   if constexpr (Ep::kStats) {
     const float2 gs = ln_group16(v);
     if (live && (c & 1) == 0) ep.lnst[(size_t)ep.srow(m) * (ep.cols() / 16) + n / 16] = gs;
   }
+}
+
+template <class Ep>
+hipError_t launch_splitk_reduce(const float* part, int splits, int M, int N, const Ep& ep,
+                                hipStream_t s) {
+  const dim3 grid(M, (N / 8 + 127) / 128), block(128);
+  switch (splits) {
+    case 2: launch(splitk_reduce_kernel<2, Ep>, grid, block, 0, s, part, M, N, ep); break;
+    case 3: launch(splitk_reduce_kernel<3, Ep>, grid, block, 0, s, part, M, N, ep); break;
+    case 4: launch(splitk_reduce_kernel<4, Ep>, grid, block, 0, s, part, M, N, ep); break;
+    case 6: launch(splitk_reduce_kernel<6, Ep>, grid, block, 0, s, part, M, N, ep); break;
+    case 8: launch(splitk_reduce_kernel<8, Ep>, grid, block, 0, s, part, M, N, ep); break;
+    case 12: launch(splitk_reduce_kernel<12, Ep>, grid, block, 0, s, part, M, N, ep); break;
+    case 16: launch(splitk_reduce_kernel<16, Ep>, grid, block, 0, s, part, M, N, ep); break;
+    default: return hipErrorInvalidValue;  // launch_plain picks only the counts above
+  }
+  return hipGetLastError();
 }
 
 // A GEMM without a folded LayerNorm whose grid cannot fill the chip and whose
@@ -1211,9 +1233,7 @@ hipError_t launch_plain(const GemmA& ga, const T* W, int M, int N, int K, const 
   const EpPartial pe{ws->part, N, nullptr};
   hipError_t e = launch_tile<T, BM, BN, WM, WN, S, 0, false>(ga, W, K, M, N, K, pe, s, ks);
   if (e != hipSuccess) return e;
-  launch(splitk_reduce_kernel<Ep>, dim3(M, (N / 8 + 127) / 128), dim3(128), 0, s,
-                     ws->part, ks, M, N, ep);
-  return hipGetLastError();
+  return launch_splitk_reduce(ws->part, ks, M, N, ep, s);
 }
 
 inline int cdiv(int a, int b) { return (a + b - 1) / b; }

@@ -269,9 +269,28 @@ __global__ void __launch_bounds__(256)
   if (m >= rows) return;
   float bv = -INFINITY;
   int bi = 0x7fffffff;
-  for (int t = lane; t < n_tiles; t += 64) {
-    float v = pval[(size_t)m * n_tiles + t];
-    int i = pidx[(size_t)m * n_tiles + t];
+  // The first 8 x 64 tiles (vocabularies up to 65536) are loaded together,
+  // indices clamped into the row and masked below, so that the row costs one
+  // memory round trip; wider rows finish in a loop.
+  constexpr int U = 8;
+  const float* prv = pval + (size_t)m * n_tiles;
+  const int* pri = pidx + (size_t)m * n_tiles;
+  float vv[U];
+  int vi[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int t = lane + 64 * u, tc = t < n_tiles ? t : n_tiles - 1;
+    vv[u] = prv[tc];
+    vi[u] = pri[tc];
+  }
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const bool ok = lane + 64 * u < n_tiles;
+    if (ok && (vv[u] > bv || (vv[u] == bv && vi[u] < bi))) { bv = vv[u]; bi = vi[u]; }
+  }
+  for (int t = lane + 64 * U; t < n_tiles; t += 64) {
+    const float v = prv[t];
+    const int i = pri[t];
     if (v > bv || (v == bv && i < bi)) { bv = v; bi = i; }
   }
 #pragma unroll
