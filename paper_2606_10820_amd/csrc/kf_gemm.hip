@@ -3,7 +3,7 @@
 //   C[m][n] = epilogue( sum_k A[m][k] * W[n][k] ),   A: activations [M][K],
 //   W: weights [N][K] (PyTorch Linear layout), fp32 accumulation.
 //
-// One workgroup of 4 wavefronts computes a BM x BN tile.  K is consumed in
+// One workgroup of 4 or 8 wavefronts computes a BM x BN tile.  K is consumed in
 // 128-byte slabs (64 bf16 / 32 fp32) staged through double-buffered LDS;
 // each wavefront issues 16x16 MFMAs (v_mfma_f32_16x16x32_bf16 for bf16,
 // v_mfma_f32_16x16x4_f32 for fp32) with the weight tile as the MFMA "A"
@@ -554,23 +554,32 @@ struct GemmA {
 // ---------------------------------------------------------------- kernel
 // S-stage LDS ring fed by direct-to-LDS loads, with a register double buffer
 // of MFMA operands (pipeline described at the K loop).  Each wavefront loads
-// 8 rows (one 128-byte slab each) per instruction: BM / 32 A instructions and
-// BN / 32 W instructions per stage.
+// 8 rows (one 128-byte slab each) per instruction: BM / (8 NWV) A instructions
+// and BN / (8 NWV) W instructions per stage for NWV wavefronts.  The 128 x 128
+// and 64 x 128 body tiles run eight wavefronts (64 x 32 and 32 x 32 per
+// wavefront), held to four wavefronts per SIMD (at most 128 registers) so that
+// two workgroups share a CU: that hides the ring's barrier and LDS latencies
+// better than four wavefronts with twice the per-wavefront tile (measured
+// 3-12 % faster per GEMM at M = 512 to 4096, the results bit for bit the same;
+// with 146 registers the folded-norm 128 x 128 tile fitted one workgroup per
+// CU and was 23 % slower than with four wavefronts).
 template <typename T, int BM, int BN, int WM, int WN, int S, int MODE, bool NORM, class Ep>
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(WM * WN == 8 ? 4 : 1)))
     gemm_kernel(GemmA ga, const T* __restrict__ W, int ldw, int M, int N, int K, Ep ep,
                 int ksplit) {
   constexpr int CH = 16 / (int)sizeof(T);  // elements per 16-byte chunk
   constexpr int BK = KCH * CH;             // K per slab
   constexpr int MW = BM / WM, NW = BN / WN;
   constexpr int TM = MW / 16, TN = NW / 16;
-  constexpr int PA = BM / 32, PW = BN / 32, PER = PA + PW;
+  constexpr int NWV = WM * WN, NT = 64 * NWV;  // wavefronts, threads
+  constexpr int RPI = 8 * NWV;                // rows one DMA instruction round covers
+  constexpr int PA = BM / RPI, PW = BN / RPI, PER = PA + PW;
   constexpr int ROWB = KCH * 16;                 // bytes per staged row
-  static_assert(WM * WN == 4, "four wavefronts");
+  static_assert(NWV == 4 || NWV == 8, "four or eight wavefronts");
   static_assert(MW % 16 == 0 && NW % 16 == 0, "16x16 MFMA tiles");
-  static_assert(BM % 32 == 0 && BN % 32 == 0, "whole DMA instructions per wavefront");
+  static_assert(BM % RPI == 0 && BN % RPI == 0, "whole DMA instructions per wavefront");
   static_assert(S >= 2 && S <= 8, "ring depth");
-  static_assert((S - 1) * (BM / 32 + BN / 32) < 64, "vmcnt range");
+  static_assert((S - 1) * PER < 64, "vmcnt range");
 
   __shared__ u32x4 sbuf[S][(BM + BN) * KCH];
   __shared__ float2 sStat[NORM ? BM : 1];
@@ -599,23 +608,23 @@ __global__ void __launch_bounds__(256)
   uint32_t aoff[PA], woff[PW];
 #pragma unroll
   for (int j = 0; j < PA; ++j) {
-    const int r = wave * 8 + 32 * j + lane / 8, c = (lane & 7) ^ ((r >> 1) & 7);
+    const int r = wave * 8 + RPI * j + lane / 8, c = (lane & 7) ^ ((r >> 1) & 7);
     const int gr = m0 + r < M ? m0 + r : M - 1;
     aoff[j] = (uint32_t)(((size_t)map_row<MODE>(gr, ga.g) * ga.lda + c * CH) * sizeof(T));
   }
 #pragma unroll
   for (int j = 0; j < PW; ++j) {
-    const int r = wave * 8 + 32 * j + lane / 8, c = (lane & 7) ^ ((r >> 1) & 7);
+    const int r = wave * 8 + RPI * j + lane / 8, c = (lane & 7) ^ ((r >> 1) & 7);
     const int gr = n0 + r < N ? n0 + r : N - 1;
     woff[j] = (uint32_t)(((size_t)gr * ldw + c * CH) * sizeof(T));
   }
   auto issue = [&](int stage, int kt) {
     const uint32_t so = (uint32_t)((kbeg + kt) * BK * (int)sizeof(T));
 #pragma unroll
-    for (int j = 0; j < PA; ++j) dma16(ra, aoff[j], so, &sbuf[stage][(wave * 8 + 32 * j) * KCH]);
+    for (int j = 0; j < PA; ++j) dma16(ra, aoff[j], so, &sbuf[stage][(wave * 8 + RPI * j) * KCH]);
 #pragma unroll
     for (int j = 0; j < PW; ++j)
-      dma16(rw, woff[j], so, &sbuf[stage][(BM + wave * 8 + 32 * j) * KCH]);
+      dma16(rw, woff[j], so, &sbuf[stage][(BM + wave * 8 + RPI * j) * KCH]);
   };
 
   // LDS read offsets within a stage.  Every row a lane reads is congruent to
@@ -683,7 +692,8 @@ __global__ void __launch_bounds__(256)
   // partials are loaded before the operand loads are issued (so waiting for
   // them does not wait for the operands) and reduced by the TPR consecutive
   // lanes that share a row.
-  constexpr int TPR = NORM ? 256 / BM : 1;
+  static_assert(!NORM || NT % BM == 0, "whole threads per row for the statistics");
+  constexpr int TPR = NORM ? NT / BM : 1;
   // float4 loads (two partials each) per lane, unrolled: whole rows up to
   // K = 1024; wider rows finish in a loop.
   constexpr int PMAX = NORM ? (32 / TPR > 0 ? 32 / TPR : 1) : 1;
@@ -818,12 +828,12 @@ __global__ void __launch_bounds__(256)
       bool by_column = false;
       if constexpr (HasColumns<Ep>::value) by_column = ep.column_tile(n0);
 #pragma unroll
-      for (int c0 = 0; c0 < MW * CPR; c0 += 256) {
+      for (int c0 = 0; c0 < MW * CPR; c0 += NT) {
         const int c = c0 + tid;
         if constexpr (HasColumns<Ep>::value) {
           if (by_column) {  // 8 consecutive rows of one column per lane
             static_assert(MW % 8 == 0, "whole 8-row groups per band");
-            if (c0 + 256 <= MW * CPR || c < MW * CPR) {
+            if (c0 + NT <= MW * CPR || c < MW * CPR) {
               const int cg = c / BN, cl = c % BN;
               const int m = m0 + pass * MW + cg * 8, n = n0 + cl;
               float v[8];
@@ -834,7 +844,7 @@ __global__ void __launch_bounds__(256)
             continue;
           }
         }
-        if (c0 + 256 <= MW * CPR || c < MW * CPR) {
+        if (c0 + NT <= MW * CPR || c < MW * CPR) {
           const int rr = c / CPR, cc = c % CPR;
           const int m = m0 + pass * MW + rr, n = n0 + cc * 8;
           const bool live = m < M && n < N;
@@ -1146,7 +1156,7 @@ hipError_t launch_tile(const GemmA& ga, const T* W, int ldw, int M, int N, int K
                        hipStream_t s, int ksplit = 1) {
   const int tiles = ((N + BN - 1) / BN) * ((M + BM - 1) / BM);
   launch((gemm_kernel<T, BM, BN, WM, WN, S, MODE, NORM, Ep>), dim3(tiles * ksplit),
-                     dim3(256), 0, s, ga, W, ldw, M, N, K, ep, ksplit);
+                     dim3(64 * WM * WN), 0, s, ga, W, ldw, M, N, K, ep, ksplit);
   return hipGetLastError();
 }
 
@@ -1253,9 +1263,9 @@ hipError_t dispatch(const GemmA& ga, const T* W, int M, int N, int K, const Ep& 
   constexpr int kFill = 256;
   if constexpr (!NORM && MODE == 0) {
     if (cdiv(M, 128) * cdiv(N, 128) >= kFill)
-      return launch_plain<T, 128, 128, 2, 2, 2>(ga, W, M, N, K, ep, s, ws);
+      return launch_plain<T, 128, 128, 2, 4, 2>(ga, W, M, N, K, ep, s, ws);
     if (cdiv(M, 64) * cdiv(N, 128) >= kFill)
-      return launch_plain<T, 64, 128, 2, 2, 3>(ga, W, M, N, K, ep, s, ws);
+      return launch_plain<T, 64, 128, 2, 4, 3>(ga, W, M, N, K, ep, s, ws);
     if (cdiv(M, 64) * cdiv(N, 64) >= kFill * 3 / 4)
       return launch_plain<T, 64, 64, 2, 2, 3>(ga, W, M, N, K, ep, s, ws);
     if (cdiv(M, 32) * cdiv(N, 64) >= kFill * 3 / 4)
@@ -1263,9 +1273,9 @@ hipError_t dispatch(const GemmA& ga, const T* W, int M, int N, int K, const Ep& 
     return launch_plain<T, 32, 32, 2, 2, 4>(ga, W, M, N, K, ep, s, ws);
   } else {
     if (cdiv(M, 128) * cdiv(N, 128) >= kFill)
-      return launch_tile<T, 128, 128, 2, 2, 2, MODE, NORM>(ga, W, K, M, N, K, ep, s);
+      return launch_tile<T, 128, 128, 2, 4, 2, MODE, NORM>(ga, W, K, M, N, K, ep, s);
     if (cdiv(M, 64) * cdiv(N, 128) >= kFill)
-      return launch_tile<T, 64, 128, 2, 2, 3, MODE, NORM>(ga, W, K, M, N, K, ep, s);
+      return launch_tile<T, 64, 128, 2, 4, 3, MODE, NORM>(ga, W, K, M, N, K, ep, s);
     if (cdiv(M, 64) * cdiv(N, 64) >= kFill * 3 / 4)
       return launch_tile<T, 64, 64, 2, 2, 3, MODE, NORM>(ga, W, K, M, N, K, ep, s);
     if (cdiv(M, 32) * cdiv(N, 64) >= kFill * 3 / 4)
@@ -1361,7 +1371,7 @@ hipError_t gemm_head_ln(const T* Xh, const LnFold& ln, const T* W, int M, int Vp
     // 128-row tiles from 129 rows on: each weight tile is read by half as many
     // workgroups (LM1B-shaped batch 64, 256 head rows: 24.5 -> 19.3 us per head)
     if (M <= 128)
-      return launch_tile<T, 64, kHeadTileN, 2, 2, 3, MODE, true>(ga, W, d, M, Vpad, d, ep, s);
+      return launch_tile<T, 64, kHeadTileN, 2, 4, 3, MODE, true>(ga, W, d, M, Vpad, d, ep, s);
     return launch_tile<T, 128, kHeadTileN, 2, 2, 2, MODE, true>(ga, W, d, M, Vpad, d, ep, s);
   };
   if (gather == 2) return go(std::integral_constant<int, 2>{});
@@ -1397,7 +1407,7 @@ hipError_t gemm_head_sample(const T* Xh, const LnFold& ln, const T* W, int M, in
   if (M <= 32)
     return launch_tile<T, 32, kHeadTileN, 1, 4, 3, 0, true>(ga, W, d, M, Vpad, d, ep, s);
   if (M <= 512)
-    return launch_tile<T, 64, kHeadTileN, 2, 2, 3, 0, true>(ga, W, d, M, Vpad, d, ep, s);
+    return launch_tile<T, 64, kHeadTileN, 2, 4, 3, 0, true>(ga, W, d, M, Vpad, d, ep, s);
   return launch_tile<T, 128, kHeadTileN, 2, 2, 2, 0, true>(ga, W, d, M, Vpad, d, ep, s);
 }
 
