@@ -1046,13 +1046,27 @@ __global__ void __launch_bounds__(64 * KW)
   // would wait for loads still in flight): batch B loads while batch A feeds
   // the MFMAs, and the other way round.
   u32x4 wa[U], xa[U], wb[U], xb[U];
-  // Steps past the end re-load the last step (valid memory); mma() skips them.
+  // Four wavefronts (one batch covers a K range of up to 8 steps): steps past
+  // the end load an earlier step instead (valid memory, and a different
+  // address from every other load of the batch: loads of one address would be
+  // merged into one and copied, and a copy waits for its load), so the batch
+  // is straight-line code.  Sixteen wavefronts (two batches of 4, six steps)
+  // keep zero-filled loads behind the step bound: with the straight-line form
+  // the compiler made each load of the second batch wait for the first batch
+  // (MLP-down at batch 1: 7.6 -> 9.0 us).  mma() skips the steps past the end.
   auto load = [&](u32x4 (&w)[U], u32x4 (&x)[U], int s0) {
 #pragma unroll
     for (int i = 0; i < U; ++i) {
-      const int t = s0 + i < steps ? s0 + i : steps - 1;
-      w[i] = pw[4 * t];
-      x[i] = pa[4 * t];
+      if constexpr (KW >= 16) {
+        const int t = s0 + i;
+        const u32x4 z = {0u, 0u, 0u, 0u};
+        w[i] = t < steps ? pw[4 * t] : z;
+        x[i] = t < steps ? pa[4 * t] : z;
+      } else {
+        const int t = s0 + i < steps ? s0 + i : (s0 + i) % steps;
+        w[i] = pw[4 * t];
+        x[i] = pa[4 * t];
+      }
     }
   };
   auto mma = [&](const u32x4 (&w)[U], const u32x4 (&x)[U], int s0) {
