@@ -287,8 +287,9 @@ int kf_selfforcing_targets(kf_ctx *ctx, int B, int N, int k, const int32_t *toke
  * While a class is selected, each of its launches is bracketed by an event
  * pair.  kf_kernel_time() synchronises and returns the summed milliseconds
  * and the launch count of one class since timing was last set. */
-#define KF_KC_EMBED 0    /* real-row embedding */
-#define KF_KC_NOISE 1    /* noise sinusoid + noise-MLP GEMMs + position add */
+#define KF_KC_EMBED 0    /* real-row embedding (in kf_generate also the noise rows' position add) */
+#define KF_KC_NOISE 1    /* noise sinusoid + noise-MLP GEMMs + position add (kf_generate: the
+                            sinusoids and GEMMs of whole chunks of passes, computed ahead) */
 #define KF_KC_NORM 2     /* standalone LayerNorm (none: every LayerNorm is folded into the GEMM that consumes it) */
 #define KF_KC_QKV 3      /* LayerNorm-folded QKV GEMM with KV append */
 #define KF_KC_ATTN 4     /* block attention */

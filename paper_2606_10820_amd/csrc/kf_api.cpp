@@ -11,6 +11,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <functional>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -38,6 +39,9 @@ constexpr size_t kServeGraphs = 16;
 // Rows per sampling-head chunk of kf_teacher_targets: the head partials of a
 // chunk take rows * (Vpad / 128) * 36 bytes (about 116 MB at vocabulary 50257).
 constexpr int kTeacherChunk = 8192;
+// Noise rows computed ahead per chunk of generate passes (kf_generate): at
+// least this many rows per chunk, or one pass of the largest batch.
+constexpr int kNoiseAheadRows = 8192;
 
 // ------------------------------------------------------------ memory plan
 struct LayerOff {
@@ -74,6 +78,8 @@ struct Plan {
   size_t tmax = 0, tsub = 0;               // sampling-head partials of one chunk
   size_t att_m = 0, att_l = 0, att_o = 0;  // attention key-split partial states
   size_t split_part = 0;                   // split-K GEMM parts
+  int nz_rows = 0;                         // noise rows computed ahead: capacity
+  size_t nzA = 0, nzH = 0, nz = 0;         // their sinusoids, hidden layer, output (fp32)
   size_t total = 0;
 };
 
@@ -218,6 +224,10 @@ void make_plan(const kf_config& c, Plan& p) {
   p.att_l = take((size_t)kAttnEntries * 4);
   p.att_o = take((size_t)kAttnEntries * (d / c.n_head) * 4);
   p.split_part = take(kSplitBytes);
+  p.nz_rows = kNoiseAheadRows > c.max_batch * c.max_k ? kNoiseAheadRows : c.max_batch * c.max_k;
+  p.nzA = take((size_t)p.nz_rows * d * es);
+  p.nzH = take((size_t)p.nz_rows * 4 * d * es);
+  p.nz = take((size_t)p.nz_rows * d * 4);
   p.total = off;
 }
 
@@ -386,6 +396,9 @@ struct StepIn {
   // kf_decode_block_noalloc: partial results in the library's device scratch
   // instead of the state buffer's workspace
   const Scratch* scr = nullptr;
+  // kf_generate: the noise rows come from the encoder output computed ahead
+  // (the embedding kernel writes them; no noise kernels in the step)
+  const kf::NoiseAhead* na = nullptr;
 };
 
 
@@ -438,11 +451,12 @@ int run_step(kf_ctx* c, const StepIn& in) {
 
   if (in.reset && in.serve) KF_HIP(c, kf::launch_seq_reset(g, s));
   else if (in.reset) KF_HIP(c, kf::launch_zero_i32(reinterpret_cast<int*>(st), 1, s));
-  if (in.nr > 0)
+  if (in.nr > 0 || (in.na && in.k > 0))
     KF_LAUNCH(c, KF_KC_EMBED,
               kf::launch_embed_real<T>(X, Xh, lnst, tok, pos, in.toks, in.tok_stride,
-                                       in.toks_by_slot ? 1 : 0, g, d, V, st, s));
-  if (in.k > 0) {
+                                       in.toks_by_slot ? 1 : 0, g, d, V, st, s,
+                                       in.k > 0 ? in.na : nullptr));
+  if (in.k > 0 && !in.na) {
     const int Mk = in.B * in.k;
     float* urec = reinterpret_cast<float*>(base + p.noise);
     KF_LAUNCH(c, KF_KC_NOISE,
@@ -713,11 +727,47 @@ void drop_serve_graphs(kf_ctx* c) {
 // context for the next call with the same arguments.  Graphs need a real
 // stream (capture is impossible on the legacy null stream) and are not used
 // while kernel timing is on.
-int repeat_step(kf_ctx* c, const StepIn& in, int count, int adv, int N, int L) {
+// The noise encoder for passes pass0 .. pass0 + npass - 1 of a lock-step
+// generate of B sequences (prompt N, k noise rows a pass), into the plan's
+// ahead buffers: sinusoids, Linear(d, 4d) + GELU, Linear(4d, d) in fp32
+// without its bias (the embedding kernel adds the bias, the position and the
+// temperature embedding when the pass runs).  One launch per layer for the
+// whole chunk instead of three or four per pass.
+template <typename T>
+int run_noise_ahead(kf_ctx* c, int B, int k, int N, uint64_t seed, int pass0, int npass) {
+  const Plan& p = c->plan;
+  char* base = c->base;
+  const int d = c->cfg.d_model, M = npass * B * k;
+  hipStream_t s = c->stream;
+  T* A = reinterpret_cast<T*>(base + p.nzA);
+  T* H = reinterpret_cast<T*>(base + p.nzH);
+  auto F = [&](size_t o) { return reinterpret_cast<const float*>(base + o); };
+  auto W = [&](size_t o) { return reinterpret_cast<const T*>(base + o); };
+  KF_LAUNCH(c, KF_KC_NOISE,
+            kf::launch_noise_sinusoid_ahead<T>(A, seed, reinterpret_cast<const double*>(base + p.omega),
+                                               B, k, N, pass0, npass, d, s));
+  KF_LAUNCH(c, KF_KC_NOISE,
+            kf::gemm_bias<T>(A, W(p.nw1), M, 4 * d, d, F(p.nb1), kf::Act::Gelu, H, 4 * d, nullptr, s));
+  KF_LAUNCH(c, KF_KC_NOISE,
+            kf::gemm_f32<T>(H, W(p.nw2), M, d, 4 * d, reinterpret_cast<float*>(base + p.nz), s));
+  return KF_OK;
+}
+
+int noise_ahead(kf_ctx* c, int B, int k, int N, uint64_t seed, int pass0, int npass) {
+  return c->cfg.dtype == KF_BF16 ? run_noise_ahead<bf16>(c, B, k, N, seed, pass0, npass)
+                                 : run_noise_ahead<float>(c, B, k, N, seed, pass0, npass);
+}
+
+// before(i) runs on the host before decode pass i = 1 .. count is issued
+// (between graph replays: it may launch work of its own on the stream).
+int repeat_step(kf_ctx* c, const StepIn& in, int count, int adv, int N, int L,
+                const std::function<int(int)>& before = nullptr) {
   if (count <= 0) return KF_OK;
   if (!c->graphs || c->stream == nullptr || c->timing) {
     for (int i = 0; i < count; ++i) {
-      int r = step(c, in);
+      int r = before ? before(i + 1) : KF_OK;
+      if (r) return r;
+      r = step(c, in);
       if (r) return r;
       c->C += adv;
     }
@@ -744,6 +794,10 @@ int repeat_step(kf_ctx* c, const StepIn& in, int count, int adv, int N, int L) {
     c->gkey = key;
   }
   for (int i = 0; i < count; ++i) {
+    if (before) {
+      int r = before(i + 1);
+      if (r) return r;
+    }
     KF_HIP(c, hipGraphLaunch(c->gexec, c->stream));
     c->C += adv;
   }
@@ -1253,15 +1307,30 @@ int kf_generate(kf_ctx* c, int B, int N, const int32_t* prompt, int L, int k, ui
   if (r) return r;
   if (L == 0) return KF_OK;
   if ((r = lockstep_begin(c, B))) return r;
+  // The noise rows of every pass (the prefill is pass 0) come from the noise
+  // encoder computed ahead, qp passes at a time.
+  const Plan& p = c->plan;
+  const int passes = L / k, qp = p.nz_rows / (B * k);
+  const void* temb = (cf.flags & KF_FLAG_TEMPERATURE) ? c->base + p.temb : nullptr;
+  const kf::NoiseAhead na0{reinterpret_cast<const float*>(c->base + p.nz),
+                           reinterpret_cast<const float*>(c->base + p.nb2), temb, N, qp, 0};
+  if ((r = noise_ahead(c, B, k, N, seed, 0, passes < qp ? passes : qp))) return r;
   StepIn in{B, N, k, prompt, N, nullptr, nullptr, seed, out_desc(c, out, L, N), true};
+  in.na = &na0;
   r = step(c, in);
   if (r) return r;
   c->live = true;
   c->B = B;
   c->C = N;
   c->pending = k;
+  kf::NoiseAhead nad = na0;
+  nad.pass = -1;  // from the committed length
   StepIn dn{B, k, k, pend_ptr(c), cf.max_k, nullptr, nullptr, seed, out_desc(c, out, L, N), false};
-  return repeat_step(c, dn, L / k - 1, k, N, L);
+  dn.na = &nad;
+  return repeat_step(c, dn, passes - 1, k, N, L, [&](int i) {
+    if (i % qp) return (int)KF_OK;
+    return noise_ahead(c, B, k, N, seed, i, passes - i < qp ? passes - i : qp);
+  });
 }
 
 int kf_prefill_ar(kf_ctx* c, int B, int N, const int32_t* prompt, const float* u, int32_t* out) {

@@ -1363,6 +1363,13 @@ hipError_t gemm_bias(const T* A, const T* W, int M, int N, int K, const float* b
 }
 
 template <typename T>
+hipError_t gemm_f32(const T* A, const T* W, int M, int N, int K, float* out, hipStream_t s) {
+  const EpPartial ep{out, N, nullptr};
+  return dispatch<T, 0, false>(GemmA{A, K, M, nullptr, nullptr, nullptr, KfStepGeom{}}, W, M, N, K,
+                               ep, s, nullptr);
+}
+
+template <typename T>
 hipError_t gemm_residual(const T* A, const T* W, int M, int N, int K, const float* bias, float* X,
                          T* Xh, float2* lnst, const SplitWs* ws, hipStream_t s) {
   EpResidual<T> ep{X, Xh, N, bias, lnst};
@@ -1459,6 +1466,7 @@ hipError_t launch_ln_fold(const T* W, T* Wout, const float* g, const float* beta
 }
 
 #define KF_INST(T)                                                                                 \
+  template hipError_t gemm_f32<T>(const T*, const T*, int, int, int, float*, hipStream_t);          \
   template hipError_t gemm_bias<T>(const T*, const T*, int, int, int, const float*, Act, T*, int, \
                                    const SplitWs*, hipStream_t);                                   \
   template hipError_t gemm_residual<T>(const T*, const T*, int, int, int, const float*, float*,   \

@@ -179,13 +179,39 @@ struct SplitWs {
   size_t bytes;
 };
 
+// The noise encoder's output computed ahead for whole chunks of the passes of a
+// lock-step generate (the encoder depends on u, the position and the
+// temperature only, never on the emitted tokens).  nz [qp passes][B*k][d]
+// (fp32, without the second layer's bias): pass p's rows sit in chunk slot
+// p % qp.  pass >= 0 names the step's pass; pass < 0 derives it from the
+// committed length, pass = (C - N) / k + 1 (a decode block of the generate).
+struct NoiseAhead {
+  const float* nz;
+  const float* bias;  // second noise-MLP layer's bias [d]
+  const void* temb;   // per-slot temperature embedding [slots][d] (compute dtype), or null
+  int N;              // prompt length of the generate
+  int qp;             // passes per chunk
+  int pass;
+};
+
 // Real-row embedding: X[b*R + i] = tok[toks[q*tok_stride + i]] + pos[C_b + i], i < nr,
 // with its compute-dtype copy Xh and LayerNorm partial sums lnst (see gemm_residual);
 // q = b, or the step's sequence slot when toks_by_slot (the pending-token buffer).
+// With na, also the step's k noise rows from the encoder output computed ahead:
+// X[b*R + nr + j] = (nz + bias) + pos[C_b + nr + j] (+ temb[slot b]).
 template <typename T>
 hipError_t launch_embed_real(float* X, T* Xh, float2* lnst, const T* tok, const T* pos,
                              const int32_t* toks, int tok_stride, int toks_by_slot, KfStepGeom g,
-                             int d, int V, KfDevState* st, hipStream_t s);
+                             int d, int V, KfDevState* st, hipStream_t s,
+                             const NoiseAhead* na = nullptr);
+
+// Sinusoids of the noise rows of passes pass0 .. pass0 + npass - 1 of a
+// lock-step generate (prompt length N, sequence b in slot b) into
+// S [npass*B*k][d]: row ((pass - pass0) B + b) k + j has u from the device
+// Philox stream at position N + pass k + j.
+template <typename T>
+hipError_t launch_noise_sinusoid_ahead(T* S, uint64_t seed, const double* omega, int B, int k,
+                                       int N, int pass0, int npass, int d, hipStream_t s);
 
 // Sinusoid of each noise row's u into S [B*k][d]; u from noise [B*k] or, when
 // noise is null, from the device Philox stream at positions C_b + nr + j.
@@ -214,6 +240,9 @@ hipError_t launch_attention(const T* Q, const T* kv, T* O, const KfDevState* st,
 template <typename T>
 hipError_t gemm_bias(const T* A, const T* W, int M, int N, int K, const float* bias, Act act,
                      T* out, int ldo, const SplitWs* ws, hipStream_t s);
+// out[M][N] = A . W^T in fp32 (no bias, no split).
+template <typename T>
+hipError_t gemm_f32(const T* A, const T* W, int M, int N, int K, float* out, hipStream_t s);
 // Residual update X[M][N] += C + bias; with a 16-bit T the updated rows are
 // also written to Xh (the compute-dtype copy of the residual stream; for fp32,
 // Xh aliases X and is not written).  Every writer of the residual stream also

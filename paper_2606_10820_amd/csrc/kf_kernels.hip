@@ -28,12 +28,41 @@ __device__ inline float wave_sum(float v) {
 
 // ------------------------------------------------------------ embedding
 // Real rows (Appendix C.1, Embed): token table row plus learned position.
+// With nz (the noise encoder's output for whole chunks of passes, computed
+// ahead by kf_generate: NoiseAhead), workgroups past the real rows write the
+// step's noise rows from it: noise MLP output + its bias + position (+ the
+// sequence's temperature embedding), the sums taken in the order the noise
+// GEMM's epilogue takes them.
 template <typename T>
 __global__ void __launch_bounds__(256)
     embed_real_kernel(float* __restrict__ X, T* __restrict__ Xh, float2* __restrict__ lnst,
                       const T* __restrict__ tok, const T* __restrict__ pos,
                       const int32_t* __restrict__ toks, int tok_stride, int toks_by_slot,
-                      KfStepGeom g, int d, int V, KfDevState* st) {
+                      KfStepGeom g, int d, int V, KfDevState* st, NoiseAhead na) {
+  const int grp = threadIdx.x;  // one thread per 16 columns (d <= 2048)
+  if ((int)blockIdx.x >= g.B * g.nr) {
+    const int q = blockIdx.x - g.B * g.nr, b = q / g.k, j = q - b * g.k;
+    const int C = g.ctx(st, b);
+    int pass = na.pass >= 0 ? na.pass : (C - na.N) / g.k + 1;
+    pass = pass > 0 ? pass : 0;  // (a lock-step generate has C >= N here)
+    const size_t row = (size_t)b * g.R + g.nr + j;
+    const float* nzr = na.nz + ((size_t)(pass % na.qp) * g.B * g.k + q) * d;
+    const T* pe = pos + (size_t)(C + g.nr + j) * d;
+    const T* tb = na.temb ? static_cast<const T*>(na.temb) + (size_t)g.slot(b) * d : nullptr;
+    if (grp < d / 16) {
+      float v[16];
+#pragma unroll
+      for (int c = 0; c < 16; ++c) {
+        const int e = grp * 16 + c;
+        v[c] = (nzr[e] + na.bias[e]) + to_f(pe[e]);
+        if (tb) v[c] += to_f(tb[e]);
+        X[row * d + e] = v[c];
+        if constexpr (sizeof(T) == 2) Xh[row * d + e] = from_f<T>(v[c]);
+      }
+      lnst[row * (d / 16) + grp] = ln_group16_one(v);
+    }
+    return;
+  }
   const int r = blockIdx.x;
   const int b = r / g.nr, i = r % g.nr;
   const int C = g.ctx(st, b);
@@ -47,8 +76,7 @@ __global__ void __launch_bounds__(256)
   const T* te = tok + (size_t)t * d;
   const T* pe = pos + (size_t)(C + i) * d;
   T* xh = Xh + row * d;
-  // one thread per 16 columns (d <= 2048): the row and its LayerNorm partials
-  const int grp = threadIdx.x;
+  // the row and its LayerNorm partials
   if (grp < d / 16) {
     float v[16];
 #pragma unroll
@@ -63,6 +91,21 @@ __global__ void __launch_bounds__(256)
 }
 
 // ------------------------------------------------------- noise sinusoid
+// One row of the sinusoid of u (the expansion described below).
+template <typename T>
+__device__ inline void sinusoid_row(T* __restrict__ row, float u, const double* __restrict__ omega,
+                                    int d) {
+  const int h = d / 2;
+  const double su = 1000.0 * (double)u;
+  for (int i = threadIdx.x; i < h; i += blockDim.x) {
+    double a = su * omega[i];
+    double sn, cs;
+    sincos(a, &sn, &cs);
+    row[i] = from_f<T>((float)cs);
+    row[h + i] = from_f<T>((float)sn);
+  }
+}
+
 // Noise rows: the scalar u of each noise token is expanded into d features,
 // cos(a_i) then sin(a_i) with a_i = 1000 u omega_i, omega_i = 10000^(-i/(d/2)),
 // evaluated in double so that fp32 u keeps its full resolution.
@@ -75,16 +118,19 @@ __global__ void __launch_bounds__(256)
   const int b = m / g.k, j = m % g.k;
   float u = noise ? noise[m] : kf_noise_u(seed, g.slot(b), g.ctx(st, b) + g.nr + j);
   if (u_out && threadIdx.x == 0) u_out[m] = u;
-  const int h = d / 2;
-  const double su = 1000.0 * (double)u;
-  T* row = S + (size_t)m * d;
-  for (int i = threadIdx.x; i < h; i += blockDim.x) {
-    double a = su * omega[i];
-    double sn, cs;
-    sincos(a, &sn, &cs);
-    row[i] = from_f<T>((float)cs);
-    row[h + i] = from_f<T>((float)sn);
-  }
+  sinusoid_row(S + (size_t)m * d, u, omega, d);
+}
+
+// The sinusoids of the noise rows of passes pass0, pass0 + 1, ... of a
+// lock-step generate (sequence b in slot b, prompt length N, k rows a pass):
+// row m = ((pass - pass0) B + b) k + j holds u at position N + pass k + j.
+template <typename T>
+__global__ void __launch_bounds__(256)
+    noise_sinusoid_ahead_kernel(T* __restrict__ S, uint64_t seed, const double* __restrict__ omega,
+                                int B, int k, int N, int pass0, int d) {
+  const int m = blockIdx.x, bk = B * k;
+  const int pass = pass0 + m / bk, q = m % bk, b = q / k, j = q - b * k;
+  sinusoid_row(S + (size_t)m * d, kf_noise_u(seed, b, N + pass * k + j), omega, d);
 }
 
 // ------------------------------------------------------ block attention
@@ -651,10 +697,21 @@ inline unsigned grid_for(size_t n, unsigned block) {
 template <typename T>
 hipError_t launch_embed_real(float* X, T* Xh, float2* lnst, const T* tok, const T* pos,
                              const int32_t* toks, int tok_stride, int toks_by_slot, KfStepGeom g,
-                             int d, int V, KfDevState* st, hipStream_t s) {
-  if (g.nr <= 0 || g.B <= 0) return hipSuccess;
-  launch(embed_real_kernel<T>, dim3(g.B * g.nr), dim3(256), 0, s, X, Xh, lnst, tok, pos, toks,
-                     tok_stride, toks_by_slot, g, d, V, st);
+                             int d, int V, KfDevState* st, hipStream_t s, const NoiseAhead* na) {
+  const int blocks = g.B * g.nr + (na ? g.B * g.k : 0);
+  if (blocks <= 0) return hipSuccess;
+  const NoiseAhead none{nullptr, nullptr, nullptr, 0, 1, 0};
+  launch(embed_real_kernel<T>, dim3(blocks), dim3(256), 0, s, X, Xh, lnst, tok, pos, toks,
+                     tok_stride, toks_by_slot, g, d, V, st, na ? *na : none);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_noise_sinusoid_ahead(T* S, uint64_t seed, const double* omega, int B, int k,
+                                       int N, int pass0, int npass, int d, hipStream_t s) {
+  if (B <= 0 || k <= 0 || npass <= 0) return hipSuccess;
+  launch(noise_sinusoid_ahead_kernel<T>, dim3(npass * B * k), dim3(256), 0, s, S, seed, omega, B,
+         k, N, pass0, d);
   return hipGetLastError();
 }
 
@@ -837,7 +894,9 @@ hipError_t launch_zero_i32(int* dst, size_t n, hipStream_t s) { return launch_ze
 #define KF_INST(T)                                                                                  \
   template hipError_t launch_embed_real<T>(float*, T*, float2*, const T*, const T*,               \
                                            const int32_t*, int, int, KfStepGeom, int, int,         \
-                                           KfDevState*, hipStream_t);                               \
+                                           KfDevState*, hipStream_t, const NoiseAhead*);            \
+  template hipError_t launch_noise_sinusoid_ahead<T>(T*, uint64_t, const double*, int, int, int,   \
+                                                     int, int, int, hipStream_t);                  \
   template hipError_t launch_noise_sinusoid<T>(T*, const float*, uint64_t, const double*,          \
                                                KfStepGeom, int, const KfDevState*, float*,          \
                                                hipStream_t);                                        \

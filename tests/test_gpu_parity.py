@@ -317,3 +317,22 @@ def test_graph_replay_matches_direct(toy):
             res[graphs] = outs
     for a, b in zip(res[False], res[True]):
         np.testing.assert_array_equal(a, b)
+
+
+def test_generate_noise_chunks_match_steps():
+    """A generate long enough for three chunks of noise rows computed ahead
+    (128 sequences, k = 4: 16 passes a chunk, 40 passes) gives exactly the
+    tokens of the explicit prefill / decode-block sequence with the same noise
+    (fp32: both noise GEMMs accumulate each element in the same order)."""
+    cfg = S.ModelConfig(2, 128, 4, 512, 1024, 256, S.DTYPE_FP32)
+    blob = S.pack_blob(cfg, S.make_weights(cfg, seed=4, random_affine=True))
+    B, N, L, k, seed = 128, 16, 160, 4, 12
+    prompt = S.prompts_uniform(5, B, N, cfg.vocab)
+    kf = _ctx(cfg, B, k, N, blob)
+    out = kf.generate(prompt, L, k, seed).cpu().numpy()
+    assert kf.get_state() == (N + L - k, k, B)
+    kf2 = _ctx(cfg, B, k, N, blob)
+    t = [kf2.prefill(prompt, k, kf2.fill_noise(seed, B, N, k)).cpu().numpy()]
+    for p in range(N + k, N + L, k):
+        t.append(kf2.decode_block(kf2.fill_noise(seed, B, p, k)).cpu().numpy())
+    np.testing.assert_array_equal(np.concatenate(t, axis=1), out)

@@ -110,3 +110,41 @@ def test_lm1b_shape_temperature_bf16(B):
     st = _teacher_forced(kf, O.Model(blob), prompt, taus, [4, 4], seed=5, tol=TOL[1],
                          rows=[0, B - 1])
     report(f"lm1b bf16 temperature B={B}", st)
+
+
+def test_toy_temperature_generate():
+    """kf_generate of a temperature-conditioned model: the noise rows of every
+    pass come from the noise encoder computed ahead for the whole generate, the
+    temperature embedding added by the embedding kernel.  Tokens against the
+    oracle on the GPU's own history (near-ties exempt), and equal to the
+    explicit prefill / decode-block sequence with the same noise, whose noise
+    rows go through the per-step encoder."""
+    blob = S.pack_blob(TOY_T, S.make_weights(TOY_T, seed=2, random_affine=True))
+    model = O.Model(blob)
+    B, N, L, k, seed = 4, 16, 48, 4, 31
+    taus = np.asarray([0.05, 0.3, 0.7, 1.0], np.float32)
+    kf = _ctx(TOY_T, blob, B, k, N)
+    kf.set_temperature(taus)
+    prompt = S.prompts_uniform(3, B, N, TOY_T.vocab)
+    out = kf.generate(prompt, L, k, seed).cpu().numpy()
+    near_total = 0
+    for b in range(B):
+        s = model.seq()
+        s.set_temperature(float(taus[b]))
+        pending = list(prompt[b])
+        for p in range(N, N + L, k):
+            u = [O.noise_u(seed, b, p + j) for j in range(k)]
+            ol, _ = s.step(pending, u, commit=True)
+            toks = out[b, p - N:p - N + k]
+            top = np.sort(ol, axis=1)
+            near = (top[:, -1] - top[:, -2]) < TOL[0] * np.abs(ol).max(axis=1)
+            assert np.all((toks == O.argmax(ol)) | near), (b, p)
+            near_total += int(near.sum())
+            pending = list(toks)
+    _log(f"temperature generate: near-ties {near_total} of {B * L}")
+    kf2 = _ctx(TOY_T, blob, B, k, N)
+    kf2.set_temperature(taus)
+    t = [kf2.prefill(prompt, k, kf2.fill_noise(seed, B, N, k)).cpu().numpy()]
+    for p in range(N + k, N + L, k):
+        t.append(kf2.decode_block(kf2.fill_noise(seed, B, p, k)).cpu().numpy())
+    np.testing.assert_array_equal(np.concatenate(t, axis=1), out)
