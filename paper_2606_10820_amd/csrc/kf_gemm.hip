@@ -563,15 +563,18 @@ struct GemmA {
 // 3-12 % faster per GEMM at M = 512 to 4096, the results bit for bit the same;
 // with 146 registers the folded-norm 128 x 128 tile fitted one workgroup per
 // CU and was 23 % slower than with four wavefronts).
-template <typename T, int BM, int BN, int WM, int WN, int S, int MODE, bool NORM, class Ep>
-__global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(WM * WN == 8 ? 4 : 1)))
+template <typename T, int BM, int BN, int WM, int WN, int S, int MODE, bool NORM, class Ep,
+          int KG = 1>
+__global__ void __launch_bounds__(64 * WM * WN * KG)
+    __attribute__((amdgpu_waves_per_eu(WM * WN * KG == 8 ? 4 : 1)))
     gemm_kernel(GemmA ga, const T* __restrict__ W, int ldw, int M, int N, int K, Ep ep,
                 int ksplit) {
   constexpr int CH = 16 / (int)sizeof(T);  // elements per 16-byte chunk
   constexpr int BK = KCH * CH;             // K per slab
   constexpr int MW = BM / WM, NW = BN / WN;
   constexpr int TM = MW / 16, TN = NW / 16;
-  constexpr int NWV = WM * WN, NT = 64 * NWV;  // wavefronts, threads
+  constexpr int NWV = WM * WN;                // wavefronts of one K group
+  constexpr int NT = 64 * NWV * KG;           // threads
   constexpr int RPI = 8 * NWV;                // rows one DMA instruction round covers
   constexpr int PA = BM / RPI, PW = BN / RPI, PER = PA + PW;
   constexpr int ROWB = KCH * 16;                 // bytes per staged row
@@ -580,11 +583,17 @@ __global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_
   static_assert(BM % RPI == 0 && BN % RPI == 0, "whole DMA instructions per wavefront");
   static_assert(S >= 2 && S <= 8, "ring depth");
   static_assert((S - 1) * PER < 64, "vmcnt range");
+  static_assert(KG == 1 || KG == 2, "one or two K groups");
+  static_assert(KG == 1 || (!NORM && !IsHead<Ep>::value), "K groups: plain epilogues only");
 
-  __shared__ u32x4 sbuf[S][(BM + BN) * KCH];
+  __shared__ u32x4 sbuf[KG][S][(BM + BN) * KCH];
   __shared__ float2 sStat[NORM ? BM : 1];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  // K group kg (of KG) runs its own ring over its share of the K steps;
+  // wave is the wavefront's index inside its group.
+  const int kg = KG == 1 ? 0 : (tid >> 6) / NWV;
+  const int wave = KG == 1 ? tid >> 6 : (tid >> 6) % NWV;
   const int wm = wave / WN, wn = wave % WN;
   const int gm = (M + BM - 1) / BM, gn = (N + BN - 1) / BN;
   // ksplit > 1 only with EpPartial: workgroup (tile, split) takes K steps
@@ -593,8 +602,8 @@ __global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_
   int tmi, tni;
   tile_coords((int)blockIdx.x / ksplit, gm, gn, tmi, tni);
   const int m0 = tmi * BM, n0 = tni * BN;
-  const int nk = K / BK / ksplit;
-  const int kbeg = split * nk;
+  const int nk = K / BK / ksplit / KG;  // K steps of this wavefront's group
+  const int kbeg = (split * KG + kg) * nk;
   if constexpr (std::is_same<Ep, EpPartial>::value) ep.part += (size_t)split * M * ep.ldp;
 
   const T* A = static_cast<const T*>(ga.A);
@@ -621,10 +630,10 @@ __global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_
   auto issue = [&](int stage, int kt) {
     const uint32_t so = (uint32_t)((kbeg + kt) * BK * (int)sizeof(T));
 #pragma unroll
-    for (int j = 0; j < PA; ++j) dma16(ra, aoff[j], so, &sbuf[stage][(wave * 8 + RPI * j) * KCH]);
+    for (int j = 0; j < PA; ++j) dma16(ra, aoff[j], so, &sbuf[kg][stage][(wave * 8 + RPI * j) * KCH]);
 #pragma unroll
     for (int j = 0; j < PW; ++j)
-      dma16(rw, woff[j], so, &sbuf[stage][(BM + wave * 8 + RPI * j) * KCH]);
+      dma16(rw, woff[j], so, &sbuf[kg][stage][(BM + wave * 8 + RPI * j) * KCH]);
   };
 
   // LDS read offsets within a stage.  Every row a lane reads is congruent to
@@ -662,7 +671,7 @@ __global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_
     u32x4 b[TM];  // activation rows (MFMA "B")
   };
   auto read_slice = [&](int stage, int s, Slice& f) {
-    const uint32_t sb = lds_addr(&sbuf[stage][0]);
+    const uint32_t sb = lds_addr(&sbuf[kg][stage][0]);
 #pragma unroll
     for (int tn = 0; tn < TN; ++tn) f.a[tn] = ds_read16(sb + rdW[s] + tn * 16 * ROWB);
 #pragma unroll
@@ -800,6 +809,35 @@ __global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_
       }
     }
   }
+  if constexpr (KG == 2) {
+    // Group 1's sums (the second half of K) are added to group 0's through
+    // LDS: the same order as a two-way split summed by the reduction kernel.
+    float4* xch = reinterpret_cast<float4*>(&sbuf[1][0][0]);
+    static_assert(NWV * TN * TM * 64 * 16 <= S * (BM + BN) * KCH * 16, "exchange fits the ring");
+    __syncthreads();  // both rings are read out
+    if (kg == 1) {
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm) {
+          const f32x4 v = acc[tn][tm];
+          xch[((wave * TN + tn) * TM + tm) * 64 + lane] = make_float4(v[0], v[1], v[2], v[3]);
+        }
+    }
+    __syncthreads();
+    if (kg == 0) {
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm) {
+          const float4 v = xch[((wave * TN + tn) * TM + tm) * 64 + lane];
+          acc[tn][tm][0] += v.x;
+          acc[tn][tm][1] += v.y;
+          acc[tn][tm][2] += v.z;
+          acc[tn][tm][3] += v.w;
+        }
+    }
+  }
 
   // Folded LayerNorm (if any) and bias for 16x16 tile (tn, tm).  The row
   // statistics of this lane's TM rows are read from LDS once, here.
@@ -830,11 +868,11 @@ __global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_
     constexpr int CPR = BN / 8;   // chunks per row
     static_assert(MW * SROW * 4 <= S * (BM + BN) * KCH * 16, "staging fits the ring");
     static_assert((MW * CPR) % 64 == 0, "whole wavefronts per chunk pass");
-    float* stage = reinterpret_cast<float*>(&sbuf[0][0]);
+    float* stage = reinterpret_cast<float*>(&sbuf[0][0][0]);
     __syncthreads();  // every wavefront is done reading the ring
 #pragma unroll
     for (int pass = 0; pass < WM; ++pass) {
-      if (wm == pass) {
+      if (kg == 0 && wm == pass) {
 #pragma unroll
         for (int tn = 0; tn < TN; ++tn)
 #pragma unroll
@@ -1189,12 +1227,13 @@ hipError_t launch_skinny(const GemmA& ga, const T* W, int M, int N, int K, const
   return hipGetLastError();
 }
 
-template <typename T, int BM, int BN, int WM, int WN, int S, int MODE, bool NORM, class Ep>
+template <typename T, int BM, int BN, int WM, int WN, int S, int MODE, bool NORM, int KG = 1,
+          class Ep>
 hipError_t launch_tile(const GemmA& ga, const T* W, int ldw, int M, int N, int K, const Ep& ep,
                        hipStream_t s, int ksplit = 1) {
   const int tiles = ((N + BN - 1) / BN) * ((M + BM - 1) / BM);
-  launch((gemm_kernel<T, BM, BN, WM, WN, S, MODE, NORM, Ep>), dim3(tiles * ksplit),
-                     dim3(64 * WM * WN), 0, s, ga, W, ldw, M, N, K, ep, ksplit);
+  launch((gemm_kernel<T, BM, BN, WM, WN, S, MODE, NORM, Ep, KG>), dim3(tiles * ksplit),
+                     dim3(64 * WM * WN * KG), 0, s, ga, W, ldw, M, N, K, ep, ksplit);
   return hipGetLastError();
 }
 
@@ -1259,27 +1298,51 @@ hipError_t launch_splitk_reduce(const float* part, int splits, int M, int N, con
 // reduced.  Short-K grids do not split: on the OWT-shaped model the
 // out-projection (K = 768) at batch 8 and 16 took 15 instead of 22.5 ms per
 // generate without its split and reduction kernel (whole generate +2.5 %).
+// Plain GEMM grids of this many tiles take two K groups per workgroup: from
+// half a workgroup per CU (smaller grids measured slower: OWT-shaped batch 16
+// -3.8 %) to one.
+constexpr int kTwoGroupMin = 128, kTwoGroupMax = 256;
+
+template <typename T, int BM, int BN, int WM, int WN, int S, int KG, class Ep>
+hipError_t launch_tile_kg(int kg, const GemmA& ga, const T* W, int M, int N, int K, const Ep& ep,
+                          hipStream_t s, int ksplit) {
+  if constexpr (KG == 2) {
+    if (kg == 2) return launch_tile<T, BM, BN, WM, WN, S, 0, false, 2>(ga, W, K, M, N, K, ep, s, ksplit);
+  }
+  return launch_tile<T, BM, BN, WM, WN, S, 0, false>(ga, W, K, M, N, K, ep, s, ksplit);
+}
+
 template <typename T, int BM, int BN, int WM, int WN, int S, class Ep>
 hipError_t launch_plain(const GemmA& ga, const T* W, int M, int N, int K, const Ep& ep,
                         hipStream_t s, const SplitWs* ws) {
   const int tiles = ((N + BN - 1) / BN) * ((M + BM - 1) / BM);
   constexpr int BK = KCH * 16 / (int)sizeof(T);
   const int nk = K / BK;
+  // A grid of one half to one workgroup per CU runs two K groups per
+  // workgroup (eight wavefronts, each group half the K steps with its own
+  // ring, the halves summed in LDS) when both rings fit the CU's LDS.
+  // (The tiles of up to 64 x 64 only: the larger ones run on grids of 256
+  // workgroups or more.)
+  constexpr bool kFit2 = BM * BN <= 64 * 64 && 2 * S * (BM + BN) * KCH * 16 <= 160 * 1024;
+  const int kg = kFit2 && tiles >= kTwoGroupMin && tiles <= kTwoGroupMax && nk % 2 == 0 && nk >= 8 ? 2 : 1;
+  const int nkg = nk / kg;
   int ks = 1;
   // Long-K grids of up to one workgroup per CU split too (in two): at
   // M = 512, K = 3072 that measured 8 % faster, reduction included.
-  if (ws && ws->part && tiles < 256 && nk >= 24) {
+  if (ws && ws->part && tiles < 256 && nkg >= 24) {
+    const int cap = kg == 2 ? (tiles < 128 ? 160 : tiles) : (tiles < 128 ? 320 : 2 * tiles);
     for (int c : {16, 12, 8, 6, 4, 3, 2}) {
-      if (nk % c == 0 && nk / c >= 2 && tiles * c <= (tiles < 128 ? 320 : 2 * tiles) &&
+      if (nkg % c == 0 && nkg / c >= 2 && tiles * c <= cap &&
           (size_t)c * M * N * sizeof(float) <= ws->bytes) {
         ks = c;
         break;
       }
     }
   }
-  if (ks == 1) return launch_tile<T, BM, BN, WM, WN, S, 0, false>(ga, W, K, M, N, K, ep, s);
+  constexpr int KGI = kFit2 ? 2 : 1;
+  if (ks == 1) return launch_tile_kg<T, BM, BN, WM, WN, S, KGI>(kg, ga, W, M, N, K, ep, s, 1);
   const EpPartial pe{ws->part, N, nullptr};
-  hipError_t e = launch_tile<T, BM, BN, WM, WN, S, 0, false>(ga, W, K, M, N, K, pe, s, ks);
+  hipError_t e = launch_tile_kg<T, BM, BN, WM, WN, S, KGI>(kg, ga, W, M, N, K, pe, s, ks);
   if (e != hipSuccess) return e;
   return launch_splitk_reduce(ws->part, ks, M, N, ep, s);
 }
