@@ -294,7 +294,9 @@ def _short(name: str) -> str:
         t = re.findall(r"Li(\d+)E", m.group(2))
         ep = re.search(r"NS0_\d+(Ep\w+?)I|NS0_\d+(Ep\w+?)E", m.group(2))
         epn = (ep.group(1) or ep.group(2)) if ep else "?"
-        return f"gemm {'x'.join(t[:2])} {epn}" + (" bf16" if "DF16b" in n else " f32")
+        kg = re.search(r"ELi([24])EEEvNS0_5GemmA", n)  # K groups per workgroup
+        groups = f" {kg.group(1)}g" if kg else ""
+        return f"gemm {'x'.join(t[:2])}{groups} {epn}" + (" bf16" if "DF16b" in n else " f32")
     if m and "gemm_skinny_kernel" in m.group(1):
         t = re.findall(r"Li(\d+)E", m.group(2))
         ep = re.search(r"NS0_\d+(Ep\w+?)I|NS0_\d+(Ep\w+?)E", m.group(2))

@@ -1299,8 +1299,8 @@ hipError_t launch_splitk_reduce(const float* part, int splits, int M, int N, con
 // out-projection (K = 768) at batch 8 and 16 took 15 instead of 22.5 ms per
 // generate without its split and reduction kernel (whole generate +2.5 %).
 // Plain GEMM grids of this many tiles take two K groups per workgroup: from
-// half a workgroup per CU (smaller grids measured slower: OWT-shaped batch 16
-// -3.8 %) to one.
+// half a workgroup per CU to one.  Smaller grids measured mixed (OWT-shaped
+// batch 4 +2.6 %, batch 8 +0.4 %, batch 16 -1.2 %).
 constexpr int kTwoGroupMin = 128, kTwoGroupMax = 256;
 
 template <typename T, int BM, int BN, int WM, int WN, int S, int KG, class Ep>
