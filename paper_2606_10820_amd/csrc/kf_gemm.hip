@@ -584,7 +584,7 @@ __global__ void __launch_bounds__(64 * WM * WN * KG)
   static_assert(S >= 2 && S <= 8, "ring depth");
   static_assert((S - 1) * PER < 64, "vmcnt range");
   static_assert(KG == 1 || KG == 2, "one or two K groups");
-  static_assert(KG == 1 || (!NORM && !IsHead<Ep>::value), "K groups: plain epilogues only");
+  static_assert(KG == 1 || !IsHead<Ep>::value, "K groups: not with the head epilogues");
 
   __shared__ u32x4 sbuf[KG][S][(BM + BN) * KCH];
   __shared__ float2 sStat[NORM ? BM : 1];
@@ -1377,6 +1377,15 @@ hipError_t dispatch(const GemmA& ga, const T* W, int M, int N, int K, const Ep& 
       return launch_tile<T, 128, 128, 2, 4, 2, MODE, NORM>(ga, W, K, M, N, K, ep, s);
     if (cdiv(M, 64) * cdiv(N, 128) >= kFill)
       return launch_tile<T, 64, 128, 2, 4, 3, MODE, NORM>(ga, W, K, M, N, K, ep, s);
+    {
+      // three quarters of a workgroup per CU or more in 64 x 96 tiles: two K
+      // groups of four wavefronts (both rings: 120 KB of LDS).  At M = 512
+      // (QKV 192 tiles, MLP-up 256) +1.2 % on the LM1B-shaped generate; with
+      // 128 tiles (MLP-up at M = 256) -2.8 % on the OWT-shaped batch 32.
+      const int t96 = cdiv(M, 64) * cdiv(N, 96), nk = K / (KCH * 16 / (int)sizeof(T));
+      if (N % 96 == 0 && t96 >= 192 && t96 <= kTwoGroupMax && nk % 2 == 0 && nk >= 8)
+        return launch_tile<T, 64, 96, 2, 2, 3, MODE, NORM, 2>(ga, W, K, M, N, K, ep, s);
+    }
     if (cdiv(M, 64) * cdiv(N, 64) >= kFill * 3 / 4)
       return launch_tile<T, 64, 64, 2, 2, 3, MODE, NORM>(ga, W, K, M, N, K, ep, s);
     if (cdiv(M, 32) * cdiv(N, 64) >= kFill * 3 / 4)
