@@ -340,7 +340,7 @@ def kernel_class(name: str, state: dict):
     a split-K part belongs to the reduction that follows it."""
     if "embed_real_kernel" in name:
         return "embed"
-    if "noise_sinusoid_kernel" in name or "EpNoiseOut" in name:
+    if "noise_sinusoid" in name or "EpNoiseOut" in name:
         return "noise"
     if "attention_mfma_kernel" in name or "attention_combine_kernel" in name:
         return "attn"
@@ -362,6 +362,46 @@ def kernel_class(name: str, state: dict):
     return None
 
 
+def class_times(path: str) -> None:
+    """Kernel time per class launch from a kernel trace, in dispatch order
+    (kernel_class): out-projection and MLP-down share one GEMM instantiation
+    and alternate; a split-K part is counted with the reduction that follows
+    it (a part with no reduction after it is the noise encoder's fp32 output
+    GEMM); an attention combine with the attention before it."""
+    import csv
+    rows = sorted(csv.DictReader(open(path)), key=lambda r: int(r["Dispatch_Id"]))
+    state, pending, cls = {}, 0.0, {}
+    for r in rows:
+        name = r["Kernel_Name"]
+        us = (float(r["End_Timestamp"]) - float(r["Start_Timestamp"])) / 1e3
+        c = kernel_class(name, state)
+        if pending and "splitk_reduce" not in name:  # a part with no reduction
+            e = cls.setdefault("noise", [0, 0.0])
+            e[0] += 1
+            e[1] += pending
+            pending = 0.0
+        if c == "pending":
+            pending = us
+            continue
+        if c is None:
+            continue
+        e = cls.setdefault(c, [0, 0.0])
+        helper = "attention_combine" in name or "splitk_reduce" in name
+        if not helper or pending:
+            e[0] += 1
+        e[1] += us + pending
+        pending = 0.0
+    if not cls:
+        return
+    tot = sum(v[1] for v in cls.values())
+    print(f"### kernel time per class launch ({os.path.basename(path)}; split-K parts and "
+          "reductions, attention and its combine counted together)\n")
+    print("| class | launches | avg us per launch | share |\n|---|---|---|---|")
+    for c, (n, t) in sorted(cls.items(), key=lambda kv: -kv[1][1]):
+        print(f"| {c} | {n} | {t / max(n, 1):.2f} | {t / tot * 100:.1f}% |")
+    print()
+
+
 def summarize(root: str, write_json: str = None) -> None:
     """Markdown summary of rocprofv3 --stats / --pmc CSV output (no GPU needed),
     with HBM traffic per kernel class; write_json stores the per-launch class
@@ -378,6 +418,8 @@ def summarize(root: str, write_json: str = None) -> None:
             print(f"| {_short(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
                   f"{float(r['MinNs']) / 1e3:.2f} | {float(r['TotalDurationNs']) / tot * 100:.1f}% |")
         print()
+    for path in glob.glob(os.path.join(root, "**", "*_kernel_trace.csv"), recursive=True):
+        class_times(path)
     pmc, seq = {}, {}
     for path in glob.glob(os.path.join(root, "**", "*_counter_collection.csv"), recursive=True):
         for r in csv.DictReader(open(path)):
