@@ -130,6 +130,18 @@ def test_lm1b_fp32_tokens():
     report("lm1b fp32 B=4, prefill + 1 block", st)
 
 
+def test_lm1b_fp32_batch64():
+    """fp32 at the benchmark's batch: the decode step (M = 512) runs the GEMMs
+    with two K groups per workgroup (out-projection and MLP-down in 32x64
+    tiles, QKV and MLP-up in 64x96 tiles with the folded LayerNorm) in fp32,
+    where any slip in the group merge shows far above the 1e-4 tolerance."""
+    B, N, k = 64, 16, 4
+    kf = _ctx(LM1B_F32, B, k, N)
+    prompt = S.prompts_zipf(3, B, N, LM1B_F32.vocab)
+    st = _blocks(kf, _model(LM1B_F32), prompt, [k, k, k], seed=4, tol=TOL[0], rows=[0, B - 1])
+    report("lm1b fp32 B=64, prefill + 2 blocks", st)
+
+
 @pytest.mark.parametrize("B", [64, 13, 1])
 def test_lm1b_bf16_ar_baseline(B):
     """AR baseline at the LM1B shape: logits within 2e-2 of the oracle.  At 13
