@@ -721,18 +721,12 @@ void drop_serve_graphs(kf_ctx* c) {
   c->sgraphs.clear();
 }
 
-// Run `count` identical steps and advance the host view of C by `adv` after
-// each.  Every launch of such a step reads C from device memory, so one
-// captured step replays unchanged; the instantiated graph is cached on the
-// context for the next call with the same arguments.  Graphs need a real
-// stream (capture is impossible on the legacy null stream) and are not used
-// while kernel timing is on.
 // The noise encoder for passes pass0 .. pass0 + npass - 1 of a lock-step
 // generate of B sequences (prompt N, k noise rows a pass), into the plan's
 // ahead buffers: sinusoids, Linear(d, 4d) + GELU, Linear(4d, d) in fp32
 // without its bias (the embedding kernel adds the bias, the position and the
-// temperature embedding when the pass runs).  One launch per layer for the
-// whole chunk instead of three or four per pass.
+// temperature embedding when the pass runs).  Three launches for the whole
+// chunk instead of three in every pass.
 template <typename T>
 int run_noise_ahead(kf_ctx* c, int B, int k, int N, uint64_t seed, int pass0, int npass) {
   const Plan& p = c->plan;
@@ -758,6 +752,12 @@ int noise_ahead(kf_ctx* c, int B, int k, int N, uint64_t seed, int pass0, int np
                                  : run_noise_ahead<float>(c, B, k, N, seed, pass0, npass);
 }
 
+// Run `count` identical steps and advance the host view of C by `adv` after
+// each.  Every launch of such a step reads C from device memory, so one
+// captured step replays unchanged; the instantiated graph is cached on the
+// context for the next call with the same arguments.  Graphs need a real
+// stream (capture is impossible on the legacy null stream) and are not used
+// while kernel timing is on.
 // before(i) runs on the host before decode pass i = 1 .. count is issued
 // (between graph replays: it may launch work of its own on the stream).
 int repeat_step(kf_ctx* c, const StepIn& in, int count, int adv, int N, int L,
