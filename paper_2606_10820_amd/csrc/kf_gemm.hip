@@ -1302,8 +1302,10 @@ hipError_t launch_splitk_reduce(const float* part, int splits, int M, int N, con
 // out-projection (K = 768) at batch 8 and 16 took 15 instead of 22.5 ms per
 // generate without its split and reduction kernel (whole generate +2.5 %).
 // Plain GEMM grids of this many tiles take two K groups per workgroup: from
-// half a workgroup per CU to one.  Smaller grids measured mixed (OWT-shaped
-// batch 4 +2.6 %, batch 8 +0.4 %, batch 16 -1.2 %).
+// half a workgroup per CU to one.  Smaller grids take them only when K is too
+// short for a split across workgroups (the K = 768 out-projection at
+// OWT-shaped batch 4 to 32: +1.0 %, +0.8 %, +0.3 %, 0 %); with the long-K
+// MLP-down as well they measured mixed (batch 4 +2.6 %, batch 16 -1.2 %).
 constexpr int kTwoGroupMin = 128, kTwoGroupMax = 256;
 
 template <typename T, int BM, int BN, int WM, int WN, int S, int KG, class Ep>
@@ -1321,13 +1323,15 @@ hipError_t launch_plain(const GemmA& ga, const T* W, int M, int N, int K, const 
   const int tiles = ((N + BN - 1) / BN) * ((M + BM - 1) / BM);
   constexpr int BK = KCH * 16 / (int)sizeof(T);
   const int nk = K / BK;
-  // A grid of one half to one workgroup per CU runs two K groups per
-  // workgroup (eight wavefronts, each group half the K steps with its own
-  // ring, the halves summed in LDS) when both rings fit the CU's LDS.
+  // A grid of one half to one workgroup per CU, or a smaller one whose K is
+  // too short to split across workgroups, runs two K groups per workgroup
+  // (eight wavefronts, each group half the K steps with its own ring, the
+  // halves summed in LDS) when both rings fit the CU's LDS.
   // (The tiles of up to 64 x 64 only: the larger ones run on grids of 256
   // workgroups or more.)
   constexpr bool kFit2 = BM * BN <= 64 * 64 && 2 * S * (BM + BN) * KCH * 16 <= 160 * 1024;
-  const int kg = kFit2 && tiles >= kTwoGroupMin && tiles <= kTwoGroupMax && nk % 2 == 0 && nk >= 8 ? 2 : 1;
+  const bool grid2 = tiles >= kTwoGroupMin ? tiles <= kTwoGroupMax : nk < 24;
+  const int kg = kFit2 && grid2 && nk % 2 == 0 && nk >= 8 ? 2 : 1;
   const int nkg = nk / kg;
   int ks = 1;
   // Long-K grids of up to one workgroup per CU split too (in two): at
