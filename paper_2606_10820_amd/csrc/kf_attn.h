@@ -222,7 +222,7 @@ __device__ __forceinline__ void attention_block(const bf16* __restrict__ Q, cons
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int gq = lane >> 4, lq = lane & 15;
   const int C = g.ctx(st, b);
-  const int q0 = qb * QB, nq = min(QB, g.R - q0);
+  const int q0 = g.qoff + qb * QB, nq = min(QB, g.R - q0);
   const int nkeys = C + q0 + nq;
   const int chunk = ((nkeys + sp.ns - 1) / sp.ns + KT - 1) / KT * KT;
   const int ks = split * chunk, ke = min(nkeys, ks + chunk);

@@ -154,15 +154,25 @@ struct EpBias {
 // Residual update X += C + bias.  With a 16-bit compute dtype the updated row
 // is also written to Xh, the compute-dtype copy of the residual stream that the
 // LayerNorm-folded GEMMs read (for fp32, Xh is X itself).
-template <typename T>
+template <typename T, bool ROWS = false>
 struct EpResidual {
   float* X;
   T* Xh;
   int ldx;
   const float* bias;
   float2* lnst;
+  // With ROWS the GEMM covers rk rows per sequence out of rR: GEMM row m is
+  // stream row (m / rk) rR + rnr + m % rk (the head rows of a step).
+  int rk = 0, rR = 0, rnr = 0;
   static constexpr bool kStats = true;
-  __device__ inline int srow(int m) const { return m; }
+  __device__ inline int srow(int m) const {
+    if constexpr (ROWS) {
+      const int b = div_u(m, rk);
+      return b * rR + rnr + (m - b * rk);
+    } else {
+      return m;
+    }
+  }
   __device__ inline int cols() const { return ldx; }
   __device__ inline void store8(int m, int n, float (&v)[8]) const {
     float x[8];
@@ -170,18 +180,21 @@ struct EpResidual {
     store8_pre(m, n, v, x);
   }
   // The same in two halves, for kernels that load the old values early.
-  __device__ inline void pre8(int m, int n, float (&x)[8]) const { get8(X + (size_t)m * ldx + n, x); }
+  __device__ inline void pre8(int m, int n, float (&x)[8]) const {
+    get8(X + (size_t)srow(m) * ldx + n, x);
+  }
   __device__ inline void store8_pre(int m, int n, float (&v)[8], const float (&x)[8]) const {
 #pragma unroll
     for (int i = 0; i < 8; ++i) v[i] += x[i];
-    put8(X + (size_t)m * ldx + n, v);
-    if constexpr (sizeof(T) == 2) put8(Xh + (size_t)m * ldx + n, v);
+    const size_t r = (size_t)srow(m);
+    put8(X + r * ldx + n, v);
+    if constexpr (sizeof(T) == 2) put8(Xh + r * ldx + n, v);
   }
 };
 template <class Ep>
 struct HasPre : std::false_type {};
-template <typename T>
-struct HasPre<EpResidual<T>> : std::true_type {};
+template <typename T, bool ROWS>
+struct HasPre<EpResidual<T, ROWS>> : std::true_type {};
 
 // QKV projection: q goes to Q [M][d]; k and v of row (b, i) go straight into
 // cache slot C_b + i of sequence b (the KV append of the step), in the page
@@ -1472,6 +1485,18 @@ hipError_t gemm_residual(const T* A, const T* W, int M, int N, int K, const floa
 }
 
 template <typename T>
+hipError_t gemm_residual_rows(const T* A, bool a_rows, KfStepGeom g, const T* W, int M, int N,
+                              int K, const float* bias, float* X, T* Xh, float2* lnst,
+                              const SplitWs* ws, hipStream_t s) {
+  EpResidual<T, true> ep{X, Xh, N, bias, lnst, g.k, g.R, g.nr};
+  if (a_rows)  // A holds every row of the step; GEMM row m reads the same row as it writes
+    return dispatch<T, 1, false>(GemmA{A, K, g.B * g.R, nullptr, nullptr, nullptr, g}, W, M, N, K,
+                                 ep, s, ws);
+  return dispatch<T, 0, false>(GemmA{A, K, M, nullptr, nullptr, nullptr, KfStepGeom{}}, W, M, N, K,
+                               ep, s, ws);
+}
+
+template <typename T>
 hipError_t gemm_noise_out(const T* A, const T* W, int M, int d, int K, const float* bias,
                           const T* pos, const T* temb, float* X, T* Xh, float2* lnst,
                           KfStepGeom g, const KfDevState* st, const SplitWs* ws, hipStream_t s) {
@@ -1494,6 +1519,14 @@ hipError_t gemm_up_ln(const T* Xh, const LnFold& ln, const T* W, int M, int N, i
   EpBias<T> ep{out, N, bias, 1};
   return dispatch<T, 0, true>(GemmA{Xh, d, M, ln.c1, ln.c2, ln.lnst, KfStepGeom{}, ln.rms}, W, M, N, d, ep,
                               s);
+}
+
+template <typename T>
+hipError_t gemm_up_ln_rows(const T* Xh, const LnFold& ln, KfStepGeom g, const T* W, int M, int N,
+                           int d, const float* bias, T* out, hipStream_t s) {
+  EpBias<T> ep{out, N, bias, 1};
+  return dispatch<T, 1, true>(GemmA{Xh, d, g.B * g.R, ln.c1, ln.c2, ln.lnst, g, ln.rms}, W, M, N, d,
+                              ep, s);
 }
 
 template <typename T>
@@ -1573,6 +1606,11 @@ hipError_t launch_ln_fold(const T* W, T* Wout, const float* g, const float* beta
                                      const float2*, hipStream_t);                                  \
   template hipError_t gemm_up_ln<T>(const T*, const LnFold&, const T*, int, int, int,             \
                                     const float*, T*, hipStream_t);                                \
+  template hipError_t gemm_up_ln_rows<T>(const T*, const LnFold&, KfStepGeom, const T*, int, int,  \
+                                         int, const float*, T*, hipStream_t);                      \
+  template hipError_t gemm_residual_rows<T>(const T*, bool, KfStepGeom, const T*, int, int, int,   \
+                                            const float*, float*, T*, float2*, const SplitWs*,     \
+                                            hipStream_t);                                          \
   template hipError_t gemm_head_ln<T>(const T*, const LnFold&, const T*, int, int, int, int, int, \
                                       KfStepGeom, float*, int*, float*, hipStream_t);              \
   template hipError_t gemm_qkv_seq<T>(const T*, const LnFold&, const T*, int, int, const float*,  \

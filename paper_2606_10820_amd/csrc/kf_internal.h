@@ -81,6 +81,7 @@ struct KfStepGeom {
   int B, R, nr, k;
   const int* map = nullptr;  // [B] sequence slots of the step, or null
   int* cs = nullptr;         // [slots] committed lengths (with map), or null
+  int qoff = 0;              // first row of each sequence the attention computes
   __device__ inline int slot(int b) const { return map ? map[b] : b; }
   __device__ inline int ctx(const KfDevState* st, int b) const { return map ? cs[map[b]] : st->C; }
 };
@@ -246,11 +247,21 @@ hipError_t gemm_f32(const T* A, const T* W, int M, int N, int K, float* out, hip
 // Residual update X[M][N] += C + bias; with a 16-bit T the updated rows are
 // also written to Xh (the compute-dtype copy of the residual stream; for fp32,
 // Xh aliases X and is not written).  Every writer of the residual stream also
-// writes lnst [rows][N / 16]: (sum x, sum x^2) over each 16 columns of the
-// updated row, the input of the next folded LayerNorm.
+// writes lnst [rows][N / 16]: per 16 columns of the updated row, the sum and
+// the sum of squared deviations from their mean, the input of the next folded
+// LayerNorm.
 template <typename T>
 hipError_t gemm_residual(const T* A, const T* W, int M, int N, int K, const float* bias, float* X,
                          T* Xh, float2* lnst, const SplitWs* ws, hipStream_t s);
+// The same for the head rows of a step only (the last layer of a step with
+// noise rows, whose real rows feed nothing after their K/V append): M = B k
+// GEMM rows, row m updating stream row (m / k) R + nr + m % k of g.  With
+// a_rows, A holds every row of the step and GEMM row m reads that same row
+// (the attention output); otherwise A has the M rows (the MLP hidden layer).
+template <typename T>
+hipError_t gemm_residual_rows(const T* A, bool a_rows, KfStepGeom g, const T* W, int M, int N,
+                              int K, const float* bias, float* X, T* Xh, float2* lnst,
+                              const SplitWs* ws, hipStream_t s);
 // LayerNorm folded into a GEMM whose weights were scaled by the gain at load
 // (W' = W diag(gain)): c1 = W' 1 and c2 = W shift.  A rows come from the
 // compute-dtype residual copy Xh [rows][d]; each row's mean and variance come
@@ -270,6 +281,11 @@ hipError_t gemm_qkv_ln(const T* Xh, const LnFold& ln, const T* W, int M, int d, 
 template <typename T>
 hipError_t gemm_up_ln(const T* Xh, const LnFold& ln, const T* W, int M, int N, int d,
                       const float* bias, T* out, hipStream_t s);
+// MLP-up of the head rows of a step only (see gemm_residual_rows): A row m is
+// stream row (m / k) R + nr + m % k, the M = B k output rows are contiguous.
+template <typename T>
+hipError_t gemm_up_ln_rows(const T* Xh, const LnFold& ln, KfStepGeom g, const T* W, int M, int N,
+                           int d, const float* bias, T* out, hipStream_t s);
 template <typename T>
 hipError_t gemm_noise_out(const T* A, const T* W, int M, int d, int K, const float* bias,
                           const T* pos, const T* temb, float* X, T* Xh, float2* lnst,

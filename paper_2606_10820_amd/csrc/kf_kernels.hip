@@ -147,7 +147,7 @@ __global__ void __launch_bounds__(256)
   constexpr int QB = 16, KT = 64, EPT = DH / 16;
   const int H = kg.H, d = H * DH;
   const int b = blockIdx.x / H, h = blockIdx.x % H;
-  const int q0 = blockIdx.y * QB;
+  const int q0 = g.qoff + blockIdx.y * QB;
   const int nq = min(QB, g.R - q0);
   const int C = g.ctx(st, b), seq = g.slot(b);
   const int nkeys = C + q0 + nq;
@@ -244,7 +244,7 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH
     attention_mfma_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ kv,
                           bf16* __restrict__ O, const KfDevState* st, KfStepGeom g, KfKvGeom kg,
                           int layer, float scale, AttnSplit sp) {
-  const int nqb = (g.R + 15) / 16;
+  const int nqb = (g.R - g.qoff + 15) / 16;
   const int split = blockIdx.x % sp.ns, rest = blockIdx.x / sp.ns;
   const int qb = rest % nqb, bh = rest / nqb;
   attention_block<DH, NW, PT>(Q, kv, O, st, g, kg, layer, scale, sp, bh / kg.H, bh % kg.H, qb,
@@ -275,8 +275,9 @@ template <int DH>
 __global__ void __launch_bounds__(DH)
     attention_combine_kernel(bf16* __restrict__ O, KfStepGeom g, int H, AttnSplit sp) {
   constexpr int NSMAX = 16;
-  const int h = blockIdx.x % H, row = blockIdx.x / H;
-  const int b = row / g.R, i = row - b * g.R, e = threadIdx.x;
+  const int h = blockIdx.x % H, rq = blockIdx.x / H, nqr = g.R - g.qoff;
+  const int b = rq / nqr, i = g.qoff + (rq - b * nqr), e = threadIdx.x;
+  const int row = b * g.R + i;
   const size_t base = (((size_t)b * H + h) * g.R + i) * sp.ns;
   float ms[NSMAX], ls[NSMAX], os[NSMAX];
 #pragma unroll
@@ -738,12 +739,12 @@ constexpr int kWideMin = 64;
 template <typename T>
 hipError_t launch_attention(const T* Q, const T* kv, T* O, const KfDevState* st, KfStepGeom g,
                             KfKvGeom kg, int layer, const AttnSplit& ws, hipStream_t s) {
-  if (g.B <= 0 || g.R <= 0) return hipSuccess;
+  if (g.B <= 0 || g.R - g.qoff <= 0) return hipSuccess;
   const float scale = 1.0f / sqrtf((float)kg.dh);
   if constexpr (sizeof(T) == 2) {
     // key splits: enough workgroups for ~512 in flight, each split at least
     // 128 keys of the full context, within the partial-state workspace
-    const int base = g.B * kg.H * ((g.R + 15) / 16);
+    const int base = g.B * kg.H * ((g.R - g.qoff + 15) / 16);
     int ns = 1;
     if (ws.o && base < 256) {
       ns = 512 / base;
@@ -759,7 +760,7 @@ hipError_t launch_attention(const T* Q, const T* kv, T* O, const KfDevState* st,
       case 32:
         launch_attention_mfma<32, 4>(grid, s, Q, kv, O, st, g, kg, layer, scale, sp);
         if (ns > 1)
-          launch(attention_combine_kernel<32>, dim3(g.B * g.R * kg.H), dim3(32), 0, s,
+          launch(attention_combine_kernel<32>, dim3(g.B * (g.R - g.qoff) * kg.H), dim3(32), 0, s,
                              O, g, kg.H, sp);
         break;
       case 64:
@@ -771,13 +772,13 @@ hipError_t launch_attention(const T* Q, const T* kv, T* O, const KfDevState* st,
         }
         launch_attention_mfma<64, 4>(grid, s, Q, kv, O, st, g, kg, layer, scale, sp);
         if (ns > 1)
-          launch(attention_combine_kernel<64>, dim3(g.B * g.R * kg.H), dim3(64), 0, s,
+          launch(attention_combine_kernel<64>, dim3(g.B * (g.R - g.qoff) * kg.H), dim3(64), 0, s,
                              O, g, kg.H, sp);
         break;
       case 128:
         launch_attention_mfma<128, 4>(grid, s, Q, kv, O, st, g, kg, layer, scale, sp);
         if (ns > 1)
-          launch(attention_combine_kernel<128>, dim3(g.B * g.R * kg.H), dim3(128), 0, s,
+          launch(attention_combine_kernel<128>, dim3(g.B * (g.R - g.qoff) * kg.H), dim3(128), 0, s,
                              O, g, kg.H, sp);
         break;
       default:
@@ -785,7 +786,7 @@ hipError_t launch_attention(const T* Q, const T* kv, T* O, const KfDevState* st,
     }
     return hipGetLastError();
   }
-  dim3 grid(g.B * kg.H, (g.R + 15) / 16);
+  dim3 grid(g.B * kg.H, (g.R - g.qoff + 15) / 16);
   switch (kg.dh) {
     case 32:
       launch((attention_kernel<T, 32>), grid, dim3(256), 0, s, Q, kv, O, st, g, kg,
