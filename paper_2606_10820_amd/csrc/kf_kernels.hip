@@ -770,6 +770,13 @@ hipError_t launch_attention(const T* Q, const T* kv, T* O, const KfDevState* st,
           ns = 1;
           break;
         }
+        if (ns == 1 && kg.T <= 128) {
+          // contexts of at most 4 key tiles: two wavefronts, so that each
+          // takes two tiles and its next-tile loads overlap its first tile
+          // (LM1B-shaped batch 64: +0.6 %; one wavefront +0.1 %)
+          launch_attention_mfma<64, 2>(grid, s, Q, kv, O, st, g, kg, layer, scale, sp);
+          break;
+        }
         launch_attention_mfma<64, 4>(grid, s, Q, kv, O, st, g, kg, layer, scale, sp);
         if (ns > 1)
           launch(attention_combine_kernel<64>, dim3(g.B * (g.R - g.qoff) * kg.H), dim3(64), 0, s,
