@@ -550,16 +550,19 @@ int run_step(kf_ctx* c, const StepIn& in) {
   const int Mh = ar ? in.B : in.B * in.k;
   float* logits = (ar || debug) ? reinterpret_cast<float*>(base + p.logits) : nullptr;
   const kf::LnFold lnf{F(p.head_c1), F(p.head_c2), lnst, rms};
+  // The argmax head commits the step itself (its first workgroup, C += nr),
+  // which saves the commit launch; the AR path commits after its sampler.
   KF_LAUNCH(c, KF_KC_HEAD,
             kf::gemm_head_ln<T>(Xh, lnf, W(p.head_w), Mh, p.Vpad, V, d, ar ? 2 : 1, g, pval, pidx,
-                                logits, s));
-  if (!ar)
+                                logits, s, ar ? nullptr : st, in.nr));
+  if (!ar) {
     KF_LAUNCH(c, KF_KC_SELECT,
-              kf::launch_argmax_select(pval, pidx, p.n_tiles, g, st, in.od, s));
-  else
+              kf::launch_argmax_select(pval, pidx, p.n_tiles, g, st, in.od, s, in.nr));
+  } else {
     KF_LAUNCH(c, KF_KC_SELECT,
               kf::launch_icdf_select(logits, V, in.u_ar, in.seed, g, st, in.od, s));
-  KF_LAUNCH(c, KF_KC_SELECT, kf::launch_commit(st, g, in.nr, s));
+    KF_LAUNCH(c, KF_KC_SELECT, kf::launch_commit(st, g, in.nr, s));
+  }
   c->last_head_rows = Mh;
   c->last_logits = logits != nullptr;
   return KF_OK;

@@ -475,6 +475,13 @@ struct EpHead {
   float* logits;
   int V;
   int n_tiles;
+  // With st: the step's commit (C += nr, or per slot with a slot map) is done
+  // by the first workgroup at its end.  No kernel of the step reads C after
+  // the layers but the selection, which then takes C - nr; the commit saves
+  // a launch per step.
+  KfDevState* st = nullptr;
+  KfStepGeom cg{};
+  int cnr = 0;
 };
 
 // Head of a temperature-scaled sampling pass over every row (teacher
@@ -1049,6 +1056,13 @@ __global__ void __launch_bounds__(64 * WM * WN * KG)
         ep.pidx[(size_t)m * ep.n_tiles + nt] = bi;
       }
     }
+    if (ep.st && blockIdx.x == 0) {
+      if (ep.cg.map) {
+        for (int b = tid; b < ep.cg.B; b += NT) ep.cg.cs[ep.cg.map[b]] += ep.cnr;
+      } else if (tid == 0) {
+        ep.st->C += ep.cnr;
+      }
+    }
   }
 }
 
@@ -1532,9 +1546,9 @@ hipError_t gemm_up_ln_rows(const T* Xh, const LnFold& ln, KfStepGeom g, const T*
 template <typename T>
 hipError_t gemm_head_ln(const T* Xh, const LnFold& ln, const T* W, int M, int Vpad, int V, int d,
                         int gather, KfStepGeom g, float* pval, int* pidx, float* logits,
-                        hipStream_t s) {
+                        hipStream_t s, KfDevState* commit_st, int commit_nr) {
   if (M <= 0) return hipSuccess;
-  EpHead ep{nullptr, pval, pidx, logits, V, Vpad / kHeadTileN};
+  EpHead ep{nullptr, pval, pidx, logits, V, Vpad / kHeadTileN, commit_st, g, commit_nr};
   const GemmA ga{Xh, d, g.B * g.R, ln.c1, ln.c2, ln.lnst, g, ln.rms};
   auto go = [&](auto mode) {
     constexpr int MODE = decltype(mode)::value;
@@ -1612,7 +1626,8 @@ hipError_t launch_ln_fold(const T* W, T* Wout, const float* g, const float* beta
                                             const float*, float*, T*, float2*, const SplitWs*,     \
                                             hipStream_t);                                          \
   template hipError_t gemm_head_ln<T>(const T*, const LnFold&, const T*, int, int, int, int, int, \
-                                      KfStepGeom, float*, int*, float*, hipStream_t);              \
+                                      KfStepGeom, float*, int*, float*, hipStream_t, KfDevState*,  \
+                                      int);                                                        \
   template hipError_t gemm_qkv_seq<T>(const T*, const LnFold&, const T*, int, int, const float*,  \
                                       T*, T*, T*, int, int, int, int, int, int, int,               \
                                       const float2*, hipStream_t);                                 \

@@ -294,11 +294,14 @@ hipError_t gemm_noise_out(const T* A, const T* W, int M, int d, int K, const flo
 // of the step, 2 = last real row per sequence): per (row, 128-column tile) the
 // maximum and its lowest column index into pval/pidx [M][Vpad/128]; columns
 // >= V are excluded.  When logits is not null the fp32 logits [M][V] are
-// written as well.  W is the gain-scaled token table [Vpad][d].
+// written as well.  W is the gain-scaled token table [Vpad][d].  With
+// commit_st, the head also commits the step (C += commit_nr, or per slot
+// through g's slot map) once its first workgroup is done: nothing after the
+// layers reads C but the selection, which is then told commit_nr.
 template <typename T>
 hipError_t gemm_head_ln(const T* Xh, const LnFold& ln, const T* W, int M, int Vpad, int V, int d,
                         int gather, KfStepGeom g, float* pval, int* pidx, float* logits,
-                        hipStream_t s);
+                        hipStream_t s, KfDevState* commit_st = nullptr, int commit_nr = 0);
 // Head of a temperature-scaled sampling pass (teacher targets) over rows
 // row0 .. row0 + M - 1 of the step (all rows are real rows; row r belongs to
 // sequence r / rows_per_seq, temperature tau[r / rows_per_seq]): per launch
@@ -353,9 +356,11 @@ hipError_t launch_ln_fold(const T* W, T* Wout, const float* gain, const float* s
 constexpr int kHeadTileN = 128;
 
 // Argmax over the head partials of each row, ties to the lowest id; writes the
-// selected tokens per KfOutDesc.  rows = B * k.
+// selected tokens per KfOutDesc.  rows = B * k.  committed: what the head has
+// already added to C (the context length of the step is C - committed).
 hipError_t launch_argmax_select(const float* pval, const int* pidx, int n_tiles, KfStepGeom g,
-                                const KfDevState* st, KfOutDesc od, hipStream_t s);
+                                const KfDevState* st, KfOutDesc od, hipStream_t s,
+                                int committed = 0);
 
 // Inverse-CDF sampling of one token per sequence from fp32 logits [B][V]:
 // smallest m with F_m > u.  u from u_in [B] or, when null, the Philox stream

@@ -309,7 +309,7 @@ __device__ inline int out_index(const KfOutDesc& od, int C, int nr, int b, int j
 // over the vocabulary from the per-tile partials; exact ties to the lowest id.
 __global__ void __launch_bounds__(256)
     argmax_select_kernel(const float* __restrict__ pval, const int* __restrict__ pidx, int n_tiles,
-                         KfStepGeom g, const KfDevState* st, KfOutDesc od) {
+                         KfStepGeom g, const KfDevState* st, KfOutDesc od, int committed) {
   const int lane = threadIdx.x & 63;
   const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int rows = g.B * g.k;
@@ -349,7 +349,7 @@ __global__ void __launch_bounds__(256)
   if (lane == 0) {
     const int b = m / g.k, j = m % g.k;
     if (bi == 0x7fffffff) bi = 0;
-    od.out[out_index(od, g.ctx(st, b), g.nr, b, j)] = bi;
+    od.out[out_index(od, g.ctx(st, b) - committed, g.nr, b, j)] = bi;
     if (od.pend) od.pend[(size_t)g.slot(b) * od.pend_stride + j] = bi;
   }
 }
@@ -814,11 +814,11 @@ hipError_t launch_attention(const T* Q, const T* kv, T* O, const KfDevState* st,
 }
 
 hipError_t launch_argmax_select(const float* pval, const int* pidx, int n_tiles, KfStepGeom g,
-                                const KfDevState* st, KfOutDesc od, hipStream_t s) {
+                                const KfDevState* st, KfOutDesc od, hipStream_t s, int committed) {
   int rows = g.B * g.k;
   if (rows <= 0) return hipSuccess;
   launch(argmax_select_kernel, dim3((rows + 3) / 4), dim3(256), 0, s, pval, pidx,
-                     n_tiles, g, st, od);
+                     n_tiles, g, st, od, committed);
   return hipGetLastError();
 }
 
