@@ -296,8 +296,9 @@ int kf_selfforcing_targets(kf_ctx *ctx, int B, int N, int k, const int32_t *toke
 #define KF_KC_OPROJ 5    /* attention-out GEMM + residual */
 #define KF_KC_MLP_UP 6   /* LayerNorm-folded MLP up GEMM + GELU */
 #define KF_KC_MLP_DOWN 7 /* MLP down GEMM + residual */
-#define KF_KC_HEAD 8     /* final-LayerNorm-folded head GEMM with argmax partials / logits */
-#define KF_KC_SELECT 9   /* argmax reduction or inverse-CDF sampler, commit */
+#define KF_KC_HEAD 8     /* final-LayerNorm-folded head GEMM with argmax partials / logits
+                            (the argmax head also commits the step: C += real rows) */
+#define KF_KC_SELECT 9   /* argmax reduction, or the AR baseline's inverse-CDF sampler and commit */
 #define KF_KC_COUNT 10
 #define KF_TIMING_ALL ((1 << KF_KC_COUNT) - 1)
 int kf_set_timing(kf_ctx *ctx, int class_mask);
