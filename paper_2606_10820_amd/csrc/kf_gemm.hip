@@ -585,7 +585,11 @@ struct GemmA {
 // better than four wavefronts with twice the per-wavefront tile (measured
 // 3-12 % faster per GEMM at M = 512 to 4096, the results bit for bit the same;
 // with 146 registers the folded-norm 128 x 128 tile fitted one workgroup per
-// CU and was 23 % slower than with four wavefronts).
+// CU and was 23 % slower than with four wavefronts).  With KG = 2 the
+// workgroup holds two such groups of WM x WN wavefronts, each with a ring of
+// its own over half of the K steps; the second group's sums are added to the
+// first's through LDS before the epilogue (grids of at most one workgroup per
+// CU, where the two rings double the operand loads in flight).
 template <typename T, int BM, int BN, int WM, int WN, int S, int MODE, bool NORM, class Ep,
           int KG = 1>
 __global__ void __launch_bounds__(64 * WM * WN * KG)
