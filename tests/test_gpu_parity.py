@@ -319,6 +319,35 @@ def test_graph_replay_matches_direct(toy):
         np.testing.assert_array_equal(a, b)
 
 
+@pytest.mark.parametrize("k", [1, 2])
+def test_generate_small_k(toy, k):
+    """kf_generate at k = 1 and 2 (the windows the bench sweep reports beside
+    k = 4): tokens against the oracle, teacher-forced on the GPU's own history,
+    and equal to the explicit prefill / decode-block sequence."""
+    blob, model = toy
+    B, N, L, seed = 4, 16, 24, 40 + k
+    kf = _ctx(TOY, B, 4, N, blob)
+    prompt = S.prompts_uniform(2, B, N, TOY.vocab)
+    out = kf.generate(prompt, L, k, seed).cpu().numpy()
+    assert kf.get_state() == (N + L - k, k, B)
+    for b in range(B):
+        s = model.seq()
+        pending = list(prompt[b])
+        for p in range(N, N + L, k):
+            u = [O.noise_u(seed, b, p + j) for j in range(k)]
+            ol, _ = s.step(pending, u, commit=True)
+            toks = out[b, p - N:p - N + k]
+            top = np.sort(ol, axis=1)
+            near = (top[:, -1] - top[:, -2]) < TOL[0] * np.abs(ol).max(axis=1)
+            assert np.all((toks == O.argmax(ol)) | near), (b, p)
+            pending = list(toks)
+    kf2 = _ctx(TOY, B, 4, N, blob)
+    t = [kf2.prefill(prompt, k, kf2.fill_noise(seed, B, N, k)).cpu().numpy()]
+    for p in range(N + k, N + L, k):
+        t.append(kf2.decode_block(kf2.fill_noise(seed, B, p, k)).cpu().numpy())
+    np.testing.assert_array_equal(np.concatenate(t, axis=1), out)
+
+
 def test_generate_noise_chunks_match_steps():
     """A generate long enough for three chunks of noise rows computed ahead
     (128 sequences, k = 4: 16 passes a chunk, 40 passes) gives exactly the
