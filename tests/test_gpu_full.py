@@ -130,6 +130,17 @@ def test_lm1b_fp32_tokens():
     report("lm1b fp32 B=4, prefill + 1 block", st)
 
 
+def test_lm1b_bf16_k2_batch32():
+    """k = 2 (the middle window of the bench sweep) at batch 32: decode steps of
+    M = 128 rows and a prefill of 576, so other GEMM tiles than the batch-64
+    k = 4 shape (and the last layer's head rows at M = 64)."""
+    B, N, k = 32, 16, 2
+    kf = _ctx(LM1B, B, 4, N)
+    prompt = S.prompts_zipf(4, B, N, LM1B.vocab)
+    st = _blocks(kf, _model(LM1B), prompt, [k, k, k], seed=6, tol=TOL[1], rows=[0, B - 1])
+    report("lm1b bf16 B=32 k=2, prefill + 2 blocks", st)
+
+
 def test_lm1b_fp32_batch64():
     """fp32 at the benchmark's batch: the decode step (M = 512) runs the GEMMs
     with two K groups per workgroup (out-projection and MLP-down in 32x64
